@@ -1,0 +1,149 @@
+"""ctypes wrapper of the WnW CPU oracle (plain C, double precision), TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of ``bench.py`` may use
+this module.  It neither imports nor links anything of the HIP library.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(HERE, "wnw_oracle.c")
+LIB = os.path.join(HERE, "libwnw_oracle.so")
+
+
+def build(verbose: bool = False) -> str:
+    """Compile the oracle with gcc (C99, OpenMP)."""
+    cmd = ["gcc", "-O2", "-std=c99", "-fopenmp", "-fPIC", "-shared", "-Wall", "-Wextra",
+           "-o", LIB + ".tmp", SRC, "-lm"]
+    if verbose:
+        print(" ".join(cmd))
+    subprocess.run(cmd, check=True)
+    os.replace(LIB + ".tmp", LIB)
+    return LIB
+
+
+class _Cfg(C.Structure):
+    _fields_ = [(n, C.c_int32) for n in (
+        "batch", "layers", "q_heads", "kv_heads", "head_dim", "audio_len", "text_len",
+        "chunk_len", "budget_bp", "top_k", "evict_lag", "next_step")]
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        # WNW_ORACLE_LIB lets the mutation tests load a deliberately broken copy of the oracle.
+        path = os.environ.get("WNW_ORACLE_LIB") or LIB
+        if path == LIB and not os.path.exists(LIB):
+            build()
+        L = C.CDLL(path)
+        P = C.c_void_p
+        L.wnwo_geometry.argtypes = [C.POINTER(_Cfg), C.POINTER(C.c_int32), C.POINTER(C.c_int32), C.POINTER(C.c_int32)]
+        L.wnwo_create.argtypes = [C.POINTER(_Cfg), P, P, P, P]
+        L.wnwo_create.restype = P
+        L.wnwo_destroy.argtypes = [P]
+        L.wnwo_keep_mask.argtypes = [P, C.c_int32, C.c_int32, C.c_int32, P]
+        L.wnwo_step.argtypes = [P, P, P, P, P, P, P, P, P]
+        L.wnwo_topk.argtypes = [P, C.c_int32, C.c_int32, P]
+        L.wnwo_tokens_for_window.argtypes = [C.c_double, C.c_double]
+        L.wnwo_tokens_for_window.restype = C.c_int32
+        _lib = L
+    return _lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(C.c_void_p)
+
+
+def make_cfg(batch, layers, q_heads, kv_heads, head_dim, audio_len, text_len, chunk_len,
+             budget_bp, top_k=0, evict_lag=0, next_step=0) -> _Cfg:
+    return _Cfg(batch, layers, q_heads, kv_heads, head_dim, audio_len, text_len, chunk_len,
+                budget_bp, top_k, evict_lag, next_step)
+
+
+def cfg_from_workload(w, batch=None, **over) -> _Cfg:
+    kw = dict(batch=batch or w.batch, layers=w.layers, q_heads=w.q_heads, kv_heads=w.kv_heads,
+              head_dim=w.head_dim, audio_len=w.audio_len, text_len=w.text_len,
+              chunk_len=w.chunk_len, budget_bp=w.budget_bp)
+    kw.update(over)
+    return make_cfg(**kw)
+
+
+def geometry(cfg: _Cfg):
+    n, k, kt = C.c_int32(), C.c_int32(), C.c_int32()
+    if lib().wnwo_geometry(C.byref(cfg), C.byref(n), C.byref(k), C.byref(kt)):
+        raise ValueError("invalid oracle configuration")
+    return n.value, k.value, kt.value
+
+
+def topk(scores: np.ndarray, k: int) -> np.ndarray:
+    s = np.ascontiguousarray(scores, dtype=np.float32)
+    out = np.empty(max(k, 1), dtype=np.int32)
+    if lib().wnwo_topk(_ptr(s), len(s), k, _ptr(out)):
+        raise ValueError("bad top-k arguments")
+    return out[:k]
+
+
+def tokens_for_window(seconds: float, rate: float) -> int:
+    return lib().wnwo_tokens_for_window(seconds, rate)
+
+
+class Oracle:
+    """Stateful oracle over one batch of sequences.  k, v: uint16 [B][L][H_kv][T][d];
+    roles uint8 [L][H_kv]; prefill fp32 [B][L][H_kv][T_a].  The arrays are referenced, not
+    copied, so they are kept alive here."""
+
+    def __init__(self, cfg: _Cfg, k, v, roles, prefill):
+        self.cfg = cfg
+        self.n_chunks, self.k, self.keep_total = geometry(cfg)
+        self._k = np.ascontiguousarray(k, dtype=np.uint16)
+        self._v = np.ascontiguousarray(v, dtype=np.uint16)
+        self._roles = np.ascontiguousarray(roles, dtype=np.uint8)
+        self._pf = np.ascontiguousarray(prefill, dtype=np.float32)
+        B, L, H, D = cfg.batch, cfg.layers, cfg.kv_heads, cfg.head_dim
+        T = cfg.audio_len + cfg.text_len
+        assert self._k.shape == (B, L, H, T, D) and self._v.shape == self._k.shape
+        assert self._roles.shape == (L, H) and self._pf.shape == (B, L, H, cfg.audio_len)
+        self.n_anchor_q = int((self._roles == 0).sum()) * (cfg.q_heads // cfg.kv_heads)
+        self._h = lib().wnwo_create(C.byref(cfg), _ptr(self._k), _ptr(self._v), _ptr(self._roles), _ptr(self._pf))
+        if not self._h:
+            raise ValueError("wnwo_create failed")
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().wnwo_destroy(self._h)
+            self._h = None
+
+    __del__ = close
+
+    def keep_mask(self, b, l, kv) -> np.ndarray:
+        m = np.empty(self.cfg.audio_len, dtype=np.uint8)
+        if lib().wnwo_keep_mask(self._h, b, l, kv, _ptr(m)):
+            raise ValueError("bad head index")
+        return m
+
+    def step(self, q, forced=None, head_mask=None):
+        c = self.cfg
+        B, L, Hq, D = c.batch, c.layers, c.q_heads, c.head_dim
+        q = np.ascontiguousarray(q, dtype=np.uint16)
+        assert q.shape == (B, L, Hq, D)
+        out = np.empty((B, L, Hq, D), dtype=np.float64)
+        scores = np.empty((B, self.n_chunks), dtype=np.float64)
+        sel = np.empty((B, max(self.k, 1)), dtype=np.int32)
+        mass = np.empty((B, max(self.n_anchor_q, 1), max(self.n_chunks, 1)), dtype=np.float64)
+        res = np.empty((B, max(self.n_chunks, 1)), dtype=np.uint8)
+        f = None if forced is None else np.ascontiguousarray(forced, dtype=np.int32).reshape(B, self.k)
+        hm = None if head_mask is None else np.ascontiguousarray(head_mask, dtype=np.uint8).reshape(L, c.kv_heads)
+        rc = lib().wnwo_step(self._h, _ptr(q), _ptr(f), _ptr(hm), _ptr(out), _ptr(scores), _ptr(sel),
+                             _ptr(mass), _ptr(res))
+        if rc:
+            raise ValueError(f"wnwo_step failed ({rc})")
+        return {"out": out, "scores": scores, "selected": sel[:, : self.k],
+                "mass": mass[:, : self.n_anchor_q, : self.n_chunks], "resident": res[:, : self.n_chunks]}

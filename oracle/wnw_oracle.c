@@ -1,0 +1,396 @@
+/*
+ * WnW decode-step oracle: plain CPU reference, TEST INFRASTRUCTURE ONLY.
+ *
+ * Written from the Method section of "WnW: Waxing-and-Waning KV Cache for Long-Form Speech
+ * LLMs" (arXiv 2608.22704).  It takes the method's steps in the paper's order, in the most
+ * direct form, accumulating in double over the exact bf16 inputs:
+ *
+ *   1. Roles (Method, "Three-Way Classification"): anchor KV-heads keep all audio KV; tidal
+ *      heads keep a prefill subset on the device and a recallable complement on the host; fixed
+ *      heads keep the subset only.  Non-audio (text) KV is always kept in full (the remark under
+ *      the retention equation, Eq. 1).
+ *   2. Prefill compression (Method, "Prefill Compression"): inside each segment, keep the top
+ *      floor(retention * segment length) audio positions by prefill score.
+ *   3. Decode-step score aggregation (Eq. 2): A_tau is the sum, over every anchor (layer,
+ *      q-head) pair, of that head's softmax weight at audio position tau; it is rebuilt from
+ *      zero at every step.
+ *   4. Dynamic chunk selection (Method, "Dynamic Chunk Selection"): a chunk's score is the mean
+ *      of A over its positions; the top-k chunks are selected; for tidal heads the complement of
+ *      a selected chunk becomes resident and is dropped after delta consecutive steps without
+ *      selection.
+ *   5. Attention of every head over what it holds: anchors over all rows, tidal heads over
+ *      kept rows + resident complements + text, fixed heads over kept rows + text.
+ *
+ * Readings taken where the paper leaves a choice (all listed in the design notes):
+ *   - chunks are disjoint runs of chunk_len audio positions, one segment per chunk; the last
+ *     chunk may be shorter and its score is the mean over the positions it has;
+ *   - retention is one uniform fraction budget_bp / 10000 for every tidal and fixed head;
+ *   - k = floor(budget_bp * T_a / (10000 * chunk_len)) unless given;
+ *   - the softmax of Eq. 2 runs over the anchor head's whole key set (audio and text); only the
+ *     audio weights enter A; the logit scale is 1 / sqrt(d);
+ *   - ties: prefill ranking prefers the lower position, chunk ranking the lower chunk id; the
+ *     ranking compares chunk scores rounded to fp32, the precision the scores are reported in;
+ *   - residency: a chunk is resident at step s iff it was selected at one of the steps
+ *     s - delta + 1 .. s, so a chunk selected once stays for delta steps;
+ *   - by default the selection of step s already serves the tidal heads of step s; with
+ *     next_step set they use the resident set left by step s - 1 (empty at the first step);
+ *   - a head whose key set is empty outputs zeros.
+ */
+#include "wnw_oracle.h"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+struct wnwo {
+    wnwo_config c;
+    int32_t n_chunks, k, keep_total, delta;
+    const uint16_t *kc, *vc;
+    uint8_t *roles;        /* [L][Hkv]                                               */
+    uint8_t *keep;         /* [B][L][Hkv][T_a] prefill keep flags of non-anchor heads */
+    int32_t *streak;       /* [B][n_chunks] steps since last selection, capped at delta */
+    uint8_t *res_prev;     /* [B][n_chunks] resident set after the previous step       */
+};
+
+static double bf16(uint16_t h)
+{
+    uint32_t u = (uint32_t)h << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+}
+
+int32_t wnwo_tokens_for_window(double seconds, double rate)
+{
+    /* Method, "Chunk Structure": n = ceil(W * r_tok). */
+    return (int32_t)ceil(seconds * rate);
+}
+
+static int32_t chunk_begin(const wnwo_config *c, int32_t ch) { return ch * c->chunk_len; }
+static int32_t chunk_end(const wnwo_config *c, int32_t ch)
+{
+    int32_t e = (ch + 1) * c->chunk_len;
+    return e < c->audio_len ? e : c->audio_len;
+}
+
+/* Positions kept at prefill inside a segment of `len` positions: floor(retention * len). */
+static int32_t keep_count(const wnwo_config *c, int32_t len)
+{
+    return (int32_t)(((int64_t)c->budget_bp * len) / 10000);
+}
+
+int wnwo_geometry(const wnwo_config *c, int32_t *n_chunks, int32_t *k, int32_t *keep_total)
+{
+    if (!c || c->batch < 1 || c->layers < 1 || c->kv_heads < 1 || c->head_dim < 1 ||
+        c->q_heads < c->kv_heads || c->q_heads % c->kv_heads || c->audio_len < 0 ||
+        c->text_len < 0 || c->chunk_len < 1 || c->budget_bp < 0 || c->budget_bp > 10000 ||
+        c->top_k < 0 || c->evict_lag < 0)
+        return -1;
+    int32_t nc = (c->audio_len + c->chunk_len - 1) / c->chunk_len;
+    int32_t kk = c->top_k ? c->top_k
+                          : (int32_t)(((int64_t)c->budget_bp * c->audio_len) / (10000LL * c->chunk_len));
+    if (kk > nc) return -1;
+    int32_t kt = 0;
+    for (int32_t ch = 0; ch < nc; ++ch) kt += keep_count(c, chunk_end(c, ch) - chunk_begin(c, ch));
+    if (n_chunks) *n_chunks = nc;
+    if (k) *k = kk;
+    if (keep_total) *keep_total = kt;
+    return 0;
+}
+
+/* ---- prefill compression: per-segment top floor(retention * len) by prefill score ---------- */
+
+typedef struct { float s; int32_t pos; } ranked;
+
+static int by_score_then_pos(const void *a, const void *b)
+{
+    const ranked *x = a, *y = b;
+    if (x->s > y->s) return -1;
+    if (x->s < y->s) return 1;
+    return (x->pos > y->pos) - (x->pos < y->pos);
+}
+
+static void prefill_keep(const wnwo_config *c, const float *score, uint8_t *keep, ranked *tmp)
+{
+    memset(keep, 0, (size_t)c->audio_len);
+    int32_t nc = (c->audio_len + c->chunk_len - 1) / c->chunk_len;
+    for (int32_t ch = 0; ch < nc; ++ch) {
+        int32_t b0 = chunk_begin(c, ch), e0 = chunk_end(c, ch), n = e0 - b0;
+        for (int32_t i = 0; i < n; ++i) { tmp[i].s = score[b0 + i]; tmp[i].pos = b0 + i; }
+        qsort(tmp, (size_t)n, sizeof *tmp, by_score_then_pos);
+        int32_t kc = keep_count(c, n);
+        for (int32_t i = 0; i < kc; ++i) keep[tmp[i].pos] = 1;
+    }
+}
+
+wnwo *wnwo_create(const wnwo_config *cfg, const uint16_t *k, const uint16_t *v,
+                  const uint8_t *roles, const float *prefill)
+{
+    int32_t nc, kk, kt;
+    if (!cfg || !k || !v || !roles || !prefill) return NULL;
+    if (wnwo_geometry(cfg, &nc, &kk, &kt)) return NULL;
+    for (int32_t i = 0; i < cfg->layers * cfg->kv_heads; ++i)
+        if (roles[i] > 2) return NULL;
+    wnwo *o = calloc(1, sizeof *o);
+    if (!o) return NULL;
+    o->c = *cfg;
+    o->n_chunks = nc;
+    o->k = kk;
+    o->keep_total = kt;
+    o->delta = cfg->evict_lag ? cfg->evict_lag : 3;
+    o->kc = k;
+    o->vc = v;
+    size_t nh = (size_t)cfg->layers * cfg->kv_heads, B = (size_t)cfg->batch;
+    o->roles = malloc(nh);
+    o->keep = malloc(B * nh * (size_t)(cfg->audio_len ? cfg->audio_len : 1));
+    o->streak = malloc(B * (size_t)(nc ? nc : 1) * sizeof(int32_t));
+    o->res_prev = calloc(B * (size_t)(nc ? nc : 1), 1);
+    ranked *tmp = malloc((size_t)(cfg->chunk_len) * sizeof *tmp);
+    if (!o->roles || !o->keep || !o->streak || !o->res_prev || !tmp) {
+        free(tmp);
+        wnwo_destroy(o);
+        return NULL;
+    }
+    memcpy(o->roles, roles, nh);
+    for (size_t b = 0; b < B; ++b)
+        for (size_t h = 0; h < nh; ++h) {
+            uint8_t *kp = o->keep + (b * nh + h) * (size_t)cfg->audio_len;
+            if (roles[h] == 0)
+                memset(kp, 1, (size_t)cfg->audio_len);         /* anchors keep all audio */
+            else
+                prefill_keep(cfg, prefill + (b * nh + h) * (size_t)cfg->audio_len, kp, tmp);
+        }
+    free(tmp);
+    /* No chunk has been selected yet: every streak starts at delta (not resident). */
+    for (size_t i = 0; i < B * (size_t)nc; ++i) o->streak[i] = o->delta;
+    return o;
+}
+
+void wnwo_destroy(wnwo *o)
+{
+    if (!o) return;
+    free(o->roles);
+    free(o->keep);
+    free(o->streak);
+    free(o->res_prev);
+    free(o);
+}
+
+int wnwo_keep_mask(const wnwo *o, int32_t b, int32_t l, int32_t kv, uint8_t *mask)
+{
+    if (!o || !mask) return -1;
+    const wnwo_config *c = &o->c;
+    if (b < 0 || b >= c->batch || l < 0 || l >= c->layers || kv < 0 || kv >= c->kv_heads)
+        return -1;
+    size_t nh = (size_t)c->layers * c->kv_heads;
+    memcpy(mask, o->keep + ((size_t)b * nh + (size_t)l * c->kv_heads + kv) * (size_t)c->audio_len,
+           (size_t)c->audio_len);
+    return 0;
+}
+
+/* ---- top-k by (score descending, id ascending) --------------------------------------------- */
+
+typedef struct { float s; int32_t id; } scored;
+
+static int by_score_then_id(const void *a, const void *b)
+{
+    const scored *x = a, *y = b;
+    if (x->s > y->s) return -1;
+    if (x->s < y->s) return 1;
+    return (x->id > y->id) - (x->id < y->id);
+}
+
+static int by_int(const void *a, const void *b)
+{
+    int32_t x = *(const int32_t *)a, y = *(const int32_t *)b;
+    return (x > y) - (x < y);
+}
+
+int wnwo_topk(const float *scores, int32_t n, int32_t k, int32_t *sel)
+{
+    if (n < 0 || k < 0 || k > n || (k && (!scores || !sel))) return -1;
+    if (!k) return 0;
+    scored *t = malloc((size_t)n * sizeof *t);
+    if (!t) return -2;
+    for (int32_t i = 0; i < n; ++i) { t[i].s = scores[i]; t[i].id = i; }
+    qsort(t, (size_t)n, sizeof *t, by_score_then_id);
+    for (int32_t i = 0; i < k; ++i) sel[i] = t[i].id;
+    free(t);
+    qsort(sel, (size_t)k, sizeof *sel, by_int);
+    return 0;
+}
+
+/* ---- softmax attention of one query over a listed key set ---------------------------------- */
+
+/* x_i = q . K[rows[i]] / sqrt(d); p = softmax(x); out = sum_i p_i V[rows[i]].  p may be NULL. */
+static void attend(const uint16_t *q, const uint16_t *K, const uint16_t *V, const int32_t *rows,
+                   int32_t n, int32_t d, double *x, double *out, double *p)
+{
+    for (int32_t j = 0; j < d; ++j) out[j] = 0.0;
+    if (n == 0) return;
+    double scale = 1.0 / sqrt((double)d), m = -INFINITY, s = 0.0;
+    for (int32_t i = 0; i < n; ++i) {
+        const uint16_t *kr = K + (size_t)rows[i] * d;
+        double acc = 0.0;
+        for (int32_t j = 0; j < d; ++j) acc += bf16(q[j]) * bf16(kr[j]);
+        x[i] = acc * scale;
+        if (x[i] > m) m = x[i];
+    }
+    for (int32_t i = 0; i < n; ++i) { x[i] = exp(x[i] - m); s += x[i]; }
+    for (int32_t i = 0; i < n; ++i) {
+        double pi = x[i] / s;
+        const uint16_t *vr = V + (size_t)rows[i] * d;
+        for (int32_t j = 0; j < d; ++j) out[j] += pi * bf16(vr[j]);
+        if (p) p[i] = pi;
+    }
+}
+
+/* ---- one decode step -------------------------------------------------------------------------- */
+
+int wnwo_step(wnwo *o, const uint16_t *q, const int32_t *forced, const uint8_t *head_mask,
+              double *out, double *scores, int32_t *selected, double *mass, uint8_t *resident)
+{
+    if (!o || !q || !out || !scores || (o->k && !selected)) return -1;
+    const wnwo_config *c = &o->c;
+    const int32_t L = c->layers, H = c->kv_heads, Hq = c->q_heads, g = Hq / H, D = c->head_dim;
+    const int32_t Ta = c->audio_len, T = Ta + c->text_len, nc = o->n_chunks, k = o->k, B = c->batch;
+    const size_t nh = (size_t)L * H;
+
+    int32_t n_anchor = 0;
+    for (size_t h = 0; h < nh; ++h) n_anchor += o->roles[h] == 0;
+    const int32_t naq = n_anchor * g;
+
+    /* Anchor KV-heads in (layer, kv) order; their q-heads j = 0..g-1 follow in that order. */
+    int32_t *anchor_of = malloc((nh ? nh : 1) * sizeof(int32_t));
+    double *m = calloc((size_t)B * (naq ? naq : 1) * (nc ? nc : 1), sizeof(double));
+    uint8_t *res_now = calloc((size_t)B * (nc ? nc : 1), 1);
+    uint8_t *res_use = calloc((size_t)B * (nc ? nc : 1), 1);
+    if (!anchor_of || !m || !res_now || !res_use) {
+        free(anchor_of); free(m); free(res_now); free(res_use);
+        return -2;
+    }
+    for (size_t h = 0, a = 0; h < nh; ++h) anchor_of[h] = o->roles[h] == 0 ? (int32_t)a++ : -1;
+
+    memset(out, 0, (size_t)B * L * Hq * D * sizeof(double));
+    int status = 0;
+
+    /* Step 1: anchor attention over all audio and text rows, and Eq. 2's per-chunk mass. */
+    #pragma omp parallel for collapse(2) schedule(dynamic)
+    for (int32_t b = 0; b < B; ++b)
+        for (int32_t hh = 0; hh < (int32_t)nh; ++hh) {
+            if (o->roles[hh] != 0) continue;
+            int32_t l = hh / H, kv = hh % H;
+            int32_t *rows = malloc((size_t)(T ? T : 1) * sizeof(int32_t));
+            double *x = malloc((size_t)(T ? T : 1) * sizeof(double));
+            double *p = malloc((size_t)(T ? T : 1) * sizeof(double));
+            if (!rows || !x || !p) {
+                #pragma omp atomic write
+                status = -2;
+                free(rows); free(x); free(p);
+                continue;
+            }
+            for (int32_t t = 0; t < T; ++t) rows[t] = t;
+            size_t hoff = (((size_t)b * L + l) * H + kv) * (size_t)T * D;
+            for (int32_t j = 0; j < g; ++j) {
+                int32_t hq = kv * g + j;
+                const uint16_t *qh = q + (((size_t)b * L + l) * Hq + hq) * D;
+                double *oh = out + (((size_t)b * L + l) * Hq + hq) * D;
+                attend(qh, o->kc + hoff, o->vc + hoff, rows, T, D, x, oh, p);
+                double *mh = m + ((size_t)b * naq + (size_t)anchor_of[hh] * g + j) * nc;
+                for (int32_t ch = 0; ch < nc; ++ch) {
+                    double acc = 0.0;
+                    for (int32_t t = chunk_begin(c, ch); t < chunk_end(c, ch); ++t) acc += p[t];
+                    mh[ch] = acc;
+                }
+            }
+            free(rows); free(x); free(p);
+        }
+    if (status) goto done;
+
+    /* A forced selection must hold distinct chunk ids (or -1) before any state changes. */
+    if (forced)
+        for (int32_t b = 0; b < B && !status; ++b)
+            for (int32_t i = 0; i < k; ++i) {
+                int32_t id = forced[(size_t)b * k + i];
+                if (id < -1 || id >= nc) status = -1;
+                for (int32_t j = 0; j < i; ++j)
+                    if (id >= 0 && forced[(size_t)b * k + j] == id) status = -1;
+            }
+    if (status) goto done;
+
+    /* Steps 2-4 per sequence: chunk scores, top-k, residency. */
+    for (int32_t b = 0; b < B; ++b) {
+        float *sf = malloc((size_t)(nc ? nc : 1) * sizeof(float));
+        int32_t *sel = malloc((size_t)(k ? k : 1) * sizeof(int32_t));
+        if (!sf || !sel) { free(sf); free(sel); status = -2; goto done; }
+        for (int32_t ch = 0; ch < nc; ++ch) {
+            double a = 0.0;
+            for (int32_t h = 0; h < naq; ++h) a += m[((size_t)b * naq + h) * nc + ch];
+            double sc = a / (double)(chunk_end(c, ch) - chunk_begin(c, ch));   /* mean over the chunk */
+            scores[(size_t)b * nc + ch] = sc;
+            sf[ch] = (float)sc;
+        }
+        if (forced) {
+            for (int32_t i = 0; i < k; ++i) sel[i] = forced[(size_t)b * k + i];
+            qsort(sel, (size_t)k, sizeof *sel, by_int);
+        } else if (wnwo_topk(sf, nc, k, sel)) {
+            status = -2;
+        }
+        if (status) { free(sf); free(sel); goto done; }
+        for (int32_t i = 0; i < k; ++i) selected[(size_t)b * k + i] = sel[i];
+
+        int32_t *st = o->streak + (size_t)b * nc;
+        uint8_t *now = res_now + (size_t)b * nc;
+        for (int32_t ch = 0; ch < nc; ++ch)
+            if (st[ch] < o->delta) st[ch] += 1;            /* one more step without selection */
+        for (int32_t i = 0; i < k; ++i)
+            if (sel[i] >= 0) st[sel[i]] = 0;                /* selected this step             */
+        for (int32_t ch = 0; ch < nc; ++ch) now[ch] = st[ch] < o->delta;
+        memcpy(res_use + (size_t)b * nc, c->next_step ? o->res_prev + (size_t)b * nc : now, (size_t)nc);
+        free(sf);
+        free(sel);
+    }
+
+    /* Step 5: tidal heads (kept + resident complements + text) and fixed heads (kept + text). */
+    #pragma omp parallel for collapse(2) schedule(dynamic)
+    for (int32_t b = 0; b < B; ++b)
+        for (int32_t hh = 0; hh < (int32_t)nh; ++hh) {
+            if (o->roles[hh] == 0 || (head_mask && !head_mask[hh])) continue;
+            int32_t l = hh / H, kv = hh % H;
+            int32_t *rows = malloc((size_t)(T ? T : 1) * sizeof(int32_t));
+            double *x = malloc((size_t)(T ? T : 1) * sizeof(double));
+            if (!rows || !x) {
+                #pragma omp atomic write
+                status = -2;
+                free(rows); free(x);
+                continue;
+            }
+            const uint8_t *kp = o->keep + ((size_t)b * nh + hh) * (size_t)Ta;
+            const uint8_t *ru = res_use + (size_t)b * nc;
+            int32_t n = 0;
+            for (int32_t t = 0; t < Ta; ++t) {
+                int32_t ch = t / c->chunk_len;
+                if (kp[t] || (o->roles[hh] == 1 && ru[ch])) rows[n++] = t;
+            }
+            for (int32_t t = Ta; t < T; ++t) rows[n++] = t;
+            size_t hoff = (((size_t)b * L + l) * H + kv) * (size_t)T * D;
+            for (int32_t j = 0; j < g; ++j) {
+                int32_t hq = kv * g + j;
+                attend(q + (((size_t)b * L + l) * Hq + hq) * D, o->kc + hoff, o->vc + hoff, rows, n, D, x,
+                       out + (((size_t)b * L + l) * Hq + hq) * D, NULL);
+            }
+            free(rows);
+            free(x);
+        }
+    if (status) goto done;
+
+    memcpy(o->res_prev, res_now, (size_t)B * nc);
+    if (mass) memcpy(mass, m, (size_t)B * naq * nc * sizeof(double));
+    if (resident) memcpy(resident, res_use, (size_t)B * nc);
+done:
+    free(anchor_of);
+    free(m);
+    free(res_now);
+    free(res_use);
+    return status;
+}

@@ -1,0 +1,69 @@
+/*
+ * WnW decode-step oracle: plain CPU reference, TEST INFRASTRUCTURE ONLY.
+ *
+ * Only the tests, the package smoke check and the benchmark's CPU-baseline leg call this
+ * code.  It shares nothing with the HIP library: not this header, not a helper, not a table.
+ *
+ * Paper: "WnW: Waxing-and-Waning KV Cache for Long-Form Speech LLMs" (arXiv 2608.22704),
+ * Method section (head triage, retention equation, prefill compression, Eq. 2 decode-step
+ * score aggregation, dynamic chunk selection).
+ *
+ * Arrays are row-major.  bf16 values are uint16 bit patterns.  Every function returns 0 on
+ * success and a negative number on invalid arguments.
+ */
+#ifndef WNW_ORACLE_H
+#define WNW_ORACLE_H
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct {
+    int32_t batch, layers, q_heads, kv_heads, head_dim;
+    int32_t audio_len, text_len;   /* T_a audio rows first, then T_t text rows            */
+    int32_t chunk_len;             /* disjoint chunks of this many audio positions         */
+    int32_t budget_bp;             /* on-GPU audio retention in basis points               */
+    int32_t top_k;                 /* 0: floor(budget_bp * T_a / (10000 * chunk_len))      */
+    int32_t evict_lag;             /* delta; 0 means 3                                     */
+    int32_t next_step;             /* 1: tidal heads use the previous step's resident set  */
+} wnwo_config;
+
+typedef struct wnwo wnwo;
+
+/* Derived sizes: number of chunks, k, kept audio rows per non-anchor head. */
+int wnwo_geometry(const wnwo_config *cfg, int32_t *n_chunks, int32_t *k, int32_t *keep_total);
+
+/* k, v: [B][L][H_kv][T_a+T_t][d] bf16, referenced (not copied) for the oracle's lifetime.
+ * roles: [L][H_kv] (0 anchor, 1 tidal, 2 fixed).  prefill: [B][L][H_kv][T_a] fp32. */
+wnwo *wnwo_create(const wnwo_config *cfg, const uint16_t *k, const uint16_t *v,
+                  const uint8_t *roles, const float *prefill);
+void wnwo_destroy(wnwo *o);
+
+/* Audio positions kept at prefill by head (b, l, kv): mask[T_a] of 0/1 (all 1 for anchors). */
+int wnwo_keep_mask(const wnwo *o, int32_t b, int32_t l, int32_t kv, uint8_t *mask);
+
+/* One decode step.
+ *   q         [B][L][H_q][d] bf16
+ *   forced    [B][k] chunk ids replacing this step's top-k (-1 = no chunk), or NULL
+ *   head_mask [L][H_kv]: outputs of non-anchor heads are computed only where non-zero
+ *             (NULL = all); anchor outputs are always computed
+ *   out       [B][L][H_q][d]         attention outputs (rows of skipped heads are zeroed)
+ *   scores    [B][n_chunks]          chunk scores (double)
+ *   selected  [B][k]                 selected chunk ids, ascending (-1 pads a forced set)
+ *   mass      [B][n_anchor*g][n_chunks] or NULL: per anchor q-head chunk mass
+ *   resident  [B][n_chunks] or NULL: 1 where the chunk's complement was attended this step
+ */
+int wnwo_step(wnwo *o, const uint16_t *q, const int32_t *forced, const uint8_t *head_mask,
+              double *out, double *scores, int32_t *selected, double *mass, uint8_t *resident);
+
+/* Top-k of n scores ordered by (score descending, id ascending); ids returned ascending. */
+int wnwo_topk(const float *scores, int32_t n, int32_t k, int32_t *sel);
+
+/* Tokens covered by a window of `seconds` at `rate` tokens per second: ceil(seconds * rate). */
+int32_t wnwo_tokens_for_window(double seconds, double rate);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

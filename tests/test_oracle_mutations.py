@@ -1,0 +1,54 @@
+"""Plant plausible mistakes in copies of the oracle (on the CPU) and require the pins to fail.
+
+Each mutant is compiled from the oracle's source with one textual change and the pin suite
+is run against it in a subprocess; a mutant that passes every pin would mean the pins leave
+that part of the oracle unchecked.
+"""
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "wnw_oracle.c")
+
+MUTANTS = {
+    "score is a sum, not a mean": (
+        "double sc = a / (double)(chunk_end(c, ch) - chunk_begin(c, ch));", "double sc = a;"),
+    "text rows left out of the anchor softmax": (
+        "attend(qh, o->kc + hoff, o->vc + hoff, rows, T, D, x, oh, p);",
+        "attend(qh, o->kc + hoff, o->vc + hoff, rows, Ta, D, x, oh, p);"),
+    "chunk ties prefer the higher id": (
+        "return (x->id > y->id) - (x->id < y->id);", "return (x->id < y->id) - (x->id > y->id);"),
+    "eviction lag one step too long": (
+        "now[ch] = st[ch] < o->delta;", "now[ch] = st[ch] <= o->delta;"),
+    "keep count rounds up": (
+        "return (int32_t)(((int64_t)c->budget_bp * len) / 10000);",
+        "return (int32_t)(((int64_t)c->budget_bp * len + 9999) / 10000);"),
+    "tidal heads ignore recalled chunks": (
+        "(o->roles[hh] == 1 && ru[ch])", "(o->roles[hh] == 1 && 0 && ru[ch])"),
+    "logit scale 1/d": ("1.0 / sqrt((double)d)", "1.0 / (double)d"),
+    "prefill ranking keeps the lowest scores": (
+        "    const ranked *x = a, *y = b;\n    if (x->s > y->s) return -1;",
+        "    const ranked *x = a, *y = b;\n    if (x->s < y->s) return -1;"),
+    "selection state not reset on selection": ("if (sel[i] >= 0) st[sel[i]] = 0;", "if (sel[i] >= 0) st[sel[i]] += 0;"),
+    "fixed heads see recalled chunks": ("(o->roles[hh] == 1 && ru[ch])", "(o->roles[hh] >= 1 && ru[ch])"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_catch_mutant(name, tmp_path):
+    old, new = MUTANTS[name]
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation anchor not unique/found: {old!r}"
+    mpath = tmp_path / "mutant.c"
+    mpath.write_text(src.replace(old, new))
+    so = tmp_path / "libmutant.so"
+    subprocess.run(["gcc", "-O1", "-std=c99", "-fopenmp", "-fPIC", "-shared", "-I", os.path.join(ROOT, "oracle"),
+                    "-o", str(so), str(mpath), "-lm"], check=True)
+    env = dict(os.environ, WNW_ORACLE_LIB=str(so))
+    r = subprocess.run([sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:cacheprovider",
+                        os.path.join(ROOT, "tests", "test_oracle_pins.py")],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    assert r.returncode != 0, f"mutant '{name}' passed every pin:\n{r.stdout[-2000:]}"

@@ -1,0 +1,264 @@
+"""Pins of the CPU oracle against things other than itself.
+
+Each test ties one part of the oracle to an independent fact: a library routine computing the
+same definition (torch's scaled_dot_product_attention in double), a closed form, a brute-force
+enumeration, a hand-worked trace, or a value printed in the paper.  A plausible mistake in the
+oracle (a dropped text term, a sum instead of a mean, a reversed tie rule, an off-by-one in the
+eviction lag, a wrong keep count) fails at least one of them.
+"""
+import itertools
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from synth.gen import f32_to_bf16, bf16_to_f32
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _rand_cache(rng, B, L, H, T, D, scale=1.0):
+    k = f32_to_bf16(rng.standard_normal((B, L, H, T, D)).astype(np.float32) * scale)
+    v = f32_to_bf16(rng.standard_normal((B, L, H, T, D)).astype(np.float32))
+    return k, v
+
+
+def _sdpa(q, k, v, mask=None):
+    """One query q [d] over rows k [T][d], v [T][e] (bf16 bit patterns or float), double."""
+    f = lambda a: torch.from_numpy(bf16_to_f32(a).astype(np.float64)) if a.dtype == np.uint16 else torch.from_numpy(a.astype(np.float64))
+    qq, kk, vv = f(q)[None, None], f(k)[None], f(v)[None]
+    m = None if mask is None else torch.from_numpy(mask.astype(bool))[None, None]
+    return torch.nn.functional.scaled_dot_product_attention(qq, kk, vv, attn_mask=m)[0, 0].numpy()
+
+
+def _small(oracle_mod, seed=0, B=2, L=2, H=3, g=2, D=16, Ta=37, Tt=5, cl=8, budget=2500, **kw):
+    rng = np.random.default_rng(seed)
+    k, v = _rand_cache(rng, B, L, H, Ta + Tt, D)
+    roles = np.array([[0, 1, 2], [1, 2, 0]], dtype=np.uint8)[:L, :H]
+    pf = rng.random((B, L, H, Ta), dtype=np.float32)
+    cfg = oracle_mod.make_cfg(B, L, H * g, H, D, Ta, Tt, cl, budget, **kw)
+    o = oracle_mod.Oracle(cfg, k, v, roles, pf)
+    q = f32_to_bf16(rng.standard_normal((B, L, H * g, D)).astype(np.float32))
+    return o, k, v, roles, pf, q
+
+
+def test_full_budget_equals_full_attention(oracle_mod):
+    """At 100 % budget every head holds every row, so WnW is plain attention (Full Cache)."""
+    o, k, v, roles, pf, q = _small(oracle_mod, budget=10000)
+    r = o.step(q)
+    B, L, Hq, D = q.shape
+    g = Hq // k.shape[2]
+    for b, l, hq in itertools.product(range(B), range(L), range(Hq)):
+        ref = _sdpa(q[b, l, hq], k[b, l, hq // g], v[b, l, hq // g])
+        np.testing.assert_allclose(r["out"][b, l, hq], ref, rtol=0, atol=1e-12)
+
+
+def test_keep_masks_are_per_segment_top_by_prefill_score(oracle_mod):
+    """Prefill compression: in every segment exactly floor(retention * len) positions are kept
+    and each kept position outranks each dropped one (score, then lower position)."""
+    rng = np.random.default_rng(3)
+    B, L, H, D, Ta, Tt, cl, budget = 2, 1, 3, 8, 70, 2, 16, 3000
+    k, v = _rand_cache(rng, B, L, H, Ta + Tt, D)
+    pf = (rng.integers(0, 4, size=(B, L, H, Ta)) / 4.0).astype(np.float32)   # heavy ties
+    roles = np.array([[0, 1, 2]], dtype=np.uint8)
+    o = oracle_mod.Oracle(oracle_mod.make_cfg(B, L, H, H, D, Ta, Tt, cl, budget), k, v, roles, pf)
+    for b, h in itertools.product(range(B), range(H)):
+        m = o.keep_mask(b, 0, h)
+        if roles[0, h] == 0:
+            assert m.all()
+            continue
+        for c0 in range(0, Ta, cl):
+            seg = range(c0, min(c0 + cl, Ta))
+            kept = [t for t in seg if m[t]]
+            drop = [t for t in seg if not m[t]]
+            assert len(kept) == (budget * len(seg)) // 10000
+            for a in kept:
+                for d in drop:
+                    assert (pf[b, 0, h, a], -a) > (pf[b, 0, h, d], -d)
+
+
+def test_chunk_mass_is_softmax_mass_of_the_chunk(oracle_mod):
+    """Eq. 2 per anchor q-head: the mass of chunk c is the attention output for V = the
+    indicator of c (library attention), and the chunk masses add up to the audio mass."""
+    o, k, v, roles, pf, q = _small(oracle_mod, seed=5, Ta=45, Tt=6, cl=8)
+    r = o.step(q)
+    B, L, Hq, D = q.shape
+    H = k.shape[2]
+    g = Hq // H
+    Ta, T, nc = 45, 51, o.n_chunks
+    ind = np.zeros((T, nc + 2))
+    for t in range(Ta):
+        ind[t, t // 8] = 1.0
+    ind[:Ta, nc] = 1.0            # audio indicator
+    ind[Ta:, nc + 1] = 1.0        # text indicator
+    a = 0
+    for l, h in itertools.product(range(L), range(H)):
+        if roles[l, h] != 0:
+            continue
+        for j in range(g):
+            for b in range(B):
+                ref = _sdpa(q[b, l, h * g + j], k[b, l, h], ind)
+                np.testing.assert_allclose(r["mass"][b, a * g + j], ref[:nc], rtol=1e-12, atol=1e-15)
+                assert abs(r["mass"][b, a * g + j].sum() - ref[nc]) < 1e-12
+                assert abs(ref[nc] + ref[nc + 1] - 1.0) < 1e-12
+        a += 1
+
+
+def test_equal_logits_closed_form(oracle_mod):
+    """q = 0 makes every logit equal: p = 1 / T on every row, so every chunk (the short last
+    one included) scores n_anchor_q / T -- a mean, not a sum -- and the tie rule selects the
+    lowest ids 0..k-1."""
+    o, k, v, roles, pf, q = _small(oracle_mod, seed=7, Ta=37, Tt=5, cl=8, budget=4000)
+    q[:] = 0
+    r = o.step(q)
+    T = 42
+    assert o.k == (4000 * 37) // (10000 * 8)
+    np.testing.assert_allclose(r["scores"], o.n_anchor_q / T, rtol=1e-13)
+    assert (r["selected"] == np.arange(o.k)).all()
+    # equal logits over the whole key set also make every output the mean of V over that set
+    B, L, Hq, D = q.shape
+    g = Hq // k.shape[2]
+    for b, l, hq in itertools.product(range(B), range(L), range(Hq)):
+        h = hq // g
+        vv = bf16_to_f32(v[b, l, h]).astype(np.float64)
+        if roles[l, h] == 0:
+            rows = np.arange(T)
+        elif roles[l, h] == 2:
+            rows = np.concatenate([np.nonzero(o.keep_mask(b, l, h))[0], np.arange(37, T)])
+        else:
+            continue
+        np.testing.assert_allclose(r["out"][b, l, hq], vv[rows].mean(axis=0), rtol=1e-12, atol=1e-14)
+
+
+def _brute_topk(s, k):
+    """The unique k-subset whose members all beat all non-members under (score desc, id asc)."""
+    n = len(s)
+    found = []
+    for sub in itertools.combinations(range(n), k):
+        ins = set(sub)
+        if all((s[i], -i) > (s[j], -j) for i in ins for j in range(n) if j not in ins):
+            found.append(sub)
+    assert len(found) == 1
+    return list(found[0])
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_topk_matches_brute_force(oracle_mod, seed):
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(1, 13))
+    k = int(rng.integers(0, n + 1))
+    s = (rng.integers(0, 5, size=n) / 7.0).astype(np.float32)   # planted ties
+    assert list(oracle_mod.topk(s, k)) == _brute_topk(list(s), k)
+
+
+def test_residency_trace_matches_hand_worked_lag(oracle_mod):
+    gold = json.load(open(os.path.join(GOLD, "residency_trace.json")))
+    rng = np.random.default_rng(11)
+    B, L, H, D, Ta, Tt, cl = 1, 1, 2, 8, 160, 3, 16           # 10 chunks
+    k, v = _rand_cache(rng, B, L, H, Ta + Tt, D)
+    roles = np.array([[0, 1]], dtype=np.uint8)
+    pf = rng.random((B, L, H, Ta), dtype=np.float32)
+    for mode, key in ((0, "resident_same_step"), (1, "resident_next_step")):
+        cfg = oracle_mod.make_cfg(B, L, H, H, D, Ta, Tt, cl, 2000, top_k=1, evict_lag=gold["delta"], next_step=mode)
+        o = oracle_mod.Oracle(cfg, k, v, roles, pf)
+        q = f32_to_bf16(rng.standard_normal((B, L, H, D)).astype(np.float32))
+        for s, want in zip(gold["selections"], gold[key]):
+            r = o.step(q, forced=np.array([[s]]))
+            assert list(np.nonzero(r["resident"][0])[0]) == want
+
+
+def test_tidal_and_fixed_attend_over_their_key_sets(oracle_mod):
+    """Tidal heads: kept rows + resident chunks + text; fixed heads: kept rows + text
+    (library attention with a boolean mask built from the keep flags and the resident set)."""
+    o, k, v, roles, pf, q = _small(oracle_mod, seed=13, Ta=64, Tt=4, cl=8, budget=2500)
+    B, L, Hq, D = q.shape
+    H = k.shape[2]
+    g = Hq // H
+    for step in range(4):
+        qs = f32_to_bf16((np.random.default_rng(100 + step).standard_normal(q.shape)).astype(np.float32))
+        r = o.step(qs)
+        for b, l, hq in itertools.product(range(B), range(L), range(Hq)):
+            h = hq // g
+            mask = np.ones(68, dtype=bool)
+            if roles[l, h] != 0:
+                keep = o.keep_mask(b, l, h).astype(bool)
+                if roles[l, h] == 1:
+                    keep |= np.repeat(r["resident"][b].astype(bool), 8)[:64]
+                mask[:64] = keep
+            ref = _sdpa(qs[b, l, hq], k[b, l, h], v[b, l, h], mask)
+            np.testing.assert_allclose(r["out"][b, l, hq], ref, rtol=0, atol=1e-12)
+
+
+def test_next_step_equals_same_step_with_previous_selection(oracle_mod):
+    """With next-step timing, step s uses the resident set of step s-1: the same as running the
+    same-step oracle on the selections shifted by one step (nothing selected at step 0)."""
+    rng = np.random.default_rng(17)
+    B, L, H, g, D, Ta, Tt, cl = 2, 2, 3, 2, 8, 96, 4, 8
+    k, v = _rand_cache(rng, B, L, H, Ta + Tt, D)
+    roles = np.array([[0, 1, 2], [1, 1, 0]], dtype=np.uint8)
+    pf = rng.random((B, L, H, Ta), dtype=np.float32)
+    nxt = oracle_mod.Oracle(oracle_mod.make_cfg(B, L, H * g, H, D, Ta, Tt, cl, 2500, next_step=1), k, v, roles, pf)
+    same = oracle_mod.Oracle(oracle_mod.make_cfg(B, L, H * g, H, D, Ta, Tt, cl, 2500), k, v, roles, pf)
+    prev_sel = np.full((B, nxt.k), -1, dtype=np.int32)
+    for s in range(6):
+        q = f32_to_bf16(rng.standard_normal((B, L, H * g, D)).astype(np.float32))
+        a = nxt.step(q)
+        b_ = same.step(q, forced=prev_sel)
+        np.testing.assert_array_equal(a["out"], b_["out"])
+        np.testing.assert_array_equal(a["resident"], b_["resident"])
+        prev_sel = a["selected"].copy()
+
+
+def test_single_text_row_and_dominant_logit(oracle_mod):
+    """Budget 0 leaves a fixed head one text row: its output is that V row.  A key with a huge
+    logit takes all the mass: the anchor output is that key's V row."""
+    rng = np.random.default_rng(19)
+    B, L, H, D, Ta, Tt, cl = 1, 1, 2, 8, 24, 1, 8
+    k, v = _rand_cache(rng, B, L, H, Ta + Tt, D)
+    q = f32_to_bf16(rng.standard_normal((B, L, H, D)).astype(np.float32))
+    k[0, 0, 0, 5] = f32_to_bf16(bf16_to_f32(q[0, 0, 0]) * 64.0)    # logit ~ 64 |q|^2 / sqrt(d)
+    roles = np.array([[0, 2]], dtype=np.uint8)
+    pf = rng.random((B, L, H, Ta), dtype=np.float32)
+    o = oracle_mod.Oracle(oracle_mod.make_cfg(B, L, H, H, D, Ta, Tt, cl, 0), k, v, roles, pf)
+    assert o.k == 0 and o.keep_total == 0
+    r = o.step(q)
+    np.testing.assert_array_equal(r["out"][0, 0, 1], bf16_to_f32(v[0, 0, 1, Ta]).astype(np.float64))
+    np.testing.assert_allclose(r["out"][0, 0, 0], bf16_to_f32(v[0, 0, 0, 5]), rtol=0, atol=1e-9)
+    assert r["mass"][0, 0].argmax() == 0 and abs(r["mass"][0, 0, 0] - 1.0) < 1e-9
+
+
+def test_chunk_structure_worked_values(oracle_mod):
+    gold = json.load(open(os.path.join(GOLD, "chunk_structure.json")))
+    for c in gold["cases"]:
+        assert oracle_mod.tokens_for_window(gold["window_seconds"]["chunk"], c["rate"]) == c["chunk_tokens"]
+        assert oracle_mod.tokens_for_window(gold["window_seconds"]["segment"], c["rate"]) == c["segment_tokens"]
+
+
+def test_workload_geometry(oracle_mod):
+    gold = json.load(open(os.path.join(GOLD, "workload_geometry.json")))
+    for c in gold["cases"]:
+        cfg = oracle_mod.make_cfg(1, 1, 4, 1, 128, c["audio_len"], 16, c["chunk_len"], c["budget_bp"])
+        assert oracle_mod.geometry(cfg) == (c["n_chunks"], c["k"], c["keep_total"])
+
+
+def test_selection_is_topk_of_fp32_scores(oracle_mod):
+    """The oracle's selection is the brute-force top-k of its own scores rounded to fp32."""
+    o, k, v, roles, pf, q = _small(oracle_mod, seed=23, Ta=96, Tt=4, cl=8, budget=2500)
+    for s in range(3):
+        qs = f32_to_bf16(np.random.default_rng(200 + s).standard_normal(q.shape).astype(np.float32))
+        r = o.step(qs)
+        for b in range(q.shape[0]):
+            assert list(r["selected"][b]) == _brute_topk(list(r["scores"][b].astype(np.float32)), o.k)
+
+
+def test_invalid_configurations_rejected(oracle_mod):
+    bad = [dict(chunk_len=0), dict(budget_bp=10001), dict(top_k=99), dict(q_heads=5)]
+    for b in bad:
+        kw = dict(batch=1, layers=1, q_heads=4, kv_heads=2, head_dim=8, audio_len=64, text_len=2,
+                  chunk_len=8, budget_bp=2000)
+        kw.update(b)
+        with pytest.raises(ValueError):
+            oracle_mod.geometry(oracle_mod.make_cfg(**kw))
