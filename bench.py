@@ -1,0 +1,166 @@
+"""Benchmark of the WnW per-token decode step on one MI355X.
+
+A step is one call of wnw_decode_step: anchor attention with chunk mass, chunk scores, top-k
+and residency, recall of newly resident complements, tidal and fixed attention, merge.
+Inputs are seeded synthetic caches of the Voxtral-mini-3B shape at 10 minutes of audio
+(30 layers, 32 query / 8 KV heads, d 128, 15 000 audio + 512 text positions, chunk 64, 20 %
+on-GPU budget; 24 anchor / 120 tidal / 96 fixed KV-heads), resident in HBM before timing.
+
+Prints one JSON line: steps/s (value), per-kernel HBM rates from HIP events recorded around the
+kernels inside the library over the timed region, the recall rate, and the CPU oracle timed on
+a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "WnW decode steps/sec + achieved HBM GB/s (attn) at 15k audio tokens, 1 GPU"
+PEAK_HBM_GBPS = 8000.0
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=16)
+    ap.add_argument("--workload", default=None, help="workload name from synth.configs (default: the 15k-audio one)")
+    ap.add_argument("--recall", choices=("kernel", "memcpy"), default="kernel")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU oracle sample (0 = skip)")
+    ap.add_argument("--no-timing", action="store_true", help="no per-kernel events (for profiler runs)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: --gpus {args.gpus} is not supported by this build "
+              "(the decode step is measured on one MI355X)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2608_22704_amd import wnw as W
+    from synth import configs, gen
+
+    w = configs.BY_NAME[args.workload] if args.workload else configs.HEADLINE
+    torch.cuda.set_device(0)
+    B, L, H, T, D, S = w.batch, w.layers, w.kv_heads, w.total_len, w.head_dim, w.steps
+    log(f"[bench] generating {w.name} (B={B}, L={L}, Hkv={H}, T={T})")
+    t0 = time.time()
+    roles = gen.roles(w)
+    kd = torch.empty((B, L, H, T, D), dtype=torch.int16, device="cuda")
+    vd = torch.empty_like(kd)
+    qd = torch.empty((S, B, L, w.q_heads, D), dtype=torch.int16, device="cuda")
+    prefill = np.empty((B, L, H, w.audio_len), dtype=np.float32)
+    host0 = None
+    for b in range(B):
+        for l, kl, vl, ql, pl in gen.iter_layers(w, b):
+            kd[b, l].copy_(torch.from_numpy(kl.view(np.int16)))
+            vd[b, l].copy_(torch.from_numpy(vl.view(np.int16)))
+            qd[:, b, l].copy_(torch.from_numpy(ql.view(np.int16)))
+            prefill[b, l] = pl
+    torch.cuda.synchronize()
+    log(f"[bench] inputs resident in HBM after {time.time() - t0:.1f}s")
+
+    flags = (0 if args.no_timing else W.WNW_F_TIMING) | (W.WNW_F_RECALL_MEMCPY if args.recall == "memcpy" else 0)
+    cfg = W.make_config(B, L, w.q_heads, H, w.audio_len, w.text_len, w.chunk_len, w.budget_bp, flags=flags)
+    stream = torch.cuda.current_stream()
+    ctx = W.wnw_init_cache(cfg, kd, vd, stream)
+    W.wnw_set_roles(ctx, roles, prefill)
+    geo = W.wnw_query_geometry(ctx)
+    del kd, vd
+    torch.cuda.empty_cache()
+    out = torch.empty((B, L, w.q_heads, D), dtype=torch.float32, device="cuda")
+    sc = torch.empty((B, geo["n_chunks"]), dtype=torch.float32, device="cuda")
+    sel = torch.empty((B, max(geo["k"], 1)), dtype=torch.int32, device="cuda")
+    log(f"[bench] set-up done: {geo}")
+
+    for s in range(args.warmup):
+        W.wnw_decode_step(ctx, qd[s % S], out, sc, sel, stream)
+    torch.cuda.synchronize()
+    st0 = W.wnw_get_stats(ctx)
+    log(f"[bench] warm-up done ({args.warmup} steps); timing {args.steps} steps")
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(args.steps):
+        W.wnw_decode_step(ctx, qd[(args.warmup + i) % S], out, sc, sel, stream)
+    torch.cuda.synchronize()
+    t_el = time.perf_counter() - t_start
+    st1 = W.wnw_get_stats(ctx)
+    log(f"[bench] timed region {t_el * 1e3:.1f} ms")
+    W.wnw_destroy(ctx)
+
+    K = args.steps
+    d = {k: st1[k] - st0[k] for k in st1 if isinstance(st1[k], (int, float))}
+    ms_step = t_el * 1e3 / K
+    res = {
+        "metric": METRIC, "value": K / t_el, "unit": "steps/s", "n_gpus": 1, "steps": K, "warmup": args.warmup,
+        "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": w.name, "batch": B, "layers": L, "q_heads": w.q_heads, "kv_heads": H,
+                   "head_dim": D, "audio_len": w.audio_len, "text_len": w.text_len, "chunk_len": w.chunk_len,
+                   "budget_bp": w.budget_bp, "roles": [w.n_anchor, w.n_tidal, w.n_fixed], "kv_storage": "bf16",
+                   "recall": args.recall},
+    }
+    chunk_mb = geo.get("chunk_bytes", 0) / 1e6
+    rec = {"new_chunks_per_step": d["recalled_chunks"] / K / B, "MB_per_step": d["recalled_bytes"] / K / 1e6,
+           "chunk_MB": chunk_mb}
+    if not args.no_timing and d["timed_steps"] > 0:
+        n = d["timed_steps"]
+        kern = {}
+        for name, key, nbytes in (("anchor_attn", "t_anchor_ms", st1["anchor_bytes"]),
+                                  ("subset_static", "t_static_ms", st1["static_bytes"])):
+            ms = d[key] / n
+            kern[name] = {"avg_ms": ms, "bytes": nbytes, "GBps": nbytes / ms / 1e6}
+        kern["select"] = {"avg_ms": d["t_select_ms"] / n}
+        kern["subset_kept"] = {"avg_ms": d["t_kept_ms"] / n}
+        kern["subset_new"] = {"avg_ms": d["t_new_ms"] / n}
+        kern["combine"] = {"avg_ms": d["t_combine_ms"] / n}
+        kern["step_gpu"] = {"avg_ms": d["t_step_ms"] / n}
+        rec["avg_ms"] = d["t_recall_ms"] / n
+        rec["GBps"] = (d["recalled_bytes"] / n) / rec["avg_ms"] / 1e6 if rec["avg_ms"] > 0 else None
+        res["kernels"] = kern
+        dom = kern["subset_static"]
+        res["roofline"] = {"bound": "hbm", "kernel": "subset_static", "achieved": dom["GBps"],
+                           "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": dom["GBps"] / PEAK_HBM_GBPS,
+                           "traffic": None}
+    res["recall"] = rec
+    res["r_gpu"] = st1["r_gpu"]
+    res["r_gpu_cpu"] = st1["r_gpu_cpu"]
+
+    if args.cpu_seconds > 0:
+        res["cpu_baseline"] = cpu_baseline(w, roles, prefill, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+def cpu_baseline(w, roles, prefill, budget_s):
+    """The CPU oracle on the first decode steps of sequence 0 of the same workload, all heads,
+    OpenMP across heads; steps/s over a bounded sample."""
+    from oracle import oracle as O
+    from synth import gen
+
+    log(f"[bench] CPU oracle sample (~{budget_s:.0f}s)")
+    seq = gen.sequence(w.with_(batch=1), 0) if w.batch == 1 else gen.sequence(w, 0)
+    o = O.Oracle(O.cfg_from_workload(w, batch=1), seq["k"][None], seq["v"][None], roles, prefill[:1])
+    n, t0 = 0, time.perf_counter()
+    while n == 0 or (time.perf_counter() - t0 < budget_s and n < w.steps):
+        o.step(seq["q"][n][None])
+        n += 1
+    el = time.perf_counter() - t0
+    o.close()
+    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return {"value": n / el, "unit": "steps/s", "cores": cores, "kind": "oracle",
+            "sample": f"first {n} decode steps of sequence 0 of {w.name}, every head, double precision ({el:.1f}s)"}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,184 @@
+/*
+ * wnw.h - C ABI of the WnW per-token decode step on one MI355X (gfx950).
+ *
+ * WnW (Waxing-and-Waning KV cache, arXiv 2608.22704) splits the KV-heads of a speech LLM into
+ * three roles (Method, "Three-Way Classification"):
+ *   anchor - keeps all of its audio KV on the GPU; its decode-time attention is the signal;
+ *   tidal  - keeps a per-segment prefill subset on the GPU and its complement in host memory,
+ *            from which chunks are recalled on demand;
+ *   fixed  - keeps the prefill subset only.
+ * Text (non-audio) KV is always kept in full (the remark under the retention equation, Eq. 1).
+ *
+ * One decode step (Method, "Decode-Step Score Aggregation", Eq. 2, and "Dynamic Chunk
+ * Selection") does, for every sequence of the batch:
+ *   1. attention of every anchor head over its full audio + text KV, which also yields the
+ *      softmax mass each anchor q-head puts on every audio chunk (Eq. 2, reset every step);
+ *   2. chunk scores = the mean over the chunk's positions of the mass summed over all anchor
+ *      (layer, q-head) pairs, and a top-k chunk selection;
+ *   3. recall of the complement of newly resident chunks from pinned host memory into tidal-head
+ *      slots; a chunk left unselected for delta consecutive steps is dropped from the GPU (its
+ *      host copy persists);
+ *   4. attention of tidal heads over kept rows + resident complements + text, and of fixed heads
+ *      over kept rows + text.
+ *
+ * Layout conventions (all row-major, bf16 = 16-bit brain float):
+ *   K/V cache  [B][L][H_kv][T_a + T_t][d]  audio rows first, then text rows
+ *   q          [B][L][H_q][d]              q-head hq belongs to KV-head hq / (H_q / H_kv)
+ *   out        [B][L][H_q][d]              fp32
+ *   scores     [B][n_chunks]               fp32
+ *   selected   [B][k]                      int32 chunk ids, ascending
+ *
+ * Chunks are disjoint runs of chunk_len audio positions (a chunk is one segment; the last chunk
+ * may be shorter).  k defaults to floor(budget * T_a / chunk_len); each tidal/fixed head keeps
+ * floor(budget * len) positions of every chunk, chosen by the caller's prefill scores (Method,
+ * "Prefill Compression"); ties prefer the lower position.  Chunk ranking breaks ties by the lower
+ * chunk id.  A chunk is resident at step s iff it was selected at one of the last delta steps
+ * (s - delta + 1 .. s).
+ *
+ * Errors: every call returns a wnw_status; no C++ exception crosses the ABI.  A failing HIP call
+ * turns the context sticky: every later call on it returns WNW_ERR_STATE.  wnw_last_error gives
+ * the message (per context, or per thread when ctx is NULL).
+ *
+ * Threading: a context is not thread-safe.  Calls on one GPU that share a context must be
+ * serialised by the caller.
+ */
+#ifndef WNW_H
+#define WNW_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    WNW_OK = 0,
+    WNW_ERR_INVALID = -1,      /* bad argument or configuration                               */
+    WNW_ERR_OOM = -2,          /* device or pinned host allocation failed                     */
+    WNW_ERR_HIP = -3,          /* a HIP runtime call failed (context is now sticky)           */
+    WNW_ERR_STATE = -4,        /* call out of order, or context in the sticky error state     */
+    WNW_ERR_UNSUPPORTED = -5   /* configuration outside what this build implements           */
+} wnw_status;
+
+typedef enum { WNW_ANCHOR = 0, WNW_TIDAL = 1, WNW_FIXED = 2 } wnw_role;
+
+enum {
+    /* Tidal heads of step s attend over the resident set left by step s-1 (the paper's timing:
+     * selection happens after the step); default is the same step. */
+    WNW_F_SELECT_NEXT_STEP = 1u,
+    /* Recall with hipMemcpyAsync on a side stream after one host wait per step, instead of
+     * the default device-side gather from mapped pinned memory. */
+    WNW_F_RECALL_MEMCPY = 2u,
+    /* Record HIP events around the kernels of every step; wnw_get_stats reports the times. */
+    WNW_F_TIMING = 4u
+};
+
+typedef struct wnw_ctx wnw_ctx;
+
+typedef struct {
+    int32_t batch;        /* B >= 1                                                  */
+    int32_t layers;       /* L >= 1                                                  */
+    int32_t q_heads;      /* H_q, a multiple of kv_heads; H_q / H_kv in {1,2,3,4,6,8} */
+    int32_t kv_heads;     /* H_kv >= 1                                               */
+    int32_t head_dim;     /* d; must be 128                                          */
+    int32_t audio_len;    /* T_a >= 0 audio positions (same for every sequence)      */
+    int32_t text_len;     /* T_t >= 0 text positions                                 */
+    int32_t chunk_len;    /* 1 .. 256 audio positions per chunk                      */
+    int32_t budget_bp;    /* on-GPU audio retention in basis points, 0 .. 10000      */
+    int32_t top_k;        /* chunks selected per step; 0 = budget-derived            */
+    int32_t evict_lag;    /* delta >= 1; 0 = 3                                       */
+    uint32_t flags;       /* WNW_F_* bits                                            */
+} wnw_config;
+
+typedef struct {
+    int64_t steps;             /* decode steps run                                       */
+    int64_t recalled_chunks;   /* (sequence, chunk) complements copied host -> device    */
+    int64_t recalled_bytes;    /* bytes copied host -> device                            */
+    int64_t dropped_chunks;    /* (sequence, chunk) complements dropped from the device  */
+    int64_t resident_chunks;   /* sum over steps and sequences of resident chunks        */
+    int32_t peak_resident;     /* largest resident set of one sequence                   */
+    int32_t n_slots;           /* recall slots per sequence                              */
+    double r_gpu;              /* paper's r_GPU: device-resident audio KV / full audio KV,
+                                  with the mean resident set over the steps run           */
+    double r_gpu_cpu;          /* paper's r_GPU+CPU: adds the host-resident complement   */
+    int64_t anchor_bytes;      /* algorithmic HBM bytes of one anchor-attention launch   */
+    int64_t static_bytes;      /* algorithmic HBM bytes of one fixed + tidal-kept-rows launch */
+    int64_t slot_rows;         /* complement rows attended, summed over steps            */
+    /* WNW_F_TIMING only: summed kernel times (ms) and the number of timed steps. */
+    int64_t timed_steps;
+    double t_anchor_ms;        /* anchor attention + chunk mass                          */
+    double t_select_ms;        /* combine, scores, top-k and residency                   */
+    double t_static_ms;        /* fixed heads + tidal kept rows                          */
+    double t_kept_ms;          /* tidal complements already resident                     */
+    double t_recall_ms;        /* host -> device recall (side stream)                    */
+    double t_new_ms;           /* tidal complements recalled this step                   */
+    double t_combine_ms;       /* merge of the tidal/fixed partial results               */
+    double t_step_ms;          /* whole step on the caller's stream                      */
+} wnw_stats;
+
+/* Create a context for one batch of caches.
+ *   cfg        copied; validated here (WNW_ERR_INVALID / WNW_ERR_UNSUPPORTED).
+ *   k_dev/v_dev  device bf16 [B][L][H_kv][T_a+T_t][d], owned by the caller, read only by
+ *              wnw_set_roles; they may be freed once it has returned.
+ *   hip_stream stream for the set-up work (NULL = the null stream).
+ *   out        receives the context; NULL on failure.
+ * Allocates nothing until wnw_set_roles. */
+wnw_status wnw_init_cache(const wnw_config *cfg, const void *k_dev, const void *v_dev,
+                          void *hip_stream, wnw_ctx **out);
+
+/* Assign roles and run prefill compression (Method, "Prefill Compression"): every tidal and
+ * fixed head keeps floor(budget * len) positions of each chunk with the highest prefill score.
+ *   roles           host uint8 [L][H_kv] of wnw_role, shared by the batch.
+ *   prefill_scores  host fp32 [B][L][H_kv][T_a]; entries of anchor heads are ignored.
+ * Builds the device tiers (anchor rows, kept rows, recall slots) and the pinned host
+ * complement, then waits for the copies.  Exactly once per context, after wnw_init_cache. */
+wnw_status wnw_set_roles(wnw_ctx *ctx, const uint8_t *roles, const float *prefill_scores);
+
+/* One decode step (Eq. 2 and "Dynamic Chunk Selection"), enqueued on hip_stream.
+ *   q_dev             device bf16 [B][L][H_q][d]
+ *   out_dev           device fp32 [B][L][H_q][d]     attention output of every q-head
+ *   chunk_scores_dev  device fp32 [B][n_chunks]      this step's chunk scores
+ *   selected_dev      device int32 [B][k]            selected chunk ids, ascending
+ *   hip_stream        caller's stream (NULL = null stream); outputs are valid once it has
+ *                     completed.  Buffers must stay valid until then.
+ * The default recall path does not block the host.  With WNW_F_RECALL_MEMCPY the call waits
+ * once, mid-step, for the selection before issuing the copies. */
+wnw_status wnw_decode_step(wnw_ctx *ctx, const void *q_dev, float *out_dev,
+                           float *chunk_scores_dev, int32_t *selected_dev, void *hip_stream);
+
+/* Derived sizes: chunks, k, kept audio rows per tidal/fixed head, recall slots per sequence,
+ * and bytes of one recalled chunk of one sequence.  Any pointer may be NULL. */
+wnw_status wnw_query_geometry(const wnw_ctx *ctx, int32_t *n_chunks, int32_t *k,
+                              int32_t *keep_total, int32_t *n_slots, int64_t *chunk_bytes);
+
+/* Counters and (with WNW_F_TIMING) kernel times; waits for the device. */
+wnw_status wnw_get_stats(wnw_ctx *ctx, wnw_stats *out);
+
+/* Replace the top-k of the following steps by the ids in sel_dev (device int32 [B][k], read
+ * when each step runs; -1 = no chunk; ids distinct, < n_chunks).  NULL restores the top-k.
+ * Scores are still computed.  Used to keep two implementations on one trajectory and to force
+ * a recall load. */
+wnw_status wnw_set_selection_override(wnw_ctx *ctx, const int32_t *sel_dev);
+
+/* Copy the device slot holding the recalled complement of (b, chunk) to host_dst (waits for
+ * the device).  Layout [n_tidal][2 (K, V)][comp_max][d] bf16; `bytes` must equal chunk_bytes.
+ * WNW_ERR_INVALID if that chunk is not resident. */
+wnw_status wnw_debug_read_slot(wnw_ctx *ctx, int32_t b, int32_t chunk, void *host_dst, size_t bytes);
+
+/* Copy the host (pinned) complement of (b, chunk) in the same layout as wnw_debug_read_slot. */
+wnw_status wnw_debug_read_host_chunk(wnw_ctx *ctx, int32_t b, int32_t chunk, void *host_dst, size_t bytes);
+
+/* Resident flags [B][n_chunks] (uint8) left by the last step (waits for the device). */
+wnw_status wnw_debug_read_resident(wnw_ctx *ctx, uint8_t *host_dst);
+
+/* Message of the last failure on ctx (or of this thread when ctx is NULL).  Never NULL. */
+const char *wnw_last_error(const wnw_ctx *ctx);
+
+/* Free every device, pinned and stream resource of ctx (waits for its work).  NULL is a no-op. */
+void wnw_destroy(wnw_ctx *ctx);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* WNW_H */

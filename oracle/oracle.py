@@ -18,12 +18,12 @@ LIB = os.path.join(HERE, "libwnw_oracle.so")
 
 def build(verbose: bool = False) -> str:
     """Compile the oracle with gcc (C99, OpenMP)."""
-    cmd = ["gcc", "-O2", "-std=c99", "-fopenmp", "-fPIC", "-shared", "-Wall", "-Wextra",
-           "-o", LIB + ".tmp", SRC, "-lm"]
+    tmp = f"{LIB}.tmp{os.getpid()}"
+    cmd = ["gcc", "-O2", "-std=c99", "-fopenmp", "-fPIC", "-shared", "-Wall", "-Wextra", "-o", tmp, SRC, "-lm"]
     if verbose:
         print(" ".join(cmd))
     subprocess.run(cmd, check=True)
-    os.replace(LIB + ".tmp", LIB)
+    os.replace(tmp, LIB)
     return LIB
 
 

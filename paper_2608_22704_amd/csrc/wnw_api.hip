@@ -1,0 +1,671 @@
+// Host orchestrator of the WnW decode step: the C ABI of include/wnw.h.
+//
+// Set-up (wnw_set_roles) performs the paper's prefill compression on the host (per segment,
+// keep the floor(retention * len) positions with the highest prefill score) and lays the cache
+// out in device tiers:
+//   anchor tier   [B][nA][T][d]       every row of every anchor head
+//   tidal tier    [B][nT][Rs][d]      kept audio rows (ascending) + text rows, Rs = keep + T_t
+//   fixed tier    [B][nF][Rs][d]      same for fixed heads (their complement is dropped)
+//   slots         [B][n_slots][nT][2][comp_max][d]   recalled complements, n_slots = delta * k
+//   host complement (pinned) [B][n_chunks][nT][2][comp_max][d]: chunk-major, so the complement
+//                 of one chunk for every tidal head of a sequence is one contiguous block.
+// A decode step is a fixed sequence of kernels on the caller's stream; recall runs on a side
+// stream joined by events (see wnw_decode_step below for the ordering argument).
+#include "wnw.h"
+#include "wnw_internal.h"
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <functional>
+#include <numeric>
+#include <string>
+#include <thread>
+#include <vector>
+
+using namespace wnw;
+
+namespace {
+
+thread_local std::string t_err = "no error";
+
+enum State { CREATED = 0, READY = 1, FAILED = 2 };
+
+// Timing events of one step.  e[] on the caller's stream: 0 start, 1 after anchor attention,
+// 2 after selection, 3 after fixed + tidal kept rows, 4 after resident complements, 5 after the
+// wait for the recall, 6 after newly recalled complements, 7 after the merge.  r[] on the side
+// stream around the recall.
+struct StepEvents {
+    hipEvent_t e[8];
+    hipEvent_t r[2];
+};
+
+}  // namespace
+
+struct wnw_ctx {
+    wnw_config cfg{};
+    Geometry g{};
+    State state = CREATED;
+    std::string err = "no error";
+    int device = 0;
+    hipStream_t setup_stream = nullptr;
+    const uint16_t *full_k = nullptr, *full_v = nullptr;
+    std::vector<int32_t> anchor_lk, tidal_lk, fixed_lk;
+
+    Tiers t{};
+    StepBuffers s{};
+    uint16_t *aK = nullptr, *aV = nullptr, *tK = nullptr, *tV = nullptr, *fK = nullptr, *fV = nullptr;
+    uint16_t *slots = nullptr, *host_comp = nullptr;
+    int32_t *d_lk = nullptr;
+    float *scores_int = nullptr;
+    int32_t *sel_int = nullptr;
+    const int32_t *override_sel = nullptr;
+
+    hipStream_t side = nullptr;
+    hipEvent_t ev_sel = nullptr, ev_rec = nullptr;
+    int32_t *h_newinfo = nullptr;      // pinned: counts [B][2] then new lists [B][k][2]
+
+    std::vector<StepEvents> pending, spare;
+    double t_acc[8] = {0};
+    int64_t timed_steps = 0, steps = 0;
+};
+
+namespace {
+
+wnw_status fail(wnw_ctx *c, wnw_status st, const char *fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    t_err = buf;
+    if (c) {
+        c->err = buf;
+        if (st == WNW_ERR_HIP) c->state = FAILED;
+    }
+    return st;
+}
+
+#define HIPCHECK(ctx, call)                                                                       \
+    do {                                                                                          \
+        hipError_t e_ = (call);                                                                   \
+        if (e_ != hipSuccess)                                                                     \
+            return fail(ctx, WNW_ERR_HIP, "%s failed: %s (%s:%d)", #call, hipGetErrorString(e_), \
+                        __FILE__, __LINE__);                                                      \
+    } while (0)
+
+struct DeviceGuard {
+    int prev = -1;
+    explicit DeviceGuard(int dev)
+    {
+        if (hipGetDevice(&prev) != hipSuccess) prev = -1;
+        if (prev != dev) (void)hipSetDevice(dev);
+    }
+    ~DeviceGuard()
+    {
+        int cur;
+        if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+    }
+};
+
+template <typename T>
+wnw_status dalloc(wnw_ctx *c, T **p, size_t n, const char *what)
+{
+    *p = nullptr;
+    if (n == 0) return WNW_OK;
+    hipError_t e = hipMalloc((void **)p, n * sizeof(T));
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        *p = nullptr;
+        return fail(c, e == hipErrorOutOfMemory ? WNW_ERR_OOM : WNW_ERR_HIP, "hipMalloc of %s (%zu bytes): %s", what,
+                    n * sizeof(T), hipGetErrorString(e));
+    }
+    return WNW_OK;
+}
+
+// Geometry that depends on the configuration only (roles fill nA/nT/nF later).
+wnw_status derive(wnw_ctx *c, const wnw_config &cfg, Geometry &g)
+{
+    if (cfg.batch < 1 || cfg.layers < 1 || cfg.kv_heads < 1 || cfg.q_heads < 1 || cfg.q_heads % cfg.kv_heads)
+        return fail(c, WNW_ERR_INVALID, "batch, layers, heads must be >= 1 and q_heads a multiple of kv_heads");
+    if (cfg.audio_len < 0 || cfg.text_len < 0 || cfg.audio_len + (int64_t)cfg.text_len < 1)
+        return fail(c, WNW_ERR_INVALID, "need audio_len, text_len >= 0 and at least one row");
+    if (cfg.chunk_len < 1) return fail(c, WNW_ERR_INVALID, "chunk_len must be >= 1");
+    if (cfg.budget_bp < 0 || cfg.budget_bp > 10000) return fail(c, WNW_ERR_INVALID, "budget_bp must be in 0..10000");
+    if (cfg.top_k < 0 || cfg.evict_lag < 0) return fail(c, WNW_ERR_INVALID, "top_k and evict_lag must be >= 0");
+    if (cfg.flags & ~(uint32_t)(WNW_F_SELECT_NEXT_STEP | WNW_F_RECALL_MEMCPY | WNW_F_TIMING))
+        return fail(c, WNW_ERR_INVALID, "unknown flag bits 0x%x", cfg.flags);
+    if (cfg.head_dim != D) return fail(c, WNW_ERR_UNSUPPORTED, "head_dim %d: only 128 is implemented", cfg.head_dim);
+    const int G = cfg.q_heads / cfg.kv_heads;
+    if (G != 1 && G != 2 && G != 3 && G != 4 && G != 6 && G != 8)
+        return fail(c, WNW_ERR_UNSUPPORTED, "GQA group %d: implemented for 1, 2, 3, 4, 6, 8", G);
+    if (cfg.chunk_len > TILE) return fail(c, WNW_ERR_UNSUPPORTED, "chunk_len %d > %d", cfg.chunk_len, TILE);
+    if (cfg.flags & WNW_F_SELECT_NEXT_STEP)
+        return fail(c, WNW_ERR_UNSUPPORTED, "next-step selection timing is not implemented in this build");
+
+    g = Geometry{};
+    g.B = cfg.batch;
+    g.L = cfg.layers;
+    g.Hq = cfg.q_heads;
+    g.Hkv = cfg.kv_heads;
+    g.G = G;
+    g.Ta = cfg.audio_len;
+    g.Tt = cfg.text_len;
+    g.T = g.Ta + g.Tt;
+    g.cl = cfg.chunk_len;
+    g.budget_bp = cfg.budget_bp;
+    g.nc = (g.Ta + g.cl - 1) / g.cl;
+    g.k = cfg.top_k ? cfg.top_k : (int)(((int64_t)cfg.budget_bp * g.Ta) / (10000LL * g.cl));
+    if (g.k > g.nc) return fail(c, WNW_ERR_INVALID, "top_k %d exceeds the %d chunks", g.k, g.nc);
+    g.delta = cfg.evict_lag ? cfg.evict_lag : 3;
+    g.keep_total = 0;
+    g.comp_max = 0;
+    for (int ch = 0; ch < g.nc; ++ch) {
+        const int len = chunk_len_of(g, ch);
+        g.keep_total += keep_of_len(g.budget_bp, len);
+        g.comp_max = std::max(g.comp_max, comp_of(g, ch));
+    }
+    g.Rs = g.keep_total + g.Tt;
+    if ((int64_t)g.delta * g.k > 4096) return fail(c, WNW_ERR_UNSUPPORTED, "delta * k = %lld slots > 4096", (long long)g.delta * g.k);
+    g.n_slots = g.delta * g.k;
+    if (g.nc > 4096) return fail(c, WNW_ERR_UNSUPPORTED, "%d chunks > 4096", g.nc);
+    g.n_tiles_a = (g.T + TILE - 1) / TILE;
+    if ((int64_t)g.n_tiles_a * G * 8 > 65536) return fail(c, WNW_ERR_UNSUPPORTED, "cache of %d rows too long", g.T);
+    g.maxc = (TILE - 1) / g.cl + 2;
+    g.n_tiles_s = (g.Rs + TILE - 1) / TILE;
+    g.sg = g.comp_max > 0 ? std::max(1, TILE / g.comp_max) : 1;
+    g.ng_kept = g.comp_max > 0 ? (g.n_slots + g.sg - 1) / g.sg : 0;
+    g.ng_new = g.comp_max > 0 ? (g.k + g.sg - 1) / g.sg : 0;
+    g.np = g.n_tiles_s + g.ng_kept + g.ng_new;
+    if ((int64_t)g.np * G * 4 > 65536) return fail(c, WNW_ERR_UNSUPPORTED, "too many partial tiles per head");
+    if (g.B > 65535 || (int64_t)g.L * g.Hkv > 65535) return fail(c, WNW_ERR_UNSUPPORTED, "batch or head count too large");
+    return WNW_OK;
+}
+
+// Per-segment prefill keep selection of one head (Method, "Prefill Compression").
+void keep_rows(const Geometry &g, const float *score, std::vector<int32_t> &kept, std::vector<int32_t> &comp_by_chunk)
+{
+    kept.clear();
+    comp_by_chunk.assign((size_t)g.nc * g.comp_max, -1);
+    std::vector<int32_t> pos;
+    for (int ch = 0; ch < g.nc; ++ch) {
+        const int b0 = ch * g.cl, len = chunk_len_of(g, ch), kc = keep_of_len(g.budget_bp, len);
+        pos.resize(len);
+        std::iota(pos.begin(), pos.end(), b0);
+        std::stable_sort(pos.begin(), pos.end(), [&](int32_t a, int32_t b) {
+            if (score[a] != score[b]) return score[a] > score[b];
+            return a < b;
+        });
+        std::sort(pos.begin(), pos.begin() + kc);
+        std::sort(pos.begin() + kc, pos.end());
+        kept.insert(kept.end(), pos.begin(), pos.begin() + kc);
+        std::copy(pos.begin() + kc, pos.end(), comp_by_chunk.begin() + (size_t)ch * g.comp_max);
+    }
+}
+
+void parallel_for(int n, const std::function<void(int)> &fn)
+{
+    int nt = (int)std::min<unsigned>(16, std::max(1u, std::thread::hardware_concurrency()));
+    nt = std::min(nt, std::max(n, 1));
+    std::vector<std::thread> th;
+    for (int w = 0; w < nt; ++w)
+        th.emplace_back([&, w] {
+            for (int i = w; i < n; i += nt) fn(i);
+        });
+    for (auto &x : th) x.join();
+}
+
+wnw_status harvest_timing(wnw_ctx *c)
+{
+    for (auto &ev : c->pending) {
+        float ms;
+        HIPCHECK(c, hipEventSynchronize(ev.e[7]));
+        HIPCHECK(c, hipEventSynchronize(ev.r[1]));
+        // anchor, select, static, kept, recall, new, combine, whole step
+        const int from[8] = {0, 1, 2, 3, -1, 5, 6, 0}, to[8] = {1, 2, 3, 4, -1, 6, 7, 7};
+        for (int i = 0; i < 8; ++i) {
+            if (from[i] < 0) {
+                HIPCHECK(c, hipEventElapsedTime(&ms, ev.r[0], ev.r[1]));
+            } else {
+                HIPCHECK(c, hipEventElapsedTime(&ms, ev.e[from[i]], ev.e[to[i]]));
+            }
+            c->t_acc[i] += ms;
+        }
+        c->timed_steps++;
+        c->spare.push_back(ev);
+    }
+    c->pending.clear();
+    return WNW_OK;
+}
+
+void free_all(wnw_ctx *c)
+{
+    void *ptrs[] = {c->aK, c->aV, c->tK, c->tV, c->fK, c->fV, c->slots, c->d_lk, c->scores_int, c->sel_int,
+                    c->s.pa_m, c->s.pa_l, c->s.pa_o, c->s.pa_mass, c->s.mass, c->s.ps_m, c->s.ps_l, c->s.ps_o,
+                    c->s.streak, c->s.slot_of, c->s.slot_chunk, c->s.kept_list, c->s.new_list, c->s.counts,
+                    c->s.stats};
+    for (void *p : ptrs)
+        if (p) (void)hipFree(p);
+    if (c->host_comp) (void)hipHostFree(c->host_comp);
+    if (c->h_newinfo) (void)hipHostFree(c->h_newinfo);
+    if (c->ev_sel) (void)hipEventDestroy(c->ev_sel);
+    if (c->ev_rec) (void)hipEventDestroy(c->ev_rec);
+    for (auto *v : {&c->pending, &c->spare})
+        for (auto &ev : *v) {
+            for (auto e : ev.e) (void)hipEventDestroy(e);
+            for (auto e : ev.r) (void)hipEventDestroy(e);
+        }
+    if (c->side) (void)hipStreamDestroy(c->side);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *wnw_last_error(const wnw_ctx *ctx)
+{
+    return ctx ? ctx->err.c_str() : t_err.c_str();
+}
+
+wnw_status wnw_init_cache(const wnw_config *cfg, const void *k_dev, const void *v_dev, void *hip_stream, wnw_ctx **out)
+{
+    if (!out) return fail(nullptr, WNW_ERR_INVALID, "out is NULL");
+    *out = nullptr;
+    if (!cfg || !k_dev || !v_dev) return fail(nullptr, WNW_ERR_INVALID, "cfg, k_dev and v_dev must not be NULL");
+    Geometry g;
+    wnw_status st = derive(nullptr, *cfg, g);
+    if (st != WNW_OK) return st;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(nullptr, WNW_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+    wnw_ctx *c = new (std::nothrow) wnw_ctx();
+    if (!c) return fail(nullptr, WNW_ERR_OOM, "context allocation failed");
+    c->cfg = *cfg;
+    c->g = g;
+    c->device = dev;
+    c->setup_stream = (hipStream_t)hip_stream;
+    c->full_k = (const uint16_t *)k_dev;
+    c->full_v = (const uint16_t *)v_dev;
+    *out = c;
+    return WNW_OK;
+}
+
+wnw_status wnw_set_roles(wnw_ctx *c, const uint8_t *roles, const float *prefill)
+{
+    if (!c) return fail(nullptr, WNW_ERR_INVALID, "ctx is NULL");
+    if (c->state != CREATED) return fail(c, WNW_ERR_STATE, "wnw_set_roles must be called once, right after wnw_init_cache");
+    if (!roles || !prefill) return fail(c, WNW_ERR_INVALID, "roles and prefill_scores must not be NULL");
+    Geometry &g = c->g;
+    const int nh = g.L * g.Hkv;
+    for (int i = 0; i < nh; ++i) {
+        if (roles[i] > WNW_FIXED) return fail(c, WNW_ERR_INVALID, "role %d of head %d is not a wnw_role", roles[i], i);
+        (roles[i] == WNW_ANCHOR ? c->anchor_lk : roles[i] == WNW_TIDAL ? c->tidal_lk : c->fixed_lk).push_back(i);
+    }
+    g.nA = (int)c->anchor_lk.size();
+    g.nT = (int)c->tidal_lk.size();
+    g.nF = (int)c->fixed_lk.size();
+    g.chunk_elems = (int64_t)g.nT * 2 * g.comp_max * D;
+    DeviceGuard dg(c->device);
+    hipStream_t st = c->setup_stream;
+    const size_t B = g.B, Dz = D;
+
+    // ---- allocations ------------------------------------------------------------------
+    wnw_status r;
+#define ALLOC(p, n, what) \
+    if ((r = dalloc(c, &(p), (size_t)(n), what)) != WNW_OK) return r
+    ALLOC(c->aK, B * g.nA * g.T * Dz, "anchor K");
+    ALLOC(c->aV, B * g.nA * g.T * Dz, "anchor V");
+    ALLOC(c->tK, B * g.nT * g.Rs * Dz, "tidal K");
+    ALLOC(c->tV, B * g.nT * g.Rs * Dz, "tidal V");
+    ALLOC(c->fK, B * g.nF * g.Rs * Dz, "fixed K");
+    ALLOC(c->fV, B * g.nF * g.Rs * Dz, "fixed V");
+    ALLOC(c->slots, B * g.n_slots * g.chunk_elems, "recall slots");
+    ALLOC(c->d_lk, (size_t)nh, "role tables");
+    ALLOC(c->scores_int, B * g.nc, "scores");
+    ALLOC(c->sel_int, B * g.k, "selection");
+    StepBuffers &s = c->s;
+    ALLOC(s.pa_m, B * g.nA * g.n_tiles_a * g.G, "anchor partial max");
+    ALLOC(s.pa_l, B * g.nA * g.n_tiles_a * g.G, "anchor partial sum");
+    ALLOC(s.pa_o, B * g.nA * g.n_tiles_a * g.G * Dz, "anchor partial out");
+    ALLOC(s.pa_mass, B * g.nA * g.n_tiles_a * g.G * g.maxc, "anchor partial mass");
+    ALLOC(s.mass, B * g.nA * g.G * g.nc, "chunk mass");
+    ALLOC(s.ps_m, B * (g.nT + g.nF) * g.np * g.G, "partial max");
+    ALLOC(s.ps_l, B * (g.nT + g.nF) * g.np * g.G, "partial sum");
+    ALLOC(s.ps_o, B * (g.nT + g.nF) * g.np * g.G * Dz, "partial out");
+    ALLOC(s.streak, B * g.nc, "streaks");
+    ALLOC(s.slot_of, B * g.nc, "slot map");
+    ALLOC(s.slot_chunk, B * g.n_slots, "slot owners");
+    ALLOC(s.kept_list, B * g.n_slots * 2, "kept list");
+    ALLOC(s.new_list, B * g.k * 2, "new list");
+    ALLOC(s.counts, B * 2, "counts");
+    ALLOC(s.stats, 8, "stats");
+#undef ALLOC
+    const size_t host_bytes = B * g.nc * (size_t)g.chunk_elems * sizeof(uint16_t);
+    if (host_bytes) {
+        hipError_t e = hipHostMalloc((void **)&c->host_comp, host_bytes, hipHostMallocDefault);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            c->host_comp = nullptr;
+            return fail(c, WNW_ERR_OOM, "pinned complement of %zu bytes: %s", host_bytes, hipGetErrorString(e));
+        }
+        void *dp = nullptr;
+        HIPCHECK(c, hipHostGetDevicePointer(&dp, c->host_comp, 0));
+        c->t.host_comp = (const uint16_t *)dp;
+    }
+    HIPCHECK(c, hipHostMalloc((void **)&c->h_newinfo, (B * 2 + B * g.k * 2 + 1) * sizeof(int32_t), hipHostMallocDefault));
+    HIPCHECK(c, hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking));
+    HIPCHECK(c, hipEventCreateWithFlags(&c->ev_sel, hipEventDisableTiming));
+    HIPCHECK(c, hipEventCreateWithFlags(&c->ev_rec, hipEventDisableTiming));
+
+    std::vector<int32_t> lk;
+    lk.insert(lk.end(), c->anchor_lk.begin(), c->anchor_lk.end());
+    lk.insert(lk.end(), c->tidal_lk.begin(), c->tidal_lk.end());
+    lk.insert(lk.end(), c->fixed_lk.begin(), c->fixed_lk.end());
+    if (nh) HIPCHECK(c, hipMemcpy(c->d_lk, lk.data(), nh * sizeof(int32_t), hipMemcpyHostToDevice));
+    c->t.anchor_lk = c->d_lk;
+    c->t.tidal_lk = c->d_lk + g.nA;
+    c->t.fixed_lk = c->d_lk + g.nA + g.nT;
+    c->t.aK = c->aK; c->t.aV = c->aV;
+    c->t.tK = c->tK; c->t.tV = c->tV;
+    c->t.fK = c->fK; c->t.fV = c->fV;
+    c->t.slots = c->slots;
+
+    // ---- per-sequence tier construction ------------------------------------------------------
+    const int nsub = g.nT + g.nF;
+    const size_t seq_rows = (size_t)g.L * g.Hkv * g.T;
+    std::vector<int32_t> static_idx((size_t)nsub * g.Rs), comp_idx((size_t)g.nc * g.nT * 2 * g.comp_max);
+    int32_t *d_idx = nullptr;
+    uint16_t *staging = nullptr;
+    const size_t idx_n = std::max(static_idx.size(), comp_idx.size());
+    if ((r = dalloc(c, &d_idx, idx_n, "set-up index")) != WNW_OK) return r;
+    if ((r = dalloc(c, &staging, (size_t)g.nc * g.chunk_elems, "complement staging")) != WNW_OK) {
+        (void)hipFree(d_idx);
+        return r;
+    }
+    auto cleanup = [&] {
+        (void)hipStreamSynchronize(st);
+        if (d_idx) (void)hipFree(d_idx);
+        if (staging) (void)hipFree(staging);
+    };
+    for (int b = 0; b < g.B; ++b) {
+        const uint16_t *fk = c->full_k + b * seq_rows * D, *fv = c->full_v + b * seq_rows * D;
+        // anchors: every row, one contiguous copy per head
+        for (int a = 0; a < g.nA; ++a) {
+            const size_t src = (size_t)c->anchor_lk[a] * g.T * D, dst = (((size_t)b * g.nA + a) * g.T) * D;
+            const size_t bytes = (size_t)g.T * D * sizeof(uint16_t);
+            hipError_t e1 = hipMemcpyAsync(c->aK + dst, fk + src, bytes, hipMemcpyDeviceToDevice, st);
+            hipError_t e2 = hipMemcpyAsync(c->aV + dst, fv + src, bytes, hipMemcpyDeviceToDevice, st);
+            if (e1 != hipSuccess || e2 != hipSuccess) {
+                cleanup();
+                return fail(c, WNW_ERR_HIP, "anchor tier copy failed: %s", hipGetErrorString(e1 != hipSuccess ? e1 : e2));
+            }
+        }
+        // keep selection (host, threaded over heads)
+        parallel_for(nsub, [&](int hi) {
+            const bool tidal = hi < g.nT;
+            const int lkh = tidal ? c->tidal_lk[hi] : c->fixed_lk[hi - g.nT];
+            const float *sc = prefill + ((size_t)b * nh + lkh) * g.Ta;
+            std::vector<int32_t> kept, comp;
+            keep_rows(g, sc, kept, comp);
+            const int32_t base = (int32_t)((size_t)lkh * g.T);
+            int32_t *si = static_idx.data() + (size_t)hi * g.Rs;
+            for (int i = 0; i < g.keep_total; ++i) si[i] = base + kept[i];
+            for (int i = 0; i < g.Tt; ++i) si[g.keep_total + i] = base + g.Ta + i;
+            if (tidal)
+                for (int ch = 0; ch < g.nc; ++ch)
+                    for (int half = 0; half < 2; ++half)
+                        for (int rr = 0; rr < g.comp_max; ++rr) {
+                            const int32_t p = comp[(size_t)ch * g.comp_max + rr];
+                            // K rows index the K cache (>= 0), V rows are encoded as -(row + 2)
+                            comp_idx[(((size_t)ch * g.nT + hi) * 2 + half) * g.comp_max + rr] =
+                                p < 0 ? -1 : (half == 0 ? base + p : -(base + p) - 2);
+                        }
+        });
+        // static rows of tidal and fixed heads
+        hipError_t e = hipMemcpyAsync(d_idx, static_idx.data(), static_idx.size() * sizeof(int32_t), hipMemcpyHostToDevice, st);
+        if (e == hipSuccess && g.nT)
+            e = launch_gather_rows(c->tK + (size_t)b * g.nT * g.Rs * D, fk, fv, d_idx, (int64_t)g.nT * g.Rs, st);
+        if (e == hipSuccess && g.nT)
+            e = launch_gather_rows(c->tV + (size_t)b * g.nT * g.Rs * D, fv, fv, d_idx, (int64_t)g.nT * g.Rs, st);
+        if (e == hipSuccess && g.nF)
+            e = launch_gather_rows(c->fK + (size_t)b * g.nF * g.Rs * D, fk, fv, d_idx + (size_t)g.nT * g.Rs, (int64_t)g.nF * g.Rs, st);
+        if (e == hipSuccess && g.nF)
+            e = launch_gather_rows(c->fV + (size_t)b * g.nF * g.Rs * D, fv, fv, d_idx + (size_t)g.nT * g.Rs, (int64_t)g.nF * g.Rs, st);
+        if (e == hipSuccess) e = hipStreamSynchronize(st);   // static_idx is rewritten next
+        // tidal complement, chunk-major, then to pinned host memory
+        if (e == hipSuccess && g.chunk_elems) {
+            e = hipMemcpyAsync(d_idx, comp_idx.data(), comp_idx.size() * sizeof(int32_t), hipMemcpyHostToDevice, st);
+            if (e == hipSuccess) e = launch_gather_rows(staging, fk, fv, d_idx, (int64_t)comp_idx.size(), st);
+            if (e == hipSuccess)
+                e = hipMemcpyAsync(c->host_comp + (size_t)b * g.nc * g.chunk_elems, staging,
+                                   (size_t)g.nc * g.chunk_elems * sizeof(uint16_t), hipMemcpyDeviceToHost, st);
+            if (e == hipSuccess) e = hipStreamSynchronize(st);
+        }
+        if (e != hipSuccess) {
+            cleanup();
+            return fail(c, WNW_ERR_HIP, "tier construction failed: %s", hipGetErrorString(e));
+        }
+    }
+    cleanup();
+
+    // ---- selection state -----------------------------------------------------------------------
+    std::vector<int32_t> init(B * g.nc, g.delta);   // never selected: not resident
+    if (!init.empty()) HIPCHECK(c, hipMemcpy(s.streak, init.data(), init.size() * sizeof(int32_t), hipMemcpyHostToDevice));
+    if (g.nc) HIPCHECK(c, hipMemset(s.slot_of, 0xff, B * g.nc * sizeof(int32_t)));
+    if (g.n_slots) HIPCHECK(c, hipMemset(s.slot_chunk, 0xff, B * g.n_slots * sizeof(int32_t)));
+    HIPCHECK(c, hipMemset(s.counts, 0, B * 2 * sizeof(int32_t)));
+    HIPCHECK(c, hipMemset(s.stats, 0, 8 * sizeof(unsigned long long)));
+    HIPCHECK(c, hipDeviceSynchronize());
+    c->full_k = c->full_v = nullptr;
+    c->state = READY;
+    return WNW_OK;
+}
+
+wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, float *out, float *scores, int32_t *selected, void *hip_stream)
+{
+    if (!c) return fail(nullptr, WNW_ERR_INVALID, "ctx is NULL");
+    if (c->state != READY)
+        return fail(c, WNW_ERR_STATE, c->state == FAILED ? "context is in the error state: %s" : "%s",
+                    c->state == FAILED ? c->err.c_str() : "wnw_set_roles has not run");
+    if (!q_dev || !out) return fail(c, WNW_ERR_INVALID, "q_dev and out_dev must not be NULL");
+    DeviceGuard dg(c->device);
+    const Geometry &g = c->g;
+    hipStream_t s0 = (hipStream_t)hip_stream;
+    const uint16_t *q = (const uint16_t *)q_dev;
+    float *sc = scores ? scores : c->scores_int;
+    int32_t *sel = selected ? selected : c->sel_int;
+    const bool timing = c->cfg.flags & WNW_F_TIMING;
+    StepEvents ev{};
+    if (timing) {
+        if (!c->spare.empty()) {
+            ev = c->spare.back();
+            c->spare.pop_back();
+        } else {
+            for (auto &e : ev.e) HIPCHECK(c, hipEventCreate(&e));
+            for (auto &e : ev.r) HIPCHECK(c, hipEventCreate(&e));
+        }
+    }
+#define MARK(i) \
+    if (timing) HIPCHECK(c, hipEventRecord(ev.e[i], s0))
+
+    // (1) anchor attention + chunk mass, (2) scores, top-k and residency
+    MARK(0);
+    HIPCHECK(c, launch_anchor(g, c->t, c->s, q, s0));
+    MARK(1);
+    HIPCHECK(c, launch_anchor_combine(g, c->t, c->s, out, s0));
+    HIPCHECK(c, launch_scores(g, c->s, sc, s0));
+    HIPCHECK(c, launch_select(g, c->s, sc, c->override_sel, sel, s0));
+    const bool memcpy_path = c->cfg.flags & WNW_F_RECALL_MEMCPY;
+    if (memcpy_path) {
+        HIPCHECK(c, hipMemcpyAsync(c->h_newinfo, c->s.counts, g.B * 2 * sizeof(int32_t), hipMemcpyDeviceToHost, s0));
+        if (g.k)
+            HIPCHECK(c, hipMemcpyAsync(c->h_newinfo + g.B * 2, c->s.new_list, (size_t)g.B * g.k * 2 * sizeof(int32_t),
+                                       hipMemcpyDeviceToHost, s0));
+    }
+    HIPCHECK(c, hipEventRecord(c->ev_sel, s0));
+    MARK(2);
+    // (3) recall on the side stream.  The new chunks' slots were freed by this step's select
+    // kernel; every kernel that could still read them (the previous step's) precedes it on s0,
+    // and the copy starts only after ev_sel, so no reader races the copy.  Nothing on s0 reads
+    // a new slot before it waits for ev_rec.
+    // (4a) meanwhile on s0: fixed heads and tidal kept rows, then complements that were already
+    // resident before this step.
+    HIPCHECK(c, launch_subset_static(g, c->t, c->s, q, s0));
+    MARK(3);
+    HIPCHECK(c, launch_subset_slots(g, c->t, c->s, q, false, s0));
+    MARK(4);
+    HIPCHECK(c, hipStreamWaitEvent(c->side, c->ev_sel, 0));
+    if (timing) HIPCHECK(c, hipEventRecord(ev.r[0], c->side));
+    if (memcpy_path) {
+        HIPCHECK(c, hipEventSynchronize(c->ev_sel));
+        const int32_t *cnt = c->h_newinfo, *nl = c->h_newinfo + g.B * 2;
+        const size_t cb = (size_t)g.chunk_elems * sizeof(uint16_t);
+        for (int b = 0; b < g.B && cb; ++b) {
+            const int n = cnt[b * 2 + 1];
+            for (int i = 0; i < n;) {
+                // merge runs of consecutive chunks landing in consecutive slots
+                int j = i + 1;
+                const int32_t *e0 = nl + ((size_t)b * g.k + i) * 2;
+                while (j < n) {
+                    const int32_t *ej = nl + ((size_t)b * g.k + j) * 2;
+                    if (ej[0] != e0[0] + (j - i) || ej[1] != e0[1] + (j - i)) break;
+                    ++j;
+                }
+                HIPCHECK(c, hipMemcpyAsync(c->slots + ((size_t)b * g.n_slots + e0[1]) * g.chunk_elems,
+                                           c->host_comp + ((size_t)b * g.nc + e0[0]) * g.chunk_elems, cb * (j - i),
+                                           hipMemcpyHostToDevice, c->side));
+                i = j;
+            }
+        }
+    } else {
+        HIPCHECK(c, launch_recall(g, c->t, c->s, c->side));
+    }
+    if (timing) HIPCHECK(c, hipEventRecord(ev.r[1], c->side));
+    HIPCHECK(c, hipEventRecord(c->ev_rec, c->side));
+    HIPCHECK(c, hipStreamWaitEvent(s0, c->ev_rec, 0));
+    MARK(5);
+    // (4b) tidal complements recalled this step, then the merge of all partials
+    HIPCHECK(c, launch_subset_slots(g, c->t, c->s, q, true, s0));
+    MARK(6);
+    HIPCHECK(c, launch_subset_combine(g, c->t, c->s, out, s0));
+    MARK(7);
+#undef MARK
+    if (timing) c->pending.push_back(ev);
+    c->steps++;
+    return WNW_OK;
+}
+
+wnw_status wnw_query_geometry(const wnw_ctx *c, int32_t *n_chunks, int32_t *k, int32_t *keep_total, int32_t *n_slots,
+                              int64_t *chunk_bytes)
+{
+    if (!c) return fail(nullptr, WNW_ERR_INVALID, "ctx is NULL");
+    if (n_chunks) *n_chunks = c->g.nc;
+    if (k) *k = c->g.k;
+    if (keep_total) *keep_total = c->g.keep_total;
+    if (n_slots) *n_slots = c->g.n_slots;
+    if (chunk_bytes) {
+        if (c->state == CREATED) return fail(const_cast<wnw_ctx *>(c), WNW_ERR_STATE, "chunk size is known after wnw_set_roles");
+        *chunk_bytes = c->g.chunk_elems * (int64_t)sizeof(uint16_t);
+    }
+    return WNW_OK;
+}
+
+wnw_status wnw_get_stats(wnw_ctx *c, wnw_stats *o)
+{
+    if (!c || !o) return fail(c, WNW_ERR_INVALID, "ctx and out must not be NULL");
+    if (c->state != READY) return fail(c, WNW_ERR_STATE, "context not ready");
+    DeviceGuard dg(c->device);
+    HIPCHECK(c, hipDeviceSynchronize());
+    wnw_status r = harvest_timing(c);
+    if (r != WNW_OK) return r;
+    unsigned long long st[8];
+    HIPCHECK(c, hipMemcpy(st, c->s.stats, sizeof st, hipMemcpyDeviceToHost));
+    const Geometry &g = c->g;
+    *o = wnw_stats{};
+    o->steps = c->steps;
+    o->recalled_chunks = (int64_t)st[0];
+    o->recalled_bytes = (int64_t)st[0] * g.chunk_elems * (int64_t)sizeof(uint16_t);
+    o->dropped_chunks = (int64_t)st[1];
+    o->resident_chunks = (int64_t)st[2];
+    o->peak_resident = (int32_t)st[4];
+    o->n_slots = g.n_slots;
+    o->slot_rows = (int64_t)st[3];
+    const double full = (double)g.L * g.Hkv * g.Ta;
+    const double res_rows = c->steps ? (double)st[3] / ((double)c->steps * g.B) : 0.0;
+    if (full > 0) {
+        o->r_gpu = ((double)g.nA * g.Ta + (double)(g.nT + g.nF) * g.keep_total + (double)g.nT * res_rows) / full;
+        o->r_gpu_cpu = o->r_gpu + (double)g.nT * (g.Ta - g.keep_total) / full;
+    }
+    o->anchor_bytes = (int64_t)g.B * g.nA * g.T * 2 * D * 2;
+    o->static_bytes = (int64_t)g.B * (g.nT + g.nF) * g.Rs * 2 * D * 2;
+    o->timed_steps = c->timed_steps;
+    o->t_anchor_ms = c->t_acc[0];
+    o->t_select_ms = c->t_acc[1];
+    o->t_static_ms = c->t_acc[2];
+    o->t_kept_ms = c->t_acc[3];
+    o->t_recall_ms = c->t_acc[4];
+    o->t_new_ms = c->t_acc[5];
+    o->t_combine_ms = c->t_acc[6];
+    o->t_step_ms = c->t_acc[7];
+    return WNW_OK;
+}
+
+wnw_status wnw_set_selection_override(wnw_ctx *c, const int32_t *sel_dev)
+{
+    if (!c) return fail(nullptr, WNW_ERR_INVALID, "ctx is NULL");
+    c->override_sel = sel_dev;
+    return WNW_OK;
+}
+
+wnw_status wnw_debug_read_slot(wnw_ctx *c, int32_t b, int32_t chunk, void *dst, size_t bytes)
+{
+    if (!c || !dst) return fail(c, WNW_ERR_INVALID, "ctx and host_dst must not be NULL");
+    if (c->state != READY) return fail(c, WNW_ERR_STATE, "context not ready");
+    const Geometry &g = c->g;
+    if (b < 0 || b >= g.B || chunk < 0 || chunk >= g.nc) return fail(c, WNW_ERR_INVALID, "(b, chunk) out of range");
+    if (bytes != (size_t)g.chunk_elems * sizeof(uint16_t)) return fail(c, WNW_ERR_INVALID, "bytes must equal chunk_bytes");
+    DeviceGuard dg(c->device);
+    HIPCHECK(c, hipDeviceSynchronize());
+    int32_t slot = -1;
+    HIPCHECK(c, hipMemcpy(&slot, c->s.slot_of + (size_t)b * g.nc + chunk, sizeof slot, hipMemcpyDeviceToHost));
+    if (slot < 0) return fail(c, WNW_ERR_INVALID, "chunk %d of sequence %d is not resident", chunk, b);
+    HIPCHECK(c, hipMemcpy(dst, c->slots + ((size_t)b * g.n_slots + slot) * g.chunk_elems, bytes, hipMemcpyDeviceToHost));
+    return WNW_OK;
+}
+
+wnw_status wnw_debug_read_host_chunk(wnw_ctx *c, int32_t b, int32_t chunk, void *dst, size_t bytes)
+{
+    if (!c || !dst) return fail(c, WNW_ERR_INVALID, "ctx and host_dst must not be NULL");
+    if (c->state != READY) return fail(c, WNW_ERR_STATE, "context not ready");
+    const Geometry &g = c->g;
+    if (b < 0 || b >= g.B || chunk < 0 || chunk >= g.nc) return fail(c, WNW_ERR_INVALID, "(b, chunk) out of range");
+    if (bytes != (size_t)g.chunk_elems * sizeof(uint16_t)) return fail(c, WNW_ERR_INVALID, "bytes must equal chunk_bytes");
+    if (bytes) memcpy(dst, c->host_comp + ((size_t)b * g.nc + chunk) * g.chunk_elems, bytes);
+    return WNW_OK;
+}
+
+wnw_status wnw_debug_read_resident(wnw_ctx *c, uint8_t *dst)
+{
+    if (!c || !dst) return fail(c, WNW_ERR_INVALID, "ctx and host_dst must not be NULL");
+    if (c->state != READY) return fail(c, WNW_ERR_STATE, "context not ready");
+    const Geometry &g = c->g;
+    DeviceGuard dg(c->device);
+    HIPCHECK(c, hipDeviceSynchronize());
+    std::vector<int32_t> so((size_t)g.B * g.nc);
+    if (!so.empty()) HIPCHECK(c, hipMemcpy(so.data(), c->s.slot_of, so.size() * sizeof(int32_t), hipMemcpyDeviceToHost));
+    for (size_t i = 0; i < so.size(); ++i) dst[i] = so[i] >= 0;
+    return WNW_OK;
+}
+
+void wnw_destroy(wnw_ctx *c)
+{
+    if (!c) return;
+    DeviceGuard dg(c->device);
+    (void)hipDeviceSynchronize();
+    free_all(c);
+    delete c;
+}
+
+}  // extern "C"

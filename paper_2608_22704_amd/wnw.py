@@ -1,0 +1,160 @@
+"""Python binding of the WnW decode-step library (libwnw.so), argument marshalling only.
+
+Function names match the C ABI of include/wnw.h.  Every computation runs in the HIP library;
+this module only converts arguments (torch tensors -> device pointers, torch streams -> HIP
+streams) and turns error codes into exceptions.  It raises at import time when the library has
+not been built: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libwnw.so")
+
+WNW_OK, WNW_ERR_INVALID, WNW_ERR_OOM, WNW_ERR_HIP, WNW_ERR_STATE, WNW_ERR_UNSUPPORTED = 0, -1, -2, -3, -4, -5
+WNW_ANCHOR, WNW_TIDAL, WNW_FIXED = 0, 1, 2
+WNW_F_SELECT_NEXT_STEP, WNW_F_RECALL_MEMCPY, WNW_F_TIMING = 1, 2, 4
+
+EXPORTS = ("wnw_init_cache", "wnw_set_roles", "wnw_decode_step", "wnw_query_geometry", "wnw_get_stats",
+           "wnw_set_selection_override", "wnw_debug_read_slot", "wnw_debug_read_host_chunk",
+           "wnw_debug_read_resident", "wnw_last_error", "wnw_destroy")
+
+
+class wnw_config(C.Structure):
+    _fields_ = [("batch", C.c_int32), ("layers", C.c_int32), ("q_heads", C.c_int32), ("kv_heads", C.c_int32),
+                ("head_dim", C.c_int32), ("audio_len", C.c_int32), ("text_len", C.c_int32),
+                ("chunk_len", C.c_int32), ("budget_bp", C.c_int32), ("top_k", C.c_int32),
+                ("evict_lag", C.c_int32), ("flags", C.c_uint32)]
+
+
+class wnw_stats(C.Structure):
+    _fields_ = [("steps", C.c_int64), ("recalled_chunks", C.c_int64), ("recalled_bytes", C.c_int64),
+                ("dropped_chunks", C.c_int64), ("resident_chunks", C.c_int64), ("peak_resident", C.c_int32),
+                ("n_slots", C.c_int32), ("r_gpu", C.c_double), ("r_gpu_cpu", C.c_double),
+                ("anchor_bytes", C.c_int64), ("static_bytes", C.c_int64), ("slot_rows", C.c_int64),
+                ("timed_steps", C.c_int64), ("t_anchor_ms", C.c_double), ("t_select_ms", C.c_double),
+                ("t_static_ms", C.c_double), ("t_kept_ms", C.c_double), ("t_recall_ms", C.c_double),
+                ("t_new_ms", C.c_double), ("t_combine_ms", C.c_double), ("t_step_ms", C.c_double)]
+
+    def as_dict(self) -> dict:
+        return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+class WnwError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"wnw status {status}: {msg}")
+        self.status = status
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build the HIP library first (__graft_entry__.build())")
+    lib = C.CDLL(LIB_PATH)
+    P, I32, I64, SZ = C.c_void_p, C.c_int32, C.c_int64, C.c_size_t
+    sig = {
+        "wnw_init_cache": ([C.POINTER(wnw_config), P, P, P, C.POINTER(P)], C.c_int),
+        "wnw_set_roles": ([P, P, P], C.c_int),
+        "wnw_decode_step": ([P, P, P, P, P, P], C.c_int),
+        "wnw_query_geometry": ([P, C.POINTER(I32), C.POINTER(I32), C.POINTER(I32), C.POINTER(I32), C.POINTER(I64)], C.c_int),
+        "wnw_get_stats": ([P, C.POINTER(wnw_stats)], C.c_int),
+        "wnw_set_selection_override": ([P, P], C.c_int),
+        "wnw_debug_read_slot": ([P, I32, I32, P, SZ], C.c_int),
+        "wnw_debug_read_host_chunk": ([P, I32, I32, P, SZ], C.c_int),
+        "wnw_debug_read_resident": ([P, P], C.c_int),
+        "wnw_last_error": ([P], C.c_char_p),
+        "wnw_destroy": ([P], None),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes, fn.restype = args, res
+    return lib
+
+
+lib = _load()
+
+
+def _check(status: int, ctx=None):
+    if status != WNW_OK:
+        raise WnwError(status, lib.wnw_last_error(ctx).decode())
+
+
+def _ptr(t):
+    """Device (or host) address of a tensor / numpy array / int, or None."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    if hasattr(t, "data_ptr"):
+        return t.data_ptr()
+    return t.ctypes.data
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    return getattr(stream, "cuda_stream", stream)
+
+
+# ---- the C ABI, one wrapper per entry point -------------------------------------------------
+
+def wnw_init_cache(cfg: wnw_config, k_dev, v_dev, stream=None):
+    h = C.c_void_p()
+    _check(lib.wnw_init_cache(C.byref(cfg), _ptr(k_dev), _ptr(v_dev), _stream(stream), C.byref(h)))
+    return h
+
+
+def wnw_set_roles(ctx, roles, prefill_scores):
+    _check(lib.wnw_set_roles(ctx, _ptr(roles), _ptr(prefill_scores)), ctx)
+
+
+def wnw_decode_step(ctx, q_dev, out_dev, chunk_scores_dev=None, selected_dev=None, stream=None):
+    _check(lib.wnw_decode_step(ctx, _ptr(q_dev), _ptr(out_dev), _ptr(chunk_scores_dev), _ptr(selected_dev),
+                               _stream(stream)), ctx)
+
+
+def wnw_query_geometry(ctx) -> dict:
+    n, k, kt, ns, cb = C.c_int32(), C.c_int32(), C.c_int32(), C.c_int32(), C.c_int64(-1)
+    _check(lib.wnw_query_geometry(ctx, C.byref(n), C.byref(k), C.byref(kt), C.byref(ns), None), ctx)
+    out = {"n_chunks": n.value, "k": k.value, "keep_total": kt.value, "n_slots": ns.value}
+    if lib.wnw_query_geometry(ctx, None, None, None, None, C.byref(cb)) == WNW_OK:
+        out["chunk_bytes"] = cb.value
+    return out
+
+
+def wnw_get_stats(ctx) -> dict:
+    st = wnw_stats()
+    _check(lib.wnw_get_stats(ctx, C.byref(st)), ctx)
+    return st.as_dict()
+
+
+def wnw_set_selection_override(ctx, sel_dev):
+    _check(lib.wnw_set_selection_override(ctx, _ptr(sel_dev)), ctx)
+
+
+def wnw_debug_read_slot(ctx, b: int, chunk: int, host_dst, nbytes: int):
+    _check(lib.wnw_debug_read_slot(ctx, b, chunk, _ptr(host_dst), nbytes), ctx)
+
+
+def wnw_debug_read_host_chunk(ctx, b: int, chunk: int, host_dst, nbytes: int):
+    _check(lib.wnw_debug_read_host_chunk(ctx, b, chunk, _ptr(host_dst), nbytes), ctx)
+
+
+def wnw_debug_read_resident(ctx, host_dst):
+    _check(lib.wnw_debug_read_resident(ctx, _ptr(host_dst)), ctx)
+
+
+def wnw_last_error(ctx=None) -> str:
+    return lib.wnw_last_error(ctx).decode()
+
+
+def wnw_destroy(ctx):
+    lib.wnw_destroy(ctx)
+
+
+def make_config(batch, layers, q_heads, kv_heads, audio_len, text_len, chunk_len, budget_bp,
+                head_dim=128, top_k=0, evict_lag=0, flags=0) -> wnw_config:
+    return wnw_config(batch, layers, q_heads, kv_heads, head_dim, audio_len, text_len, chunk_len, budget_bp,
+                      top_k, evict_lag, flags)

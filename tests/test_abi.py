@@ -1,0 +1,71 @@
+"""The C-ABI library on the CPU: it builds, loads, exports every declared entry point, its
+header compiles as C99 and C++17, and argument validation answers without a GPU."""
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "wnw.h")
+
+
+@pytest.fixture(scope="module")
+def W():
+    from paper_2608_22704_amd import build
+    if not os.path.exists(build.LIB):
+        build.build()
+    from paper_2608_22704_amd import wnw
+    return wnw
+
+
+def declared():
+    src = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(wnw_[a-z_]+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported(W):
+    names = declared()
+    assert len(names) >= 11
+    assert set(names) == set(W.EXPORTS)
+    out = subprocess.run(["nm", "-D", "--defined-only", W.LIB_PATH], capture_output=True, text=True, check=True).stdout
+    exported = set(re.findall(r" T (wnw_[a-z_]+)", out))
+    assert set(names) <= exported
+
+
+@pytest.mark.parametrize("cmd", [["gcc", "-std=c99", "-Wall", "-Wextra", "-pedantic", "-x", "c"],
+                                 ["g++", "-std=c++17", "-Wall", "-Wextra", "-pedantic", "-x", "c++"]])
+def test_header_compiles(cmd, tmp_path):
+    src = tmp_path / "use.c"
+    src.write_text('#include "wnw.h"\nint main(void){ wnw_config c = {0}; (void)c; return (int)WNW_OK; }\n')
+    subprocess.run(cmd + ["-I", os.path.join(ROOT, "include"), "-fsyntax-only", str(src)], check=True)
+
+
+def test_validation_without_gpu(W):
+    good = dict(batch=1, layers=1, q_heads=24, kv_heads=8, audio_len=1000, text_len=64, chunk_len=32, budget_bp=2000)
+    cases = [
+        (dict(head_dim=64), W.WNW_ERR_UNSUPPORTED),
+        (dict(q_heads=20), W.WNW_ERR_INVALID),          # not a multiple of kv_heads
+        (dict(q_heads=40), W.WNW_ERR_UNSUPPORTED),      # group 5
+        (dict(budget_bp=10001), W.WNW_ERR_INVALID),
+        (dict(chunk_len=0), W.WNW_ERR_INVALID),
+        (dict(chunk_len=300), W.WNW_ERR_UNSUPPORTED),
+        (dict(top_k=100), W.WNW_ERR_INVALID),           # more than the 32 chunks
+        (dict(audio_len=0, text_len=0), W.WNW_ERR_INVALID),
+        (dict(flags=1 << 10), W.WNW_ERR_INVALID),
+    ]
+    for over, want in cases:
+        kw = dict(good)
+        kw.update(over)
+        cfg = W.make_config(**kw)
+        with pytest.raises(W.WnwError) as e:
+            W.wnw_init_cache(cfg, 1, 1, stream=0)
+        assert e.value.status == want, (over, str(e.value))
+        assert W.wnw_last_error(None)
+    with pytest.raises(W.WnwError) as e:
+        W.wnw_init_cache(W.make_config(**good), None, 1, stream=0)
+    assert e.value.status == W.WNW_ERR_INVALID
+    # NULL context everywhere
+    assert W.lib.wnw_set_roles(None, None, None) == W.WNW_ERR_INVALID
+    assert W.lib.wnw_decode_step(None, None, None, None, None, None) == W.WNW_ERR_INVALID
+    W.wnw_destroy(None)

@@ -1,0 +1,224 @@
+"""GPU parity of the HIP decode step against the CPU oracle, through the C ABI.
+
+Every test prints the case it runs before touching the GPU.
+"""
+import numpy as np
+import pytest
+
+from synth import configs, gen
+from synth.configs import Workload
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from oracle import oracle as O
+    O.build()
+
+
+def _run(w, steps=None, head_mask_fn=None, **kw):
+    from tests.wnw_harness import Lockstep, log
+    log(f"[case] {w.name} B={w.batch} L={w.layers} Hq={w.q_heads} Hkv={w.kv_heads} Ta={w.audio_len} "
+        f"Tt={w.text_len} chunk={w.chunk_len} budget={kw.get('budget_bp', w.budget_bp)} {kw}")
+    h = Lockstep(w, **kw)
+    try:
+        n = w.steps if steps is None else steps
+        for s in range(n):
+            h.step(s, None if head_mask_fn is None else head_mask_fn(s, h))
+            if s % 32 == 31:
+                log(f"[step] {w.name}: {s + 1}/{n}, max out err {h.max_err:.3g}")
+        log(f"[done] {w.name}: {n} steps, max out err {h.max_err:.3g}, max score rel {h.max_score_rel:.3g}, "
+            f"excused flips {h.flips}")
+        return h
+    finally:
+        h.close()
+
+
+def test_tiny_single_layer():
+    _run(configs.TINY)
+
+
+def test_tiny_memcpy_recall_path():
+    from paper_2608_22704_amd import wnw as W
+    _run(configs.TINY.with_(steps=4), flags=W.WNW_F_RECALL_MEMCPY)
+
+
+def test_qwen_shaped_all_steps():
+    _run(configs.QWEN_10MIN)
+
+
+def _sampled(n_heads):
+    def fn(s, h):
+        L, H = h.w.layers, h.w.kv_heads
+        if s < 4:
+            return np.ones((L, H), dtype=np.uint8)
+        rng = np.random.default_rng(1000 + s)
+        m = np.zeros(L * H, dtype=np.uint8)
+        m[rng.choice(L * H, size=n_heads, replace=False)] = 1
+        return m.reshape(L, H)
+    return fn
+
+
+def test_voxtral_shaped_all_steps_sampled_heads():
+    _run(configs.VOXTRAL_10MIN, head_mask_fn=_sampled(16))
+
+
+def _small(name, seed_id, L=2, Hq=8, Hkv=4, Ta=300, Tt=9, cl=32, budget=2000, steps=6, roles=None, B=2):
+    n = L * Hkv
+    a, t, f = roles if roles is not None else (max(1, n // 4), max(1, n // 2), n - max(1, n // 4) - max(1, n // 2))
+    return Workload(name, seed_id, B, L, Hq, Hkv, 128, Ta, Tt, cl, budget, steps, a, t, f)
+
+
+EDGE = [
+    _small("g1_chunk7", 101, Hq=4, Hkv=4, cl=7),
+    _small("g2_chunk50_ragged", 102, Hq=8, cl=50, Ta=517),
+    _small("g6_chunk100", 103, Hq=12, Hkv=2, cl=100, Ta=1111, Tt=3),
+    _small("g8_chunk256_long_tail", 104, Hq=16, Hkv=2, cl=256, Ta=1300, Tt=300),
+    _small("g4_chunk1", 105, Hq=8, Hkv=2, cl=1, Ta=97, budget=2500),
+    _small("no_text", 106, Tt=0),
+    _small("budget_zero", 107, budget=0),
+    _small("budget_full", 108, budget=10000),
+    _small("audio_shorter_than_chunk", 109, Ta=20, cl=64, budget=5000),
+    _small("text_only", 110, Ta=0, Tt=40),
+    _small("all_tidal_but_one_anchor", 111, L=1, Hkv=4, Hq=12, roles=(1, 3, 0)),
+    _small("anchors_only", 112, L=1, Hkv=4, Hq=8, roles=(4, 0, 0)),
+    _small("batch3_tile_ragged", 113, B=3, Ta=777, Tt=1, cl=37, budget=3000, steps=9),
+]
+
+
+@pytest.mark.parametrize("w", EDGE, ids=[w.name for w in EDGE])
+def test_edge_shapes(w):
+    _run(w)
+
+
+def test_budget_full_is_full_attention():
+    """At 100 % budget every head must equal plain attention over its whole cache."""
+    import torch
+    from tests.wnw_harness import Lockstep, log
+    w = _small("full_budget_sdpa", 120, budget=10000, steps=2)
+    log("[case] full budget vs SDPA")
+    h = Lockstep(w)
+    try:
+        out, _, _, _ = h.gpu_step(0)
+        k = torch.from_numpy(gen.bf16_to_f32(h.ok_).astype(np.float64))
+        v = torch.from_numpy(gen.bf16_to_f32(h.ov_).astype(np.float64))
+        q = torch.from_numpy(gen.bf16_to_f32(h.q[0]).astype(np.float64))
+        g = w.group
+        ref = torch.nn.functional.scaled_dot_product_attention(
+            q.unsqueeze(-2), k.repeat_interleave(g, dim=2), v.repeat_interleave(g, dim=2)).squeeze(-2)
+        assert np.abs(out - ref.numpy()).max() <= 2e-2
+    finally:
+        h.close()
+
+
+def test_recall_bytes_identical_to_host_copy_and_cache():
+    from tests.wnw_harness import Lockstep, log
+    w = configs.TINY.with_(steps=1)
+    log("[case] recall byte identity, tiny workload")
+    h = Lockstep(w)
+    try:
+        _, _, sel, _ = h.gpu_step(0)
+        W = h.W
+        nbytes = h.geo["chunk_bytes"]
+        kd, vd = h.ok_[0], h.ov_[0]                       # [L][H][T][D] of sequence 0
+        tidal = [(l, kv) for l in range(w.layers) for kv in range(w.kv_heads) if h.roles[l, kv] == 1]
+        assert sel.shape[1] == h.k and h.k > 0
+        for c in sel[0]:
+            dev = np.empty(nbytes // 2, dtype=np.uint16)
+            hst = np.empty(nbytes // 2, dtype=np.uint16)
+            W.wnw_debug_read_slot(h.ctx, 0, int(c), dev, nbytes)
+            W.wnw_debug_read_host_chunk(h.ctx, 0, int(c), hst, nbytes)
+            assert np.array_equal(dev, hst)
+            comp_max = nbytes // 2 // (len(tidal) * 2 * 128)
+            blk = dev.reshape(len(tidal), 2, comp_max, 128)
+            for ti, (l, kv) in enumerate(tidal):
+                keep = h.oracle.keep_mask(0, l, kv)
+                c0, c1 = int(c) * w.chunk_len, min((int(c) + 1) * w.chunk_len, w.audio_len)
+                rows = [t for t in range(c0, c1) if not keep[t]]
+                assert np.array_equal(blk[ti, 0, : len(rows)], kd[l, kv, rows])
+                assert np.array_equal(blk[ti, 1, : len(rows)], vd[l, kv, rows])
+                assert not blk[ti, :, len(rows):].any()
+        with pytest.raises(W.WnwError):
+            notres = [c for c in range(h.nc) if c not in set(sel[0].tolist())][0]
+            W.wnw_debug_read_slot(h.ctx, 0, notres, np.empty(nbytes // 2, dtype=np.uint16), nbytes)
+    finally:
+        h.close()
+
+
+def test_two_runs_bit_identical():
+    from tests.wnw_harness import Lockstep, log
+    w = _small("determinism", 130, steps=5)
+    log("[case] determinism")
+    outs = []
+    for _ in range(2):
+        h = Lockstep(w)
+        try:
+            outs.append([h.gpu_step(s) for s in range(w.steps)])
+        finally:
+            h.close()
+    for a, b in zip(*outs):
+        for x, y in zip(a, b):
+            assert np.array_equal(x, y)
+
+
+def test_selection_override_and_call_order():
+    import torch
+    from tests.wnw_harness import Lockstep, log, to_dev
+    w = _small("override", 140, steps=5, cl=16, Ta=160)
+    log("[case] override and call order")
+    h = Lockstep(w)
+    W = h.W
+    try:
+        k = h.k
+        forced = np.full((w.batch, k), -1, dtype=np.int32)
+        forced[:, 0] = 3
+        if k > 1:
+            forced[:, 1] = 7
+        fd = torch.from_numpy(forced).cuda()
+        W.wnw_set_selection_override(h.ctx, fd)
+        for s in range(3):
+            out, sc, sel, res = h.gpu_step(s)
+            r = h.oracle.step(h.q[s], forced=forced)
+            assert (res == r["resident"]).all()
+            assert np.abs(out - r["out"]).max() <= 2e-2
+            assert sorted(x for x in sel[0] if x >= 0) == sorted(x for x in forced[0] if x >= 0)
+        W.wnw_set_selection_override(h.ctx, None)
+        with pytest.raises(W.WnwError) as e:
+            W.wnw_set_roles(h.ctx, h.roles, h.prefill)
+        assert e.value.status == W.WNW_ERR_STATE
+        with pytest.raises(W.WnwError) as e:
+            W.wnw_decode_step(h.ctx, None, h.out)
+        assert e.value.status == W.WNW_ERR_INVALID
+    finally:
+        h.close()
+    kd = torch.zeros((1, 1, 2, 40, 128), dtype=torch.int16, device="cuda")
+    cfg = W.make_config(1, 1, 2, 2, 32, 8, 8, 2000)
+    ctx = W.wnw_init_cache(cfg, kd, kd)
+    try:
+        with pytest.raises(W.WnwError) as e:
+            W.wnw_decode_step(ctx, kd, torch.zeros(256, device="cuda"))
+        assert e.value.status == W.WNW_ERR_STATE
+    finally:
+        W.wnw_destroy(ctx)
+
+
+def test_timing_stats():
+    from paper_2608_22704_amd import wnw as W
+    from tests.wnw_harness import Lockstep, log
+    w = _small("timing", 150, steps=4)
+    log("[case] timing statistics")
+    h = Lockstep(w, flags=W.WNW_F_TIMING)
+    try:
+        for s in range(w.steps):
+            h.gpu_step(s)
+        st = W.wnw_get_stats(h.ctx)
+        assert st["steps"] == w.steps and st["timed_steps"] == w.steps
+        assert st["t_anchor_ms"] > 0 and st["t_static_ms"] > 0 and st["t_step_ms"] > 0
+        assert 0 < st["r_gpu"] <= st["r_gpu_cpu"] <= 1.0 + 1e-9
+        assert st["anchor_bytes"] == w.batch * w.n_anchor * w.total_len * 512
+    finally:
+        h.close()

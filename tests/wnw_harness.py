@@ -1,0 +1,153 @@
+"""Lock-step comparison of the HIP decode step (through the C ABI) with the CPU oracle.
+
+Both sides consume the same seeded inputs (synth.gen).  The GPU runs free: it selects its own
+chunks.  Each step its selection is checked against the oracle's chunk scores (a valid top-k,
+up to chunks whose oracle score lies within 1e-6 of the k-th score), and the oracle is then
+stepped with that same selection so that the two keep one trajectory.
+
+Tolerances (bf16 storage, fp32 accumulation on the GPU, double in the oracle):
+  outputs       max |gpu - oracle| <= 2e-2 over every compared head
+  chunk scores  |gpu - oracle| <= 1e-5 * |oracle| per chunk
+  selection     equal sets, except chunks within 1e-6 (relative) of the k-th oracle score
+  residency     equal sets of resident chunks after every step
+"""
+from __future__ import annotations
+
+import sys
+import time
+
+import numpy as np
+
+from oracle import oracle as O
+from synth import gen
+
+OUT_TOL = 2e-2
+SCORE_RTOL = 1e-5
+SEL_EXCUSE = 1e-6
+
+
+def log(msg: str):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def to_dev(a: np.ndarray):
+    import torch
+    if a.dtype == np.uint16:
+        a = a.view(np.int16)
+    return torch.from_numpy(np.ascontiguousarray(a)).to("cuda")
+
+
+def check_selection(gpu_sel: np.ndarray, oracle_scores: np.ndarray, k: int) -> int:
+    """Raise unless gpu_sel is the top-k of the oracle's fp32 scores up to excused near-ties.
+    Returns the number of excused differences."""
+    if k == 0:
+        assert gpu_sel.size == 0
+        return 0
+    s32 = oracle_scores.astype(np.float32)
+    ref = O.topk(s32, k)
+    diff = set(int(c) for c in gpu_sel) ^ set(int(c) for c in ref)
+    if not diff:
+        return 0
+    kth = float(np.sort(s32)[::-1][k - 1])
+    tol = SEL_EXCUSE * abs(kth)
+    bad = [c for c in diff if abs(float(s32[c]) - kth) > tol]
+    assert not bad, f"selection differs beyond near-ties: chunks {sorted(bad)} (k-th score {kth:.9g})"
+    assert len(set(int(c) for c in gpu_sel)) == k and all(0 <= c < len(s32) for c in gpu_sel)
+    return len(diff) // 2
+
+
+class Lockstep:
+    """One workload, a subset `seqs` of its sequences checked against the oracle (the GPU runs
+    all w.batch sequences)."""
+
+    def __init__(self, w, flags: int = 0, seqs=None, budget_bp=None, data=None, top_k=0):
+        import torch
+        from paper_2608_22704_amd import wnw as W
+        self.W, self.torch = W, torch
+        if budget_bp is not None:
+            w = w.with_(budget_bp=budget_bp)
+        self.w = w
+        self.seqs = list(range(w.batch)) if seqs is None else list(seqs)
+        B, L, H, T, D = w.batch, w.layers, w.kv_heads, w.total_len, w.head_dim
+        t0 = time.time()
+        self.roles = gen.roles(w)
+        kd = torch.empty((B, L, H, T, D), dtype=torch.int16, device="cuda")
+        vd = torch.empty_like(kd)
+        self.q = np.empty((w.steps, B, L, w.q_heads, D), dtype=np.uint16)
+        self.prefill = np.empty((B, L, H, w.audio_len), dtype=np.float32)
+        host = {}
+        for b in range(B):
+            if data is not None:
+                seq = data[b]
+            else:
+                seq = gen.sequence(w, b)
+            kd[b].copy_(to_dev(seq["k"]))
+            vd[b].copy_(to_dev(seq["v"]))
+            self.q[:, b] = seq["q"]
+            self.prefill[b] = seq["prefill"]
+            if b in self.seqs:
+                host[b] = seq
+        torch.cuda.synchronize()
+        log(f"[harness] {w.name}: inputs ready in {time.time() - t0:.1f}s")
+        self.cfg = W.make_config(B, L, w.q_heads, H, w.audio_len, w.text_len, w.chunk_len, w.budget_bp,
+                                 top_k=top_k, flags=flags)
+        self.ctx = W.wnw_init_cache(self.cfg, kd, vd)
+        W.wnw_set_roles(self.ctx, self.roles, self.prefill)
+        del kd, vd
+        torch.cuda.empty_cache()
+        self.geo = W.wnw_query_geometry(self.ctx)
+        ocfg = O.cfg_from_workload(w, batch=len(self.seqs), top_k=top_k)
+        self.ok_ = np.stack([host[b]["k"] for b in self.seqs])
+        self.ov_ = np.stack([host[b]["v"] for b in self.seqs])
+        self.oracle = O.Oracle(ocfg, self.ok_, self.ov_, self.roles, self.prefill[self.seqs])
+        assert (self.oracle.n_chunks, self.oracle.k, self.oracle.keep_total) == \
+            (self.geo["n_chunks"], self.geo["k"], self.geo["keep_total"])
+        self.k, self.nc = self.geo["k"], self.geo["n_chunks"]
+        self.out = torch.empty((B, L, w.q_heads, D), dtype=torch.float32, device="cuda")
+        self.scores = torch.empty((B, max(self.nc, 1)), dtype=torch.float32, device="cuda")
+        self.sel = torch.empty((B, max(self.k, 1)), dtype=torch.int32, device="cuda")
+        self.flips = 0
+        self.max_err = 0.0
+        self.max_score_rel = 0.0
+        self.step_i = 0
+
+    def close(self):
+        if getattr(self, "ctx", None) is not None:
+            self.W.wnw_destroy(self.ctx)
+            self.ctx = None
+        if getattr(self, "oracle", None) is not None:
+            self.oracle.close()
+
+    def gpu_step(self, s: int):
+        qd = to_dev(self.q[s])
+        self.W.wnw_decode_step(self.ctx, qd, self.out, self.scores, self.sel)
+        self.torch.cuda.synchronize()
+        res = np.empty((self.w.batch, max(self.nc, 1)), dtype=np.uint8)
+        self.W.wnw_debug_read_resident(self.ctx, res)
+        return (self.out.cpu().numpy(), self.scores.cpu().numpy()[:, : self.nc],
+                self.sel.cpu().numpy()[:, : self.k], res[:, : self.nc])
+
+    def step(self, s: int, head_mask=None):
+        out, sc, sel, res = self.gpu_step(s)
+        idx = self.seqs
+        r = self.oracle.step(self.q[s][idx], forced=sel[idx] if self.k else None, head_mask=head_mask)
+        for j, b in enumerate(idx):
+            so = r["scores"][j]
+            rel = np.abs(sc[b].astype(np.float64) - so) / np.maximum(np.abs(so), 1e-300)
+            self.max_score_rel = max(self.max_score_rel, float(rel.max(initial=0.0)))
+            assert (np.abs(sc[b].astype(np.float64) - so) <= SCORE_RTOL * np.abs(so)).all(), \
+                f"step {s} seq {b}: chunk score rel err {rel.max():.3g}"
+            self.flips += check_selection(sel[b], so, self.k)
+            assert (res[b] == r["resident"][j]).all(), f"step {s} seq {b}: resident sets differ"
+        # outputs: anchors always, non-anchor heads where the mask asks for them
+        L, H, g = self.w.layers, self.w.kv_heads, self.w.group
+        m = np.ones((L, H), dtype=bool) if head_mask is None else np.asarray(head_mask, dtype=bool).reshape(L, H)
+        m = m | (self.roles == 0)
+        mq = np.repeat(m, g, axis=1)                          # [L][Hq]
+        for j, b in enumerate(idx):
+            err = np.abs(out[b][mq].astype(np.float64) - r["out"][j][mq]).max(initial=0.0)
+            self.max_err = max(self.max_err, float(err))
+            assert err <= OUT_TOL, f"step {s} seq {b}: output max abs err {err:.4g}"
+        self.step_i += 1
+        return out, sc, sel, r
