@@ -97,10 +97,28 @@ def main():
     t_el = time.perf_counter() - t_start
     st1 = W.wnw_get_stats(ctx)
     log(f"[bench] timed region {t_el * 1e3:.1f} ms")
+
+    # Second region: the selection pinned to the last step's chunks (all resident after one
+    # step), so no complement is recalled and the tidal/fixed launch streams HBM only.
+    nr = max(8, args.steps // 4)
+    pinned = sel.clone()
+    W.wnw_set_selection_override(ctx, pinned)
+    for i in range(4):
+        W.wnw_decode_step(ctx, qd[i % S], out, sc, sel, stream)
+    torch.cuda.synchronize()
+    st2 = W.wnw_get_stats(ctx)
+    t2 = time.perf_counter()
+    for i in range(nr):
+        W.wnw_decode_step(ctx, qd[i % S], out, sc, sel, stream)
+    torch.cuda.synchronize()
+    t2 = time.perf_counter() - t2
+    st3 = W.wnw_get_stats(ctx)
+    W.wnw_set_selection_override(ctx, None)
     W.wnw_destroy(ctx)
 
     K = args.steps
     d = {k: st1[k] - st0[k] for k in st1 if isinstance(st1[k], (int, float))}
+    d2 = {k: st3[k] - st2[k] for k in st3 if isinstance(st3[k], (int, float))}
     ms_step = t_el * 1e3 / K
     res = {
         "metric": METRIC, "value": K / t_el, "unit": "steps/s", "n_gpus": 1, "steps": K, "warmup": args.warmup,
@@ -112,27 +130,43 @@ def main():
                    "recall": args.recall},
     }
     chunk_mb = geo.get("chunk_bytes", 0) / 1e6
-    rec = {"new_chunks_per_step": d["recalled_chunks"] / K / B, "MB_per_step": d["recalled_bytes"] / K / 1e6,
-           "chunk_MB": chunk_mb}
+    rec = {"copied_chunks_per_step": d["recalled_chunks"] / K / B,
+           "revived_chunks_per_step": d["revived_chunks"] / K / B,
+           "MB_per_step": d["recalled_bytes"] / K / 1e6, "chunk_MB": chunk_mb}
+    row_bytes = 2 * D * 2                      # K + V of one position, bf16
     if not args.no_timing and d["timed_steps"] > 0:
-        n = d["timed_steps"]
-        kern = {}
-        for name, key, nbytes in (("anchor_attn", "t_anchor_ms", st1["anchor_bytes"]),
-                                  ("subset_static", "t_static_ms", st1["static_bytes"])):
-            ms = d[key] / n
-            kern[name] = {"avg_ms": ms, "bytes": nbytes, "GBps": nbytes / ms / 1e6}
-        kern["select"] = {"avg_ms": d["t_select_ms"] / n}
-        kern["subset_kept"] = {"avg_ms": d["t_kept_ms"] / n}
-        kern["subset_new"] = {"avg_ms": d["t_new_ms"] / n}
-        kern["combine"] = {"avg_ms": d["t_combine_ms"] / n}
-        kern["step_gpu"] = {"avg_ms": d["t_step_ms"] / n}
-        rec["avg_ms"] = d["t_recall_ms"] / n
-        rec["GBps"] = (d["recalled_bytes"] / n) / rec["avg_ms"] / 1e6 if rec["avg_ms"] > 0 else None
+        n, n2 = d["timed_steps"], d2["timed_steps"]
+        anchor_ms = d["t_anchor_ms"] / n
+        tf_bytes = st1["static_bytes"] + d["slot_rows"] / K * w.n_tidal * row_bytes
+        tf2_bytes = st1["static_bytes"] + d2["slot_rows"] / nr * w.n_tidal * row_bytes
+        kern = {
+            "anchor_attn": {"avg_ms": anchor_ms, "bytes": st1["anchor_bytes"],
+                            "GBps": st1["anchor_bytes"] / anchor_ms / 1e6},
+            "merge_select": {"avg_ms": d["t_select_ms"] / n},
+            "tidal_fixed_with_recall": {"avg_ms": d["t_tidal_fixed_ms"] / n, "hbm_bytes": tf_bytes,
+                                        "pcie_bytes": d["recalled_bytes"] / K},
+            "tidal_fixed_no_recall": {"avg_ms": d2["t_tidal_fixed_ms"] / n2, "bytes": tf2_bytes,
+                                      "GBps": tf2_bytes / (d2["t_tidal_fixed_ms"] / n2) / 1e6,
+                                      "region": f"{nr} steps, selection pinned to resident chunks"},
+            "new_slots": {"avg_ms": d["t_new_ms"] / n},
+            "combine": {"avg_ms": d["t_combine_ms"] / n},
+            "step_gpu": {"avg_ms": d["t_step_ms"] / n},
+            "step_no_recall": {"avg_ms": t2 * 1e3 / nr},
+        }
+        if args.recall == "memcpy":
+            rec["copy_ms"] = d["t_recall_ms"] / n
+            rec["GBps"] = (d["recalled_bytes"] / n) / rec["copy_ms"] / 1e6 if rec["copy_ms"] > 0 else None
+        else:
+            # host->device bytes over the launch that carries them (recall and attention overlap)
+            tfm = d["t_tidal_fixed_ms"] / n
+            rec["GBps_over_tidal_fixed_launch"] = (d["recalled_bytes"] / n) / tfm / 1e6 if tfm > 0 else None
+        # overlap: share of the recall-carrying launch not explained by its HBM-only duration
+        rec["step_ms_with_recall"] = ms_step
+        rec["step_ms_no_recall"] = t2 * 1e3 / nr
         res["kernels"] = kern
-        dom = kern["subset_static"]
-        res["roofline"] = {"bound": "hbm", "kernel": "subset_static", "achieved": dom["GBps"],
-                           "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": dom["GBps"] / PEAK_HBM_GBPS,
-                           "traffic": None}
+        a = kern["anchor_attn"]
+        res["roofline"] = {"bound": "hbm", "kernel": "anchor_attn", "achieved": a["GBps"], "peak": PEAK_HBM_GBPS,
+                           "unit": "GB/s", "frac": a["GBps"] / PEAK_HBM_GBPS, "traffic": None}
     res["recall"] = rec
     res["r_gpu"] = st1["r_gpu"]
     res["r_gpu_cpu"] = st1["r_gpu_cpu"]

@@ -68,7 +68,8 @@ enum {
      * selection happens after the step); default is the same step. */
     WNW_F_SELECT_NEXT_STEP = 1u,
     /* Recall with hipMemcpyAsync on a side stream after one host wait per step, instead of
-     * the default device-side gather from mapped pinned memory. */
+     * the default: work-groups of the tidal/fixed launch read the complements from mapped
+     * pinned memory, copy them to their slots and attend to them in the same pass. */
     WNW_F_RECALL_MEMCPY = 2u,
     /* Record HIP events around the kernels of every step; wnw_get_stats reports the times. */
     WNW_F_TIMING = 4u
@@ -94,6 +95,8 @@ typedef struct {
 typedef struct {
     int64_t steps;             /* decode steps run                                       */
     int64_t recalled_chunks;   /* (sequence, chunk) complements copied host -> device    */
+    int64_t revived_chunks;    /* newly resident complements whose bytes were still in a
+                                  freed slot, so no copy was needed                        */
     int64_t recalled_bytes;    /* bytes copied host -> device                            */
     int64_t dropped_chunks;    /* (sequence, chunk) complements dropped from the device  */
     int64_t resident_chunks;   /* sum over steps and sequences of resident chunks        */
@@ -103,18 +106,20 @@ typedef struct {
                                   with the mean resident set over the steps run           */
     double r_gpu_cpu;          /* paper's r_GPU+CPU: adds the host-resident complement   */
     int64_t anchor_bytes;      /* algorithmic HBM bytes of one anchor-attention launch   */
-    int64_t static_bytes;      /* algorithmic HBM bytes of one fixed + tidal-kept-rows launch */
+    int64_t static_bytes;      /* algorithmic HBM bytes of the fixed heads + tidal kept rows    */
     int64_t slot_rows;         /* complement rows attended, summed over steps            */
-    /* WNW_F_TIMING only: summed kernel times (ms) and the number of timed steps. */
+    /* WNW_F_TIMING only: summed times (ms) between HIP events recorded on the caller's stream
+     * around the step's launches, and the number of timed steps. */
     int64_t timed_steps;
-    double t_anchor_ms;        /* anchor attention + chunk mass                          */
-    double t_select_ms;        /* combine, scores, top-k and residency                   */
-    double t_static_ms;        /* fixed heads + tidal kept rows                          */
-    double t_kept_ms;          /* tidal complements already resident                     */
-    double t_recall_ms;        /* host -> device recall (side stream)                    */
-    double t_new_ms;           /* tidal complements recalled this step                   */
-    double t_combine_ms;       /* merge of the tidal/fixed partial results               */
-    double t_step_ms;          /* whole step on the caller's stream                      */
+    double t_anchor_ms;        /* anchor attention + chunk mass                                 */
+    double t_select_ms;        /* anchor merge, chunk scores, top-k, residency, slots           */
+    double t_tidal_fixed_ms;   /* fixed heads, tidal kept rows and resident complements; on the
+                                  default path also the recall of new complements (read from
+                                  pinned host memory and attended in the same launch)           */
+    double t_new_ms;           /* WNW_F_RECALL_MEMCPY: attention over complements copied this step */
+    double t_combine_ms;       /* merge of the tidal/fixed partial results                      */
+    double t_step_ms;          /* whole step on the caller's stream                             */
+    double t_recall_ms;        /* WNW_F_RECALL_MEMCPY: host -> device copies on the side stream  */
 } wnw_stats;
 
 /* Create a context for one batch of caches.

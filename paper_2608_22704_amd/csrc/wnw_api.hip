@@ -33,11 +33,11 @@ thread_local std::string t_err = "no error";
 enum State { CREATED = 0, READY = 1, FAILED = 2 };
 
 // Timing events of one step.  e[] on the caller's stream: 0 start, 1 after anchor attention,
-// 2 after selection, 3 after fixed + tidal kept rows, 4 after resident complements, 5 after the
-// wait for the recall, 6 after newly recalled complements, 7 after the merge.  r[] on the side
-// stream around the recall.
+// 2 after merge + selection, 3 after the tidal/fixed kernel, 4 after the attention over copied
+// complements (host-waited recall path only), 5 after the final merge.  r[] on the side stream
+// around the host-waited copies.
 struct StepEvents {
-    hipEvent_t e[8];
+    hipEvent_t e[6];
     hipEvent_t r[2];
 };
 
@@ -141,7 +141,7 @@ wnw_status derive(wnw_ctx *c, const wnw_config &cfg, Geometry &g)
     const int G = cfg.q_heads / cfg.kv_heads;
     if (G != 1 && G != 2 && G != 3 && G != 4 && G != 6 && G != 8)
         return fail(c, WNW_ERR_UNSUPPORTED, "GQA group %d: implemented for 1, 2, 3, 4, 6, 8", G);
-    if (cfg.chunk_len > TILE) return fail(c, WNW_ERR_UNSUPPORTED, "chunk_len %d > %d", cfg.chunk_len, TILE);
+    if (cfg.chunk_len > MAX_CHUNK) return fail(c, WNW_ERR_UNSUPPORTED, "chunk_len %d > %d", cfg.chunk_len, MAX_CHUNK);
     if (cfg.flags & WNW_F_SELECT_NEXT_STEP)
         return fail(c, WNW_ERR_UNSUPPORTED, "next-step selection timing is not implemented in this build");
 
@@ -170,15 +170,17 @@ wnw_status derive(wnw_ctx *c, const wnw_config &cfg, Geometry &g)
     g.Rs = g.keep_total + g.Tt;
     if ((int64_t)g.delta * g.k > 4096) return fail(c, WNW_ERR_UNSUPPORTED, "delta * k = %lld slots > 4096", (long long)g.delta * g.k);
     g.n_slots = g.delta * g.k;
-    if (g.nc > 4096) return fail(c, WNW_ERR_UNSUPPORTED, "%d chunks > 4096", g.nc);
-    g.n_tiles_a = (g.T + TILE - 1) / TILE;
+    if (select_shared_bytes(g) > 150 * 1024)
+        return fail(c, WNW_ERR_UNSUPPORTED, "%d chunks with %d slots exceed the selection kernel's shared memory", g.nc,
+                    g.n_slots);
+    g.n_tiles_a = (g.T + TILE_A - 1) / TILE_A;
     if ((int64_t)g.n_tiles_a * G * 8 > 65536) return fail(c, WNW_ERR_UNSUPPORTED, "cache of %d rows too long", g.T);
-    g.maxc = (TILE - 1) / g.cl + 2;
-    g.n_tiles_s = (g.Rs + TILE - 1) / TILE;
-    g.sg = g.comp_max > 0 ? std::max(1, TILE / g.comp_max) : 1;
+    g.maxc = (TILE_A - 1) / g.cl + 2;
+    g.n_tiles_s = (g.Rs + TILE_S - 1) / TILE_S;
+    g.slot_tile = g.comp_max <= TILE_S ? TILE_S : 2 * TILE_S;
+    g.sg = g.comp_max > 0 ? g.slot_tile / g.comp_max : 1;
     g.ng_kept = g.comp_max > 0 ? (g.n_slots + g.sg - 1) / g.sg : 0;
-    g.ng_new = g.comp_max > 0 ? (g.k + g.sg - 1) / g.sg : 0;
-    g.np = g.n_tiles_s + g.ng_kept + g.ng_new;
+    g.np = g.n_tiles_s + g.ng_kept + (g.comp_max > 0 ? g.k : 0);
     if ((int64_t)g.np * G * 4 > 65536) return fail(c, WNW_ERR_UNSUPPORTED, "too many partial tiles per head");
     if (g.B > 65535 || (int64_t)g.L * g.Hkv > 65535) return fail(c, WNW_ERR_UNSUPPORTED, "batch or head count too large");
     return WNW_OK;
@@ -219,19 +221,20 @@ void parallel_for(int n, const std::function<void(int)> &fn)
 
 wnw_status harvest_timing(wnw_ctx *c)
 {
+    const bool memcpy_path = c->cfg.flags & WNW_F_RECALL_MEMCPY;
     for (auto &ev : c->pending) {
         float ms;
-        HIPCHECK(c, hipEventSynchronize(ev.e[7]));
-        HIPCHECK(c, hipEventSynchronize(ev.r[1]));
-        // anchor, select, static, kept, recall, new, combine, whole step
-        const int from[8] = {0, 1, 2, 3, -1, 5, 6, 0}, to[8] = {1, 2, 3, 4, -1, 6, 7, 7};
-        for (int i = 0; i < 8; ++i) {
-            if (from[i] < 0) {
-                HIPCHECK(c, hipEventElapsedTime(&ms, ev.r[0], ev.r[1]));
-            } else {
-                HIPCHECK(c, hipEventElapsedTime(&ms, ev.e[from[i]], ev.e[to[i]]));
-            }
+        HIPCHECK(c, hipEventSynchronize(ev.e[5]));
+        // anchor, select, tidal/fixed, new, combine, step
+        const int from[6] = {0, 1, 2, 3, 4, 0}, to[6] = {1, 2, 3, 4, 5, 5};
+        for (int i = 0; i < 6; ++i) {
+            HIPCHECK(c, hipEventElapsedTime(&ms, ev.e[from[i]], ev.e[to[i]]));
             c->t_acc[i] += ms;
+        }
+        if (memcpy_path) {
+            HIPCHECK(c, hipEventSynchronize(ev.r[1]));
+            HIPCHECK(c, hipEventElapsedTime(&ms, ev.r[0], ev.r[1]));
+            c->t_acc[6] += ms;
         }
         c->timed_steps++;
         c->spare.push_back(ev);
@@ -244,8 +247,8 @@ void free_all(wnw_ctx *c)
 {
     void *ptrs[] = {c->aK, c->aV, c->tK, c->tV, c->fK, c->fV, c->slots, c->d_lk, c->scores_int, c->sel_int,
                     c->s.pa_m, c->s.pa_l, c->s.pa_o, c->s.pa_mass, c->s.mass, c->s.ps_m, c->s.ps_l, c->s.ps_o,
-                    c->s.streak, c->s.slot_of, c->s.slot_chunk, c->s.kept_list, c->s.new_list, c->s.counts,
-                    c->s.stats};
+                    c->s.streak, c->s.slot_of, c->s.slot_last, c->s.slot_data, c->s.slot_busy, c->s.slot_since,
+                    c->s.step, c->s.kept_list, c->s.new_list, c->s.counts, c->s.stats};
     for (void *p : ptrs)
         if (p) (void)hipFree(p);
     if (c->host_comp) (void)hipHostFree(c->host_comp);
@@ -336,7 +339,11 @@ wnw_status wnw_set_roles(wnw_ctx *c, const uint8_t *roles, const float *prefill)
     ALLOC(s.ps_o, B * (g.nT + g.nF) * g.np * g.G * Dz, "partial out");
     ALLOC(s.streak, B * g.nc, "streaks");
     ALLOC(s.slot_of, B * g.nc, "slot map");
-    ALLOC(s.slot_chunk, B * g.n_slots, "slot owners");
+    ALLOC(s.slot_last, B * g.nc, "slot history");
+    ALLOC(s.slot_data, B * g.n_slots, "slot contents");
+    ALLOC(s.slot_busy, B * g.n_slots, "slot owners");
+    ALLOC(s.slot_since, B * g.n_slots, "slot ages");
+    ALLOC(s.step, B, "step counters");
     ALLOC(s.kept_list, B * g.n_slots * 2, "kept list");
     ALLOC(s.new_list, B * g.k * 2, "new list");
     ALLOC(s.counts, B * 2, "counts");
@@ -454,7 +461,13 @@ wnw_status wnw_set_roles(wnw_ctx *c, const uint8_t *roles, const float *prefill)
     std::vector<int32_t> init(B * g.nc, g.delta);   // never selected: not resident
     if (!init.empty()) HIPCHECK(c, hipMemcpy(s.streak, init.data(), init.size() * sizeof(int32_t), hipMemcpyHostToDevice));
     if (g.nc) HIPCHECK(c, hipMemset(s.slot_of, 0xff, B * g.nc * sizeof(int32_t)));
-    if (g.n_slots) HIPCHECK(c, hipMemset(s.slot_chunk, 0xff, B * g.n_slots * sizeof(int32_t)));
+    if (g.nc) HIPCHECK(c, hipMemset(s.slot_last, 0xff, B * g.nc * sizeof(int32_t)));
+    if (g.n_slots) {
+        HIPCHECK(c, hipMemset(s.slot_data, 0xff, B * g.n_slots * sizeof(int32_t)));
+        HIPCHECK(c, hipMemset(s.slot_busy, 0, B * g.n_slots * sizeof(int32_t)));
+        HIPCHECK(c, hipMemset(s.slot_since, 0, B * g.n_slots * sizeof(int32_t)));
+    }
+    HIPCHECK(c, hipMemset(s.step, 0, B * sizeof(int32_t)));
     HIPCHECK(c, hipMemset(s.counts, 0, B * 2 * sizeof(int32_t)));
     HIPCHECK(c, hipMemset(s.stats, 0, 8 * sizeof(unsigned long long)));
     HIPCHECK(c, hipDeviceSynchronize());
@@ -495,30 +508,32 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, float *out, float *sco
     HIPCHECK(c, launch_anchor(g, c->t, c->s, q, s0));
     MARK(1);
     HIPCHECK(c, launch_anchor_combine(g, c->t, c->s, out, s0));
-    HIPCHECK(c, launch_scores(g, c->s, sc, s0));
     HIPCHECK(c, launch_select(g, c->s, sc, c->override_sel, sel, s0));
     const bool memcpy_path = c->cfg.flags & WNW_F_RECALL_MEMCPY;
-    if (memcpy_path) {
+    if (!memcpy_path) {
+        MARK(2);
+        // (3) + (4) in one launch: its first work-groups copy the complements listed for recall
+        // from mapped pinned memory into their slots and attend to them as they arrive, the
+        // others run the fixed heads and the tidal rows already on the device.  The slots being
+        // written were freed by this step's select kernel; every kernel that could still read
+        // them (the previous step's) precedes it on this stream.
+        HIPCHECK(c, launch_tidal_fixed(g, c->t, c->s, q, true, s0));
+        MARK(3);
+        MARK(4);
+    } else {
         HIPCHECK(c, hipMemcpyAsync(c->h_newinfo, c->s.counts, g.B * 2 * sizeof(int32_t), hipMemcpyDeviceToHost, s0));
         if (g.k)
             HIPCHECK(c, hipMemcpyAsync(c->h_newinfo + g.B * 2, c->s.new_list, (size_t)g.B * g.k * 2 * sizeof(int32_t),
                                        hipMemcpyDeviceToHost, s0));
-    }
-    HIPCHECK(c, hipEventRecord(c->ev_sel, s0));
-    MARK(2);
-    // (3) recall on the side stream.  The new chunks' slots were freed by this step's select
-    // kernel; every kernel that could still read them (the previous step's) precedes it on s0,
-    // and the copy starts only after ev_sel, so no reader races the copy.  Nothing on s0 reads
-    // a new slot before it waits for ev_rec.
-    // (4a) meanwhile on s0: fixed heads and tidal kept rows, then complements that were already
-    // resident before this step.
-    HIPCHECK(c, launch_subset_static(g, c->t, c->s, q, s0));
-    MARK(3);
-    HIPCHECK(c, launch_subset_slots(g, c->t, c->s, q, false, s0));
-    MARK(4);
-    HIPCHECK(c, hipStreamWaitEvent(c->side, c->ev_sel, 0));
-    if (timing) HIPCHECK(c, hipEventRecord(ev.r[0], c->side));
-    if (memcpy_path) {
+        HIPCHECK(c, hipEventRecord(c->ev_sel, s0));
+        MARK(2);
+        // (4a) device-resident rows while the host waits for the selection and issues the copies
+        HIPCHECK(c, launch_tidal_fixed(g, c->t, c->s, q, false, s0));
+        MARK(3);
+        // (3) copies on the side stream.  The target slots were freed by this step's select
+        // kernel, which follows every earlier reader on s0; the copies start after ev_sel.
+        HIPCHECK(c, hipStreamWaitEvent(c->side, c->ev_sel, 0));
+        if (timing) HIPCHECK(c, hipEventRecord(ev.r[0], c->side));
         HIPCHECK(c, hipEventSynchronize(c->ev_sel));
         const int32_t *cnt = c->h_newinfo, *nl = c->h_newinfo + g.B * 2;
         const size_t cb = (size_t)g.chunk_elems * sizeof(uint16_t);
@@ -539,18 +554,15 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, float *out, float *sco
                 i = j;
             }
         }
-    } else {
-        HIPCHECK(c, launch_recall(g, c->t, c->s, c->side));
+        if (timing) HIPCHECK(c, hipEventRecord(ev.r[1], c->side));
+        HIPCHECK(c, hipEventRecord(c->ev_rec, c->side));
+        HIPCHECK(c, hipStreamWaitEvent(s0, c->ev_rec, 0));
+        // (4b) the complements copied this step
+        HIPCHECK(c, launch_new_slots(g, c->t, c->s, q, s0));
+        MARK(4);
     }
-    if (timing) HIPCHECK(c, hipEventRecord(ev.r[1], c->side));
-    HIPCHECK(c, hipEventRecord(c->ev_rec, c->side));
-    HIPCHECK(c, hipStreamWaitEvent(s0, c->ev_rec, 0));
-    MARK(5);
-    // (4b) tidal complements recalled this step, then the merge of all partials
-    HIPCHECK(c, launch_subset_slots(g, c->t, c->s, q, true, s0));
-    MARK(6);
     HIPCHECK(c, launch_subset_combine(g, c->t, c->s, out, s0));
-    MARK(7);
+    MARK(5);
 #undef MARK
     if (timing) c->pending.push_back(ev);
     c->steps++;
@@ -600,15 +612,15 @@ wnw_status wnw_get_stats(wnw_ctx *c, wnw_stats *o)
     }
     o->anchor_bytes = (int64_t)g.B * g.nA * g.T * 2 * D * 2;
     o->static_bytes = (int64_t)g.B * (g.nT + g.nF) * g.Rs * 2 * D * 2;
+    o->revived_chunks = (int64_t)st[6];
     o->timed_steps = c->timed_steps;
     o->t_anchor_ms = c->t_acc[0];
     o->t_select_ms = c->t_acc[1];
-    o->t_static_ms = c->t_acc[2];
-    o->t_kept_ms = c->t_acc[3];
-    o->t_recall_ms = c->t_acc[4];
-    o->t_new_ms = c->t_acc[5];
-    o->t_combine_ms = c->t_acc[6];
-    o->t_step_ms = c->t_acc[7];
+    o->t_tidal_fixed_ms = c->t_acc[2];
+    o->t_new_ms = c->t_acc[3];
+    o->t_combine_ms = c->t_acc[4];
+    o->t_step_ms = c->t_acc[5];
+    o->t_recall_ms = c->t_acc[6];
     return WNW_OK;
 }
 

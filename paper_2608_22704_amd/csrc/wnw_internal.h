@@ -7,8 +7,10 @@
 namespace wnw {
 
 constexpr int D = 128;          // head dimension handled by the kernels
-constexpr int TILE = 256;       // key rows per attention work-group
 constexpr int NT = 256;         // threads per attention work-group (4 wavefronts)
+constexpr int TILE_A = 128;     // anchor key rows per work-group
+constexpr int TILE_S = 128;     // tidal/fixed kept rows per work-group (slot groups: 128 or 256)
+constexpr int MAX_CHUNK = 256;  // longest chunk the slot kernels handle
 constexpr int SEL_THREADS = 1024;
 
 // Everything the kernels need to know about the cache and the step, fixed at set-up.
@@ -23,9 +25,10 @@ struct Geometry {
     int nA, nT, nF;             // anchor / tidal / fixed KV-heads over all layers
     int n_tiles_a, maxc;        // anchor tiles per head, chunk entries per anchor tile
     int n_tiles_s;              // static tiles per tidal/fixed head
+    int slot_tile;              // rows of one slot-group work-group (TILE_S or 2 * TILE_S)
     int sg;                     // slots per slot-group work-group
-    int ng_kept, ng_new;        // slot groups for kept / newly recalled complements
-    int np;                     // partial entries per tidal/fixed head
+    int ng_kept;                // slot groups for kept complements (new ones: one partial each)
+    int np;                     // partial entries per tidal/fixed head: static tiles, kept groups, k new
     int64_t chunk_elems;        // bf16 elements of one recalled chunk of one sequence
 };
 
@@ -66,11 +69,15 @@ struct StepBuffers {
     // selection state
     int32_t *streak;            // [B][nc]
     int32_t *slot_of;           // [B][nc]  slot holding the chunk's complement or -1
-    int32_t *slot_chunk;        // [B][n_slots] chunk held by the slot or -1
+    int32_t *slot_last;         // [B][nc]  slot that last received the chunk's bytes or -1
+    int32_t *slot_data;         // [B][n_slots] chunk whose bytes the slot holds or -1
+    int32_t *slot_busy;         // [B][n_slots] 1 while assigned to a resident chunk
+    int32_t *slot_since;        // [B][n_slots] step at which the slot was last freed
+    int32_t *step;              // [B] steps run
     int32_t *kept_list;         // [B][n_slots][2] (chunk, slot) resident before and now
     int32_t *new_list;          // [B][k][2]       (chunk, slot) newly resident this step
     int32_t *counts;            // [B][2] kept, new
-    unsigned long long *stats;  // [8] recalled, dropped, resident, slot_rows, peak
+    unsigned long long *stats;  // [8] recalled, dropped, resident, slot_rows, peak, exhausted, revived
 };
 
 // Launchers (wnw_kernels.hip).  Each returns the launch status.
@@ -78,14 +85,20 @@ hipError_t launch_anchor(const Geometry &g, const Tiers &t, const StepBuffers &s
                          hipStream_t st);
 hipError_t launch_anchor_combine(const Geometry &g, const Tiers &t, const StepBuffers &s, float *out,
                                  hipStream_t st);
-hipError_t launch_scores(const Geometry &g, const StepBuffers &s, float *scores, hipStream_t st);
-hipError_t launch_select(const Geometry &g, const StepBuffers &s, const float *scores, const int32_t *override_sel,
+// Scores, selection, residency and slot bookkeeping (writes scores[B][nc] and selected[B][k]).
+hipError_t launch_select(const Geometry &g, const StepBuffers &s, float *scores, const int32_t *override_sel,
                          int32_t *selected, hipStream_t st);
-hipError_t launch_recall(const Geometry &g, const Tiers &t, const StepBuffers &s, hipStream_t st);
-hipError_t launch_subset_static(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q,
-                                hipStream_t st);
-hipError_t launch_subset_slots(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q,
-                               bool new_list, hipStream_t st);
+// Shared memory of the select kernel (bounded at set-up).
+inline size_t select_shared_bytes(const Geometry &g)
+{
+    return (size_t)g.nc * (4 * 8 + 4 + 4 * 4) + (size_t)g.n_slots * 12;
+}
+// Fixed heads, tidal kept rows and resident complements; with `recall`, also the copy of the
+// complements listed for recall from mapped pinned memory, attended to as they arrive.
+hipError_t launch_tidal_fixed(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, bool recall,
+                              hipStream_t st);
+// Complements already copied to their slots by the host-waited recall path.
+hipError_t launch_new_slots(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st);
 hipError_t launch_subset_combine(const Geometry &g, const Tiers &t, const StepBuffers &s, float *out,
                                  hipStream_t st);
 // Set-up: dst[i] = row idx[i] of src_k (idx >= 0), row -idx[i]-2 of src_v (idx <= -2), or zeros

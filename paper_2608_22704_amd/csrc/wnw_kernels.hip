@@ -2,7 +2,7 @@
 //
 // Work decomposition (all kernels are launched by wnw_api.hip on the caller's stream, the
 // recall on a side stream):
-//   anchor_attn     one work-group per (sequence, anchor KV-head, tile of TILE key rows): the
+//   anchor_attn     one work-group per (sequence, anchor KV-head, tile of TILE_A key rows): the
 //                   g q-heads' logits, the tile max, exp, the per-chunk softmax mass (Eq. 2) and
 //                   the unnormalised P.V partial.  Logits and masses are kept in double: the
 //                   chunk ranking must agree with an fp64 reference to well under 1e-6.
@@ -17,19 +17,20 @@
 //   subset_combine  merge of a tidal/fixed head's partials.
 //
 // Layout inside a tile: 16 lanes share one 256-byte key row (8 bf16 = 16 bytes each), so one
-// wavefront load moves 4 rows (1 KiB) fully coalesced; a work-group of 4 wavefronts covers 256
-// rows in 16 steps.  Dot products are reduced across the 16 lanes with cross-lane shuffles.
+// wavefront load moves 4 rows (1 KiB) fully coalesced.  A wavefront owns RPL such 4-row steps
+// and issues all of its K and V loads before computing, so every wavefront keeps 2 * RPL KiB in
+// flight.  Dot products are reduced across the 16 lanes of a row with DPP row permutes.
 #include "wnw_internal.h"
 
 #include <math.h>
+
+#include <algorithm>
 
 namespace wnw {
 
 namespace {
 
 constexpr int WAVES = NT / 64;
-constexpr int ROWS_PER_WAVE = TILE / WAVES;   // 64
-constexpr int STEPS = ROWS_PER_WAVE / 4;      // 16 steps of 4 rows
 constexpr double SCALE_D = 0.088388347648318440550;   // 1 / sqrt(128)
 constexpr float SCALE_F = 0.08838834764831845f;
 
@@ -41,11 +42,29 @@ __device__ inline void unpack8(const uint4 u, float f[8])
     f[6] = __uint_as_float(u.w << 16); f[7] = __uint_as_float(u.w & 0xffff0000u);
 }
 
+// DPP permutes inside a 16-lane row: quad_perm [1,0,3,2] (xor 1), quad_perm [2,3,0,1] (xor 2),
+// row_half_mirror (lane i <-> 7-i inside each 8) and row_mirror (i <-> 15-i).  After the four
+// add steps every lane of the row holds the same, bitwise identical sum.
+template <int CTRL>
+__device__ inline float dpp(float v)
+{
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+template <int CTRL>
+__device__ inline double dpp(double v)
+{
+    const unsigned long long u = (unsigned long long)__double_as_longlong(v);
+    const int lo = __builtin_amdgcn_update_dpp(0, (int)(unsigned)(u & 0xffffffffull), CTRL, 0xF, 0xF, false);
+    const int hi = __builtin_amdgcn_update_dpp(0, (int)(unsigned)(u >> 32), CTRL, 0xF, 0xF, false);
+    return __longlong_as_double((long long)(((unsigned long long)(unsigned)hi << 32) | (unsigned)lo));
+}
 template <typename T>
 __device__ inline T sum16(T v)
 {
-#pragma unroll
-    for (int o = 1; o < 16; o <<= 1) v += __shfl_xor(v, o);
+    v += dpp<0xB1>(v);
+    v += dpp<0x4E>(v);
+    v += dpp<0x141>(v);
+    v += dpp<0x140>(v);
     return v;
 }
 
@@ -107,6 +126,8 @@ __device__ inline void block_sum(T v[G], T *red)
 // -------------------------------------------------------------------------------------------
 // Anchor attention + chunk mass (double logits)
 // -------------------------------------------------------------------------------------------
+constexpr int RPL_A = TILE_A / (4 * WAVES);   // 4-row steps per wavefront (8)
+
 template <int G>
 __global__ __launch_bounds__(NT) void anchor_attn_kernel(Geometry g, Tiers t, StepBuffers s,
                                                          const uint16_t *__restrict__ q)
@@ -118,62 +139,72 @@ __global__ __launch_bounds__(NT) void anchor_attn_kernel(Geometry g, Tiers t, St
     const uint16_t *__restrict__ K = t.aK + hrow * D;
     const uint16_t *__restrict__ V = t.aV + hrow * D;
     const uint16_t *__restrict__ qh = q + (((size_t)b * g.L + l) * g.Hq + (size_t)kv * G) * D;
+    const int t0 = tile * TILE_A;
 
-    __shared__ double xs[G * TILE];      // logits -> probabilities -> (as float) wave partials
+    __shared__ double xs[G * TILE_A];    // logits, then probabilities relative to the tile max
+    __shared__ float wo[WAVES * G * D];  // per-wavefront P.V partials
     __shared__ double red[WAVES * G];
 
+    // q first, then every K and V load of this wavefront (loads return in issue order)
+    uint4 qr[G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) qr[h] = *(const uint4 *)(qh + h * D + sub * 8);
+    uint4 kr[RPL_A], vr[RPL_A];
+#pragma unroll
+    for (int i = 0; i < RPL_A; ++i) {
+        const int row = t0 + wave * 4 * RPL_A + i * 4 + rg;
+        kr[i] = row < g.T ? *(const uint4 *)(K + (size_t)row * D + sub * 8) : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < RPL_A; ++i) {
+        const int row = t0 + wave * 4 * RPL_A + i * 4 + rg;
+        vr[i] = row < g.T ? *(const uint4 *)(V + (size_t)row * D + sub * 8) : make_uint4(0, 0, 0, 0);
+    }
     double qd[G][8];
 #pragma unroll
     for (int h = 0; h < G; ++h) {
         float f[8];
-        unpack8(*(const uint4 *)(qh + h * D + sub * 8), f);
+        unpack8(qr[h], f);
 #pragma unroll
         for (int e = 0; e < 8; ++e) qd[h][e] = (double)f[e];
     }
-
-    const int t0 = tile * TILE;
-    // Pass 1: x = q.k / sqrt(d), exact products, double accumulation.
-    for (int i0 = 0; i0 < STEPS; i0 += 4) {
-        uint4 kr[4];
+    // x = q.k / sqrt(d): exact bf16 products, double accumulation
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int row = t0 + wave * ROWS_PER_WAVE + (i0 + u) * 4 + rg;
-            kr[u] = row < g.T ? *(const uint4 *)(K + (size_t)row * D + sub * 8) : make_uint4(0, 0, 0, 0);
+    for (int i = 0; i < RPL_A; ++i) {
+        const int r = wave * 4 * RPL_A + i * 4 + rg;
+        float f[8];
+        unpack8(kr[i], f);
+        double acc[G];
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+            acc[h] = 0.0;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc[h] = fma(qd[h][e], (double)f[e], acc[h]);
+            acc[h] = sum16(acc[h]);
         }
+        if (sub == 0) {
+            const bool ok = t0 + r < g.T;
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int r = wave * ROWS_PER_WAVE + (i0 + u) * 4 + rg;
-            float f[8];
-            unpack8(kr[u], f);
-            double acc[G];
-#pragma unroll
-            for (int h = 0; h < G; ++h) {
-                acc[h] = 0.0;
-#pragma unroll
-                for (int e = 0; e < 8; ++e) acc[h] = fma(qd[h][e], (double)f[e], acc[h]);
-                acc[h] = sum16(acc[h]);
-            }
-            if (sub == 0) {
-                const bool ok = t0 + r < g.T;
-#pragma unroll
-                for (int h = 0; h < G; ++h) xs[h * TILE + r] = ok ? acc[h] * SCALE_D : -INFINITY;
-            }
+            for (int h = 0; h < G; ++h) xs[h * TILE_A + r] = ok ? acc[h] * SCALE_D : -INFINITY;
         }
     }
     __syncthreads();
 
-    // Tile max, probabilities relative to it, and their sum.
+    // tile max, probabilities relative to it (double exp), their sum
     double m[G], p[G];
 #pragma unroll
-    for (int h = 0; h < G; ++h) m[h] = xs[h * TILE + tid];
+    for (int h = 0; h < G; ++h) m[h] = tid < TILE_A ? xs[h * TILE_A + tid] : -INFINITY;
     block_max<G>(m, red);
 #pragma unroll
     for (int h = 0; h < G; ++h) {
-        const double x = xs[h * TILE + tid];
-        p[h] = (m[h] == -INFINITY) ? 0.0 : exp(x - m[h]);
-        xs[h * TILE + tid] = p[h];
+        p[h] = 0.0;
+        if (tid < TILE_A) {
+            const double x = xs[h * TILE_A + tid];
+            p[h] = (m[h] == -INFINITY) ? 0.0 : exp(x - m[h]);
+            xs[h * TILE_A + tid] = p[h];
+        }
     }
-    block_sum<G>(p, red);     // p[h] now holds the tile sum l; also a barrier for xs
+    block_sum<G>(p, red);     // p[h] now holds the tile sum; also publishes xs
 
     const size_t pidx = ((size_t)b * g.nA + ai) * g.n_tiles_a + tile;
     if (tid == 0) {
@@ -183,40 +214,38 @@ __global__ __launch_bounds__(NT) void anchor_attn_kernel(Geometry g, Tiers t, St
             s.pa_l[pidx * G + h] = p[h];
         }
     }
-    // Per-chunk mass of this tile (Eq. 2 restricted to the tile), fixed summation order.
+    // per-chunk mass of this tile (Eq. 2 restricted to the tile): 16 lanes per (head, chunk)
+    // entry, each summing a fixed stride of rows, then a DPP sum (fixed order)
     const int c_first = t0 / g.cl;
-    for (int idx = tid; idx < G * g.maxc; idx += NT) {
-        const int h = idx / g.maxc, c = c_first + (idx - h * g.maxc);
-        const int r0 = max(c * g.cl, t0), r1 = min(min((c + 1) * g.cl, t0 + TILE), g.Ta);
+    for (int base = 0; base < G * g.maxc * 16; base += NT) {
+        const int idx = base + tid, grp = idx >> 4, k = idx & 15;
+        const bool valid = grp < G * g.maxc;
         double acc = 0.0;
-        for (int r = r0; r < r1; ++r) acc += xs[h * TILE + (r - t0)];
-        s.pa_mass[pidx * G * g.maxc + idx] = acc;
+        if (valid) {
+            const int h = grp / g.maxc, c = c_first + (grp - h * g.maxc);
+            const int r0 = max(c * g.cl, t0), r1 = min(min((c + 1) * g.cl, t0 + TILE_A), g.Ta);
+            for (int r = r0 + k; r < r1; r += 16) acc += xs[h * TILE_A + (r - t0)];
+        }
+        acc = sum16(acc);
+        if (valid && k == 0) s.pa_mass[pidx * G * g.maxc + grp] = acc;
     }
 
-    // Pass 2: unnormalised P.V in fp32.
+    // unnormalised P.V in fp32
     float acc[G][8];
 #pragma unroll
     for (int h = 0; h < G; ++h)
 #pragma unroll
         for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
-    for (int i0 = 0; i0 < STEPS; i0 += 4) {
-        uint4 vr[4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int row = t0 + wave * ROWS_PER_WAVE + (i0 + u) * 4 + rg;
-            vr[u] = row < g.T ? *(const uint4 *)(V + (size_t)row * D + sub * 8) : make_uint4(0, 0, 0, 0);
-        }
+    for (int i = 0; i < RPL_A; ++i) {
+        const int r = wave * 4 * RPL_A + i * 4 + rg;
+        float f[8];
+        unpack8(vr[i], f);
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int r = wave * ROWS_PER_WAVE + (i0 + u) * 4 + rg;
-            float f[8];
-            unpack8(vr[u], f);
+        for (int h = 0; h < G; ++h) {
+            const float ph = (float)xs[h * TILE_A + r];
 #pragma unroll
-            for (int h = 0; h < G; ++h) {
-                const float ph = (float)xs[h * TILE + r];
-#pragma unroll
-                for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(ph, f[e], acc[h][e]);
-            }
+            for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(ph, f[e], acc[h][e]);
         }
     }
 #pragma unroll
@@ -226,83 +255,103 @@ __global__ __launch_bounds__(NT) void anchor_attn_kernel(Geometry g, Tiers t, St
             acc[h][e] += __shfl_xor(acc[h][e], 16);
             acc[h][e] += __shfl_xor(acc[h][e], 32);
         }
-    __syncthreads();                     // every read of xs is done
-    float *ored = (float *)xs;           // [WAVES][G][D]
     if (rg == 0)
 #pragma unroll
         for (int h = 0; h < G; ++h)
 #pragma unroll
-            for (int e = 0; e < 8; ++e) ored[(wave * G + h) * D + sub * 8 + e] = acc[h][e];
+            for (int e = 0; e < 8; ++e) wo[(wave * G + h) * D + sub * 8 + e] = acc[h][e];
     __syncthreads();
     for (int idx = tid; idx < G * D; idx += NT) {
         float o = 0.f;
 #pragma unroll
-        for (int w = 0; w < WAVES; ++w) o += ored[w * G * D + idx];
+        for (int w = 0; w < WAVES; ++w) o += wo[w * G * D + idx];
         s.pa_o[pidx * G * D + idx] = o;
     }
 }
 
-template <int G>
-__global__ __launch_bounds__(NT) void anchor_combine_kernel(Geometry g, Tiers t, StepBuffers s, float *out)
+template <typename T>
+__device__ inline T block_max1(T v, T *red)
 {
-    const int ai = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
-    extern __shared__ double fac[];      // [n_tiles_a][G]
-    __shared__ double Mh[G], Lh[G];
-    const size_t base = ((size_t)b * g.nA + ai) * g.n_tiles_a;
-    const int nt = g.n_tiles_a;
-    if (tid < G) {
-        double M = -INFINITY;
-        for (int i = 0; i < nt; ++i) M = fmax(M, s.pa_m[(base + i) * G + tid]);
-        double L = 0.0;
-        if (M > -INFINITY)
-            for (int i = 0; i < nt; ++i) {
-                const double mi = s.pa_m[(base + i) * G + tid];
-                if (mi > -INFINITY) L += s.pa_l[(base + i) * G + tid] * exp(mi - M);
-            }
-        Mh[tid] = M;
-        Lh[tid] = L;
-    }
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    v = wave_max(v);
+    if (lane == 0) red[wave] = v;
     __syncthreads();
-    for (int idx = tid; idx < nt * G; idx += NT) {
-        const int h = idx % G;
-        const double mi = s.pa_m[base * G + idx];
-        fac[idx] = (Lh[h] > 0.0 && mi > -INFINITY) ? exp(mi - Mh[h]) / Lh[h] : 0.0;
-    }
+    T m = red[0];
+    for (int w = 1; w < nw; ++w) m = fmax(m, red[w]);
     __syncthreads();
-    const int lk = t.anchor_lk[ai], l = lk / g.Hkv, kv = lk - l * g.Hkv;
-    float *oh = out + (((size_t)b * g.L + l) * g.Hq + (size_t)kv * G) * D;
-    for (int idx = tid; idx < G * D; idx += NT) {
-        const int h = idx / D;
-        double acc = 0.0;
-        for (int i = 0; i < nt; ++i) acc += (double)s.pa_o[(base + i) * G * D + idx] * fac[i * G + h];
-        oh[idx] = (float)acc;
-    }
-    double *mass = s.mass + ((size_t)b * g.nA + ai) * G * (size_t)g.nc;
-    for (int idx = tid; idx < G * g.nc; idx += NT) {
-        const int h = idx / g.nc, c = idx - h * g.nc;
-        const int t_lo = (c * g.cl) / TILE, t_hi = (min((c + 1) * g.cl, g.Ta) - 1) / TILE;
-        double acc = 0.0;
-        for (int i = t_lo; i <= t_hi; ++i) {
-            const int j = c - (i * TILE) / g.cl;
-            acc += s.pa_mass[((base + i) * G + h) * g.maxc + j] * fac[i * G + h];
-        }
-        mass[idx] = acc;
-    }
+    return m;
 }
 
-__global__ void scores_kernel(Geometry g, StepBuffers s, float *scores)
+template <typename T>
+__device__ inline T block_sum1(T v, T *red)
 {
-    const int i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= g.B * g.nc) return;
-    const int b = i / g.nc, c = i - b * g.nc, naq = g.nA * g.G;
-    const double *m = s.mass + (size_t)b * naq * g.nc + c;
-    double acc = 0.0;
-    for (int a = 0; a < naq; ++a) acc += m[(size_t)a * g.nc];
-    scores[i] = (float)(acc / (double)chunk_len_of(g, c));
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    v = wave_sum(v);
+    if (lane == 0) red[wave] = v;
+    __syncthreads();
+    T m = red[0];
+    for (int w = 1; w < nw; ++w) m += red[w];
+    __syncthreads();
+    return m;
+}
+
+// Log-sum-exp merge of the tiles of one (anchor KV-head, q-head): output row and the head's
+// normalised per-chunk softmax mass (Eq. 2 for this head), all in double.  COMBINE_THREADS
+// threads: the tiles of every output column are split over COMBINE_THREADS / D groups, summed
+// in a fixed order.
+constexpr int COMBINE_THREADS = 1024;
+constexpr int CGROUPS = COMBINE_THREADS / D;
+
+template <int G>
+__global__ __launch_bounds__(COMBINE_THREADS) void anchor_combine_kernel(Geometry g, Tiers t, StepBuffers s, float *out)
+{
+    const int ai = blockIdx.x, h = blockIdx.y, b = blockIdx.z, tid = threadIdx.x;
+    extern __shared__ double fac[];      // [n_tiles_a]
+    __shared__ double red[COMBINE_THREADS / 64];
+    __shared__ double ocol[CGROUPS][D];
+    const int nt = g.n_tiles_a;
+    const size_t base = ((size_t)b * g.nA + ai) * nt;
+    double m = -INFINITY;
+    for (int i = tid; i < nt; i += COMBINE_THREADS) m = fmax(m, s.pa_m[(base + i) * G + h]);
+    const double M = block_max1(m, red);
+    double l = 0.0;
+    for (int i = tid; i < nt; i += COMBINE_THREADS) {
+        const double mi = s.pa_m[(base + i) * G + h];
+        const double f = (M > -INFINITY && mi > -INFINITY) ? exp(mi - M) : 0.0;
+        fac[i] = f;
+        l += s.pa_l[(base + i) * G + h] * f;
+    }
+    const double L = block_sum1(l, red);      // also publishes fac[]
+    const double inv = L > 0.0 ? 1.0 / L : 0.0;
+    {
+        const int d = tid % D, grp = tid / D;
+        const int i0 = grp * nt / CGROUPS, i1 = (grp + 1) * nt / CGROUPS;
+        double acc = 0.0;
+#pragma unroll 8
+        for (int i = i0; i < i1; ++i) acc += (double)s.pa_o[((base + i) * G + h) * D + d] * fac[i];
+        ocol[grp][d] = acc;
+        __syncthreads();
+        if (grp == 0) {
+#pragma unroll
+            for (int j = 1; j < CGROUPS; ++j) acc += ocol[j][d];
+            const int lk = t.anchor_lk[ai], ll = lk / g.Hkv, kv = lk - ll * g.Hkv;
+            out[(((size_t)b * g.L + ll) * g.Hq + (size_t)kv * G + h) * D + d] = (float)(acc * inv);
+        }
+    }
+    double *mass = s.mass + (((size_t)b * g.nA + ai) * G + h) * (size_t)g.nc;
+    for (int c = tid; c < g.nc; c += COMBINE_THREADS) {
+        const int t_lo = (c * g.cl) / TILE_A, t_hi = (min((c + 1) * g.cl, g.Ta) - 1) / TILE_A;
+        double acc = 0.0;
+        for (int i = t_lo; i <= t_hi; ++i) {
+            const int j = c - (i * TILE_A) / g.cl;
+            acc += s.pa_mass[((base + i) * G + h) * g.maxc + j] * fac[i];
+        }
+        mass[c] = acc * inv;
+    }
 }
 
 // -------------------------------------------------------------------------------------------
-// Selection, residency and slot bookkeeping: one work-group per sequence.
+// Chunk scores, selection, residency and slot bookkeeping: one work-group per sequence.
 // -------------------------------------------------------------------------------------------
 __device__ int block_scan_excl(int *a, int n, int *wsum)
 {
@@ -336,35 +385,70 @@ __device__ int block_scan_excl(int *a, int n, int *wsum)
     return carry;
 }
 
-__global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuffers s, const float *__restrict__ scores,
+constexpr int SCORE_PARTS = 4;   // anchor q-heads split in this many fixed ranges per chunk
+
+// Per sequence b:
+//   scores   score_c = (sum over anchor q-heads of their chunk mass) / |c|, double, fixed order
+//   select   top-k by (fp32 score desc, id asc), or the caller's override
+//   streaks  0 when selected, else +1 (capped at delta); resident iff streak < delta
+//   slots    chunks that stop being resident free their slot; a newly resident chunk whose
+//            bytes still sit in a free slot (never overwritten since) takes that slot back with
+//            no copy; the others take free slots in least-recently-freed order (never-used
+//            slots first) and are listed for recall
+//   lists    kept list = resident with their bytes on the device; new list = to be recalled
+__global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuffers s, float *__restrict__ scores,
                                                              const int32_t *__restrict__ ovr, int32_t *__restrict__ selected)
 {
     const int b = blockIdx.x, tid = threadIdx.x, nthr = blockDim.x;
-    const int nc = g.nc, k = g.k, ns = g.n_slots;
-    extern __shared__ int smem[];
-    float *sc = (float *)smem;           // [nc]
-    int *fsel = smem + nc;               // [nc] selected flag
-    int *fnew = fsel + nc;               // [nc] newly resident flag
-    int *fkept = fnew + nc;              // [nc] resident before and now
-    int *rank = fkept + nc;              // [nc] scan scratch
-    int *ffree = rank + nc;              // [ns] free slot flag
-    int *freelist = ffree + ns;          // [ns] free slots ascending
+    const int nc = g.nc, k = g.k, ns = g.n_slots, naq = g.nA * g.G;
+    extern __shared__ double sdyn[];
+    double *part = sdyn;                              // [SCORE_PARTS][nc]
+    float *sc = (float *)(part + SCORE_PARTS * nc);   // [nc]
+    int *fsel = (int *)(sc + nc);                     // [nc]
+    int *fnew = fsel + nc;                            // [nc]
+    int *fkept = fnew + nc;                           // [nc]
+    int *rank = fkept + nc;                           // [nc]
+    int *sfree = rank + nc;                           // [ns] free flag, then rank
+    int *freelist = sfree + ns;                       // [ns]
+    int *skey = freelist + ns;                        // [ns] ordering key of free slots
     __shared__ int wsum[SEL_THREADS / 64 + 1];
-    __shared__ int ndrop, nrows;
+    __shared__ int ndrop, nrows, nrev;
 
+    int32_t *streak = s.streak + (size_t)b * nc, *slot_of = s.slot_of + (size_t)b * nc;
+    int32_t *slot_last = s.slot_last + (size_t)b * nc;
+    int32_t *slot_data = s.slot_data + (size_t)b * ns, *slot_busy = s.slot_busy + (size_t)b * ns;
+    int32_t *slot_since = s.slot_since + (size_t)b * ns;
+    const int step = s.step[b];
+
+    // scores
+    for (int idx = tid; idx < SCORE_PARTS * nc; idx += nthr) {
+        const int p = idx / nc, c = idx - p * nc;
+        const int a0 = p * naq / SCORE_PARTS, a1 = (p + 1) * naq / SCORE_PARTS;
+        const double *m = s.mass + ((size_t)b * naq + a0) * nc + c;
+        double acc = 0.0;
+#pragma unroll 8
+        for (int a = a0; a < a1; ++a) acc += m[(size_t)(a - a0) * nc];
+        part[idx] = acc;
+    }
+    if (tid == 0) ndrop = nrows = nrev = 0;
+    __syncthreads();
     for (int c = tid; c < nc; c += nthr) {
-        sc[c] = scores[(size_t)b * nc + c];
+        double acc = part[c];
+        for (int p = 1; p < SCORE_PARTS; ++p) acc += part[p * nc + c];
+        const float v = (float)(acc / (double)chunk_len_of(g, c));
+        sc[c] = v;
+        scores[(size_t)b * nc + c] = v;
         fsel[c] = 0;
     }
-    if (tid == 0) ndrop = nrows = 0;
     __syncthreads();
+
+    // selection
     if (ovr) {
         for (int i = tid; i < k; i += nthr) {
             const int c = ovr[(size_t)b * k + i];
             if (c >= 0 && c < nc) fsel[c] = 1;
         }
     } else {
-        // rank of chunk c under (score desc, id asc); selected iff rank < k
         for (int c = tid; c < nc; c += nthr) {
             const float v = sc[c];
             int cnt = 0;
@@ -377,8 +461,7 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
     }
     __syncthreads();
 
-    int32_t *streak = s.streak + (size_t)b * nc, *slot_of = s.slot_of + (size_t)b * nc;
-    int32_t *slot_chunk = s.slot_chunk + (size_t)b * ns;
+    // streaks, residency, drops
     for (int c = tid; c < nc; c += nthr) {
         int st = streak[c];
         st = fsel[c] ? 0 : min(st + 1, g.delta);
@@ -387,7 +470,8 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
         const int slot = slot_of[c];
         const bool was = slot >= 0;
         if (was && !now) {
-            slot_chunk[slot] = -1;
+            slot_busy[slot] = 0;
+            slot_since[slot] = step;
             slot_of[c] = -1;
             atomicAdd(&ndrop, 1);
         }
@@ -395,6 +479,19 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
         fkept[c] = now && was;
         if (now) atomicAdd(&nrows, comp_of(g, c));
     }
+    __syncthreads();
+    // revival: the chunk's bytes are still in the free slot it last occupied
+    for (int c = tid; c < nc; c += nthr)
+        if (fnew[c]) {
+            const int sl = slot_last[c];
+            if (sl >= 0 && !slot_busy[sl] && slot_data[sl] == c) {
+                slot_busy[sl] = 1;
+                slot_of[c] = sl;
+                fnew[c] = 0;
+                fkept[c] = 1;
+                atomicAdd(&nrev, 1);
+            }
+        }
     __syncthreads();
 
     // selected ids, ascending
@@ -406,21 +503,36 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
             if (fsel[c]) selected[(size_t)b * k + rank[c]] = c;
         for (int i = nsel + tid; i < k; i += nthr) selected[(size_t)b * k + i] = -1;
     }
-    __syncthreads();
 
-    // free slots, ascending
-    for (int i = tid; i < ns; i += nthr) ffree[i] = slot_chunk[i] < 0;
+    // free slots ordered by (holds data, freed at step, slot id): never-used first, then the
+    // least recently freed.  Key: -1 for busy slots, else (holds data) * 2^30 + freed-at step.
+    for (int i = tid; i < ns; i += nthr) {
+        sfree[i] = !slot_busy[i];
+        skey[i] = slot_busy[i] ? -1 : ((slot_data[i] >= 0 ? 1 : 0) << 30) + slot_since[i];
+    }
     __syncthreads();
-    for (int i = tid; i < ns; i += nthr) freelist[i] = ffree[i];
+    for (int i = tid; i < ns; i += nthr) {
+        freelist[i] = -1;
+        if (!sfree[i]) continue;
+        const int ki = skey[i];
+        int r = 0;
+        for (int j = 0; j < ns; ++j) {
+            const int kj = skey[j];
+            r += kj >= 0 && (kj < ki || (kj == ki && j < i));
+        }
+        freelist[i] = r;
+    }
     __syncthreads();
-    const int nfree = block_scan_excl(freelist, ns, wsum);   // freelist holds ranks now
-    for (int i = tid; i < ns; i += nthr) ffree[i] = ffree[i] ? freelist[i] : -1;
+    int nfree = 0;
+    for (int i = 0; i < ns; ++i) nfree += sfree[i];
+    __syncthreads();
+    for (int i = tid; i < ns; i += nthr) sfree[i] = freelist[i];
     __syncthreads();
     for (int i = tid; i < ns; i += nthr)
-        if (ffree[i] >= 0) freelist[ffree[i]] = i;
+        if (sfree[i] >= 0) freelist[sfree[i]] = i;
     __syncthreads();
 
-    // newly resident chunks take the free slots in order (lowest id -> lowest slot)
+    // chunks to recall take the free slots in that order (lowest id first)
     for (int c = tid; c < nc; c += nthr) rank[c] = fnew[c];
     __syncthreads();
     const int nnew = block_scan_excl(rank, nc, wsum);
@@ -429,7 +541,9 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
         if (fnew[c] && rank[c] < nfree && rank[c] < k) {
             const int slot = freelist[rank[c]];
             slot_of[c] = slot;
-            slot_chunk[slot] = c;
+            slot_last[c] = slot;
+            slot_busy[slot] = 1;
+            slot_data[slot] = c;
             nl[rank[c] * 2] = c;
             nl[rank[c] * 2 + 1] = slot;
         }
@@ -448,117 +562,111 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
         const int nn = min(nnew, min(nfree, k));
         s.counts[b * 2] = nkept;
         s.counts[b * 2 + 1] = nn;
+        s.step[b] = step + 1;
         atomicAdd(&s.stats[0], (unsigned long long)nn);
         atomicAdd(&s.stats[1], (unsigned long long)ndrop);
         atomicAdd(&s.stats[2], (unsigned long long)(nkept + nn));
         atomicAdd(&s.stats[3], (unsigned long long)nrows);
         atomicMax(&s.stats[4], (unsigned long long)(nkept + nn));
         if (nnew > nn) atomicAdd(&s.stats[5], 1ull);   // slot exhaustion (never expected)
+        atomicAdd(&s.stats[6], (unsigned long long)nrev);
     }
 }
 
 // -------------------------------------------------------------------------------------------
-// Recall: newly resident complements, mapped pinned host memory -> device slots.
+// Tidal / fixed attention (fp32 logits).  Each wavefront runs its own softmax over its 4 * RPL
+// rows (no barrier until the end); the four wavefront partials are merged in shared memory.
 // -------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void recall_kernel(Geometry g, Tiers t, StepBuffers s)
-{
-    const int i = blockIdx.y, b = blockIdx.z;
-    if (i >= s.counts[b * 2 + 1]) return;
-    const int c = s.new_list[((size_t)b * g.k + i) * 2], slot = s.new_list[((size_t)b * g.k + i) * 2 + 1];
-    const uint4 *src = (const uint4 *)(t.host_comp + ((size_t)b * g.nc + c) * g.chunk_elems);
-    uint4 *dst = (uint4 *)(t.slots + ((size_t)b * g.n_slots + slot) * g.chunk_elems);
-    const size_t n16 = (size_t)g.chunk_elems * 2 / 16;
-    for (size_t j = (size_t)blockIdx.x * blockDim.x + threadIdx.x; j < n16; j += (size_t)gridDim.x * blockDim.x)
-        dst[j] = src[j];
-}
+// Source rows of one key position (nullptr when the position is not in the tile) and, for the
+// recall path, where to copy them.
+struct RowPtr {
+    const uint16_t *k, *v;
+    uint16_t *kd = nullptr, *vd = nullptr;
+};
 
-// -------------------------------------------------------------------------------------------
-// Tidal / fixed attention (fp32 logits): one tile of up to TILE rows given by a row map.
-// -------------------------------------------------------------------------------------------
-template <int G, class RowMap>
-__device__ inline void subset_tile(const uint16_t *__restrict__ qh, RowMap map, float *pm, float *pl, float *po)
+template <int G, int RPL, class RowMap>
+__device__ inline void subset_tile(const uint16_t *__restrict__ qh, const RowMap &map, float *pm, float *pl, float *po)
 {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, sub = lane & 15, rg = lane >> 4;
-    __shared__ float xs[WAVES * G * D];  // logits (G*TILE) -> probabilities -> wave partials
-    __shared__ float red[WAVES * G];
-    static_assert(WAVES * D >= TILE, "partial buffer must hold the logits");
+    __shared__ float wm[WAVES * G], wl[WAVES * G];
+    __shared__ float wo[WAVES * G * D];
 
+    uint4 qr[G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) qr[h] = *(const uint4 *)(qh + h * D + sub * 8);
+    uint4 kr[RPL], vr[RPL];
+    bool ok[RPL];
+#pragma unroll
+    for (int i = 0; i < RPL; ++i) {
+        const RowPtr rp = map.row(wave * 4 * RPL + i * 4 + rg);
+        ok[i] = rp.k != nullptr;
+        kr[i] = ok[i] ? *(const uint4 *)(rp.k + sub * 8) : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < RPL; ++i) {
+        const RowPtr rp = map.row(wave * 4 * RPL + i * 4 + rg);
+        vr[i] = ok[i] ? *(const uint4 *)(rp.v + sub * 8) : make_uint4(0, 0, 0, 0);
+    }
     float qf[G][8];
 #pragma unroll
-    for (int h = 0; h < G; ++h) unpack8(*(const uint4 *)(qh + h * D + sub * 8), qf[h]);
+    for (int h = 0; h < G; ++h) unpack8(qr[h], qf[h]);
 
-    for (int i0 = 0; i0 < STEPS; i0 += 4) {
-        uint4 kr[4];
+    if constexpr (RowMap::copies) {
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int r = wave * ROWS_PER_WAVE + (i0 + u) * 4 + rg;
-            const uint16_t *kp = map.k(r);
-            kr[u] = kp ? *(const uint4 *)(kp + sub * 8) : make_uint4(0, 0, 0, 0);
-        }
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int r = wave * ROWS_PER_WAVE + (i0 + u) * 4 + rg;
-            float f[8];
-            unpack8(kr[u], f);
-            float acc[G];
-#pragma unroll
-            for (int h = 0; h < G; ++h) {
-                acc[h] = 0.f;
-#pragma unroll
-                for (int e = 0; e < 8; ++e) acc[h] = fmaf(qf[h][e], f[e], acc[h]);
-                acc[h] = sum16(acc[h]);
+        for (int i = 0; i < RPL; ++i)
+            if (ok[i]) {
+                const RowPtr rp = map.row(wave * 4 * RPL + i * 4 + rg);
+                *(uint4 *)(rp.kd + sub * 8) = kr[i];
+                *(uint4 *)(rp.vd + sub * 8) = vr[i];
             }
-            if (sub == 0) {
-                const bool ok = map.valid(r);
-#pragma unroll
-                for (int h = 0; h < G; ++h) xs[h * TILE + r] = ok ? acc[h] * SCALE_F : -INFINITY;
-            }
-        }
     }
-    __syncthreads();
-    float m[G], p[G];
+    float x[RPL][G];
 #pragma unroll
-    for (int h = 0; h < G; ++h) m[h] = xs[h * TILE + tid];
-    block_max<G>(m, red);
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-        const float x = xs[h * TILE + tid];
-        p[h] = (m[h] == -INFINITY) ? 0.f : __expf(x - m[h]);
-        xs[h * TILE + tid] = p[h];
-    }
-    block_sum<G>(p, red);
-    if (tid == 0)
+    for (int i = 0; i < RPL; ++i) {
+        float f[8];
+        unpack8(kr[i], f);
 #pragma unroll
         for (int h = 0; h < G; ++h) {
-            pm[h] = m[h];
-            pl[h] = p[h];
+            float acc = 0.f;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc = fmaf(qf[h][e], f[e], acc);
+            acc = sum16(acc);
+            x[i][h] = ok[i] ? acc * SCALE_F : -INFINITY;
         }
-
+    }
+    float m[G], l[G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+        float mm = x[0][h];
+#pragma unroll
+        for (int i = 1; i < RPL; ++i) mm = fmaxf(mm, x[i][h]);
+        mm = fmaxf(mm, __shfl_xor(mm, 16));
+        mm = fmaxf(mm, __shfl_xor(mm, 32));
+        m[h] = mm;
+        float ll = 0.f;
+#pragma unroll
+        for (int i = 0; i < RPL; ++i) {
+            const float pv = (mm == -INFINITY) ? 0.f : __expf(x[i][h] - mm);
+            x[i][h] = pv;
+            ll += pv;
+        }
+        ll += __shfl_xor(ll, 16);
+        ll += __shfl_xor(ll, 32);
+        l[h] = ll;
+    }
     float acc[G][8];
 #pragma unroll
     for (int h = 0; h < G; ++h)
 #pragma unroll
         for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
-    for (int i0 = 0; i0 < STEPS; i0 += 4) {
-        uint4 vr[4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int r = wave * ROWS_PER_WAVE + (i0 + u) * 4 + rg;
-            const uint16_t *vp = map.v(r);
-            vr[u] = vp ? *(const uint4 *)(vp + sub * 8) : make_uint4(0, 0, 0, 0);
-        }
+    for (int i = 0; i < RPL; ++i) {
+        float f[8];
+        unpack8(vr[i], f);
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int r = wave * ROWS_PER_WAVE + (i0 + u) * 4 + rg;
-            float f[8];
-            unpack8(vr[u], f);
+        for (int h = 0; h < G; ++h)
 #pragma unroll
-            for (int h = 0; h < G; ++h) {
-                const float ph = xs[h * TILE + r];
-#pragma unroll
-                for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(ph, f[e], acc[h][e]);
-            }
-        }
+            for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(x[i][h], f[e], acc[h][e]);
     }
 #pragma unroll
     for (int h = 0; h < G; ++h)
@@ -567,121 +675,290 @@ __device__ inline void subset_tile(const uint16_t *__restrict__ qh, RowMap map, 
             acc[h][e] += __shfl_xor(acc[h][e], 16);
             acc[h][e] += __shfl_xor(acc[h][e], 32);
         }
-    __syncthreads();
     if (rg == 0)
 #pragma unroll
         for (int h = 0; h < G; ++h)
 #pragma unroll
-            for (int e = 0; e < 8; ++e) xs[(wave * G + h) * D + sub * 8 + e] = acc[h][e];
+            for (int e = 0; e < 8; ++e) wo[(wave * G + h) * D + sub * 8 + e] = acc[h][e];
+    if (lane == 0)
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+            wm[wave * G + h] = m[h];
+            wl[wave * G + h] = l[h];
+        }
     __syncthreads();
     for (int idx = tid; idx < G * D; idx += NT) {
+        const int h = idx / D;
+        float M = wm[h];
+#pragma unroll
+        for (int w = 1; w < WAVES; ++w) M = fmaxf(M, wm[w * G + h]);
         float o = 0.f;
 #pragma unroll
-        for (int w = 0; w < WAVES; ++w) o += xs[w * G * D + idx];
+        for (int w = 0; w < WAVES; ++w) {
+            const float mw = wm[w * G + h];
+            if (mw > -INFINITY) o += wo[w * G * D + idx] * __expf(mw - M);
+        }
         po[idx] = o;
     }
+    if (tid < G) {
+        float M = wm[tid];
+#pragma unroll
+        for (int w = 1; w < WAVES; ++w) M = fmaxf(M, wm[w * G + tid]);
+        float L = 0.f;
+#pragma unroll
+        for (int w = 0; w < WAVES; ++w) {
+            const float mw = wm[w * G + tid];
+            if (mw > -INFINITY) L += wl[w * G + tid] * __expf(mw - M);
+        }
+        pm[tid] = M;
+        pl[tid] = L;
+    }
+    __syncthreads();   // the shared partials may be reused by the next tile of this work-group
 }
 
 struct StaticRows {
+    static constexpr bool copies = false;
     const uint16_t *K, *V;
     int t0, R;
-    __device__ bool valid(int r) const { return t0 + r < R; }
-    __device__ const uint16_t *k(int r) const { return valid(r) ? K + (size_t)(t0 + r) * D : nullptr; }
-    __device__ const uint16_t *v(int r) const { return valid(r) ? V + (size_t)(t0 + r) * D : nullptr; }
+    __device__ RowPtr row(int r) const
+    {
+        if (t0 + r >= R) return {nullptr, nullptr};
+        const size_t o = (size_t)(t0 + r) * D;
+        return {K + o, V + o};
+    }
 };
 
+// Rows of a group of resident complements.  The group's entries are staged in shared memory as
+// (K row base, valid rows) so that the row map needs no global load.
 struct SlotRows {
-    const uint16_t *slots;   // base of this sequence's slots
-    const int32_t *list;     // (chunk, slot) entries of this group
-    int n_entries, ti, comp_max, nT, Ta, cl, budget_bp;
-    __device__ const uint16_t *row(int r, int half) const
+    static constexpr bool copies = false;
+    const uint16_t *const *kbase;   // [sg] first K row of the tidal head in the entry's slot
+    const int *nrows;               // [sg] valid rows of the entry (complement length)
+    int n_entries, comp_max;
+    __device__ RowPtr row(int r) const
     {
         const int e = r / comp_max, rr = r - e * comp_max;
-        if (e >= n_entries) return nullptr;
-        const int c = list[e * 2], slot = list[e * 2 + 1];
-        const int len = min((c + 1) * cl, Ta) - c * cl;
-        if (rr >= len - keep_of_len(budget_bp, len)) return nullptr;
-        return slots + ((((size_t)slot * nT + ti) * 2 + half) * comp_max + rr) * D;
+        if (e >= n_entries || rr >= nrows[e]) return {nullptr, nullptr};
+        const uint16_t *k = kbase[e] + (size_t)rr * D;
+        return {k, k + (size_t)comp_max * D};
     }
-    __device__ bool valid(int r) const { return row(r, 0) != nullptr; }
-    __device__ const uint16_t *k(int r) const { return row(r, 0); }
-    __device__ const uint16_t *v(int r) const { return row(r, 1); }
 };
 
+// Rows of one recalled unit (a tidal head's complement of one chunk): read from the mapped
+// pinned host block, copied through to the device slot on the way.
+struct RecallRows {
+    static constexpr bool copies = true;
+    const uint16_t *src;     // host block: comp_max K rows then comp_max V rows
+    uint16_t *dst;           // device slot block, same layout
+    int nrows, comp_max;
+    __device__ RowPtr row(int r) const
+    {
+        if (r >= nrows) return {nullptr, nullptr};
+        const size_t ko = (size_t)r * D, vo = (size_t)(comp_max + r) * D;
+        return {src + ko, src + vo, dst + ko, dst + vo};
+    }
+};
+
+constexpr int RPL_S = TILE_S / (4 * WAVES);   // 8
+constexpr int RECALL_WGS = 64;                // work-groups that recall (fills the host link)
+
 template <int G>
-__global__ __launch_bounds__(NT) void subset_static_kernel(Geometry g, Tiers t, StepBuffers s, const uint16_t *__restrict__ q)
+__device__ inline void static_tile(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, int tile,
+                                   int hi, int b)
 {
-    const int tile = blockIdx.x, hi = blockIdx.y, b = blockIdx.z;
     const bool tidal = hi < g.nT;
     const int idx = tidal ? hi : hi - g.nT;
     const int lk = tidal ? t.tidal_lk[idx] : t.fixed_lk[idx], l = lk / g.Hkv, kv = lk - l * g.Hkv;
     const size_t hb = ((size_t)b * (tidal ? g.nT : g.nF) + idx) * (size_t)g.Rs * D;
-    StaticRows map{(tidal ? t.tK : t.fK) + hb, (tidal ? t.tV : t.fV) + hb, tile * TILE, g.Rs};
+    const StaticRows map{(tidal ? t.tK : t.fK) + hb, (tidal ? t.tV : t.fV) + hb, tile * TILE_S, g.Rs};
     const uint16_t *qh = q + (((size_t)b * g.L + l) * g.Hq + (size_t)kv * G) * D;
     const size_t p = ((size_t)b * (g.nT + g.nF) + hi) * g.np + tile;
-    subset_tile<G>(qh, map, s.ps_m + p * G, s.ps_l + p * G, s.ps_o + p * G * D);
+    subset_tile<G, RPL_S>(qh, map, s.ps_m + p * G, s.ps_l + p * G, s.ps_o + p * G * D);
 }
 
-template <int G>
-__global__ __launch_bounds__(NT) void subset_slots_kernel(Geometry g, Tiers t, StepBuffers s, const uint16_t *__restrict__ q,
-                                                          int which)
+// Slot group `grp` of list `which` (0 kept, 1 new) of tidal head ti; epg entries per group.
+template <int G, int RPL>
+__device__ inline void slot_group(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, int grp,
+                                  int ti, int b, int which, int epg)
 {
-    const int grp = blockIdx.x, ti = blockIdx.y, b = blockIdx.z;
     const int cnt = s.counts[b * 2 + which];
-    if (grp * g.sg >= cnt) return;
-    const int32_t *list = which ? s.new_list + (size_t)b * g.k * 2 : s.kept_list + (size_t)b * g.n_slots * 2;
+    if (grp * epg >= cnt) return;
+    constexpr int MAXE = 4 * RPL * WAVES;   // entries of one group never exceed its rows
+    __shared__ const uint16_t *kbase[MAXE];
+    __shared__ int nrows[MAXE];
+    const int n_entries = min(epg, cnt - grp * epg);
+    const int32_t *list = (which ? s.new_list + (size_t)b * g.k * 2 : s.kept_list + (size_t)b * g.n_slots * 2) +
+                          (size_t)grp * epg * 2;
+    for (int e = threadIdx.x; e < n_entries; e += NT) {
+        const int c = list[e * 2], slot = list[e * 2 + 1];
+        kbase[e] = t.slots + ((size_t)b * g.n_slots + slot) * g.chunk_elems + (size_t)ti * 2 * g.comp_max * D;
+        nrows[e] = comp_of(g, c);
+    }
+    __syncthreads();
     const int lk = t.tidal_lk[ti], l = lk / g.Hkv, kv = lk - l * g.Hkv;
-    SlotRows map{t.slots + (size_t)b * g.n_slots * g.chunk_elems, list + grp * g.sg * 2,
-                 min(g.sg, cnt - grp * g.sg), ti, g.comp_max, g.nT, g.Ta, g.cl, g.budget_bp};
+    const SlotRows map{kbase, nrows, n_entries, g.comp_max};
     const uint16_t *qh = q + (((size_t)b * g.L + l) * g.Hq + (size_t)kv * G) * D;
     const size_t p = ((size_t)b * (g.nT + g.nF) + ti) * g.np + g.n_tiles_s + (which ? g.ng_kept : 0) + grp;
-    subset_tile<G>(qh, map, s.ps_m + p * G, s.ps_l + p * G, s.ps_o + p * G * D);
+    subset_tile<G, RPL>(qh, map, s.ps_m + p * G, s.ps_l + p * G, s.ps_o + p * G * D);
 }
 
+// Recall work-group w of nw: walks the units (sequence, new entry, tidal head); each unit's
+// complement block is read from mapped pinned memory, copied to its slot and attended to in
+// the same pass.  The number of work-groups, not their width, bounds the reads in flight.
+template <int G, int RPL>
+__device__ inline void recall_units(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, int w,
+                                    int nw)
+{
+    int total = 0;
+    for (int b = 0; b < g.B; ++b) total += s.counts[b * 2 + 1] * g.nT;
+    for (int u = w; u < total; u += nw) {
+        int b = 0, r = u;
+        while (r >= s.counts[b * 2 + 1] * g.nT) r -= s.counts[b++ * 2 + 1] * g.nT;
+        const int e = r / g.nT, ti = r - e * g.nT;
+        const int c = s.new_list[((size_t)b * g.k + e) * 2], slot = s.new_list[((size_t)b * g.k + e) * 2 + 1];
+        const size_t off = (size_t)ti * 2 * g.comp_max * D;
+        const uint16_t *src = t.host_comp + ((size_t)b * g.nc + c) * g.chunk_elems + off;
+        uint16_t *dst = t.slots + ((size_t)b * g.n_slots + slot) * g.chunk_elems + off;
+        const int nr = comp_of(g, c);
+        // rows past the chunk's complement (short last chunk) are zero padding: copied for a
+        // byte-identical slot, not attended
+        for (int j = threadIdx.x; j < (g.comp_max - nr) * 2 * (D / 8); j += NT) {
+            const int half = j / ((g.comp_max - nr) * (D / 8)), rem = j - half * (g.comp_max - nr) * (D / 8);
+            const size_t o = ((size_t)half * g.comp_max + nr) * D + (size_t)rem * 8;
+            *(uint4 *)(dst + o) = *(const uint4 *)(src + o);
+        }
+        const int lk = t.tidal_lk[ti], l = lk / g.Hkv, kv = lk - l * g.Hkv;
+        const uint16_t *qh = q + (((size_t)b * g.L + l) * g.Hq + (size_t)kv * G) * D;
+        const size_t p = ((size_t)b * (g.nT + g.nF) + ti) * g.np + g.n_tiles_s + g.ng_kept + e;
+        const RecallRows map{src, dst, nr, g.comp_max};
+        subset_tile<G, RPL>(qh, map, s.ps_m + p * G, s.ps_l + p * G, s.ps_o + p * G * D);
+    }
+}
+
+// Fixed heads, tidal kept rows, tidal complements resident since the last step, and (first
+// n_recall work-groups) recall + attention of the complements that became resident this step.
+// One launch: the recall work-groups hold the host link busy while the others stream HBM.
+template <int G, int RPLK, int RPLN>
+__global__ __launch_bounds__(NT) void tidal_fixed_kernel(Geometry g, Tiers t, StepBuffers s, const uint16_t *__restrict__ q,
+                                                         int n_recall)
+{
+    int bid = blockIdx.x;
+    if (bid < n_recall) {
+        recall_units<G, RPLN>(g, t, s, q, bid, n_recall);
+        return;
+    }
+    bid -= n_recall;
+    const int nh = g.nT + g.nF, n_static = g.n_tiles_s * nh * g.B;
+    if (bid < n_static) {
+        const int tile = bid % g.n_tiles_s, rest = bid / g.n_tiles_s;
+        static_tile<G>(g, t, s, q, tile, rest % nh, rest / nh);
+        return;
+    }
+    bid -= n_static;
+    const int grp = bid % g.ng_kept, rest = bid / g.ng_kept;
+    slot_group<G, RPLK>(g, t, s, q, grp, rest % g.nT, rest / g.nT, 0, g.sg);
+}
+
+// Complements copied by hipMemcpyAsync (host-waited recall path): one entry per work-group.
+template <int G, int RPL>
+__global__ __launch_bounds__(NT) void new_slots_kernel(Geometry g, Tiers t, StepBuffers s, const uint16_t *__restrict__ q)
+{
+    slot_group<G, RPL>(g, t, s, q, blockIdx.x, blockIdx.y, blockIdx.z, 1, 1);
+}
+
+// Merge of one tidal/fixed KV-head's partials (static tiles, kept groups, new groups):
+// COMBINE_THREADS threads; the partials of every output column are split over groups of
+// threads and summed in a fixed order.
 template <int G>
-__global__ __launch_bounds__(NT) void subset_combine_kernel(Geometry g, Tiers t, StepBuffers s, float *out)
+__global__ __launch_bounds__(COMBINE_THREADS) void subset_combine_kernel(Geometry g, Tiers t, StepBuffers s, float *out)
 {
     const int hi = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
     const bool tidal = hi < g.nT;
     extern __shared__ float sfac[];      // [np][G]
-    __shared__ float Mh[G], Lh[G];
+    constexpr int NW = COMBINE_THREADS / 64;
+    constexpr int OG = COMBINE_THREADS / (G * D) > 0 ? COMBINE_THREADS / (G * D) : 1;   // groups per output
+    __shared__ float red[NW * G];
+    __shared__ float Linv[G];
+    __shared__ float opart[OG > 1 ? OG : 1][G * D > COMBINE_THREADS ? 1 : G * D];
     const int nk = tidal ? min((s.counts[b * 2] + g.sg - 1) / g.sg, g.ng_kept) : 0;
-    const int nn = tidal ? min((s.counts[b * 2 + 1] + g.sg - 1) / g.sg, g.ng_new) : 0;
+    // one partial per new entry; none exist when complements are empty (100 % budget)
+    const int nn = tidal ? min(s.counts[b * 2 + 1], g.np - g.n_tiles_s - g.ng_kept) : 0;
     const int nvalid = g.n_tiles_s + nk + nn;
-    // valid partial j -> its slot in the per-head partial array
-    auto slot_of_valid = [&](int j) {
+    auto part = [&](int j) {
         if (j < g.n_tiles_s) return j;
         j -= g.n_tiles_s;
         if (j < nk) return g.n_tiles_s + j;
         return g.n_tiles_s + g.ng_kept + (j - nk);
     };
     const size_t base = ((size_t)b * (g.nT + g.nF) + hi) * g.np;
-    if (tid < G) {
-        float M = -INFINITY;
-        for (int j = 0; j < nvalid; ++j) M = fmaxf(M, s.ps_m[(base + slot_of_valid(j)) * G + tid]);
-        float L = 0.f;
-        if (M > -INFINITY)
-            for (int j = 0; j < nvalid; ++j) {
-                const float mj = s.ps_m[(base + slot_of_valid(j)) * G + tid];
-                if (mj > -INFINITY) L += s.ps_l[(base + slot_of_valid(j)) * G + tid] * __expf(mj - M);
-            }
-        Mh[tid] = M;
-        Lh[tid] = L;
+    const int lane = tid & 63, wave = tid >> 6;
+    float mloc[G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) mloc[h] = -INFINITY;
+    for (int j = tid; j < nvalid; j += COMBINE_THREADS)
+#pragma unroll
+        for (int h = 0; h < G; ++h) mloc[h] = fmaxf(mloc[h], s.ps_m[(base + part(j)) * G + h]);
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+        mloc[h] = wave_max(mloc[h]);
+        if (lane == 0) red[wave * G + h] = mloc[h];
     }
     __syncthreads();
-    for (int idx = tid; idx < nvalid * G; idx += NT) {
-        const int j = idx / G, h = idx - j * G;
-        const float mj = s.ps_m[(base + slot_of_valid(j)) * G + h];
-        sfac[idx] = (Lh[h] > 0.f && mj > -INFINITY) ? __expf(mj - Mh[h]) / Lh[h] : 0.f;
+    float M[G], lsum[G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+        M[h] = red[h];
+        for (int w = 1; w < NW; ++w) M[h] = fmaxf(M[h], red[w * G + h]);
+        lsum[h] = 0.f;
+    }
+    __syncthreads();
+    for (int j = tid; j < nvalid; j += COMBINE_THREADS)
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+            const float mj = s.ps_m[(base + part(j)) * G + h];
+            const float f = (M[h] > -INFINITY && mj > -INFINITY) ? __expf(mj - M[h]) : 0.f;
+            sfac[j * G + h] = f;
+            lsum[h] += s.ps_l[(base + part(j)) * G + h] * f;
+        }
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+        lsum[h] = wave_sum(lsum[h]);
+        if (lane == 0) red[wave * G + h] = lsum[h];
+    }
+    __syncthreads();
+    if (tid < G) {
+        float L = red[tid];
+        for (int w = 1; w < NW; ++w) L += red[w * G + tid];
+        Linv[tid] = L > 0.f ? 1.f / L : 0.f;
     }
     __syncthreads();
     const int lk = tidal ? t.tidal_lk[hi] : t.fixed_lk[hi - g.nT], l = lk / g.Hkv, kv = lk - l * g.Hkv;
     float *oh = out + (((size_t)b * g.L + l) * g.Hq + (size_t)kv * G) * D;
-    for (int idx = tid; idx < G * D; idx += NT) {
-        const int h = idx / D;
+    if constexpr (OG > 1) {
+        // threads beyond OG * G * D (when G * D does not divide the block) only join the barrier
+        const int idx = tid % (G * D), grp = tid / (G * D), h = idx / D;
+        const bool act = grp < OG;
         float acc = 0.f;
-        for (int j = 0; j < nvalid; ++j) acc += s.ps_o[(base + slot_of_valid(j)) * G * D + idx] * sfac[j * G + h];
-        oh[idx] = acc;
+        if (act) {
+            const int j0 = grp * nvalid / OG, j1 = (grp + 1) * nvalid / OG;
+#pragma unroll 8
+            for (int j = j0; j < j1; ++j) acc += s.ps_o[(base + part(j)) * G * D + idx] * sfac[j * G + h];
+            opart[grp][idx] = acc;
+        }
+        __syncthreads();
+        if (grp == 0) {
+#pragma unroll
+            for (int q2 = 1; q2 < OG; ++q2) acc += opart[q2][idx];
+            oh[idx] = acc * Linv[h];
+        }
+    } else {
+        for (int idx = tid; idx < G * D; idx += COMBINE_THREADS) {
+            const int h = idx / D;
+            float acc = 0.f;
+#pragma unroll 8
+            for (int j = 0; j < nvalid; ++j) acc += s.ps_o[(base + part(j)) * G * D + idx] * sfac[j * G + h];
+            oh[idx] = acc * Linv[h];
+        }
     }
 }
 
@@ -731,28 +1008,37 @@ struct AnchorCombineL {
     static hipError_t run(const Geometry &g, const Tiers &t, const StepBuffers &s, float *out, hipStream_t st)
     {
         if (g.nA == 0) return hipSuccess;
-        const size_t shm = (size_t)(g.n_tiles_a ? g.n_tiles_a : 1) * G * sizeof(double);
-        hipLaunchKernelGGL(anchor_combine_kernel<G>, dim3(g.nA, g.B), dim3(NT), shm, st, g, t, s, out);
+        const size_t shm = (size_t)g.n_tiles_a * sizeof(double);
+        hipLaunchKernelGGL(anchor_combine_kernel<G>, dim3(g.nA, G, g.B), dim3(COMBINE_THREADS), shm, st, g, t, s, out);
         return hipGetLastError();
     }
 };
 template <int G>
-struct StaticL {
-    static hipError_t run(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st)
-    {
-        if (g.nT + g.nF == 0 || g.n_tiles_s == 0) return hipSuccess;
-        hipLaunchKernelGGL(subset_static_kernel<G>, dim3(g.n_tiles_s, g.nT + g.nF, g.B), dim3(NT), 0, st, g, t, s, q);
-        return hipGetLastError();
-    }
-};
-template <int G>
-struct SlotsL {
-    static hipError_t run(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, bool nl,
+struct TidalFixedL {
+    static hipError_t run(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, bool recall,
                           hipStream_t st)
     {
-        const int ng = nl ? g.ng_new : g.ng_kept;
-        if (g.nT == 0 || ng == 0) return hipSuccess;
-        hipLaunchKernelGGL(subset_slots_kernel<G>, dim3(ng, g.nT, g.B), dim3(NT), 0, st, g, t, s, q, nl ? 1 : 0);
+        const int n_recall = (recall && g.k > 0 && g.chunk_elems > 0 && g.nT > 0) ? RECALL_WGS : 0;
+        const long long n = n_recall + (long long)g.n_tiles_s * (g.nT + g.nF) * g.B + (long long)g.ng_kept * g.nT * g.B;
+        if (n == 0) return hipSuccess;
+        if (g.slot_tile == TILE_S)
+            hipLaunchKernelGGL((tidal_fixed_kernel<G, TILE_S / 16, TILE_S / 16>), dim3((unsigned)n), dim3(NT), 0, st, g, t,
+                               s, q, n_recall);
+        else
+            hipLaunchKernelGGL((tidal_fixed_kernel<G, TILE_S / 8, TILE_S / 8>), dim3((unsigned)n), dim3(NT), 0, st, g, t,
+                               s, q, n_recall);
+        return hipGetLastError();
+    }
+};
+template <int G>
+struct NewSlotsL {
+    static hipError_t run(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st)
+    {
+        if (g.nT == 0 || g.k == 0 || g.comp_max == 0) return hipSuccess;
+        if (g.slot_tile == TILE_S)
+            hipLaunchKernelGGL((new_slots_kernel<G, TILE_S / 16>), dim3(g.k, g.nT, g.B), dim3(NT), 0, st, g, t, s, q);
+        else
+            hipLaunchKernelGGL((new_slots_kernel<G, TILE_S / 8>), dim3(g.k, g.nT, g.B), dim3(NT), 0, st, g, t, s, q);
         return hipGetLastError();
     }
 };
@@ -762,7 +1048,7 @@ struct CombineL {
     {
         if (g.nT + g.nF == 0) return hipSuccess;
         const size_t shm = (size_t)(g.np ? g.np : 1) * G * sizeof(float);
-        hipLaunchKernelGGL(subset_combine_kernel<G>, dim3(g.nT + g.nF, g.B), dim3(NT), shm, st, g, t, s, out);
+        hipLaunchKernelGGL(subset_combine_kernel<G>, dim3(g.nT + g.nF, g.B), dim3(COMBINE_THREADS), shm, st, g, t, s, out);
         return hipGetLastError();
     }
 };
@@ -779,39 +1065,23 @@ hipError_t launch_anchor_combine(const Geometry &g, const Tiers &t, const StepBu
     return dispatch_g<AnchorCombineL>(g.G, g, t, s, out, st);
 }
 
-hipError_t launch_scores(const Geometry &g, const StepBuffers &s, float *scores, hipStream_t st)
-{
-    const int n = g.B * g.nc;
-    if (n == 0) return hipSuccess;
-    hipLaunchKernelGGL(scores_kernel, dim3((n + 255) / 256), dim3(256), 0, st, g, s, scores);
-    return hipGetLastError();
-}
-
-hipError_t launch_select(const Geometry &g, const StepBuffers &s, const float *scores, const int32_t *ovr,
+hipError_t launch_select(const Geometry &g, const StepBuffers &s, float *scores, const int32_t *ovr,
                          int32_t *selected, hipStream_t st)
 {
     if (g.nc == 0) return hipSuccess;
-    const size_t shm = (size_t)(5 * g.nc + 2 * g.n_slots) * sizeof(int);
-    hipLaunchKernelGGL(select_kernel, dim3(g.B), dim3(SEL_THREADS), shm, st, g, s, scores, ovr, selected);
+    hipLaunchKernelGGL(select_kernel, dim3(g.B), dim3(SEL_THREADS), select_shared_bytes(g), st, g, s, scores, ovr, selected);
     return hipGetLastError();
 }
 
-hipError_t launch_recall(const Geometry &g, const Tiers &t, const StepBuffers &s, hipStream_t st)
+hipError_t launch_tidal_fixed(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, bool recall,
+                              hipStream_t st)
 {
-    if (g.k == 0 || g.chunk_elems == 0 || g.nT == 0) return hipSuccess;
-    hipLaunchKernelGGL(recall_kernel, dim3(16, g.k, g.B), dim3(256), 0, st, g, t, s);
-    return hipGetLastError();
+    return dispatch_g<TidalFixedL>(g.G, g, t, s, q, recall, st);
 }
 
-hipError_t launch_subset_static(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st)
+hipError_t launch_new_slots(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st)
 {
-    return dispatch_g<StaticL>(g.G, g, t, s, q, st);
-}
-
-hipError_t launch_subset_slots(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, bool new_list,
-                               hipStream_t st)
-{
-    return dispatch_g<SlotsL>(g.G, g, t, s, q, new_list, st);
+    return dispatch_g<NewSlotsL>(g.G, g, t, s, q, st);
 }
 
 hipError_t launch_subset_combine(const Geometry &g, const Tiers &t, const StepBuffers &s, float *out, hipStream_t st)

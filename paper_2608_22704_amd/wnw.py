@@ -30,13 +30,14 @@ class wnw_config(C.Structure):
 
 
 class wnw_stats(C.Structure):
-    _fields_ = [("steps", C.c_int64), ("recalled_chunks", C.c_int64), ("recalled_bytes", C.c_int64),
+    _fields_ = [("steps", C.c_int64), ("recalled_chunks", C.c_int64), ("revived_chunks", C.c_int64),
+                ("recalled_bytes", C.c_int64),
                 ("dropped_chunks", C.c_int64), ("resident_chunks", C.c_int64), ("peak_resident", C.c_int32),
                 ("n_slots", C.c_int32), ("r_gpu", C.c_double), ("r_gpu_cpu", C.c_double),
                 ("anchor_bytes", C.c_int64), ("static_bytes", C.c_int64), ("slot_rows", C.c_int64),
                 ("timed_steps", C.c_int64), ("t_anchor_ms", C.c_double), ("t_select_ms", C.c_double),
-                ("t_static_ms", C.c_double), ("t_kept_ms", C.c_double), ("t_recall_ms", C.c_double),
-                ("t_new_ms", C.c_double), ("t_combine_ms", C.c_double), ("t_step_ms", C.c_double)]
+                ("t_tidal_fixed_ms", C.c_double), ("t_new_ms", C.c_double), ("t_combine_ms", C.c_double),
+                ("t_step_ms", C.c_double), ("t_recall_ms", C.c_double)]
 
     def as_dict(self) -> dict:
         return {name: getattr(self, name) for name, _ in self._fields_}

@@ -150,4 +150,4 @@ class Lockstep:
             self.max_err = max(self.max_err, float(err))
             assert err <= OUT_TOL, f"step {s} seq {b}: output max abs err {err:.4g}"
         self.step_i += 1
-        return out, sc, sel, r
+        return out, sc, sel, res
