@@ -40,6 +40,8 @@ def main():
     ap.add_argument("--recall", choices=("kernel", "memcpy"), default="kernel")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU oracle sample (0 = skip)")
     ap.add_argument("--no-timing", action="store_true", help="no per-kernel events (for profiler runs)")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="first run a plain 256 MiB device copy (the reference for hardware byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: --gpus {args.gpus} is not supported by this build "
@@ -84,6 +86,13 @@ def main():
     sel = torch.empty((B, max(geo["k"], 1)), dtype=torch.int32, device="cuda")
     log(f"[bench] set-up done: {geo}")
 
+    if args.calibrate_copy:
+        src = torch.ones(128 << 20, dtype=torch.int16, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     for s in range(args.warmup):
         W.wnw_decode_step(ctx, qd[s % S], out, sc, sel, stream)
     torch.cuda.synchronize()
@@ -166,7 +175,8 @@ def main():
         res["kernels"] = kern
         a = kern["anchor_attn"]
         res["roofline"] = {"bound": "hbm", "kernel": "anchor_attn", "achieved": a["GBps"], "peak": PEAK_HBM_GBPS,
-                           "unit": "GB/s", "frac": a["GBps"] / PEAK_HBM_GBPS, "traffic": None}
+                           "unit": "GB/s", "frac": a["GBps"] / PEAK_HBM_GBPS,
+                           "traffic": measured_traffic("anchor_attn", w.name)}
     res["recall"] = rec
     res["r_gpu"] = st1["r_gpu"]
     res["r_gpu_cpu"] = st1["r_gpu_cpu"]
@@ -174,6 +184,31 @@ def main():
     if args.cpu_seconds > 0:
         res["cpu_baseline"] = cpu_baseline(w, roles, prefill, args.cpu_seconds)
     print(json.dumps(res), flush=True)
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter summary
+    (FETCH_SIZE + WRITE_SIZE per dispatch, each scaled by what the counter reads for a plain
+    copy of known size), or None when there is no summary or the kernel source has changed
+    since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_pmc.txt")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            vals[k.strip()] = v.strip()
+    src = os.path.join(ROOT, "paper_2608_22704_amd", "csrc", "wnw_kernels.hip")
+    if vals.get("kernels_source_sha256") != hashlib.sha256(open(src, "rb").read()).hexdigest():
+        return None
+    try:
+        fetch = float(vals["fetch_kib_per_dispatch"]) * 1024 / float(vals["fetch_copy_factor"])
+        write = float(vals["write_kib_per_dispatch"]) * 1024 / float(vals["write_copy_factor"])
+    except (KeyError, ValueError, ZeroDivisionError):
+        return None
+    return fetch + write
 
 
 def cpu_baseline(w, roles, prefill, budget_s):
