@@ -125,15 +125,32 @@ __device__ inline void block_sum(T v[G], T *red)
 
 // -------------------------------------------------------------------------------------------
 // Anchor attention + chunk mass (double logits)
+//
+// Logits come from v_mfma_f64_4x4x4f64 (four independent 4x4x4 blocks per wavefront).  On
+// gfx950 lane l = 16k + 4*blk + x holds A_blk[x][k] and B_blk[k][x], and the result
+// D_blk[i][j] lands in lane 16i + 4*blk + j.  With A = key rows and B = q^T, one instruction
+// multiplies 16 keys (4 per block) by 4 q-heads over 4 dimensions.  The dimension index is
+// permuted consistently on both operands: lane l feeds dimension 32k + t to instruction t, so it
+// reads 64 contiguous bytes of its key row; 32 instructions cover d = 128.  For groups of 6 or 8
+// q-heads, blocks 0-1 take heads 0-3 and blocks 2-3 heads 4-7 over the same 8 keys.  Products of
+// bf16 values are exact in double, so the logits match a double reference to rounding.
+//
+// Each wavefront owns 32 rows of the tile and runs its own softmax on them straight from the
+// instruction's result layout (one (key, head) logit per lane, so every exp is computed once);
+// P.V needs only the wavefront's own probabilities.  The four wavefronts meet once, to merge.
 // -------------------------------------------------------------------------------------------
-constexpr int RPL_A = TILE_A / (4 * WAVES);   // 4-row steps per wavefront (8)
-
 template <int G>
 __global__ __launch_bounds__(NT) void anchor_attn_kernel(Geometry g, Tiers t, StepBuffers s,
                                                          const uint16_t *__restrict__ q)
 {
+    constexpr int HG = G <= 4 ? 1 : 2;        // groups of 4 q-heads per instruction
+    constexpr int KG = 16 / HG;               // keys per instruction
+    constexpr int RW = TILE_A / WAVES;        // key rows per wavefront (32)
+    constexpr int NKG = RW / KG;              // key groups per wavefront
+    constexpr int RPL = RW / 4;               // 4-row steps per wavefront in the P.V layout
     const int tile = blockIdx.x, ai = blockIdx.y, b = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, sub = lane & 15, rg = lane >> 4;
+    const int kq = lane >> 4, blk = (lane >> 2) & 3, x4 = lane & 3;
     const int lk = t.anchor_lk[ai], l = lk / g.Hkv, kv = lk - l * g.Hkv;
     const size_t hrow = ((size_t)b * g.nA + ai) * (size_t)g.T;
     const uint16_t *__restrict__ K = t.aK + hrow * D;
@@ -141,78 +158,142 @@ __global__ __launch_bounds__(NT) void anchor_attn_kernel(Geometry g, Tiers t, St
     const uint16_t *__restrict__ qh = q + (((size_t)b * g.L + l) * g.Hq + (size_t)kv * G) * D;
     const int t0 = tile * TILE_A;
 
-    __shared__ double xs[G * TILE_A];    // logits, then probabilities relative to the tile max
-    __shared__ float wo[WAVES * G * D];  // per-wavefront P.V partials
-    __shared__ double red[WAVES * G];
+    __shared__ double xs[G * TILE_A];    // probabilities relative to their wavefront's maximum
+    __shared__ float xf[G * TILE_A];     // the same in fp32, for P.V
+    __shared__ float wo[WAVES * 4 * G * D];   // P.V partials per (wavefront, 4-row group)
+    __shared__ double wm[WAVES * G], wl[WAVES * G];
+    __shared__ double wf[WAVES * G];     // merge factors exp(m_w - M)
 
-    // q first, then every K and V load of this wavefront (loads return in issue order)
-    uint4 qr[G];
+    // q (B operand: head hB, dims 32kq..32kq+31), then the key rows (A operand), then V rows
+    const int hB = (HG == 1 ? 0 : (blk >> 1) * 4) + x4;
+    uint4 qr[4];
 #pragma unroll
-    for (int h = 0; h < G; ++h) qr[h] = *(const uint4 *)(qh + h * D + sub * 8);
-    uint4 kr[RPL_A], vr[RPL_A];
+    for (int u = 0; u < 4; ++u)
+        qr[u] = hB < G ? *(const uint4 *)(qh + hB * D + kq * 32 + u * 8) : make_uint4(0, 0, 0, 0);
+    const int keyA = (HG == 1 ? blk * 4 : (blk & 1) * 4) + x4;
+    uint4 kr[NKG][4];
 #pragma unroll
-    for (int i = 0; i < RPL_A; ++i) {
-        const int row = t0 + wave * 4 * RPL_A + i * 4 + rg;
-        kr[i] = row < g.T ? *(const uint4 *)(K + (size_t)row * D + sub * 8) : make_uint4(0, 0, 0, 0);
+    for (int kg = 0; kg < NKG; ++kg) {
+        const int row = t0 + wave * RW + kg * KG + keyA;
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            kr[kg][u] = row < g.T ? *(const uint4 *)(K + (size_t)row * D + kq * 32 + u * 8) : make_uint4(0, 0, 0, 0);
     }
+    uint4 vr[RPL];
 #pragma unroll
-    for (int i = 0; i < RPL_A; ++i) {
-        const int row = t0 + wave * 4 * RPL_A + i * 4 + rg;
+    for (int i = 0; i < RPL; ++i) {
+        const int row = t0 + wave * RW + i * 4 + rg;
         vr[i] = row < g.T ? *(const uint4 *)(V + (size_t)row * D + sub * 8) : make_uint4(0, 0, 0, 0);
     }
-    double qd[G][8];
+
+    // logits of (key keyD, head hD) per key group
+    const int keyD = (HG == 1 ? blk * 4 : (blk & 1) * 4) + kq;
+    const int hD = (HG == 1 ? 0 : (blk >> 1) * 4) + x4;
+    double xv[NKG];
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-        float f[8];
-        unpack8(qr[h], f);
+    for (int kg = 0; kg < NKG; ++kg) {
+        double acc0 = 0.0, acc1 = 0.0;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) qd[h][e] = (double)f[e];
+        for (int u = 0; u < 4; ++u) {
+            float f[8], qf[8];
+            unpack8(kr[kg][u], f);
+            unpack8(qr[u], qf);
+#pragma unroll
+            for (int e = 0; e < 8; e += 2) {
+                acc0 = __builtin_amdgcn_mfma_f64_4x4x4f64((double)f[e], (double)qf[e], acc0, 0, 0, 0);
+                acc1 = __builtin_amdgcn_mfma_f64_4x4x4f64((double)f[e + 1], (double)qf[e + 1], acc1, 0, 0, 0);
+            }
+        }
+        const int rr = wave * RW + kg * KG + keyD;
+        xv[kg] = (hD < G && t0 + rr < g.T) ? (acc0 + acc1) * SCALE_D : -INFINITY;
     }
-    // x = q.k / sqrt(d): exact bf16 products, double accumulation
+    // wavefront softmax per head: the lanes of one head differ in bits 2, 4, 5 (and 3 when
+    // all four blocks share the heads)
+    double m = xv[0];
 #pragma unroll
-    for (int i = 0; i < RPL_A; ++i) {
-        const int r = wave * 4 * RPL_A + i * 4 + rg;
+    for (int kg = 1; kg < NKG; ++kg) m = fmax(m, xv[kg]);
+    m = fmax(m, __shfl_xor(m, 4));
+    if (HG == 1) m = fmax(m, __shfl_xor(m, 8));
+    m = fmax(m, __shfl_xor(m, 16));
+    m = fmax(m, __shfl_xor(m, 32));
+    double lsum = 0.0;
+#pragma unroll
+    for (int kg = 0; kg < NKG; ++kg) {
+        const double pv = (m == -INFINITY || xv[kg] == -INFINITY) ? 0.0 : exp(xv[kg] - m);
+        if (hD < G) {
+            xs[hD * TILE_A + wave * RW + kg * KG + keyD] = pv;
+            xf[hD * TILE_A + wave * RW + kg * KG + keyD] = (float)pv;
+        }
+        lsum += pv;
+    }
+    lsum += __shfl_xor(lsum, 4);
+    if (HG == 1) lsum += __shfl_xor(lsum, 8);
+    lsum += __shfl_xor(lsum, 16);
+    lsum += __shfl_xor(lsum, 32);
+    if (hD < G && kq == 0 && (HG == 1 ? blk == 0 : (blk & 1) == 0)) {
+        wm[wave * G + hD] = m;
+        wl[wave * G + hD] = lsum;
+    }
+    // the wavefront reads back only its own probabilities: a wavefront-scope fence suffices
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+    // unnormalised P.V in fp32, relative to the wavefront maximum
+    float acc[G][8];
+#pragma unroll
+    for (int h = 0; h < G; ++h)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
+#pragma unroll
+    for (int i = 0; i < RPL; ++i) {
+        const int rr = wave * RW + i * 4 + rg;
         float f[8];
-        unpack8(kr[i], f);
-        double acc[G];
+        unpack8(vr[i], f);
 #pragma unroll
         for (int h = 0; h < G; ++h) {
-            acc[h] = 0.0;
+            const float ph = xf[h * TILE_A + rr];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) acc[h] = fma(qd[h][e], (double)f[e], acc[h]);
-            acc[h] = sum16(acc[h]);
+            for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(ph, f[e], acc[h][e]);
         }
-        if (sub == 0) {
-            const bool ok = t0 + r < g.T;
+    }
 #pragma unroll
-            for (int h = 0; h < G; ++h) xs[h * TILE_A + r] = ok ? acc[h] * SCALE_D : -INFINITY;
-        }
+    for (int h = 0; h < G; ++h) {
+        float4 *dst = (float4 *)(wo + ((wave * 4 + rg) * G + h) * D + sub * 8);
+        dst[0] = make_float4(acc[h][0], acc[h][1], acc[h][2], acc[h][3]);
+        dst[1] = make_float4(acc[h][4], acc[h][5], acc[h][6], acc[h][7]);
     }
     __syncthreads();
 
-    // tile max, probabilities relative to it (double exp), their sum
-    double m[G], p[G];
-#pragma unroll
-    for (int h = 0; h < G; ++h) m[h] = tid < TILE_A ? xs[h * TILE_A + tid] : -INFINITY;
-    block_max<G>(m, red);
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-        p[h] = 0.0;
-        if (tid < TILE_A) {
-            const double x = xs[h * TILE_A + tid];
-            p[h] = (m[h] == -INFINITY) ? 0.0 : exp(x - m[h]);
-            xs[h * TILE_A + tid] = p[h];
-        }
-    }
-    block_sum<G>(p, red);     // p[h] now holds the tile sum; also publishes xs
-
+    // merge of the four wavefronts: tile maximum, factors, sums, outputs, per-chunk masses
     const size_t pidx = ((size_t)b * g.nA + ai) * g.n_tiles_a + tile;
-    if (tid == 0) {
+    if (tid < WAVES * G) {
+        const int h = tid % G, w = tid / G;
+        double M = wm[h];
 #pragma unroll
-        for (int h = 0; h < G; ++h) {
-            s.pa_m[pidx * G + h] = m[h];
-            s.pa_l[pidx * G + h] = p[h];
+        for (int w2 = 1; w2 < WAVES; ++w2) M = fmax(M, wm[w2 * G + h]);
+        const double mw = wm[w * G + h];
+        wf[tid] = (M == -INFINITY || mw == -INFINITY) ? 0.0 : exp(mw - M);
+        if (w == 0) s.pa_m[pidx * G + h] = M;
+    }
+    __syncthreads();
+    if (tid < G) {
+        double L = 0.0;
+#pragma unroll
+        for (int w = 0; w < WAVES; ++w) L += wl[w * G + tid] * wf[w * G + tid];
+        s.pa_l[pidx * G + tid] = L;
+    }
+    for (int idx = tid; idx < G * D; idx += NT) {
+        const int h = idx / D;
+        float o = 0.f;
+#pragma unroll
+        for (int w = 0; w < WAVES; ++w) {
+            float ow = 0.f;
+#pragma unroll
+            for (int r4 = 0; r4 < 4; ++r4) ow += wo[(w * 4 + r4) * G * D + idx];
+            o += ow * (float)wf[w * G + h];
         }
+        s.pa_o[pidx * G * D + idx] = o;
     }
     // per-chunk mass of this tile (Eq. 2 restricted to the tile): 16 lanes per (head, chunk)
     // entry, each summing a fixed stride of rows, then a DPP sum (fixed order)
@@ -220,52 +301,14 @@ __global__ __launch_bounds__(NT) void anchor_attn_kernel(Geometry g, Tiers t, St
     for (int base = 0; base < G * g.maxc * 16; base += NT) {
         const int idx = base + tid, grp = idx >> 4, k = idx & 15;
         const bool valid = grp < G * g.maxc;
-        double acc = 0.0;
+        double acc2 = 0.0;
         if (valid) {
             const int h = grp / g.maxc, c = c_first + (grp - h * g.maxc);
             const int r0 = max(c * g.cl, t0), r1 = min(min((c + 1) * g.cl, t0 + TILE_A), g.Ta);
-            for (int r = r0 + k; r < r1; r += 16) acc += xs[h * TILE_A + (r - t0)];
+            for (int rr = r0 + k; rr < r1; rr += 16) acc2 += xs[h * TILE_A + (rr - t0)] * wf[((rr - t0) / RW) * G + h];
         }
-        acc = sum16(acc);
-        if (valid && k == 0) s.pa_mass[pidx * G * g.maxc + grp] = acc;
-    }
-
-    // unnormalised P.V in fp32
-    float acc[G][8];
-#pragma unroll
-    for (int h = 0; h < G; ++h)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
-#pragma unroll
-    for (int i = 0; i < RPL_A; ++i) {
-        const int r = wave * 4 * RPL_A + i * 4 + rg;
-        float f[8];
-        unpack8(vr[i], f);
-#pragma unroll
-        for (int h = 0; h < G; ++h) {
-            const float ph = (float)xs[h * TILE_A + r];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(ph, f[e], acc[h][e]);
-        }
-    }
-#pragma unroll
-    for (int h = 0; h < G; ++h)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            acc[h][e] += __shfl_xor(acc[h][e], 16);
-            acc[h][e] += __shfl_xor(acc[h][e], 32);
-        }
-    if (rg == 0)
-#pragma unroll
-        for (int h = 0; h < G; ++h)
-#pragma unroll
-            for (int e = 0; e < 8; ++e) wo[(wave * G + h) * D + sub * 8 + e] = acc[h][e];
-    __syncthreads();
-    for (int idx = tid; idx < G * D; idx += NT) {
-        float o = 0.f;
-#pragma unroll
-        for (int w = 0; w < WAVES; ++w) o += wo[w * G * D + idx];
-        s.pa_o[pidx * G * D + idx] = o;
+        acc2 = sum16(acc2);
+        if (valid && k == 0) s.pa_mass[pidx * G * g.maxc + grp] = acc2;
     }
 }
 
