@@ -248,3 +248,21 @@ def test_resident_slots_match_host_copies_over_steps():
         assert st["revived_chunks"] > 0
     finally:
         h.close()
+
+
+# ---- full-size batched and long-form workloads: every sequence runs on the GPU; the oracle
+# checks the sequences, heads and steps it can afford (sampled outputs at full size).
+
+def test_voxtral_b16_full_size_sampled():
+    """Batch 16 of the 15k-audio cache, 256 steps: per-sequence selection, residency, scores
+    and outputs of sequences 0 and 9 against the oracle at every step, sampled heads."""
+    _run(configs.VOXTRAL_10MIN_B16, head_mask_fn=_sampled(8), seqs=[0, 9])
+
+
+@pytest.mark.parametrize("w", [configs.VOXTRAL_60MIN_B4_20, configs.VOXTRAL_60MIN_B4_10],
+                         ids=["budget20", "budget10"])
+def test_voxtral_60min_b4_full_size_sampled(w):
+    """Batch 4 of 90k audio + 1k text positions, chunk 128: the first 24 of 512 steps, sequence 2
+    against the oracle with sampled heads (the oracle's anchor pass alone is ~2 G multiply-adds
+    per step per sequence)."""
+    _run(w, steps=24, head_mask_fn=_sampled(6), seqs=[2])
