@@ -38,6 +38,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=16)
     ap.add_argument("--workload", default=None, help="workload name from synth.configs (default: the 15k-audio one)")
     ap.add_argument("--recall", choices=("kernel", "memcpy"), default="kernel")
+    ap.add_argument("--timing", choices=("same", "next"), default="same",
+                    help="selection timing: the step's own selection serves its tidal heads, or the next step's")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU oracle sample (0 = skip)")
     ap.add_argument("--no-timing", action="store_true", help="no per-kernel events (for profiler runs)")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -73,7 +75,8 @@ def main():
     torch.cuda.synchronize()
     log(f"[bench] inputs resident in HBM after {time.time() - t0:.1f}s")
 
-    flags = (0 if args.no_timing else W.WNW_F_TIMING) | (W.WNW_F_RECALL_MEMCPY if args.recall == "memcpy" else 0)
+    flags = ((0 if args.no_timing else W.WNW_F_TIMING) | (W.WNW_F_RECALL_MEMCPY if args.recall == "memcpy" else 0)
+             | (W.WNW_F_SELECT_NEXT_STEP if args.timing == "next" else 0))
     cfg = W.make_config(B, L, w.q_heads, H, w.audio_len, w.text_len, w.chunk_len, w.budget_bp, flags=flags)
     stream = torch.cuda.current_stream()
     ctx = W.wnw_init_cache(cfg, kd, vd, stream)
@@ -136,7 +139,7 @@ def main():
         "config": {"workload": w.name, "batch": B, "layers": L, "q_heads": w.q_heads, "kv_heads": H,
                    "head_dim": D, "audio_len": w.audio_len, "text_len": w.text_len, "chunk_len": w.chunk_len,
                    "budget_bp": w.budget_bp, "roles": [w.n_anchor, w.n_tidal, w.n_fixed], "kv_storage": "bf16",
-                   "recall": args.recall},
+                   "recall": args.recall, "selection_timing": args.timing},
     }
     chunk_mb = geo.get("chunk_bytes", 0) / 1e6
     rec = {"copied_chunks_per_step": d["recalled_chunks"] / K / B,
@@ -162,7 +165,8 @@ def main():
             "step_gpu": {"avg_ms": d["t_step_ms"] / n},
             "step_no_recall": {"avg_ms": t2 * 1e3 / nr},
         }
-        if args.recall == "memcpy":
+        if args.recall == "memcpy" or args.timing == "next":
+            # side-stream recall (host-issued copies, or the copy kernel of next-step timing)
             rec["copy_ms"] = d["t_recall_ms"] / n
             rec["GBps"] = (d["recalled_bytes"] / n) / rec["copy_ms"] / 1e6 if rec["copy_ms"] > 0 else None
         else:

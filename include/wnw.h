@@ -64,8 +64,11 @@ typedef enum {
 typedef enum { WNW_ANCHOR = 0, WNW_TIDAL = 1, WNW_FIXED = 2 } wnw_role;
 
 enum {
-    /* Tidal heads of step s attend over the resident set left by step s-1 (the paper's timing:
-     * selection happens after the step); default is the same step. */
+    /* Tidal heads of step s attend over the resident set left by step s-1 (the paper's timing,
+     * Method, "Dynamic Chunk Selection": the selection made after a step serves the next one);
+     * default is the same step.  The chunks that become resident at step s are recalled on a
+     * side stream, overlapped with the rest of step s and the anchor attention of step s+1;
+     * a dropped chunk keeps its slot one step longer, so n_slots = (delta + 1) * k. */
     WNW_F_SELECT_NEXT_STEP = 1u,
     /* Recall with hipMemcpyAsync on a side stream after one host wait per step, instead of
      * the default: work-groups of the tidal/fixed launch read the complements from mapped
@@ -119,7 +122,8 @@ typedef struct {
     double t_new_ms;           /* WNW_F_RECALL_MEMCPY: attention over complements copied this step */
     double t_combine_ms;       /* merge of the tidal/fixed partial results                      */
     double t_step_ms;          /* whole step on the caller's stream                             */
-    double t_recall_ms;        /* WNW_F_RECALL_MEMCPY: host -> device copies on the side stream  */
+    double t_recall_ms;        /* WNW_F_RECALL_MEMCPY or WNW_F_SELECT_NEXT_STEP: recall on the
+                                  side stream                                                    */
 } wnw_stats;
 
 /* Create a context for one batch of caches.
@@ -167,14 +171,17 @@ wnw_status wnw_get_stats(wnw_ctx *ctx, wnw_stats *out);
 wnw_status wnw_set_selection_override(wnw_ctx *ctx, const int32_t *sel_dev);
 
 /* Copy the device slot holding the recalled complement of (b, chunk) to host_dst (waits for
- * the device).  Layout [n_tidal][2 (K, V)][comp_max][d] bf16; `bytes` must equal chunk_bytes.
+ * the device).  Valid for chunks resident after the last step (with WNW_F_SELECT_NEXT_STEP, also
+ * those recalled during it).  Layout [n_tidal][2 (K, V)][comp_max][d] bf16; `bytes` must equal chunk_bytes.
  * WNW_ERR_INVALID if that chunk is not resident. */
 wnw_status wnw_debug_read_slot(wnw_ctx *ctx, int32_t b, int32_t chunk, void *host_dst, size_t bytes);
 
 /* Copy the host (pinned) complement of (b, chunk) in the same layout as wnw_debug_read_slot. */
 wnw_status wnw_debug_read_host_chunk(wnw_ctx *ctx, int32_t b, int32_t chunk, void *host_dst, size_t bytes);
 
-/* Resident flags [B][n_chunks] (uint8) left by the last step (waits for the device). */
+/* Flags [B][n_chunks] (uint8) of the complements the last step's tidal heads attended: the
+ * resident set of that step, or of the step before it with WNW_F_SELECT_NEXT_STEP (waits for
+ * the device). */
 wnw_status wnw_debug_read_resident(wnw_ctx *ctx, uint8_t *host_dst);
 
 /* Message of the last failure on ctx (or of this thread when ctx is NULL).  Never NULL. */

@@ -7,6 +7,7 @@
 //   tidal tier    [B][nT][Rs][d]      kept audio rows (ascending) + text rows, Rs = keep + T_t
 //   fixed tier    [B][nF][Rs][d]      same for fixed heads (their complement is dropped)
 //   slots         [B][n_slots][nT][2][comp_max][d]   recalled complements, n_slots = delta * k
+//                 (delta + 1) * k with next-step timing
 //   host complement (pinned) [B][n_chunks][nT][2][comp_max][d]: chunk-major, so the complement
 //                 of one chunk for every tidal head of a sequence is one contiguous block.
 // A decode step is a fixed sequence of kernels on the caller's stream; recall runs on a side
@@ -64,6 +65,7 @@ struct wnw_ctx {
 
     hipStream_t side = nullptr;
     hipEvent_t ev_sel = nullptr, ev_rec = nullptr;
+    bool rec_pending = false;          // next-step timing: a recall issued on `side` not yet joined
     int32_t *h_newinfo = nullptr;      // pinned: counts [B][2] then new lists [B][k][2]
 
     std::vector<StepEvents> pending, spare;
@@ -142,8 +144,6 @@ wnw_status derive(wnw_ctx *c, const wnw_config &cfg, Geometry &g)
     if (G != 1 && G != 2 && G != 3 && G != 4 && G != 6 && G != 8)
         return fail(c, WNW_ERR_UNSUPPORTED, "GQA group %d: implemented for 1, 2, 3, 4, 6, 8", G);
     if (cfg.chunk_len > MAX_CHUNK) return fail(c, WNW_ERR_UNSUPPORTED, "chunk_len %d > %d", cfg.chunk_len, MAX_CHUNK);
-    if (cfg.flags & WNW_F_SELECT_NEXT_STEP)
-        return fail(c, WNW_ERR_UNSUPPORTED, "next-step selection timing is not implemented in this build");
 
     g = Geometry{};
     g.B = cfg.batch;
@@ -160,6 +160,7 @@ wnw_status derive(wnw_ctx *c, const wnw_config &cfg, Geometry &g)
     g.k = cfg.top_k ? cfg.top_k : (int)(((int64_t)cfg.budget_bp * g.Ta) / (10000LL * g.cl));
     if (g.k > g.nc) return fail(c, WNW_ERR_INVALID, "top_k %d exceeds the %d chunks", g.k, g.nc);
     g.delta = cfg.evict_lag ? cfg.evict_lag : 3;
+    g.next_step = (cfg.flags & WNW_F_SELECT_NEXT_STEP) ? 1 : 0;
     g.keep_total = 0;
     g.comp_max = 0;
     for (int ch = 0; ch < g.nc; ++ch) {
@@ -168,8 +169,11 @@ wnw_status derive(wnw_ctx *c, const wnw_config &cfg, Geometry &g)
         g.comp_max = std::max(g.comp_max, comp_of(g, ch));
     }
     g.Rs = g.keep_total + g.Tt;
-    if ((int64_t)g.delta * g.k > 4096) return fail(c, WNW_ERR_UNSUPPORTED, "delta * k = %lld slots > 4096", (long long)g.delta * g.k);
-    g.n_slots = g.delta * g.k;
+    // Slots: the resident set holds at most delta * k chunks.  With next-step timing the chunks
+    // dropped at a step keep their slots until that step's attention has read them: k more.
+    const int64_t ns = ((int64_t)g.delta + g.next_step) * g.k;
+    if (ns > 4096) return fail(c, WNW_ERR_UNSUPPORTED, "%lld recall slots > 4096", (long long)ns);
+    g.n_slots = (int)ns;
     if (select_shared_bytes(g) > 150 * 1024)
         return fail(c, WNW_ERR_UNSUPPORTED, "%d chunks with %d slots exceed the selection kernel's shared memory", g.nc,
                     g.n_slots);
@@ -179,7 +183,8 @@ wnw_status derive(wnw_ctx *c, const wnw_config &cfg, Geometry &g)
     g.n_tiles_s = (g.Rs + TILE_S - 1) / TILE_S;
     g.slot_tile = g.comp_max <= TILE_S ? TILE_S : 2 * TILE_S;
     g.sg = g.comp_max > 0 ? g.slot_tile / g.comp_max : 1;
-    g.ng_kept = g.comp_max > 0 ? (g.n_slots + g.sg - 1) / g.sg : 0;
+    // the kept list holds at most delta * k entries in both timings
+    g.ng_kept = g.comp_max > 0 ? (g.delta * g.k + g.sg - 1) / g.sg : 0;
     g.np = g.n_tiles_s + g.ng_kept + (g.comp_max > 0 ? g.k : 0);
     if ((int64_t)g.np * G * 4 > 65536) return fail(c, WNW_ERR_UNSUPPORTED, "too many partial tiles per head");
     if (g.B > 65535 || (int64_t)g.L * g.Hkv > 65535) return fail(c, WNW_ERR_UNSUPPORTED, "batch or head count too large");
@@ -219,6 +224,32 @@ void parallel_for(int n, const std::function<void(int)> &fn)
     for (auto &x : th) x.join();
 }
 
+// Host-issued recall: one hipMemcpyAsync per run of consecutive chunks landing in consecutive
+// slots, from the counts and new lists staged in h_newinfo (already complete on the host).
+wnw_status issue_copies(wnw_ctx *c, hipStream_t st)
+{
+    const Geometry &g = c->g;
+    const int32_t *cnt = c->h_newinfo, *nl = c->h_newinfo + g.B * 2;
+    const size_t cb = (size_t)g.chunk_elems * sizeof(uint16_t);
+    for (int b = 0; b < g.B && cb; ++b) {
+        const int n = cnt[b * 2 + 1];
+        for (int i = 0; i < n;) {
+            int j = i + 1;
+            const int32_t *e0 = nl + ((size_t)b * g.k + i) * 2;
+            while (j < n) {
+                const int32_t *ej = nl + ((size_t)b * g.k + j) * 2;
+                if (ej[0] != e0[0] + (j - i) || ej[1] != e0[1] + (j - i)) break;
+                ++j;
+            }
+            HIPCHECK(c, hipMemcpyAsync(c->slots + ((size_t)b * g.n_slots + e0[1]) * g.chunk_elems,
+                                       c->host_comp + ((size_t)b * g.nc + e0[0]) * g.chunk_elems, cb * (j - i),
+                                       hipMemcpyHostToDevice, st));
+            i = j;
+        }
+    }
+    return WNW_OK;
+}
+
 wnw_status harvest_timing(wnw_ctx *c)
 {
     const bool memcpy_path = c->cfg.flags & WNW_F_RECALL_MEMCPY;
@@ -231,7 +262,7 @@ wnw_status harvest_timing(wnw_ctx *c)
             HIPCHECK(c, hipEventElapsedTime(&ms, ev.e[from[i]], ev.e[to[i]]));
             c->t_acc[i] += ms;
         }
-        if (memcpy_path) {
+        if (memcpy_path || c->g.next_step) {
             HIPCHECK(c, hipEventSynchronize(ev.r[1]));
             HIPCHECK(c, hipEventElapsedTime(&ms, ev.r[0], ev.r[1]));
             c->t_acc[6] += ms;
@@ -247,7 +278,7 @@ void free_all(wnw_ctx *c)
 {
     void *ptrs[] = {c->aK, c->aV, c->tK, c->tV, c->fK, c->fV, c->slots, c->d_lk, c->scores_int, c->sel_int,
                     c->s.pa_m, c->s.pa_l, c->s.pa_o, c->s.pa_mass, c->s.mass, c->s.ps_m, c->s.ps_l, c->s.ps_o,
-                    c->s.streak, c->s.slot_of, c->s.slot_last, c->s.slot_data, c->s.slot_busy, c->s.slot_since,
+                    c->s.streak, c->s.slot_of, c->s.slot_last, c->s.att, c->s.slot_data, c->s.slot_busy, c->s.slot_since,
                     c->s.step, c->s.kept_list, c->s.new_list, c->s.counts, c->s.stats};
     for (void *p : ptrs)
         if (p) (void)hipFree(p);
@@ -340,6 +371,7 @@ wnw_status wnw_set_roles(wnw_ctx *c, const uint8_t *roles, const float *prefill)
     ALLOC(s.streak, B * g.nc, "streaks");
     ALLOC(s.slot_of, B * g.nc, "slot map");
     ALLOC(s.slot_last, B * g.nc, "slot history");
+    ALLOC(s.att, B * g.nc, "attended complements");
     ALLOC(s.slot_data, B * g.n_slots, "slot contents");
     ALLOC(s.slot_busy, B * g.n_slots, "slot owners");
     ALLOC(s.slot_since, B * g.n_slots, "slot ages");
@@ -462,6 +494,7 @@ wnw_status wnw_set_roles(wnw_ctx *c, const uint8_t *roles, const float *prefill)
     if (!init.empty()) HIPCHECK(c, hipMemcpy(s.streak, init.data(), init.size() * sizeof(int32_t), hipMemcpyHostToDevice));
     if (g.nc) HIPCHECK(c, hipMemset(s.slot_of, 0xff, B * g.nc * sizeof(int32_t)));
     if (g.nc) HIPCHECK(c, hipMemset(s.slot_last, 0xff, B * g.nc * sizeof(int32_t)));
+    if (g.nc) HIPCHECK(c, hipMemset(s.att, 0, B * g.nc * sizeof(int32_t)));
     if (g.n_slots) {
         HIPCHECK(c, hipMemset(s.slot_data, 0xff, B * g.n_slots * sizeof(int32_t)));
         HIPCHECK(c, hipMemset(s.slot_busy, 0, B * g.n_slots * sizeof(int32_t)));
@@ -508,9 +541,45 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, float *out, float *sco
     HIPCHECK(c, launch_anchor(g, c->t, c->s, q, s0));
     MARK(1);
     HIPCHECK(c, launch_anchor_combine(g, c->t, c->s, out, s0));
+    if (c->rec_pending) {
+        // next-step timing: the previous step's recall (on the side stream) reads the new list
+        // that the select kernel rewrites, and fills the slots this step's tidal heads read
+        HIPCHECK(c, hipStreamWaitEvent(s0, c->ev_rec, 0));
+        c->rec_pending = false;
+    }
     HIPCHECK(c, launch_select(g, c->s, sc, c->override_sel, sel, s0));
     const bool memcpy_path = c->cfg.flags & WNW_F_RECALL_MEMCPY;
-    if (!memcpy_path) {
+    if (g.next_step) {
+        // Next-step timing: this step's tidal heads read only slots filled before it, so the
+        // copies of the chunks that became resident now run on the side stream, overlapped with
+        // the rest of this step and the anchor attention of the next one.  Their target slots
+        // were free at this step's selection: no kernel on s0 from here on reads them until the
+        // next step has waited for ev_rec.
+        HIPCHECK(c, hipEventRecord(c->ev_sel, s0));
+        HIPCHECK(c, hipStreamWaitEvent(c->side, c->ev_sel, 0));
+        if (timing) HIPCHECK(c, hipEventRecord(ev.r[0], c->side));
+        if (!memcpy_path) {
+            HIPCHECK(c, launch_recall(g, c->t, c->s, c->side));
+        } else {
+            HIPCHECK(c, hipMemcpyAsync(c->h_newinfo, c->s.counts, g.B * 2 * sizeof(int32_t), hipMemcpyDeviceToHost, c->side));
+            if (g.k)
+                HIPCHECK(c, hipMemcpyAsync(c->h_newinfo + g.B * 2, c->s.new_list, (size_t)g.B * g.k * 2 * sizeof(int32_t),
+                                           hipMemcpyDeviceToHost, c->side));
+            HIPCHECK(c, hipEventRecord(c->ev_rec, c->side));
+        }
+        MARK(2);
+        HIPCHECK(c, launch_tidal_fixed(g, c->t, c->s, q, false, s0));
+        MARK(3);
+        MARK(4);
+        if (memcpy_path) {
+            HIPCHECK(c, hipEventSynchronize(c->ev_rec));
+            wnw_status r = issue_copies(c, c->side);
+            if (r != WNW_OK) return r;
+        }
+        if (timing) HIPCHECK(c, hipEventRecord(ev.r[1], c->side));
+        HIPCHECK(c, hipEventRecord(c->ev_rec, c->side));
+        c->rec_pending = true;
+    } else if (!memcpy_path) {
         MARK(2);
         // (3) + (4) in one launch: its first work-groups copy the complements listed for recall
         // from mapped pinned memory into their slots and attend to them as they arrive, the
@@ -535,25 +604,8 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, float *out, float *sco
         HIPCHECK(c, hipStreamWaitEvent(c->side, c->ev_sel, 0));
         if (timing) HIPCHECK(c, hipEventRecord(ev.r[0], c->side));
         HIPCHECK(c, hipEventSynchronize(c->ev_sel));
-        const int32_t *cnt = c->h_newinfo, *nl = c->h_newinfo + g.B * 2;
-        const size_t cb = (size_t)g.chunk_elems * sizeof(uint16_t);
-        for (int b = 0; b < g.B && cb; ++b) {
-            const int n = cnt[b * 2 + 1];
-            for (int i = 0; i < n;) {
-                // merge runs of consecutive chunks landing in consecutive slots
-                int j = i + 1;
-                const int32_t *e0 = nl + ((size_t)b * g.k + i) * 2;
-                while (j < n) {
-                    const int32_t *ej = nl + ((size_t)b * g.k + j) * 2;
-                    if (ej[0] != e0[0] + (j - i) || ej[1] != e0[1] + (j - i)) break;
-                    ++j;
-                }
-                HIPCHECK(c, hipMemcpyAsync(c->slots + ((size_t)b * g.n_slots + e0[1]) * g.chunk_elems,
-                                           c->host_comp + ((size_t)b * g.nc + e0[0]) * g.chunk_elems, cb * (j - i),
-                                           hipMemcpyHostToDevice, c->side));
-                i = j;
-            }
-        }
+        wnw_status r = issue_copies(c, c->side);
+        if (r != WNW_OK) return r;
         if (timing) HIPCHECK(c, hipEventRecord(ev.r[1], c->side));
         HIPCHECK(c, hipEventRecord(c->ev_rec, c->side));
         HIPCHECK(c, hipStreamWaitEvent(s0, c->ev_rec, 0));
@@ -665,9 +717,9 @@ wnw_status wnw_debug_read_resident(wnw_ctx *c, uint8_t *dst)
     const Geometry &g = c->g;
     DeviceGuard dg(c->device);
     HIPCHECK(c, hipDeviceSynchronize());
-    std::vector<int32_t> so((size_t)g.B * g.nc);
-    if (!so.empty()) HIPCHECK(c, hipMemcpy(so.data(), c->s.slot_of, so.size() * sizeof(int32_t), hipMemcpyDeviceToHost));
-    for (size_t i = 0; i < so.size(); ++i) dst[i] = so[i] >= 0;
+    std::vector<int32_t> att((size_t)g.B * g.nc);
+    if (!att.empty()) HIPCHECK(c, hipMemcpy(att.data(), c->s.att, att.size() * sizeof(int32_t), hipMemcpyDeviceToHost));
+    for (size_t i = 0; i < att.size(); ++i) dst[i] = att[i] != 0;
     return WNW_OK;
 }
 

@@ -12,6 +12,7 @@ constexpr int TILE_A = 128;     // anchor key rows per work-group
 constexpr int TILE_S = 128;     // tidal/fixed kept rows per work-group (slot groups: 128 or 256)
 constexpr int MAX_CHUNK = 256;  // longest chunk the slot kernels handle
 constexpr int SEL_THREADS = 1024;
+constexpr int SCORE_PARTS = 4;   // fixed ranges of anchor q-heads summed per chunk score
 
 // Everything the kernels need to know about the cache and the step, fixed at set-up.
 struct Geometry {
@@ -19,6 +20,7 @@ struct Geometry {
     int Ta, Tt, T;              // audio, text and total rows of an anchor head
     int cl, budget_bp;          // chunk length, retention in basis points
     int nc, k, delta;           // chunks, selected per step, eviction lag
+    int next_step;              // 1: tidal heads of step s attend over the resident set of step s-1
     int keep_total, Rs;         // kept audio rows per non-anchor head; static rows = keep + text
     int comp_max;               // complement rows of a full chunk (chunk_len - keep(chunk_len))
     int n_slots;                // recall slots per sequence (delta * k)
@@ -71,9 +73,10 @@ struct StepBuffers {
     int32_t *slot_of;           // [B][nc]  slot holding the chunk's complement or -1
     int32_t *slot_last;         // [B][nc]  slot that last received the chunk's bytes or -1
     int32_t *slot_data;         // [B][n_slots] chunk whose bytes the slot holds or -1
-    int32_t *slot_busy;         // [B][n_slots] 1 while assigned to a resident chunk
+    int32_t *slot_busy;         // [B][n_slots] 0 free, 1 owned, 2 freed once this step has read it
     int32_t *slot_since;        // [B][n_slots] step at which the slot was last freed
     int32_t *step;              // [B] steps run
+    int32_t *att;               // [B][nc]  complements attended by the last step
     int32_t *kept_list;         // [B][n_slots][2] (chunk, slot) resident before and now
     int32_t *new_list;          // [B][k][2]       (chunk, slot) newly resident this step
     int32_t *counts;            // [B][2] kept, new
@@ -91,12 +94,15 @@ hipError_t launch_select(const Geometry &g, const StepBuffers &s, float *scores,
 // Shared memory of the select kernel (bounded at set-up).
 inline size_t select_shared_bytes(const Geometry &g)
 {
-    return (size_t)g.nc * (4 * 8 + 4 + 4 * 4) + (size_t)g.n_slots * 12;
+    return (size_t)g.nc * (SCORE_PARTS * 8 + 4 + 8 * 4) + (size_t)g.n_slots * 5 * 4;
 }
 // Fixed heads, tidal kept rows and resident complements; with `recall`, also the copy of the
 // complements listed for recall from mapped pinned memory, attended to as they arrive.
 hipError_t launch_tidal_fixed(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, bool recall,
                               hipStream_t st);
+// Next-step timing: copy of the complements listed for recall from mapped pinned memory into
+// their slots, no attention (they are attended from the next step on).
+hipError_t launch_recall(const Geometry &g, const Tiers &t, const StepBuffers &s, hipStream_t st);
 // Complements already copied to their slots by the host-waited recall path.
 hipError_t launch_new_slots(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st);
 hipError_t launch_subset_combine(const Geometry &g, const Tiers &t, const StepBuffers &s, float *out,

@@ -428,42 +428,66 @@ __device__ int block_scan_excl(int *a, int n, int *wsum)
     return carry;
 }
 
-constexpr int SCORE_PARTS = 4;   // anchor q-heads split in this many fixed ranges per chunk
 
-// Per sequence b:
+
+// Per sequence b (state staged in shared memory, written back at the end):
 //   scores   score_c = (sum over anchor q-heads of their chunk mass) / |c|, double, fixed order
 //   select   top-k by (fp32 score desc, id asc), or the caller's override
 //   streaks  0 when selected, else +1 (capped at delta); resident iff streak < delta
-//   slots    chunks that stop being resident free their slot; a newly resident chunk whose
-//            bytes still sit in a free slot (never overwritten since) takes that slot back with
-//            no copy; the others take free slots in least-recently-freed order (never-used
-//            slots first) and are listed for recall
-//   lists    kept list = resident with their bytes on the device; new list = to be recalled
+//   attended this step: the resident set R_s (same-step timing) or R_{s-1} (next-step timing)
+//   slots    a chunk that stops being resident frees its slot (next-step timing: one step later,
+//            after this step's attention has read it); a newly resident chunk whose bytes still
+//            sit in a free slot (never overwritten since) takes it back with no copy; the others
+//            take free slots in least-recently-freed order (never-used slots first) and are
+//            listed for recall
+//   lists    kept list = attended this step with bytes already on the device; new list = to
+//            recall (attended in the same launch with same-step timing, from the next step on
+//            with next-step timing)
 __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuffers s, float *__restrict__ scores,
                                                              const int32_t *__restrict__ ovr, int32_t *__restrict__ selected)
 {
     const int b = blockIdx.x, tid = threadIdx.x, nthr = blockDim.x;
     const int nc = g.nc, k = g.k, ns = g.n_slots, naq = g.nA * g.G;
+    const bool nxt = g.next_step;
     extern __shared__ double sdyn[];
     double *part = sdyn;                              // [SCORE_PARTS][nc]
     float *sc = (float *)(part + SCORE_PARTS * nc);   // [nc]
-    int *fsel = (int *)(sc + nc);                     // [nc]
-    int *fnew = fsel + nc;                            // [nc]
-    int *fkept = fnew + nc;                           // [nc]
-    int *rank = fkept + nc;                           // [nc]
-    int *sfree = rank + nc;                           // [ns] free flag, then rank
-    int *freelist = sfree + ns;                       // [ns]
-    int *skey = freelist + ns;                        // [ns] ordering key of free slots
+    int *fsel = (int *)(sc + nc);                     // [nc] selected
+    int *st = fsel + nc;                              // [nc] streak
+    int *sof = st + nc;                               // [nc] slot of the chunk or -1
+    int *slast = sof + nc;                            // [nc] slot that last received the chunk
+    int *fnew = slast + nc;                           // [nc] to recall
+    int *fkept = fnew + nc;                           // [nc] attended from a slot already filled
+    int *fdrop = fkept + nc;                          // [nc] leaves the resident set
+    int *rank = fdrop + nc;                           // [nc] scan scratch
+    int *busy = rank + nc;                            // [ns] 0 free, 1 owned, 2 freed after this step
+    int *sdata = busy + ns;                           // [ns] chunk whose bytes the slot holds
+    int *since = sdata + ns;                          // [ns] step at which the slot was freed
+    int *skey = since + ns;                           // [ns] ordering key of free slots
+    int *freelist = skey + ns;                        // [ns] free slots in order
     __shared__ int wsum[SEL_THREADS / 64 + 1];
-    __shared__ int ndrop, nrows, nrev;
+    __shared__ int ndrop, nrows, nrev, nfree;
 
-    int32_t *streak = s.streak + (size_t)b * nc, *slot_of = s.slot_of + (size_t)b * nc;
-    int32_t *slot_last = s.slot_last + (size_t)b * nc;
-    int32_t *slot_data = s.slot_data + (size_t)b * ns, *slot_busy = s.slot_busy + (size_t)b * ns;
-    int32_t *slot_since = s.slot_since + (size_t)b * ns;
+    int32_t *g_streak = s.streak + (size_t)b * nc, *g_slot_of = s.slot_of + (size_t)b * nc;
+    int32_t *g_slot_last = s.slot_last + (size_t)b * nc;
+    int32_t *g_att = s.att + (size_t)b * nc;
+    int32_t *g_data = s.slot_data + (size_t)b * ns, *g_busy = s.slot_busy + (size_t)b * ns;
+    int32_t *g_since = s.slot_since + (size_t)b * ns;
     const int step = s.step[b];
 
-    // scores
+    // state in, chunk scores
+    for (int c = tid; c < nc; c += nthr) {
+        st[c] = g_streak[c];
+        sof[c] = g_slot_of[c];
+        slast[c] = g_slot_last[c];
+        fsel[c] = 0;
+    }
+    for (int i = tid; i < ns; i += nthr) {
+        const int bz = g_busy[i];
+        busy[i] = bz == 2 ? 0 : bz;                   // frees deferred by the previous step
+        sdata[i] = g_data[i];
+        since[i] = g_since[i];
+    }
     for (int idx = tid; idx < SCORE_PARTS * nc; idx += nthr) {
         const int p = idx / nc, c = idx - p * nc;
         const int a0 = p * naq / SCORE_PARTS, a1 = (p + 1) * naq / SCORE_PARTS;
@@ -473,7 +497,7 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
         for (int a = a0; a < a1; ++a) acc += m[(size_t)(a - a0) * nc];
         part[idx] = acc;
     }
-    if (tid == 0) ndrop = nrows = nrev = 0;
+    if (tid == 0) ndrop = nrows = nrev = nfree = 0;
     __syncthreads();
     for (int c = tid; c < nc; c += nthr) {
         double acc = part[c];
@@ -481,7 +505,6 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
         const float v = (float)(acc / (double)chunk_len_of(g, c));
         sc[c] = v;
         scores[(size_t)b * nc + c] = v;
-        fsel[c] = 0;
     }
     __syncthreads();
 
@@ -506,32 +529,32 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
 
     // streaks, residency, drops
     for (int c = tid; c < nc; c += nthr) {
-        int st = streak[c];
-        st = fsel[c] ? 0 : min(st + 1, g.delta);
-        streak[c] = st;
-        const bool now = st < g.delta;
-        const int slot = slot_of[c];
-        const bool was = slot >= 0;
-        if (was && !now) {
-            slot_busy[slot] = 0;
-            slot_since[slot] = step;
-            slot_of[c] = -1;
+        const int stc = fsel[c] ? 0 : min(st[c] + 1, g.delta);
+        st[c] = stc;
+        const bool now = stc < g.delta;
+        const bool owned = sof[c] >= 0;     // has a slot: resident after the previous step
+        fdrop[c] = owned && !now;
+        fnew[c] = now && !owned;
+        fkept[c] = nxt ? owned : (now && owned);
+        const bool att = nxt ? owned : now;
+        g_att[c] = att;
+        if (att) atomicAdd(&nrows, comp_of(g, c));
+        if (fdrop[c]) {
+            busy[sof[c]] = nxt ? 2 : 0;
+            since[sof[c]] = step;
             atomicAdd(&ndrop, 1);
         }
-        fnew[c] = now && !was;
-        fkept[c] = now && was;
-        if (now) atomicAdd(&nrows, comp_of(g, c));
     }
     __syncthreads();
     // revival: the chunk's bytes are still in the free slot it last occupied
     for (int c = tid; c < nc; c += nthr)
         if (fnew[c]) {
-            const int sl = slot_last[c];
-            if (sl >= 0 && !slot_busy[sl] && slot_data[sl] == c) {
-                slot_busy[sl] = 1;
-                slot_of[c] = sl;
+            const int sl = slast[c];
+            if (sl >= 0 && busy[sl] == 0 && sdata[sl] == c) {
+                busy[sl] = 1;
+                sof[c] = sl;
                 fnew[c] = 0;
-                fkept[c] = 1;
+                if (!nxt) fkept[c] = 1;
                 atomicAdd(&nrev, 1);
             }
         }
@@ -548,32 +571,35 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
     }
 
     // free slots ordered by (holds data, freed at step, slot id): never-used first, then the
-    // least recently freed.  Key: -1 for busy slots, else (holds data) * 2^30 + freed-at step.
-    for (int i = tid; i < ns; i += nthr) {
-        sfree[i] = !slot_busy[i];
-        skey[i] = slot_busy[i] ? -1 : ((slot_data[i] >= 0 ? 1 : 0) << 30) + slot_since[i];
-    }
+    // least recently freed.  Key: -1 for slots not free, else (holds data) * 2^30 + freed-at step.
+    for (int i = tid; i < ns; i += nthr) skey[i] = busy[i] ? -1 : ((sdata[i] >= 0 ? 1 : 0) << 30) + since[i];
     __syncthreads();
     for (int i = tid; i < ns; i += nthr) {
-        freelist[i] = -1;
-        if (!sfree[i]) continue;
         const int ki = skey[i];
+        if (ki < 0) continue;
         int r = 0;
         for (int j = 0; j < ns; ++j) {
             const int kj = skey[j];
             r += kj >= 0 && (kj < ki || (kj == ki && j < i));
         }
-        freelist[i] = r;
+        freelist[r] = i;   // the ranks of the free slots are 0 .. nfree-1, each once
+        atomicAdd(&nfree, 1);
     }
     __syncthreads();
-    int nfree = 0;
-    for (int i = 0; i < ns; ++i) nfree += sfree[i];
+
+    // kept list first (it needs the slots of chunks dropped now under next-step timing)
+    for (int c = tid; c < nc; c += nthr) rank[c] = fkept[c];
     __syncthreads();
-    for (int i = tid; i < ns; i += nthr) sfree[i] = freelist[i];
+    const int nkept = block_scan_excl(rank, nc, wsum);
+    int32_t *kl = s.kept_list + (size_t)b * ns * 2;
+    for (int c = tid; c < nc; c += nthr)
+        if (fkept[c]) {
+            kl[rank[c] * 2] = c;
+            kl[rank[c] * 2 + 1] = sof[c];
+        }
     __syncthreads();
-    for (int i = tid; i < ns; i += nthr)
-        if (sfree[i] >= 0) freelist[sfree[i]] = i;
-    __syncthreads();
+    for (int c = tid; c < nc; c += nthr)
+        if (fdrop[c]) sof[c] = -1;
 
     // chunks to recall take the free slots in that order (lowest id first)
     for (int c = tid; c < nc; c += nthr) rank[c] = fnew[c];
@@ -583,24 +609,26 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
     for (int c = tid; c < nc; c += nthr)
         if (fnew[c] && rank[c] < nfree && rank[c] < k) {
             const int slot = freelist[rank[c]];
-            slot_of[c] = slot;
-            slot_last[c] = slot;
-            slot_busy[slot] = 1;
-            slot_data[slot] = c;
+            sof[c] = slot;
+            slast[c] = slot;
+            busy[slot] = 1;
+            sdata[slot] = c;
             nl[rank[c] * 2] = c;
             nl[rank[c] * 2 + 1] = slot;
         }
     __syncthreads();
 
-    for (int c = tid; c < nc; c += nthr) rank[c] = fkept[c];
-    __syncthreads();
-    const int nkept = block_scan_excl(rank, nc, wsum);
-    int32_t *kl = s.kept_list + (size_t)b * ns * 2;
-    for (int c = tid; c < nc; c += nthr)
-        if (fkept[c]) {
-            kl[rank[c] * 2] = c;
-            kl[rank[c] * 2 + 1] = slot_of[c];
-        }
+    // state out
+    for (int c = tid; c < nc; c += nthr) {
+        g_streak[c] = st[c];
+        g_slot_of[c] = sof[c];
+        g_slot_last[c] = slast[c];
+    }
+    for (int i = tid; i < ns; i += nthr) {
+        g_busy[i] = busy[i];
+        g_data[i] = sdata[i];
+        g_since[i] = since[i];
+    }
     if (tid == 0) {
         const int nn = min(nnew, min(nfree, k));
         s.counts[b * 2] = nkept;
@@ -608,9 +636,11 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
         s.step[b] = step + 1;
         atomicAdd(&s.stats[0], (unsigned long long)nn);
         atomicAdd(&s.stats[1], (unsigned long long)ndrop);
-        atomicAdd(&s.stats[2], (unsigned long long)(nkept + nn));
+        // resident set after the step: |R_s|
+        const int nres = nxt ? nkept - ndrop + nrev + nn : nkept + nn;
+        atomicAdd(&s.stats[2], (unsigned long long)nres);
         atomicAdd(&s.stats[3], (unsigned long long)nrows);
-        atomicMax(&s.stats[4], (unsigned long long)(nkept + nn));
+        atomicMax(&s.stats[4], (unsigned long long)nres);
         if (nnew > nn) atomicAdd(&s.stats[5], 1ull);   // slot exhaustion (never expected)
         atomicAdd(&s.stats[6], (unsigned long long)nrev);
     }
@@ -902,6 +932,26 @@ __global__ __launch_bounds__(NT) void tidal_fixed_kernel(Geometry g, Tiers t, St
     slot_group<G, RPLK>(g, t, s, q, grp, rest % g.nT, rest / g.nT, 0, g.sg);
 }
 
+// Next-step timing: copy only.  Work-group w of the grid walks the units (sequence, new entry,
+// tidal head) and copies each unit's block (K and V complement rows, padding included) from
+// mapped pinned memory to its slot; the rows are attended from the next step on.
+__global__ __launch_bounds__(NT) void recall_copy_kernel(Geometry g, Tiers t, StepBuffers s)
+{
+    int total = 0;
+    for (int b = 0; b < g.B; ++b) total += s.counts[b * 2 + 1] * g.nT;
+    const int n16 = 2 * g.comp_max * (D / 8);   // 16-byte vectors per unit
+    for (int u = blockIdx.x; u < total; u += gridDim.x) {
+        int b = 0, r = u;
+        while (r >= s.counts[b * 2 + 1] * g.nT) r -= s.counts[b++ * 2 + 1] * g.nT;
+        const int e = r / g.nT, ti = r - e * g.nT;
+        const int c = s.new_list[((size_t)b * g.k + e) * 2], slot = s.new_list[((size_t)b * g.k + e) * 2 + 1];
+        const size_t off = (size_t)ti * 2 * g.comp_max * D;
+        const uint4 *src = (const uint4 *)(t.host_comp + ((size_t)b * g.nc + c) * g.chunk_elems + off);
+        uint4 *dst = (uint4 *)(t.slots + ((size_t)b * g.n_slots + slot) * g.chunk_elems + off);
+        for (int j = threadIdx.x; j < n16; j += NT) dst[j] = src[j];
+    }
+}
+
 // Complements copied by hipMemcpyAsync (host-waited recall path): one entry per work-group.
 template <int G, int RPL>
 __global__ __launch_bounds__(NT) void new_slots_kernel(Geometry g, Tiers t, StepBuffers s, const uint16_t *__restrict__ q)
@@ -925,7 +975,7 @@ __global__ __launch_bounds__(COMBINE_THREADS) void subset_combine_kernel(Geometr
     __shared__ float opart[OG > 1 ? OG : 1][G * D > COMBINE_THREADS ? 1 : G * D];
     const int nk = tidal ? min((s.counts[b * 2] + g.sg - 1) / g.sg, g.ng_kept) : 0;
     // one partial per new entry; none exist when complements are empty (100 % budget)
-    const int nn = tidal ? min(s.counts[b * 2 + 1], g.np - g.n_tiles_s - g.ng_kept) : 0;
+    const int nn = (tidal && !g.next_step) ? min(s.counts[b * 2 + 1], g.np - g.n_tiles_s - g.ng_kept) : 0;
     const int nvalid = g.n_tiles_s + nk + nn;
     auto part = [&](int j) {
         if (j < g.n_tiles_s) return j;
@@ -1120,6 +1170,13 @@ hipError_t launch_tidal_fixed(const Geometry &g, const Tiers &t, const StepBuffe
                               hipStream_t st)
 {
     return dispatch_g<TidalFixedL>(g.G, g, t, s, q, recall, st);
+}
+
+hipError_t launch_recall(const Geometry &g, const Tiers &t, const StepBuffers &s, hipStream_t st)
+{
+    if (g.nT == 0 || g.k == 0 || g.comp_max == 0) return hipSuccess;
+    hipLaunchKernelGGL(recall_copy_kernel, dim3(RECALL_WGS), dim3(NT), 0, st, g, t, s);
+    return hipGetLastError();
 }
 
 hipError_t launch_new_slots(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st)

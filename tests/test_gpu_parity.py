@@ -266,3 +266,88 @@ def test_voxtral_60min_b4_full_size_sampled(w):
     against the oracle with sampled heads (the oracle's anchor pass alone is ~2 G multiply-adds
     per step per sequence)."""
     _run(w, steps=24, head_mask_fn=_sampled(6), seqs=[2])
+
+
+# ---- next-step selection timing: the tidal heads of step s attend over the resident set left
+# by step s-1; the oracle runs the same timing (its next_step mode).
+
+def _next(extra=0):
+    from paper_2608_22704_amd import wnw as W
+    return W.WNW_F_SELECT_NEXT_STEP | extra
+
+
+def test_next_step_tiny():
+    _run(configs.TINY.with_(steps=6), flags=_next())
+
+
+@pytest.mark.parametrize("w", EDGE, ids=[w.name for w in EDGE])
+def test_next_step_edge_shapes(w):
+    _run(w, flags=_next())
+
+
+def test_next_step_memcpy_recall_path():
+    from paper_2608_22704_amd import wnw as W
+    _run(_small("next_memcpy", 170, L=2, Hq=8, Hkv=4, Ta=480, Tt=5, cl=16, steps=12),
+         flags=_next(W.WNW_F_RECALL_MEMCPY))
+
+
+def test_next_step_qwen_shaped_all_steps():
+    _run(configs.QWEN_10MIN, flags=_next())
+
+
+def test_next_step_voxtral_shaped_sampled_heads():
+    _run(configs.VOXTRAL_10MIN.with_(steps=64), head_mask_fn=_sampled(16), flags=_next())
+
+
+@pytest.mark.parametrize("memcpy", [False, True], ids=["zero_copy", "memcpy"])
+def test_next_step_slots_over_steps(memcpy):
+    """Next-step timing: after every step the chunks holding a slot are the resident set that the
+    following step attends to, and each slot (recalled during the step, or revived) is
+    byte-identical to the chunk's host complement."""
+    from paper_2608_22704_amd import wnw as W
+    from tests.wnw_harness import Lockstep, log
+    w = _small("next_slots_over_steps", 161, L=2, Hq=8, Hkv=4, Ta=480, Tt=5, cl=16, budget=2000, steps=24)
+    log(f"[case] next-step slots vs host copies over 24 steps, memcpy={memcpy}")
+    h = Lockstep(w, flags=_next(W.WNW_F_RECALL_MEMCPY if memcpy else 0))
+    try:
+        nbytes = h.geo["chunk_bytes"]
+        assert h.geo["n_slots"] == 4 * h.k
+        held_before = None
+        for s in range(w.steps):
+            _, _, _, res = h.step(s)
+            if held_before is not None:
+                assert np.array_equal(res, held_before), f"step {s}: attended set is not the previous resident set"
+            held = np.zeros_like(res)
+            for b in range(w.batch):
+                for c in range(h.nc):
+                    dev = np.empty(nbytes // 2, dtype=np.uint16)
+                    try:
+                        W.wnw_debug_read_slot(h.ctx, b, c, dev, nbytes)
+                    except W.WnwError:
+                        continue
+                    held[b, c] = 1
+                    hst = np.empty(nbytes // 2, dtype=np.uint16)
+                    W.wnw_debug_read_host_chunk(h.ctx, b, c, hst, nbytes)
+                    assert np.array_equal(dev, hst), f"step {s} seq {b} chunk {c}"
+            held_before = held
+        st = W.wnw_get_stats(h.ctx)
+        log(f"[done] recalled {st['recalled_chunks']} revived {st['revived_chunks']} dropped {st['dropped_chunks']}")
+        assert st["revived_chunks"] > 0
+    finally:
+        h.close()
+
+
+def test_next_step_two_runs_bit_identical():
+    from tests.wnw_harness import Lockstep, log
+    w = _small("determinism_next", 131, steps=5)
+    log("[case] determinism, next-step timing")
+    outs = []
+    for _ in range(2):
+        h = Lockstep(w, flags=_next())
+        try:
+            outs.append([h.gpu_step(s) for s in range(w.steps)])
+        finally:
+            h.close()
+    for a, b in zip(*outs):
+        for x, y in zip(a, b):
+            assert np.array_equal(x, y)

@@ -97,7 +97,8 @@ class Lockstep:
         del kd, vd
         torch.cuda.empty_cache()
         self.geo = W.wnw_query_geometry(self.ctx)
-        ocfg = O.cfg_from_workload(w, batch=len(self.seqs), top_k=top_k)
+        self.next_step = 1 if flags & W.WNW_F_SELECT_NEXT_STEP else 0
+        ocfg = O.cfg_from_workload(w, batch=len(self.seqs), top_k=top_k, next_step=self.next_step)
         self.ok_ = np.stack([host[b]["k"] for b in self.seqs])
         self.ov_ = np.stack([host[b]["v"] for b in self.seqs])
         self.oracle = O.Oracle(ocfg, self.ok_, self.ov_, self.roles, self.prefill[self.seqs])
