@@ -126,28 +126,58 @@ __device__ inline void block_sum(T v[G], T *red)
 // -------------------------------------------------------------------------------------------
 // Anchor attention + chunk mass (double logits)
 //
+// Loads: K and V rows are read fully coalesced (one wavefront instruction = 4 whole rows) with
+// nontemporal loads (every byte is read once per step).  Each wavefront owns 32 rows of the tile.
+//
 // Logits come from v_mfma_f64_4x4x4f64 (four independent 4x4x4 blocks per wavefront).  On
 // gfx950 lane l = 16k + 4*blk + x holds A_blk[x][k] and B_blk[k][x], and the result
 // D_blk[i][j] lands in lane 16i + 4*blk + j.  With A = key rows and B = q^T, one instruction
-// multiplies 16 keys (4 per block) by 4 q-heads over 4 dimensions.  The dimension index is
-// permuted consistently on both operands: lane l feeds dimension 32k + t to instruction t, so it
-// reads 64 contiguous bytes of its key row; 32 instructions cover d = 128.  For groups of 6 or 8
-// q-heads, blocks 0-1 take heads 0-3 and blocks 2-3 heads 4-7 over the same 8 keys.  Products of
-// bf16 values are exact in double, so the logits match a double reference to rounding.
+// multiplies 16 keys (4 per block) by 4 q-heads over 4 dimensions; lane l feeds dimension 32k + t
+// to instruction t, so it needs 64 contiguous bytes of its key row.  The coalesced K rows reach
+// that layout through a per-wavefront LDS region whose 16-byte units are XOR-swizzled by the row
+// (unit p of row r at r*16 + (p ^ (r & 15))), so both the stores and the operand reads are free
+// of bank conflicts.  For groups of 6 or 8 q-heads, blocks 0-1 take heads 0-3 and blocks 2-3
+// heads 4-7 over the same 8 keys.  Products of bf16 values are exact in double, so the logits
+// match a double reference to rounding.
 //
-// Each wavefront owns 32 rows of the tile and runs its own softmax on them straight from the
-// instruction's result layout (one (key, head) logit per lane, so every exp is computed once);
-// P.V needs only the wavefront's own probabilities.  The four wavefronts meet once, to merge.
+// Softmax: the four wavefronts agree on the tile maximum M (one barrier) before any exp, so the
+// probabilities, their sums, the chunk masses and the P.V partials all share M and merge by
+// plain sums.  exp(y) is evaluated as 2^n * 2^f with n = rint(y log2 e) and f in [-1/2, 1/2]
+// taken in double and 2^f by the hardware exp2 in fp32 (relative error ~1e-7).
+//
+// P.V runs on v_mfma_f32_4x4x1 (16 blocks): lane l = 4*blk + j feeds B_blk[0][j] = its own V
+// element (row 4i + rg, dimension 8*sub + e) and A_blk[h][0] = P[h][row 4i + rg] with h = l & 3,
+// so D_blk[h][j] accumulates, per lane, the same sums a per-lane FMA loop would.
 // -------------------------------------------------------------------------------------------
-template <int G>
-__global__ __launch_bounds__(NT) void anchor_attn_kernel(Geometry g, Tiers t, StepBuffers s,
-                                                         const uint16_t *__restrict__ q)
+__device__ inline uint4 load_nt(const uint16_t *p)
 {
-    constexpr int HG = G <= 4 ? 1 : 2;        // groups of 4 q-heads per instruction
-    constexpr int KG = 16 / HG;               // keys per instruction
+    typedef unsigned v4u __attribute__((ext_vector_type(4)));
+    const v4u a = __builtin_nontemporal_load((const v4u *)p);
+    return make_uint4(a.x, a.y, a.z, a.w);
+}
+
+// exp(y) for y <= 0 (see above); 0 below 2^-1022
+__device__ inline double exp_nonpos(double y)
+{
+    const double tt = y * 1.4426950408889634074;
+    const double n = rint(tt);
+    const float e = __builtin_amdgcn_exp2f((float)(tt - n));
+    return tt < -1022.0 ? 0.0 : ldexp((double)e, (int)n);
+}
+
+template <int G>
+__global__ __launch_bounds__(NT, G <= 4 ? 4 : 2) void anchor_attn_kernel(Geometry g, Tiers t, StepBuffers s,
+                                                                         const uint16_t *__restrict__ q)
+{
+    typedef float v4f __attribute__((ext_vector_type(4)));
+    constexpr int HG = G <= 4 ? 1 : 2;        // groups of 4 q-heads per logit instruction
+    constexpr int KG = 16 / HG;               // keys per logit instruction
     constexpr int RW = TILE_A / WAVES;        // key rows per wavefront (32)
-    constexpr int NKG = RW / KG;              // key groups per wavefront
-    constexpr int RPL = RW / 4;               // 4-row steps per wavefront in the P.V layout
+    constexpr int NKG = RW / KG;              // key groups per wavefront (2 or 4)
+    constexpr int RPL = RW / 4;               // coalesced 4-row steps per wavefront
+    constexpr int OGR = G <= 4 ? 4 : 2;       // row groups kept in the P.V partial store
+    constexpr int HS = (G + 3) / 4;           // sets of 4 heads for P.V
+    static_assert(NKG % 2 == 0, "key groups are processed in pairs");
     const int tile = blockIdx.x, ai = blockIdx.y, b = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, sub = lane & 15, rg = lane >> 4;
     const int kq = lane >> 4, blk = (lane >> 2) & 3, x4 = lane & 3;
@@ -157,58 +187,75 @@ __global__ __launch_bounds__(NT) void anchor_attn_kernel(Geometry g, Tiers t, St
     const uint16_t *__restrict__ V = t.aV + hrow * D;
     const uint16_t *__restrict__ qh = q + (((size_t)b * g.L + l) * g.Hq + (size_t)kv * G) * D;
     const int t0 = tile * TILE_A;
+    // chunk masses from wavefront sums when every wavefront's audio rows lie in one chunk and no
+    // wavefront of this tile straddles the audio/text boundary
+    const bool fast_mass = g.cl % RW == 0 && !(t0 < g.Ta && g.Ta < t0 + TILE_A && g.Ta % RW != 0);
 
-    __shared__ double xs[G * TILE_A];    // probabilities relative to their wavefront's maximum
-    __shared__ float xf[G * TILE_A];     // the same in fp32, for P.V
-    __shared__ float wo[WAVES * 4 * G * D];   // P.V partials per (wavefront, 4-row group)
+    __shared__ uint4 kst[WAVES][RW * 16];     // swizzled K rows; afterwards the P.V partials
+    __shared__ double xs[G * TILE_A];         // probabilities (per-row chunk masses only)
+    __shared__ float xf[G * TILE_A];          // probabilities in fp32, for P.V
     __shared__ double wm[WAVES * G], wl[WAVES * G];
-    __shared__ double wf[WAVES * G];     // merge factors exp(m_w - M)
+    float *wo = (float *)&kst[wave][0];       // [OGR][G][D] of this wavefront
 
-    // q (B operand: head hB, dims 32kq..32kq+31), then the key rows (A operand), then V rows
+    // q (B operand: head hB, dims 32kq..32kq+31), then K and V rows
     const int hB = (HG == 1 ? 0 : (blk >> 1) * 4) + x4;
     uint4 qr[4];
 #pragma unroll
     for (int u = 0; u < 4; ++u)
         qr[u] = hB < G ? *(const uint4 *)(qh + hB * D + kq * 32 + u * 8) : make_uint4(0, 0, 0, 0);
-    const int keyA = (HG == 1 ? blk * 4 : (blk & 1) * 4) + x4;
-    uint4 kr[NKG][4];
-#pragma unroll
-    for (int kg = 0; kg < NKG; ++kg) {
-        const int row = t0 + wave * RW + kg * KG + keyA;
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-            kr[kg][u] = row < g.T ? *(const uint4 *)(K + (size_t)row * D + kq * 32 + u * 8) : make_uint4(0, 0, 0, 0);
-    }
-    uint4 vr[RPL];
+    uint4 kr[RPL], vr[RPL];
 #pragma unroll
     for (int i = 0; i < RPL; ++i) {
         const int row = t0 + wave * RW + i * 4 + rg;
-        vr[i] = row < g.T ? *(const uint4 *)(V + (size_t)row * D + sub * 8) : make_uint4(0, 0, 0, 0);
+        kr[i] = row < g.T ? load_nt(K + (size_t)row * D + sub * 8) : make_uint4(0, 0, 0, 0);
     }
+#pragma unroll
+    for (int i = 0; i < RPL; ++i) {
+        const int row = t0 + wave * RW + i * 4 + rg;
+        vr[i] = row < g.T ? load_nt(V + (size_t)row * D + sub * 8) : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < RPL; ++i) {
+        const int r = i * 4 + rg;
+        kst[wave][r * 16 + (sub ^ (r & 15))] = kr[i];
+    }
+    // each wavefront reads back only its own rows: a wavefront-scope fence suffices
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 
-    // logits of (key keyD, head hD) per key group
+    // logits of (key keyD, head hD) per key group; key groups in pairs, four accumulator chains
+    const int keyA = (HG == 1 ? blk * 4 : (blk & 1) * 4) + x4;
     const int keyD = (HG == 1 ? blk * 4 : (blk & 1) * 4) + kq;
     const int hD = (HG == 1 ? 0 : (blk >> 1) * 4) + x4;
     double xv[NKG];
 #pragma unroll
-    for (int kg = 0; kg < NKG; ++kg) {
-        double acc0 = 0.0, acc1 = 0.0;
+    for (int kp = 0; kp < NKG; kp += 2) {
+        double a00 = 0.0, a01 = 0.0, a10 = 0.0, a11 = 0.0;
+        const int r0 = kp * KG + keyA, r1 = r0 + KG;
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-            float f[8], qf[8];
-            unpack8(kr[kg][u], f);
+            const uint4 k0 = kst[wave][r0 * 16 + ((kq * 4 + u) ^ (r0 & 15))];
+            const uint4 k1 = kst[wave][r1 * 16 + ((kq * 4 + u) ^ (r1 & 15))];
+            float f0[8], f1[8], qf[8];
+            unpack8(k0, f0);
+            unpack8(k1, f1);
             unpack8(qr[u], qf);
 #pragma unroll
             for (int e = 0; e < 8; e += 2) {
-                acc0 = __builtin_amdgcn_mfma_f64_4x4x4f64((double)f[e], (double)qf[e], acc0, 0, 0, 0);
-                acc1 = __builtin_amdgcn_mfma_f64_4x4x4f64((double)f[e + 1], (double)qf[e + 1], acc1, 0, 0, 0);
+                const double qa = (double)qf[e], qb = (double)qf[e + 1];
+                a00 = __builtin_amdgcn_mfma_f64_4x4x4f64((double)f0[e], qa, a00, 0, 0, 0);
+                a10 = __builtin_amdgcn_mfma_f64_4x4x4f64((double)f1[e], qa, a10, 0, 0, 0);
+                a01 = __builtin_amdgcn_mfma_f64_4x4x4f64((double)f0[e + 1], qb, a01, 0, 0, 0);
+                a11 = __builtin_amdgcn_mfma_f64_4x4x4f64((double)f1[e + 1], qb, a11, 0, 0, 0);
             }
         }
-        const int rr = wave * RW + kg * KG + keyD;
-        xv[kg] = (hD < G && t0 + rr < g.T) ? (acc0 + acc1) * SCALE_D : -INFINITY;
+        const int rr0 = t0 + wave * RW + kp * KG + keyD;
+        xv[kp] = (hD < G && rr0 < g.T) ? (a00 + a01) * SCALE_D : -INFINITY;
+        xv[kp + 1] = (hD < G && rr0 + KG < g.T) ? (a10 + a11) * SCALE_D : -INFINITY;
     }
-    // wavefront softmax per head: the lanes of one head differ in bits 2, 4, 5 (and 3 when
-    // all four blocks share the heads)
+    // wavefront maximum per head (lanes of one head differ in bits 2, 4, 5, and 3 when all four
+    // blocks share the heads), then the tile maximum over the four wavefronts
     double m = xv[0];
 #pragma unroll
     for (int kg = 1; kg < NKG; ++kg) m = fmax(m, xv[kg]);
@@ -216,13 +263,21 @@ __global__ __launch_bounds__(NT) void anchor_attn_kernel(Geometry g, Tiers t, St
     if (HG == 1) m = fmax(m, __shfl_xor(m, 8));
     m = fmax(m, __shfl_xor(m, 16));
     m = fmax(m, __shfl_xor(m, 32));
+    const bool head_lane = hD < G && kq == 0 && (HG == 1 ? blk == 0 : (blk & 1) == 0);
+    if (head_lane) wm[wave * G + hD] = m;
+    __syncthreads();
+    if (hD < G) {
+#pragma unroll
+        for (int w = 0; w < WAVES; ++w) m = fmax(m, wm[w * G + hD]);
+    }
     double lsum = 0.0;
 #pragma unroll
     for (int kg = 0; kg < NKG; ++kg) {
-        const double pv = (m == -INFINITY || xv[kg] == -INFINITY) ? 0.0 : exp(xv[kg] - m);
+        const double pv = (m == -INFINITY || xv[kg] == -INFINITY) ? 0.0 : exp_nonpos(xv[kg] - m);
         if (hD < G) {
-            xs[hD * TILE_A + wave * RW + kg * KG + keyD] = pv;
-            xf[hD * TILE_A + wave * RW + kg * KG + keyD] = (float)pv;
+            const int rr = wave * RW + kg * KG + keyD;
+            if (!fast_mass) xs[hD * TILE_A + rr] = pv;
+            xf[hD * TILE_A + rr] = (float)pv;
         }
         lsum += pv;
     }
@@ -230,74 +285,85 @@ __global__ __launch_bounds__(NT) void anchor_attn_kernel(Geometry g, Tiers t, St
     if (HG == 1) lsum += __shfl_xor(lsum, 8);
     lsum += __shfl_xor(lsum, 16);
     lsum += __shfl_xor(lsum, 32);
-    if (hD < G && kq == 0 && (HG == 1 ? blk == 0 : (blk & 1) == 0)) {
-        wm[wave * G + hD] = m;
-        wl[wave * G + hD] = lsum;
-    }
-    // the wavefront reads back only its own probabilities: a wavefront-scope fence suffices
+    if (head_lane) wl[wave * G + hD] = lsum;
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 
-    // unnormalised P.V in fp32, relative to the wavefront maximum
-    float acc[G][8];
+    // P.V (unnormalised, relative to M) on the matrix cores
+    v4f dacc[HS][8];
 #pragma unroll
-    for (int h = 0; h < G; ++h)
+    for (int hs = 0; hs < HS; ++hs)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
+        for (int e = 0; e < 8; ++e) dacc[hs][e] = v4f{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int i = 0; i < RPL; ++i) {
         const int rr = wave * RW + i * 4 + rg;
         float f[8];
         unpack8(vr[i], f);
 #pragma unroll
-        for (int h = 0; h < G; ++h) {
-            const float ph = xf[h * TILE_A + rr];
+        for (int hs = 0; hs < HS; ++hs) {
+            const int h = hs * 4 + (lane & 3);
+            const float pa = h < G ? xf[h * TILE_A + rr] : 0.f;
 #pragma unroll
-            for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(ph, f[e], acc[h][e]);
+            for (int e = 0; e < 8; ++e) dacc[hs][e] = __builtin_amdgcn_mfma_f32_4x4x1f32(pa, f[e], dacc[hs][e], 0, 0, 0);
         }
     }
+    float acc[G][8];
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-        float4 *dst = (float4 *)(wo + ((wave * 4 + rg) * G + h) * D + sub * 8);
-        dst[0] = make_float4(acc[h][0], acc[h][1], acc[h][2], acc[h][3]);
-        dst[1] = make_float4(acc[h][4], acc[h][5], acc[h][6], acc[h][7]);
+    for (int h = 0; h < G; ++h)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            acc[h][e] = dacc[h / 4][e][h % 4];
+            if (OGR == 2) acc[h][e] += __shfl_xor(acc[h][e], 32);
+        }
+    if (rg < OGR) {
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+            float4 *dst = (float4 *)(wo + (rg * G + h) * D + sub * 8);
+            dst[0] = make_float4(acc[h][0], acc[h][1], acc[h][2], acc[h][3]);
+            dst[1] = make_float4(acc[h][4], acc[h][5], acc[h][6], acc[h][7]);
+        }
     }
     __syncthreads();
 
-    // merge of the four wavefronts: tile maximum, factors, sums, outputs, per-chunk masses
+    // tile partials: maximum, sum, P.V and per-chunk masses, all relative to M
     const size_t pidx = ((size_t)b * g.nA + ai) * g.n_tiles_a + tile;
-    if (tid < WAVES * G) {
-        const int h = tid % G, w = tid / G;
-        double M = wm[h];
-#pragma unroll
-        for (int w2 = 1; w2 < WAVES; ++w2) M = fmax(M, wm[w2 * G + h]);
-        const double mw = wm[w * G + h];
-        wf[tid] = (M == -INFINITY || mw == -INFINITY) ? 0.0 : exp(mw - M);
-        if (w == 0) s.pa_m[pidx * G + h] = M;
-    }
-    __syncthreads();
     if (tid < G) {
-        double L = 0.0;
+        double M = wm[tid], L = 0.0;
 #pragma unroll
-        for (int w = 0; w < WAVES; ++w) L += wl[w * G + tid] * wf[w * G + tid];
+        for (int w = 1; w < WAVES; ++w) M = fmax(M, wm[w * G + tid]);
+#pragma unroll
+        for (int w = 0; w < WAVES; ++w) L += wl[w * G + tid];
+        s.pa_m[pidx * G + tid] = M;
         s.pa_l[pidx * G + tid] = L;
     }
     for (int idx = tid; idx < G * D; idx += NT) {
-        const int h = idx / D;
         float o = 0.f;
 #pragma unroll
         for (int w = 0; w < WAVES; ++w) {
-            float ow = 0.f;
+            const float *ww = (const float *)&kst[w][0];
 #pragma unroll
-            for (int r4 = 0; r4 < 4; ++r4) ow += wo[(w * 4 + r4) * G * D + idx];
-            o += ow * (float)wf[w * G + h];
+            for (int r4 = 0; r4 < OGR; ++r4) o += ww[r4 * G * D + idx];
         }
         s.pa_o[pidx * G * D + idx] = o;
     }
-    // per-chunk mass of this tile (Eq. 2 restricted to the tile): 16 lanes per (head, chunk)
-    // entry, each summing a fixed stride of rows, then a DPP sum (fixed order)
     const int c_first = t0 / g.cl;
+    if (fast_mass) {
+        if (tid < G * g.maxc) {
+            const int h = tid / g.maxc, c = c_first + (tid - h * g.maxc);
+            double acc2 = 0.0;
+#pragma unroll
+            for (int w = 0; w < WAVES; ++w) {
+                const int r0 = t0 + w * RW;
+                if (r0 >= c * g.cl && r0 < (c + 1) * g.cl && r0 < g.Ta) acc2 += wl[w * G + h];
+            }
+            s.pa_mass[pidx * G * g.maxc + tid] = acc2;
+        }
+        return;
+    }
+    // general chunk lengths: 16 lanes per (head, chunk) entry sum a fixed stride of rows, then a
+    // DPP sum (fixed order)
     for (int base = 0; base < G * g.maxc * 16; base += NT) {
         const int idx = base + tid, grp = idx >> 4, k = idx & 15;
         const bool valid = grp < G * g.maxc;
@@ -305,7 +371,7 @@ __global__ __launch_bounds__(NT) void anchor_attn_kernel(Geometry g, Tiers t, St
         if (valid) {
             const int h = grp / g.maxc, c = c_first + (grp - h * g.maxc);
             const int r0 = max(c * g.cl, t0), r1 = min(min((c + 1) * g.cl, t0 + TILE_A), g.Ta);
-            for (int rr = r0 + k; rr < r1; rr += 16) acc2 += xs[h * TILE_A + (rr - t0)] * wf[((rr - t0) / RW) * G + h];
+            for (int rr = r0 + k; rr < r1; rr += 16) acc2 += xs[h * TILE_A + (rr - t0)];
         }
         acc2 = sum16(acc2);
         if (valid && k == 0) s.pa_mass[pidx * G * g.maxc + grp] = acc2;
