@@ -116,14 +116,16 @@ typedef struct {
     int64_t timed_steps;
     double t_anchor_ms;        /* anchor attention + chunk mass                                 */
     double t_select_ms;        /* anchor merge, chunk scores, top-k, residency, slots           */
-    double t_tidal_fixed_ms;   /* fixed heads, tidal kept rows and resident complements; on the
-                                  default path also the recall of new complements (read from
-                                  pinned host memory and attended in the same launch)           */
-    double t_new_ms;           /* WNW_F_RECALL_MEMCPY: attention over complements copied this step */
+    double t_tidal_fixed_ms;   /* fixed heads, tidal kept rows, complements already on the device;
+                                  with same-step timing (default recall) also the recall and the
+                                  attention over the recalled complements, in the same launch   */
+    double t_new_ms;           /* WNW_F_RECALL_MEMCPY with same-step timing: attention over the
+                                  complements copied this step                                  */
     double t_combine_ms;       /* merge of the tidal/fixed partial results                      */
     double t_step_ms;          /* whole step on the caller's stream                             */
-    double t_recall_ms;        /* WNW_F_RECALL_MEMCPY or WNW_F_SELECT_NEXT_STEP: recall on the
-                                  side stream                                                    */
+    double t_recall_ms;        /* the recall: the launch that carries it (same-step timing), the
+                                  copy kernel on the side stream (next-step timing) or the
+                                  host-issued copies (WNW_F_RECALL_MEMCPY)                      */
 } wnw_stats;
 
 /* Create a context for one batch of caches.
@@ -144,7 +146,9 @@ wnw_status wnw_init_cache(const wnw_config *cfg, const void *k_dev, const void *
  * complement, then waits for the copies.  Exactly once per context, after wnw_init_cache. */
 wnw_status wnw_set_roles(wnw_ctx *ctx, const uint8_t *roles, const float *prefill_scores);
 
-/* One decode step (Eq. 2 and "Dynamic Chunk Selection"), enqueued on hip_stream.
+/* One decode step (Eq. 2 and "Dynamic Chunk Selection"), enqueued on hip_stream (with
+ * WNW_F_SELECT_NEXT_STEP or WNW_F_RECALL_MEMCPY the recall runs on an internal stream, joined by
+ * events).
  *   q_dev             device bf16 [B][L][H_q][d]
  *   out_dev           device fp32 [B][L][H_q][d]     attention output of every q-head
  *   chunk_scores_dev  device fp32 [B][n_chunks]      this step's chunk scores

@@ -34,9 +34,9 @@ thread_local std::string t_err = "no error";
 enum State { CREATED = 0, READY = 1, FAILED = 2 };
 
 // Timing events of one step.  e[] on the caller's stream: 0 start, 1 after anchor attention,
-// 2 after merge + selection, 3 after the tidal/fixed kernel, 4 after the attention over copied
-// complements (host-waited recall path only), 5 after the final merge.  r[] on the side stream
-// around the host-waited copies.
+// 2 after merge + selection, 3 after the tidal/fixed kernel, 4 once the complements recalled
+// this step have been attended to (same-step timing), 5 after the final merge.  r[] on the side
+// stream around the recall.
 struct StepEvents {
     hipEvent_t e[6];
     hipEvent_t r[2];
@@ -252,7 +252,6 @@ wnw_status issue_copies(wnw_ctx *c, hipStream_t st)
 
 wnw_status harvest_timing(wnw_ctx *c)
 {
-    const bool memcpy_path = c->cfg.flags & WNW_F_RECALL_MEMCPY;
     for (auto &ev : c->pending) {
         float ms;
         HIPCHECK(c, hipEventSynchronize(ev.e[5]));
@@ -262,11 +261,9 @@ wnw_status harvest_timing(wnw_ctx *c)
             HIPCHECK(c, hipEventElapsedTime(&ms, ev.e[from[i]], ev.e[to[i]]));
             c->t_acc[i] += ms;
         }
-        if (memcpy_path || c->g.next_step) {
-            HIPCHECK(c, hipEventSynchronize(ev.r[1]));
-            HIPCHECK(c, hipEventElapsedTime(&ms, ev.r[0], ev.r[1]));
-            c->t_acc[6] += ms;
-        }
+        HIPCHECK(c, hipEventSynchronize(ev.r[1]));
+        HIPCHECK(c, hipEventElapsedTime(&ms, ev.r[0], ev.r[1]));
+        c->t_acc[6] += ms;
         c->timed_steps++;
         c->spare.push_back(ev);
     }
@@ -582,11 +579,13 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, float *out, float *sco
     } else if (!memcpy_path) {
         MARK(2);
         // (3) + (4) in one launch: its first work-groups copy the complements listed for recall
-        // from mapped pinned memory into their slots and attend to them as they arrive, the
-        // others run the fixed heads and the tidal rows already on the device.  The slots being
-        // written were freed by this step's select kernel; every kernel that could still read
-        // them (the previous step's) precedes it on this stream.
+        // from mapped pinned memory into their slots and attend to them, the others run the fixed
+        // heads and the tidal rows already on the device.  The slots being written were freed by
+        // this step's select kernel; every kernel that could still read them (the previous
+        // step's) precedes it on this stream.
+        if (timing) HIPCHECK(c, hipEventRecord(ev.r[0], s0));
         HIPCHECK(c, launch_tidal_fixed(g, c->t, c->s, q, true, s0));
+        if (timing) HIPCHECK(c, hipEventRecord(ev.r[1], s0));
         MARK(3);
         MARK(4);
     } else {

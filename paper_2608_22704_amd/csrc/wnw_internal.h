@@ -96,8 +96,9 @@ inline size_t select_shared_bytes(const Geometry &g)
 {
     return (size_t)g.nc * (SCORE_PARTS * 8 + 4 + 8 * 4) + (size_t)g.n_slots * 5 * 4;
 }
-// Fixed heads, tidal kept rows and resident complements; with `recall`, also the copy of the
-// complements listed for recall from mapped pinned memory, attended to as they arrive.
+// Fixed heads, tidal kept rows and the tidal complements already in their slots; with `recall`
+// (same-step timing), also the copy of the complements listed for recall from mapped pinned
+// memory into their slots and the attention over them.
 hipError_t launch_tidal_fixed(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, bool recall,
                               hipStream_t st);
 // Next-step timing: copy of the complements listed for recall from mapped pinned memory into

@@ -11,9 +11,11 @@
 //   scores          per chunk: fixed-order sum over anchor q-heads / chunk length (mean).
 //   select          one work-group per sequence: top-k by (score desc, id asc), streaks,
 //                   residency, slot assignment, kept/new lists.
-//   recall          copies newly resident complements from mapped pinned host memory.
-//   subset_static   tidal and fixed heads over their kept rows + text (fp32 logits).
-//   subset_slots    tidal heads over resident complements (kept list, then new list).
+//   tidal_fixed     tidal and fixed heads over their kept rows + text, and tidal heads over the
+//                   complements already in their slots (fp32 logits).
+//                   With same-step timing its first work-groups recall: they copy newly resident
+//                   complements from mapped pinned host memory into their slots and attend to them.
+//   recall_copy     next-step recall (side stream): the copy only.
 //   subset_combine  merge of a tidal/fixed head's partials.
 //
 // Layout inside a tile: 16 lanes share one 256-byte key row (8 bf16 = 16 bytes each), so one
@@ -720,111 +722,196 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
 // recall path, where to copy them.
 struct RowPtr {
     const uint16_t *k, *v;
-    uint16_t *kd = nullptr, *vd = nullptr;
+};
+
+// One work-group = 4 wavefronts; wavefront w owns rows [w * 4 * RPL, (w + 1) * 4 * RPL) of the
+// tile's row map, in sub-tiles of 32 rows (RPL = 8 or 16).  Rows are loaded fully coalesced
+// (16 lanes per 256-byte row).
+//
+// Logits (fp32, exact bf16 products) on v_mfma_f32_4x4x4_16b_bf16: lane l = 4*blk + i feeds
+// A_blk[i][0..3] and B_blk[0..3][i], and D_blk[i][j] lands in lane 4*blk + j, register i.
+// Block blk = 8*dh + kb takes keys 4*kb .. 4*kb + 3 of the sub-tile over dimension half dh
+// (sixteen instructions of four dimensions each); one cross-half add completes the dot
+// products.  A comes from the wavefront's K rows staged in LDS (16-byte units swizzled by row),
+// B from q staged in LDS (rows padded to 272 bytes so that the eight (head, half) reads of an
+// instruction hit distinct banks).  P.V runs on v_mfma_f32_4x4x1 as in the anchor kernel.
+// Shared memory of one subset tile; one instance per work-group, whichever row map it runs.
+template <int G, int RPL>
+struct SubsetSmem {
+    static constexpr int NR = 4 * RPL, HS = (G + 3) / 4, QS = 136;
+    uint4 kst[WAVES][NR * 16];                // K rows, then the P.V partials of each wavefront
+    uint16_t qs[HS * 4 * QS];                 // q, rows padded to 272 bytes
+    float xf[G * WAVES * NR];                 // probabilities
+    float wm[WAVES * G], wl[WAVES * G];
 };
 
 template <int G, int RPL, class RowMap>
-__device__ inline void subset_tile(const uint16_t *__restrict__ qh, const RowMap &map, float *pm, float *pl, float *po)
+__device__ inline void subset_tile(const uint16_t *__restrict__ qh, const RowMap &map, float *pm, float *pl, float *po,
+                                   SubsetSmem<G, RPL> &sm)
 {
+    typedef float v4f __attribute__((ext_vector_type(4)));
+    typedef short v4s __attribute__((ext_vector_type(4)));
+    constexpr int NR = 4 * RPL;               // rows per wavefront
+    constexpr int NSUB = NR / 32;             // 32-row sub-tiles per wavefront
+    constexpr int HS = (G + 3) / 4;           // sets of 4 heads
+    constexpr int OGR = G <= 4 ? 4 : 2;       // row groups kept in the P.V partial store
+    constexpr int QS = 136;                   // padded q row, in uint16
+    static_assert(NR % 32 == 0, "wavefront rows come in 32-row sub-tiles");
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, sub = lane & 15, rg = lane >> 4;
-    __shared__ float wm[WAVES * G], wl[WAVES * G];
-    __shared__ float wo[WAVES * G * D];
+    const int j4 = lane & 3, kb = (lane >> 2) & 7, dh = lane >> 5;
+    auto &kst = sm.kst;
+    uint16_t *qs = sm.qs;
+    float *xf = sm.xf, *wm = sm.wm, *wl = sm.wl;
+    float *wo = (float *)&kst[wave][0];
 
-    uint4 qr[G];
-#pragma unroll
-    for (int h = 0; h < G; ++h) qr[h] = *(const uint4 *)(qh + h * D + sub * 8);
+    for (int i = tid; i < HS * 4 * (D / 8); i += NT) {
+        const int h = i / (D / 8), u = i - h * (D / 8);
+        *(uint4 *)(qs + h * QS + u * 8) = h < G ? *(const uint4 *)(qh + h * D + u * 8) : make_uint4(0, 0, 0, 0);
+    }
     uint4 kr[RPL], vr[RPL];
     bool ok[RPL];
 #pragma unroll
     for (int i = 0; i < RPL; ++i) {
-        const RowPtr rp = map.row(wave * 4 * RPL + i * 4 + rg);
+        const RowPtr rp = map.row(wave * NR + i * 4 + rg);
         ok[i] = rp.k != nullptr;
         kr[i] = ok[i] ? *(const uint4 *)(rp.k + sub * 8) : make_uint4(0, 0, 0, 0);
     }
 #pragma unroll
     for (int i = 0; i < RPL; ++i) {
-        const RowPtr rp = map.row(wave * 4 * RPL + i * 4 + rg);
+        const RowPtr rp = map.row(wave * NR + i * 4 + rg);
         vr[i] = ok[i] ? *(const uint4 *)(rp.v + sub * 8) : make_uint4(0, 0, 0, 0);
     }
-    float qf[G][8];
-#pragma unroll
-    for (int h = 0; h < G; ++h) unpack8(qr[h], qf[h]);
-
     if constexpr (RowMap::copies) {
+        // rows read from host memory are also written to their device slot on the way
 #pragma unroll
         for (int i = 0; i < RPL; ++i)
             if (ok[i]) {
-                const RowPtr rp = map.row(wave * 4 * RPL + i * 4 + rg);
-                *(uint4 *)(rp.kd + sub * 8) = kr[i];
-                *(uint4 *)(rp.vd + sub * 8) = vr[i];
+                const int r = wave * NR + i * 4 + rg;
+                *(uint4 *)(map.kdst(r) + sub * 8) = kr[i];
+                *(uint4 *)(map.vdst(r) + sub * 8) = vr[i];
             }
     }
-    float x[RPL][G];
 #pragma unroll
     for (int i = 0; i < RPL; ++i) {
-        float f[8];
-        unpack8(kr[i], f);
+        const int r = i * 4 + rg;
+        kst[wave][r * 16 + (sub ^ (r & 15))] = kr[i];
+    }
+    __syncthreads();   // q staged; each wavefront's K rows are its own
+
+    // logits: key sub*32 + 4*kb + i, head hs*4 + j4, register i of lg[sub][hs]
+    v4f lg[NSUB][HS];
 #pragma unroll
-        for (int h = 0; h < G; ++h) {
-            float acc = 0.f;
+    for (int sb = 0; sb < NSUB; ++sb)
 #pragma unroll
-            for (int e = 0; e < 8; ++e) acc = fmaf(qf[h][e], f[e], acc);
-            acc = sum16(acc);
-            x[i][h] = ok[i] ? acc * SCALE_F : -INFINITY;
+        for (int hs = 0; hs < HS; ++hs) lg[sb][hs] = v4f{0.f, 0.f, 0.f, 0.f};
+    const int rA = 4 * kb + j4;               // A row of this lane within a sub-tile
+#pragma unroll
+    for (int p8 = 0; p8 < 8; ++p8) {
+        const int unit = 8 * dh + p8;
+        uint4 qb[HS];
+#pragma unroll
+        for (int hs = 0; hs < HS; ++hs) qb[hs] = *(const uint4 *)(qs + (hs * 4 + j4) * QS + unit * 8);
+#pragma unroll
+        for (int sb = 0; sb < NSUB; ++sb) {
+            const int r = sb * 32 + rA;
+            const uint4 ka = kst[wave][r * 16 + (unit ^ (r & 15))];
+            const v4s a0 = __builtin_bit_cast(v4s, make_uint2(ka.x, ka.y));
+            const v4s a1 = __builtin_bit_cast(v4s, make_uint2(ka.z, ka.w));
+#pragma unroll
+            for (int hs = 0; hs < HS; ++hs) {
+                lg[sb][hs] = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(a0, __builtin_bit_cast(v4s, make_uint2(qb[hs].x, qb[hs].y)),
+                                                                    lg[sb][hs], 0, 0, 0);
+                lg[sb][hs] = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(a1, __builtin_bit_cast(v4s, make_uint2(qb[hs].z, qb[hs].w)),
+                                                                    lg[sb][hs], 0, 0, 0);
+            }
         }
     }
-    float m[G], l[G];
+    // complete the dot products across the two dimension halves; scale and mask
+    float m[HS], l[HS];
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-        float mm = x[0][h];
+    for (int hs = 0; hs < HS; ++hs) {
+        const bool hv = hs * 4 + j4 < G;
+        float mm = -INFINITY;
 #pragma unroll
-        for (int i = 1; i < RPL; ++i) mm = fmaxf(mm, x[i][h]);
+        for (int sb = 0; sb < NSUB; ++sb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                float x = lg[sb][hs][i];
+                x += __shfl_xor(x, 32);
+                const int r = wave * NR + sb * 32 + 4 * kb + i;
+                x = (hv && map.row(r).k != nullptr) ? x * SCALE_F : -INFINITY;
+                lg[sb][hs][i] = x;
+                mm = fmaxf(mm, x);
+            }
+        mm = fmaxf(mm, __shfl_xor(mm, 4));
+        mm = fmaxf(mm, __shfl_xor(mm, 8));
         mm = fmaxf(mm, __shfl_xor(mm, 16));
-        mm = fmaxf(mm, __shfl_xor(mm, 32));
-        m[h] = mm;
         float ll = 0.f;
 #pragma unroll
-        for (int i = 0; i < RPL; ++i) {
-            const float pv = (mm == -INFINITY) ? 0.f : __expf(x[i][h] - mm);
-            x[i][h] = pv;
-            ll += pv;
-        }
+        for (int sb = 0; sb < NSUB; ++sb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float pv = (mm == -INFINITY) ? 0.f : __expf(lg[sb][hs][i] - mm);
+                lg[sb][hs][i] = pv;
+                ll += pv;
+            }
+        ll += __shfl_xor(ll, 4);
+        ll += __shfl_xor(ll, 8);
         ll += __shfl_xor(ll, 16);
-        ll += __shfl_xor(ll, 32);
-        l[h] = ll;
+        m[hs] = mm;
+        l[hs] = ll;
+        if (hv && dh == 0) {
+#pragma unroll
+            for (int sb = 0; sb < NSUB; ++sb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) xf[(hs * 4 + j4) * (WAVES * NR) + wave * NR + sb * 32 + 4 * kb + i] = lg[sb][hs][i];
+        }
+        if (hv && lane < 4) {
+            wm[wave * G + hs * 4 + j4] = mm;
+            wl[wave * G + hs * 4 + j4] = ll;
+        }
+    }
+    // each wavefront reads back only its own probabilities
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+    // P.V (unnormalised, relative to the wavefront maximum)
+    v4f dacc[HS][8];
+#pragma unroll
+    for (int hs = 0; hs < HS; ++hs)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) dacc[hs][e] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < RPL; ++i) {
+        const int rr = wave * NR + i * 4 + rg;
+        float f[8];
+        unpack8(vr[i], f);
+#pragma unroll
+        for (int hs = 0; hs < HS; ++hs) {
+            const int h = hs * 4 + j4;
+            const float pa = h < G ? xf[h * (WAVES * NR) + rr] : 0.f;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) dacc[hs][e] = __builtin_amdgcn_mfma_f32_4x4x1f32(pa, f[e], dacc[hs][e], 0, 0, 0);
+        }
     }
     float acc[G][8];
 #pragma unroll
     for (int h = 0; h < G; ++h)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
-#pragma unroll
-    for (int i = 0; i < RPL; ++i) {
-        float f[8];
-        unpack8(vr[i], f);
-#pragma unroll
-        for (int h = 0; h < G; ++h)
-#pragma unroll
-            for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(x[i][h], f[e], acc[h][e]);
-    }
-#pragma unroll
-    for (int h = 0; h < G; ++h)
-#pragma unroll
         for (int e = 0; e < 8; ++e) {
-            acc[h][e] += __shfl_xor(acc[h][e], 16);
-            acc[h][e] += __shfl_xor(acc[h][e], 32);
+            acc[h][e] = dacc[h / 4][e][h % 4];
+            if (OGR == 2) acc[h][e] += __shfl_xor(acc[h][e], 32);
         }
-    if (rg == 0)
-#pragma unroll
-        for (int h = 0; h < G; ++h)
-#pragma unroll
-            for (int e = 0; e < 8; ++e) wo[(wave * G + h) * D + sub * 8 + e] = acc[h][e];
-    if (lane == 0)
+    // the K region of this wavefront is dead: it takes the P.V partials
+    if (rg < OGR) {
 #pragma unroll
         for (int h = 0; h < G; ++h) {
-            wm[wave * G + h] = m[h];
-            wl[wave * G + h] = l[h];
+            float4 *dst = (float4 *)(wo + (rg * G + h) * D + sub * 8);
+            dst[0] = make_float4(acc[h][0], acc[h][1], acc[h][2], acc[h][3]);
+            dst[1] = make_float4(acc[h][4], acc[h][5], acc[h][6], acc[h][7]);
         }
+    }
     __syncthreads();
     for (int idx = tid; idx < G * D; idx += NT) {
         const int h = idx / D;
@@ -835,7 +922,13 @@ __device__ inline void subset_tile(const uint16_t *__restrict__ qh, const RowMap
 #pragma unroll
         for (int w = 0; w < WAVES; ++w) {
             const float mw = wm[w * G + h];
-            if (mw > -INFINITY) o += wo[w * G * D + idx] * __expf(mw - M);
+            if (mw > -INFINITY) {
+                const float *ww = (const float *)&kst[w][0];
+                float ow = 0.f;
+#pragma unroll
+                for (int r4 = 0; r4 < OGR; ++r4) ow += ww[r4 * G * D + idx];
+                o += ow * __expf(mw - M);
+            }
         }
         po[idx] = o;
     }
@@ -852,7 +945,7 @@ __device__ inline void subset_tile(const uint16_t *__restrict__ qh, const RowMap
         pm[tid] = M;
         pl[tid] = L;
     }
-    __syncthreads();   // the shared partials may be reused by the next tile of this work-group
+    __syncthreads();   // the shared buffers may be reused by the next tile of this work-group
 }
 
 struct StaticRows {
@@ -883,27 +976,30 @@ struct SlotRows {
     }
 };
 
-// Rows of one recalled unit (a tidal head's complement of one chunk): read from the mapped
-// pinned host block, copied through to the device slot on the way.
+// Rows of one recalled complement block (a tidal head's complement of one chunk): comp_max K rows,
+// then comp_max V rows, of which the first nrows are valid.  They are read from the mapped pinned
+// host block and copied through to the device slot on the way.
 struct RecallRows {
     static constexpr bool copies = true;
-    const uint16_t *src;     // host block: comp_max K rows then comp_max V rows
+    const uint16_t *src;     // host block
     uint16_t *dst;           // device slot block, same layout
     int nrows, comp_max;
     __device__ RowPtr row(int r) const
     {
         if (r >= nrows) return {nullptr, nullptr};
-        const size_t ko = (size_t)r * D, vo = (size_t)(comp_max + r) * D;
-        return {src + ko, src + vo, dst + ko, dst + vo};
+        const uint16_t *k = src + (size_t)r * D;
+        return {k, k + (size_t)comp_max * D};
     }
+    __device__ uint16_t *kdst(int r) const { return dst + (size_t)r * D; }
+    __device__ uint16_t *vdst(int r) const { return dst + (size_t)(comp_max + r) * D; }
 };
 
 constexpr int RPL_S = TILE_S / (4 * WAVES);   // 8
-constexpr int RECALL_WGS = 64;                // work-groups that recall (fills the host link)
+constexpr int RECALL_WGS = 64;                // work-groups that recall (they fill the host link)
 
 template <int G>
 __device__ inline void static_tile(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, int tile,
-                                   int hi, int b)
+                                   int hi, int b, SubsetSmem<G, RPL_S> &sm)
 {
     const bool tidal = hi < g.nT;
     const int idx = tidal ? hi : hi - g.nT;
@@ -912,13 +1008,13 @@ __device__ inline void static_tile(const Geometry &g, const Tiers &t, const Step
     const StaticRows map{(tidal ? t.tK : t.fK) + hb, (tidal ? t.tV : t.fV) + hb, tile * TILE_S, g.Rs};
     const uint16_t *qh = q + (((size_t)b * g.L + l) * g.Hq + (size_t)kv * G) * D;
     const size_t p = ((size_t)b * (g.nT + g.nF) + hi) * g.np + tile;
-    subset_tile<G, RPL_S>(qh, map, s.ps_m + p * G, s.ps_l + p * G, s.ps_o + p * G * D);
+    subset_tile<G, RPL_S>(qh, map, s.ps_m + p * G, s.ps_l + p * G, s.ps_o + p * G * D, sm);
 }
 
 // Slot group `grp` of list `which` (0 kept, 1 new) of tidal head ti; epg entries per group.
 template <int G, int RPL>
 __device__ inline void slot_group(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, int grp,
-                                  int ti, int b, int which, int epg)
+                                  int ti, int b, int which, int epg, SubsetSmem<G, RPL> &sm)
 {
     const int cnt = s.counts[b * 2 + which];
     if (grp * epg >= cnt) return;
@@ -938,15 +1034,15 @@ __device__ inline void slot_group(const Geometry &g, const Tiers &t, const StepB
     const SlotRows map{kbase, nrows, n_entries, g.comp_max};
     const uint16_t *qh = q + (((size_t)b * g.L + l) * g.Hq + (size_t)kv * G) * D;
     const size_t p = ((size_t)b * (g.nT + g.nF) + ti) * g.np + g.n_tiles_s + (which ? g.ng_kept : 0) + grp;
-    subset_tile<G, RPL>(qh, map, s.ps_m + p * G, s.ps_l + p * G, s.ps_o + p * G * D);
+    subset_tile<G, RPL>(qh, map, s.ps_m + p * G, s.ps_l + p * G, s.ps_o + p * G * D, sm);
 }
 
 // Recall work-group w of nw: walks the units (sequence, new entry, tidal head); each unit's
-// complement block is read from mapped pinned memory, copied to its slot and attended to in
-// the same pass.  The number of work-groups, not their width, bounds the reads in flight.
+// complement block is read from mapped pinned memory, copied to its slot and attended to in the
+// same pass.  The number of work-groups, not their width, bounds the host reads in flight.
 template <int G, int RPL>
 __device__ inline void recall_units(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, int w,
-                                    int nw)
+                                    int nw, SubsetSmem<G, RPL> &sm)
 {
     int total = 0;
     for (int b = 0; b < g.B; ++b) total += s.counts[b * 2 + 1] * g.nT;
@@ -970,32 +1066,41 @@ __device__ inline void recall_units(const Geometry &g, const Tiers &t, const Ste
         const uint16_t *qh = q + (((size_t)b * g.L + l) * g.Hq + (size_t)kv * G) * D;
         const size_t p = ((size_t)b * (g.nT + g.nF) + ti) * g.np + g.n_tiles_s + g.ng_kept + e;
         const RecallRows map{src, dst, nr, g.comp_max};
-        subset_tile<G, RPL>(qh, map, s.ps_m + p * G, s.ps_l + p * G, s.ps_o + p * G * D);
+        subset_tile<G, RPL>(qh, map, s.ps_m + p * G, s.ps_l + p * G, s.ps_o + p * G * D, sm);
     }
 }
 
-// Fixed heads, tidal kept rows, tidal complements resident since the last step, and (first
-// n_recall work-groups) recall + attention of the complements that became resident this step.
-// One launch: the recall work-groups hold the host link busy while the others stream HBM.
-template <int G, int RPLK, int RPLN>
-__global__ __launch_bounds__(NT) void tidal_fixed_kernel(Geometry g, Tiers t, StepBuffers s, const uint16_t *__restrict__ q,
-                                                         int n_recall)
+// Fixed heads, tidal kept rows and tidal complements already in their slots: static tiles
+// first, then groups of kept entries.  With REC (same-step timing), the first RECALL_WGS
+// work-groups also copy the complements listed for recall from mapped pinned memory into their
+// slots and attend to them: the step is bound by the host link then, and the copies start with
+// the launch.  Without REC the kernel keeps to its lean register budget.
+template <int G, int RPLK, bool REC>
+__global__ __launch_bounds__(NT, REC ? (RPLK == RPL_S ? 2 : 1) : (RPLK == RPL_S ? (G <= 4 ? 4 : 3) : 2)) void tidal_fixed_kernel(
+    Geometry g, Tiers t, StepBuffers s, const uint16_t *__restrict__ q)
 {
+    union Smem {
+        SubsetSmem<G, RPL_S> st;
+        SubsetSmem<G, RPLK> sl;
+    };
+    __shared__ Smem sm;   // one block for whichever path this work-group runs
     int bid = blockIdx.x;
-    if (bid < n_recall) {
-        recall_units<G, RPLN>(g, t, s, q, bid, n_recall);
-        return;
+    if constexpr (REC) {
+        if (bid < RECALL_WGS) {
+            recall_units<G, RPLK>(g, t, s, q, bid, RECALL_WGS, sm.sl);
+            return;
+        }
+        bid -= RECALL_WGS;
     }
-    bid -= n_recall;
     const int nh = g.nT + g.nF, n_static = g.n_tiles_s * nh * g.B;
     if (bid < n_static) {
         const int tile = bid % g.n_tiles_s, rest = bid / g.n_tiles_s;
-        static_tile<G>(g, t, s, q, tile, rest % nh, rest / nh);
+        static_tile<G>(g, t, s, q, tile, rest % nh, rest / nh, sm.st);
         return;
     }
     bid -= n_static;
     const int grp = bid % g.ng_kept, rest = bid / g.ng_kept;
-    slot_group<G, RPLK>(g, t, s, q, grp, rest % g.nT, rest / g.nT, 0, g.sg);
+    slot_group<G, RPLK>(g, t, s, q, grp, rest % g.nT, rest / g.nT, 0, g.sg, sm.sl);
 }
 
 // Next-step timing: copy only.  Work-group w of the grid walks the units (sequence, new entry,
@@ -1020,9 +1125,10 @@ __global__ __launch_bounds__(NT) void recall_copy_kernel(Geometry g, Tiers t, St
 
 // Complements copied by hipMemcpyAsync (host-waited recall path): one entry per work-group.
 template <int G, int RPL>
-__global__ __launch_bounds__(NT) void new_slots_kernel(Geometry g, Tiers t, StepBuffers s, const uint16_t *__restrict__ q)
+__global__ __launch_bounds__(NT, RPL == RPL_S ? 4 : 2) void new_slots_kernel(Geometry g, Tiers t, StepBuffers s, const uint16_t *__restrict__ q)
 {
-    slot_group<G, RPL>(g, t, s, q, blockIdx.x, blockIdx.y, blockIdx.z, 1, 1);
+    __shared__ SubsetSmem<G, RPL> sm;
+    slot_group<G, RPL>(g, t, s, q, blockIdx.x, blockIdx.y, blockIdx.z, 1, 1, sm);
 }
 
 // Merge of one tidal/fixed KV-head's partials (static tiles, kept groups, new groups):
@@ -1177,15 +1283,18 @@ struct TidalFixedL {
     static hipError_t run(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, bool recall,
                           hipStream_t st)
     {
-        const int n_recall = (recall && g.k > 0 && g.chunk_elems > 0 && g.nT > 0) ? RECALL_WGS : 0;
-        const long long n = n_recall + (long long)g.n_tiles_s * (g.nT + g.nF) * g.B + (long long)g.ng_kept * g.nT * g.B;
+        recall = recall && g.nT > 0 && g.k > 0 && g.comp_max > 0;
+        const long long n = (recall ? RECALL_WGS : 0) + (long long)g.n_tiles_s * (g.nT + g.nF) * g.B +
+                            (long long)g.ng_kept * g.nT * g.B;
         if (n == 0) return hipSuccess;
-        if (g.slot_tile == TILE_S)
-            hipLaunchKernelGGL((tidal_fixed_kernel<G, TILE_S / 16, TILE_S / 16>), dim3((unsigned)n), dim3(NT), 0, st, g, t,
-                               s, q, n_recall);
-        else
-            hipLaunchKernelGGL((tidal_fixed_kernel<G, TILE_S / 8, TILE_S / 8>), dim3((unsigned)n), dim3(NT), 0, st, g, t,
-                               s, q, n_recall);
+        const dim3 grid((unsigned)n), block(NT);
+        if (g.slot_tile == TILE_S) {
+            if (recall) hipLaunchKernelGGL((tidal_fixed_kernel<G, TILE_S / 16, true>), grid, block, 0, st, g, t, s, q);
+            else hipLaunchKernelGGL((tidal_fixed_kernel<G, TILE_S / 16, false>), grid, block, 0, st, g, t, s, q);
+        } else {
+            if (recall) hipLaunchKernelGGL((tidal_fixed_kernel<G, TILE_S / 8, true>), grid, block, 0, st, g, t, s, q);
+            else hipLaunchKernelGGL((tidal_fixed_kernel<G, TILE_S / 8, false>), grid, block, 0, st, g, t, s, q);
+        }
         return hipGetLastError();
     }
 };
