@@ -64,7 +64,7 @@ struct wnw_ctx {
     const int32_t *override_sel = nullptr;
 
     hipStream_t side = nullptr;
-    hipEvent_t ev_sel = nullptr, ev_rec = nullptr;
+    hipEvent_t ev_sel = nullptr, ev_rec = nullptr, ev_nl = nullptr;
     bool rec_pending = false;          // next-step timing: a recall issued on `side` not yet joined
     int32_t *h_newinfo = nullptr;      // pinned: counts [B][2] then new lists [B][k][2]
 
@@ -283,6 +283,7 @@ void free_all(wnw_ctx *c)
     if (c->h_newinfo) (void)hipHostFree(c->h_newinfo);
     if (c->ev_sel) (void)hipEventDestroy(c->ev_sel);
     if (c->ev_rec) (void)hipEventDestroy(c->ev_rec);
+    if (c->ev_nl) (void)hipEventDestroy(c->ev_nl);
     for (auto *v : {&c->pending, &c->spare})
         for (auto &ev : *v) {
             for (auto e : ev.e) (void)hipEventDestroy(e);
@@ -374,8 +375,8 @@ wnw_status wnw_set_roles(wnw_ctx *c, const uint8_t *roles, const float *prefill)
     ALLOC(s.slot_since, B * g.n_slots, "slot ages");
     ALLOC(s.step, B, "step counters");
     ALLOC(s.kept_list, B * g.n_slots * 2, "kept list");
-    ALLOC(s.new_list, B * g.k * 2, "new list");
-    ALLOC(s.counts, B * 2, "counts");
+    ALLOC(s.new_list, 2 * B * g.k * 2, "new lists");   // two, alternating by step
+    ALLOC(s.counts, 2 * B * 2, "counts");
     ALLOC(s.stats, 8, "stats");
 #undef ALLOC
     const size_t host_bytes = B * g.nc * (size_t)g.chunk_elems * sizeof(uint16_t);
@@ -394,6 +395,7 @@ wnw_status wnw_set_roles(wnw_ctx *c, const uint8_t *roles, const float *prefill)
     HIPCHECK(c, hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking));
     HIPCHECK(c, hipEventCreateWithFlags(&c->ev_sel, hipEventDisableTiming));
     HIPCHECK(c, hipEventCreateWithFlags(&c->ev_rec, hipEventDisableTiming));
+    HIPCHECK(c, hipEventCreateWithFlags(&c->ev_nl, hipEventDisableTiming));
 
     std::vector<int32_t> lk;
     lk.insert(lk.end(), c->anchor_lk.begin(), c->anchor_lk.end());
@@ -498,7 +500,7 @@ wnw_status wnw_set_roles(wnw_ctx *c, const uint8_t *roles, const float *prefill)
         HIPCHECK(c, hipMemset(s.slot_since, 0, B * g.n_slots * sizeof(int32_t)));
     }
     HIPCHECK(c, hipMemset(s.step, 0, B * sizeof(int32_t)));
-    HIPCHECK(c, hipMemset(s.counts, 0, B * 2 * sizeof(int32_t)));
+    HIPCHECK(c, hipMemset(s.counts, 0, 2 * B * 2 * sizeof(int32_t)));
     HIPCHECK(c, hipMemset(s.stats, 0, 8 * sizeof(unsigned long long)));
     HIPCHECK(c, hipDeviceSynchronize());
     c->full_k = c->full_v = nullptr;
@@ -526,50 +528,58 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, float *out, float *sco
             ev = c->spare.back();
             c->spare.pop_back();
         } else {
-            for (auto &e : ev.e) HIPCHECK(c, hipEventCreate(&e));
-            for (auto &e : ev.r) HIPCHECK(c, hipEventCreate(&e));
+            // timing only: no system-scope fence (cache write-back and invalidation) on record,
+            // which would slow the kernels that follow and blur the measurement
+            for (auto &e : ev.e) HIPCHECK(c, hipEventCreateWithFlags(&e, hipEventDisableSystemFence));
+            for (auto &e : ev.r) HIPCHECK(c, hipEventCreateWithFlags(&e, hipEventDisableSystemFence));
         }
     }
 #define MARK(i) \
     if (timing) HIPCHECK(c, hipEventRecord(ev.e[i], s0))
 
-    // (1) anchor attention + chunk mass, (2) scores, top-k and residency
+    // The counts and new lists alternate between two buffers by step, so that the next step's
+    // select kernel never rewrites the list a recall still reads (next-step timing).
+    StepBuffers sb = c->s;
+    const int par = (int)(c->steps & 1);
+    sb.counts += (size_t)par * g.B * 2;
+    sb.new_list += (size_t)par * g.B * g.k * 2;
+
+    // (1) anchor attention + chunk mass, (2) scores, top-k and residency.  With next-step
+    // timing the static tidal/fixed tiles (kept rows + text) join the anchor launch.
     MARK(0);
-    HIPCHECK(c, launch_anchor(g, c->t, c->s, q, s0));
+    if (g.next_step)
+        HIPCHECK(c, launch_attention(g, c->t, sb, q, s0));
+    else
+        HIPCHECK(c, launch_anchor(g, c->t, sb, q, s0));
     MARK(1);
-    HIPCHECK(c, launch_anchor_combine(g, c->t, c->s, out, s0));
-    if (c->rec_pending) {
-        // next-step timing: the previous step's recall (on the side stream) reads the new list
-        // that the select kernel rewrites, and fills the slots this step's tidal heads read
-        HIPCHECK(c, hipStreamWaitEvent(s0, c->ev_rec, 0));
-        c->rec_pending = false;
-    }
-    HIPCHECK(c, launch_select(g, c->s, sc, c->override_sel, sel, s0));
+    HIPCHECK(c, launch_anchor_combine(g, c->t, sb, out, s0));
+    HIPCHECK(c, launch_select(g, sb, sc, c->override_sel, sel, s0));
     const bool memcpy_path = c->cfg.flags & WNW_F_RECALL_MEMCPY;
     if (g.next_step) {
-        // Next-step timing: this step's tidal heads read only slots filled before it, so the
-        // copies of the chunks that became resident now run on the side stream, overlapped with
-        // the rest of this step and the anchor attention of the next one.  Their target slots
-        // were free at this step's selection: no kernel on s0 from here on reads them until the
-        // next step has waited for ev_rec.
+        // Next-step timing: the chunks that became resident now are copied on the side stream,
+        // back to back with the previous step's copies, while this step's tidal heads read only
+        // slots filled before it.  The target slots were free at this step's selection, which
+        // follows on s0 every reader of them (up to the previous step's tidal kernel).
         HIPCHECK(c, hipEventRecord(c->ev_sel, s0));
         HIPCHECK(c, hipStreamWaitEvent(c->side, c->ev_sel, 0));
         if (timing) HIPCHECK(c, hipEventRecord(ev.r[0], c->side));
         if (!memcpy_path) {
-            HIPCHECK(c, launch_recall(g, c->t, c->s, c->side));
+            HIPCHECK(c, launch_recall(g, c->t, sb, c->side));
         } else {
-            HIPCHECK(c, hipMemcpyAsync(c->h_newinfo, c->s.counts, g.B * 2 * sizeof(int32_t), hipMemcpyDeviceToHost, c->side));
+            HIPCHECK(c, hipMemcpyAsync(c->h_newinfo, sb.counts, g.B * 2 * sizeof(int32_t), hipMemcpyDeviceToHost, c->side));
             if (g.k)
-                HIPCHECK(c, hipMemcpyAsync(c->h_newinfo + g.B * 2, c->s.new_list, (size_t)g.B * g.k * 2 * sizeof(int32_t),
+                HIPCHECK(c, hipMemcpyAsync(c->h_newinfo + g.B * 2, sb.new_list, (size_t)g.B * g.k * 2 * sizeof(int32_t),
                                            hipMemcpyDeviceToHost, c->side));
-            HIPCHECK(c, hipEventRecord(c->ev_rec, c->side));
+            HIPCHECK(c, hipEventRecord(c->ev_nl, c->side));
         }
+        // this step's tidal heads read the complements the previous step recalled
+        if (c->rec_pending) HIPCHECK(c, hipStreamWaitEvent(s0, c->ev_rec, 0));
         MARK(2);
-        HIPCHECK(c, launch_tidal_fixed(g, c->t, c->s, q, false, s0));
+        HIPCHECK(c, launch_tidal_fixed(g, c->t, sb, q, false, false, s0));
         MARK(3);
         MARK(4);
         if (memcpy_path) {
-            HIPCHECK(c, hipEventSynchronize(c->ev_rec));
+            HIPCHECK(c, hipEventSynchronize(c->ev_nl));
             wnw_status r = issue_copies(c, c->side);
             if (r != WNW_OK) return r;
         }
@@ -584,19 +594,19 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, float *out, float *sco
         // this step's select kernel; every kernel that could still read them (the previous
         // step's) precedes it on this stream.
         if (timing) HIPCHECK(c, hipEventRecord(ev.r[0], s0));
-        HIPCHECK(c, launch_tidal_fixed(g, c->t, c->s, q, true, s0));
+        HIPCHECK(c, launch_tidal_fixed(g, c->t, sb, q, true, true, s0));
         if (timing) HIPCHECK(c, hipEventRecord(ev.r[1], s0));
         MARK(3);
         MARK(4);
     } else {
-        HIPCHECK(c, hipMemcpyAsync(c->h_newinfo, c->s.counts, g.B * 2 * sizeof(int32_t), hipMemcpyDeviceToHost, s0));
+        HIPCHECK(c, hipMemcpyAsync(c->h_newinfo, sb.counts, g.B * 2 * sizeof(int32_t), hipMemcpyDeviceToHost, s0));
         if (g.k)
-            HIPCHECK(c, hipMemcpyAsync(c->h_newinfo + g.B * 2, c->s.new_list, (size_t)g.B * g.k * 2 * sizeof(int32_t),
+            HIPCHECK(c, hipMemcpyAsync(c->h_newinfo + g.B * 2, sb.new_list, (size_t)g.B * g.k * 2 * sizeof(int32_t),
                                        hipMemcpyDeviceToHost, s0));
         HIPCHECK(c, hipEventRecord(c->ev_sel, s0));
         MARK(2);
         // (4a) device-resident rows while the host waits for the selection and issues the copies
-        HIPCHECK(c, launch_tidal_fixed(g, c->t, c->s, q, false, s0));
+        HIPCHECK(c, launch_tidal_fixed(g, c->t, sb, q, false, true, s0));
         MARK(3);
         // (3) copies on the side stream.  The target slots were freed by this step's select
         // kernel, which follows every earlier reader on s0; the copies start after ev_sel.
@@ -609,10 +619,10 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, float *out, float *sco
         HIPCHECK(c, hipEventRecord(c->ev_rec, c->side));
         HIPCHECK(c, hipStreamWaitEvent(s0, c->ev_rec, 0));
         // (4b) the complements copied this step
-        HIPCHECK(c, launch_new_slots(g, c->t, c->s, q, s0));
+        HIPCHECK(c, launch_new_slots(g, c->t, sb, q, s0));
         MARK(4);
     }
-    HIPCHECK(c, launch_subset_combine(g, c->t, c->s, out, s0));
+    HIPCHECK(c, launch_subset_combine(g, c->t, sb, out, s0));
     MARK(5);
 #undef MARK
     if (timing) c->pending.push_back(ev);

@@ -96,11 +96,14 @@ inline size_t select_shared_bytes(const Geometry &g)
 {
     return (size_t)g.nc * (SCORE_PARTS * 8 + 4 + 8 * 4) + (size_t)g.n_slots * 5 * 4;
 }
-// Fixed heads, tidal kept rows and the tidal complements already in their slots; with `recall`
+// Fixed heads (with `with_static`), tidal kept rows and the tidal complements already in their
+// slots; with `recall`
 // (same-step timing), also the copy of the complements listed for recall from mapped pinned
 // memory into their slots and the attention over them.
 hipError_t launch_tidal_fixed(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, bool recall,
-                              hipStream_t st);
+                              bool with_static, hipStream_t st);
+// Anchor attention + chunk mass together with the static tidal/fixed tiles (next-step timing).
+hipError_t launch_attention(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st);
 // Next-step timing: copy of the complements listed for recall from mapped pinned memory into
 // their slots, no attention (they are attended from the next step on).
 hipError_t launch_recall(const Geometry &g, const Tiers &t, const StepBuffers &s, hipStream_t st);

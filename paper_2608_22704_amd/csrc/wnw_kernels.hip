@@ -6,6 +6,7 @@
 //                   g q-heads' logits, the tile max, exp, the per-chunk softmax mass (Eq. 2) and
 //                   the unnormalised P.V partial.  Logits and masses are kept in double: the
 //                   chunk ranking must agree with an fp64 reference to well under 1e-6.
+//   attention       (next-step timing) anchor tiles and the static tidal/fixed tiles in one launch.
 //   anchor_combine  log-sum-exp merge of the tiles of one anchor head -> its outputs and its
 //                   normalised chunk masses.
 //   scores          per chunk: fixed-order sum over anchor q-heads / chunk length (mean).
@@ -167,9 +168,19 @@ __device__ inline double exp_nonpos(double y)
     return tt < -1022.0 ? 0.0 : ldexp((double)e, (int)n);
 }
 
+// Shared memory of one anchor tile.
 template <int G>
-__global__ __launch_bounds__(NT, G <= 4 ? 4 : 2) void anchor_attn_kernel(Geometry g, Tiers t, StepBuffers s,
-                                                                         const uint16_t *__restrict__ q)
+struct AnchorSmem {
+    static constexpr int RW = TILE_A / WAVES;
+    uint4 kst[WAVES][RW * 16];                // swizzled K rows; afterwards the P.V partials
+    double xs[G * TILE_A];                    // probabilities (per-row chunk masses only)
+    float xf[G * TILE_A];                     // probabilities in fp32, for P.V
+    double wm[WAVES * G], wl[WAVES * G];
+};
+
+template <int G>
+__device__ inline void anchor_tile(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *__restrict__ q,
+                                   int tile, int ai, int b, AnchorSmem<G> &sm)
 {
     typedef float v4f __attribute__((ext_vector_type(4)));
     constexpr int HG = G <= 4 ? 1 : 2;        // groups of 4 q-heads per logit instruction
@@ -180,7 +191,6 @@ __global__ __launch_bounds__(NT, G <= 4 ? 4 : 2) void anchor_attn_kernel(Geometr
     constexpr int OGR = G <= 4 ? 4 : 2;       // row groups kept in the P.V partial store
     constexpr int HS = (G + 3) / 4;           // sets of 4 heads for P.V
     static_assert(NKG % 2 == 0, "key groups are processed in pairs");
-    const int tile = blockIdx.x, ai = blockIdx.y, b = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, sub = lane & 15, rg = lane >> 4;
     const int kq = lane >> 4, blk = (lane >> 2) & 3, x4 = lane & 3;
     const int lk = t.anchor_lk[ai], l = lk / g.Hkv, kv = lk - l * g.Hkv;
@@ -193,10 +203,9 @@ __global__ __launch_bounds__(NT, G <= 4 ? 4 : 2) void anchor_attn_kernel(Geometr
     // wavefront of this tile straddles the audio/text boundary
     const bool fast_mass = g.cl % RW == 0 && !(t0 < g.Ta && g.Ta < t0 + TILE_A && g.Ta % RW != 0);
 
-    __shared__ uint4 kst[WAVES][RW * 16];     // swizzled K rows; afterwards the P.V partials
-    __shared__ double xs[G * TILE_A];         // probabilities (per-row chunk masses only)
-    __shared__ float xf[G * TILE_A];          // probabilities in fp32, for P.V
-    __shared__ double wm[WAVES * G], wl[WAVES * G];
+    auto &kst = sm.kst;
+    double *xs = sm.xs, *wm = sm.wm, *wl = sm.wl;
+    float *xf = sm.xf;
     float *wo = (float *)&kst[wave][0];       // [OGR][G][D] of this wavefront
 
     // q (B operand: head hB, dims 32kq..32kq+31), then K and V rows
@@ -378,6 +387,14 @@ __global__ __launch_bounds__(NT, G <= 4 ? 4 : 2) void anchor_attn_kernel(Geometr
         acc2 = sum16(acc2);
         if (valid && k == 0) s.pa_mass[pidx * G * g.maxc + grp] = acc2;
     }
+}
+
+template <int G>
+__global__ __launch_bounds__(NT, G <= 4 ? 4 : 2) void anchor_attn_kernel(Geometry g, Tiers t, StepBuffers s,
+                                                                         const uint16_t *__restrict__ q)
+{
+    __shared__ AnchorSmem<G> sm;
+    anchor_tile<G>(g, t, s, q, blockIdx.x, blockIdx.y, blockIdx.z, sm);
 }
 
 template <typename T>
@@ -1071,13 +1088,13 @@ __device__ inline void recall_units(const Geometry &g, const Tiers &t, const Ste
 }
 
 // Fixed heads, tidal kept rows and tidal complements already in their slots: static tiles
-// first, then groups of kept entries.  With REC (same-step timing), the first RECALL_WGS
+// first (unless the attention launch ran them), then groups of kept entries.  With REC (same-step timing), the first RECALL_WGS
 // work-groups also copy the complements listed for recall from mapped pinned memory into their
 // slots and attend to them: the step is bound by the host link then, and the copies start with
 // the launch.  Without REC the kernel keeps to its lean register budget.
 template <int G, int RPLK, bool REC>
 __global__ __launch_bounds__(NT, REC ? (RPLK == RPL_S ? 2 : 1) : (RPLK == RPL_S ? (G <= 4 ? 4 : 3) : 2)) void tidal_fixed_kernel(
-    Geometry g, Tiers t, StepBuffers s, const uint16_t *__restrict__ q)
+    Geometry g, Tiers t, StepBuffers s, const uint16_t *__restrict__ q, int with_static)
 {
     union Smem {
         SubsetSmem<G, RPL_S> st;
@@ -1092,7 +1109,7 @@ __global__ __launch_bounds__(NT, REC ? (RPLK == RPL_S ? 2 : 1) : (RPLK == RPL_S 
         }
         bid -= RECALL_WGS;
     }
-    const int nh = g.nT + g.nF, n_static = g.n_tiles_s * nh * g.B;
+    const int nh = g.nT + g.nF, n_static = with_static ? g.n_tiles_s * nh * g.B : 0;
     if (bid < n_static) {
         const int tile = bid % g.n_tiles_s, rest = bid / g.n_tiles_s;
         static_tile<G>(g, t, s, q, tile, rest % nh, rest / nh, sm.st);
@@ -1103,9 +1120,40 @@ __global__ __launch_bounds__(NT, REC ? (RPLK == RPL_S ? 2 : 1) : (RPLK == RPL_S 
     slot_group<G, RPLK>(g, t, s, q, grp, rest % g.nT, rest / g.nT, 0, g.sg, sm.sl);
 }
 
-// Next-step timing: copy only.  Work-group w of the grid walks the units (sequence, new entry,
+// Anchor tiles and the static tidal/fixed tiles (kept rows + text, which no selection changes)
+// in one launch, interleaved evenly along the grid: the anchor tiles' arithmetic (fp64 logits)
+// overlaps the static tiles' streaming.  Used with next-step timing, where the static tiles need
+// not wait for this step's selection.
+template <int G>
+__global__ __launch_bounds__(NT, G <= 4 ? 4 : 2) void attention_kernel(Geometry g, Tiers t, StepBuffers s,
+                                                                       const uint16_t *__restrict__ q)
+{
+    union Smem {
+        AnchorSmem<G> a;
+        SubsetSmem<G, RPL_S> st;
+    };
+    __shared__ Smem sm;
+    const long long na = (long long)g.n_tiles_a * g.nA * g.B;
+    const long long nh = g.nT + g.nF, n = na + (long long)g.n_tiles_s * nh * g.B;
+    const long long p = blockIdx.x, a0 = p * na / n, a1 = (p + 1) * na / n;
+    if (a1 > a0) {
+        // anchors before this position: a0, so this is anchor tile a0
+        const int tile = (int)(a0 % g.n_tiles_a);
+        const long long rest = a0 / g.n_tiles_a;
+        anchor_tile<G>(g, t, s, q, tile, (int)(rest % g.nA), (int)(rest / g.nA), sm.a);
+    } else {
+        const long long i = p - a0;   // static tiles before this position
+        const int tile = (int)(i % g.n_tiles_s);
+        const long long rest = i / g.n_tiles_s;
+        static_tile<G>(g, t, s, q, tile, (int)(rest % nh), (int)(rest / nh), sm.st);
+    }
+}
+
+// Next-step timing: copy only.  Work-group w of RECALL_WGS walks the units (sequence, new entry,
 // tidal head) and copies each unit's block (K and V complement rows, padding included) from
-// mapped pinned memory to its slot; the rows are attended from the next step on.
+// mapped pinned memory to its slot, eight 16-byte reads in flight per thread; the rows are
+// attended from the next step on.  Host reads take ~15 us, so the link needs about a megabyte
+// in flight: the number of work-groups, each holding one unit, sets the rate.
 __global__ __launch_bounds__(NT) void recall_copy_kernel(Geometry g, Tiers t, StepBuffers s)
 {
     int total = 0;
@@ -1119,7 +1167,19 @@ __global__ __launch_bounds__(NT) void recall_copy_kernel(Geometry g, Tiers t, St
         const size_t off = (size_t)ti * 2 * g.comp_max * D;
         const uint4 *src = (const uint4 *)(t.host_comp + ((size_t)b * g.nc + c) * g.chunk_elems + off);
         uint4 *dst = (uint4 *)(t.slots + ((size_t)b * g.n_slots + slot) * g.chunk_elems + off);
-        for (int j = threadIdx.x; j < n16; j += NT) dst[j] = src[j];
+        for (int j0 = 0; j0 < n16; j0 += 8 * NT) {
+            uint4 v[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const int j = j0 + k * NT + threadIdx.x;
+                if (j < n16) v[k] = src[j];
+            }
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const int j = j0 + k * NT + threadIdx.x;
+                if (j < n16) dst[j] = v[k];
+            }
+        }
     }
 }
 
@@ -1281,20 +1341,31 @@ struct AnchorCombineL {
 template <int G>
 struct TidalFixedL {
     static hipError_t run(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, bool recall,
-                          hipStream_t st)
+                          bool with_static, hipStream_t st)
     {
         recall = recall && g.nT > 0 && g.k > 0 && g.comp_max > 0;
-        const long long n = (recall ? RECALL_WGS : 0) + (long long)g.n_tiles_s * (g.nT + g.nF) * g.B +
+        const long long n = (recall ? RECALL_WGS : 0) + (with_static ? (long long)g.n_tiles_s * (g.nT + g.nF) * g.B : 0) +
                             (long long)g.ng_kept * g.nT * g.B;
         if (n == 0) return hipSuccess;
         const dim3 grid((unsigned)n), block(NT);
+        const int ws = with_static ? 1 : 0;
         if (g.slot_tile == TILE_S) {
-            if (recall) hipLaunchKernelGGL((tidal_fixed_kernel<G, TILE_S / 16, true>), grid, block, 0, st, g, t, s, q);
-            else hipLaunchKernelGGL((tidal_fixed_kernel<G, TILE_S / 16, false>), grid, block, 0, st, g, t, s, q);
+            if (recall) hipLaunchKernelGGL((tidal_fixed_kernel<G, TILE_S / 16, true>), grid, block, 0, st, g, t, s, q, ws);
+            else hipLaunchKernelGGL((tidal_fixed_kernel<G, TILE_S / 16, false>), grid, block, 0, st, g, t, s, q, ws);
         } else {
-            if (recall) hipLaunchKernelGGL((tidal_fixed_kernel<G, TILE_S / 8, true>), grid, block, 0, st, g, t, s, q);
-            else hipLaunchKernelGGL((tidal_fixed_kernel<G, TILE_S / 8, false>), grid, block, 0, st, g, t, s, q);
+            if (recall) hipLaunchKernelGGL((tidal_fixed_kernel<G, TILE_S / 8, true>), grid, block, 0, st, g, t, s, q, ws);
+            else hipLaunchKernelGGL((tidal_fixed_kernel<G, TILE_S / 8, false>), grid, block, 0, st, g, t, s, q, ws);
         }
+        return hipGetLastError();
+    }
+};
+template <int G>
+struct AttentionL {
+    static hipError_t run(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st)
+    {
+        const long long n = (long long)g.n_tiles_a * g.nA * g.B + (long long)g.n_tiles_s * (g.nT + g.nF) * g.B;
+        if (n == 0) return hipSuccess;
+        hipLaunchKernelGGL(attention_kernel<G>, dim3((unsigned)n), dim3(NT), 0, st, g, t, s, q);
         return hipGetLastError();
     }
 };
@@ -1342,9 +1413,14 @@ hipError_t launch_select(const Geometry &g, const StepBuffers &s, float *scores,
 }
 
 hipError_t launch_tidal_fixed(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, bool recall,
-                              hipStream_t st)
+                              bool with_static, hipStream_t st)
 {
-    return dispatch_g<TidalFixedL>(g.G, g, t, s, q, recall, st);
+    return dispatch_g<TidalFixedL>(g.G, g, t, s, q, recall, with_static, st);
+}
+
+hipError_t launch_attention(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st)
+{
+    return dispatch_g<AttentionL>(g.G, g, t, s, q, st);
 }
 
 hipError_t launch_recall(const Geometry &g, const Tiers &t, const StepBuffers &s, hipStream_t st)
