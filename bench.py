@@ -34,6 +34,50 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
+def overlap_sweep(W, torch, w, ctx, geo, qd, out, sc, sel, stream, args, ms_no_recall):
+    """Force about N newly resident chunks per step through the selection override: k - N chunks
+    stay selected, N more rotate through the remaining chunks.  For each N: steps/s, chunks
+    copied and revived per step, recall time, and overlap = 1 - (T_step - T_no_recall) / T_recall
+    (the share of the recall hidden behind the rest of the step)."""
+    B, S, k, nc = w.batch, w.steps, geo["k"], geo["n_chunks"]
+    res = []
+    for n_new in (1, 2, 4, 8, 24):
+        if n_new > k or nc - (k - n_new) < n_new:
+            continue
+        steps, warm = 40, 8
+        core = np.arange(k - n_new, dtype=np.int32)
+        pool = np.arange(k - n_new, nc, dtype=np.int32)
+        sched = np.empty((warm + steps, B, k), dtype=np.int32)
+        for s in range(warm + steps):
+            rot = pool[(s * n_new + np.arange(n_new)) % len(pool)]
+            sched[s, :] = np.sort(np.concatenate([core, rot]))
+        sd = torch.from_numpy(sched).cuda()
+        for s in range(warm):
+            W.wnw_set_selection_override(ctx, sd[s])
+            W.wnw_decode_step(ctx, qd[s % S], out, sc, sel, stream)
+        torch.cuda.synchronize()
+        a = W.wnw_get_stats(ctx)
+        t0 = time.perf_counter()
+        for s in range(warm, warm + steps):
+            W.wnw_set_selection_override(ctx, sd[s])
+            W.wnw_decode_step(ctx, qd[s % S], out, sc, sel, stream)
+        torch.cuda.synchronize()
+        el = time.perf_counter() - t0
+        b = W.wnw_get_stats(ctx)
+        ms = el * 1e3 / steps
+        nt = b["timed_steps"] - a["timed_steps"]
+        rec_ms = (b["t_recall_ms"] - a["t_recall_ms"]) / nt if nt else None
+        ov = None
+        if rec_ms:
+            ov = max(0.0, min(1.0, 1.0 - (ms - ms_no_recall) / rec_ms))
+        res.append({"new_per_step": n_new, "steps_per_s": 1e3 / ms, "ms_per_step": ms,
+                    "copied_per_step": (b["recalled_chunks"] - a["recalled_chunks"]) / steps / B,
+                    "revived_per_step": (b["revived_chunks"] - a["revived_chunks"]) / steps / B,
+                    "recall_ms": rec_ms, "overlap": ov})
+        log(f"[bench] sweep {n_new} new/step: {1e3 / ms:.0f} steps/s, overlap {ov}")
+    return res
+
+
 def run_timing(W, torch, w, timing, recall, kd, vd, qd, roles, prefill, args):
     """Set up one context with the given selection timing and recall path, run the warm-up and
     the timed steps, then a second region with the selection pinned (no recall).  Returns the
@@ -85,13 +129,16 @@ def run_timing(W, torch, w, timing, recall, kd, vd, qd, roles, prefill, args):
         torch.cuda.synchronize()
         t2 = time.perf_counter() - t2
         st3 = W.wnw_get_stats(ctx)
+        sweep = []
+        if args.sweep and timing == "next" and geo["k"] > 0:
+            sweep = overlap_sweep(W, torch, w, ctx, geo, qd, out, sc, sel, stream, args, t2 * 1e3 / nr)
         W.wnw_set_selection_override(ctx, None)
     finally:
         W.wnw_destroy(ctx)
     K = args.steps
     d = {k: st1[k] - st0[k] for k in st1 if isinstance(st1[k], (int, float))}
     d2 = {k: st3[k] - st2[k] for k in st3 if isinstance(st3[k], (int, float))}
-    r = {"value": K / t_el, "ms_per_step": t_el * 1e3 / K, "geo": geo, "st1": st1,
+    r = {"value": K / t_el, "ms_per_step": t_el * 1e3 / K, "geo": geo, "st1": st1, "sweep": sweep,
          "recall": {"copied_chunks_per_step": d["recalled_chunks"] / K / B,
                     "revived_chunks_per_step": d["revived_chunks"] / K / B,
                     "MB_per_step": d["recalled_bytes"] / K / 1e6, "chunk_MB": geo.get("chunk_bytes", 0) / 1e6,
@@ -139,6 +186,8 @@ def main():
                     help="selection timing of the headline run: the selection made after step s serves step s+1 "
                          "(the paper's timing; the recall overlaps the step) or step s itself")
     ap.add_argument("--no-other-timing", action="store_true", help="skip the run with the other selection timing")
+    ap.add_argument("--no-sweep", dest="sweep", action="store_false",
+                    help="skip the overlap sweep (forced 1..24 newly resident chunks per step)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU oracle sample (0 = skip)")
     ap.add_argument("--no-timing", action="store_true", help="no per-kernel events (for profiler runs)")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -177,7 +226,7 @@ def main():
     other = None
     if not args.no_other_timing:
         other_timing = "same" if args.timing == "next" else "next"
-        args_other = argparse.Namespace(**{**vars(args), "calibrate_copy": False})
+        args_other = argparse.Namespace(**{**vars(args), "calibrate_copy": False, "sweep": False})
         other = run_timing(W, torch, w, other_timing, args.recall, kd, vd, qd, roles, prefill, args_other)
     del kd, vd
     torch.cuda.empty_cache()
@@ -205,6 +254,12 @@ def main():
                            "note": "achieved: over the timed steps, the recall's host reads running beside it; "
                                    "achieved_without_recall: selection pinned, no recall"}
     res["recall"] = main_run["recall"]
+    if main_run.get("sweep"):
+        res["overlap_sweep"] = main_run["sweep"]
+        # share of the recall hidden behind the step at the workload's own recall load
+        rm = main_run["recall"]
+        if rm.get("ms"):
+            res["recall"]["overlap"] = max(0.0, min(1.0, 1.0 - (main_run["ms_per_step"] - rm["step_ms_no_recall"]) / rm["ms"]))
     res["r_gpu"] = st1["r_gpu"]
     res["r_gpu_cpu"] = st1["r_gpu_cpu"]
     if other is not None:
@@ -245,23 +300,34 @@ def measured_traffic(kernel, workload):
 
 
 def cpu_baseline(w, roles, prefill, budget_s):
-    """The CPU oracle on the first decode steps of sequence 0 of the same workload, all heads,
-    OpenMP across heads; steps/s over a bounded sample."""
+    """The CPU oracle on the first decode steps of sequence 0 of the same workload, all heads:
+    steps/s over a bounded sample with every host thread (OpenMP across heads), then over a
+    shorter sample with one thread."""
     from oracle import oracle as O
     from synth import gen
 
-    log(f"[bench] CPU oracle sample (~{budget_s:.0f}s)")
+    log(f"[bench] CPU oracle sample (~{budget_s:.0f}s + ~{budget_s * 2 / 3:.0f}s on one thread)")
     seq = gen.sequence(w.with_(batch=1), 0) if w.batch == 1 else gen.sequence(w, 0)
-    o = O.Oracle(O.cfg_from_workload(w, batch=1), seq["k"][None], seq["v"][None], roles, prefill[:1])
-    n, t0 = 0, time.perf_counter()
-    while n == 0 or (time.perf_counter() - t0 < budget_s and n < w.steps):
-        o.step(seq["q"][n][None])
-        n += 1
-    el = time.perf_counter() - t0
-    o.close()
-    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+
+    def sample(seconds):
+        o = O.Oracle(O.cfg_from_workload(w, batch=1), seq["k"][None], seq["v"][None], roles, prefill[:1])
+        n, t0 = 0, time.perf_counter()
+        while n == 0 or (time.perf_counter() - t0 < seconds and n < w.steps):
+            o.step(seq["q"][n][None])
+            n += 1
+        el = time.perf_counter() - t0
+        o.close()
+        return n, el
+
+    cores = O.set_threads(0)
+    n, el = sample(budget_s)
+    O.set_threads(1)
+    n1, el1 = sample(budget_s * 2 / 3)
+    O.set_threads(cores)
     return {"value": n / el, "unit": "steps/s", "cores": cores, "kind": "oracle",
-            "sample": f"first {n} decode steps of sequence 0 of {w.name}, every head, double precision ({el:.1f}s)"}
+            "sample": f"first {n} decode steps of sequence 0 of {w.name}, every head, double precision, "
+                      f"{cores} threads ({el:.1f}s)",
+            "value_1_core": n1 / el1, "sample_1_core": f"first {n1} steps on one thread ({el1:.1f}s)"}
 
 
 if __name__ == "__main__":

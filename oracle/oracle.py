@@ -54,6 +54,8 @@ def lib():
         L.wnwo_topk.argtypes = [P, C.c_int32, C.c_int32, P]
         L.wnwo_tokens_for_window.argtypes = [C.c_double, C.c_double]
         L.wnwo_tokens_for_window.restype = C.c_int32
+        L.wnwo_set_threads.argtypes = [C.c_int]
+        L.wnwo_set_threads.restype = C.c_int
         _lib = L
     return _lib
 
@@ -93,6 +95,11 @@ def topk(scores: np.ndarray, k: int) -> np.ndarray:
 
 def tokens_for_window(seconds: float, rate: float) -> int:
     return lib().wnwo_tokens_for_window(seconds, rate)
+
+
+def set_threads(n: int) -> int:
+    """Threads of the oracle's parallel loops from now on (n <= 0: unchanged); returns the count."""
+    return lib().wnwo_set_threads(n)
 
 
 class Oracle:

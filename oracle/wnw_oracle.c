@@ -41,6 +41,9 @@
 #include <math.h>
 #include <stdlib.h>
 #include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
 
 struct wnwo {
     wnwo_config c;
@@ -393,4 +396,16 @@ done:
     free(res_now);
     free(res_use);
     return status;
+}
+
+/* Threads of the parallel loops (timing only; results do not depend on it). */
+int wnwo_set_threads(int n)
+{
+#ifdef _OPENMP
+    if (n > 0) omp_set_num_threads(n);
+    return omp_get_max_threads();
+#else
+    (void)n;
+    return 1;
+#endif
 }

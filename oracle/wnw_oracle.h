@@ -63,6 +63,10 @@ int wnwo_topk(const float *scores, int32_t n, int32_t k, int32_t *sel);
 /* Tokens covered by a window of `seconds` at `rate` tokens per second: ceil(seconds * rate). */
 int32_t wnwo_tokens_for_window(double seconds, double rate);
 
+/* Threads used by the parallel loops from now on (n <= 0: unchanged); returns the count in use.
+ * Timing only: every result is independent of it. */
+int wnwo_set_threads(int n);
+
 #ifdef __cplusplus
 }
 #endif
