@@ -30,7 +30,7 @@ def build(verbose: bool = False) -> str:
 class _Cfg(C.Structure):
     _fields_ = [(n, C.c_int32) for n in (
         "batch", "layers", "q_heads", "kv_heads", "head_dim", "audio_len", "text_len",
-        "chunk_len", "budget_bp", "top_k", "evict_lag", "next_step")]
+        "chunk_len", "budget_bp", "top_k", "evict_lag", "next_step", "chunk_span")]
 
 
 _lib = None
@@ -54,6 +54,7 @@ def lib():
         L.wnwo_topk.argtypes = [P, C.c_int32, C.c_int32, P]
         L.wnwo_tokens_for_window.argtypes = [C.c_double, C.c_double]
         L.wnwo_tokens_for_window.restype = C.c_int32
+        L.wnwo_segments.argtypes = [C.POINTER(_Cfg), C.POINTER(C.c_int32)]
         L.wnwo_set_threads.argtypes = [C.c_int]
         L.wnwo_set_threads.restype = C.c_int
         _lib = L
@@ -65,9 +66,9 @@ def _ptr(a):
 
 
 def make_cfg(batch, layers, q_heads, kv_heads, head_dim, audio_len, text_len, chunk_len,
-             budget_bp, top_k=0, evict_lag=0, next_step=0) -> _Cfg:
+             budget_bp, top_k=0, evict_lag=0, next_step=0, chunk_span=1) -> _Cfg:
     return _Cfg(batch, layers, q_heads, kv_heads, head_dim, audio_len, text_len, chunk_len,
-                budget_bp, top_k, evict_lag, next_step)
+                budget_bp, top_k, evict_lag, next_step, chunk_span)
 
 
 def cfg_from_workload(w, batch=None, **over) -> _Cfg:
@@ -83,6 +84,13 @@ def geometry(cfg: _Cfg):
     if lib().wnwo_geometry(C.byref(cfg), C.byref(n), C.byref(k), C.byref(kt)):
         raise ValueError("invalid oracle configuration")
     return n.value, k.value, kt.value
+
+
+def segments(cfg: _Cfg) -> int:
+    n = C.c_int32()
+    if lib().wnwo_segments(C.byref(cfg), C.byref(n)):
+        raise ValueError("invalid oracle configuration")
+    return n.value
 
 
 def topk(scores: np.ndarray, k: int) -> np.ndarray:
@@ -110,6 +118,7 @@ class Oracle:
     def __init__(self, cfg: _Cfg, k, v, roles, prefill):
         self.cfg = cfg
         self.n_chunks, self.k, self.keep_total = geometry(cfg)
+        self.n_segments = segments(cfg)   # the unit of masses and residency (= chunks when disjoint)
         self._k = np.ascontiguousarray(k, dtype=np.uint16)
         self._v = np.ascontiguousarray(v, dtype=np.uint16)
         self._roles = np.ascontiguousarray(roles, dtype=np.uint8)
@@ -144,8 +153,9 @@ class Oracle:
         out = np.empty((B, L, Hq, D), dtype=np.float64)
         scores = np.empty((B, self.n_chunks), dtype=np.float64)
         sel = np.empty((B, max(self.k, 1)), dtype=np.int32)
-        mass = np.empty((B, max(self.n_anchor_q, 1), max(self.n_chunks, 1)), dtype=np.float64)
-        res = np.empty((B, max(self.n_chunks, 1)), dtype=np.uint8)
+        ns = self.n_segments
+        mass = np.empty((B, max(self.n_anchor_q, 1), max(ns, 1)), dtype=np.float64)
+        res = np.empty((B, max(ns, 1)), dtype=np.uint8)
         f = None if forced is None else np.ascontiguousarray(forced, dtype=np.int32).reshape(B, self.k)
         hm = None if head_mask is None else np.ascontiguousarray(head_mask, dtype=np.uint8).reshape(L, c.kv_heads)
         rc = lib().wnwo_step(self._h, _ptr(q), _ptr(f), _ptr(hm), _ptr(out), _ptr(scores), _ptr(sel),
@@ -153,4 +163,4 @@ class Oracle:
         if rc:
             raise ValueError(f"wnwo_step failed ({rc})")
         return {"out": out, "scores": scores, "selected": sel[:, : self.k],
-                "mass": mass[:, : self.n_anchor_q, : self.n_chunks], "resident": res[:, : self.n_chunks]}
+                "mass": mass[:, : self.n_anchor_q, : ns], "resident": res[:, : ns]}

@@ -22,8 +22,11 @@
  *      kept rows + resident complements + text, fixed heads over kept rows + text.
  *
  * Readings taken where the paper leaves a choice (all listed in the design notes):
- *   - chunks are disjoint runs of chunk_len audio positions, one segment per chunk; the last
- *     chunk may be shorter and its score is the mean over the positions it has;
+ *   - by default chunks are disjoint runs of chunk_len audio positions, one segment per chunk;
+ *     with chunk_span = 2 a chunk is two consecutive segments of chunk_len / 2 positions and a
+ *     chunk starts at every segment (Method, "Chunk Structure"); the last segment may be
+ *     shorter and a chunk's score is the mean over the positions it has; a selected chunk makes
+ *     both of its segments resident;
  *   - retention is one uniform fraction budget_bp / 10000 for every tidal and fixed head;
  *   - k = floor(budget_bp * T_a / (10000 * chunk_len)) unless given;
  *   - the softmax of Eq. 2 runs over the anchor head's whole key set (audio and text); only the
@@ -47,12 +50,12 @@
 
 struct wnwo {
     wnwo_config c;
-    int32_t n_chunks, k, keep_total, delta;
+    int32_t n_chunks, n_seg, span, k, keep_total, delta;
     const uint16_t *kc, *vc;
     uint8_t *roles;        /* [L][Hkv]                                               */
     uint8_t *keep;         /* [B][L][Hkv][T_a] prefill keep flags of non-anchor heads */
     int32_t *streak;       /* [B][n_chunks] steps since last selection, capped at delta */
-    uint8_t *res_prev;     /* [B][n_chunks] resident set after the previous step       */
+    uint8_t *res_prev;     /* [B][n_seg] resident segments after the previous step     */
 };
 
 static double bf16(uint16_t h)
@@ -69,11 +72,27 @@ int32_t wnwo_tokens_for_window(double seconds, double rate)
     return (int32_t)ceil(seconds * rate);
 }
 
-static int32_t chunk_begin(const wnwo_config *c, int32_t ch) { return ch * c->chunk_len; }
-static int32_t chunk_end(const wnwo_config *c, int32_t ch)
+/* Segments: runs of chunk_len / span audio positions, the last one possibly shorter. */
+static int32_t span_of(const wnwo_config *c) { return c->chunk_span == 2 ? 2 : 1; }
+static int32_t seg_len(const wnwo_config *c) { return c->chunk_len / span_of(c); }
+static int32_t seg_count(const wnwo_config *c) { return (c->audio_len + seg_len(c) - 1) / seg_len(c); }
+static int32_t seg_begin(const wnwo_config *c, int32_t j) { return j * seg_len(c); }
+static int32_t seg_end(const wnwo_config *c, int32_t j)
 {
-    int32_t e = (ch + 1) * c->chunk_len;
+    int32_t e = (j + 1) * seg_len(c);
     return e < c->audio_len ? e : c->audio_len;
+}
+/* Chunks: one per segment start; with span 2, chunk c = segments c and c + 1, so there is one
+ * chunk fewer than segments (a single segment forms a chunk on its own). */
+static int32_t chunk_count(const wnwo_config *c)
+{
+    int32_t ns = seg_count(c);
+    return (span_of(c) == 2 && ns >= 2) ? ns - 1 : ns;
+}
+static int32_t chunk_last_seg(const wnwo_config *c, int32_t ch)
+{
+    int32_t last = ch + span_of(c) - 1, ns = seg_count(c);
+    return last < ns ? last : ns - 1;
 }
 
 /* Positions kept at prefill inside a segment of `len` positions: floor(retention * len). */
@@ -87,17 +106,25 @@ int wnwo_geometry(const wnwo_config *c, int32_t *n_chunks, int32_t *k, int32_t *
     if (!c || c->batch < 1 || c->layers < 1 || c->kv_heads < 1 || c->head_dim < 1 ||
         c->q_heads < c->kv_heads || c->q_heads % c->kv_heads || c->audio_len < 0 ||
         c->text_len < 0 || c->chunk_len < 1 || c->budget_bp < 0 || c->budget_bp > 10000 ||
-        c->top_k < 0 || c->evict_lag < 0)
+        c->top_k < 0 || c->evict_lag < 0 || c->chunk_span < 0 || c->chunk_span > 2 ||
+        (c->chunk_span == 2 && c->chunk_len % 2))
         return -1;
-    int32_t nc = (c->audio_len + c->chunk_len - 1) / c->chunk_len;
+    int32_t nc = chunk_count(c), ns = seg_count(c);
     int32_t kk = c->top_k ? c->top_k
                           : (int32_t)(((int64_t)c->budget_bp * c->audio_len) / (10000LL * c->chunk_len));
     if (kk > nc) return -1;
     int32_t kt = 0;
-    for (int32_t ch = 0; ch < nc; ++ch) kt += keep_count(c, chunk_end(c, ch) - chunk_begin(c, ch));
+    for (int32_t j = 0; j < ns; ++j) kt += keep_count(c, seg_end(c, j) - seg_begin(c, j));
     if (n_chunks) *n_chunks = nc;
     if (k) *k = kk;
     if (keep_total) *keep_total = kt;
+    return 0;
+}
+
+int wnwo_segments(const wnwo_config *c, int32_t *n_segments)
+{
+    if (wnwo_geometry(c, NULL, NULL, NULL)) return -1;
+    if (n_segments) *n_segments = seg_count(c);
     return 0;
 }
 
@@ -116,9 +143,9 @@ static int by_score_then_pos(const void *a, const void *b)
 static void prefill_keep(const wnwo_config *c, const float *score, uint8_t *keep, ranked *tmp)
 {
     memset(keep, 0, (size_t)c->audio_len);
-    int32_t nc = (c->audio_len + c->chunk_len - 1) / c->chunk_len;
-    for (int32_t ch = 0; ch < nc; ++ch) {
-        int32_t b0 = chunk_begin(c, ch), e0 = chunk_end(c, ch), n = e0 - b0;
+    int32_t ns = seg_count(c);
+    for (int32_t j = 0; j < ns; ++j) {
+        int32_t b0 = seg_begin(c, j), e0 = seg_end(c, j), n = e0 - b0;
         for (int32_t i = 0; i < n; ++i) { tmp[i].s = score[b0 + i]; tmp[i].pos = b0 + i; }
         qsort(tmp, (size_t)n, sizeof *tmp, by_score_then_pos);
         int32_t kc = keep_count(c, n);
@@ -138,6 +165,8 @@ wnwo *wnwo_create(const wnwo_config *cfg, const uint16_t *k, const uint16_t *v,
     if (!o) return NULL;
     o->c = *cfg;
     o->n_chunks = nc;
+    o->n_seg = seg_count(cfg);
+    o->span = span_of(cfg);
     o->k = kk;
     o->keep_total = kt;
     o->delta = cfg->evict_lag ? cfg->evict_lag : 3;
@@ -147,7 +176,7 @@ wnwo *wnwo_create(const wnwo_config *cfg, const uint16_t *k, const uint16_t *v,
     o->roles = malloc(nh);
     o->keep = malloc(B * nh * (size_t)(cfg->audio_len ? cfg->audio_len : 1));
     o->streak = malloc(B * (size_t)(nc ? nc : 1) * sizeof(int32_t));
-    o->res_prev = calloc(B * (size_t)(nc ? nc : 1), 1);
+    o->res_prev = calloc(B * (size_t)(o->n_seg ? o->n_seg : 1), 1);
     ranked *tmp = malloc((size_t)(cfg->chunk_len) * sizeof *tmp);
     if (!o->roles || !o->keep || !o->streak || !o->res_prev || !tmp) {
         free(tmp);
@@ -256,7 +285,7 @@ int wnwo_step(wnwo *o, const uint16_t *q, const int32_t *forced, const uint8_t *
     if (!o || !q || !out || !scores || (o->k && !selected)) return -1;
     const wnwo_config *c = &o->c;
     const int32_t L = c->layers, H = c->kv_heads, Hq = c->q_heads, g = Hq / H, D = c->head_dim;
-    const int32_t Ta = c->audio_len, T = Ta + c->text_len, nc = o->n_chunks, k = o->k, B = c->batch;
+    const int32_t Ta = c->audio_len, T = Ta + c->text_len, nc = o->n_chunks, ns = o->n_seg, k = o->k, B = c->batch;
     const size_t nh = (size_t)L * H;
 
     int32_t n_anchor = 0;
@@ -265,9 +294,9 @@ int wnwo_step(wnwo *o, const uint16_t *q, const int32_t *forced, const uint8_t *
 
     /* Anchor KV-heads in (layer, kv) order; their q-heads j = 0..g-1 follow in that order. */
     int32_t *anchor_of = malloc((nh ? nh : 1) * sizeof(int32_t));
-    double *m = calloc((size_t)B * (naq ? naq : 1) * (nc ? nc : 1), sizeof(double));
-    uint8_t *res_now = calloc((size_t)B * (nc ? nc : 1), 1);
-    uint8_t *res_use = calloc((size_t)B * (nc ? nc : 1), 1);
+    double *m = calloc((size_t)B * (naq ? naq : 1) * (ns ? ns : 1), sizeof(double));
+    uint8_t *res_now = calloc((size_t)B * (ns ? ns : 1), 1);
+    uint8_t *res_use = calloc((size_t)B * (ns ? ns : 1), 1);
     if (!anchor_of || !m || !res_now || !res_use) {
         free(anchor_of); free(m); free(res_now); free(res_use);
         return -2;
@@ -277,7 +306,7 @@ int wnwo_step(wnwo *o, const uint16_t *q, const int32_t *forced, const uint8_t *
     memset(out, 0, (size_t)B * L * Hq * D * sizeof(double));
     int status = 0;
 
-    /* Step 1: anchor attention over all audio and text rows, and Eq. 2's per-chunk mass. */
+    /* Step 1: anchor attention over all audio and text rows, and Eq. 2's mass per segment. */
     #pragma omp parallel for collapse(2) schedule(dynamic)
     for (int32_t b = 0; b < B; ++b)
         for (int32_t hh = 0; hh < (int32_t)nh; ++hh) {
@@ -299,11 +328,11 @@ int wnwo_step(wnwo *o, const uint16_t *q, const int32_t *forced, const uint8_t *
                 const uint16_t *qh = q + (((size_t)b * L + l) * Hq + hq) * D;
                 double *oh = out + (((size_t)b * L + l) * Hq + hq) * D;
                 attend(qh, o->kc + hoff, o->vc + hoff, rows, T, D, x, oh, p);
-                double *mh = m + ((size_t)b * naq + (size_t)anchor_of[hh] * g + j) * nc;
-                for (int32_t ch = 0; ch < nc; ++ch) {
+                double *mh = m + ((size_t)b * naq + (size_t)anchor_of[hh] * g + j) * ns;
+                for (int32_t sg = 0; sg < ns; ++sg) {
                     double acc = 0.0;
-                    for (int32_t t = chunk_begin(c, ch); t < chunk_end(c, ch); ++t) acc += p[t];
-                    mh[ch] = acc;
+                    for (int32_t t = seg_begin(c, sg); t < seg_end(c, sg); ++t) acc += p[t];
+                    mh[sg] = acc;
                 }
             }
             free(rows); free(x); free(p);
@@ -327,9 +356,12 @@ int wnwo_step(wnwo *o, const uint16_t *q, const int32_t *forced, const uint8_t *
         int32_t *sel = malloc((size_t)(k ? k : 1) * sizeof(int32_t));
         if (!sf || !sel) { free(sf); free(sel); status = -2; goto done; }
         for (int32_t ch = 0; ch < nc; ++ch) {
+            /* A summed over the chunk's positions (its segments), divided by their number */
             double a = 0.0;
-            for (int32_t h = 0; h < naq; ++h) a += m[((size_t)b * naq + h) * nc + ch];
-            double sc = a / (double)(chunk_end(c, ch) - chunk_begin(c, ch));   /* mean over the chunk */
+            const int32_t s1 = chunk_last_seg(c, ch);
+            for (int32_t h = 0; h < naq; ++h)
+                for (int32_t sg = ch; sg <= s1; ++sg) a += m[((size_t)b * naq + h) * ns + sg];
+            double sc = a / (double)(seg_end(c, s1) - seg_begin(c, ch));   /* mean over the chunk */
             scores[(size_t)b * nc + ch] = sc;
             sf[ch] = (float)sc;
         }
@@ -343,13 +375,16 @@ int wnwo_step(wnwo *o, const uint16_t *q, const int32_t *forced, const uint8_t *
         for (int32_t i = 0; i < k; ++i) selected[(size_t)b * k + i] = sel[i];
 
         int32_t *st = o->streak + (size_t)b * nc;
-        uint8_t *now = res_now + (size_t)b * nc;
+        uint8_t *now = res_now + (size_t)b * ns;
         for (int32_t ch = 0; ch < nc; ++ch)
             if (st[ch] < o->delta) st[ch] += 1;            /* one more step without selection */
         for (int32_t i = 0; i < k; ++i)
             if (sel[i] >= 0) st[sel[i]] = 0;                /* selected this step             */
-        for (int32_t ch = 0; ch < nc; ++ch) now[ch] = st[ch] < o->delta;
-        memcpy(res_use + (size_t)b * nc, c->next_step ? o->res_prev + (size_t)b * nc : now, (size_t)nc);
+        /* resident chunks, and the segments they cover */
+        for (int32_t ch = 0; ch < nc; ++ch)
+            if (st[ch] < o->delta)
+                for (int32_t sg = ch; sg <= chunk_last_seg(c, ch); ++sg) now[sg] = 1;
+        memcpy(res_use + (size_t)b * ns, c->next_step ? o->res_prev + (size_t)b * ns : now, (size_t)ns);
         free(sf);
         free(sel);
     }
@@ -369,11 +404,11 @@ int wnwo_step(wnwo *o, const uint16_t *q, const int32_t *forced, const uint8_t *
                 continue;
             }
             const uint8_t *kp = o->keep + ((size_t)b * nh + hh) * (size_t)Ta;
-            const uint8_t *ru = res_use + (size_t)b * nc;
+            const uint8_t *ru = res_use + (size_t)b * ns;
             int32_t n = 0;
             for (int32_t t = 0; t < Ta; ++t) {
-                int32_t ch = t / c->chunk_len;
-                if (kp[t] || (o->roles[hh] == 1 && ru[ch])) rows[n++] = t;
+                int32_t sg = t / seg_len(c);
+                if (kp[t] || (o->roles[hh] == 1 && ru[sg])) rows[n++] = t;
             }
             for (int32_t t = Ta; t < T; ++t) rows[n++] = t;
             size_t hoff = (((size_t)b * L + l) * H + kv) * (size_t)T * D;
@@ -387,9 +422,9 @@ int wnwo_step(wnwo *o, const uint16_t *q, const int32_t *forced, const uint8_t *
         }
     if (status) goto done;
 
-    memcpy(o->res_prev, res_now, (size_t)B * nc);
-    if (mass) memcpy(mass, m, (size_t)B * naq * nc * sizeof(double));
-    if (resident) memcpy(resident, res_use, (size_t)B * nc);
+    memcpy(o->res_prev, res_now, (size_t)B * ns);
+    if (mass) memcpy(mass, m, (size_t)B * naq * ns * sizeof(double));
+    if (resident) memcpy(resident, res_use, (size_t)B * ns);
 done:
     free(anchor_of);
     free(m);

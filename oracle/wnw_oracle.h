@@ -22,17 +22,24 @@ extern "C" {
 typedef struct {
     int32_t batch, layers, q_heads, kv_heads, head_dim;
     int32_t audio_len, text_len;   /* T_a audio rows first, then T_t text rows            */
-    int32_t chunk_len;             /* disjoint chunks of this many audio positions         */
+    int32_t chunk_len;             /* audio positions per chunk                            */
     int32_t budget_bp;             /* on-GPU audio retention in basis points               */
     int32_t top_k;                 /* 0: floor(budget_bp * T_a / (10000 * chunk_len))      */
     int32_t evict_lag;             /* delta; 0 means 3                                     */
     int32_t next_step;             /* 1: tidal heads use the previous step's resident set  */
+    int32_t chunk_span;            /* segments per chunk: 0 or 1 disjoint chunks (one segment
+                                      each); 2 the paper's chunks of two consecutive segments
+                                      of chunk_len / 2 positions, one chunk per segment start  */
 } wnwo_config;
 
 typedef struct wnwo wnwo;
 
-/* Derived sizes: number of chunks, k, kept audio rows per non-anchor head. */
+/* Derived sizes: number of chunks (the selection's candidates), k, kept audio rows per
+ * non-anchor head. */
 int wnwo_geometry(const wnwo_config *cfg, int32_t *n_chunks, int32_t *k, int32_t *keep_total);
+
+/* Number of segments (the unit of prefill keep sets, chunk mass and residency). */
+int wnwo_segments(const wnwo_config *cfg, int32_t *n_segments);
 
 /* k, v: [B][L][H_kv][T_a+T_t][d] bf16, referenced (not copied) for the oracle's lifetime.
  * roles: [L][H_kv] (0 anchor, 1 tidal, 2 fixed).  prefill: [B][L][H_kv][T_a] fp32. */
@@ -51,8 +58,9 @@ int wnwo_keep_mask(const wnwo *o, int32_t b, int32_t l, int32_t kv, uint8_t *mas
  *   out       [B][L][H_q][d]         attention outputs (rows of skipped heads are zeroed)
  *   scores    [B][n_chunks]          chunk scores (double)
  *   selected  [B][k]                 selected chunk ids, ascending (-1 pads a forced set)
- *   mass      [B][n_anchor*g][n_chunks] or NULL: per anchor q-head chunk mass
- *   resident  [B][n_chunks] or NULL: 1 where the chunk's complement was attended this step
+ *   mass      [B][n_anchor*g][n_segments] or NULL: per anchor q-head segment mass
+ *   resident  [B][n_segments] or NULL: 1 where the segment's complement was attended this step
+ * With disjoint chunks a segment is a chunk.
  */
 int wnwo_step(wnwo *o, const uint16_t *q, const int32_t *forced, const uint8_t *head_mask,
               double *out, double *scores, int32_t *selected, double *mass, uint8_t *resident);

@@ -15,25 +15,31 @@ SRC = os.path.join(ROOT, "oracle", "wnw_oracle.c")
 
 MUTANTS = {
     "score is a sum, not a mean": (
-        "double sc = a / (double)(chunk_end(c, ch) - chunk_begin(c, ch));", "double sc = a;"),
+        "double sc = a / (double)(seg_end(c, s1) - seg_begin(c, ch));", "double sc = a;"),
     "text rows left out of the anchor softmax": (
         "attend(qh, o->kc + hoff, o->vc + hoff, rows, T, D, x, oh, p);",
         "attend(qh, o->kc + hoff, o->vc + hoff, rows, Ta, D, x, oh, p);"),
     "chunk ties prefer the higher id": (
         "return (x->id > y->id) - (x->id < y->id);", "return (x->id < y->id) - (x->id > y->id);"),
     "eviction lag one step too long": (
-        "now[ch] = st[ch] < o->delta;", "now[ch] = st[ch] <= o->delta;"),
+        "            if (st[ch] < o->delta)\n", "            if (st[ch] <= o->delta)\n"),
     "keep count rounds up": (
         "return (int32_t)(((int64_t)c->budget_bp * len) / 10000);",
         "return (int32_t)(((int64_t)c->budget_bp * len + 9999) / 10000);"),
     "tidal heads ignore recalled chunks": (
-        "(o->roles[hh] == 1 && ru[ch])", "(o->roles[hh] == 1 && 0 && ru[ch])"),
+        "(o->roles[hh] == 1 && ru[sg])", "(o->roles[hh] == 1 && 0 && ru[sg])"),
     "logit scale 1/d": ("1.0 / sqrt((double)d)", "1.0 / (double)d"),
     "prefill ranking keeps the lowest scores": (
         "    const ranked *x = a, *y = b;\n    if (x->s > y->s) return -1;",
         "    const ranked *x = a, *y = b;\n    if (x->s < y->s) return -1;"),
     "selection state not reset on selection": ("if (sel[i] >= 0) st[sel[i]] = 0;", "if (sel[i] >= 0) st[sel[i]] += 0;"),
-    "fixed heads see recalled chunks": ("(o->roles[hh] == 1 && ru[ch])", "(o->roles[hh] >= 1 && ru[ch])"),
+    "fixed heads see recalled chunks": ("(o->roles[hh] == 1 && ru[sg])", "(o->roles[hh] >= 1 && ru[sg])"),
+    "an overlapping chunk covers one segment": (
+        "int32_t last = ch + span_of(c) - 1, ns = seg_count(c);", "int32_t last = ch, ns = seg_count(c);"),
+    "overlapping chunk scored on its first segment": (
+        "for (int32_t sg = ch; sg <= s1; ++sg) a +=", "for (int32_t sg = ch; sg <= ch; ++sg) a +="),
+    "overlapping chunks start every other segment": (
+        "return (span_of(c) == 2 && ns >= 2) ? ns - 1 : ns;", "return (span_of(c) == 2 && ns >= 2) ? ns / 2 : ns;"),
 }
 
 

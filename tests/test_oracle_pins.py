@@ -262,3 +262,94 @@ def test_invalid_configurations_rejected(oracle_mod):
         kw.update(b)
         with pytest.raises(ValueError):
             oracle_mod.geometry(oracle_mod.make_cfg(**kw))
+
+
+# ---- the paper's overlapping chunks (Method, "Chunk Structure"): a chunk is two consecutive
+# segments of chunk_len / 2 positions and one chunk starts at every segment.
+
+def test_span2_geometry(oracle_mod):
+    """Segments of chunk_len / 2; one chunk per segment start except the last; keep counts per
+    segment; odd chunk lengths rejected."""
+    cfg = oracle_mod.make_cfg(1, 1, 4, 1, 8, 100, 4, 16, 2500, chunk_span=2)
+    n, k, kt = oracle_mod.geometry(cfg)
+    assert oracle_mod.segments(cfg) == 13                  # ceil(100 / 8)
+    assert n == 12                                         # chunks start at segments 0..11
+    assert k == (2500 * 100) // (10000 * 16)               # floor(budget * T_a / chunk_len) = 1
+    assert kt == 12 * 2 + (4 * 2500) // 10000              # 12 full segments keep 2, the 4-long one 1
+    with pytest.raises(ValueError):
+        oracle_mod.geometry(oracle_mod.make_cfg(1, 1, 4, 1, 8, 100, 4, 15, 2500, chunk_span=2))
+
+
+def test_span2_residency_trace_matches_hand_worked_segments(oracle_mod):
+    gold = json.load(open(os.path.join(GOLD, "residency_trace_span2.json")))
+    rng = np.random.default_rng(29)
+    B, L, H, D, Ta, Tt, cl = 1, 1, 2, 8, 96, 3, 16           # 12 segments of 8, 11 chunks
+    k, v = _rand_cache(rng, B, L, H, Ta + Tt, D)
+    roles = np.array([[0, 1]], dtype=np.uint8)
+    pf = rng.random((B, L, H, Ta), dtype=np.float32)
+    for mode, key in ((0, "resident_segments_same_step"), (1, "resident_segments_next_step")):
+        cfg = oracle_mod.make_cfg(B, L, H, H, D, Ta, Tt, cl, 2000, top_k=1, evict_lag=gold["delta"],
+                                  next_step=mode, chunk_span=2)
+        o = oracle_mod.Oracle(cfg, k, v, roles, pf)
+        q = f32_to_bf16(rng.standard_normal((B, L, H, D)).astype(np.float32))
+        for s, want in zip(gold["selections"], gold[key]):
+            r = o.step(q, forced=np.array([[s]]))
+            assert list(np.nonzero(r["resident"][0])[0]) == want
+
+
+def test_span2_even_chunks_are_the_disjoint_chunks_of_twice_the_segment(oracle_mod):
+    """Chunk 2j of the overlapping layout covers the same positions as chunk j of the disjoint
+    layout with chunks of two segments: same scores.  Segment masses equal the disjoint layout's
+    chunk masses at one segment per chunk (pinned against SDPA elsewhere)."""
+    rng = np.random.default_rng(31)
+    B, L, H, g, D, Ta, Tt, seg = 2, 2, 3, 2, 8, 96, 4, 6     # 16 full segments, chunks of 12
+    k, v = _rand_cache(rng, B, L, H, Ta + Tt, D)
+    roles = np.array([[0, 1, 2], [1, 0, 0]], dtype=np.uint8)
+    pf = rng.random((B, L, H, Ta), dtype=np.float32)
+    span2 = oracle_mod.Oracle(oracle_mod.make_cfg(B, L, H * g, H, D, Ta, Tt, 2 * seg, 2500, chunk_span=2), k, v, roles, pf)
+    disj = oracle_mod.Oracle(oracle_mod.make_cfg(B, L, H * g, H, D, Ta, Tt, 2 * seg, 2500), k, v, roles, pf)
+    unit = oracle_mod.Oracle(oracle_mod.make_cfg(B, L, H * g, H, D, Ta, Tt, seg, 2500), k, v, roles, pf)
+    assert span2.n_chunks == Ta // seg - 1 and disj.n_chunks == Ta // (2 * seg)
+    for s in range(3):
+        q = f32_to_bf16(rng.standard_normal((B, L, H * g, D)).astype(np.float32))
+        a, b_, u = span2.step(q), disj.step(q), unit.step(q)
+        np.testing.assert_allclose(a["scores"][:, 0::2], b_["scores"], rtol=1e-13, atol=0)
+        np.testing.assert_allclose(a["mass"], u["mass"], rtol=1e-13, atol=1e-300)
+
+
+def test_span2_tidal_heads_attend_over_resident_segments(oracle_mod):
+    """Tidal heads: kept rows + the resident segments (both segments of every resident chunk) +
+    text, against SDPA with that mask; fixed heads: kept rows + text."""
+    rng = np.random.default_rng(37)
+    B, L, H, g, D, Ta, Tt, cl = 2, 2, 3, 2, 8, 64, 4, 16
+    k, v = _rand_cache(rng, B, L, H, Ta + Tt, D)
+    roles = np.array([[0, 1, 2], [1, 2, 0]], dtype=np.uint8)
+    pf = rng.random((B, L, H, Ta), dtype=np.float32)
+    o = oracle_mod.Oracle(oracle_mod.make_cfg(B, L, H * g, H, D, Ta, Tt, cl, 2500, chunk_span=2), k, v, roles, pf)
+    for step in range(4):
+        q = f32_to_bf16(rng.standard_normal((B, L, H * g, D)).astype(np.float32))
+        r = o.step(q)
+        for b in range(B):
+            segs = set()
+            for c in r["selected"][b]:
+                segs |= {int(c), int(c) + 1}
+            assert segs <= set(np.nonzero(r["resident"][b])[0].tolist())
+        for b, l, hq in itertools.product(range(B), range(L), range(H * g)):
+            h = hq // g
+            mask = np.ones(Ta + Tt, dtype=bool)
+            if roles[l, h] != 0:
+                keep = o.keep_mask(b, l, h).astype(bool)
+                if roles[l, h] == 1:
+                    keep |= np.repeat(r["resident"][b].astype(bool), cl // 2)[:Ta]
+                mask[:Ta] = keep
+            ref = _sdpa(q[b, l, hq], k[b, l, h], v[b, l, h], mask)
+            np.testing.assert_allclose(r["out"][b, l, hq], ref, rtol=0, atol=1e-12)
+
+
+def test_span2_selection_is_topk_of_fp32_scores(oracle_mod):
+    o, k, v, roles, pf, q = _small(oracle_mod, seed=41, Ta=96, Tt=4, cl=8, budget=2500, chunk_span=2)
+    for s in range(3):
+        qs = f32_to_bf16(np.random.default_rng(300 + s).standard_normal(q.shape).astype(np.float32))
+        r = o.step(qs)
+        for b in range(q.shape[0]):
+            assert list(r["selected"][b]) == _brute_topk(list(r["scores"][b].astype(np.float32)), o.k)
