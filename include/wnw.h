@@ -27,13 +27,15 @@
  *   out        [B][L][H_q][d]              fp32
  *   scores     [B][n_chunks]               fp32
  *   selected   [B][k]                      int32 chunk ids, ascending
+ *   resident   [B][n_segments]             flags (wnw_debug_read_resident)
  *
- * Chunks are disjoint runs of chunk_len audio positions (a chunk is one segment; the last chunk
- * may be shorter).  k defaults to floor(budget * T_a / chunk_len); each tidal/fixed head keeps
- * floor(budget * len) positions of every chunk, chosen by the caller's prefill scores (Method,
- * "Prefill Compression"); ties prefer the lower position.  Chunk ranking breaks ties by the lower
- * chunk id.  A chunk is resident at step s iff it was selected at one of the last delta steps
- * (s - delta + 1 .. s).
+ * Segments are runs of chunk_len audio positions (chunk_len / 2 with WNW_F_OVERLAP_CHUNKS); the
+ * last one may be shorter.  By default a chunk is one segment.  k defaults to
+ * floor(budget * T_a / chunk_len); each tidal/fixed head keeps floor(budget * len) positions of
+ * every segment, chosen by the caller's prefill scores (Method, "Prefill Compression"); ties
+ * prefer the lower position.  Chunk ranking breaks ties by the lower chunk id.  A chunk is
+ * resident at step s iff it was selected at one of the last delta steps (s - delta + 1 .. s); a
+ * segment is resident iff a resident chunk covers it.
  *
  * Errors: every call returns a wnw_status; no C++ exception crosses the ABI.  A failing HIP call
  * turns the context sticky: every later call on it returns WNW_ERR_STATE.  wnw_last_error gives
@@ -75,7 +77,14 @@ enum {
      * pinned memory, copy them to their slots and attend to them in the same pass. */
     WNW_F_RECALL_MEMCPY = 2u,
     /* Record HIP events around the kernels of every step; wnw_get_stats reports the times. */
-    WNW_F_TIMING = 4u
+    WNW_F_TIMING = 4u,
+    /* The paper's chunk structure (Method, "Chunk Structure"): a chunk is two consecutive
+     * segments of chunk_len / 2 positions and a chunk starts at every segment (stride one
+     * segment), so there is one chunk fewer than segments.  Selection and eviction streaks are
+     * per chunk; keep sets, masses, residency, slots and recall are per segment (a resident
+     * chunk makes both its segments resident).  chunk_len must be even.  Default: disjoint
+     * chunks of chunk_len positions, each its own segment. */
+    WNW_F_OVERLAP_CHUNKS = 8u
 };
 
 typedef struct wnw_ctx wnw_ctx;
@@ -160,10 +169,15 @@ wnw_status wnw_set_roles(wnw_ctx *ctx, const uint8_t *roles, const float *prefil
 wnw_status wnw_decode_step(wnw_ctx *ctx, const void *q_dev, float *out_dev,
                            float *chunk_scores_dev, int32_t *selected_dev, void *hip_stream);
 
-/* Derived sizes: chunks, k, kept audio rows per tidal/fixed head, recall slots per sequence,
- * and bytes of one recalled chunk of one sequence.  Any pointer may be NULL. */
+/* Derived sizes: chunks (the selection's candidates), k, kept audio rows per tidal/fixed head,
+ * recall slots per sequence, and bytes of one recalled segment of one sequence (all tidal
+ * heads; a segment is a chunk unless WNW_F_OVERLAP_CHUNKS).  Any pointer may be NULL. */
 wnw_status wnw_query_geometry(const wnw_ctx *ctx, int32_t *n_chunks, int32_t *k,
                               int32_t *keep_total, int32_t *n_slots, int64_t *chunk_bytes);
+
+/* Number of segments (the unit of residency and recall; equal to n_chunks unless
+ * WNW_F_OVERLAP_CHUNKS, then n_chunks + 1).  The pointer may be NULL. */
+wnw_status wnw_query_segments(const wnw_ctx *ctx, int32_t *n_segments);
 
 /* Counters and (with WNW_F_TIMING) kernel times; waits for the device. */
 wnw_status wnw_get_stats(wnw_ctx *ctx, wnw_stats *out);
@@ -174,18 +188,18 @@ wnw_status wnw_get_stats(wnw_ctx *ctx, wnw_stats *out);
  * a recall load. */
 wnw_status wnw_set_selection_override(wnw_ctx *ctx, const int32_t *sel_dev);
 
-/* Copy the device slot holding the recalled complement of (b, chunk) to host_dst (waits for
- * the device).  Valid for chunks resident after the last step (with WNW_F_SELECT_NEXT_STEP, also
- * those recalled during it).  Layout [n_tidal][2 (K, V)][comp_max][d] bf16; `bytes` must equal chunk_bytes.
- * WNW_ERR_INVALID if that chunk is not resident. */
+/* Copy the device slot holding the recalled complement of (b, segment) to host_dst (waits for
+ * the device).  Valid for segments resident after the last step (with WNW_F_SELECT_NEXT_STEP,
+ * also those recalled during it).  Layout [n_tidal][2 (K, V)][comp_max][d] bf16; `bytes` must
+ * equal chunk_bytes.  WNW_ERR_INVALID if that segment is not resident. */
 wnw_status wnw_debug_read_slot(wnw_ctx *ctx, int32_t b, int32_t chunk, void *host_dst, size_t bytes);
 
-/* Copy the host (pinned) complement of (b, chunk) in the same layout as wnw_debug_read_slot. */
+/* Copy the host (pinned) complement of (b, segment) in the same layout as wnw_debug_read_slot. */
 wnw_status wnw_debug_read_host_chunk(wnw_ctx *ctx, int32_t b, int32_t chunk, void *host_dst, size_t bytes);
 
-/* Flags [B][n_chunks] (uint8) of the complements the last step's tidal heads attended: the
- * resident set of that step, or of the step before it with WNW_F_SELECT_NEXT_STEP (waits for
- * the device). */
+/* Flags [B][n_segments] (uint8) of the segment complements the last step's tidal heads
+ * attended: the resident set of that step, or of the step before it with
+ * WNW_F_SELECT_NEXT_STEP (waits for the device). */
 wnw_status wnw_debug_read_resident(wnw_ctx *ctx, uint8_t *host_dst);
 
 /* Message of the last failure on ctx (or of this thread when ctx is NULL).  Never NULL. */

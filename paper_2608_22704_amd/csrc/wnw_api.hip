@@ -137,13 +137,17 @@ wnw_status derive(wnw_ctx *c, const wnw_config &cfg, Geometry &g)
     if (cfg.chunk_len < 1) return fail(c, WNW_ERR_INVALID, "chunk_len must be >= 1");
     if (cfg.budget_bp < 0 || cfg.budget_bp > 10000) return fail(c, WNW_ERR_INVALID, "budget_bp must be in 0..10000");
     if (cfg.top_k < 0 || cfg.evict_lag < 0) return fail(c, WNW_ERR_INVALID, "top_k and evict_lag must be >= 0");
-    if (cfg.flags & ~(uint32_t)(WNW_F_SELECT_NEXT_STEP | WNW_F_RECALL_MEMCPY | WNW_F_TIMING))
+    if (cfg.flags & ~(uint32_t)(WNW_F_SELECT_NEXT_STEP | WNW_F_RECALL_MEMCPY | WNW_F_TIMING | WNW_F_OVERLAP_CHUNKS))
         return fail(c, WNW_ERR_INVALID, "unknown flag bits 0x%x", cfg.flags);
+    const int span = (cfg.flags & WNW_F_OVERLAP_CHUNKS) ? 2 : 1;
+    if (span == 2 && cfg.chunk_len % 2)
+        return fail(c, WNW_ERR_INVALID, "overlapping chunks need an even chunk_len (two segments), got %d", cfg.chunk_len);
     if (cfg.head_dim != D) return fail(c, WNW_ERR_UNSUPPORTED, "head_dim %d: only 128 is implemented", cfg.head_dim);
     const int G = cfg.q_heads / cfg.kv_heads;
     if (G != 1 && G != 2 && G != 3 && G != 4 && G != 6 && G != 8)
         return fail(c, WNW_ERR_UNSUPPORTED, "GQA group %d: implemented for 1, 2, 3, 4, 6, 8", G);
-    if (cfg.chunk_len > MAX_CHUNK) return fail(c, WNW_ERR_UNSUPPORTED, "chunk_len %d > %d", cfg.chunk_len, MAX_CHUNK);
+    if (cfg.chunk_len / span > MAX_CHUNK)
+        return fail(c, WNW_ERR_UNSUPPORTED, "segments of %d positions > %d", cfg.chunk_len / span, MAX_CHUNK);
 
     g = Geometry{};
     g.B = cfg.batch;
@@ -154,11 +158,14 @@ wnw_status derive(wnw_ctx *c, const wnw_config &cfg, Geometry &g)
     g.Ta = cfg.audio_len;
     g.Tt = cfg.text_len;
     g.T = g.Ta + g.Tt;
-    g.cl = cfg.chunk_len;
+    g.span = span;
+    g.cl = cfg.chunk_len / span;   // segment length
     g.budget_bp = cfg.budget_bp;
     g.nc = (g.Ta + g.cl - 1) / g.cl;
-    g.k = cfg.top_k ? cfg.top_k : (int)(((int64_t)cfg.budget_bp * g.Ta) / (10000LL * g.cl));
-    if (g.k > g.nc) return fail(c, WNW_ERR_INVALID, "top_k %d exceeds the %d chunks", g.k, g.nc);
+    g.nchk = (span == 2 && g.nc >= 2) ? g.nc - 1 : g.nc;
+    g.k = cfg.top_k ? cfg.top_k : (int)(((int64_t)cfg.budget_bp * g.Ta) / (10000LL * cfg.chunk_len));
+    if (g.k > g.nchk) return fail(c, WNW_ERR_INVALID, "top_k %d exceeds the %d chunks", g.k, g.nchk);
+    g.knew = std::min(g.nc, span * g.k);
     g.delta = cfg.evict_lag ? cfg.evict_lag : 3;
     g.next_step = (cfg.flags & WNW_F_SELECT_NEXT_STEP) ? 1 : 0;
     g.keep_total = 0;
@@ -169,9 +176,10 @@ wnw_status derive(wnw_ctx *c, const wnw_config &cfg, Geometry &g)
         g.comp_max = std::max(g.comp_max, comp_of(g, ch));
     }
     g.Rs = g.keep_total + g.Tt;
-    // Slots: the resident set holds at most delta * k chunks.  With next-step timing the chunks
-    // dropped at a step keep their slots until that step's attention has read them: k more.
-    const int64_t ns = ((int64_t)g.delta + g.next_step) * g.k;
+    // Slots: the resident set holds at most delta * k chunks, i.e. span * delta * k segments.
+    // With next-step timing the segments dropped at a step keep their slots until that step's
+    // attention has read them: span * k more.  Never more than one per segment.
+    const int64_t ns = std::min<int64_t>(g.nc, ((int64_t)g.delta + g.next_step) * span * g.k);
     if (ns > 4096) return fail(c, WNW_ERR_UNSUPPORTED, "%lld recall slots > 4096", (long long)ns);
     g.n_slots = (int)ns;
     if (select_shared_bytes(g) > 150 * 1024)
@@ -183,9 +191,10 @@ wnw_status derive(wnw_ctx *c, const wnw_config &cfg, Geometry &g)
     g.n_tiles_s = (g.Rs + TILE_S - 1) / TILE_S;
     g.slot_tile = g.comp_max <= TILE_S ? TILE_S : 2 * TILE_S;
     g.sg = g.comp_max > 0 ? g.slot_tile / g.comp_max : 1;
-    // the kept list holds at most delta * k entries in both timings
-    g.ng_kept = g.comp_max > 0 ? (g.delta * g.k + g.sg - 1) / g.sg : 0;
-    g.np = g.n_tiles_s + g.ng_kept + (g.comp_max > 0 ? g.k : 0);
+    // the kept list holds at most the resident segments (span * delta * k) in both timings
+    const int kept_max = (int)std::min<int64_t>(g.nc, (int64_t)g.delta * span * g.k);
+    g.ng_kept = g.comp_max > 0 ? (kept_max + g.sg - 1) / g.sg : 0;
+    g.np = g.n_tiles_s + g.ng_kept + (g.comp_max > 0 ? g.knew : 0);
     if ((int64_t)g.np * G * 4 > 65536) return fail(c, WNW_ERR_UNSUPPORTED, "too many partial tiles per head");
     if (g.B > 65535 || (int64_t)g.L * g.Hkv > 65535) return fail(c, WNW_ERR_UNSUPPORTED, "batch or head count too large");
     return WNW_OK;
@@ -235,9 +244,9 @@ wnw_status issue_copies(wnw_ctx *c, hipStream_t st)
         const int n = cnt[b * 2 + 1];
         for (int i = 0; i < n;) {
             int j = i + 1;
-            const int32_t *e0 = nl + ((size_t)b * g.k + i) * 2;
+            const int32_t *e0 = nl + ((size_t)b * g.knew + i) * 2;
             while (j < n) {
-                const int32_t *ej = nl + ((size_t)b * g.k + j) * 2;
+                const int32_t *ej = nl + ((size_t)b * g.knew + j) * 2;
                 if (ej[0] != e0[0] + (j - i) || ej[1] != e0[1] + (j - i)) break;
                 ++j;
             }
@@ -355,7 +364,7 @@ wnw_status wnw_set_roles(wnw_ctx *c, const uint8_t *roles, const float *prefill)
     ALLOC(c->fV, B * g.nF * g.Rs * Dz, "fixed V");
     ALLOC(c->slots, B * g.n_slots * g.chunk_elems, "recall slots");
     ALLOC(c->d_lk, (size_t)nh, "role tables");
-    ALLOC(c->scores_int, B * g.nc, "scores");
+    ALLOC(c->scores_int, B * g.nchk, "scores");
     ALLOC(c->sel_int, B * g.k, "selection");
     StepBuffers &s = c->s;
     ALLOC(s.pa_m, B * g.nA * g.n_tiles_a * g.G, "anchor partial max");
@@ -366,7 +375,7 @@ wnw_status wnw_set_roles(wnw_ctx *c, const uint8_t *roles, const float *prefill)
     ALLOC(s.ps_m, B * (g.nT + g.nF) * g.np * g.G, "partial max");
     ALLOC(s.ps_l, B * (g.nT + g.nF) * g.np * g.G, "partial sum");
     ALLOC(s.ps_o, B * (g.nT + g.nF) * g.np * g.G * Dz, "partial out");
-    ALLOC(s.streak, B * g.nc, "streaks");
+    ALLOC(s.streak, B * g.nchk, "streaks");
     ALLOC(s.slot_of, B * g.nc, "slot map");
     ALLOC(s.slot_last, B * g.nc, "slot history");
     ALLOC(s.att, B * g.nc, "attended complements");
@@ -375,7 +384,7 @@ wnw_status wnw_set_roles(wnw_ctx *c, const uint8_t *roles, const float *prefill)
     ALLOC(s.slot_since, B * g.n_slots, "slot ages");
     ALLOC(s.step, B, "step counters");
     ALLOC(s.kept_list, B * g.n_slots * 2, "kept list");
-    ALLOC(s.new_list, 2 * B * g.k * 2, "new lists");   // two, alternating by step
+    ALLOC(s.new_list, 2 * B * g.knew * 2, "new lists");   // two, alternating by step
     ALLOC(s.counts, 2 * B * 2, "counts");
     ALLOC(s.stats, 8, "stats");
 #undef ALLOC
@@ -391,7 +400,7 @@ wnw_status wnw_set_roles(wnw_ctx *c, const uint8_t *roles, const float *prefill)
         HIPCHECK(c, hipHostGetDevicePointer(&dp, c->host_comp, 0));
         c->t.host_comp = (const uint16_t *)dp;
     }
-    HIPCHECK(c, hipHostMalloc((void **)&c->h_newinfo, (B * 2 + B * g.k * 2 + 1) * sizeof(int32_t), hipHostMallocDefault));
+    HIPCHECK(c, hipHostMalloc((void **)&c->h_newinfo, (B * 2 + B * g.knew * 2 + 1) * sizeof(int32_t), hipHostMallocDefault));
     HIPCHECK(c, hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking));
     HIPCHECK(c, hipEventCreateWithFlags(&c->ev_sel, hipEventDisableTiming));
     HIPCHECK(c, hipEventCreateWithFlags(&c->ev_rec, hipEventDisableTiming));
@@ -489,7 +498,7 @@ wnw_status wnw_set_roles(wnw_ctx *c, const uint8_t *roles, const float *prefill)
     cleanup();
 
     // ---- selection state -----------------------------------------------------------------------
-    std::vector<int32_t> init(B * g.nc, g.delta);   // never selected: not resident
+    std::vector<int32_t> init(B * g.nchk, g.delta);   // never selected: not resident
     if (!init.empty()) HIPCHECK(c, hipMemcpy(s.streak, init.data(), init.size() * sizeof(int32_t), hipMemcpyHostToDevice));
     if (g.nc) HIPCHECK(c, hipMemset(s.slot_of, 0xff, B * g.nc * sizeof(int32_t)));
     if (g.nc) HIPCHECK(c, hipMemset(s.slot_last, 0xff, B * g.nc * sizeof(int32_t)));
@@ -542,7 +551,7 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, float *out, float *sco
     StepBuffers sb = c->s;
     const int par = (int)(c->steps & 1);
     sb.counts += (size_t)par * g.B * 2;
-    sb.new_list += (size_t)par * g.B * g.k * 2;
+    sb.new_list += (size_t)par * g.B * g.knew * 2;
 
     // (1) anchor attention + chunk mass, (2) scores, top-k and residency.  With next-step
     // timing the static tidal/fixed tiles (kept rows + text) join the anchor launch.
@@ -567,8 +576,8 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, float *out, float *sco
             HIPCHECK(c, launch_recall(g, c->t, sb, c->side));
         } else {
             HIPCHECK(c, hipMemcpyAsync(c->h_newinfo, sb.counts, g.B * 2 * sizeof(int32_t), hipMemcpyDeviceToHost, c->side));
-            if (g.k)
-                HIPCHECK(c, hipMemcpyAsync(c->h_newinfo + g.B * 2, sb.new_list, (size_t)g.B * g.k * 2 * sizeof(int32_t),
+            if (g.knew)
+                HIPCHECK(c, hipMemcpyAsync(c->h_newinfo + g.B * 2, sb.new_list, (size_t)g.B * g.knew * 2 * sizeof(int32_t),
                                            hipMemcpyDeviceToHost, c->side));
             HIPCHECK(c, hipEventRecord(c->ev_nl, c->side));
         }
@@ -600,8 +609,8 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, float *out, float *sco
         MARK(4);
     } else {
         HIPCHECK(c, hipMemcpyAsync(c->h_newinfo, sb.counts, g.B * 2 * sizeof(int32_t), hipMemcpyDeviceToHost, s0));
-        if (g.k)
-            HIPCHECK(c, hipMemcpyAsync(c->h_newinfo + g.B * 2, sb.new_list, (size_t)g.B * g.k * 2 * sizeof(int32_t),
+        if (g.knew)
+            HIPCHECK(c, hipMemcpyAsync(c->h_newinfo + g.B * 2, sb.new_list, (size_t)g.B * g.knew * 2 * sizeof(int32_t),
                                        hipMemcpyDeviceToHost, s0));
         HIPCHECK(c, hipEventRecord(c->ev_sel, s0));
         MARK(2);
@@ -634,7 +643,7 @@ wnw_status wnw_query_geometry(const wnw_ctx *c, int32_t *n_chunks, int32_t *k, i
                               int64_t *chunk_bytes)
 {
     if (!c) return fail(nullptr, WNW_ERR_INVALID, "ctx is NULL");
-    if (n_chunks) *n_chunks = c->g.nc;
+    if (n_chunks) *n_chunks = c->g.nchk;
     if (k) *k = c->g.k;
     if (keep_total) *keep_total = c->g.keep_total;
     if (n_slots) *n_slots = c->g.n_slots;
@@ -642,6 +651,13 @@ wnw_status wnw_query_geometry(const wnw_ctx *c, int32_t *n_chunks, int32_t *k, i
         if (c->state == CREATED) return fail(const_cast<wnw_ctx *>(c), WNW_ERR_STATE, "chunk size is known after wnw_set_roles");
         *chunk_bytes = c->g.chunk_elems * (int64_t)sizeof(uint16_t);
     }
+    return WNW_OK;
+}
+
+wnw_status wnw_query_segments(const wnw_ctx *c, int32_t *n_segments)
+{
+    if (!c) return fail(nullptr, WNW_ERR_INVALID, "ctx is NULL");
+    if (n_segments) *n_segments = c->g.nc;
     return WNW_OK;
 }
 
@@ -697,7 +713,7 @@ wnw_status wnw_debug_read_slot(wnw_ctx *c, int32_t b, int32_t chunk, void *dst, 
     if (!c || !dst) return fail(c, WNW_ERR_INVALID, "ctx and host_dst must not be NULL");
     if (c->state != READY) return fail(c, WNW_ERR_STATE, "context not ready");
     const Geometry &g = c->g;
-    if (b < 0 || b >= g.B || chunk < 0 || chunk >= g.nc) return fail(c, WNW_ERR_INVALID, "(b, chunk) out of range");
+    if (b < 0 || b >= g.B || chunk < 0 || chunk >= g.nc) return fail(c, WNW_ERR_INVALID, "(b, segment) out of range");
     if (bytes != (size_t)g.chunk_elems * sizeof(uint16_t)) return fail(c, WNW_ERR_INVALID, "bytes must equal chunk_bytes");
     DeviceGuard dg(c->device);
     HIPCHECK(c, hipDeviceSynchronize());
@@ -713,7 +729,7 @@ wnw_status wnw_debug_read_host_chunk(wnw_ctx *c, int32_t b, int32_t chunk, void 
     if (!c || !dst) return fail(c, WNW_ERR_INVALID, "ctx and host_dst must not be NULL");
     if (c->state != READY) return fail(c, WNW_ERR_STATE, "context not ready");
     const Geometry &g = c->g;
-    if (b < 0 || b >= g.B || chunk < 0 || chunk >= g.nc) return fail(c, WNW_ERR_INVALID, "(b, chunk) out of range");
+    if (b < 0 || b >= g.B || chunk < 0 || chunk >= g.nc) return fail(c, WNW_ERR_INVALID, "(b, segment) out of range");
     if (bytes != (size_t)g.chunk_elems * sizeof(uint16_t)) return fail(c, WNW_ERR_INVALID, "bytes must equal chunk_bytes");
     if (bytes) memcpy(dst, c->host_comp + ((size_t)b * g.nc + chunk) * g.chunk_elems, bytes);
     return WNW_OK;

@@ -18,19 +18,24 @@ constexpr int SCORE_PARTS = 4;   // fixed ranges of anchor q-heads summed per ch
 struct Geometry {
     int B, L, Hq, Hkv, G;
     int Ta, Tt, T;              // audio, text and total rows of an anchor head
-    int cl, budget_bp;          // chunk length, retention in basis points
-    int nc, k, delta;           // chunks, selected per step, eviction lag
+    int cl, budget_bp;          // segment length (the unit of keep sets, masses, residency,
+                                // slots and recall), retention in basis points
+    int span;                   // segments per chunk: 1 disjoint chunks, 2 overlapping chunks
+    int nc;                     // segments
+    int nchk;                   // chunks (the selection's candidates): segments - span + 1
+    int k, knew, delta;         // chunks selected per step, segments newly resident per step at
+                                // most (span * k), eviction lag
     int next_step;              // 1: tidal heads of step s attend over the resident set of step s-1
     int keep_total, Rs;         // kept audio rows per non-anchor head; static rows = keep + text
     int comp_max;               // complement rows of a full chunk (chunk_len - keep(chunk_len))
-    int n_slots;                // recall slots per sequence (delta * k)
+    int n_slots;                // recall slots per sequence
     int nA, nT, nF;             // anchor / tidal / fixed KV-heads over all layers
     int n_tiles_a, maxc;        // anchor tiles per head, chunk entries per anchor tile
     int n_tiles_s;              // static tiles per tidal/fixed head
     int slot_tile;              // rows of one slot-group work-group (TILE_S or 2 * TILE_S)
     int sg;                     // slots per slot-group work-group
     int ng_kept;                // slot groups for kept complements (new ones: one partial each)
-    int np;                     // partial entries per tidal/fixed head: static tiles, kept groups, k new
+    int np;                     // partial entries per tidal/fixed head: static tiles, kept groups, knew new
     int64_t chunk_elems;        // bf16 elements of one recalled chunk of one sequence
 };
 
@@ -68,17 +73,17 @@ struct StepBuffers {
     // tidal/fixed partials, head index = tidal 0..nT-1 then fixed nT..nT+nF-1
     float *ps_m, *ps_l;         // [B][nT+nF][np][G]
     float *ps_o;                // [B][nT+nF][np][G][D]
-    // selection state
-    int32_t *streak;            // [B][nc]
-    int32_t *slot_of;           // [B][nc]  slot holding the chunk's complement or -1
-    int32_t *slot_last;         // [B][nc]  slot that last received the chunk's bytes or -1
-    int32_t *slot_data;         // [B][n_slots] chunk whose bytes the slot holds or -1
+    // selection state (chunks for the selection and streaks; segments for everything else)
+    int32_t *streak;            // [B][nchk] steps since the chunk's last selection, capped at delta
+    int32_t *slot_of;           // [B][nc]  slot holding the segment's complement or -1
+    int32_t *slot_last;         // [B][nc]  slot that last received the segment's bytes or -1
+    int32_t *slot_data;         // [B][n_slots] segment whose bytes the slot holds or -1
     int32_t *slot_busy;         // [B][n_slots] 0 free, 1 owned, 2 freed once this step has read it
     int32_t *slot_since;        // [B][n_slots] step at which the slot was last freed
     int32_t *step;              // [B] steps run
-    int32_t *att;               // [B][nc]  complements attended by the last step
-    int32_t *kept_list;         // [B][n_slots][2] (chunk, slot) resident before and now
-    int32_t *new_list;          // [B][k][2]       (chunk, slot) newly resident this step
+    int32_t *att;               // [B][nc]  segment complements attended by the last step
+    int32_t *kept_list;         // [B][n_slots][2] (segment, slot) attended from a filled slot
+    int32_t *new_list;          // [B][knew][2]    (segment, slot) newly resident this step
     int32_t *counts;            // [B][2] kept, new
     unsigned long long *stats;  // [8] recalled, dropped, resident, slot_rows, peak, exhausted, revived
 };

@@ -515,16 +515,22 @@ __device__ int block_scan_excl(int *a, int n, int *wsum)
 
 
 
-// Per sequence b (state staged in shared memory, written back at the end):
-//   scores   score_c = (sum over anchor q-heads of their chunk mass) / |c|, double, fixed order
-//   select   top-k by (fp32 score desc, id asc), or the caller's override
-//   streaks  0 when selected, else +1 (capped at delta); resident iff streak < delta
-//   attended this step: the resident set R_s (same-step timing) or R_{s-1} (next-step timing)
-//   slots    a chunk that stops being resident frees its slot (next-step timing: one step later,
-//            after this step's attention has read it); a newly resident chunk whose bytes still
-//            sit in a free slot (never overwritten since) takes it back with no copy; the others
-//            take free slots in least-recently-freed order (never-used slots first) and are
-//            listed for recall
+// Per sequence b (state staged in shared memory, written back at the end).  Chunks (nchk) are
+// the selection's candidates; segments (nc) are the unit of masses, residency, slots and
+// recall.  With disjoint chunks a chunk is a segment; with overlapping chunks chunk c is
+// segments c and c + 1.
+//   scores   score_c = (sum over anchor q-heads and the chunk's segments of their mass) / |c|,
+//            double, fixed order
+//   select   top-k chunks by (fp32 score desc, id asc), or the caller's override
+//   streaks  per chunk: 0 when selected, else +1 (capped at delta); a chunk is resident iff its
+//            streak < delta, a segment iff a resident chunk covers it
+//   attended this step: the resident segments of this step (same-step timing) or of the step
+//            before (next-step timing)
+//   slots    a segment that stops being resident frees its slot (next-step timing: one step
+//            later, after this step's attention has read it); a newly resident segment whose
+//            bytes still sit in a free slot (never overwritten since) takes it back with no copy;
+//            the others take free slots in least-recently-freed order (never-used slots first)
+//            and are listed for recall
 //   lists    kept list = attended this step with bytes already on the device; new list = to
 //            recall (attended in the same launch with same-step timing, from the next step on
 //            with next-step timing)
@@ -532,40 +538,42 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
                                                              const int32_t *__restrict__ ovr, int32_t *__restrict__ selected)
 {
     const int b = blockIdx.x, tid = threadIdx.x, nthr = blockDim.x;
-    const int nc = g.nc, k = g.k, ns = g.n_slots, naq = g.nA * g.G;
-    const bool nxt = g.next_step;
+    const int nu = g.nc, nk = g.nchk, k = g.k, ns = g.n_slots, naq = g.nA * g.G;
+    const bool nxt = g.next_step, two = g.span == 2;
     extern __shared__ double sdyn[];
-    double *part = sdyn;                              // [SCORE_PARTS][nc]
-    float *sc = (float *)(part + SCORE_PARTS * nc);   // [nc]
-    int *fsel = (int *)(sc + nc);                     // [nc] selected
-    int *st = fsel + nc;                              // [nc] streak
-    int *sof = st + nc;                               // [nc] slot of the chunk or -1
-    int *slast = sof + nc;                            // [nc] slot that last received the chunk
-    int *fnew = slast + nc;                           // [nc] to recall
-    int *fkept = fnew + nc;                           // [nc] attended from a slot already filled
-    int *fdrop = fkept + nc;                          // [nc] leaves the resident set
-    int *rank = fdrop + nc;                           // [nc] scan scratch
-    int *busy = rank + nc;                            // [ns] 0 free, 1 owned, 2 freed after this step
-    int *sdata = busy + ns;                           // [ns] chunk whose bytes the slot holds
+    double *part = sdyn;                              // [SCORE_PARTS][nu]; row 0 then segment sums
+    float *sc = (float *)(part + SCORE_PARTS * nu);   // [nk] chunk scores
+    int *fsel = (int *)(sc + nu);                     // [nk] selected
+    int *st = fsel + nu;                              // [nk] streak
+    int *sof = st + nu;                               // [nu] slot of the segment or -1
+    int *slast = sof + nu;                            // [nu] slot that last received the segment
+    int *fnew = slast + nu;                           // [nu] to recall
+    int *fkept = fnew + nu;                           // [nu] attended from a slot already filled
+    int *fdrop = fkept + nu;                          // [nu] leaves the resident set
+    int *rank = fdrop + nu;                           // [nu] scan scratch
+    int *busy = rank + nu;                            // [ns] 0 free, 1 owned, 2 freed after this step
+    int *sdata = busy + ns;                           // [ns] segment whose bytes the slot holds
     int *since = sdata + ns;                          // [ns] step at which the slot was freed
     int *skey = since + ns;                           // [ns] ordering key of free slots
     int *freelist = skey + ns;                        // [ns] free slots in order
     __shared__ int wsum[SEL_THREADS / 64 + 1];
     __shared__ int ndrop, nrows, nrev, nfree;
 
-    int32_t *g_streak = s.streak + (size_t)b * nc, *g_slot_of = s.slot_of + (size_t)b * nc;
-    int32_t *g_slot_last = s.slot_last + (size_t)b * nc;
-    int32_t *g_att = s.att + (size_t)b * nc;
+    int32_t *g_streak = s.streak + (size_t)b * nk, *g_slot_of = s.slot_of + (size_t)b * nu;
+    int32_t *g_slot_last = s.slot_last + (size_t)b * nu;
+    int32_t *g_att = s.att + (size_t)b * nu;
     int32_t *g_data = s.slot_data + (size_t)b * ns, *g_busy = s.slot_busy + (size_t)b * ns;
     int32_t *g_since = s.slot_since + (size_t)b * ns;
     const int step = s.step[b];
 
-    // state in, chunk scores
-    for (int c = tid; c < nc; c += nthr) {
+    // state in, segment masses
+    for (int c = tid; c < nk; c += nthr) {
         st[c] = g_streak[c];
-        sof[c] = g_slot_of[c];
-        slast[c] = g_slot_last[c];
         fsel[c] = 0;
+    }
+    for (int u = tid; u < nu; u += nthr) {
+        sof[u] = g_slot_of[u];
+        slast[u] = g_slot_last[u];
     }
     for (int i = tid; i < ns; i += nthr) {
         const int bz = g_busy[i];
@@ -573,23 +581,30 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
         sdata[i] = g_data[i];
         since[i] = g_since[i];
     }
-    for (int idx = tid; idx < SCORE_PARTS * nc; idx += nthr) {
-        const int p = idx / nc, c = idx - p * nc;
+    for (int idx = tid; idx < SCORE_PARTS * nu; idx += nthr) {
+        const int p = idx / nu, u = idx - p * nu;
         const int a0 = p * naq / SCORE_PARTS, a1 = (p + 1) * naq / SCORE_PARTS;
-        const double *m = s.mass + ((size_t)b * naq + a0) * nc + c;
+        const double *m = s.mass + ((size_t)b * naq + a0) * nu + u;
         double acc = 0.0;
 #pragma unroll 8
-        for (int a = a0; a < a1; ++a) acc += m[(size_t)(a - a0) * nc];
+        for (int a = a0; a < a1; ++a) acc += m[(size_t)(a - a0) * nu];
         part[idx] = acc;
     }
     if (tid == 0) ndrop = nrows = nrev = nfree = 0;
     __syncthreads();
-    for (int c = tid; c < nc; c += nthr) {
-        double acc = part[c];
-        for (int p = 1; p < SCORE_PARTS; ++p) acc += part[p * nc + c];
-        const float v = (float)(acc / (double)chunk_len_of(g, c));
+    for (int u = tid; u < nu; u += nthr) {
+        double acc = part[u];
+        for (int p = 1; p < SCORE_PARTS; ++p) acc += part[p * nu + u];
+        part[u] = acc;                                // each thread rewrites only its own segment
+    }
+    __syncthreads();
+    for (int c = tid; c < nk; c += nthr) {
+        const bool pair = two && c + 1 < nu;
+        const double acc = pair ? part[c] + part[c + 1] : part[c];
+        const int len = chunk_len_of(g, c) + (pair ? chunk_len_of(g, c + 1) : 0);
+        const float v = (float)(acc / (double)len);
         sc[c] = v;
-        scores[(size_t)b * nc + c] = v;
+        scores[(size_t)b * nk + c] = v;
     }
     __syncthreads();
 
@@ -597,60 +612,60 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
     if (ovr) {
         for (int i = tid; i < k; i += nthr) {
             const int c = ovr[(size_t)b * k + i];
-            if (c >= 0 && c < nc) fsel[c] = 1;
+            if (c >= 0 && c < nk) fsel[c] = 1;
         }
     } else {
-        for (int c = tid; c < nc; c += nthr) {
+        for (int c = tid; c < nk; c += nthr) {
             const float v = sc[c];
             int cnt = 0;
-            for (int j = 0; j < nc; ++j) {
-                const float u = sc[j];
-                cnt += (u > v) || (u == v && j < c);
+            for (int j = 0; j < nk; ++j) {
+                const float w = sc[j];
+                cnt += (w > v) || (w == v && j < c);
             }
             fsel[c] = cnt < k;
         }
     }
     __syncthreads();
+    for (int c = tid; c < nk; c += nthr) st[c] = fsel[c] ? 0 : min(st[c] + 1, g.delta);
+    __syncthreads();
 
-    // streaks, residency, drops
-    for (int c = tid; c < nc; c += nthr) {
-        const int stc = fsel[c] ? 0 : min(st[c] + 1, g.delta);
-        st[c] = stc;
-        const bool now = stc < g.delta;
-        const bool owned = sof[c] >= 0;     // has a slot: resident after the previous step
-        fdrop[c] = owned && !now;
-        fnew[c] = now && !owned;
-        fkept[c] = nxt ? owned : (now && owned);
+    // segment residency, drops
+    for (int u = tid; u < nu; u += nthr) {
+        const bool now = (u < nk && st[u] < g.delta) || (two && u >= 1 && u - 1 < nk && st[u - 1] < g.delta);
+        const bool owned = sof[u] >= 0;     // has a slot: resident after the previous step
+        fdrop[u] = owned && !now;
+        fnew[u] = now && !owned;
+        fkept[u] = nxt ? owned : (now && owned);
         const bool att = nxt ? owned : now;
-        g_att[c] = att;
-        if (att) atomicAdd(&nrows, comp_of(g, c));
-        if (fdrop[c]) {
-            busy[sof[c]] = nxt ? 2 : 0;
-            since[sof[c]] = step;
+        g_att[u] = att;
+        if (att) atomicAdd(&nrows, comp_of(g, u));
+        if (fdrop[u]) {
+            busy[sof[u]] = nxt ? 2 : 0;
+            since[sof[u]] = step;
             atomicAdd(&ndrop, 1);
         }
     }
     __syncthreads();
-    // revival: the chunk's bytes are still in the free slot it last occupied
-    for (int c = tid; c < nc; c += nthr)
-        if (fnew[c]) {
-            const int sl = slast[c];
-            if (sl >= 0 && busy[sl] == 0 && sdata[sl] == c) {
+    // revival: the segment's bytes are still in the free slot it last occupied
+    for (int u = tid; u < nu; u += nthr)
+        if (fnew[u]) {
+            const int sl = slast[u];
+            if (sl >= 0 && busy[sl] == 0 && sdata[sl] == u) {
                 busy[sl] = 1;
-                sof[c] = sl;
-                fnew[c] = 0;
-                if (!nxt) fkept[c] = 1;
+                sof[u] = sl;
+                fnew[u] = 0;
+                if (!nxt) fkept[u] = 1;
                 atomicAdd(&nrev, 1);
             }
         }
     __syncthreads();
 
-    // selected ids, ascending
-    for (int c = tid; c < nc; c += nthr) rank[c] = fsel[c];
+    // selected chunk ids, ascending
+    for (int c = tid; c < nk; c += nthr) rank[c] = fsel[c];
     __syncthreads();
-    const int nsel = block_scan_excl(rank, nc, wsum);
+    const int nsel = block_scan_excl(rank, nk, wsum);
     if (selected) {
-        for (int c = tid; c < nc; c += nthr)
+        for (int c = tid; c < nk; c += nthr)
             if (fsel[c]) selected[(size_t)b * k + rank[c]] = c;
         for (int i = nsel + tid; i < k; i += nthr) selected[(size_t)b * k + i] = -1;
     }
@@ -672,42 +687,42 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
     }
     __syncthreads();
 
-    // kept list first (it needs the slots of chunks dropped now under next-step timing)
-    for (int c = tid; c < nc; c += nthr) rank[c] = fkept[c];
+    // kept list first (it needs the slots of segments dropped now under next-step timing)
+    for (int u = tid; u < nu; u += nthr) rank[u] = fkept[u];
     __syncthreads();
-    const int nkept = block_scan_excl(rank, nc, wsum);
+    const int nkept = block_scan_excl(rank, nu, wsum);
     int32_t *kl = s.kept_list + (size_t)b * ns * 2;
-    for (int c = tid; c < nc; c += nthr)
-        if (fkept[c]) {
-            kl[rank[c] * 2] = c;
-            kl[rank[c] * 2 + 1] = sof[c];
+    for (int u = tid; u < nu; u += nthr)
+        if (fkept[u]) {
+            kl[rank[u] * 2] = u;
+            kl[rank[u] * 2 + 1] = sof[u];
         }
     __syncthreads();
-    for (int c = tid; c < nc; c += nthr)
-        if (fdrop[c]) sof[c] = -1;
+    for (int u = tid; u < nu; u += nthr)
+        if (fdrop[u]) sof[u] = -1;
 
-    // chunks to recall take the free slots in that order (lowest id first)
-    for (int c = tid; c < nc; c += nthr) rank[c] = fnew[c];
+    // segments to recall take the free slots in that order (lowest id first)
+    for (int u = tid; u < nu; u += nthr) rank[u] = fnew[u];
     __syncthreads();
-    const int nnew = block_scan_excl(rank, nc, wsum);
-    int32_t *nl = s.new_list + (size_t)b * k * 2;
-    for (int c = tid; c < nc; c += nthr)
-        if (fnew[c] && rank[c] < nfree && rank[c] < k) {
-            const int slot = freelist[rank[c]];
-            sof[c] = slot;
-            slast[c] = slot;
+    const int nnew = block_scan_excl(rank, nu, wsum);
+    int32_t *nl = s.new_list + (size_t)b * g.knew * 2;
+    for (int u = tid; u < nu; u += nthr)
+        if (fnew[u] && rank[u] < nfree && rank[u] < g.knew) {
+            const int slot = freelist[rank[u]];
+            sof[u] = slot;
+            slast[u] = slot;
             busy[slot] = 1;
-            sdata[slot] = c;
-            nl[rank[c] * 2] = c;
-            nl[rank[c] * 2 + 1] = slot;
+            sdata[slot] = u;
+            nl[rank[u] * 2] = u;
+            nl[rank[u] * 2 + 1] = slot;
         }
     __syncthreads();
 
     // state out
-    for (int c = tid; c < nc; c += nthr) {
-        g_streak[c] = st[c];
-        g_slot_of[c] = sof[c];
-        g_slot_last[c] = slast[c];
+    for (int c = tid; c < nk; c += nthr) g_streak[c] = st[c];
+    for (int u = tid; u < nu; u += nthr) {
+        g_slot_of[u] = sof[u];
+        g_slot_last[u] = slast[u];
     }
     for (int i = tid; i < ns; i += nthr) {
         g_busy[i] = busy[i];
@@ -715,13 +730,13 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
         g_since[i] = since[i];
     }
     if (tid == 0) {
-        const int nn = min(nnew, min(nfree, k));
+        const int nn = min(nnew, min(nfree, g.knew));
         s.counts[b * 2] = nkept;
         s.counts[b * 2 + 1] = nn;
         s.step[b] = step + 1;
         atomicAdd(&s.stats[0], (unsigned long long)nn);
         atomicAdd(&s.stats[1], (unsigned long long)ndrop);
-        // resident set after the step: |R_s|
+        // resident segments after the step
         const int nres = nxt ? nkept - ndrop + nrev + nn : nkept + nn;
         atomicAdd(&s.stats[2], (unsigned long long)nres);
         atomicAdd(&s.stats[3], (unsigned long long)nrows);
@@ -1039,7 +1054,7 @@ __device__ inline void slot_group(const Geometry &g, const Tiers &t, const StepB
     __shared__ const uint16_t *kbase[MAXE];
     __shared__ int nrows[MAXE];
     const int n_entries = min(epg, cnt - grp * epg);
-    const int32_t *list = (which ? s.new_list + (size_t)b * g.k * 2 : s.kept_list + (size_t)b * g.n_slots * 2) +
+    const int32_t *list = (which ? s.new_list + (size_t)b * g.knew * 2 : s.kept_list + (size_t)b * g.n_slots * 2) +
                           (size_t)grp * epg * 2;
     for (int e = threadIdx.x; e < n_entries; e += NT) {
         const int c = list[e * 2], slot = list[e * 2 + 1];
@@ -1067,7 +1082,7 @@ __device__ inline void recall_units(const Geometry &g, const Tiers &t, const Ste
         int b = 0, r = u;
         while (r >= s.counts[b * 2 + 1] * g.nT) r -= s.counts[b++ * 2 + 1] * g.nT;
         const int e = r / g.nT, ti = r - e * g.nT;
-        const int c = s.new_list[((size_t)b * g.k + e) * 2], slot = s.new_list[((size_t)b * g.k + e) * 2 + 1];
+        const int c = s.new_list[((size_t)b * g.knew + e) * 2], slot = s.new_list[((size_t)b * g.knew + e) * 2 + 1];
         const size_t off = (size_t)ti * 2 * g.comp_max * D;
         const uint16_t *src = t.host_comp + ((size_t)b * g.nc + c) * g.chunk_elems + off;
         uint16_t *dst = t.slots + ((size_t)b * g.n_slots + slot) * g.chunk_elems + off;
@@ -1163,7 +1178,7 @@ __global__ __launch_bounds__(NT) void recall_copy_kernel(Geometry g, Tiers t, St
         int b = 0, r = u;
         while (r >= s.counts[b * 2 + 1] * g.nT) r -= s.counts[b++ * 2 + 1] * g.nT;
         const int e = r / g.nT, ti = r - e * g.nT;
-        const int c = s.new_list[((size_t)b * g.k + e) * 2], slot = s.new_list[((size_t)b * g.k + e) * 2 + 1];
+        const int c = s.new_list[((size_t)b * g.knew + e) * 2], slot = s.new_list[((size_t)b * g.knew + e) * 2 + 1];
         const size_t off = (size_t)ti * 2 * g.comp_max * D;
         const uint4 *src = (const uint4 *)(t.host_comp + ((size_t)b * g.nc + c) * g.chunk_elems + off);
         uint4 *dst = (uint4 *)(t.slots + ((size_t)b * g.n_slots + slot) * g.chunk_elems + off);
@@ -1375,9 +1390,9 @@ struct NewSlotsL {
     {
         if (g.nT == 0 || g.k == 0 || g.comp_max == 0) return hipSuccess;
         if (g.slot_tile == TILE_S)
-            hipLaunchKernelGGL((new_slots_kernel<G, TILE_S / 16>), dim3(g.k, g.nT, g.B), dim3(NT), 0, st, g, t, s, q);
+            hipLaunchKernelGGL((new_slots_kernel<G, TILE_S / 16>), dim3(g.knew, g.nT, g.B), dim3(NT), 0, st, g, t, s, q);
         else
-            hipLaunchKernelGGL((new_slots_kernel<G, TILE_S / 8>), dim3(g.k, g.nT, g.B), dim3(NT), 0, st, g, t, s, q);
+            hipLaunchKernelGGL((new_slots_kernel<G, TILE_S / 8>), dim3(g.knew, g.nT, g.B), dim3(NT), 0, st, g, t, s, q);
         return hipGetLastError();
     }
 };

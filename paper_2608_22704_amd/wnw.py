@@ -15,9 +15,10 @@ LIB_PATH = os.path.join(PKG, "libwnw.so")
 
 WNW_OK, WNW_ERR_INVALID, WNW_ERR_OOM, WNW_ERR_HIP, WNW_ERR_STATE, WNW_ERR_UNSUPPORTED = 0, -1, -2, -3, -4, -5
 WNW_ANCHOR, WNW_TIDAL, WNW_FIXED = 0, 1, 2
-WNW_F_SELECT_NEXT_STEP, WNW_F_RECALL_MEMCPY, WNW_F_TIMING = 1, 2, 4
+WNW_F_SELECT_NEXT_STEP, WNW_F_RECALL_MEMCPY, WNW_F_TIMING, WNW_F_OVERLAP_CHUNKS = 1, 2, 4, 8
 
-EXPORTS = ("wnw_init_cache", "wnw_set_roles", "wnw_decode_step", "wnw_query_geometry", "wnw_get_stats",
+EXPORTS = ("wnw_init_cache", "wnw_set_roles", "wnw_decode_step", "wnw_query_geometry", "wnw_query_segments",
+           "wnw_get_stats",
            "wnw_set_selection_override", "wnw_debug_read_slot", "wnw_debug_read_host_chunk",
            "wnw_debug_read_resident", "wnw_last_error", "wnw_destroy")
 
@@ -59,6 +60,7 @@ def _load():
         "wnw_set_roles": ([P, P, P], C.c_int),
         "wnw_decode_step": ([P, P, P, P, P, P], C.c_int),
         "wnw_query_geometry": ([P, C.POINTER(I32), C.POINTER(I32), C.POINTER(I32), C.POINTER(I32), C.POINTER(I64)], C.c_int),
+        "wnw_query_segments": ([P, C.POINTER(I32)], C.c_int),
         "wnw_get_stats": ([P, C.POINTER(wnw_stats)], C.c_int),
         "wnw_set_selection_override": ([P, P], C.c_int),
         "wnw_debug_read_slot": ([P, I32, I32, P, SZ], C.c_int),
@@ -120,6 +122,9 @@ def wnw_query_geometry(ctx) -> dict:
     n, k, kt, ns, cb = C.c_int32(), C.c_int32(), C.c_int32(), C.c_int32(), C.c_int64(-1)
     _check(lib.wnw_query_geometry(ctx, C.byref(n), C.byref(k), C.byref(kt), C.byref(ns), None), ctx)
     out = {"n_chunks": n.value, "k": k.value, "keep_total": kt.value, "n_slots": ns.value}
+    seg = C.c_int32()
+    _check(lib.wnw_query_segments(ctx, C.byref(seg)), ctx)
+    out["n_segments"] = seg.value
     if lib.wnw_query_geometry(ctx, None, None, None, None, C.byref(cb)) == WNW_OK:
         out["chunk_bytes"] = cb.value
     return out

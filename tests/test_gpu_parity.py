@@ -351,3 +351,98 @@ def test_next_step_two_runs_bit_identical():
     for a, b in zip(*outs):
         for x, y in zip(a, b):
             assert np.array_equal(x, y)
+
+
+# ---- overlapping chunks: a chunk is two consecutive half-length segments and a chunk starts at
+# every segment; selection per chunk, residency and recall per segment (the oracle's chunk_span 2).
+
+def _ovl(extra=0):
+    from paper_2608_22704_amd import wnw as W
+    return W.WNW_F_OVERLAP_CHUNKS | extra
+
+
+EDGE_OVL = [
+    _small("ovl_g1_chunk8", 201, Hq=4, Hkv=4, cl=8),
+    _small("ovl_g2_chunk50_ragged", 202, Hq=8, cl=50, Ta=517),
+    _small("ovl_g6_chunk100", 203, Hq=12, Hkv=2, cl=100, Ta=1111, Tt=3),
+    _small("ovl_g8_chunk512_long_tail", 204, Hq=16, Hkv=2, cl=512, Ta=1300, Tt=300, budget=5000),
+    _small("ovl_g4_chunk2", 205, Hq=8, Hkv=2, cl=2, Ta=97, budget=2500),
+    _small("ovl_no_text", 206, Tt=0),
+    _small("ovl_budget_zero", 207, budget=0),
+    _small("ovl_budget_full", 208, budget=10000),
+    _small("ovl_audio_shorter_than_segment", 209, Ta=20, cl=64, budget=5000),
+    _small("ovl_text_only", 210, Ta=0, Tt=40),
+    _small("ovl_all_tidal_but_one_anchor", 211, L=1, Hkv=4, Hq=12, roles=(1, 3, 0)),
+    _small("ovl_batch3_tile_ragged", 213, B=3, Ta=777, Tt=1, cl=38, budget=3000, steps=9),
+]
+
+
+@pytest.mark.parametrize("w", EDGE_OVL, ids=[w.name for w in EDGE_OVL])
+def test_overlap_edge_shapes(w):
+    _run(w, flags=_ovl())
+
+
+@pytest.mark.parametrize("w", EDGE_OVL, ids=[w.name for w in EDGE_OVL])
+def test_overlap_next_step_edge_shapes(w):
+    _run(w, flags=_ovl(_next()))
+
+
+def test_overlap_two_segments_one_chunk():
+    """Two segments make one chunk, which top-k 1 selects at every step."""
+    _run(_small("ovl_two_segments", 214, Ta=60, cl=64, budget=2000), flags=_ovl(), top_k=1)
+
+
+def test_overlap_memcpy_recall_paths():
+    from paper_2608_22704_amd import wnw as W
+    w = _small("ovl_memcpy", 215, L=2, Hq=8, Hkv=4, Ta=480, Tt=5, cl=32, steps=10)
+    _run(w, flags=_ovl(W.WNW_F_RECALL_MEMCPY))
+    _run(w, flags=_ovl(_next(W.WNW_F_RECALL_MEMCPY)))
+
+
+def test_overlap_qwen_shaped_all_steps():
+    _run(configs.QWEN_10MIN, flags=_ovl(_next()))
+
+
+def test_overlap_voxtral_shaped_sampled_heads():
+    _run(configs.VOXTRAL_10MIN.with_(steps=64), head_mask_fn=_sampled(16), flags=_ovl(_next()))
+
+
+@pytest.mark.parametrize("nxt", [False, True], ids=["same_step", "next_step"])
+def test_overlap_slots_over_steps(nxt):
+    """Every segment that holds a slot after a step is byte-identical to its host complement, the
+    segments held are those the following step attends to (next-step timing), and segments are
+    revived."""
+    from paper_2608_22704_amd import wnw as W
+    from tests.wnw_harness import Lockstep, log
+    w = _small("ovl_slots_over_steps", 216, L=2, Hq=8, Hkv=4, Ta=480, Tt=5, cl=32, budget=2000, steps=24)
+    log(f"[case] overlapping chunks, slots vs host copies over 24 steps, next_step={nxt}")
+    h = Lockstep(w, flags=_ovl(_next() if nxt else 0))
+    try:
+        nbytes = h.geo["chunk_bytes"]
+        assert h.nseg == h.nc + 1
+        assert h.geo["n_slots"] == min(h.nseg, (3 + nxt) * 2 * h.k)
+        held_before = None
+        for s in range(w.steps):
+            _, _, _, res = h.step(s)
+            if nxt and held_before is not None:
+                assert np.array_equal(res, held_before), f"step {s}: attended set is not the previous resident set"
+            held = np.zeros_like(res)
+            for b in range(w.batch):
+                for c in range(h.nseg):
+                    dev = np.empty(nbytes // 2, dtype=np.uint16)
+                    try:
+                        W.wnw_debug_read_slot(h.ctx, b, c, dev, nbytes)
+                    except W.WnwError:
+                        continue
+                    held[b, c] = 1
+                    hst = np.empty(nbytes // 2, dtype=np.uint16)
+                    W.wnw_debug_read_host_chunk(h.ctx, b, c, hst, nbytes)
+                    assert np.array_equal(dev, hst), f"step {s} seq {b} segment {c}"
+            if not nxt:
+                assert np.array_equal(held, res), f"step {s}: held slots are not the resident segments"
+            held_before = held
+        st = W.wnw_get_stats(h.ctx)
+        log(f"[done] recalled {st['recalled_chunks']} revived {st['revived_chunks']} dropped {st['dropped_chunks']}")
+        assert st["revived_chunks"] > 0
+    finally:
+        h.close()

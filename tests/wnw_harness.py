@@ -98,13 +98,16 @@ class Lockstep:
         torch.cuda.empty_cache()
         self.geo = W.wnw_query_geometry(self.ctx)
         self.next_step = 1 if flags & W.WNW_F_SELECT_NEXT_STEP else 0
-        ocfg = O.cfg_from_workload(w, batch=len(self.seqs), top_k=top_k, next_step=self.next_step)
+        span = 2 if flags & W.WNW_F_OVERLAP_CHUNKS else 1
+        ocfg = O.cfg_from_workload(w, batch=len(self.seqs), top_k=top_k, next_step=self.next_step,
+                                   chunk_span=span)
         self.ok_ = np.stack([host[b]["k"] for b in self.seqs])
         self.ov_ = np.stack([host[b]["v"] for b in self.seqs])
         self.oracle = O.Oracle(ocfg, self.ok_, self.ov_, self.roles, self.prefill[self.seqs])
         assert (self.oracle.n_chunks, self.oracle.k, self.oracle.keep_total) == \
             (self.geo["n_chunks"], self.geo["k"], self.geo["keep_total"])
-        self.k, self.nc = self.geo["k"], self.geo["n_chunks"]
+        assert self.oracle.n_segments == self.geo["n_segments"]
+        self.k, self.nc, self.nseg = self.geo["k"], self.geo["n_chunks"], self.geo["n_segments"]
         self.out = torch.empty((B, L, w.q_heads, D), dtype=torch.float32, device="cuda")
         self.scores = torch.empty((B, max(self.nc, 1)), dtype=torch.float32, device="cuda")
         self.sel = torch.empty((B, max(self.k, 1)), dtype=torch.int32, device="cuda")
@@ -124,10 +127,10 @@ class Lockstep:
         qd = to_dev(self.q[s])
         self.W.wnw_decode_step(self.ctx, qd, self.out, self.scores, self.sel)
         self.torch.cuda.synchronize()
-        res = np.empty((self.w.batch, max(self.nc, 1)), dtype=np.uint8)
+        res = np.empty((self.w.batch, max(self.nseg, 1)), dtype=np.uint8)
         self.W.wnw_debug_read_resident(self.ctx, res)
         return (self.out.cpu().numpy(), self.scores.cpu().numpy()[:, : self.nc],
-                self.sel.cpu().numpy()[:, : self.k], res[:, : self.nc])
+                self.sel.cpu().numpy()[:, : self.k], res[:, : self.nseg])
 
     def step(self, s: int, head_mask=None):
         out, sc, sel, res = self.gpu_step(s)
