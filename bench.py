@@ -78,13 +78,14 @@ def overlap_sweep(W, torch, w, ctx, geo, qd, out, sc, sel, stream, args, ms_no_r
     return res
 
 
-def run_timing(W, torch, w, timing, recall, kd, vd, qd, roles, prefill, args):
+def run_timing(W, torch, w, timing, recall, kd, vd, qd, roles, prefill, args, chunks="disjoint"):
     """Set up one context with the given selection timing and recall path, run the warm-up and
     the timed steps, then a second region with the selection pinned (no recall).  Returns the
     context-independent numbers; the context is destroyed."""
     B, L, H, D, S = w.batch, w.layers, w.kv_heads, w.head_dim, w.steps
     flags = ((0 if args.no_timing else W.WNW_F_TIMING) | (W.WNW_F_RECALL_MEMCPY if recall == "memcpy" else 0)
-             | (W.WNW_F_SELECT_NEXT_STEP if timing == "next" else 0))
+             | (W.WNW_F_SELECT_NEXT_STEP if timing == "next" else 0)
+             | (W.WNW_F_OVERLAP_CHUNKS if chunks == "overlap" else 0))
     cfg = W.make_config(B, L, w.q_heads, H, w.audio_len, w.text_len, w.chunk_len, w.budget_bp, flags=flags)
     stream = torch.cuda.current_stream()
     ctx = W.wnw_init_cache(cfg, kd, vd, stream)
@@ -94,7 +95,7 @@ def run_timing(W, torch, w, timing, recall, kd, vd, qd, roles, prefill, args):
         out = torch.empty((B, L, w.q_heads, D), dtype=torch.float32, device="cuda")
         sc = torch.empty((B, geo["n_chunks"]), dtype=torch.float32, device="cuda")
         sel = torch.empty((B, max(geo["k"], 1)), dtype=torch.int32, device="cuda")
-        log(f"[bench] {timing}-step timing, {recall} recall: set-up done {geo}")
+        log(f"[bench] {timing}-step timing, {recall} recall, {chunks} chunks: set-up done {geo}")
         if args.calibrate_copy:
             src = torch.ones(128 << 20, dtype=torch.int16, device="cuda")
             dst = torch.empty_like(src)
@@ -113,7 +114,7 @@ def run_timing(W, torch, w, timing, recall, kd, vd, qd, roles, prefill, args):
         torch.cuda.synchronize()
         t_el = time.perf_counter() - t_start
         st1 = W.wnw_get_stats(ctx)
-        log(f"[bench] {timing}-step timed region {t_el * 1e3:.1f} ms")
+        log(f"[bench] {timing}-step, {chunks} chunks: timed region {t_el * 1e3:.1f} ms")
         # Second region: the selection pinned to the last step's chunks (all resident after one
         # step), so no complement is recalled and every launch streams HBM only.
         nr = max(8, args.steps // 4)
@@ -186,6 +187,10 @@ def main():
                     help="selection timing of the headline run: the selection made after step s serves step s+1 "
                          "(the paper's timing; the recall overlaps the step) or step s itself")
     ap.add_argument("--no-other-timing", action="store_true", help="skip the run with the other selection timing")
+    ap.add_argument("--chunks", choices=("disjoint", "overlap"), default="disjoint",
+                    help="chunk structure of the headline run: disjoint chunks of chunk_len positions, or chunks of "
+                         "two chunk_len/2 segments starting at every segment")
+    ap.add_argument("--no-other-chunks", action="store_true", help="skip the run with the other chunk structure")
     ap.add_argument("--no-sweep", dest="sweep", action="store_false",
                     help="skip the overlap sweep (forced 1..24 newly resident chunks per step)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU oracle sample (0 = skip)")
@@ -222,12 +227,16 @@ def main():
     torch.cuda.synchronize()
     log(f"[bench] inputs resident in HBM after {time.time() - t0:.1f}s")
 
-    main_run = run_timing(W, torch, w, args.timing, args.recall, kd, vd, qd, roles, prefill, args)
-    other = None
+    main_run = run_timing(W, torch, w, args.timing, args.recall, kd, vd, qd, roles, prefill, args, args.chunks)
+    other = other_ch = None
+    args_other = argparse.Namespace(**{**vars(args), "calibrate_copy": False, "sweep": False})
     if not args.no_other_timing:
         other_timing = "same" if args.timing == "next" else "next"
-        args_other = argparse.Namespace(**{**vars(args), "calibrate_copy": False, "sweep": False})
-        other = run_timing(W, torch, w, other_timing, args.recall, kd, vd, qd, roles, prefill, args_other)
+        other = run_timing(W, torch, w, other_timing, args.recall, kd, vd, qd, roles, prefill, args_other, args.chunks)
+    other_chunks = "overlap" if args.chunks == "disjoint" else "disjoint"
+    if not args.no_other_chunks:
+        other_ch = run_timing(W, torch, w, args.timing, args.recall, kd, vd, qd, roles, prefill, args_other,
+                              other_chunks)
     del kd, vd
     torch.cuda.empty_cache()
 
@@ -240,7 +249,7 @@ def main():
         "config": {"workload": w.name, "batch": B, "layers": L, "q_heads": w.q_heads, "kv_heads": H,
                    "head_dim": D, "audio_len": w.audio_len, "text_len": w.text_len, "chunk_len": w.chunk_len,
                    "budget_bp": w.budget_bp, "roles": [w.n_anchor, w.n_tidal, w.n_fixed], "kv_storage": "bf16",
-                   "selection_timing": args.timing, "recall": args.recall},
+                   "selection_timing": args.timing, "recall": args.recall, "chunks": args.chunks},
     }
     if "kernels" in main_run:
         k = main_run["kernels"]
@@ -268,6 +277,13 @@ def main():
         if "kernels" in other:
             o["kernels"] = other["kernels"]
         res["other_timing"] = o
+    if other_ch is not None:
+        o = {"chunks": other_chunks, "selection_timing": args.timing, "value": other_ch["value"], "unit": "steps/s",
+             "ms_per_step": other_ch["ms_per_step"], "n_chunks": other_ch["geo"]["n_chunks"],
+             "n_segments": other_ch["geo"]["n_segments"], "recall": other_ch["recall"]}
+        if "kernels" in other_ch:
+            o["kernels"] = other_ch["kernels"]
+        res["other_chunks"] = o
 
     if args.cpu_seconds > 0:
         res["cpu_baseline"] = cpu_baseline(w, roles, prefill, args.cpu_seconds)

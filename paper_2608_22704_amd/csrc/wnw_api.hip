@@ -555,12 +555,12 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, float *out, float *sco
 
     // (1) anchor attention + chunk mass, (2) scores, top-k and residency.  With next-step
     // timing the static tidal/fixed tiles (kept rows + text) join the anchor launch.
-    MARK(0);
+    // markers 0 and 1 are the first launch's own start and end (its dispatch excluded)
+    hipEvent_t e0 = timing ? ev.e[0] : nullptr, e1 = timing ? ev.e[1] : nullptr;
     if (g.next_step)
-        HIPCHECK(c, launch_attention(g, c->t, sb, q, s0));
+        HIPCHECK(c, launch_attention(g, c->t, sb, q, s0, e0, e1));
     else
-        HIPCHECK(c, launch_anchor(g, c->t, sb, q, s0));
-    MARK(1);
+        HIPCHECK(c, launch_anchor(g, c->t, sb, q, s0, e0, e1));
     HIPCHECK(c, launch_anchor_combine(g, c->t, sb, out, s0));
     HIPCHECK(c, launch_select(g, sb, sc, c->override_sel, sel, s0));
     const bool memcpy_path = c->cfg.flags & WNW_F_RECALL_MEMCPY;

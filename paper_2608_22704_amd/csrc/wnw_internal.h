@@ -88,9 +88,11 @@ struct StepBuffers {
     unsigned long long *stats;  // [8] recalled, dropped, resident, slot_rows, peak, exhausted, revived
 };
 
-// Launchers (wnw_kernels.hip).  Each returns the launch status.
+// Launchers (wnw_kernels.hip).  Each returns the launch status.  Where a launcher takes two
+// events (either may be null), they are bound to the kernel's own dispatch and carry its start
+// and end times (hipExtLaunchKernel), or are recorded back to back when there is nothing to launch.
 hipError_t launch_anchor(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q,
-                         hipStream_t st);
+                         hipStream_t st, hipEvent_t e0, hipEvent_t e1);
 hipError_t launch_anchor_combine(const Geometry &g, const Tiers &t, const StepBuffers &s, float *out,
                                  hipStream_t st);
 // Scores, selection, residency and slot bookkeeping (writes scores[B][nc] and selected[B][k]).
@@ -108,7 +110,8 @@ inline size_t select_shared_bytes(const Geometry &g)
 hipError_t launch_tidal_fixed(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, bool recall,
                               bool with_static, hipStream_t st);
 // Anchor attention + chunk mass together with the static tidal/fixed tiles (next-step timing).
-hipError_t launch_attention(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st);
+hipError_t launch_attention(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st,
+                            hipEvent_t e0, hipEvent_t e1);
 // Next-step timing: copy of the complements listed for recall from mapped pinned memory into
 // their slots, no attention (they are attended from the next step on).
 hipError_t launch_recall(const Geometry &g, const Tiers &t, const StepBuffers &s, hipStream_t st);

@@ -25,6 +25,8 @@
 // flight.  Dot products are reduced across the 16 lanes of a row with DPP row permutes.
 #include "wnw_internal.h"
 
+#include <hip/hip_ext.h>
+
 #include <math.h>
 
 #include <algorithm>
@@ -1320,6 +1322,15 @@ __global__ void gather_rows_kernel(uint16_t *__restrict__ dst, const uint16_t *_
     ((uint4 *)(dst + row * D))[part] = v;
 }
 
+// Timing events of a launch that has no work: both recorded on the stream (the interval is empty).
+hipError_t record_pair(hipEvent_t e0, hipEvent_t e1, hipStream_t st)
+{
+    hipError_t r = hipSuccess;
+    if (e0) r = hipEventRecord(e0, st);
+    if (e1 && r == hipSuccess) r = hipEventRecord(e1, st);
+    return r;
+}
+
 template <template <int> class F, typename... A>
 hipError_t dispatch_g(int G, A... args)
 {
@@ -1336,10 +1347,12 @@ hipError_t dispatch_g(int G, A... args)
 
 template <int G>
 struct AnchorL {
-    static hipError_t run(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st)
+    static hipError_t run(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st,
+                          hipEvent_t e0, hipEvent_t e1)
     {
-        if (g.nA == 0 || g.n_tiles_a == 0) return hipSuccess;
-        hipLaunchKernelGGL(anchor_attn_kernel<G>, dim3(g.n_tiles_a, g.nA, g.B), dim3(NT), 0, st, g, t, s, q);
+        if (g.nA == 0 || g.n_tiles_a == 0) return record_pair(e0, e1, st);
+        hipExtLaunchKernelGGL(anchor_attn_kernel<G>, dim3(g.n_tiles_a, g.nA, g.B), dim3(NT), 0, st, e0, e1, 0, g, t,
+                              s, q);
         return hipGetLastError();
     }
 };
@@ -1376,11 +1389,12 @@ struct TidalFixedL {
 };
 template <int G>
 struct AttentionL {
-    static hipError_t run(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st)
+    static hipError_t run(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st,
+                          hipEvent_t e0, hipEvent_t e1)
     {
         const long long n = (long long)g.n_tiles_a * g.nA * g.B + (long long)g.n_tiles_s * (g.nT + g.nF) * g.B;
-        if (n == 0) return hipSuccess;
-        hipLaunchKernelGGL(attention_kernel<G>, dim3((unsigned)n), dim3(NT), 0, st, g, t, s, q);
+        if (n == 0) return record_pair(e0, e1, st);
+        hipExtLaunchKernelGGL(attention_kernel<G>, dim3((unsigned)n), dim3(NT), 0, st, e0, e1, 0, g, t, s, q);
         return hipGetLastError();
     }
 };
@@ -1409,9 +1423,10 @@ struct CombineL {
 
 }  // namespace
 
-hipError_t launch_anchor(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st)
+hipError_t launch_anchor(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st,
+                         hipEvent_t e0, hipEvent_t e1)
 {
-    return dispatch_g<AnchorL>(g.G, g, t, s, q, st);
+    return dispatch_g<AnchorL>(g.G, g, t, s, q, st, e0, e1);
 }
 
 hipError_t launch_anchor_combine(const Geometry &g, const Tiers &t, const StepBuffers &s, float *out, hipStream_t st)
@@ -1433,9 +1448,10 @@ hipError_t launch_tidal_fixed(const Geometry &g, const Tiers &t, const StepBuffe
     return dispatch_g<TidalFixedL>(g.G, g, t, s, q, recall, with_static, st);
 }
 
-hipError_t launch_attention(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st)
+hipError_t launch_attention(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st,
+                            hipEvent_t e0, hipEvent_t e1)
 {
-    return dispatch_g<AttentionL>(g.G, g, t, s, q, st);
+    return dispatch_g<AttentionL>(g.G, g, t, s, q, st, e0, e1);
 }
 
 hipError_t launch_recall(const Geometry &g, const Tiers &t, const StepBuffers &s, hipStream_t st)
