@@ -48,6 +48,8 @@ def lib():
         L.wnwo_geometry.argtypes = [C.POINTER(_Cfg), C.POINTER(C.c_int32), C.POINTER(C.c_int32), C.POINTER(C.c_int32)]
         L.wnwo_create.argtypes = [C.POINTER(_Cfg), P, P, P, P]
         L.wnwo_create.restype = P
+        L.wnwo_create_retention.argtypes = [C.POINTER(_Cfg), P, P, P, P, P, C.c_float]
+        L.wnwo_create_retention.restype = P
         L.wnwo_destroy.argtypes = [P]
         L.wnwo_keep_mask.argtypes = [P, C.c_int32, C.c_int32, C.c_int32, P]
         L.wnwo_step.argtypes = [P, P, P, P, P, P, P, P, P]
@@ -115,7 +117,9 @@ class Oracle:
     roles uint8 [L][H_kv]; prefill fp32 [B][L][H_kv][T_a].  The arrays are referenced, not
     copied, so they are kept alive here."""
 
-    def __init__(self, cfg: _Cfg, k, v, roles, prefill):
+    def __init__(self, cfg: _Cfg, k, v, roles, prefill, importance=None, lam=None):
+        """importance [L][H_kv] fp32 and lam (fp32): per-head retention min(importance * lam, 1)
+        of Eq. 1 instead of the uniform budget."""
         self.cfg = cfg
         self.n_chunks, self.k, self.keep_total = geometry(cfg)
         self.n_segments = segments(cfg)   # the unit of masses and residency (= chunks when disjoint)
@@ -128,7 +132,12 @@ class Oracle:
         assert self._k.shape == (B, L, H, T, D) and self._v.shape == self._k.shape
         assert self._roles.shape == (L, H) and self._pf.shape == (B, L, H, cfg.audio_len)
         self.n_anchor_q = int((self._roles == 0).sum()) * (cfg.q_heads // cfg.kv_heads)
-        self._h = lib().wnwo_create(C.byref(cfg), _ptr(self._k), _ptr(self._v), _ptr(self._roles), _ptr(self._pf))
+        self._imp = None if importance is None else np.ascontiguousarray(importance, dtype=np.float32)
+        if self._imp is not None:
+            assert self._imp.shape == (L, H) and lam is not None
+        self._h = lib().wnwo_create_retention(C.byref(cfg), _ptr(self._k), _ptr(self._v), _ptr(self._roles),
+                                              _ptr(self._pf), _ptr(self._imp),
+                                              float(np.float32(lam)) if lam is not None else 0.0)
         if not self._h:
             raise ValueError("wnwo_create failed")
 

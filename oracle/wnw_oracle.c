@@ -27,7 +27,8 @@
  *     chunk starts at every segment (Method, "Chunk Structure"); the last segment may be
  *     shorter and a chunk's score is the mean over the positions it has; a selected chunk makes
  *     both of its segments resident;
- *   - retention is one uniform fraction budget_bp / 10000 for every tidal and fixed head;
+ *   - retention is one uniform fraction budget_bp / 10000 for every tidal and fixed head, or,
+ *     given per-head importance and lambda, min(importance * lambda, 1) per head (Eq. 1);
  *   - k = floor(budget_bp * T_a / (10000 * chunk_len)) unless given;
  *   - the softmax of Eq. 2 runs over the anchor head's whole key set (audio and text); only the
  *     audio weights enter A; the logit scale is 1 / sqrt(d);
@@ -95,10 +96,23 @@ static int32_t chunk_last_seg(const wnwo_config *c, int32_t ch)
     return last < ns ? last : ns - 1;
 }
 
-/* Positions kept at prefill inside a segment of `len` positions: floor(retention * len). */
+/* Positions kept at prefill inside a segment of `len` positions: floor(retention * len), with
+ * the uniform retention budget_bp / 10000. */
 static int32_t keep_count(const wnwo_config *c, int32_t len)
 {
     return (int32_t)(((int64_t)c->budget_bp * len) / 10000);
+}
+
+/* Eq. 1: the audio retention of a non-anchor head is its normalised importance times lambda,
+ * clipped at 1 (taken in double: the product of the two fp32 inputs is exact there).  Its keep
+ * count in a segment of `len` positions is floor(retention * len).  Without per-head importance
+ * the uniform budget applies. */
+static int32_t keep_count_head(const wnwo_config *c, const float *importance, float lambda, size_t h, int32_t len)
+{
+    if (!importance) return keep_count(c, len);
+    double r = (double)importance[h] * (double)lambda;
+    if (r > 1.0) r = 1.0;
+    return (int32_t)floor(r * (double)len);
 }
 
 int wnwo_geometry(const wnwo_config *c, int32_t *n_chunks, int32_t *k, int32_t *keep_total)
@@ -140,7 +154,8 @@ static int by_score_then_pos(const void *a, const void *b)
     return (x->pos > y->pos) - (x->pos < y->pos);
 }
 
-static void prefill_keep(const wnwo_config *c, const float *score, uint8_t *keep, ranked *tmp)
+static void prefill_keep(const wnwo_config *c, const float *importance, float lambda, size_t h,
+                         const float *score, uint8_t *keep, ranked *tmp)
 {
     memset(keep, 0, (size_t)c->audio_len);
     int32_t ns = seg_count(c);
@@ -148,7 +163,7 @@ static void prefill_keep(const wnwo_config *c, const float *score, uint8_t *keep
         int32_t b0 = seg_begin(c, j), e0 = seg_end(c, j), n = e0 - b0;
         for (int32_t i = 0; i < n; ++i) { tmp[i].s = score[b0 + i]; tmp[i].pos = b0 + i; }
         qsort(tmp, (size_t)n, sizeof *tmp, by_score_then_pos);
-        int32_t kc = keep_count(c, n);
+        int32_t kc = keep_count_head(c, importance, lambda, h, n);
         for (int32_t i = 0; i < kc; ++i) keep[tmp[i].pos] = 1;
     }
 }
@@ -156,11 +171,23 @@ static void prefill_keep(const wnwo_config *c, const float *score, uint8_t *keep
 wnwo *wnwo_create(const wnwo_config *cfg, const uint16_t *k, const uint16_t *v,
                   const uint8_t *roles, const float *prefill)
 {
+    return wnwo_create_retention(cfg, k, v, roles, prefill, NULL, 0.0f);
+}
+
+wnwo *wnwo_create_retention(const wnwo_config *cfg, const uint16_t *k, const uint16_t *v,
+                            const uint8_t *roles, const float *prefill, const float *importance,
+                            float lambda)
+{
     int32_t nc, kk, kt;
     if (!cfg || !k || !v || !roles || !prefill) return NULL;
     if (wnwo_geometry(cfg, &nc, &kk, &kt)) return NULL;
     for (int32_t i = 0; i < cfg->layers * cfg->kv_heads; ++i)
         if (roles[i] > 2) return NULL;
+    if (importance) {
+        if (!(lambda >= 0.0f) || isinf(lambda)) return NULL;
+        for (int32_t i = 0; i < cfg->layers * cfg->kv_heads; ++i)
+            if (!(importance[i] >= 0.0f && importance[i] <= 1.0f)) return NULL;
+    }
     wnwo *o = calloc(1, sizeof *o);
     if (!o) return NULL;
     o->c = *cfg;
@@ -190,7 +217,8 @@ wnwo *wnwo_create(const wnwo_config *cfg, const uint16_t *k, const uint16_t *v,
             if (roles[h] == 0)
                 memset(kp, 1, (size_t)cfg->audio_len);         /* anchors keep all audio */
             else
-                prefill_keep(cfg, prefill + (b * nh + h) * (size_t)cfg->audio_len, kp, tmp);
+                prefill_keep(cfg, importance, lambda, h, prefill + (b * nh + h) * (size_t)cfg->audio_len,
+                             kp, tmp);
         }
     free(tmp);
     /* No chunk has been selected yet: every streak starts at delta (not resident). */

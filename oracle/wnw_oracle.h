@@ -45,6 +45,12 @@ int wnwo_segments(const wnwo_config *cfg, int32_t *n_segments);
  * roles: [L][H_kv] (0 anchor, 1 tidal, 2 fixed).  prefill: [B][L][H_kv][T_a] fp32. */
 wnwo *wnwo_create(const wnwo_config *cfg, const uint16_t *k, const uint16_t *v,
                   const uint8_t *roles, const float *prefill);
+/* As wnwo_create, with the per-head audio retention of Eq. 1: retention = min(importance *
+ * lambda, 1) for every tidal and fixed head (importance [L][H_kv] fp32 in [0, 1], lambda >= 0
+ * finite; anchors keep all audio).  importance NULL means the uniform budget. */
+wnwo *wnwo_create_retention(const wnwo_config *cfg, const uint16_t *k, const uint16_t *v,
+                            const uint8_t *roles, const float *prefill, const float *importance,
+                            float lambda);
 void wnwo_destroy(wnwo *o);
 
 /* Audio positions kept at prefill by head (b, l, kv): mask[T_a] of 0/1 (all 1 for anchors). */

@@ -40,6 +40,11 @@ MUTANTS = {
         "for (int32_t sg = ch; sg <= s1; ++sg) a +=", "for (int32_t sg = ch; sg <= ch; ++sg) a +="),
     "overlapping chunks start every other segment": (
         "return (span_of(c) == 2 && ns >= 2) ? ns - 1 : ns;", "return (span_of(c) == 2 && ns >= 2) ? ns / 2 : ns;"),
+    "per-head retention ignores lambda": (
+        "double r = (double)importance[h] * (double)lambda;", "double r = (double)importance[h];"),
+    "per-head keep count rounds to nearest": (
+        "return (int32_t)floor(r * (double)len);", "return (int32_t)floor(r * (double)len + 0.5);"),
+    "per-head retention ignored": ("if (!importance) return keep_count(c, len);", "return keep_count(c, len);"),
 }
 
 

@@ -353,3 +353,118 @@ def test_span2_selection_is_topk_of_fp32_scores(oracle_mod):
         r = o.step(qs)
         for b in range(q.shape[0]):
             assert list(r["selected"][b]) == _brute_topk(list(r["scores"][b].astype(np.float32)), o.k)
+
+
+# ---- per-head retention (Eq. 1): retention = min(importance * lambda, 1) per tidal/fixed head
+
+def _retention_case(oracle_mod, seed, imp, lam, B=2, D=8, Ta=70, Tt=3, cl=16, g=2, pf=None, **kw):
+    rng = np.random.default_rng(seed)
+    L, H = imp.shape
+    k, v = _rand_cache(rng, B, L, H, Ta + Tt, D)
+    roles = (np.arange(L * H).reshape(L, H) % 3).astype(np.uint8)   # anchor, tidal, fixed in turn
+    if pf is None:
+        pf = rng.random((B, L, H, Ta), dtype=np.float32)
+    cfg = oracle_mod.make_cfg(B, L, H * g, H, D, Ta, Tt, cl, 2000, **kw)
+    o = oracle_mod.Oracle(cfg, k, v, roles, pf, importance=imp, lam=lam)
+    return o, k, v, roles, pf
+
+
+def test_retention_keep_counts_follow_eq1(oracle_mod):
+    """Per segment, floor(min(importance * lambda, 1) * len) positions are kept (exact rational
+    arithmetic; the case has no product within 1e-9 of an integer), each outranking every
+    dropped one; importance 0 keeps nothing, importance * lambda >= 1 keeps every position,
+    anchors keep everything."""
+    from fractions import Fraction
+    rng = np.random.default_rng(41)
+    L, H, Ta, cl = 3, 4, 70, 16
+    imp = rng.random((L, H), dtype=np.float32)
+    imp[0, 1], imp[1, 1], imp[2, 2] = 0.0, 1.0, 0.0
+    lam = np.float32(0.7310585)
+    pf = (rng.integers(0, 4, size=(2, L, H, Ta)) / 4.0).astype(np.float32)   # heavy ties
+    o, k, v, roles, pf = _retention_case(oracle_mod, 5, imp, lam, Ta=Ta, cl=cl, pf=pf)
+    lam2 = np.float32(3.0)
+    o2, *_ = _retention_case(oracle_mod, 5, imp, lam2, Ta=Ta, cl=cl, pf=pf)
+    for oo, lm in ((o, lam), (o2, lam2)):
+        for b, l, h in itertools.product(range(2), range(L), range(H)):
+            m = oo.keep_mask(b, l, h)
+            if roles[l, h] == 0:
+                assert m.all()
+                continue
+            r = min(Fraction(float(imp[l, h])) * Fraction(float(lm)), Fraction(1))
+            for c0 in range(0, Ta, cl):
+                seg = range(c0, min(c0 + cl, Ta))
+                x = r * len(seg)
+                assert x.denominator == 1 or abs(float(x - round(x))) > 1e-9
+                kept = [t for t in seg if m[t]]
+                drop = [t for t in seg if not m[t]]
+                assert len(kept) == math.floor(x), (l, h, c0)
+                for a in kept:
+                    for d in drop:
+                        assert (pf[b, l, h, a], -a) > (pf[b, l, h, d], -d)
+    assert not o.keep_mask(0, 0, 1).any() and o.keep_mask(0, 1, 1).sum() == math.floor(float(lam) * 16) * 4 + math.floor(float(lam) * 6)
+    assert o2.keep_mask(0, 1, 1).all()
+
+
+def test_retention_uniform_importance_is_the_uniform_budget(oracle_mod):
+    """importance 0.25 with lambda 1, and 0.5 with lambda 0.5, give retention 1/4 exactly: the
+    keep sets and every output equal those of the uniform 25 % budget."""
+    rng = np.random.default_rng(43)
+    B, L, H, g, D, Ta, Tt, cl = 2, 2, 3, 2, 8, 64, 4, 8
+    k, v = _rand_cache(rng, B, L, H, Ta + Tt, D)
+    roles = np.array([[0, 1, 2], [1, 2, 0]], dtype=np.uint8)
+    pf = rng.random((B, L, H, Ta), dtype=np.float32)
+    cfg = oracle_mod.make_cfg(B, L, H * g, H, D, Ta, Tt, cl, 2500)
+    ref = oracle_mod.Oracle(cfg, k, v, roles, pf)
+    alts = [oracle_mod.Oracle(cfg, k, v, roles, pf, importance=np.full((L, H), s, np.float32), lam=lm)
+            for s, lm in ((0.25, 1.0), (0.5, 0.5))]
+    for b, l, h in itertools.product(range(B), range(L), range(H)):
+        for a in alts:
+            assert np.array_equal(a.keep_mask(b, l, h), ref.keep_mask(b, l, h))
+    for step in range(3):
+        q = f32_to_bf16(rng.standard_normal((B, L, H * g, D)).astype(np.float32))
+        r0 = ref.step(q)
+        for a in alts:
+            r = a.step(q)
+            assert np.array_equal(r["out"], r0["out"]) and np.array_equal(r["resident"], r0["resident"])
+
+
+def test_retention_heads_attend_over_their_own_key_sets(oracle_mod):
+    """Heterogeneous retention (including 0 and 1): every tidal head attends over its own kept
+    rows + the resident chunks + text and every fixed head over its own kept rows + text (SDPA
+    with that mask); a tidal or fixed head at retention 1 is plain attention."""
+    rng = np.random.default_rng(47)
+    L, H, Ta, Tt, cl, g = 2, 6, 64, 4, 8, 2
+    imp = rng.random((L, H), dtype=np.float32)
+    imp[0, 1], imp[0, 2], imp[1, 4] = 0.0, 1.0, 1.0       # tidal at 0, fixed at 1, tidal at 1
+    o, k, v, roles, pf = _retention_case(oracle_mod, 9, imp, np.float32(1.0), Ta=Ta, Tt=Tt, cl=cl, g=g)
+    assert roles[0, 1] == 1 and roles[0, 2] == 2 and roles[1, 4] == 1
+    B = 2
+    for step in range(4):
+        q = f32_to_bf16(rng.standard_normal((B, L, H * g, 8)).astype(np.float32))
+        r = o.step(q)
+        for b, l, hq in itertools.product(range(B), range(L), range(H * g)):
+            h = hq // g
+            mask = np.ones(Ta + Tt, dtype=bool)
+            if roles[l, h] != 0:
+                keep = o.keep_mask(b, l, h).astype(bool)
+                if roles[l, h] == 1:
+                    keep |= np.repeat(r["resident"][b].astype(bool), cl)[:Ta]
+                mask[:Ta] = keep
+            ref = _sdpa(q[b, l, hq], k[b, l, h], v[b, l, h], mask)
+            np.testing.assert_allclose(r["out"][b, l, hq], ref, rtol=0, atol=1e-12)
+            if (l, h) in ((0, 2), (1, 4)):
+                full = _sdpa(q[b, l, hq], k[b, l, h], v[b, l, h])
+                np.testing.assert_allclose(r["out"][b, l, hq], full, rtol=0, atol=1e-12)
+
+
+def test_retention_invalid_inputs_rejected(oracle_mod):
+    rng = np.random.default_rng(1)
+    k, v = _rand_cache(rng, 1, 1, 3, 20, 8)
+    roles = np.array([[0, 1, 2]], dtype=np.uint8)
+    pf = rng.random((1, 1, 3, 16), dtype=np.float32)
+    cfg = oracle_mod.make_cfg(1, 1, 3, 3, 8, 16, 4, 8, 2000)
+    for imp, lam in ((np.array([[0.5, 1.5, 0.5]]), 1.0), (np.array([[0.5, -0.1, 0.5]]), 1.0),
+                     (np.array([[0.5, np.nan, 0.5]]), 1.0), (np.full((1, 3), 0.5), -1.0),
+                     (np.full((1, 3), 0.5), np.inf), (np.full((1, 3), 0.5), np.nan)):
+        with pytest.raises(ValueError):
+            oracle_mod.Oracle(cfg, k, v, roles, pf, importance=imp.astype(np.float32), lam=lam)
