@@ -152,8 +152,9 @@ def run_timing(W, torch, w, timing, recall, kd, vd, qd, roles, prefill, args, ch
     first_bytes = st1["anchor_bytes"] + (st1["static_bytes"] if timing == "next" else 0)
     first = "attention" if timing == "next" else "anchor_attn"
     static_in_tf = st1["static_bytes"] if timing == "same" else 0
-    tf_bytes = static_in_tf + d["slot_rows"] / K * w.n_tidal * row_bytes
-    tf2_bytes = static_in_tf + d2["slot_rows"] / nr * w.n_tidal * row_bytes
+    # slot_rows: complement rows attended, summed over steps, sequences and tidal heads
+    tf_bytes = static_in_tf + d["slot_rows"] / K * row_bytes
+    tf2_bytes = static_in_tf + d2["slot_rows"] / nr * row_bytes
     a_ms, a2_ms = d["t_anchor_ms"] / n, d2["t_anchor_ms"] / n2
     r["first"] = first
     r["kernels"] = {

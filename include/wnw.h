@@ -119,7 +119,8 @@ typedef struct {
     double r_gpu_cpu;          /* paper's r_GPU+CPU: adds the host-resident complement   */
     int64_t anchor_bytes;      /* algorithmic HBM bytes of one anchor-attention launch   */
     int64_t static_bytes;      /* algorithmic HBM bytes of the fixed heads + tidal kept rows    */
-    int64_t slot_rows;         /* complement rows attended, summed over steps            */
+    int64_t slot_rows;         /* complement rows attended, summed over steps, sequences
+                                  and tidal heads                                         */
     /* WNW_F_TIMING only: summed times (ms) between HIP events recorded on the caller's stream
      * around the step's launches, and the number of timed steps. */
     int64_t timed_steps;
@@ -147,8 +148,20 @@ typedef struct {
 wnw_status wnw_init_cache(const wnw_config *cfg, const void *k_dev, const void *v_dev,
                           void *hip_stream, wnw_ctx **out);
 
+/* Per-head audio retention of Eq. 1 (Method, "Three-Way Classification"): every tidal and
+ * fixed head keeps the fraction retention = min(importance * lambda, 1) of the audio positions
+ * of each segment (taken in double: floor(retention * len)); anchors keep everything and text
+ * is always kept.  Without this call the retention is budget_bp / 10000 for every head.
+ *   importance  host fp32 [L][H_kv], each in [0, 1] (entries of anchor heads are ignored);
+ *               copied.  NULL restores the uniform budget.
+ *   lambda      finite, >= 0.
+ * Only before wnw_set_roles (WNW_ERR_STATE after it); WNW_ERR_INVALID for values outside
+ * those ranges.  k still comes from top_k or budget_bp. */
+wnw_status wnw_set_retention(wnw_ctx *ctx, const float *importance, float lambda);
+
 /* Assign roles and run prefill compression (Method, "Prefill Compression"): every tidal and
- * fixed head keeps floor(budget * len) positions of each chunk with the highest prefill score.
+ * fixed head keeps floor(retention * len) positions of each segment with the highest prefill
+ * score.
  *   roles           host uint8 [L][H_kv] of wnw_role, shared by the batch.
  *   prefill_scores  host fp32 [B][L][H_kv][T_a]; entries of anchor heads are ignored.
  * Builds the device tiers (anchor rows, kept rows, recall slots) and the pinned host
@@ -169,15 +182,19 @@ wnw_status wnw_set_roles(wnw_ctx *ctx, const uint8_t *roles, const float *prefil
 wnw_status wnw_decode_step(wnw_ctx *ctx, const void *q_dev, float *out_dev,
                            float *chunk_scores_dev, int32_t *selected_dev, void *hip_stream);
 
-/* Derived sizes: chunks (the selection's candidates), k, kept audio rows per tidal/fixed head,
- * recall slots per sequence, and bytes of one recalled segment of one sequence (all tidal
- * heads; a segment is a chunk unless WNW_F_OVERLAP_CHUNKS).  Any pointer may be NULL. */
+/* Derived sizes: chunks (the selection's candidates), k, kept audio rows per tidal/fixed head
+ * (-1 after wnw_set_retention: see wnw_query_head_keep), recall slots per sequence, and bytes of
+ * one recalled segment of one sequence (all tidal heads; a segment is a chunk unless
+ * WNW_F_OVERLAP_CHUNKS; known after wnw_set_roles).  Any pointer may be NULL. */
 wnw_status wnw_query_geometry(const wnw_ctx *ctx, int32_t *n_chunks, int32_t *k,
                               int32_t *keep_total, int32_t *n_slots, int64_t *chunk_bytes);
 
 /* Number of segments (the unit of residency and recall; equal to n_chunks unless
  * WNW_F_OVERLAP_CHUNKS, then n_chunks + 1).  The pointer may be NULL. */
 wnw_status wnw_query_segments(const wnw_ctx *ctx, int32_t *n_segments);
+
+/* Kept audio rows of every head, host int32 [L][H_kv] (T_a for anchors).  After wnw_set_roles. */
+wnw_status wnw_query_head_keep(const wnw_ctx *ctx, int32_t *keep);
 
 /* Counters and (with WNW_F_TIMING) kernel times; waits for the device. */
 wnw_status wnw_get_stats(wnw_ctx *ctx, wnw_stats *out);
@@ -190,7 +207,9 @@ wnw_status wnw_set_selection_override(wnw_ctx *ctx, const int32_t *sel_dev);
 
 /* Copy the device slot holding the recalled complement of (b, segment) to host_dst (waits for
  * the device).  Valid for segments resident after the last step (with WNW_F_SELECT_NEXT_STEP,
- * also those recalled during it).  Layout [n_tidal][2 (K, V)][comp_max][d] bf16; `bytes` must
+ * also those recalled during it).  Layout: per tidal head in role order (roles scanned in
+ * [L][H_kv] order), its complement K rows then V rows, c rows each, where c is that head's
+ * complement of a full segment (zero rows pad a shorter last segment); bf16 [..][d]; `bytes` must
  * equal chunk_bytes.  WNW_ERR_INVALID if that segment is not resident. */
 wnw_status wnw_debug_read_slot(wnw_ctx *ctx, int32_t b, int32_t chunk, void *host_dst, size_t bytes);
 

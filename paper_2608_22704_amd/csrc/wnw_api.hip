@@ -1,21 +1,24 @@
 // Host orchestrator of the WnW decode step: the C ABI of include/wnw.h.
 //
 // Set-up (wnw_set_roles) performs the paper's prefill compression on the host (per segment,
-// keep the floor(retention * len) positions with the highest prefill score) and lays the cache
-// out in device tiers:
+// keep the floor(retention * len) positions with the highest prefill score, retention uniform
+// or per head by Eq. 1) and lays the cache out in device tiers:
 //   anchor tier   [B][nA][T][d]       every row of every anchor head
-//   tidal tier    [B][nT][Rs][d]      kept audio rows (ascending) + text rows, Rs = keep + T_t
-//   fixed tier    [B][nF][Rs][d]      same for fixed heads (their complement is dropped)
-//   slots         [B][n_slots][nT][2][comp_max][d]   recalled complements, n_slots = delta * k
-//                 (delta + 1) * k with next-step timing
-//   host complement (pinned) [B][n_chunks][nT][2][comp_max][d]: chunk-major, so the complement
-//                 of one chunk for every tidal head of a sequence is one contiguous block.
+//   tidal tier    [B][RsT][d]         per tidal head in turn: kept audio rows (ascending) + text
+//   fixed tier    [B][RsF][d]         same for fixed heads (their complement is dropped)
+//   slots         [B][n_slots][blk_rows][d]   recalled segment blocks, n_slots from delta, k and
+//                 the chunk span (one more k's worth with next-step timing)
+//   host complement (pinned) [B][n_segments][blk_rows][d]: segment-major; the block of one
+//                 segment holds, per tidal head in turn, its complement K rows then V rows
+//                 (cfull of that head each, zero-padded in a short last segment), so the
+//                 complement of one segment for every tidal head of a sequence is contiguous.
 // A decode step is a fixed sequence of kernels on the caller's stream; recall runs on a side
 // stream joined by events (see wnw_decode_step below for the ordering argument).
 #include "wnw.h"
 #include "wnw_internal.h"
 
 #include <algorithm>
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -53,12 +56,18 @@ struct wnw_ctx {
     hipStream_t setup_stream = nullptr;
     const uint16_t *full_k = nullptr, *full_v = nullptr;
     std::vector<int32_t> anchor_lk, tidal_lk, fixed_lk;
+    std::vector<float> importance;     // [L][Hkv] per-head importance (Eq. 1), empty: uniform budget
+    float lambda = 0.f;
+    std::vector<HeadRows> hrows;       // [nT + nF]
+    std::vector<int32_t> head_keep;    // [nT + nF] kept audio rows
+    int64_t keep_sum_t = 0;            // kept audio rows over the tidal heads
 
     Tiers t{};
     StepBuffers s{};
     uint16_t *aK = nullptr, *aV = nullptr, *tK = nullptr, *tV = nullptr, *fK = nullptr, *fV = nullptr;
     uint16_t *slots = nullptr, *host_comp = nullptr;
-    int32_t *d_lk = nullptr;
+    int32_t *d_lk = nullptr, *d_tile_head = nullptr;
+    HeadRows *d_hr = nullptr;
     float *scores_int = nullptr;
     int32_t *sel_int = nullptr;
     const int32_t *override_sel = nullptr;
@@ -169,13 +178,7 @@ wnw_status derive(wnw_ctx *c, const wnw_config &cfg, Geometry &g)
     g.delta = cfg.evict_lag ? cfg.evict_lag : 3;
     g.next_step = (cfg.flags & WNW_F_SELECT_NEXT_STEP) ? 1 : 0;
     g.keep_total = 0;
-    g.comp_max = 0;
-    for (int ch = 0; ch < g.nc; ++ch) {
-        const int len = chunk_len_of(g, ch);
-        g.keep_total += keep_of_len(g.budget_bp, len);
-        g.comp_max = std::max(g.comp_max, comp_of(g, ch));
-    }
-    g.Rs = g.keep_total + g.Tt;
+    for (int ch = 0; ch < g.nc; ++ch) g.keep_total += keep_of_len(g.budget_bp, chunk_len_of(g, ch));
     // Slots: the resident set holds at most delta * k chunks, i.e. span * delta * k segments.
     // With next-step timing the segments dropped at a step keep their slots until that step's
     // attention has read them: span * k more.  Never more than one per segment.
@@ -188,26 +191,105 @@ wnw_status derive(wnw_ctx *c, const wnw_config &cfg, Geometry &g)
     g.n_tiles_a = (g.T + TILE_A - 1) / TILE_A;
     if ((int64_t)g.n_tiles_a * G * 8 > 65536) return fail(c, WNW_ERR_UNSUPPORTED, "cache of %d rows too long", g.T);
     g.maxc = (TILE_A - 1) / g.cl + 2;
-    g.n_tiles_s = (g.Rs + TILE_S - 1) / TILE_S;
-    g.slot_tile = g.comp_max <= TILE_S ? TILE_S : 2 * TILE_S;
-    g.sg = g.comp_max > 0 ? g.slot_tile / g.comp_max : 1;
-    // the kept list holds at most the resident segments (span * delta * k) in both timings
-    const int kept_max = (int)std::min<int64_t>(g.nc, (int64_t)g.delta * span * g.k);
-    g.ng_kept = g.comp_max > 0 ? (kept_max + g.sg - 1) / g.sg : 0;
-    g.np = g.n_tiles_s + g.ng_kept + (g.comp_max > 0 ? g.knew : 0);
-    if ((int64_t)g.np * G * 4 > 65536) return fail(c, WNW_ERR_UNSUPPORTED, "too many partial tiles per head");
     if (g.B > 65535 || (int64_t)g.L * g.Hkv > 65535) return fail(c, WNW_ERR_UNSUPPORTED, "batch or head count too large");
     return WNW_OK;
 }
 
-// Per-segment prefill keep selection of one head (Method, "Prefill Compression").
-void keep_rows(const Geometry &g, const float *score, std::vector<int32_t> &kept, std::vector<int32_t> &comp_by_chunk)
+// Keep count of a segment of `len` positions of the head at l * Hkv + kv: floor(retention *
+// len), with the uniform budget or with Eq. 1's per-head retention min(importance * lambda, 1)
+// (taken in double, where the product of the two fp32 inputs is exact).
+int head_keep_of_len(const wnw_ctx *c, int lkh, int len)
 {
+    if (c->importance.empty()) return keep_of_len(c->g.budget_bp, len);
+    double r = (double)c->importance[lkh] * (double)c->lambda;
+    if (r > 1.0) r = 1.0;
+    return (int)std::floor(r * (double)len);
+}
+
+// Per-head rows of the tidal and fixed heads, once the roles are known: static tiers, segment
+// complement blocks, static tiles and partial entries (HeadRows).
+wnw_status layout_heads(wnw_ctx *c)
+{
+    Geometry &g = c->g;
+    const int nsub = g.nT + g.nF;
+    c->hrows.assign(nsub, HeadRows{});
+    c->head_keep.assign(nsub, 0);
+    const int len0 = g.nc ? chunk_len_of(g, 0) : 0, lenl = g.nc ? chunk_len_of(g, g.nc - 1) : 0;
+    int64_t rowT = 0, rowF = 0, tiles = 0, coff = 0;
+    g.comp_max = g.csum_full = g.csum_last = 0;
+    g.keep_sum = 0;
+    c->keep_sum_t = 0;
+    for (int hi = 0; hi < nsub; ++hi) {
+        const bool tidal = hi < g.nT;
+        const int lkh = tidal ? c->tidal_lk[hi] : c->fixed_lk[hi - g.nT];
+        const int k0 = head_keep_of_len(c, lkh, len0), kl = head_keep_of_len(c, lkh, lenl);
+        const int keep = g.nc ? (g.nc - 1) * k0 + kl : 0;
+        HeadRows &h = c->hrows[hi];
+        h.rs = keep + g.Tt;
+        h.nts = (h.rs + TILE_S - 1) / TILE_S;
+        h.tile0 = (int)tiles;
+        tiles += h.nts;
+        h.srow = (int)(tidal ? rowT : rowF);
+        (tidal ? rowT : rowF) += h.rs;
+        h.sg = 1;
+        if (tidal) {
+            // the longest segment has the largest complement; the max guards the stride anyway
+            h.cfull = std::max(len0 - k0, lenl - kl);
+            h.clast = lenl - kl;
+            h.coff = (int)coff;
+            coff += 2 * h.cfull;
+            g.csum_full += h.cfull;
+            g.csum_last += h.clast;
+            g.comp_max = std::max(g.comp_max, h.cfull);
+            c->keep_sum_t += keep;
+        }
+        c->head_keep[hi] = keep;
+        g.keep_sum += keep;
+    }
+    if (rowT > INT32_MAX / 2 || rowF > INT32_MAX / 2 || tiles * g.B > INT32_MAX / 2 || coff * D > INT32_MAX)
+        return fail(c, WNW_ERR_UNSUPPORTED, "static tiers or complement blocks too large");
+    g.RsT = (int)rowT;
+    g.RsF = (int)rowF;
+    g.n_static = (int)tiles;
+    g.blk_rows = (int)coff;
+    g.chunk_elems = coff * D;
+    g.slot_tile = g.comp_max <= TILE_S ? TILE_S : 2 * TILE_S;
+    // the kept list holds at most the resident segments (span * delta * k) in both timings
+    const int kept_max = (int)std::min<int64_t>(g.nc, (int64_t)g.delta * g.span * g.k);
+    int64_t P = 0;
+    g.ng_kept = g.np_max = 0;
+    for (int hi = 0; hi < nsub; ++hi) {
+        HeadRows &h = c->hrows[hi];
+        if (h.cfull > 0) {
+            h.sg = g.slot_tile / h.cfull;
+            h.ngk = (kept_max + h.sg - 1) / h.sg;
+        }
+        g.ng_kept = std::max(g.ng_kept, h.ngk);
+        h.pbase = (int)P;
+        const int np = h.nts + (h.cfull > 0 ? h.ngk + g.knew : 0);
+        P += np;
+        g.np_max = std::max(g.np_max, np);
+    }
+    if ((int64_t)g.np_max * g.G * 4 > 65536) return fail(c, WNW_ERR_UNSUPPORTED, "too many partial tiles per head");
+    if (P * g.B > INT32_MAX / 2) return fail(c, WNW_ERR_UNSUPPORTED, "too many partial tiles");
+    const int64_t grid_max = std::max((int64_t)g.n_tiles_a * g.nA * g.B + (int64_t)g.n_static * g.B,
+                                      1024 + (int64_t)g.n_static * g.B + (int64_t)g.ng_kept * g.nT * g.B);
+    if (grid_max > INT32_MAX) return fail(c, WNW_ERR_UNSUPPORTED, "launch grid too large");
+    g.P = (int)P;
+    return WNW_OK;
+}
+
+// Per-segment prefill keep selection of one head (Method, "Prefill Compression"); the
+// complement of segment ch goes to comp_by_seg[ch * cstride ..] (cstride >= every complement).
+void keep_rows(const wnw_ctx *c, int lkh, const float *score, int cstride, std::vector<int32_t> &kept,
+               std::vector<int32_t> &comp_by_seg)
+{
+    const Geometry &g = c->g;
     kept.clear();
-    comp_by_chunk.assign((size_t)g.nc * g.comp_max, -1);
+    comp_by_seg.assign((size_t)g.nc * cstride, -1);
     std::vector<int32_t> pos;
     for (int ch = 0; ch < g.nc; ++ch) {
-        const int b0 = ch * g.cl, len = chunk_len_of(g, ch), kc = keep_of_len(g.budget_bp, len);
+        const int b0 = ch * g.cl, len = chunk_len_of(g, ch), kc = head_keep_of_len(c, lkh, len);
         pos.resize(len);
         std::iota(pos.begin(), pos.end(), b0);
         std::stable_sort(pos.begin(), pos.end(), [&](int32_t a, int32_t b) {
@@ -217,7 +299,7 @@ void keep_rows(const Geometry &g, const float *score, std::vector<int32_t> &kept
         std::sort(pos.begin(), pos.begin() + kc);
         std::sort(pos.begin() + kc, pos.end());
         kept.insert(kept.end(), pos.begin(), pos.begin() + kc);
-        std::copy(pos.begin() + kc, pos.end(), comp_by_chunk.begin() + (size_t)ch * g.comp_max);
+        if (cstride) std::copy(pos.begin() + kc, pos.end(), comp_by_seg.begin() + (size_t)ch * cstride);
     }
 }
 
@@ -282,7 +364,8 @@ wnw_status harvest_timing(wnw_ctx *c)
 
 void free_all(wnw_ctx *c)
 {
-    void *ptrs[] = {c->aK, c->aV, c->tK, c->tV, c->fK, c->fV, c->slots, c->d_lk, c->scores_int, c->sel_int,
+    void *ptrs[] = {c->aK, c->aV, c->tK, c->tV, c->fK, c->fV, c->slots, c->d_lk, c->d_tile_head, c->d_hr,
+                    c->scores_int, c->sel_int,
                     c->s.pa_m, c->s.pa_l, c->s.pa_o, c->s.pa_mass, c->s.mass, c->s.ps_m, c->s.ps_l, c->s.ps_o,
                     c->s.streak, c->s.slot_of, c->s.slot_last, c->s.att, c->s.slot_data, c->s.slot_busy, c->s.slot_since,
                     c->s.step, c->s.kept_list, c->s.new_list, c->s.counts, c->s.stats};
@@ -347,7 +430,8 @@ wnw_status wnw_set_roles(wnw_ctx *c, const uint8_t *roles, const float *prefill)
     g.nA = (int)c->anchor_lk.size();
     g.nT = (int)c->tidal_lk.size();
     g.nF = (int)c->fixed_lk.size();
-    g.chunk_elems = (int64_t)g.nT * 2 * g.comp_max * D;
+    wnw_status lr = layout_heads(c);
+    if (lr != WNW_OK) return lr;
     DeviceGuard dg(c->device);
     hipStream_t st = c->setup_stream;
     const size_t B = g.B, Dz = D;
@@ -358,12 +442,14 @@ wnw_status wnw_set_roles(wnw_ctx *c, const uint8_t *roles, const float *prefill)
     if ((r = dalloc(c, &(p), (size_t)(n), what)) != WNW_OK) return r
     ALLOC(c->aK, B * g.nA * g.T * Dz, "anchor K");
     ALLOC(c->aV, B * g.nA * g.T * Dz, "anchor V");
-    ALLOC(c->tK, B * g.nT * g.Rs * Dz, "tidal K");
-    ALLOC(c->tV, B * g.nT * g.Rs * Dz, "tidal V");
-    ALLOC(c->fK, B * g.nF * g.Rs * Dz, "fixed K");
-    ALLOC(c->fV, B * g.nF * g.Rs * Dz, "fixed V");
+    ALLOC(c->tK, B * g.RsT * Dz, "tidal K");
+    ALLOC(c->tV, B * g.RsT * Dz, "tidal V");
+    ALLOC(c->fK, B * g.RsF * Dz, "fixed K");
+    ALLOC(c->fV, B * g.RsF * Dz, "fixed V");
     ALLOC(c->slots, B * g.n_slots * g.chunk_elems, "recall slots");
     ALLOC(c->d_lk, (size_t)nh, "role tables");
+    ALLOC(c->d_hr, c->hrows.size(), "head rows");
+    ALLOC(c->d_tile_head, (size_t)g.n_static, "static tile table");
     ALLOC(c->scores_int, B * g.nchk, "scores");
     ALLOC(c->sel_int, B * g.k, "selection");
     StepBuffers &s = c->s;
@@ -372,9 +458,9 @@ wnw_status wnw_set_roles(wnw_ctx *c, const uint8_t *roles, const float *prefill)
     ALLOC(s.pa_o, B * g.nA * g.n_tiles_a * g.G * Dz, "anchor partial out");
     ALLOC(s.pa_mass, B * g.nA * g.n_tiles_a * g.G * g.maxc, "anchor partial mass");
     ALLOC(s.mass, B * g.nA * g.G * g.nc, "chunk mass");
-    ALLOC(s.ps_m, B * (g.nT + g.nF) * g.np * g.G, "partial max");
-    ALLOC(s.ps_l, B * (g.nT + g.nF) * g.np * g.G, "partial sum");
-    ALLOC(s.ps_o, B * (g.nT + g.nF) * g.np * g.G * Dz, "partial out");
+    ALLOC(s.ps_m, B * g.P * g.G, "partial max");
+    ALLOC(s.ps_l, B * g.P * g.G, "partial sum");
+    ALLOC(s.ps_o, B * g.P * g.G * Dz, "partial out");
     ALLOC(s.streak, B * g.nchk, "streaks");
     ALLOC(s.slot_of, B * g.nc, "slot map");
     ALLOC(s.slot_last, B * g.nc, "slot history");
@@ -411,6 +497,17 @@ wnw_status wnw_set_roles(wnw_ctx *c, const uint8_t *roles, const float *prefill)
     lk.insert(lk.end(), c->tidal_lk.begin(), c->tidal_lk.end());
     lk.insert(lk.end(), c->fixed_lk.begin(), c->fixed_lk.end());
     if (nh) HIPCHECK(c, hipMemcpy(c->d_lk, lk.data(), nh * sizeof(int32_t), hipMemcpyHostToDevice));
+    if (!c->hrows.empty())
+        HIPCHECK(c, hipMemcpy(c->d_hr, c->hrows.data(), c->hrows.size() * sizeof(HeadRows), hipMemcpyHostToDevice));
+    {
+        std::vector<int32_t> th((size_t)g.n_static);
+        for (int hi = 0; hi < (int)c->hrows.size(); ++hi)
+            for (int j = 0; j < c->hrows[hi].nts; ++j) th[(size_t)c->hrows[hi].tile0 + j] = hi;
+        if (!th.empty())
+            HIPCHECK(c, hipMemcpy(c->d_tile_head, th.data(), th.size() * sizeof(int32_t), hipMemcpyHostToDevice));
+    }
+    c->t.hr = c->d_hr;
+    c->t.tile_head = c->d_tile_head;
     c->t.anchor_lk = c->d_lk;
     c->t.tidal_lk = c->d_lk + g.nA;
     c->t.fixed_lk = c->d_lk + g.nA + g.nT;
@@ -422,7 +519,7 @@ wnw_status wnw_set_roles(wnw_ctx *c, const uint8_t *roles, const float *prefill)
     // ---- per-sequence tier construction ------------------------------------------------------
     const int nsub = g.nT + g.nF;
     const size_t seq_rows = (size_t)g.L * g.Hkv * g.T;
-    std::vector<int32_t> static_idx((size_t)nsub * g.Rs), comp_idx((size_t)g.nc * g.nT * 2 * g.comp_max);
+    std::vector<int32_t> static_idx((size_t)g.RsT + g.RsF), comp_idx((size_t)g.nc * g.blk_rows);
     int32_t *d_idx = nullptr;
     uint16_t *staging = nullptr;
     const size_t idx_n = std::max(static_idx.size(), comp_idx.size());
@@ -454,32 +551,34 @@ wnw_status wnw_set_roles(wnw_ctx *c, const uint8_t *roles, const float *prefill)
             const bool tidal = hi < g.nT;
             const int lkh = tidal ? c->tidal_lk[hi] : c->fixed_lk[hi - g.nT];
             const float *sc = prefill + ((size_t)b * nh + lkh) * g.Ta;
+            const HeadRows &hr = c->hrows[hi];
+            const int keep = c->head_keep[hi];
             std::vector<int32_t> kept, comp;
-            keep_rows(g, sc, kept, comp);
+            keep_rows(c, lkh, sc, hr.cfull, kept, comp);
             const int32_t base = (int32_t)((size_t)lkh * g.T);
-            int32_t *si = static_idx.data() + (size_t)hi * g.Rs;
-            for (int i = 0; i < g.keep_total; ++i) si[i] = base + kept[i];
-            for (int i = 0; i < g.Tt; ++i) si[g.keep_total + i] = base + g.Ta + i;
+            int32_t *si = static_idx.data() + (tidal ? 0 : (size_t)g.RsT) + hr.srow;
+            for (int i = 0; i < keep; ++i) si[i] = base + kept[i];
+            for (int i = 0; i < g.Tt; ++i) si[keep + i] = base + g.Ta + i;
             if (tidal)
                 for (int ch = 0; ch < g.nc; ++ch)
                     for (int half = 0; half < 2; ++half)
-                        for (int rr = 0; rr < g.comp_max; ++rr) {
-                            const int32_t p = comp[(size_t)ch * g.comp_max + rr];
+                        for (int rr = 0; rr < hr.cfull; ++rr) {
+                            const int32_t p = comp[(size_t)ch * hr.cfull + rr];
                             // K rows index the K cache (>= 0), V rows are encoded as -(row + 2)
-                            comp_idx[(((size_t)ch * g.nT + hi) * 2 + half) * g.comp_max + rr] =
+                            comp_idx[(size_t)ch * g.blk_rows + hr.coff + (size_t)half * hr.cfull + rr] =
                                 p < 0 ? -1 : (half == 0 ? base + p : -(base + p) - 2);
                         }
         });
         // static rows of tidal and fixed heads
         hipError_t e = hipMemcpyAsync(d_idx, static_idx.data(), static_idx.size() * sizeof(int32_t), hipMemcpyHostToDevice, st);
-        if (e == hipSuccess && g.nT)
-            e = launch_gather_rows(c->tK + (size_t)b * g.nT * g.Rs * D, fk, fv, d_idx, (int64_t)g.nT * g.Rs, st);
-        if (e == hipSuccess && g.nT)
-            e = launch_gather_rows(c->tV + (size_t)b * g.nT * g.Rs * D, fv, fv, d_idx, (int64_t)g.nT * g.Rs, st);
-        if (e == hipSuccess && g.nF)
-            e = launch_gather_rows(c->fK + (size_t)b * g.nF * g.Rs * D, fk, fv, d_idx + (size_t)g.nT * g.Rs, (int64_t)g.nF * g.Rs, st);
-        if (e == hipSuccess && g.nF)
-            e = launch_gather_rows(c->fV + (size_t)b * g.nF * g.Rs * D, fv, fv, d_idx + (size_t)g.nT * g.Rs, (int64_t)g.nF * g.Rs, st);
+        if (e == hipSuccess && g.RsT)
+            e = launch_gather_rows(c->tK + (size_t)b * g.RsT * D, fk, fv, d_idx, g.RsT, st);
+        if (e == hipSuccess && g.RsT)
+            e = launch_gather_rows(c->tV + (size_t)b * g.RsT * D, fv, fv, d_idx, g.RsT, st);
+        if (e == hipSuccess && g.RsF)
+            e = launch_gather_rows(c->fK + (size_t)b * g.RsF * D, fk, fv, d_idx + (size_t)g.RsT, g.RsF, st);
+        if (e == hipSuccess && g.RsF)
+            e = launch_gather_rows(c->fV + (size_t)b * g.RsF * D, fv, fv, d_idx + (size_t)g.RsT, g.RsF, st);
         if (e == hipSuccess) e = hipStreamSynchronize(st);   // static_idx is rewritten next
         // tidal complement, chunk-major, then to pinned host memory
         if (e == hipSuccess && g.chunk_elems) {
@@ -645,12 +744,41 @@ wnw_status wnw_query_geometry(const wnw_ctx *c, int32_t *n_chunks, int32_t *k, i
     if (!c) return fail(nullptr, WNW_ERR_INVALID, "ctx is NULL");
     if (n_chunks) *n_chunks = c->g.nchk;
     if (k) *k = c->g.k;
-    if (keep_total) *keep_total = c->g.keep_total;
+    if (keep_total) *keep_total = c->importance.empty() ? c->g.keep_total : -1;
     if (n_slots) *n_slots = c->g.n_slots;
     if (chunk_bytes) {
         if (c->state == CREATED) return fail(const_cast<wnw_ctx *>(c), WNW_ERR_STATE, "chunk size is known after wnw_set_roles");
         *chunk_bytes = c->g.chunk_elems * (int64_t)sizeof(uint16_t);
     }
+    return WNW_OK;
+}
+
+wnw_status wnw_set_retention(wnw_ctx *c, const float *importance, float lambda)
+{
+    if (!c) return fail(nullptr, WNW_ERR_INVALID, "ctx is NULL");
+    if (c->state != CREATED) return fail(c, WNW_ERR_STATE, "wnw_set_retention must come before wnw_set_roles");
+    const size_t nh = (size_t)c->g.L * c->g.Hkv;
+    if (!importance) {
+        c->importance.clear();
+        return WNW_OK;
+    }
+    if (!(lambda >= 0.f) || std::isinf(lambda)) return fail(c, WNW_ERR_INVALID, "lambda must be finite and >= 0");
+    for (size_t i = 0; i < nh; ++i)
+        if (!(importance[i] >= 0.f && importance[i] <= 1.f))
+            return fail(c, WNW_ERR_INVALID, "importance of head %zu is not in [0, 1]", i);
+    c->importance.assign(importance, importance + nh);
+    c->lambda = lambda;
+    return WNW_OK;
+}
+
+wnw_status wnw_query_head_keep(const wnw_ctx *c, int32_t *keep)
+{
+    if (!c || !keep) return fail(const_cast<wnw_ctx *>(c), WNW_ERR_INVALID, "ctx and keep must not be NULL");
+    if (c->state == CREATED) return fail(const_cast<wnw_ctx *>(c), WNW_ERR_STATE, "keep counts are known after wnw_set_roles");
+    const Geometry &g = c->g;
+    for (int a : c->anchor_lk) keep[a] = g.Ta;
+    for (int i = 0; i < g.nT; ++i) keep[c->tidal_lk[i]] = c->head_keep[i];
+    for (int i = 0; i < g.nF; ++i) keep[c->fixed_lk[i]] = c->head_keep[g.nT + i];
     return WNW_OK;
 }
 
@@ -684,11 +812,12 @@ wnw_status wnw_get_stats(wnw_ctx *c, wnw_stats *o)
     const double full = (double)g.L * g.Hkv * g.Ta;
     const double res_rows = c->steps ? (double)st[3] / ((double)c->steps * g.B) : 0.0;
     if (full > 0) {
-        o->r_gpu = ((double)g.nA * g.Ta + (double)(g.nT + g.nF) * g.keep_total + (double)g.nT * res_rows) / full;
-        o->r_gpu_cpu = o->r_gpu + (double)g.nT * (g.Ta - g.keep_total) / full;
+        // slot_rows sums the attended complement rows over the tidal heads
+        o->r_gpu = ((double)g.nA * g.Ta + (double)g.keep_sum + res_rows) / full;
+        o->r_gpu_cpu = o->r_gpu + ((double)g.nT * g.Ta - (double)c->keep_sum_t) / full;
     }
     o->anchor_bytes = (int64_t)g.B * g.nA * g.T * 2 * D * 2;
-    o->static_bytes = (int64_t)g.B * (g.nT + g.nF) * g.Rs * 2 * D * 2;
+    o->static_bytes = (int64_t)g.B * ((int64_t)g.RsT + g.RsF) * 2 * D * 2;
     o->revived_chunks = (int64_t)st[6];
     o->timed_steps = c->timed_steps;
     o->t_anchor_ms = c->t_acc[0];

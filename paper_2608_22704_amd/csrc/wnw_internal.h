@@ -26,17 +26,39 @@ struct Geometry {
     int k, knew, delta;         // chunks selected per step, segments newly resident per step at
                                 // most (span * k), eviction lag
     int next_step;              // 1: tidal heads of step s attend over the resident set of step s-1
-    int keep_total, Rs;         // kept audio rows per non-anchor head; static rows = keep + text
-    int comp_max;               // complement rows of a full chunk (chunk_len - keep(chunk_len))
+    int keep_total;             // kept audio rows per non-anchor head with the uniform budget
+                                // (-1 with per-head retention)
     int n_slots;                // recall slots per sequence
     int nA, nT, nF;             // anchor / tidal / fixed KV-heads over all layers
     int n_tiles_a, maxc;        // anchor tiles per head, chunk entries per anchor tile
-    int n_tiles_s;              // static tiles per tidal/fixed head
+    // Set with the roles (per-head rows, see HeadRows):
+    int RsT, RsF;               // rows of a sequence's tidal / fixed static tier
+    int n_static;               // static tiles of one sequence (all tidal and fixed heads)
+    int P, np_max;              // partial entries of one sequence; most of one head
+    int comp_max;               // largest complement of one segment of one tidal head
+    int blk_rows;               // rows of one segment's complement block (every tidal head, K and V)
+    int csum_full, csum_last;   // complement rows of a full / the last segment over all tidal heads
+    int64_t keep_sum;           // kept audio rows over all non-anchor heads
     int slot_tile;              // rows of one slot-group work-group (TILE_S or 2 * TILE_S)
-    int sg;                     // slots per slot-group work-group
-    int ng_kept;                // slot groups for kept complements (new ones: one partial each)
-    int np;                     // partial entries per tidal/fixed head: static tiles, kept groups, knew new
-    int64_t chunk_elems;        // bf16 elements of one recalled chunk of one sequence
+    int ng_kept;                // kept-slot groups of the head with the most
+    int64_t chunk_elems;        // bf16 elements of one segment's complement block (blk_rows * D)
+};
+
+// Rows of one non-anchor head (tidal heads 0..nT-1, then fixed heads), whose audio retention
+// may differ from head to head (Eq. 1).  Partials of a head: its static tiles, then (tidal) its
+// kept groups, then one per newly resident segment.
+struct HeadRows {
+    int srow;    // first row of the head in its sequence's static tier (tidal or fixed)
+    int rs;      // static rows: kept audio rows (ascending) + text rows
+    int nts;     // static tiles
+    int tile0;   // first static tile of the head among its sequence's static tiles
+    int pbase;   // first partial entry of the head among its sequence's partials
+    // tidal heads (0 for fixed heads)
+    int cfull;   // complement rows of a full segment (the longest one)
+    int clast;   // complement rows of the last segment
+    int coff;    // first row of the head in a segment's complement block: cfull K rows, cfull V rows
+    int sg;      // kept slots per slot-group work-group (>= 1)
+    int ngk;     // kept-slot groups
 };
 
 // Keep count of a chunk of `len` positions: floor(retention * len).
@@ -49,19 +71,16 @@ __host__ __device__ inline int chunk_len_of(const Geometry &g, int c)
     int e = (c + 1) * g.cl;
     return (e < g.Ta ? e : g.Ta) - c * g.cl;
 }
-__host__ __device__ inline int comp_of(const Geometry &g, int c)
-{
-    int len = chunk_len_of(g, c);
-    return len - keep_of_len(g.budget_bp, len);
-}
 
 struct Tiers {
     const uint16_t *aK, *aV;    // [B][nA][T][D]
-    const uint16_t *tK, *tV;    // [B][nT][Rs][D]
-    const uint16_t *fK, *fV;    // [B][nF][Rs][D]
-    uint16_t *slots;            // [B][n_slots][nT][2][comp_max][D]
-    const uint16_t *host_comp;  // device view of pinned [B][nc][nT][2][comp_max][D]
+    const uint16_t *tK, *tV;    // [B][RsT][D]: tidal heads one after the other (HeadRows::srow, rs)
+    const uint16_t *fK, *fV;    // [B][RsF][D]: fixed heads likewise
+    uint16_t *slots;            // [B][n_slots][blk_rows][D]
+    const uint16_t *host_comp;  // device view of pinned [B][nc][blk_rows][D]
     const int32_t *anchor_lk, *tidal_lk, *fixed_lk;  // l * Hkv + kv of each role's heads
+    const HeadRows *hr;         // [nT + nF]
+    const int32_t *tile_head;   // [n_static] head of each static tile of a sequence
 };
 
 struct StepBuffers {
@@ -71,8 +90,8 @@ struct StepBuffers {
     double *pa_mass;            // [B][nA][n_tiles_a][G][maxc]
     double *mass;               // [B][nA*G][nc]
     // tidal/fixed partials, head index = tidal 0..nT-1 then fixed nT..nT+nF-1
-    float *ps_m, *ps_l;         // [B][nT+nF][np][G]
-    float *ps_o;                // [B][nT+nF][np][G][D]
+    float *ps_m, *ps_l;         // [B][P][G]    (HeadRows::pbase + entry)
+    float *ps_o;                // [B][P][G][D]
     // selection state (chunks for the selection and streaks; segments for everything else)
     int32_t *streak;            // [B][nchk] steps since the chunk's last selection, capped at delta
     int32_t *slot_of;           // [B][nc]  slot holding the segment's complement or -1

@@ -640,7 +640,7 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
         fkept[u] = nxt ? owned : (now && owned);
         const bool att = nxt ? owned : now;
         g_att[u] = att;
-        if (att) atomicAdd(&nrows, comp_of(g, u));
+        if (att) atomicAdd(&nrows, u == nu - 1 ? g.csum_last : g.csum_full);
         if (fdrop[u]) {
             busy[sof[u]] = nxt ? 2 : 0;
             since[sof[u]] = step;
@@ -1031,27 +1031,32 @@ struct RecallRows {
 constexpr int RPL_S = TILE_S / (4 * WAVES);   // 8
 constexpr int RECALL_WGS = 64;                // work-groups that recall (they fill the host link)
 
+// Static tile j (of the sequence's n_static) of sequence b: kept rows + text of one head.
 template <int G>
-__device__ inline void static_tile(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, int tile,
-                                   int hi, int b, SubsetSmem<G, RPL_S> &sm)
+__device__ inline void static_tile(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, int j,
+                                   int b, SubsetSmem<G, RPL_S> &sm)
 {
+    const int hi = t.tile_head[j];
+    const HeadRows hr = t.hr[hi];
+    const int tile = j - hr.tile0;
     const bool tidal = hi < g.nT;
-    const int idx = tidal ? hi : hi - g.nT;
-    const int lk = tidal ? t.tidal_lk[idx] : t.fixed_lk[idx], l = lk / g.Hkv, kv = lk - l * g.Hkv;
-    const size_t hb = ((size_t)b * (tidal ? g.nT : g.nF) + idx) * (size_t)g.Rs * D;
-    const StaticRows map{(tidal ? t.tK : t.fK) + hb, (tidal ? t.tV : t.fV) + hb, tile * TILE_S, g.Rs};
+    const int lk = tidal ? t.tidal_lk[hi] : t.fixed_lk[hi - g.nT], l = lk / g.Hkv, kv = lk - l * g.Hkv;
+    const size_t hb = ((size_t)b * (tidal ? g.RsT : g.RsF) + hr.srow) * D;
+    const StaticRows map{(tidal ? t.tK : t.fK) + hb, (tidal ? t.tV : t.fV) + hb, tile * TILE_S, hr.rs};
     const uint16_t *qh = q + (((size_t)b * g.L + l) * g.Hq + (size_t)kv * G) * D;
-    const size_t p = ((size_t)b * (g.nT + g.nF) + hi) * g.np + tile;
+    const size_t p = (size_t)b * g.P + hr.pbase + tile;
     subset_tile<G, RPL_S>(qh, map, s.ps_m + p * G, s.ps_l + p * G, s.ps_o + p * G * D, sm);
 }
 
-// Slot group `grp` of list `which` (0 kept, 1 new) of tidal head ti; epg entries per group.
+// Slot group `grp` of list `which` (0 kept: the head's sg entries per group; 1 new: one entry)
+// of tidal head ti.
 template <int G, int RPL>
 __device__ inline void slot_group(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, int grp,
-                                  int ti, int b, int which, int epg, SubsetSmem<G, RPL> &sm)
+                                  int ti, int b, int which, SubsetSmem<G, RPL> &sm)
 {
-    const int cnt = s.counts[b * 2 + which];
-    if (grp * epg >= cnt) return;
+    const HeadRows hr = t.hr[ti];
+    const int cnt = s.counts[b * 2 + which], epg = which ? 1 : hr.sg;
+    if (hr.cfull == 0 || (!which && grp >= hr.ngk) || grp * epg >= cnt) return;
     constexpr int MAXE = 4 * RPL * WAVES;   // entries of one group never exceed its rows
     __shared__ const uint16_t *kbase[MAXE];
     __shared__ int nrows[MAXE];
@@ -1060,14 +1065,14 @@ __device__ inline void slot_group(const Geometry &g, const Tiers &t, const StepB
                           (size_t)grp * epg * 2;
     for (int e = threadIdx.x; e < n_entries; e += NT) {
         const int c = list[e * 2], slot = list[e * 2 + 1];
-        kbase[e] = t.slots + ((size_t)b * g.n_slots + slot) * g.chunk_elems + (size_t)ti * 2 * g.comp_max * D;
-        nrows[e] = comp_of(g, c);
+        kbase[e] = t.slots + ((size_t)b * g.n_slots + slot) * g.chunk_elems + (size_t)hr.coff * D;
+        nrows[e] = c == g.nc - 1 ? hr.clast : hr.cfull;
     }
     __syncthreads();
     const int lk = t.tidal_lk[ti], l = lk / g.Hkv, kv = lk - l * g.Hkv;
-    const SlotRows map{kbase, nrows, n_entries, g.comp_max};
+    const SlotRows map{kbase, nrows, n_entries, hr.cfull};
     const uint16_t *qh = q + (((size_t)b * g.L + l) * g.Hq + (size_t)kv * G) * D;
-    const size_t p = ((size_t)b * (g.nT + g.nF) + ti) * g.np + g.n_tiles_s + (which ? g.ng_kept : 0) + grp;
+    const size_t p = (size_t)b * g.P + hr.pbase + hr.nts + (which ? hr.ngk : 0) + grp;
     subset_tile<G, RPL>(qh, map, s.ps_m + p * G, s.ps_l + p * G, s.ps_o + p * G * D, sm);
 }
 
@@ -1084,22 +1089,24 @@ __device__ inline void recall_units(const Geometry &g, const Tiers &t, const Ste
         int b = 0, r = u;
         while (r >= s.counts[b * 2 + 1] * g.nT) r -= s.counts[b++ * 2 + 1] * g.nT;
         const int e = r / g.nT, ti = r - e * g.nT;
+        const HeadRows hr = t.hr[ti];
+        if (hr.cfull == 0) continue;   // retention 1: nothing of this head to recall
         const int c = s.new_list[((size_t)b * g.knew + e) * 2], slot = s.new_list[((size_t)b * g.knew + e) * 2 + 1];
-        const size_t off = (size_t)ti * 2 * g.comp_max * D;
+        const size_t off = (size_t)hr.coff * D;
         const uint16_t *src = t.host_comp + ((size_t)b * g.nc + c) * g.chunk_elems + off;
         uint16_t *dst = t.slots + ((size_t)b * g.n_slots + slot) * g.chunk_elems + off;
-        const int nr = comp_of(g, c);
-        // rows past the chunk's complement (short last chunk) are zero padding: copied for a
+        const int cm = hr.cfull, nr = c == g.nc - 1 ? hr.clast : cm;
+        // rows past the segment's complement (short last segment) are zero padding: copied for a
         // byte-identical slot, not attended
-        for (int j = threadIdx.x; j < (g.comp_max - nr) * 2 * (D / 8); j += NT) {
-            const int half = j / ((g.comp_max - nr) * (D / 8)), rem = j - half * (g.comp_max - nr) * (D / 8);
-            const size_t o = ((size_t)half * g.comp_max + nr) * D + (size_t)rem * 8;
+        for (int j = threadIdx.x; j < (cm - nr) * 2 * (D / 8); j += NT) {
+            const int half = j / ((cm - nr) * (D / 8)), rem = j - half * (cm - nr) * (D / 8);
+            const size_t o = ((size_t)half * cm + nr) * D + (size_t)rem * 8;
             *(uint4 *)(dst + o) = *(const uint4 *)(src + o);
         }
         const int lk = t.tidal_lk[ti], l = lk / g.Hkv, kv = lk - l * g.Hkv;
         const uint16_t *qh = q + (((size_t)b * g.L + l) * g.Hq + (size_t)kv * G) * D;
-        const size_t p = ((size_t)b * (g.nT + g.nF) + ti) * g.np + g.n_tiles_s + g.ng_kept + e;
-        const RecallRows map{src, dst, nr, g.comp_max};
+        const size_t p = (size_t)b * g.P + hr.pbase + hr.nts + hr.ngk + e;
+        const RecallRows map{src, dst, nr, cm};
         subset_tile<G, RPL>(qh, map, s.ps_m + p * G, s.ps_l + p * G, s.ps_o + p * G * D, sm);
     }
 }
@@ -1126,15 +1133,14 @@ __global__ __launch_bounds__(NT, REC ? (RPLK == RPL_S ? 2 : 1) : (RPLK == RPL_S 
         }
         bid -= RECALL_WGS;
     }
-    const int nh = g.nT + g.nF, n_static = with_static ? g.n_tiles_s * nh * g.B : 0;
+    const int n_static = with_static ? g.n_static * g.B : 0;
     if (bid < n_static) {
-        const int tile = bid % g.n_tiles_s, rest = bid / g.n_tiles_s;
-        static_tile<G>(g, t, s, q, tile, rest % nh, rest / nh, sm.st);
+        static_tile<G>(g, t, s, q, bid % g.n_static, bid / g.n_static, sm.st);
         return;
     }
     bid -= n_static;
     const int grp = bid % g.ng_kept, rest = bid / g.ng_kept;
-    slot_group<G, RPLK>(g, t, s, q, grp, rest % g.nT, rest / g.nT, 0, g.sg, sm.sl);
+    slot_group<G, RPLK>(g, t, s, q, grp, rest % g.nT, rest / g.nT, 0, sm.sl);
 }
 
 // Anchor tiles and the static tidal/fixed tiles (kept rows + text, which no selection changes)
@@ -1151,7 +1157,7 @@ __global__ __launch_bounds__(NT, G <= 4 ? 4 : 2) void attention_kernel(Geometry 
     };
     __shared__ Smem sm;
     const long long na = (long long)g.n_tiles_a * g.nA * g.B;
-    const long long nh = g.nT + g.nF, n = na + (long long)g.n_tiles_s * nh * g.B;
+    const long long n = na + (long long)g.n_static * g.B;
     const long long p = blockIdx.x, a0 = p * na / n, a1 = (p + 1) * na / n;
     if (a1 > a0) {
         // anchors before this position: a0, so this is anchor tile a0
@@ -1160,42 +1166,42 @@ __global__ __launch_bounds__(NT, G <= 4 ? 4 : 2) void attention_kernel(Geometry 
         anchor_tile<G>(g, t, s, q, tile, (int)(rest % g.nA), (int)(rest / g.nA), sm.a);
     } else {
         const long long i = p - a0;   // static tiles before this position
-        const int tile = (int)(i % g.n_tiles_s);
-        const long long rest = i / g.n_tiles_s;
-        static_tile<G>(g, t, s, q, tile, (int)(rest % nh), (int)(rest / nh), sm.st);
+        static_tile<G>(g, t, s, q, (int)(i % g.n_static), (int)(i / g.n_static), sm.st);
     }
 }
 
 // Next-step timing: copy only.  Work-group w of RECALL_WGS walks the units (sequence, new entry,
-// tidal head) and copies each unit's block (K and V complement rows, padding included) from
-// mapped pinned memory to its slot, eight 16-byte reads in flight per thread; the rows are
-// attended from the next step on.  Host reads take ~15 us, so the link needs about a megabyte
-// in flight: the number of work-groups, each holding one unit, sets the rate.
+// piece) and copies each piece of the entry's segment block (every tidal head's K and V
+// complement rows, padding included; 32 KB per piece) from mapped pinned memory to its slot,
+// eight 16-byte reads in flight per thread; the rows are attended from the next step on.  Host
+// reads take ~15 us, so the link needs about a megabyte in flight: the number of work-groups,
+// each holding one piece, sets the rate.
 __global__ __launch_bounds__(NT) void recall_copy_kernel(Geometry g, Tiers t, StepBuffers s)
 {
+    constexpr int PIECE = 8 * NT;                                  // 16-byte vectors per piece
+    const long long n16 = g.chunk_elems / 8;                       // 16-byte vectors per block
+    const int npc = (int)((n16 + PIECE - 1) / PIECE);
     int total = 0;
-    for (int b = 0; b < g.B; ++b) total += s.counts[b * 2 + 1] * g.nT;
-    const int n16 = 2 * g.comp_max * (D / 8);   // 16-byte vectors per unit
+    for (int b = 0; b < g.B; ++b) total += s.counts[b * 2 + 1] * npc;
     for (int u = blockIdx.x; u < total; u += gridDim.x) {
         int b = 0, r = u;
-        while (r >= s.counts[b * 2 + 1] * g.nT) r -= s.counts[b++ * 2 + 1] * g.nT;
-        const int e = r / g.nT, ti = r - e * g.nT;
+        while (r >= s.counts[b * 2 + 1] * npc) r -= s.counts[b++ * 2 + 1] * npc;
+        const int e = r / npc, pc = r - e * npc;
         const int c = s.new_list[((size_t)b * g.knew + e) * 2], slot = s.new_list[((size_t)b * g.knew + e) * 2 + 1];
-        const size_t off = (size_t)ti * 2 * g.comp_max * D;
-        const uint4 *src = (const uint4 *)(t.host_comp + ((size_t)b * g.nc + c) * g.chunk_elems + off);
-        uint4 *dst = (uint4 *)(t.slots + ((size_t)b * g.n_slots + slot) * g.chunk_elems + off);
-        for (int j0 = 0; j0 < n16; j0 += 8 * NT) {
-            uint4 v[8];
+        const long long j0 = (long long)pc * PIECE;
+        const uint4 *src = (const uint4 *)(t.host_comp + ((size_t)b * g.nc + c) * g.chunk_elems) + j0;
+        uint4 *dst = (uint4 *)(t.slots + ((size_t)b * g.n_slots + slot) * g.chunk_elems) + j0;
+        const int nv = (int)min((long long)PIECE, n16 - j0);
+        uint4 v[8];
 #pragma unroll
-            for (int k = 0; k < 8; ++k) {
-                const int j = j0 + k * NT + threadIdx.x;
-                if (j < n16) v[k] = src[j];
-            }
+        for (int k = 0; k < 8; ++k) {
+            const int j = k * NT + threadIdx.x;
+            if (j < nv) v[k] = src[j];
+        }
 #pragma unroll
-            for (int k = 0; k < 8; ++k) {
-                const int j = j0 + k * NT + threadIdx.x;
-                if (j < n16) dst[j] = v[k];
-            }
+        for (int k = 0; k < 8; ++k) {
+            const int j = k * NT + threadIdx.x;
+            if (j < nv) dst[j] = v[k];
         }
     }
 }
@@ -1205,7 +1211,7 @@ template <int G, int RPL>
 __global__ __launch_bounds__(NT, RPL == RPL_S ? 4 : 2) void new_slots_kernel(Geometry g, Tiers t, StepBuffers s, const uint16_t *__restrict__ q)
 {
     __shared__ SubsetSmem<G, RPL> sm;
-    slot_group<G, RPL>(g, t, s, q, blockIdx.x, blockIdx.y, blockIdx.z, 1, 1, sm);
+    slot_group<G, RPL>(g, t, s, q, blockIdx.x, blockIdx.y, blockIdx.z, 1, sm);
 }
 
 // Merge of one tidal/fixed KV-head's partials (static tiles, kept groups, new groups):
@@ -1216,23 +1222,25 @@ __global__ __launch_bounds__(COMBINE_THREADS) void subset_combine_kernel(Geometr
 {
     const int hi = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
     const bool tidal = hi < g.nT;
-    extern __shared__ float sfac[];      // [np][G]
+    extern __shared__ float sfac[];      // [np_max][G]
     constexpr int NW = COMBINE_THREADS / 64;
     constexpr int OG = COMBINE_THREADS / (G * D) > 0 ? COMBINE_THREADS / (G * D) : 1;   // groups per output
     __shared__ float red[NW * G];
     __shared__ float Linv[G];
     __shared__ float opart[OG > 1 ? OG : 1][G * D > COMBINE_THREADS ? 1 : G * D];
-    const int nk = tidal ? min((s.counts[b * 2] + g.sg - 1) / g.sg, g.ng_kept) : 0;
-    // one partial per new entry; none exist when complements are empty (100 % budget)
-    const int nn = (tidal && !g.next_step) ? min(s.counts[b * 2 + 1], g.np - g.n_tiles_s - g.ng_kept) : 0;
-    const int nvalid = g.n_tiles_s + nk + nn;
+    const HeadRows hr = t.hr[hi];
+    const bool recalls = tidal && hr.cfull > 0;   // no complement at retention 1
+    const int nk = recalls ? min((s.counts[b * 2] + hr.sg - 1) / hr.sg, hr.ngk) : 0;
+    // one partial per new entry (same-step timing)
+    const int nn = (recalls && !g.next_step) ? min(s.counts[b * 2 + 1], g.knew) : 0;
+    const int nts = hr.nts, ngk = hr.ngk, nvalid = nts + nk + nn;
     auto part = [&](int j) {
-        if (j < g.n_tiles_s) return j;
-        j -= g.n_tiles_s;
-        if (j < nk) return g.n_tiles_s + j;
-        return g.n_tiles_s + g.ng_kept + (j - nk);
+        if (j < nts) return j;
+        j -= nts;
+        if (j < nk) return nts + j;
+        return nts + ngk + (j - nk);
     };
-    const size_t base = ((size_t)b * (g.nT + g.nF) + hi) * g.np;
+    const size_t base = (size_t)b * g.P + hr.pbase;
     const int lane = tid & 63, wave = tid >> 6;
     float mloc[G];
 #pragma unroll
@@ -1372,7 +1380,7 @@ struct TidalFixedL {
                           bool with_static, hipStream_t st)
     {
         recall = recall && g.nT > 0 && g.k > 0 && g.comp_max > 0;
-        const long long n = (recall ? RECALL_WGS : 0) + (with_static ? (long long)g.n_tiles_s * (g.nT + g.nF) * g.B : 0) +
+        const long long n = (recall ? RECALL_WGS : 0) + (with_static ? (long long)g.n_static * g.B : 0) +
                             (long long)g.ng_kept * g.nT * g.B;
         if (n == 0) return hipSuccess;
         const dim3 grid((unsigned)n), block(NT);
@@ -1392,7 +1400,7 @@ struct AttentionL {
     static hipError_t run(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st,
                           hipEvent_t e0, hipEvent_t e1)
     {
-        const long long n = (long long)g.n_tiles_a * g.nA * g.B + (long long)g.n_tiles_s * (g.nT + g.nF) * g.B;
+        const long long n = (long long)g.n_tiles_a * g.nA * g.B + (long long)g.n_static * g.B;
         if (n == 0) return record_pair(e0, e1, st);
         hipExtLaunchKernelGGL(attention_kernel<G>, dim3((unsigned)n), dim3(NT), 0, st, e0, e1, 0, g, t, s, q);
         return hipGetLastError();
@@ -1415,7 +1423,7 @@ struct CombineL {
     static hipError_t run(const Geometry &g, const Tiers &t, const StepBuffers &s, float *out, hipStream_t st)
     {
         if (g.nT + g.nF == 0) return hipSuccess;
-        const size_t shm = (size_t)(g.np ? g.np : 1) * G * sizeof(float);
+        const size_t shm = (size_t)(g.np_max ? g.np_max : 1) * G * sizeof(float);
         hipLaunchKernelGGL(subset_combine_kernel<G>, dim3(g.nT + g.nF, g.B), dim3(COMBINE_THREADS), shm, st, g, t, s, out);
         return hipGetLastError();
     }

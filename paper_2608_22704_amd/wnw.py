@@ -10,6 +10,8 @@ from __future__ import annotations
 import ctypes as C
 import os
 
+import numpy as np
+
 PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libwnw.so")
 
@@ -17,8 +19,8 @@ WNW_OK, WNW_ERR_INVALID, WNW_ERR_OOM, WNW_ERR_HIP, WNW_ERR_STATE, WNW_ERR_UNSUPP
 WNW_ANCHOR, WNW_TIDAL, WNW_FIXED = 0, 1, 2
 WNW_F_SELECT_NEXT_STEP, WNW_F_RECALL_MEMCPY, WNW_F_TIMING, WNW_F_OVERLAP_CHUNKS = 1, 2, 4, 8
 
-EXPORTS = ("wnw_init_cache", "wnw_set_roles", "wnw_decode_step", "wnw_query_geometry", "wnw_query_segments",
-           "wnw_get_stats",
+EXPORTS = ("wnw_init_cache", "wnw_set_retention", "wnw_set_roles", "wnw_decode_step", "wnw_query_geometry",
+           "wnw_query_segments", "wnw_query_head_keep", "wnw_get_stats",
            "wnw_set_selection_override", "wnw_debug_read_slot", "wnw_debug_read_host_chunk",
            "wnw_debug_read_resident", "wnw_last_error", "wnw_destroy")
 
@@ -58,6 +60,8 @@ def _load():
     sig = {
         "wnw_init_cache": ([C.POINTER(wnw_config), P, P, P, C.POINTER(P)], C.c_int),
         "wnw_set_roles": ([P, P, P], C.c_int),
+        "wnw_set_retention": ([P, P, C.c_float], C.c_int),
+        "wnw_query_head_keep": ([P, P], C.c_int),
         "wnw_decode_step": ([P, P, P, P, P, P], C.c_int),
         "wnw_query_geometry": ([P, C.POINTER(I32), C.POINTER(I32), C.POINTER(I32), C.POINTER(I32), C.POINTER(I64)], C.c_int),
         "wnw_query_segments": ([P, C.POINTER(I32)], C.c_int),
@@ -109,8 +113,20 @@ def wnw_init_cache(cfg: wnw_config, k_dev, v_dev, stream=None):
     return h
 
 
+def wnw_set_retention(ctx, importance, lam):
+    """importance: host fp32 [L][H_kv] (or None for the uniform budget); lam: the scale."""
+    imp = None if importance is None else np.ascontiguousarray(importance, dtype=np.float32)
+    _check(lib.wnw_set_retention(ctx, _ptr(imp), float(lam)), ctx)
+
+
 def wnw_set_roles(ctx, roles, prefill_scores):
     _check(lib.wnw_set_roles(ctx, _ptr(roles), _ptr(prefill_scores)), ctx)
+
+
+def wnw_query_head_keep(ctx, layers, kv_heads) -> np.ndarray:
+    keep = np.empty((layers, kv_heads), dtype=np.int32)
+    _check(lib.wnw_query_head_keep(ctx, _ptr(keep)), ctx)
+    return keep
 
 
 def wnw_decode_step(ctx, q_dev, out_dev, chunk_scores_dev=None, selected_dev=None, stream=None):

@@ -34,7 +34,7 @@ import numpy as np
 
 from .configs import Workload
 
-TAG_K, TAG_V, TAG_Z, TAG_DRIFT, TAG_ROLES, TAG_PREFILL = 1, 2, 3, 4, 5, 6
+TAG_K, TAG_V, TAG_Z, TAG_DRIFT, TAG_ROLES, TAG_PREFILL, TAG_IMPORTANCE = 1, 2, 3, 4, 5, 6, 7
 ANCHOR, TIDAL, FIXED = 0, 1, 2
 
 
@@ -117,6 +117,12 @@ def head_queries(w: Workload, b: int, l: int, kv: int, k_bf16: np.ndarray, drift
 
 def prefill_scores(w: Workload, b: int, l: int, kv: int) -> np.ndarray:
     return _rng(seq_seed(w, b), TAG_PREFILL, l, kv).random(w.audio_len, dtype=np.float32)
+
+
+def importance(w: Workload) -> np.ndarray:
+    """Normalised per-head importance [L][H_kv] fp32, U(0, 1), shared by the batch (the input of
+    the per-head retention schedule; calibration, which would produce it, is not modelled)."""
+    return _rng(seed_base(w), TAG_IMPORTANCE).random((w.layers, w.kv_heads), dtype=np.float32)
 
 
 def _head_job(w, b, l, kv, dpos):

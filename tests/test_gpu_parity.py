@@ -446,3 +446,108 @@ def test_overlap_slots_over_steps(nxt):
         assert st["revived_chunks"] > 0
     finally:
         h.close()
+
+
+# ---- per-head retention (Eq. 1): retention = min(importance * lambda, 1) per tidal/fixed head;
+# static tiers, complements and slots are ragged by head.
+
+def _imp(w, seed, zeros=(), ones=()):
+    rng = np.random.default_rng(seed)
+    imp = rng.random((w.layers, w.kv_heads), dtype=np.float32)
+    for lh in zeros:
+        imp[lh] = 0.0
+    for lh in ones:
+        imp[lh] = 1.0
+    return imp
+
+
+RET = [
+    (_small("ret_mixed", 301, L=2, Hq=8, Hkv=4, Ta=300, cl=32), 1.0, ((0, 1),), ((1, 2),)),
+    (_small("ret_g8_chunk256", 302, Hq=16, Hkv=2, L=3, cl=256, Ta=1300, Tt=300), 1.0, ((1, 0),), ()),
+    (_small("ret_g1_chunk7", 303, Hq=4, Hkv=4, cl=7), 0.6, (), ((0, 3),)),
+    (_small("ret_chunk1", 304, Hq=8, Hkv=2, L=3, cl=1, Ta=97), 1.0, (), ()),
+    (_small("ret_scale_up", 305, L=2, Hq=12, Hkv=4, Ta=517, cl=50, Tt=3), 2.5, (), ()),
+    (_small("ret_batch3", 306, B=3, Ta=777, Tt=1, cl=37, steps=9), 0.4, ((0, 0), (1, 1)), ()),
+]
+
+
+def _ret_run(w, lam, zeros, ones, seed, **kw):
+    return _run(w, importance=_imp(w, seed, zeros, ones), lam=lam, **kw)
+
+
+@pytest.mark.parametrize("case", RET, ids=[c[0].name for c in RET])
+def test_retention_edge_shapes(case):
+    w, lam, zeros, ones = case
+    _ret_run(w, lam, zeros, ones, w.seed_id)
+
+
+@pytest.mark.parametrize("case", RET, ids=[c[0].name for c in RET])
+def test_retention_next_step_edge_shapes(case):
+    w, lam, zeros, ones = case
+    _ret_run(w, lam, zeros, ones, w.seed_id, flags=_next())
+
+
+def test_retention_overlap_and_memcpy():
+    from paper_2608_22704_amd import wnw as W
+    w = _small("ret_ovl", 307, L=2, Hq=8, Hkv=4, Ta=480, Tt=5, cl=32, steps=10)
+    _ret_run(w, 0.7, ((0, 1),), ((1, 1),), 307, flags=_ovl(_next()))
+    _ret_run(w, 0.7, ((0, 1),), ((1, 1),), 307, flags=_ovl(W.WNW_F_RECALL_MEMCPY))
+    _ret_run(w, 0.7, ((0, 1),), ((1, 1),), 307, flags=_next(W.WNW_F_RECALL_MEMCPY))
+
+
+def test_retention_all_heads_full_and_all_empty():
+    """Retention 1 everywhere: no complement, nothing recalled, every head is plain attention.
+    Retention 0 everywhere: tidal heads see text + resident chunks, fixed heads text only."""
+    w = _small("ret_extremes", 308, L=2, Hq=8, Hkv=4, Ta=300, cl=32, steps=4)
+    h = _run(w, importance=np.ones((2, 4), np.float32), lam=1.0)
+    assert h.geo["keep_total"] == -1 and (h.head_keep == w.audio_len).all()
+    _run(w, importance=np.ones((2, 4), np.float32), lam=0.0, flags=_next())
+
+
+def test_retention_qwen_shaped_all_steps():
+    _run(configs.QWEN_10MIN, importance=gen.importance(configs.QWEN_10MIN), lam=0.4, flags=_next())
+
+
+def test_retention_voxtral_shaped_sampled_heads():
+    w = configs.VOXTRAL_10MIN.with_(steps=48)
+    _run(w, head_mask_fn=_sampled(16), importance=gen.importance(w), lam=0.4, flags=_next())
+
+
+def test_retention_recall_bytes_ragged_layout():
+    """Per segment block: every tidal head in role order, its complement K rows then V rows with
+    that head's own row count (padding zero); device slot = host block = the cache's rows."""
+    from tests.wnw_harness import Lockstep, log
+    w = _small("ret_bytes", 309, L=2, Hq=8, Hkv=4, Ta=300, Tt=5, cl=32, steps=2)
+    log("[case] ragged recall bytes")
+    h = Lockstep(w, importance=_imp(w, 309, ((0, 1),), ((1, 2),)), lam=1.0)
+    try:
+        _, _, sel, res = h.gpu_step(0)
+        W = h.W
+        nbytes = h.geo["chunk_bytes"]
+        kd, vd = h.ok_[0], h.ov_[0]
+        tidal = [(l, kv) for l in range(w.layers) for kv in range(w.kv_heads) if h.roles[l, kv] == 1]
+        segs = [(c0, min(c0 + w.chunk_len, w.audio_len)) for c0 in range(0, w.audio_len, w.chunk_len)]
+        comps = []
+        for l, kv in tidal:
+            keep = h.oracle.keep_mask(0, l, kv)
+            comps.append(max(sum(1 for t in range(a, e) if not keep[t]) for a, e in segs))
+        assert nbytes == 2 * 128 * 2 * sum(comps)
+        for c in np.nonzero(res[0])[0]:
+            dev = np.empty(nbytes // 2, dtype=np.uint16)
+            hst = np.empty(nbytes // 2, dtype=np.uint16)
+            W.wnw_debug_read_slot(h.ctx, 0, int(c), dev, nbytes)
+            W.wnw_debug_read_host_chunk(h.ctx, 0, int(c), hst, nbytes)
+            assert np.array_equal(dev, hst)
+            off = 0
+            for (l, kv), cm in zip(tidal, comps):
+                blk = dev[off * 128:(off + 2 * cm) * 128].reshape(2, cm, 128)
+                off += 2 * cm
+                keep = h.oracle.keep_mask(0, l, kv)
+                a, e = segs[int(c)]
+                rows = [t for t in range(a, e) if not keep[t]]
+                assert np.array_equal(blk[0, : len(rows)], kd[l, kv, rows])
+                assert np.array_equal(blk[1, : len(rows)], vd[l, kv, rows])
+                assert not blk[:, len(rows):].any()
+            assert off * 128 * 2 == nbytes
+    finally:
+        h.close()

@@ -61,7 +61,7 @@ class Lockstep:
     """One workload, a subset `seqs` of its sequences checked against the oracle (the GPU runs
     all w.batch sequences)."""
 
-    def __init__(self, w, flags: int = 0, seqs=None, budget_bp=None, data=None, top_k=0):
+    def __init__(self, w, flags: int = 0, seqs=None, budget_bp=None, data=None, top_k=0, importance=None, lam=None):
         import torch
         from paper_2608_22704_amd import wnw as W
         self.W, self.torch = W, torch
@@ -93,6 +93,8 @@ class Lockstep:
         self.cfg = W.make_config(B, L, w.q_heads, H, w.audio_len, w.text_len, w.chunk_len, w.budget_bp,
                                  top_k=top_k, flags=flags)
         self.ctx = W.wnw_init_cache(self.cfg, kd, vd)
+        if importance is not None:
+            W.wnw_set_retention(self.ctx, importance, lam)
         W.wnw_set_roles(self.ctx, self.roles, self.prefill)
         del kd, vd
         torch.cuda.empty_cache()
@@ -103,9 +105,14 @@ class Lockstep:
                                    chunk_span=span)
         self.ok_ = np.stack([host[b]["k"] for b in self.seqs])
         self.ov_ = np.stack([host[b]["v"] for b in self.seqs])
-        self.oracle = O.Oracle(ocfg, self.ok_, self.ov_, self.roles, self.prefill[self.seqs])
-        assert (self.oracle.n_chunks, self.oracle.k, self.oracle.keep_total) == \
-            (self.geo["n_chunks"], self.geo["k"], self.geo["keep_total"])
+        self.oracle = O.Oracle(ocfg, self.ok_, self.ov_, self.roles, self.prefill[self.seqs], importance=importance,
+                               lam=lam)
+        assert (self.oracle.n_chunks, self.oracle.k) == (self.geo["n_chunks"], self.geo["k"])
+        assert self.geo["keep_total"] == (self.oracle.keep_total if importance is None else -1)
+        # kept audio rows of every head against the oracle's keep sets
+        self.head_keep = W.wnw_query_head_keep(self.ctx, L, H)
+        okeep = np.array([[self.oracle.keep_mask(0, l, h).sum() for h in range(H)] for l in range(L)])
+        assert np.array_equal(self.head_keep, okeep), "per-head keep counts differ from the oracle"
         assert self.oracle.n_segments == self.geo["n_segments"]
         self.k, self.nc, self.nseg = self.geo["k"], self.geo["n_chunks"], self.geo["n_segments"]
         self.out = torch.empty((B, L, w.q_heads, D), dtype=torch.float32, device="cuda")
