@@ -78,7 +78,7 @@ def overlap_sweep(W, torch, w, ctx, geo, qd, out, sc, sel, stream, args, ms_no_r
     return res
 
 
-def run_timing(W, torch, w, timing, recall, kd, vd, qd, roles, prefill, args, chunks="disjoint"):
+def run_timing(W, torch, w, timing, recall, kd, vd, qd, roles, prefill, args, chunks="disjoint", retention="uniform"):
     """Set up one context with the given selection timing and recall path, run the warm-up and
     the timed steps, then a second region with the selection pinned (no recall).  Returns the
     context-independent numbers; the context is destroyed."""
@@ -90,12 +90,15 @@ def run_timing(W, torch, w, timing, recall, kd, vd, qd, roles, prefill, args, ch
     stream = torch.cuda.current_stream()
     ctx = W.wnw_init_cache(cfg, kd, vd, stream)
     try:
+        if retention == "per-head":
+            from synth import gen
+            W.wnw_set_retention(ctx, gen.importance(w), args.lam)
         W.wnw_set_roles(ctx, roles, prefill)
         geo = W.wnw_query_geometry(ctx)
         out = torch.empty((B, L, w.q_heads, D), dtype=torch.float32, device="cuda")
         sc = torch.empty((B, geo["n_chunks"]), dtype=torch.float32, device="cuda")
         sel = torch.empty((B, max(geo["k"], 1)), dtype=torch.int32, device="cuda")
-        log(f"[bench] {timing}-step timing, {recall} recall, {chunks} chunks: set-up done {geo}")
+        log(f"[bench] {timing}-step timing, {recall} recall, {chunks} chunks, {retention} retention: set-up done {geo}")
         if args.calibrate_copy:
             src = torch.ones(128 << 20, dtype=torch.int16, device="cuda")
             dst = torch.empty_like(src)
@@ -140,6 +143,7 @@ def run_timing(W, torch, w, timing, recall, kd, vd, qd, roles, prefill, args, ch
     d = {k: st1[k] - st0[k] for k in st1 if isinstance(st1[k], (int, float))}
     d2 = {k: st3[k] - st2[k] for k in st3 if isinstance(st3[k], (int, float))}
     r = {"value": K / t_el, "ms_per_step": t_el * 1e3 / K, "geo": geo, "st1": st1, "sweep": sweep,
+         "r_gpu": st1["r_gpu"], "r_gpu_cpu": st1["r_gpu_cpu"],
          "recall": {"copied_chunks_per_step": d["recalled_chunks"] / K / B,
                     "revived_chunks_per_step": d["revived_chunks"] / K / B,
                     "MB_per_step": d["recalled_bytes"] / K / 1e6, "chunk_MB": geo.get("chunk_bytes", 0) / 1e6,
@@ -192,6 +196,11 @@ def main():
                     help="chunk structure of the headline run: disjoint chunks of chunk_len positions, or chunks of "
                          "two chunk_len/2 segments starting at every segment")
     ap.add_argument("--no-other-chunks", action="store_true", help="skip the run with the other chunk structure")
+    ap.add_argument("--retention", choices=("uniform", "per-head"), default="uniform",
+                    help="audio retention of the headline run: the workload's uniform budget, or min(importance * "
+                         "lambda, 1) per head with seeded U(0,1) importance")
+    ap.add_argument("--lam", type=float, default=0.4, help="lambda of the per-head retention (0.4: mean 20 %%)")
+    ap.add_argument("--no-other-retention", action="store_true", help="skip the run with the other retention")
     ap.add_argument("--no-sweep", dest="sweep", action="store_false",
                     help="skip the overlap sweep (forced 1..24 newly resident chunks per step)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU oracle sample (0 = skip)")
@@ -228,16 +237,23 @@ def main():
     torch.cuda.synchronize()
     log(f"[bench] inputs resident in HBM after {time.time() - t0:.1f}s")
 
-    main_run = run_timing(W, torch, w, args.timing, args.recall, kd, vd, qd, roles, prefill, args, args.chunks)
+    main_run = run_timing(W, torch, w, args.timing, args.recall, kd, vd, qd, roles, prefill, args, args.chunks,
+                          args.retention)
     other = other_ch = None
     args_other = argparse.Namespace(**{**vars(args), "calibrate_copy": False, "sweep": False})
     if not args.no_other_timing:
         other_timing = "same" if args.timing == "next" else "next"
-        other = run_timing(W, torch, w, other_timing, args.recall, kd, vd, qd, roles, prefill, args_other, args.chunks)
+        other = run_timing(W, torch, w, other_timing, args.recall, kd, vd, qd, roles, prefill, args_other, args.chunks,
+                           args.retention)
     other_chunks = "overlap" if args.chunks == "disjoint" else "disjoint"
     if not args.no_other_chunks:
         other_ch = run_timing(W, torch, w, args.timing, args.recall, kd, vd, qd, roles, prefill, args_other,
-                              other_chunks)
+                              other_chunks, args.retention)
+    other_retention = "per-head" if args.retention == "uniform" else "uniform"
+    other_ret = None
+    if not args.no_other_retention:
+        other_ret = run_timing(W, torch, w, args.timing, args.recall, kd, vd, qd, roles, prefill, args_other,
+                               args.chunks, other_retention)
     del kd, vd
     torch.cuda.empty_cache()
 
@@ -250,7 +266,8 @@ def main():
         "config": {"workload": w.name, "batch": B, "layers": L, "q_heads": w.q_heads, "kv_heads": H,
                    "head_dim": D, "audio_len": w.audio_len, "text_len": w.text_len, "chunk_len": w.chunk_len,
                    "budget_bp": w.budget_bp, "roles": [w.n_anchor, w.n_tidal, w.n_fixed], "kv_storage": "bf16",
-                   "selection_timing": args.timing, "recall": args.recall, "chunks": args.chunks},
+                   "selection_timing": args.timing, "recall": args.recall, "chunks": args.chunks,
+                   "retention": args.retention if args.retention == "uniform" else f"per-head, lambda {args.lam}"},
     }
     if "kernels" in main_run:
         k = main_run["kernels"]
@@ -285,6 +302,14 @@ def main():
         if "kernels" in other_ch:
             o["kernels"] = other_ch["kernels"]
         res["other_chunks"] = o
+    if other_ret is not None:
+        o = {"retention": other_retention if other_retention == "uniform" else f"per-head, lambda {args.lam}",
+             "chunks": args.chunks, "selection_timing": args.timing, "value": other_ret["value"], "unit": "steps/s",
+             "ms_per_step": other_ret["ms_per_step"], "r_gpu": other_ret["r_gpu"], "r_gpu_cpu": other_ret["r_gpu_cpu"],
+             "recall": other_ret["recall"]}
+        if "kernels" in other_ret:
+            o["kernels"] = other_ret["kernels"]
+        res["other_retention"] = o
 
     if args.cpu_seconds > 0:
         res["cpu_baseline"] = cpu_baseline(w, roles, prefill, args.cpu_seconds)
