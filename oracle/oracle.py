@@ -30,7 +30,7 @@ def build(verbose: bool = False) -> str:
 class _Cfg(C.Structure):
     _fields_ = [(n, C.c_int32) for n in (
         "batch", "layers", "q_heads", "kv_heads", "head_dim", "audio_len", "text_len",
-        "chunk_len", "budget_bp", "top_k", "evict_lag", "next_step", "chunk_span")]
+        "chunk_len", "budget_bp", "top_k", "evict_lag", "next_step", "chunk_span", "prefill_global")]
 
 
 _lib = None
@@ -57,6 +57,7 @@ def lib():
         L.wnwo_tokens_for_window.argtypes = [C.c_double, C.c_double]
         L.wnwo_tokens_for_window.restype = C.c_int32
         L.wnwo_segments.argtypes = [C.POINTER(_Cfg), C.POINTER(C.c_int32)]
+        L.wnwo_prefill_scores.argtypes = [C.POINTER(_Cfg), P, P, P]
         L.wnwo_set_threads.argtypes = [C.c_int]
         L.wnwo_set_threads.restype = C.c_int
         _lib = L
@@ -68,9 +69,9 @@ def _ptr(a):
 
 
 def make_cfg(batch, layers, q_heads, kv_heads, head_dim, audio_len, text_len, chunk_len,
-             budget_bp, top_k=0, evict_lag=0, next_step=0, chunk_span=1) -> _Cfg:
+             budget_bp, top_k=0, evict_lag=0, next_step=0, chunk_span=1, prefill_global=0) -> _Cfg:
     return _Cfg(batch, layers, q_heads, kv_heads, head_dim, audio_len, text_len, chunk_len,
-                budget_bp, top_k, evict_lag, next_step, chunk_span)
+                budget_bp, top_k, evict_lag, next_step, chunk_span, prefill_global)
 
 
 def cfg_from_workload(w, batch=None, **over) -> _Cfg:
@@ -105,6 +106,18 @@ def topk(scores: np.ndarray, k: int) -> np.ndarray:
 
 def tokens_for_window(seconds: float, rate: float) -> int:
     return lib().wnwo_tokens_for_window(seconds, rate)
+
+
+def prefill_scores(cfg: _Cfg, k, q_text) -> np.ndarray:
+    """Text-to-audio attention sums [B][L][H_kv][T_a] (double) of Prefill Compression."""
+    k = np.ascontiguousarray(k, dtype=np.uint16)
+    q = np.ascontiguousarray(q_text, dtype=np.uint16)
+    B, L, H, Hq, Ta, Tt, D = cfg.batch, cfg.layers, cfg.kv_heads, cfg.q_heads, cfg.audio_len, cfg.text_len, cfg.head_dim
+    assert k.shape == (B, L, H, Ta + Tt, D) and q.shape == (B, L, Hq, Tt, D)
+    p = np.empty((B, L, H, Ta), dtype=np.float64)
+    if lib().wnwo_prefill_scores(C.byref(cfg), _ptr(k), _ptr(q), _ptr(p)):
+        raise ValueError("wnwo_prefill_scores failed")
+    return p
 
 
 def set_threads(n: int) -> int:

@@ -159,6 +159,16 @@ static void prefill_keep(const wnwo_config *c, const float *importance, float la
 {
     memset(keep, 0, (size_t)c->audio_len);
     int32_t ns = seg_count(c);
+    if (c->prefill_global) {
+        /* Global variant (ablation of per-segment selection): the same number of positions,
+         * the sum of the per-segment counts, ranked over the whole audio of the head. */
+        int32_t total = 0;
+        for (int32_t j = 0; j < ns; ++j) total += keep_count_head(c, importance, lambda, h, seg_end(c, j) - seg_begin(c, j));
+        for (int32_t i = 0; i < c->audio_len; ++i) { tmp[i].s = score[i]; tmp[i].pos = i; }
+        qsort(tmp, (size_t)c->audio_len, sizeof *tmp, by_score_then_pos);
+        for (int32_t i = 0; i < total; ++i) keep[tmp[i].pos] = 1;
+        return;
+    }
     for (int32_t j = 0; j < ns; ++j) {
         int32_t b0 = seg_begin(c, j), e0 = seg_end(c, j), n = e0 - b0;
         for (int32_t i = 0; i < n; ++i) { tmp[i].s = score[b0 + i]; tmp[i].pos = b0 + i; }
@@ -204,7 +214,7 @@ wnwo *wnwo_create_retention(const wnwo_config *cfg, const uint16_t *k, const uin
     o->keep = malloc(B * nh * (size_t)(cfg->audio_len ? cfg->audio_len : 1));
     o->streak = malloc(B * (size_t)(nc ? nc : 1) * sizeof(int32_t));
     o->res_prev = calloc(B * (size_t)(o->n_seg ? o->n_seg : 1), 1);
-    ranked *tmp = malloc((size_t)(cfg->chunk_len) * sizeof *tmp);
+    ranked *tmp = malloc((size_t)(cfg->prefill_global ? (cfg->audio_len ? cfg->audio_len : 1) : cfg->chunk_len) * sizeof *tmp);
     if (!o->roles || !o->keep || !o->streak || !o->res_prev || !tmp) {
         free(tmp);
         wnwo_destroy(o);
@@ -303,6 +313,38 @@ static void attend(const uint16_t *q, const uint16_t *K, const uint16_t *V, cons
         for (int32_t j = 0; j < d; ++j) out[j] += pi * bf16(vr[j]);
         if (p) p[i] = pi;
     }
+}
+
+/* ---- prefill scores (Method, "Prefill Compression") ------------------------------------------- */
+
+/* p[b][l][kv][tau] = sum over the text tokens t and over the q-heads of KV-head kv of the
+ * softmax weight that text token t puts on audio position tau.  Text token t (row T_a + t)
+ * attends causally: to every audio row and to text rows up to its own. */
+int wnwo_prefill_scores(const wnwo_config *c, const uint16_t *k, const uint16_t *q_text, double *p)
+{
+    if (!c || !k || !p || (c->text_len && !q_text) || wnwo_geometry(c, NULL, NULL, NULL)) return -1;
+    const int32_t B = c->batch, L = c->layers, H = c->kv_heads, Hq = c->q_heads, g = Hq / H, D = c->head_dim;
+    const int32_t Ta = c->audio_len, Tt = c->text_len, T = Ta + Tt;
+    const int64_t n = (int64_t)B * L * H;
+#pragma omp parallel for schedule(dynamic)
+    for (int64_t i = 0; i < n; ++i) {
+        const int32_t b = (int32_t)(i / ((int64_t)L * H)), l = (int32_t)(i / H % L), kv = (int32_t)(i % H);
+        const uint16_t *K = k + (size_t)i * T * D;
+        double *ph = p + (size_t)i * Ta;
+        double *x = malloc((size_t)(T ? T : 1) * sizeof(double));
+        int32_t *rows = malloc((size_t)(T ? T : 1) * sizeof(int32_t));
+        double *o = malloc((size_t)D * sizeof(double)), *w = malloc((size_t)(T ? T : 1) * sizeof(double));
+        for (int32_t r = 0; r < T; ++r) rows[r] = r;
+        for (int32_t t = 0; t < Ta; ++t) ph[t] = 0.0;
+        for (int32_t j = 0; j < g; ++j)
+            for (int32_t t = 0; t < Tt; ++t) {
+                const uint16_t *qv = q_text + ((((size_t)b * L + l) * Hq + (size_t)kv * g + j) * Tt + t) * D;
+                attend(qv, K, K, rows, Ta + t + 1, D, x, o, w);
+                for (int32_t tau = 0; tau < Ta; ++tau) ph[tau] += w[tau];
+            }
+        free(x); free(rows); free(o); free(w);
+    }
+    return 0;
 }
 
 /* ---- one decode step -------------------------------------------------------------------------- */

@@ -30,6 +30,8 @@ typedef struct {
     int32_t chunk_span;            /* segments per chunk: 0 or 1 disjoint chunks (one segment
                                       each); 2 the paper's chunks of two consecutive segments
                                       of chunk_len / 2 positions, one chunk per segment start  */
+    int32_t prefill_global;        /* 1: prefill keeps the same number of positions, ranked over
+                                      the whole audio of a head instead of per segment          */
 } wnwo_config;
 
 typedef struct wnwo wnwo;
@@ -55,6 +57,13 @@ void wnwo_destroy(wnwo *o);
 
 /* Audio positions kept at prefill by head (b, l, kv): mask[T_a] of 0/1 (all 1 for anchors). */
 int wnwo_keep_mask(const wnwo *o, int32_t b, int32_t l, int32_t kv, uint8_t *mask);
+
+/* Prefill scores of Prefill Compression: p [B][L][H_kv][T_a] (double) = the attention weight
+ * that the text tokens put on each audio position, summed over the text tokens and over the
+ * q-heads of the KV-head; text token t attends to every audio row and to text rows 0..t.
+ *   k       [B][L][H_kv][T_a+T_t][d] bf16
+ *   q_text  [B][L][H_q][T_t][d] bf16, the text tokens' queries at prefill */
+int wnwo_prefill_scores(const wnwo_config *cfg, const uint16_t *k, const uint16_t *q_text, double *p);
 
 /* One decode step.
  *   q         [B][L][H_q][d] bf16

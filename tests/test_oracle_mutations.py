@@ -45,6 +45,14 @@ MUTANTS = {
     "per-head keep count rounds to nearest": (
         "return (int32_t)floor(r * (double)len);", "return (int32_t)floor(r * (double)len + 0.5);"),
     "per-head retention ignored": ("if (!importance) return keep_count(c, len);", "return keep_count(c, len);"),
+    "prefill text tokens see every text row": (
+        "attend(qv, K, K, rows, Ta + t + 1, D, x, o, w);", "attend(qv, K, K, rows, T, D, x, o, w);"),
+    "prefill scores from the first q-head only": (
+        "        for (int32_t j = 0; j < g; ++j)\n            for (int32_t t = 0; t < Tt; ++t) {",
+        "        for (int32_t j = 0; j < 1; ++j)\n            for (int32_t t = 0; t < Tt; ++t) {"),
+    "global prefill keeps the last segment's count": (
+        "for (int32_t j = 0; j < ns; ++j) total += keep_count_head(",
+        "for (int32_t j = 0; j < ns; ++j) total = keep_count_head("),
 }
 
 

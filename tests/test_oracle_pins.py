@@ -468,3 +468,74 @@ def test_retention_invalid_inputs_rejected(oracle_mod):
                      (np.full((1, 3), 0.5), np.inf), (np.full((1, 3), 0.5), np.nan)):
         with pytest.raises(ValueError):
             oracle_mod.Oracle(cfg, k, v, roles, pf, importance=imp.astype(np.float32), lam=lam)
+
+
+# ---- prefill compression: text-to-audio attention sums and the global top-k variant
+
+def _prefill_case(oracle_mod, seed, B=2, L=2, H=2, g=2, D=16, Ta=29, Tt=6, scale=1.0):
+    rng = np.random.default_rng(seed)
+    k, _ = _rand_cache(rng, B, L, H, Ta + Tt, D, scale=scale)
+    q = f32_to_bf16(rng.standard_normal((B, L, H * g, Tt, D)).astype(np.float32) * scale)
+    cfg = oracle_mod.make_cfg(B, L, H * g, H, D, Ta, Tt, 8, 2000)
+    return cfg, k, q
+
+
+def test_prefill_scores_equal_library_causal_attention(oracle_mod):
+    """p equals causal SDPA (double) of the text queries over all rows with V = one-hot audio
+    indicators, summed over the text tokens and the q-heads of each KV-head."""
+    cfg, k, q = _prefill_case(oracle_mod, 51, scale=2.0)
+    p = oracle_mod.prefill_scores(cfg, k, q)
+    B, L, H, Ta, Tt, g = cfg.batch, cfg.layers, cfg.kv_heads, cfg.audio_len, cfg.text_len, cfg.q_heads // cfg.kv_heads
+    T = Ta + Tt
+    onehot = np.zeros((T, Ta))
+    onehot[np.arange(Ta), np.arange(Ta)] = 1.0
+    mask = np.zeros((Tt, T), dtype=bool)
+    for t in range(Tt):
+        mask[t, : Ta + t + 1] = True
+    f = lambda a: torch.from_numpy(bf16_to_f32(a).astype(np.float64))
+    for b, l, kv in itertools.product(range(B), range(L), range(H)):
+        ref = np.zeros(Ta)
+        for j in range(g):
+            o = torch.nn.functional.scaled_dot_product_attention(
+                f(q[b, l, kv * g + j])[None], f(k[b, l, kv])[None], torch.from_numpy(onehot)[None],
+                attn_mask=torch.from_numpy(mask)[None])[0].numpy()
+            ref += o.sum(axis=0)
+        np.testing.assert_allclose(p[b, l, kv], ref, rtol=0, atol=1e-12)
+
+
+def test_prefill_scores_zero_queries_closed_form(oracle_mod):
+    """q = 0: text token t spreads its weight evenly over its T_a + t + 1 keys, so every audio
+    position gets g * sum_t 1 / (T_a + t + 1); no text gives p = 0."""
+    cfg, k, q = _prefill_case(oracle_mod, 53)
+    q[:] = 0
+    p = oracle_mod.prefill_scores(cfg, k, q)
+    g, Ta, Tt = cfg.q_heads // cfg.kv_heads, cfg.audio_len, cfg.text_len
+    np.testing.assert_allclose(p, g * sum(1.0 / (Ta + t + 1) for t in range(Tt)), rtol=1e-14, atol=0)
+    cfg0 = oracle_mod.make_cfg(1, 1, 2, 1, 16, 10, 0, 4, 2000)
+    k0 = f32_to_bf16(np.random.default_rng(1).standard_normal((1, 1, 1, 10, 16)).astype(np.float32))
+    assert not oracle_mod.prefill_scores(cfg0, k0, np.zeros((1, 1, 2, 0, 16), np.uint16)).any()
+
+
+def test_prefill_global_keep_is_brute_force_top(oracle_mod):
+    """Global variant: the per-segment total of floor(retention * len) positions, the best over
+    the whole audio by (score desc, position asc); with one segment it equals per-segment
+    selection."""
+    rng = np.random.default_rng(55)
+    B, L, H, D, Ta, Tt, cl, budget = 2, 1, 3, 8, 70, 2, 16, 3000
+    k, v = _rand_cache(rng, B, L, H, Ta + Tt, D)
+    pf = (rng.integers(0, 6, size=(B, L, H, Ta)) / 6.0).astype(np.float32)   # ties
+    roles = np.array([[0, 1, 2]], dtype=np.uint8)
+    o = oracle_mod.Oracle(oracle_mod.make_cfg(B, L, H, H, D, Ta, Tt, cl, budget, prefill_global=1), k, v, roles, pf)
+    total = sum((budget * (min(c0 + cl, Ta) - c0)) // 10000 for c0 in range(0, Ta, cl))
+    for b, h in itertools.product(range(B), range(1, H)):
+        order = sorted(range(Ta), key=lambda t: (-float(pf[b, 0, h, t]), t))
+        want = np.zeros(Ta, dtype=np.uint8)
+        want[order[:total]] = 1
+        assert np.array_equal(o.keep_mask(b, 0, h), want)
+    one = dict(B=1, L=1, H=3, D=8, Ta=14, Tt=2, cl=16)
+    k1, v1 = _rand_cache(rng, 1, 1, 3, 16, 8)
+    pf1 = rng.random((1, 1, 3, 14), dtype=np.float32)
+    a = oracle_mod.Oracle(oracle_mod.make_cfg(1, 1, 3, 3, 8, 14, 2, 16, 4000, prefill_global=1), k1, v1, roles, pf1)
+    s = oracle_mod.Oracle(oracle_mod.make_cfg(1, 1, 3, 3, 8, 14, 2, 16, 4000), k1, v1, roles, pf1)
+    for h in range(3):
+        assert np.array_equal(a.keep_mask(0, 0, h), s.keep_mask(0, 0, h))
