@@ -168,6 +168,25 @@ wnw_status wnw_set_retention(wnw_ctx *ctx, const float *importance, float lambda
  * complement, then waits for the copies.  Exactly once per context, after wnw_init_cache. */
 wnw_status wnw_set_roles(wnw_ctx *ctx, const uint8_t *roles, const float *prefill_scores);
 
+/* Prefill scores of Prefill Compression, on the device: p [B][L][H_kv][T_a] fp32, for every
+ * KV-head, the softmax weight that the text tokens put on each audio position, summed over the
+ * text tokens and over the g q-heads of the KV-head.  Text token t (cache row T_a + t) attends
+ * to every audio row and to text rows 0..t; logit scale 1 / sqrt(d); bf16 products summed in
+ * fp32.
+ *   q_text_dev  device bf16 [B][L][H_q][T_t][d]: the text tokens' queries at prefill (may be
+ *               NULL when T_t = 0, then p = 0)
+ *   scores_dev  device fp32 [B][L][H_kv][T_a], written
+ * Reads the full cache given to wnw_init_cache, so only before wnw_set_roles / _device
+ * (WNW_ERR_STATE after).  Runs on the stream given to wnw_init_cache and waits for it; uses a
+ * temporary device buffer of B * L * H_q * T_t * 8 bytes. */
+wnw_status wnw_prefill_scores(wnw_ctx *ctx, const void *q_text_dev, float *scores_dev);
+
+/* As wnw_set_roles, with the prefill scores in device memory (e.g. from wnw_prefill_scores):
+ * the per-segment ranking (same rule and ties) runs on the device and the tiers are built from
+ * its keep flags.  The same scores give the same tiers as wnw_set_roles.  On failure (or a
+ * failure of wnw_set_roles) the context is in the error state and can only be destroyed. */
+wnw_status wnw_set_roles_device(wnw_ctx *ctx, const uint8_t *roles, const float *prefill_scores_dev);
+
 /* One decode step (Eq. 2 and "Dynamic Chunk Selection"), enqueued on hip_stream (with
  * WNW_F_SELECT_NEXT_STEP or WNW_F_RECALL_MEMCPY the recall runs on an internal stream, joined by
  * events).

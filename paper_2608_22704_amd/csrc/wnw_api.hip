@@ -225,6 +225,8 @@ wnw_status layout_heads(wnw_ctx *c)
         const int k0 = head_keep_of_len(c, lkh, len0), kl = head_keep_of_len(c, lkh, lenl);
         const int keep = g.nc ? (g.nc - 1) * k0 + kl : 0;
         HeadRows &h = c->hrows[hi];
+        h.kfull = k0;
+        h.klast = kl;
         h.rs = keep + g.Tt;
         h.nts = (h.rs + TILE_S - 1) / TILE_S;
         h.tile0 = (int)tiles;
@@ -279,28 +281,47 @@ wnw_status layout_heads(wnw_ctx *c)
     return WNW_OK;
 }
 
-// Per-segment prefill keep selection of one head (Method, "Prefill Compression"); the
-// complement of segment ch goes to comp_by_seg[ch * cstride ..] (cstride >= every complement).
-void keep_rows(const wnw_ctx *c, int lkh, const float *score, int cstride, std::vector<int32_t> &kept,
-               std::vector<int32_t> &comp_by_seg)
+// Per-segment prefill keep selection of one head (Method, "Prefill Compression"): in segment
+// ch the kfull (klast for the last segment) positions with the highest score, ties to the
+// lower position.  flags[T_a] = 1 for kept positions.
+void keep_flags_host(const Geometry &g, const HeadRows &hr, const float *score, uint8_t *flags)
 {
-    const Geometry &g = c->g;
-    kept.clear();
-    comp_by_seg.assign((size_t)g.nc * cstride, -1);
     std::vector<int32_t> pos;
     for (int ch = 0; ch < g.nc; ++ch) {
-        const int b0 = ch * g.cl, len = chunk_len_of(g, ch), kc = head_keep_of_len(c, lkh, len);
+        const int b0 = ch * g.cl, len = chunk_len_of(g, ch), kc = ch == g.nc - 1 ? hr.klast : hr.kfull;
         pos.resize(len);
         std::iota(pos.begin(), pos.end(), b0);
         std::stable_sort(pos.begin(), pos.end(), [&](int32_t a, int32_t b) {
             if (score[a] != score[b]) return score[a] > score[b];
             return a < b;
         });
-        std::sort(pos.begin(), pos.begin() + kc);
-        std::sort(pos.begin() + kc, pos.end());
-        kept.insert(kept.end(), pos.begin(), pos.begin() + kc);
-        if (cstride) std::copy(pos.begin() + kc, pos.end(), comp_by_seg.begin() + (size_t)ch * cstride);
+        for (int i = 0; i < len; ++i) flags[pos[i]] = i < kc;
     }
+}
+
+// Kept positions (ascending) and, per segment, the complement (ascending) into
+// comp_by_seg[ch * cfull ..] (tidal heads).  False if the flags do not hold kfull / klast kept
+// positions per segment (the layout was sized for those counts).
+bool rows_from_flags(const Geometry &g, const HeadRows &hr, const uint8_t *flags, std::vector<int32_t> &kept,
+                     std::vector<int32_t> &comp_by_seg)
+{
+    kept.clear();
+    comp_by_seg.assign((size_t)g.nc * hr.cfull, -1);
+    for (int ch = 0; ch < g.nc; ++ch) {
+        const int b0 = ch * g.cl, e0 = b0 + chunk_len_of(g, ch), kc = ch == g.nc - 1 ? hr.klast : hr.kfull;
+        int nk = 0, nd = 0;
+        for (int t = b0; t < e0; ++t) {
+            if (flags[t]) {
+                kept.push_back(t);
+                ++nk;
+            } else if (hr.cfull > 0) {   // fixed heads drop their complement
+                if (nd >= hr.cfull) return false;
+                comp_by_seg[(size_t)ch * hr.cfull + nd++] = t;
+            }
+        }
+        if (nk != kc) return false;
+    }
+    return true;
 }
 
 void parallel_for(int n, const std::function<void(int)> &fn)
@@ -416,22 +437,34 @@ wnw_status wnw_init_cache(const wnw_config *cfg, const void *k_dev, const void *
     return WNW_OK;
 }
 
-wnw_status wnw_set_roles(wnw_ctx *c, const uint8_t *roles, const float *prefill)
+}  // extern "C"
+
+namespace {
+
+// Roles and per-head rows; nothing allocated.
+wnw_status assign_roles(wnw_ctx *c, const uint8_t *roles)
 {
-    if (!c) return fail(nullptr, WNW_ERR_INVALID, "ctx is NULL");
-    if (c->state != CREATED) return fail(c, WNW_ERR_STATE, "wnw_set_roles must be called once, right after wnw_init_cache");
-    if (!roles || !prefill) return fail(c, WNW_ERR_INVALID, "roles and prefill_scores must not be NULL");
     Geometry &g = c->g;
     const int nh = g.L * g.Hkv;
-    for (int i = 0; i < nh; ++i) {
+    for (int i = 0; i < nh; ++i)
         if (roles[i] > WNW_FIXED) return fail(c, WNW_ERR_INVALID, "role %d of head %d is not a wnw_role", roles[i], i);
+    c->anchor_lk.clear();
+    c->tidal_lk.clear();
+    c->fixed_lk.clear();
+    for (int i = 0; i < nh; ++i)
         (roles[i] == WNW_ANCHOR ? c->anchor_lk : roles[i] == WNW_TIDAL ? c->tidal_lk : c->fixed_lk).push_back(i);
-    }
     g.nA = (int)c->anchor_lk.size();
     g.nT = (int)c->tidal_lk.size();
     g.nF = (int)c->fixed_lk.size();
-    wnw_status lr = layout_heads(c);
-    if (lr != WNW_OK) return lr;
+    return layout_heads(c);
+}
+
+// Allocations and tier construction, from host prefill scores (ranked on the host) or from keep
+// flags [B][nT + nF][T_a] already ranked on the device.
+wnw_status build_tiers(wnw_ctx *c, const float *prefill, const uint8_t *keep_all)
+{
+    Geometry &g = c->g;
+    const int nh = g.L * g.Hkv;
     DeviceGuard dg(c->device);
     hipStream_t st = c->setup_stream;
     const size_t B = g.B, Dz = D;
@@ -546,15 +579,27 @@ wnw_status wnw_set_roles(wnw_ctx *c, const uint8_t *roles, const float *prefill)
                 return fail(c, WNW_ERR_HIP, "anchor tier copy failed: %s", hipGetErrorString(e1 != hipSuccess ? e1 : e2));
             }
         }
-        // keep selection (host, threaded over heads)
+        // keep selection (host ranking, or the device's flags), threaded over heads
+        std::vector<uint8_t> bad(nsub, 0);
         parallel_for(nsub, [&](int hi) {
             const bool tidal = hi < g.nT;
             const int lkh = tidal ? c->tidal_lk[hi] : c->fixed_lk[hi - g.nT];
-            const float *sc = prefill + ((size_t)b * nh + lkh) * g.Ta;
             const HeadRows &hr = c->hrows[hi];
             const int keep = c->head_keep[hi];
+            std::vector<uint8_t> fl;
+            const uint8_t *flags;
+            if (keep_all) {
+                flags = keep_all + ((size_t)b * nsub + hi) * g.Ta;
+            } else {
+                fl.resize(g.Ta);
+                keep_flags_host(g, hr, prefill + ((size_t)b * nh + lkh) * g.Ta, fl.data());
+                flags = fl.data();
+            }
             std::vector<int32_t> kept, comp;
-            keep_rows(c, lkh, sc, hr.cfull, kept, comp);
+            if (!rows_from_flags(g, hr, flags, kept, comp)) {
+                bad[hi] = 1;
+                return;
+            }
             const int32_t base = (int32_t)((size_t)lkh * g.T);
             int32_t *si = static_idx.data() + (tidal ? 0 : (size_t)g.RsT) + hr.srow;
             for (int i = 0; i < keep; ++i) si[i] = base + kept[i];
@@ -569,6 +614,11 @@ wnw_status wnw_set_roles(wnw_ctx *c, const uint8_t *roles, const float *prefill)
                                 p < 0 ? -1 : (half == 0 ? base + p : -(base + p) - 2);
                         }
         });
+        for (int hi = 0; hi < nsub; ++hi)
+            if (bad[hi]) {
+                cleanup();
+                return fail(c, WNW_ERR_HIP, "keep flags of sequence %d, head %d do not match the keep counts", b, hi);
+            }
         // static rows of tidal and fixed heads
         hipError_t e = hipMemcpyAsync(d_idx, static_idx.data(), static_idx.size() * sizeof(int32_t), hipMemcpyHostToDevice, st);
         if (e == hipSuccess && g.RsT)
@@ -613,6 +663,90 @@ wnw_status wnw_set_roles(wnw_ctx *c, const uint8_t *roles, const float *prefill)
     HIPCHECK(c, hipDeviceSynchronize());
     c->full_k = c->full_v = nullptr;
     c->state = READY;
+    return WNW_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+wnw_status wnw_set_roles(wnw_ctx *c, const uint8_t *roles, const float *prefill)
+{
+    if (!c) return fail(nullptr, WNW_ERR_INVALID, "ctx is NULL");
+    if (c->state != CREATED) return fail(c, WNW_ERR_STATE, "wnw_set_roles must be called once, right after wnw_init_cache");
+    if (!roles || !prefill) return fail(c, WNW_ERR_INVALID, "roles and prefill_scores must not be NULL");
+    wnw_status r = assign_roles(c, roles);
+    if (r != WNW_OK) return r;
+    r = build_tiers(c, prefill, nullptr);
+    if (r != WNW_OK) c->state = FAILED;
+    return r;
+}
+
+wnw_status wnw_set_roles_device(wnw_ctx *c, const uint8_t *roles, const float *prefill_dev)
+{
+    if (!c) return fail(nullptr, WNW_ERR_INVALID, "ctx is NULL");
+    if (c->state != CREATED)
+        return fail(c, WNW_ERR_STATE, "wnw_set_roles_device must be called once, right after wnw_init_cache");
+    if (!roles || !prefill_dev) return fail(c, WNW_ERR_INVALID, "roles and prefill_scores_dev must not be NULL");
+    wnw_status r = assign_roles(c, roles);
+    if (r != WNW_OK) return r;
+    const Geometry &g = c->g;
+    const int nsub = g.nT + g.nF;
+    DeviceGuard dg(c->device);
+    std::vector<uint8_t> flags((size_t)g.B * nsub * g.Ta);
+    if (!flags.empty()) {
+        // per-segment ranking on the device; the flags come back for the index construction
+        std::vector<int32_t> sub_lk(c->tidal_lk);
+        sub_lk.insert(sub_lk.end(), c->fixed_lk.begin(), c->fixed_lk.end());
+        std::vector<int2> sk(nsub);
+        for (int hi = 0; hi < nsub; ++hi) sk[hi] = make_int2(c->hrows[hi].kfull, c->hrows[hi].klast);
+        int32_t *d_sub = nullptr;
+        int2 *d_sk = nullptr;
+        uint8_t *d_flags = nullptr;
+        hipError_t e = hipMalloc((void **)&d_sub, nsub * sizeof(int32_t));
+        if (e == hipSuccess) e = hipMalloc((void **)&d_sk, nsub * sizeof(int2));
+        if (e == hipSuccess) e = hipMalloc((void **)&d_flags, flags.size());
+        hipStream_t st = c->setup_stream;
+        if (e == hipSuccess) e = hipMemcpyAsync(d_sub, sub_lk.data(), nsub * sizeof(int32_t), hipMemcpyHostToDevice, st);
+        if (e == hipSuccess) e = hipMemcpyAsync(d_sk, sk.data(), nsub * sizeof(int2), hipMemcpyHostToDevice, st);
+        if (e == hipSuccess) e = launch_prefill_keep(g, nsub, d_sub, d_sk, prefill_dev, d_flags, st);
+        if (e == hipSuccess) e = hipMemcpyAsync(flags.data(), d_flags, flags.size(), hipMemcpyDeviceToHost, st);
+        if (e == hipSuccess) e = hipStreamSynchronize(st);
+        (void)hipFree(d_sub);
+        (void)hipFree(d_sk);
+        (void)hipFree(d_flags);
+        if (e != hipSuccess) {
+            c->state = FAILED;
+            return fail(c, WNW_ERR_HIP, "device keep selection failed: %s", hipGetErrorString(e));
+        }
+    }
+    r = build_tiers(c, nullptr, flags.data());
+    if (r != WNW_OK) c->state = FAILED;
+    return r;
+}
+
+wnw_status wnw_prefill_scores(wnw_ctx *c, const void *q_text_dev, float *scores_dev)
+{
+    if (!c) return fail(nullptr, WNW_ERR_INVALID, "ctx is NULL");
+    if (c->state != CREATED) return fail(c, WNW_ERR_STATE, "wnw_prefill_scores needs the full cache: call it before wnw_set_roles");
+    const Geometry &g = c->g;
+    if (!scores_dev || (g.Tt > 0 && !q_text_dev))
+        return fail(c, WNW_ERR_INVALID, "scores_dev (and q_text_dev when text_len > 0) must not be NULL");
+    DeviceGuard dg(c->device);
+    float2 *stats = nullptr;
+    const size_t ns = (size_t)g.B * g.L * g.Hq * g.Tt;
+    if (ns) {
+        hipError_t e = hipMalloc((void **)&stats, ns * sizeof(float2));
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            return fail(c, e == hipErrorOutOfMemory ? WNW_ERR_OOM : WNW_ERR_HIP, "prefill statistics: %s", hipGetErrorString(e));
+        }
+    }
+    hipStream_t st = c->setup_stream;
+    hipError_t e = launch_prefill_scores(g, c->full_k, (const uint16_t *)q_text_dev, stats, scores_dev, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (stats) (void)hipFree(stats);
+    if (e != hipSuccess) return fail(c, WNW_ERR_HIP, "prefill scores failed: %s", hipGetErrorString(e));
     return WNW_OK;
 }
 

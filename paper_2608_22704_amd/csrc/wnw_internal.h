@@ -59,6 +59,8 @@ struct HeadRows {
     int coff;    // first row of the head in a segment's complement block: cfull K rows, cfull V rows
     int sg;      // kept slots per slot-group work-group (>= 1)
     int ngk;     // kept-slot groups
+    int kfull;   // kept positions of a full segment (set-up)
+    int klast;   // kept positions of the last segment (set-up)
 };
 
 // Keep count of a chunk of `len` positions: floor(retention * len).
@@ -138,6 +140,14 @@ hipError_t launch_recall(const Geometry &g, const Tiers &t, const StepBuffers &s
 hipError_t launch_new_slots(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st);
 hipError_t launch_subset_combine(const Geometry &g, const Tiers &t, const StepBuffers &s, float *out,
                                  hipStream_t st);
+// Prefill scores (wnw_prefill.hip): p [B][L][Hkv][Ta] fp32 from the full K cache
+// [B][L][Hkv][T][D] and the text queries [B][L][Hq][Tt][D]; stats [B][L][Hq][Tt] is scratch.
+hipError_t launch_prefill_scores(const Geometry &g, const uint16_t *K, const uint16_t *q_text, float2 *stats,
+                                 float *p, hipStream_t st);
+// Per-segment keep flags [B][n_sub][Ta] of the non-anchor heads sub_lk[n_sub] (l * Hkv + kv),
+// keeping seg_keep[h].x positions of a full segment and .y of the last one.
+hipError_t launch_prefill_keep(const Geometry &g, int n_sub, const int32_t *sub_lk, const int2 *seg_keep,
+                               const float *p, uint8_t *keep, hipStream_t st);
 // Set-up: dst[i] = row idx[i] of src_k (idx >= 0), row -idx[i]-2 of src_v (idx <= -2), or zeros
 // (idx == -1); a row is D bf16.
 hipError_t launch_gather_rows(uint16_t *dst, const uint16_t *src_k, const uint16_t *src_v, const int32_t *idx,

@@ -19,7 +19,8 @@ WNW_OK, WNW_ERR_INVALID, WNW_ERR_OOM, WNW_ERR_HIP, WNW_ERR_STATE, WNW_ERR_UNSUPP
 WNW_ANCHOR, WNW_TIDAL, WNW_FIXED = 0, 1, 2
 WNW_F_SELECT_NEXT_STEP, WNW_F_RECALL_MEMCPY, WNW_F_TIMING, WNW_F_OVERLAP_CHUNKS = 1, 2, 4, 8
 
-EXPORTS = ("wnw_init_cache", "wnw_set_retention", "wnw_set_roles", "wnw_decode_step", "wnw_query_geometry",
+EXPORTS = ("wnw_init_cache", "wnw_set_retention", "wnw_set_roles", "wnw_prefill_scores", "wnw_set_roles_device",
+           "wnw_decode_step", "wnw_query_geometry",
            "wnw_query_segments", "wnw_query_head_keep", "wnw_get_stats",
            "wnw_set_selection_override", "wnw_debug_read_slot", "wnw_debug_read_host_chunk",
            "wnw_debug_read_resident", "wnw_last_error", "wnw_destroy")
@@ -61,6 +62,8 @@ def _load():
         "wnw_init_cache": ([C.POINTER(wnw_config), P, P, P, C.POINTER(P)], C.c_int),
         "wnw_set_roles": ([P, P, P], C.c_int),
         "wnw_set_retention": ([P, P, C.c_float], C.c_int),
+        "wnw_prefill_scores": ([P, P, P], C.c_int),
+        "wnw_set_roles_device": ([P, P, P], C.c_int),
         "wnw_query_head_keep": ([P, P], C.c_int),
         "wnw_decode_step": ([P, P, P, P, P, P], C.c_int),
         "wnw_query_geometry": ([P, C.POINTER(I32), C.POINTER(I32), C.POINTER(I32), C.POINTER(I32), C.POINTER(I64)], C.c_int),
@@ -121,6 +124,14 @@ def wnw_set_retention(ctx, importance, lam):
 
 def wnw_set_roles(ctx, roles, prefill_scores):
     _check(lib.wnw_set_roles(ctx, _ptr(roles), _ptr(prefill_scores)), ctx)
+
+
+def wnw_prefill_scores(ctx, q_text_dev, scores_dev):
+    _check(lib.wnw_prefill_scores(ctx, _ptr(q_text_dev), _ptr(scores_dev)), ctx)
+
+
+def wnw_set_roles_device(ctx, roles, prefill_scores_dev):
+    _check(lib.wnw_set_roles_device(ctx, _ptr(roles), _ptr(prefill_scores_dev)), ctx)
 
 
 def wnw_query_head_keep(ctx, layers, kv_heads) -> np.ndarray:

@@ -35,6 +35,7 @@ import numpy as np
 from .configs import Workload
 
 TAG_K, TAG_V, TAG_Z, TAG_DRIFT, TAG_ROLES, TAG_PREFILL, TAG_IMPORTANCE = 1, 2, 3, 4, 5, 6, 7
+TAG_QTEXT, TAG_QTEXT_POS = 8, 9
 ANCHOR, TIDAL, FIXED = 0, 1, 2
 
 
@@ -117,6 +118,22 @@ def head_queries(w: Workload, b: int, l: int, kv: int, k_bf16: np.ndarray, drift
 
 def prefill_scores(w: Workload, b: int, l: int, kv: int) -> np.ndarray:
     return _rng(seq_seed(w, b), TAG_PREFILL, l, kv).random(w.audio_len, dtype=np.float32)
+
+
+def text_queries(w: Workload, b: int, l: int, kv: int, k_bf16: np.ndarray) -> np.ndarray:
+    """uint16 [g][T_t][d]: the text tokens' queries at prefill for the q-heads of one KV-head,
+    built like the decode queries: N(0,1) noise plus drift_gain times the key of one audio
+    position drawn uniformly per (q-head, token)."""
+    seed = seq_seed(w, b)
+    out = np.empty((w.group, w.text_len, w.head_dim), dtype=np.uint16)
+    for j in range(w.group):
+        hq = kv * w.group + j
+        z = _rng(seed, TAG_QTEXT, l, hq).standard_normal((w.text_len, w.head_dim), dtype=np.float32)
+        if w.audio_len > 0:
+            pos = _rng(seed, TAG_QTEXT_POS, l, hq).integers(0, w.audio_len, size=w.text_len)
+            z += np.float32(w.drift_gain) * bf16_to_f32(k_bf16[pos])
+        out[j] = f32_to_bf16(z)
+    return out
 
 
 def importance(w: Workload) -> np.ndarray:

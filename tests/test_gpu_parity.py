@@ -551,3 +551,109 @@ def test_retention_recall_bytes_ragged_layout():
             assert off * 128 * 2 == nbytes
     finally:
         h.close()
+
+
+# ---- prefill compression on the device: text-to-audio attention sums (wnw_prefill_scores) and
+# the per-segment ranking (wnw_set_roles_device); the scores are checked against the oracle's,
+# then the oracle takes the device's fp32 scores and the decode steps run in lock step.
+
+PRE = [
+    _small("pre_g2", 401, Tt=9),
+    _small("pre_g1_text_ragged", 402, Hq=4, Hkv=4, Tt=77, Ta=333, cl=40),
+    _small("pre_g4_long_text", 403, Hq=8, Hkv=2, Tt=300, Ta=517, cl=50),
+    _small("pre_g8_chunk256", 404, Hq=16, Hkv=2, Tt=130, Ta=1300, cl=256),
+    _small("pre_g6", 405, Hq=12, Hkv=2, Tt=3, Ta=1111, cl=100),
+    _small("pre_no_text", 406, Tt=0),
+    _small("pre_batch3", 407, B=3, Ta=777, Tt=65, cl=37, steps=4),
+]
+
+
+@pytest.mark.parametrize("w", PRE, ids=[w.name for w in PRE])
+def test_prefill_device_lockstep(w):
+    h = _run(w, prefill_device=True)
+    from tests.wnw_harness import log
+    log(f"[prefill] {w.name}: max prefill score rel err {h.prefill_err:.3g}")
+
+
+def test_prefill_device_with_overlap_and_retention():
+    w = _small("pre_ovl_ret", 408, L=2, Hq=8, Hkv=4, Ta=480, Tt=33, cl=32, steps=6)
+    _run(w, prefill_device=True, flags=_ovl(_next()))
+    _run(w, prefill_device=True, importance=_imp(w, 408, ((0, 1),), ((1, 2),)), lam=1.0, flags=_next())
+
+
+def test_prefill_device_ranking_equals_host_ranking():
+    """The same fp32 scores through wnw_set_roles_device and wnw_set_roles give byte-identical
+    host complements and bitwise identical steps."""
+    import torch
+    from paper_2608_22704_amd import wnw as W
+    from tests.wnw_harness import log, to_dev
+    w = _small("pre_dev_vs_host", 409, L=2, Hq=8, Hkv=4, Ta=517, Tt=20, cl=50, steps=5)
+    log("[case] device ranking vs host ranking")
+    B, L, H, T, D = w.batch, w.layers, w.kv_heads, w.total_len, w.head_dim
+    kd = torch.empty((B, L, H, T, D), dtype=torch.int16, device="cuda")
+    vd = torch.empty_like(kd)
+    qs = []
+    for b in range(B):
+        seq = gen.sequence(w, b)
+        kd[b].copy_(to_dev(seq["k"]))
+        vd[b].copy_(to_dev(seq["v"]))
+        qs.append(seq["q"])
+    rng = np.random.default_rng(7)
+    sc = (rng.integers(0, 50, size=(B, L, H, w.audio_len)) / 50.0).astype(np.float32)   # many ties
+    roles = gen.roles(w)
+    cfg = W.make_config(B, L, w.q_heads, H, w.audio_len, w.text_len, w.chunk_len, w.budget_bp)
+    ctxs = [W.wnw_init_cache(cfg, kd, vd), W.wnw_init_cache(cfg, kd, vd)]
+    try:
+        W.wnw_set_roles(ctxs[0], roles, sc)
+        W.wnw_set_roles_device(ctxs[1], roles, torch.from_numpy(sc).cuda())
+        geo = W.wnw_query_geometry(ctxs[0])
+        nb = geo["chunk_bytes"]
+        for b in range(B):
+            for c in range(geo["n_segments"]):
+                a0, a1 = np.empty(nb // 2, np.uint16), np.empty(nb // 2, np.uint16)
+                W.wnw_debug_read_host_chunk(ctxs[0], b, c, a0, nb)
+                W.wnw_debug_read_host_chunk(ctxs[1], b, c, a1, nb)
+                assert np.array_equal(a0, a1), f"seq {b} segment {c}"
+        outs = [torch.empty((B, L, w.q_heads, D), dtype=torch.float32, device="cuda") for _ in ctxs]
+        for s in range(w.steps):
+            q = to_dev(np.stack([qs[b][s] for b in range(B)]))
+            for c, o in zip(ctxs, outs):
+                W.wnw_decode_step(c, q, o)
+            torch.cuda.synchronize()
+            assert torch.equal(outs[0], outs[1]), f"step {s}"
+    finally:
+        for c in ctxs:
+            W.wnw_destroy(c)
+
+
+def test_prefill_scores_voxtral_full_size_sampled():
+    """Full-size 15k-audio cache with 512 text tokens: device scores of sampled heads against the
+    oracle (every head is computed on the device)."""
+    import torch
+    from paper_2608_22704_amd import wnw as W
+    from tests.wnw_harness import PREFILL_RTOL, log, to_dev
+    from oracle import oracle as O
+    w = configs.VOXTRAL_10MIN
+    log("[case] prefill scores, 15k audio + 512 text, sampled heads")
+    B, L, H, T, D = w.batch, w.layers, w.kv_heads, w.total_len, w.head_dim
+    seq = gen.sequence(w, 0)
+    kd = to_dev(seq["k"])[None].contiguous()
+    qt = np.stack([gen.text_queries(w, 0, l, kv, seq["k"][l, kv]) for l in range(L) for kv in range(H)])
+    qt = qt.reshape(L, w.q_heads, w.text_len, D)
+    cfg = W.make_config(B, L, w.q_heads, H, w.audio_len, w.text_len, w.chunk_len, w.budget_bp)
+    ctx = W.wnw_init_cache(cfg, kd, kd)
+    try:
+        sc = torch.empty((B, L, H, w.audio_len), dtype=torch.float32, device="cuda")
+        W.wnw_prefill_scores(ctx, to_dev(qt)[None].contiguous(), sc)
+        torch.cuda.synchronize()
+        got = sc.cpu().numpy()[0]
+    finally:
+        W.wnw_destroy(ctx)
+    rng = np.random.default_rng(11)
+    heads = [(int(x) // H, int(x) % H) for x in rng.choice(L * H, size=3, replace=False)]
+    for l, kv in heads:
+        c1 = O.make_cfg(1, 1, w.group, 1, D, w.audio_len, w.text_len, w.chunk_len, w.budget_bp)
+        ref = O.prefill_scores(c1, seq["k"][l, kv][None, None, None], qt[l, kv * w.group:(kv + 1) * w.group][None, None])[0, 0, 0]
+        rel = np.abs(got[l, kv] - ref) / np.maximum(ref, 1e-300)
+        log(f"[prefill] head ({l},{kv}): max rel err {rel.max():.3g}")
+        assert (rel <= PREFILL_RTOL).all()

@@ -23,6 +23,11 @@ from synth import gen
 
 OUT_TOL = 2e-2
 SCORE_RTOL = 1e-5
+# Prefill scores on the device: bf16 products are exact in fp32 and 128 of them are summed in
+# fp32, so a logit carries at most ~128 * 2^-24 * sum|q_i k_i| (<= 2e-4 after the 1/sqrt(d)
+# scale for these inputs) absolute error, which is the relative error of every softmax weight
+# and so of every sum of them; 1e-3 leaves a margin.
+PREFILL_RTOL = 1e-3
 SEL_EXCUSE = 1e-6
 
 
@@ -57,11 +62,52 @@ def check_selection(gpu_sel: np.ndarray, oracle_scores: np.ndarray, k: int) -> i
     return len(diff) // 2
 
 
+def check_prefill(w, seg, seqs, host, gpu_scores, roles, importance, lam) -> float:
+    """Device prefill scores against the oracle's (double), relative per entry; the keep sets
+    that the fp32 scores give (per-segment ranking, the library's rule) must be those of the
+    double scores except at positions whose score lies within PREFILL_RTOL of the segment's
+    boundary.  Returns the largest relative error."""
+    L, H, Ta, Tt, D = w.layers, w.kv_heads, w.audio_len, w.text_len, w.head_dim
+    cfg1 = O.cfg_from_workload(w, batch=1)
+    worst = 0.0
+    for b in seqs:
+        ref = O.prefill_scores(cfg1, host[b]["k"][None], host[b]["q_text"][None])[0]
+        got = gpu_scores[b].astype(np.float64)
+        rel = np.abs(got - ref) / np.maximum(np.abs(ref), 1e-300)
+        worst = max(worst, float(rel.max(initial=0.0)))
+        assert (rel <= PREFILL_RTOL).all(), f"seq {b}: prefill score rel err {rel.max():.3g}"
+        for l in range(L):
+            for kv in range(H):
+                if roles[l, kv] == 0:
+                    continue
+                for c0 in range(0, Ta, seg):
+                    e0 = min(c0 + seg, Ta)
+                    n = e0 - c0
+                    if importance is None:
+                        kc = (w.budget_bp * n) // 10000
+                    else:
+                        kc = int(np.floor(min(float(importance[l, kv]) * float(np.float32(lam)), 1.0) * n))
+                    if kc in (0, n):
+                        continue
+                    r, gsc = ref[l, kv, c0:e0], gpu_scores[b, l, kv, c0:e0]
+                    ko = set(sorted(range(n), key=lambda i: (-r[i], i))[:kc])
+                    kg = set(sorted(range(n), key=lambda i: (-float(gsc[i]), i))[:kc])
+                    bound = sorted(r, reverse=True)[kc - 1]
+                    for i in ko ^ kg:
+                        assert abs(r[i] - bound) <= PREFILL_RTOL * bound, \
+                            f"seq {b} head ({l},{kv}) segment {c0}: keep sets differ beyond near-ties"
+    return worst
+
+
 class Lockstep:
     """One workload, a subset `seqs` of its sequences checked against the oracle (the GPU runs
     all w.batch sequences)."""
 
-    def __init__(self, w, flags: int = 0, seqs=None, budget_bp=None, data=None, top_k=0, importance=None, lam=None):
+    def __init__(self, w, flags: int = 0, seqs=None, budget_bp=None, data=None, top_k=0, importance=None, lam=None,
+                 prefill_device=False):
+        """prefill_device: the prefill scores come from wnw_prefill_scores over the synthetic text
+        queries, the keep sets from wnw_set_roles_device; the scores are checked against the
+        oracle's (double) and then given to the oracle as its prefill input."""
         import torch
         from paper_2608_22704_amd import wnw as W
         self.W, self.torch = W, torch
@@ -76,6 +122,7 @@ class Lockstep:
         vd = torch.empty_like(kd)
         self.q = np.empty((w.steps, B, L, w.q_heads, D), dtype=np.uint16)
         self.prefill = np.empty((B, L, H, w.audio_len), dtype=np.float32)
+        qt = torch.empty((B, L, w.q_heads, w.text_len, D), dtype=torch.int16, device="cuda") if prefill_device else None
         host = {}
         for b in range(B):
             if data is not None:
@@ -86,6 +133,10 @@ class Lockstep:
             vd[b].copy_(to_dev(seq["v"]))
             self.q[:, b] = seq["q"]
             self.prefill[b] = seq["prefill"]
+            if prefill_device:
+                seq["q_text"] = np.stack([gen.text_queries(w, b, l, kv, seq["k"][l, kv])
+                                          for l in range(L) for kv in range(H)]).reshape(L, w.q_heads, w.text_len, D)
+                qt[b].copy_(to_dev(seq["q_text"]))
             if b in self.seqs:
                 host[b] = seq
         torch.cuda.synchronize()
@@ -95,7 +146,17 @@ class Lockstep:
         self.ctx = W.wnw_init_cache(self.cfg, kd, vd)
         if importance is not None:
             W.wnw_set_retention(self.ctx, importance, lam)
-        W.wnw_set_roles(self.ctx, self.roles, self.prefill)
+        if prefill_device:
+            sc = torch.empty((B, L, H, w.audio_len), dtype=torch.float32, device="cuda")
+            W.wnw_prefill_scores(self.ctx, qt, sc)
+            torch.cuda.synchronize()
+            self.prefill = sc.cpu().numpy()
+            seg = w.chunk_len // 2 if flags & W.WNW_F_OVERLAP_CHUNKS else w.chunk_len
+            self.prefill_err = check_prefill(w, seg, self.seqs, host, self.prefill, self.roles, importance, lam)
+            W.wnw_set_roles_device(self.ctx, self.roles, sc)
+            del qt, sc
+        else:
+            W.wnw_set_roles(self.ctx, self.roles, self.prefill)
         del kd, vd
         torch.cuda.empty_cache()
         self.geo = W.wnw_query_geometry(self.ctx)
