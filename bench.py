@@ -28,6 +28,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "WnW decode steps/sec + achieved HBM GB/s (attn) at 15k audio tokens, 1 GPU"
 PEAK_HBM_GBPS = 8000.0
+PEAK_BF16_TFLOPS = 2500.0      # dense bf16 MFMA
 
 
 def log(msg):
@@ -201,6 +202,7 @@ def main():
                          "lambda, 1) per head with seeded U(0,1) importance")
     ap.add_argument("--lam", type=float, default=0.4, help="lambda of the per-head retention (0.4: mean 20 %%)")
     ap.add_argument("--no-other-retention", action="store_true", help="skip the run with the other retention")
+    ap.add_argument("--no-prefill", action="store_true", help="skip the prefill-compression measurement")
     ap.add_argument("--no-sweep", dest="sweep", action="store_false",
                     help="skip the overlap sweep (forced 1..24 newly resident chunks per step)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU oracle sample (0 = skip)")
@@ -254,6 +256,7 @@ def main():
     if not args.no_other_retention:
         other_ret = run_timing(W, torch, w, args.timing, args.recall, kd, vd, qd, roles, prefill, args_other,
                                args.chunks, other_retention)
+    prefill_res = None if args.no_prefill else prefill_bench(W, torch, w, kd, vd, roles)
     del kd, vd
     torch.cuda.empty_cache()
 
@@ -311,6 +314,8 @@ def main():
             o["kernels"] = other_ret["kernels"]
         res["other_retention"] = o
 
+    if prefill_res is not None:
+        res["prefill"] = prefill_res
     if args.cpu_seconds > 0:
         res["cpu_baseline"] = cpu_baseline(w, roles, prefill, args.cpu_seconds)
     print(json.dumps(res), flush=True)
@@ -339,6 +344,56 @@ def measured_traffic(kernel, workload):
     except (KeyError, ValueError, ZeroDivisionError):
         return None
     return fetch + write
+
+
+def prefill_bench(W, torch, w, kd, vd, roles, reps=5):
+    """Prefill compression on the device for the workload: wnw_prefill_scores (text-to-audio
+    attention sums over the synthetic text queries, two MFMA passes) timed with events on the
+    set-up stream, then wnw_set_roles_device against wnw_set_roles (host ranking) on the same
+    scores.  Algorithmic flops: 2 d per logit, each logit computed once per pass over its
+    causal key set (pass 1: T_a + t + 1 keys for text token t; pass 2: the T_a audio keys)."""
+    from synth import gen
+    B, L, H, D, Ta, Tt, g = w.batch, w.layers, w.kv_heads, w.head_dim, w.audio_len, w.text_len, w.group
+    qt = torch.empty((B, L, w.q_heads, Tt, D), dtype=torch.int16, device="cuda")
+    for b in range(B):
+        kb = kd[b].cpu().numpy().view(np.uint16)
+        for l in range(L):
+            for kv in range(H):
+                qt[b, l, kv * g:(kv + 1) * g].copy_(torch.from_numpy(gen.text_queries(w, b, l, kv, kb[l, kv]).view(np.int16)))
+    sc = torch.empty((B, L, H, Ta), dtype=torch.float32, device="cuda")
+    cfg = W.make_config(B, L, w.q_heads, H, Ta, Tt, w.chunk_len, w.budget_bp, flags=W.WNW_F_SELECT_NEXT_STEP)
+    stream = torch.cuda.current_stream()
+    flop = 2.0 * D * g * L * H * B * (Tt * (Ta + 1) + Tt * (Tt - 1) / 2 + Tt * Ta)
+    ctx = W.wnw_init_cache(cfg, kd, vd, stream)
+    try:
+        W.wnw_prefill_scores(ctx, qt, sc)            # warm-up
+        ms = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            W.wnw_prefill_scores(ctx, qt, sc)
+            e1.record(stream)
+            e1.synchronize()
+            ms.append(e0.elapsed_time(e1))
+        t0 = time.perf_counter()
+        W.wnw_set_roles_device(ctx, roles, sc)
+        t_dev = time.perf_counter() - t0
+    finally:
+        W.wnw_destroy(ctx)
+    host_sc = sc.cpu().numpy()
+    ctx = W.wnw_init_cache(cfg, kd, vd, stream)
+    try:
+        t0 = time.perf_counter()
+        W.wnw_set_roles(ctx, roles, host_sc)
+        t_host = time.perf_counter() - t0
+    finally:
+        W.wnw_destroy(ctx)
+    avg = sum(ms) / len(ms)
+    tf = flop / (avg * 1e-3) / 1e12
+    log(f"[bench] prefill scores {avg:.3f} ms ({tf:.0f} TFLOP/s); set_roles device {t_dev:.2f} s, host {t_host:.2f} s")
+    return {"scores_ms": avg, "flop": flop, "achieved_tflops": tf, "peak_tflops": PEAK_BF16_TFLOPS,
+            "frac": tf / PEAK_BF16_TFLOPS, "set_roles_device_s": t_dev, "set_roles_host_s": t_host,
+            "note": "one-time set-up, outside the decode step; scores_ms over both MFMA passes (HIP events)"}
 
 
 def cpu_baseline(w, roles, prefill, budget_s):

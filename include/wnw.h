@@ -178,7 +178,7 @@ wnw_status wnw_set_roles(wnw_ctx *ctx, const uint8_t *roles, const float *prefil
  *   scores_dev  device fp32 [B][L][H_kv][T_a], written
  * Reads the full cache given to wnw_init_cache, so only before wnw_set_roles / _device
  * (WNW_ERR_STATE after).  Runs on the stream given to wnw_init_cache and waits for it; uses a
- * temporary device buffer of B * L * H_q * T_t * 8 bytes. */
+ * temporary device buffer of B * L * H_q * T_t * 4 bytes. */
 wnw_status wnw_prefill_scores(wnw_ctx *ctx, const void *q_text_dev, float *scores_dev);
 
 /* As wnw_set_roles, with the prefill scores in device memory (e.g. from wnw_prefill_scores):

@@ -733,10 +733,10 @@ wnw_status wnw_prefill_scores(wnw_ctx *c, const void *q_text_dev, float *scores_
     if (!scores_dev || (g.Tt > 0 && !q_text_dev))
         return fail(c, WNW_ERR_INVALID, "scores_dev (and q_text_dev when text_len > 0) must not be NULL");
     DeviceGuard dg(c->device);
-    float2 *stats = nullptr;
+    float *stats = nullptr;
     const size_t ns = (size_t)g.B * g.L * g.Hq * g.Tt;
     if (ns) {
-        hipError_t e = hipMalloc((void **)&stats, ns * sizeof(float2));
+        hipError_t e = hipMalloc((void **)&stats, ns * sizeof(float));
         if (e != hipSuccess) {
             (void)hipGetLastError();
             return fail(c, e == hipErrorOutOfMemory ? WNW_ERR_OOM : WNW_ERR_HIP, "prefill statistics: %s", hipGetErrorString(e));

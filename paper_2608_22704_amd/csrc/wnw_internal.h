@@ -141,8 +141,8 @@ hipError_t launch_new_slots(const Geometry &g, const Tiers &t, const StepBuffers
 hipError_t launch_subset_combine(const Geometry &g, const Tiers &t, const StepBuffers &s, float *out,
                                  hipStream_t st);
 // Prefill scores (wnw_prefill.hip): p [B][L][Hkv][Ta] fp32 from the full K cache
-// [B][L][Hkv][T][D] and the text queries [B][L][Hq][Tt][D]; stats [B][L][Hq][Tt] is scratch.
-hipError_t launch_prefill_scores(const Geometry &g, const uint16_t *K, const uint16_t *q_text, float2 *stats,
+// [B][L][Hkv][T][D] and the text queries [B][L][Hq][Tt][D]; lse [B][L][Hq][Tt] is scratch.
+hipError_t launch_prefill_scores(const Geometry &g, const uint16_t *K, const uint16_t *q_text, float *lse,
                                  float *p, hipStream_t st);
 // Per-segment keep flags [B][n_sub][Ta] of the non-anchor heads sub_lk[n_sub] (l * Hkv + kv),
 // keeping seg_keep[h].x positions of a full segment and .y of the last one.

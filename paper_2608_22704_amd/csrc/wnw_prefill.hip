@@ -6,10 +6,10 @@
 // and to text rows 0..t.  Per KV-head this is S = Q K^T with Q the g * T_t text query rows and K
 // the T_a + T_t key rows, a dense contraction, so both passes run on
 // v_mfma_f32_16x16x32_bf16 (bf16 operands, fp32 accumulation):
-//   pass 1 (prefill_rowstats_kernel): per query row, the softmax maximum and sum over its
-//           causal key set;
+//   pass 1 (prefill_rowstats_kernel): per query row, the log-sum-exp of its logits over its
+//           causal key set (base 2);
 //   pass 2 (prefill_colsum_kernel): per audio key, the sum over all query rows of
-//           exp(s - max) / sum.  Audio keys are visible to every text row, so pass 2 needs no mask.
+//           exp(s - lse).  Audio keys are visible to every text row, so pass 2 needs no mask.
 // Operand layout of v_mfma_f32_16x16x32_bf16 (wave64): lane l holds A row l % 16 and B column
 // l % 16, each at k = 8 * (l / 16) .. + 8 (of 32); the 16x16 fp32 result holds column l % 16 of
 // rows 4 * (l / 16) + i in element i.
@@ -41,13 +41,33 @@ __device__ inline f32x4_t mfma16(bf16x8_t a, bf16x8_t b, f32x4_t c)
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
-// Stage TILE rows of D bf16 (rows >= n are zero) into padded LDS rows.
-__device__ inline void stage_rows(uint4 *dst, const uint16_t *src, int r0, int n)
+// A tile of TILE rows of D bf16 goes global -> registers (load, rows >= n read as zero) ->
+// padded LDS rows (store), so the next tile's loads overlap the current tile's arithmetic.
+constexpr int SPT = TILE * (D / 8) / NT;   // 16-byte pieces per thread
+__device__ inline void tile_load(uint4 v[SPT], const uint16_t *src, int r0, int n)
 {
-    for (int i = threadIdx.x; i < TILE * (D / 8); i += NT) {
-        const int rr = i >> 4, c = i & 15, r = r0 + rr;
-        dst[rr * PADU + c] = r < n ? *(const uint4 *)(src + (size_t)r * D + c * 8) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int j = 0; j < SPT; ++j) {
+        const int i = threadIdx.x + j * NT, r = r0 + (i >> 4);
+        v[j] = r < n ? *(const uint4 *)(src + (size_t)r * D + (i & 15) * 8) : make_uint4(0, 0, 0, 0);
     }
+}
+__device__ inline void tile_store(uint4 *dst, const uint4 v[SPT])
+{
+#pragma unroll
+    for (int j = 0; j < SPT; ++j) {
+        const int i = threadIdx.x + j * NT;
+        dst[(i >> 4) * PADU + (i & 15)] = v[j];
+    }
+}
+
+// Work-group w is dispatched to accelerator die (XCD) w % 8, each with its own L2.  The
+// returned order gives the work-groups of one die consecutive logical indices, so the blocks
+// of one KV-head (which share its K or Q rows) run on one die and share its L2.
+__device__ inline int xcd_order(int w, int n)
+{
+    const int q = n / 8, r = n % 8, x = w % 8;
+    return x * q + min(x, r) + w / 8;
 }
 
 // Merge of two (max, sum) pairs of base-2 softmax statistics.
@@ -60,20 +80,22 @@ __device__ inline void merge_ms(float &m, float &l, float m2, float l2)
     l = a + b;
 }
 
-// Pass 1.  Grid (ceil(g * T_t / RS_ROWS), L * H_kv, B).  Wave w owns query rows
+// Pass 1.  Grid: ceil(g * T_t / RS_ROWS) row blocks for each of the B * L * H_kv KV-heads,
+// in XCD order.  Wave w owns query rows
 // r0 + 32 w .. + 32 (two 16-row blocks) of KV-head (b, lk); rows r = j * T_t + t (q-head j of
 // the group, text token t).  Each lane keeps an online (max, sum) for the four rows it holds in
 // the result layout, over the keys of its column; the 16 columns are merged at the end.
 __global__ __launch_bounds__(NT) void prefill_rowstats_kernel(Geometry g, const uint16_t *__restrict__ K,
-                                                             const uint16_t *__restrict__ qt, float2 *__restrict__ stats)
+                                                             const uint16_t *__restrict__ qt, float *__restrict__ lse)
 {
-    const int lk = blockIdx.y, b = blockIdx.z, l = lk / g.Hkv, kv = lk - l * g.Hkv;
+    const int R = g.G * g.Tt, nrb = (R + RS_ROWS - 1) / RS_ROWS;
+    const int v = xcd_order(blockIdx.x, gridDim.x), hd = v / nrb, rblk = v - hd * nrb;
+    const int b = hd / (g.L * g.Hkv), lk = hd - b * g.L * g.Hkv, l = lk / g.Hkv, kv = lk - l * g.Hkv;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, col = lane & 15, grp = lane >> 4;
-    const int R = g.G * g.Tt;
-    const uint16_t *Kh = K + ((size_t)b * g.L * g.Hkv + lk) * (size_t)g.T * D;
+    const uint16_t *Kh = K + (size_t)hd * g.T * D;
     const size_t qbase = (((size_t)b * g.L + l) * g.Hq + (size_t)kv * g.G) * g.Tt;
     const uint16_t *Qh = qt + qbase * D;
-    const int rw = blockIdx.x * RS_ROWS + wave * 32;
+    const int rw = rblk * RS_ROWS + wave * 32;
 
     bf16x8_t qf[2][4];
 #pragma unroll
@@ -96,35 +118,61 @@ __global__ __launch_bounds__(NT) void prefill_rowstats_kernel(Geometry g, const 
             s[rb][i] = 0.f;
         }
 
-    __shared__ uint4 ks[TILE * PADU];
-    for (int k0 = 0; k0 < g.T; k0 += TILE) {
-        __syncthreads();
-        stage_rows(ks, Kh, k0, g.T);
-        __syncthreads();
+    __shared__ uint4 kbuf[2][TILE * PADU];
+    uint4 pre[SPT];
+    tile_load(pre, Kh, 0, g.T);
+    tile_store(kbuf[0], pre);
+    __syncthreads();
+    for (int k0 = 0, it = 0; k0 < g.T; k0 += TILE, ++it) {
+        const uint4 *ks = kbuf[it & 1];
+        const bool more = k0 + TILE < g.T;
+        if (more) tile_load(pre, Kh, k0 + TILE, g.T);
+        // logits of the tile: x[rb][kb][i] for row 4 * grp + i of block rb, key k0 + 16 kb + col
+        f32x4_t x[2][TILE / 16];
 #pragma unroll
         for (int kb = 0; kb < TILE / 16; ++kb) {
             bf16x8_t kf[4];
 #pragma unroll
             for (int kk = 0; kk < 4; ++kk) kf[kk] = as_bf8(ks[(kb * 16 + col) * PADU + grp + 4 * kk]);
-            const int key = k0 + kb * 16 + col;
 #pragma unroll
             for (int rb = 0; rb < 2; ++rb) {
                 f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int kk = 0; kk < 4; ++kk) acc = mfma16(qf[rb][kk], kf[kk], acc);
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    if (key > lim[rb][i]) continue;   // causal mask (and rows past the end)
-                    const float x = acc[i] * C2;
-                    if (x > m[rb][i]) {
-                        s[rb][i] = s[rb][i] * exp2f(m[rb][i] - x) + 1.f;
-                        m[rb][i] = x;
-                    } else {
-                        s[rb][i] += exp2f(x - m[rb][i]);
-                    }
-                }
+                x[rb][kb] = acc * C2;
             }
         }
+        // keys past a row's causal limit (text rows after its token, rows past the end, keys
+        // past the cache) drop out; tiles entirely inside the audio need no mask
+        if (k0 + TILE > g.Ta) {
+#pragma unroll
+            for (int kb = 0; kb < TILE / 16; ++kb) {
+                const int key = k0 + kb * 16 + col;
+#pragma unroll
+                for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        if (key > lim[rb][i]) x[rb][kb][i] = -INFINITY;
+            }
+        }
+        // one rescale per row and tile: the lane's four keys of the tile at once
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                float mt = x[rb][0][i];
+#pragma unroll
+                for (int kb = 1; kb < TILE / 16; ++kb) mt = fmaxf(mt, x[rb][kb][i]);
+                if (mt == -INFINITY) continue;   // every key of the tile masked for this row
+                const float mn = fmaxf(m[rb][i], mt);
+                float acc = s[rb][i] * exp2f(m[rb][i] - mn);   // exp2(-inf) = 0 for an empty row
+#pragma unroll
+                for (int kb = 0; kb < TILE / 16; ++kb) acc += exp2f(x[rb][kb][i] - mn);
+                s[rb][i] = acc;
+                m[rb][i] = mn;
+            }
+        if (more) tile_store(kbuf[(it + 1) & 1], pre);
+        __syncthreads();
     }
     // merge the 16 columns of each row (lanes of one group), in a fixed order
 #pragma unroll
@@ -142,25 +190,27 @@ __global__ __launch_bounds__(NT) void prefill_rowstats_kernel(Geometry g, const 
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int r = rw + rb * 16 + 4 * grp + i;
-                if (r < R) stats[qbase + r] = make_float2(m[rb][i], 1.f / s[rb][i]);
+                if (r < R) lse[qbase + r] = m[rb][i] + log2f(s[rb][i]);
             }
 }
 
-// Pass 2.  Grid (ceil(T_a / CS_KEYS), L * H_kv, B).  Wave w owns audio keys k0 + 32 w .. + 32
+// Pass 2.  Grid: ceil(T_a / CS_KEYS) key blocks for each of the B * L * H_kv KV-heads, in XCD
+// order.  Wave w owns audio keys k0 + 32 w .. + 32
 // (two 16-key blocks, their K fragments held in registers); the work-group walks every query row
-// of the KV-head in tiles of TILE rows staged in LDS with their statistics, and each lane adds
-// exp2(s * C2 - max) / sum over the rows it holds for its key column.
+// of the KV-head in tiles of TILE rows staged in LDS with their log-sum-exp, and each lane adds
+// exp2(s * C2 - lse) over the rows it holds for its key column.
 __global__ __launch_bounds__(NT) void prefill_colsum_kernel(Geometry g, const uint16_t *__restrict__ K,
                                                            const uint16_t *__restrict__ qt,
-                                                           const float2 *__restrict__ stats, float *__restrict__ p)
+                                                           const float *__restrict__ lse, float *__restrict__ p)
 {
-    const int lk = blockIdx.y, b = blockIdx.z, l = lk / g.Hkv, kv = lk - l * g.Hkv;
+    const int R = g.G * g.Tt, nkb = (g.Ta + CS_KEYS - 1) / CS_KEYS;
+    const int v = xcd_order(blockIdx.x, gridDim.x), hd = v / nkb, kblk = v - hd * nkb;
+    const int b = hd / (g.L * g.Hkv), lk = hd - b * g.L * g.Hkv, l = lk / g.Hkv, kv = lk - l * g.Hkv;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, col = lane & 15, grp = lane >> 4;
-    const int R = g.G * g.Tt;
-    const uint16_t *Kh = K + ((size_t)b * g.L * g.Hkv + lk) * (size_t)g.T * D;
+    const uint16_t *Kh = K + (size_t)hd * g.T * D;
     const size_t qbase = (((size_t)b * g.L + l) * g.Hq + (size_t)kv * g.G) * g.Tt;
     const uint16_t *Qh = qt + qbase * D;
-    const int kw = blockIdx.x * CS_KEYS + wave * 32;
+    const int kw = kblk * CS_KEYS + wave * 32;
 
     bf16x8_t kf[2][4];
 #pragma unroll
@@ -172,22 +222,30 @@ __global__ __launch_bounds__(NT) void prefill_colsum_kernel(Geometry g, const ui
                                            : make_uint4(0, 0, 0, 0));
     }
     float acc[2] = {0.f, 0.f};
-    __shared__ uint4 qs[TILE * PADU];
-    __shared__ float2 sst[TILE];
-    for (int r0 = 0; r0 < R; r0 += TILE) {
-        __syncthreads();
-        stage_rows(qs, Qh, r0, R);
-        if (threadIdx.x < TILE) {
-            const int r = r0 + threadIdx.x;
-            sst[threadIdx.x] = r < R ? stats[qbase + r] : make_float2(0.f, 0.f);   // a padding row adds 0
+    __shared__ uint4 qbuf[2][TILE * PADU];
+    __shared__ float sbuf[2][TILE];
+    uint4 pre[SPT];
+    float pl = 0.f;
+    // a padding row adds exp2(-inf) = 0
+    auto lse_of = [&](int r) { return r < R ? lse[qbase + r] : INFINITY; };
+    tile_load(pre, Qh, 0, R);
+    tile_store(qbuf[0], pre);
+    if (threadIdx.x < TILE) sbuf[0][threadIdx.x] = lse_of(threadIdx.x);
+    __syncthreads();
+    for (int r0 = 0, it = 0; r0 < R; r0 += TILE, ++it) {
+        const uint4 *qs = qbuf[it & 1];
+        const float *sst = sbuf[it & 1];
+        const bool more = r0 + TILE < R;
+        if (more) {
+            tile_load(pre, Qh, r0 + TILE, R);
+            if (threadIdx.x < TILE) pl = lse_of(r0 + TILE + threadIdx.x);
         }
-        __syncthreads();
 #pragma unroll
         for (int rb = 0; rb < TILE / 16; ++rb) {
             bf16x8_t qf[4];
 #pragma unroll
             for (int kk = 0; kk < 4; ++kk) qf[kk] = as_bf8(qs[(rb * 16 + col) * PADU + grp + 4 * kk]);
-            float2 st[4];
+            float st[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i) st[i] = sst[rb * 16 + 4 * grp + i];
 #pragma unroll
@@ -196,9 +254,14 @@ __global__ __launch_bounds__(NT) void prefill_colsum_kernel(Geometry g, const ui
 #pragma unroll
                 for (int kk = 0; kk < 4; ++kk) sc = mfma16(qf[kk], kf[kb][kk], sc);
 #pragma unroll
-                for (int i = 0; i < 4; ++i) acc[kb] += exp2f(sc[i] * C2 - st[i].x) * st[i].y;
+                for (int i = 0; i < 4; ++i) acc[kb] += exp2f(fmaf(sc[i], C2, -st[i]));
             }
         }
+        if (more) {
+            tile_store(qbuf[(it + 1) & 1], pre);
+            if (threadIdx.x < TILE) sbuf[(it + 1) & 1][threadIdx.x] = pl;
+        }
+        __syncthreads();
     }
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
@@ -209,7 +272,7 @@ __global__ __launch_bounds__(NT) void prefill_colsum_kernel(Geometry g, const ui
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
             const int key = kw + kb * 16 + col;
-            if (key < g.Ta) p[((size_t)b * g.L * g.Hkv + lk) * g.Ta + key] = acc[kb];
+            if (key < g.Ta) p[(size_t)hd * g.Ta + key] = acc[kb];
         }
 }
 
@@ -240,18 +303,20 @@ __global__ __launch_bounds__(NT) void prefill_keep_kernel(Geometry g, const int3
 
 }  // namespace
 
-hipError_t launch_prefill_scores(const Geometry &g, const uint16_t *K, const uint16_t *q_text, float2 *stats,
+hipError_t launch_prefill_scores(const Geometry &g, const uint16_t *K, const uint16_t *q_text, float *lse,
                                  float *p, hipStream_t st)
 {
     const int R = g.G * g.Tt;
     if (g.Ta == 0) return hipSuccess;
     if (R == 0) return hipMemsetAsync(p, 0, (size_t)g.B * g.L * g.Hkv * g.Ta * sizeof(float), st);
-    hipLaunchKernelGGL(prefill_rowstats_kernel, dim3((R + RS_ROWS - 1) / RS_ROWS, g.L * g.Hkv, g.B), dim3(NT), 0, st, g,
-                       K, q_text, stats);
+    const long long nheads = (long long)g.B * g.L * g.Hkv;
+    const long long n1 = (long long)((R + RS_ROWS - 1) / RS_ROWS) * nheads;
+    const long long n2 = (long long)((g.Ta + CS_KEYS - 1) / CS_KEYS) * nheads;
+    if (n1 > INT32_MAX || n2 > INT32_MAX) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(prefill_rowstats_kernel, dim3((unsigned)n1), dim3(NT), 0, st, g, K, q_text, lse);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(prefill_colsum_kernel, dim3((g.Ta + CS_KEYS - 1) / CS_KEYS, g.L * g.Hkv, g.B), dim3(NT), 0, st,
-                       g, K, q_text, (const float2 *)stats, p);
+    hipLaunchKernelGGL(prefill_colsum_kernel, dim3((unsigned)n2), dim3(NT), 0, st, g, K, q_text, (const float *)lse, p);
     return hipGetLastError();
 }
 
