@@ -84,7 +84,12 @@ enum {
      * per chunk; keep sets, masses, residency, slots and recall are per segment (a resident
      * chunk makes both its segments resident).  chunk_len must be even.  Default: disjoint
      * chunks of chunk_len positions, each its own segment. */
-    WNW_F_OVERLAP_CHUNKS = 8u
+    WNW_F_OVERLAP_CHUNKS = 8u,
+    /* Prefill compression without the per-segment quota: a head keeps the same number of audio
+     * positions (the sum of its per-segment counts), the best over its whole audio; a segment
+     * may then be kept whole or not at all, and complements differ in size from segment to
+     * segment.  Default: per segment. */
+    WNW_F_PREFILL_GLOBAL = 16u
 };
 
 typedef struct wnw_ctx wnw_ctx;

@@ -61,12 +61,14 @@ struct wnw_ctx {
     std::vector<HeadRows> hrows;       // [nT + nF]
     std::vector<int32_t> head_keep;    // [nT + nF] kept audio rows
     int64_t keep_sum_t = 0;            // kept audio rows over the tidal heads
+    std::vector<int32_t> comp_rows;    // [B][nc][nT] complement rows of each unit
+    std::vector<int32_t> seg_rows;     // [B][nc] their sum over the tidal heads
 
     Tiers t{};
     StepBuffers s{};
     uint16_t *aK = nullptr, *aV = nullptr, *tK = nullptr, *tV = nullptr, *fK = nullptr, *fV = nullptr;
     uint16_t *slots = nullptr, *host_comp = nullptr;
-    int32_t *d_lk = nullptr, *d_tile_head = nullptr;
+    int32_t *d_lk = nullptr, *d_tile_head = nullptr, *d_comp_rows = nullptr, *d_seg_rows = nullptr;
     HeadRows *d_hr = nullptr;
     float *scores_int = nullptr;
     int32_t *sel_int = nullptr;
@@ -146,7 +148,8 @@ wnw_status derive(wnw_ctx *c, const wnw_config &cfg, Geometry &g)
     if (cfg.chunk_len < 1) return fail(c, WNW_ERR_INVALID, "chunk_len must be >= 1");
     if (cfg.budget_bp < 0 || cfg.budget_bp > 10000) return fail(c, WNW_ERR_INVALID, "budget_bp must be in 0..10000");
     if (cfg.top_k < 0 || cfg.evict_lag < 0) return fail(c, WNW_ERR_INVALID, "top_k and evict_lag must be >= 0");
-    if (cfg.flags & ~(uint32_t)(WNW_F_SELECT_NEXT_STEP | WNW_F_RECALL_MEMCPY | WNW_F_TIMING | WNW_F_OVERLAP_CHUNKS))
+    if (cfg.flags & ~(uint32_t)(WNW_F_SELECT_NEXT_STEP | WNW_F_RECALL_MEMCPY | WNW_F_TIMING | WNW_F_OVERLAP_CHUNKS |
+                                WNW_F_PREFILL_GLOBAL))
         return fail(c, WNW_ERR_INVALID, "unknown flag bits 0x%x", cfg.flags);
     const int span = (cfg.flags & WNW_F_OVERLAP_CHUNKS) ? 2 : 1;
     if (span == 2 && cfg.chunk_len % 2)
@@ -206,17 +209,17 @@ int head_keep_of_len(const wnw_ctx *c, int lkh, int len)
     return (int)std::floor(r * (double)len);
 }
 
-// Per-head rows of the tidal and fixed heads, once the roles are known: static tiers, segment
-// complement blocks, static tiles and partial entries (HeadRows).
-wnw_status layout_heads(wnw_ctx *c)
+// Keep counts and static rows of the tidal and fixed heads, once the roles are known: kept
+// positions per segment, static tier rows and tiles (HeadRows).  The complement layout follows
+// from the keep flags (plan_comp).
+wnw_status plan_keep(wnw_ctx *c)
 {
     Geometry &g = c->g;
     const int nsub = g.nT + g.nF;
     c->hrows.assign(nsub, HeadRows{});
     c->head_keep.assign(nsub, 0);
     const int len0 = g.nc ? chunk_len_of(g, 0) : 0, lenl = g.nc ? chunk_len_of(g, g.nc - 1) : 0;
-    int64_t rowT = 0, rowF = 0, tiles = 0, coff = 0;
-    g.comp_max = g.csum_full = g.csum_last = 0;
+    int64_t rowT = 0, rowF = 0, tiles = 0;
     g.keep_sum = 0;
     c->keep_sum_t = 0;
     for (int hi = 0; hi < nsub; ++hi) {
@@ -234,25 +237,48 @@ wnw_status layout_heads(wnw_ctx *c)
         h.srow = (int)(tidal ? rowT : rowF);
         (tidal ? rowT : rowF) += h.rs;
         h.sg = 1;
-        if (tidal) {
-            // the longest segment has the largest complement; the max guards the stride anyway
-            h.cfull = std::max(len0 - k0, lenl - kl);
-            h.clast = lenl - kl;
-            h.coff = (int)coff;
-            coff += 2 * h.cfull;
-            g.csum_full += h.cfull;
-            g.csum_last += h.clast;
-            g.comp_max = std::max(g.comp_max, h.cfull);
-            c->keep_sum_t += keep;
-        }
+        if (tidal) c->keep_sum_t += keep;
         c->head_keep[hi] = keep;
         g.keep_sum += keep;
     }
-    if (rowT > INT32_MAX / 2 || rowF > INT32_MAX / 2 || tiles * g.B > INT32_MAX / 2 || coff * D > INT32_MAX)
-        return fail(c, WNW_ERR_UNSUPPORTED, "static tiers or complement blocks too large");
+    if (rowT > INT32_MAX / 2 || rowF > INT32_MAX / 2 || tiles * g.B > INT32_MAX / 2)
+        return fail(c, WNW_ERR_UNSUPPORTED, "static tiers too large");
     g.RsT = (int)rowT;
     g.RsF = (int)rowF;
     g.n_static = (int)tiles;
+    return WNW_OK;
+}
+
+// Complement layout from the keep flags [B][nT + nF][T_a]: rows of every (sequence, segment,
+// tidal head) complement (comp_rows) and their sum per (sequence, segment) (seg_rows); per
+// tidal head the largest over the batch is its block stride (cfull); block offsets, slot groups
+// and partial entries follow.
+wnw_status plan_comp(wnw_ctx *c, const uint8_t *flags)
+{
+    Geometry &g = c->g;
+    const int nsub = g.nT + g.nF;
+    c->comp_rows.assign((size_t)g.B * g.nc * g.nT, 0);
+    c->seg_rows.assign((size_t)g.B * g.nc, 0);
+    for (int b = 0; b < g.B; ++b)
+        for (int ti = 0; ti < g.nT; ++ti) {
+            const uint8_t *f = flags + ((size_t)b * nsub + ti) * g.Ta;
+            for (int ch = 0; ch < g.nc; ++ch) {
+                const int b0 = ch * g.cl, e0 = b0 + chunk_len_of(g, ch);
+                int n = 0;
+                for (int t = b0; t < e0; ++t) n += f[t] == 0;
+                c->comp_rows[((size_t)b * g.nc + ch) * g.nT + ti] = n;
+                c->seg_rows[(size_t)b * g.nc + ch] += n;
+                c->hrows[ti].cfull = std::max(c->hrows[ti].cfull, n);
+            }
+        }
+    int64_t coff = 0;
+    g.comp_max = 0;
+    for (int ti = 0; ti < g.nT; ++ti) {
+        c->hrows[ti].coff = (int)coff;
+        coff += 2 * c->hrows[ti].cfull;
+        g.comp_max = std::max(g.comp_max, c->hrows[ti].cfull);
+    }
+    if (coff * D > INT32_MAX) return fail(c, WNW_ERR_UNSUPPORTED, "complement blocks too large");
     g.blk_rows = (int)coff;
     g.chunk_elems = coff * D;
     g.slot_tile = g.comp_max <= TILE_S ? TILE_S : 2 * TILE_S;
@@ -281,47 +307,58 @@ wnw_status layout_heads(wnw_ctx *c)
     return WNW_OK;
 }
 
-// Per-segment prefill keep selection of one head (Method, "Prefill Compression"): in segment
-// ch the kfull (klast for the last segment) positions with the highest score, ties to the
-// lower position.  flags[T_a] = 1 for kept positions.
-void keep_flags_host(const Geometry &g, const HeadRows &hr, const float *score, uint8_t *flags)
+// Prefill keep selection of one head on the host (Method, "Prefill Compression"), positions
+// ranked by (score descending, position ascending): per segment, the kfull (klast for the last
+// segment) best; or, globally, the same total over the whole audio.  flags[T_a] = 1 for kept
+// positions.  False if a score is NaN.
+bool keep_flags_host(const Geometry &g, const HeadRows &hr, bool global, const float *score, uint8_t *flags)
 {
+    for (int t = 0; t < g.Ta; ++t)
+        if (std::isnan(score[t])) return false;
+    auto better = [&](int32_t a, int32_t b) {
+        if (score[a] != score[b]) return score[a] > score[b];
+        return a < b;
+    };
     std::vector<int32_t> pos;
+    if (global) {
+        const int keep = g.nc ? (g.nc - 1) * hr.kfull + hr.klast : 0;
+        pos.resize(g.Ta);
+        std::iota(pos.begin(), pos.end(), 0);
+        std::sort(pos.begin(), pos.end(), better);
+        for (int i = 0; i < g.Ta; ++i) flags[pos[i]] = i < keep;
+        return true;
+    }
     for (int ch = 0; ch < g.nc; ++ch) {
         const int b0 = ch * g.cl, len = chunk_len_of(g, ch), kc = ch == g.nc - 1 ? hr.klast : hr.kfull;
         pos.resize(len);
         std::iota(pos.begin(), pos.end(), b0);
-        std::stable_sort(pos.begin(), pos.end(), [&](int32_t a, int32_t b) {
-            if (score[a] != score[b]) return score[a] > score[b];
-            return a < b;
-        });
+        std::sort(pos.begin(), pos.end(), better);
         for (int i = 0; i < len; ++i) flags[pos[i]] = i < kc;
     }
+    return true;
 }
 
 // Kept positions (ascending) and, per segment, the complement (ascending) into
-// comp_by_seg[ch * cfull ..] (tidal heads).  False if the flags do not hold kfull / klast kept
-// positions per segment (the layout was sized for those counts).
-bool rows_from_flags(const Geometry &g, const HeadRows &hr, const uint8_t *flags, std::vector<int32_t> &kept,
-                     std::vector<int32_t> &comp_by_seg)
+// comp_by_seg[ch * cfull ..] (tidal heads; fixed heads drop theirs).  False if the flags do not
+// hold `keep` kept positions or a complement exceeds the stride (the layout was sized for them).
+bool rows_from_flags(const Geometry &g, const HeadRows &hr, int keep, bool tidal, const uint8_t *flags,
+                     std::vector<int32_t> &kept, std::vector<int32_t> &comp_by_seg)
 {
     kept.clear();
     comp_by_seg.assign((size_t)g.nc * hr.cfull, -1);
     for (int ch = 0; ch < g.nc; ++ch) {
-        const int b0 = ch * g.cl, e0 = b0 + chunk_len_of(g, ch), kc = ch == g.nc - 1 ? hr.klast : hr.kfull;
-        int nk = 0, nd = 0;
+        const int b0 = ch * g.cl, e0 = b0 + chunk_len_of(g, ch);
+        int nd = 0;
         for (int t = b0; t < e0; ++t) {
             if (flags[t]) {
                 kept.push_back(t);
-                ++nk;
-            } else if (hr.cfull > 0) {   // fixed heads drop their complement
+            } else if (tidal) {
                 if (nd >= hr.cfull) return false;
                 comp_by_seg[(size_t)ch * hr.cfull + nd++] = t;
             }
         }
-        if (nk != kc) return false;
     }
-    return true;
+    return (int)kept.size() == keep;
 }
 
 void parallel_for(int n, const std::function<void(int)> &fn)
@@ -386,6 +423,7 @@ wnw_status harvest_timing(wnw_ctx *c)
 void free_all(wnw_ctx *c)
 {
     void *ptrs[] = {c->aK, c->aV, c->tK, c->tV, c->fK, c->fV, c->slots, c->d_lk, c->d_tile_head, c->d_hr,
+                    c->d_comp_rows, c->d_seg_rows,
                     c->scores_int, c->sel_int,
                     c->s.pa_m, c->s.pa_l, c->s.pa_o, c->s.pa_mass, c->s.mass, c->s.ps_m, c->s.ps_l, c->s.ps_o,
                     c->s.streak, c->s.slot_of, c->s.slot_last, c->s.att, c->s.slot_data, c->s.slot_busy, c->s.slot_since,
@@ -456,21 +494,22 @@ wnw_status assign_roles(wnw_ctx *c, const uint8_t *roles)
     g.nA = (int)c->anchor_lk.size();
     g.nT = (int)c->tidal_lk.size();
     g.nF = (int)c->fixed_lk.size();
-    return layout_heads(c);
+    return plan_keep(c);
 }
 
-// Allocations and tier construction, from host prefill scores (ranked on the host) or from keep
-// flags [B][nT + nF][T_a] already ranked on the device.
-wnw_status build_tiers(wnw_ctx *c, const float *prefill, const uint8_t *keep_all)
+// Complement layout, allocations and tier construction from the keep flags [B][nT + nF][T_a]
+// (ranked on the host or on the device).
+wnw_status build_tiers(wnw_ctx *c, const uint8_t *keep_all)
 {
     Geometry &g = c->g;
     const int nh = g.L * g.Hkv;
     DeviceGuard dg(c->device);
     hipStream_t st = c->setup_stream;
     const size_t B = g.B, Dz = D;
+    wnw_status r = plan_comp(c, keep_all);
+    if (r != WNW_OK) return r;
 
     // ---- allocations ------------------------------------------------------------------
-    wnw_status r;
 #define ALLOC(p, n, what) \
     if ((r = dalloc(c, &(p), (size_t)(n), what)) != WNW_OK) return r
     ALLOC(c->aK, B * g.nA * g.T * Dz, "anchor K");
@@ -483,6 +522,8 @@ wnw_status build_tiers(wnw_ctx *c, const float *prefill, const uint8_t *keep_all
     ALLOC(c->d_lk, (size_t)nh, "role tables");
     ALLOC(c->d_hr, c->hrows.size(), "head rows");
     ALLOC(c->d_tile_head, (size_t)g.n_static, "static tile table");
+    ALLOC(c->d_comp_rows, c->comp_rows.size(), "complement rows");
+    ALLOC(c->d_seg_rows, c->seg_rows.size(), "segment rows");
     ALLOC(c->scores_int, B * g.nchk, "scores");
     ALLOC(c->sel_int, B * g.k, "selection");
     StepBuffers &s = c->s;
@@ -539,6 +580,12 @@ wnw_status build_tiers(wnw_ctx *c, const float *prefill, const uint8_t *keep_all
         if (!th.empty())
             HIPCHECK(c, hipMemcpy(c->d_tile_head, th.data(), th.size() * sizeof(int32_t), hipMemcpyHostToDevice));
     }
+    if (!c->comp_rows.empty())
+        HIPCHECK(c, hipMemcpy(c->d_comp_rows, c->comp_rows.data(), c->comp_rows.size() * sizeof(int32_t), hipMemcpyHostToDevice));
+    if (!c->seg_rows.empty())
+        HIPCHECK(c, hipMemcpy(c->d_seg_rows, c->seg_rows.data(), c->seg_rows.size() * sizeof(int32_t), hipMemcpyHostToDevice));
+    c->t.comp_rows = c->d_comp_rows;
+    c->s.seg_rows = c->d_seg_rows;
     c->t.hr = c->d_hr;
     c->t.tile_head = c->d_tile_head;
     c->t.anchor_lk = c->d_lk;
@@ -579,24 +626,16 @@ wnw_status build_tiers(wnw_ctx *c, const float *prefill, const uint8_t *keep_all
                 return fail(c, WNW_ERR_HIP, "anchor tier copy failed: %s", hipGetErrorString(e1 != hipSuccess ? e1 : e2));
             }
         }
-        // keep selection (host ranking, or the device's flags), threaded over heads
+        // row lists from the keep flags, threaded over heads
         std::vector<uint8_t> bad(nsub, 0);
         parallel_for(nsub, [&](int hi) {
             const bool tidal = hi < g.nT;
             const int lkh = tidal ? c->tidal_lk[hi] : c->fixed_lk[hi - g.nT];
             const HeadRows &hr = c->hrows[hi];
             const int keep = c->head_keep[hi];
-            std::vector<uint8_t> fl;
-            const uint8_t *flags;
-            if (keep_all) {
-                flags = keep_all + ((size_t)b * nsub + hi) * g.Ta;
-            } else {
-                fl.resize(g.Ta);
-                keep_flags_host(g, hr, prefill + ((size_t)b * nh + lkh) * g.Ta, fl.data());
-                flags = fl.data();
-            }
+            const uint8_t *flags = keep_all + ((size_t)b * nsub + hi) * g.Ta;
             std::vector<int32_t> kept, comp;
-            if (!rows_from_flags(g, hr, flags, kept, comp)) {
+            if (!rows_from_flags(g, hr, keep, tidal, flags, kept, comp)) {
                 bad[hi] = 1;
                 return;
             }
@@ -677,7 +716,19 @@ wnw_status wnw_set_roles(wnw_ctx *c, const uint8_t *roles, const float *prefill)
     if (!roles || !prefill) return fail(c, WNW_ERR_INVALID, "roles and prefill_scores must not be NULL");
     wnw_status r = assign_roles(c, roles);
     if (r != WNW_OK) return r;
-    r = build_tiers(c, prefill, nullptr);
+    const Geometry &g = c->g;
+    const int nsub = g.nT + g.nF, nh = g.L * g.Hkv;
+    const bool global = c->cfg.flags & WNW_F_PREFILL_GLOBAL;
+    std::vector<uint8_t> flags((size_t)g.B * nsub * g.Ta), ok((size_t)g.B * nsub, 1);
+    parallel_for(g.B * nsub, [&](int i) {
+        const int b = i / nsub, hi = i - b * nsub;
+        const int lkh = hi < g.nT ? c->tidal_lk[hi] : c->fixed_lk[hi - g.nT];
+        ok[i] = keep_flags_host(g, c->hrows[hi], global, prefill + ((size_t)b * nh + lkh) * g.Ta,
+                                flags.data() + (size_t)i * g.Ta);
+    });
+    for (size_t i = 0; i < ok.size(); ++i)
+        if (!ok[i]) return fail(c, WNW_ERR_INVALID, "prefill scores of sequence %zu hold NaN", i / nsub);
+    r = build_tiers(c, flags.data());
     if (r != WNW_OK) c->state = FAILED;
     return r;
 }
@@ -709,7 +760,9 @@ wnw_status wnw_set_roles_device(wnw_ctx *c, const uint8_t *roles, const float *p
         hipStream_t st = c->setup_stream;
         if (e == hipSuccess) e = hipMemcpyAsync(d_sub, sub_lk.data(), nsub * sizeof(int32_t), hipMemcpyHostToDevice, st);
         if (e == hipSuccess) e = hipMemcpyAsync(d_sk, sk.data(), nsub * sizeof(int2), hipMemcpyHostToDevice, st);
-        if (e == hipSuccess) e = launch_prefill_keep(g, nsub, d_sub, d_sk, prefill_dev, d_flags, st);
+        if (e == hipSuccess)
+            e = launch_prefill_keep(g, nsub, d_sub, d_sk, (c->cfg.flags & WNW_F_PREFILL_GLOBAL) != 0, prefill_dev, d_flags,
+                                    st);
         if (e == hipSuccess) e = hipMemcpyAsync(flags.data(), d_flags, flags.size(), hipMemcpyDeviceToHost, st);
         if (e == hipSuccess) e = hipStreamSynchronize(st);
         (void)hipFree(d_sub);
@@ -719,8 +772,11 @@ wnw_status wnw_set_roles_device(wnw_ctx *c, const uint8_t *roles, const float *p
             c->state = FAILED;
             return fail(c, WNW_ERR_HIP, "device keep selection failed: %s", hipGetErrorString(e));
         }
+        // the ranking marks a NaN score with 2
+        for (size_t i = 0; i < flags.size(); ++i)
+            if (flags[i] > 1) return fail(c, WNW_ERR_INVALID, "prefill scores of sequence %zu hold NaN", i / ((size_t)nsub * g.Ta));
     }
-    r = build_tiers(c, nullptr, flags.data());
+    r = build_tiers(c, flags.data());
     if (r != WNW_OK) c->state = FAILED;
     return r;
 }

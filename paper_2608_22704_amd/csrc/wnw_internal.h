@@ -37,7 +37,6 @@ struct Geometry {
     int P, np_max;              // partial entries of one sequence; most of one head
     int comp_max;               // largest complement of one segment of one tidal head
     int blk_rows;               // rows of one segment's complement block (every tidal head, K and V)
-    int csum_full, csum_last;   // complement rows of a full / the last segment over all tidal heads
     int64_t keep_sum;           // kept audio rows over all non-anchor heads
     int slot_tile;              // rows of one slot-group work-group (TILE_S or 2 * TILE_S)
     int ng_kept;                // kept-slot groups of the head with the most
@@ -54,8 +53,7 @@ struct HeadRows {
     int tile0;   // first static tile of the head among its sequence's static tiles
     int pbase;   // first partial entry of the head among its sequence's partials
     // tidal heads (0 for fixed heads)
-    int cfull;   // complement rows of a full segment (the longest one)
-    int clast;   // complement rows of the last segment
+    int cfull;   // block stride: the head's largest complement of one segment over the batch
     int coff;    // first row of the head in a segment's complement block: cfull K rows, cfull V rows
     int sg;      // kept slots per slot-group work-group (>= 1)
     int ngk;     // kept-slot groups
@@ -83,6 +81,7 @@ struct Tiers {
     const int32_t *anchor_lk, *tidal_lk, *fixed_lk;  // l * Hkv + kv of each role's heads
     const HeadRows *hr;         // [nT + nF]
     const int32_t *tile_head;   // [n_static] head of each static tile of a sequence
+    const int32_t *comp_rows;   // [B][nc][nT] complement rows of each (sequence, segment, tidal head)
 };
 
 struct StepBuffers {
@@ -107,6 +106,7 @@ struct StepBuffers {
     int32_t *new_list;          // [B][knew][2]    (segment, slot) newly resident this step
     int32_t *counts;            // [B][2] kept, new
     unsigned long long *stats;  // [8] recalled, dropped, resident, slot_rows, peak, exhausted, revived
+    const int32_t *seg_rows;    // [B][nc] complement rows of a segment over the tidal heads
 };
 
 // Launchers (wnw_kernels.hip).  Each returns the launch status.  Where a launcher takes two
@@ -146,7 +146,9 @@ hipError_t launch_prefill_scores(const Geometry &g, const uint16_t *K, const uin
                                  float *p, hipStream_t st);
 // Per-segment keep flags [B][n_sub][Ta] of the non-anchor heads sub_lk[n_sub] (l * Hkv + kv),
 // keeping seg_keep[h].x positions of a full segment and .y of the last one.
-hipError_t launch_prefill_keep(const Geometry &g, int n_sub, const int32_t *sub_lk, const int2 *seg_keep,
+// With `global`, the same total is ranked over the whole audio of the head instead.  A NaN
+// score is marked 2.
+hipError_t launch_prefill_keep(const Geometry &g, int n_sub, const int32_t *sub_lk, const int2 *seg_keep, bool global,
                                const float *p, uint8_t *keep, hipStream_t st);
 // Set-up: dst[i] = row idx[i] of src_k (idx >= 0), row -idx[i]-2 of src_v (idx <= -2), or zeros
 // (idx == -1); a row is D bf16.

@@ -640,7 +640,7 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
         fkept[u] = nxt ? owned : (now && owned);
         const bool att = nxt ? owned : now;
         g_att[u] = att;
-        if (att) atomicAdd(&nrows, u == nu - 1 ? g.csum_last : g.csum_full);
+        if (att) atomicAdd(&nrows, s.seg_rows[(size_t)b * nu + u]);
         if (fdrop[u]) {
             busy[sof[u]] = nxt ? 2 : 0;
             since[sof[u]] = step;
@@ -1066,7 +1066,7 @@ __device__ inline void slot_group(const Geometry &g, const Tiers &t, const StepB
     for (int e = threadIdx.x; e < n_entries; e += NT) {
         const int c = list[e * 2], slot = list[e * 2 + 1];
         kbase[e] = t.slots + ((size_t)b * g.n_slots + slot) * g.chunk_elems + (size_t)hr.coff * D;
-        nrows[e] = c == g.nc - 1 ? hr.clast : hr.cfull;
+        nrows[e] = t.comp_rows[((size_t)b * g.nc + c) * g.nT + ti];
     }
     __syncthreads();
     const int lk = t.tidal_lk[ti], l = lk / g.Hkv, kv = lk - l * g.Hkv;
@@ -1095,7 +1095,7 @@ __device__ inline void recall_units(const Geometry &g, const Tiers &t, const Ste
         const size_t off = (size_t)hr.coff * D;
         const uint16_t *src = t.host_comp + ((size_t)b * g.nc + c) * g.chunk_elems + off;
         uint16_t *dst = t.slots + ((size_t)b * g.n_slots + slot) * g.chunk_elems + off;
-        const int cm = hr.cfull, nr = c == g.nc - 1 ? hr.clast : cm;
+        const int cm = hr.cfull, nr = t.comp_rows[((size_t)b * g.nc + c) * g.nT + ti];
         // rows past the segment's complement (short last segment) are zero padding: copied for a
         // byte-identical slot, not attended
         for (int j = threadIdx.x; j < (cm - nr) * 2 * (D / 8); j += NT) {

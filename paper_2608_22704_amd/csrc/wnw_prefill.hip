@@ -1,5 +1,6 @@
 // Prefill compression on the device (Method, "Prefill Compression"): the text-to-audio attention
-// sums that rank a head's audio positions, and the per-segment keep selection from them.
+// sums that rank a head's audio positions, and the keep selection from them (per segment, or
+// over the whole audio of a head for the global variant).
 //
 // p[b][l][kv][tau] = sum over the text tokens t and the g q-heads of KV-head kv of the softmax
 // weight that text token t puts on audio position tau; text token t attends to every audio row
@@ -297,7 +298,83 @@ __global__ __launch_bounds__(NT) void prefill_keep_kernel(Geometry g, const int3
             const float w = ph[u];
             rank += (w > v) || (w == v && u < tau);
         }
-        kh[tau] = rank < k;
+        kh[tau] = isnan(v) ? 2 : rank < k;
+    }
+}
+
+// Order-preserving key of a score: larger score, larger key; -0 and +0 are one key (they compare
+// equal, so they tie and the lower position wins, as in the per-segment ranking).
+__device__ inline uint32_t score_key(float v)
+{
+    uint32_t u = __float_as_uint(v);
+    if (u == 0x80000000u) u = 0;
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Global variant: one work-group per non-anchor head keeps the total of its per-segment counts,
+// ranked over the whole audio.  A radix selection (four 8-bit digits, most significant first)
+// finds the key v of the k-th best score and how many positions holding exactly v are kept;
+// those go to the lowest positions (a block-wide prefix count in position order).
+__global__ __launch_bounds__(NT) void prefill_keep_global_kernel(Geometry g, const int32_t *__restrict__ sub_lk,
+                                                                const int2 *__restrict__ seg_keep,
+                                                                const float *__restrict__ p, uint8_t *__restrict__ keep)
+{
+    const int hi = blockIdx.x, b = blockIdx.y, nsub = gridDim.x, tid = threadIdx.x;
+    const int2 kc = seg_keep[hi];
+    const int total = g.nc ? (g.nc - 1) * kc.x + kc.y : 0;
+    const float *ph = p + ((size_t)b * g.L * g.Hkv + sub_lk[hi]) * g.Ta;
+    uint8_t *kh = keep + ((size_t)b * nsub + hi) * g.Ta;
+    __shared__ int hist[256];
+    __shared__ uint32_t s_prefix;
+    __shared__ int s_need, s_scan[NT];
+    uint32_t prefix = 0, mask = 0;
+    int need = total;
+    if (total > 0) {
+        for (int shift = 24; shift >= 0; shift -= 8) {
+            hist[tid] = 0;   // NT == 256 bins
+            __syncthreads();
+            for (int t = tid; t < g.Ta; t += NT) {
+                const uint32_t key = score_key(ph[t]);
+                if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255], 1);
+            }
+            __syncthreads();
+            if (tid == 0) {
+                int cum = 0, d = 255;
+                for (; d > 0; --d) {
+                    if (cum + hist[d] >= need) break;
+                    cum += hist[d];
+                }
+                s_prefix = prefix | ((uint32_t)d << shift);
+                s_need = need - cum;
+            }
+            __syncthreads();
+            prefix = s_prefix;
+            need = s_need;
+            mask |= 255u << shift;
+            __syncthreads();
+        }
+    }
+    // keep: key > v, or key == v among the first `need` such positions
+    int base = 0;
+    for (int t0 = 0; t0 < g.Ta; t0 += NT) {
+        const int t = t0 + tid;
+        const float v = t < g.Ta ? ph[t] : 0.f;
+        const uint32_t key = score_key(v);
+        const int tie = (total > 0 && t < g.Ta && key == prefix) ? 1 : 0;
+        s_scan[tid] = tie;
+        __syncthreads();
+        for (int o = 1; o < NT; o <<= 1) {   // inclusive prefix sum
+            const int add = tid >= o ? s_scan[tid - o] : 0;
+            __syncthreads();
+            s_scan[tid] += add;
+            __syncthreads();
+        }
+        if (t < g.Ta) {
+            const int before = base + s_scan[tid] - tie;
+            kh[t] = isnan(v) ? 2 : (total > 0 && (key > prefix || (tie && before < need)));
+        }
+        base += s_scan[NT - 1];
+        __syncthreads();
     }
 }
 
@@ -320,11 +397,14 @@ hipError_t launch_prefill_scores(const Geometry &g, const uint16_t *K, const uin
     return hipGetLastError();
 }
 
-hipError_t launch_prefill_keep(const Geometry &g, int n_sub, const int32_t *sub_lk, const int2 *seg_keep,
+hipError_t launch_prefill_keep(const Geometry &g, int n_sub, const int32_t *sub_lk, const int2 *seg_keep, bool global,
                                const float *p, uint8_t *keep, hipStream_t st)
 {
     if (n_sub == 0 || g.Ta == 0) return hipSuccess;
-    hipLaunchKernelGGL(prefill_keep_kernel, dim3(n_sub, g.B), dim3(NT), 0, st, g, sub_lk, seg_keep, p, keep);
+    if (global)
+        hipLaunchKernelGGL(prefill_keep_global_kernel, dim3(n_sub, g.B), dim3(NT), 0, st, g, sub_lk, seg_keep, p, keep);
+    else
+        hipLaunchKernelGGL(prefill_keep_kernel, dim3(n_sub, g.B), dim3(NT), 0, st, g, sub_lk, seg_keep, p, keep);
     return hipGetLastError();
 }
 

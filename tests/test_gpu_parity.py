@@ -581,9 +581,10 @@ def test_prefill_device_with_overlap_and_retention():
     _run(w, prefill_device=True, importance=_imp(w, 408, ((0, 1),), ((1, 2),)), lam=1.0, flags=_next())
 
 
-def test_prefill_device_ranking_equals_host_ranking():
+@pytest.mark.parametrize("glob", [False, True], ids=["per_segment", "global"])
+def test_prefill_device_ranking_equals_host_ranking(glob):
     """The same fp32 scores through wnw_set_roles_device and wnw_set_roles give byte-identical
-    host complements and bitwise identical steps."""
+    host complements and bitwise identical steps (ties, -0 and +0 included)."""
     import torch
     from paper_2608_22704_amd import wnw as W
     from tests.wnw_harness import log, to_dev
@@ -599,9 +600,11 @@ def test_prefill_device_ranking_equals_host_ranking():
         vd[b].copy_(to_dev(seq["v"]))
         qs.append(seq["q"])
     rng = np.random.default_rng(7)
-    sc = (rng.integers(0, 50, size=(B, L, H, w.audio_len)) / 50.0).astype(np.float32)   # many ties
+    sc = (rng.integers(-25, 25, size=(B, L, H, w.audio_len)) / 50.0).astype(np.float32)   # many ties
+    sc[rng.random(sc.shape) < 0.05] = -0.0
     roles = gen.roles(w)
-    cfg = W.make_config(B, L, w.q_heads, H, w.audio_len, w.text_len, w.chunk_len, w.budget_bp)
+    cfg = W.make_config(B, L, w.q_heads, H, w.audio_len, w.text_len, w.chunk_len, w.budget_bp,
+                        flags=W.WNW_F_PREFILL_GLOBAL if glob else 0)
     ctxs = [W.wnw_init_cache(cfg, kd, vd), W.wnw_init_cache(cfg, kd, vd)]
     try:
         W.wnw_set_roles(ctxs[0], roles, sc)
@@ -657,3 +660,33 @@ def test_prefill_scores_voxtral_full_size_sampled():
         rel = np.abs(got[l, kv] - ref) / np.maximum(ref, 1e-300)
         log(f"[prefill] head ({l},{kv}): max rel err {rel.max():.3g}")
         assert (rel <= PREFILL_RTOL).all()
+
+
+# ---- global prefill variant: the per-segment total kept over the whole audio of a head (ablation
+# of per-segment selection); complements then differ in size from segment to segment.
+
+def _glob(extra=0):
+    from paper_2608_22704_amd import wnw as W
+    return W.WNW_F_PREFILL_GLOBAL | extra
+
+
+GLOB = [
+    _small("glob_g2", 501, Tt=9),
+    _small("glob_g1_chunk7", 502, Hq=4, Hkv=4, cl=7),
+    _small("glob_g8_chunk256", 503, Hq=16, Hkv=2, cl=256, Ta=1300, Tt=300),
+    _small("glob_batch3", 504, B=3, Ta=777, Tt=1, cl=37, budget=3000, steps=9),
+    _small("glob_low_budget", 505, Ta=600, cl=16, budget=500, steps=8),
+]
+
+
+@pytest.mark.parametrize("w", GLOB, ids=[w.name for w in GLOB])
+def test_prefill_global_lockstep(w):
+    _run(w, flags=_glob())
+    _run(w, flags=_glob(_next()))
+
+
+def test_prefill_global_device_scores_and_variants():
+    w = _small("glob_dev", 506, L=2, Hq=8, Hkv=4, Ta=480, Tt=33, cl=32, steps=6)
+    _run(w, prefill_device=True, flags=_glob(_next()))
+    _run(w, prefill_device=True, flags=_glob(_ovl()))
+    _run(w, flags=_glob(_next()), importance=_imp(w, 506, ((0, 1),), ((1, 2),)), lam=1.0)

@@ -62,7 +62,7 @@ def check_selection(gpu_sel: np.ndarray, oracle_scores: np.ndarray, k: int) -> i
     return len(diff) // 2
 
 
-def check_prefill(w, seg, seqs, host, gpu_scores, roles, importance, lam) -> float:
+def check_prefill(w, seg, seqs, host, gpu_scores, roles, importance, lam, global_=False) -> float:
     """Device prefill scores against the oracle's (double), relative per entry; the keep sets
     that the fp32 scores give (per-segment ranking, the library's rule) must be those of the
     double scores except at positions whose score lies within PREFILL_RTOL of the segment's
@@ -80,13 +80,16 @@ def check_prefill(w, seg, seqs, host, gpu_scores, roles, importance, lam) -> flo
             for kv in range(H):
                 if roles[l, kv] == 0:
                     continue
-                for c0 in range(0, Ta, seg):
-                    e0 = min(c0 + seg, Ta)
-                    n = e0 - c0
+                def count(n):
                     if importance is None:
-                        kc = (w.budget_bp * n) // 10000
-                    else:
-                        kc = int(np.floor(min(float(importance[l, kv]) * float(np.float32(lam)), 1.0) * n))
+                        return (w.budget_bp * n) // 10000
+                    return int(np.floor(min(float(importance[l, kv]) * float(np.float32(lam)), 1.0) * n))
+                segs = [(c0, min(c0 + seg, Ta)) for c0 in range(0, Ta, seg)]
+                # the global variant ranks the per-segment total over the whole audio
+                groups = [(0, Ta, sum(count(e - a) for a, e in segs))] if global_ else \
+                    [(a, e, count(e - a)) for a, e in segs]
+                for c0, e0, kc in groups:
+                    n = e0 - c0
                     if kc in (0, n):
                         continue
                     r, gsc = ref[l, kv, c0:e0], gpu_scores[b, l, kv, c0:e0]
@@ -152,7 +155,8 @@ class Lockstep:
             torch.cuda.synchronize()
             self.prefill = sc.cpu().numpy()
             seg = w.chunk_len // 2 if flags & W.WNW_F_OVERLAP_CHUNKS else w.chunk_len
-            self.prefill_err = check_prefill(w, seg, self.seqs, host, self.prefill, self.roles, importance, lam)
+            self.prefill_err = check_prefill(w, seg, self.seqs, host, self.prefill, self.roles, importance, lam,
+                                             bool(flags & W.WNW_F_PREFILL_GLOBAL))
             W.wnw_set_roles_device(self.ctx, self.roles, sc)
             del qt, sc
         else:
@@ -163,7 +167,7 @@ class Lockstep:
         self.next_step = 1 if flags & W.WNW_F_SELECT_NEXT_STEP else 0
         span = 2 if flags & W.WNW_F_OVERLAP_CHUNKS else 1
         ocfg = O.cfg_from_workload(w, batch=len(self.seqs), top_k=top_k, next_step=self.next_step,
-                                   chunk_span=span)
+                                   chunk_span=span, prefill_global=1 if flags & W.WNW_F_PREFILL_GLOBAL else 0)
         self.ok_ = np.stack([host[b]["k"] for b in self.seqs])
         self.ov_ = np.stack([host[b]["v"] for b in self.seqs])
         self.oracle = O.Oracle(ocfg, self.ok_, self.ov_, self.roles, self.prefill[self.seqs], importance=importance,
