@@ -30,7 +30,7 @@ def build(verbose: bool = False) -> str:
 class _Cfg(C.Structure):
     _fields_ = [(n, C.c_int32) for n in (
         "batch", "layers", "q_heads", "kv_heads", "head_dim", "audio_len", "text_len",
-        "chunk_len", "budget_bp", "top_k", "evict_lag", "next_step", "chunk_span", "prefill_global")]
+        "chunk_len", "budget_bp", "top_k", "evict_lag", "next_step", "chunk_span", "prefill_global", "max_new")]
 
 
 _lib = None
@@ -58,6 +58,7 @@ def lib():
         L.wnwo_tokens_for_window.restype = C.c_int32
         L.wnwo_segments.argtypes = [C.POINTER(_Cfg), C.POINTER(C.c_int32)]
         L.wnwo_prefill_scores.argtypes = [C.POINTER(_Cfg), P, P, P]
+        L.wnwo_append.argtypes = [P, P, P]
         L.wnwo_set_threads.argtypes = [C.c_int]
         L.wnwo_set_threads.restype = C.c_int
         _lib = L
@@ -69,9 +70,9 @@ def _ptr(a):
 
 
 def make_cfg(batch, layers, q_heads, kv_heads, head_dim, audio_len, text_len, chunk_len,
-             budget_bp, top_k=0, evict_lag=0, next_step=0, chunk_span=1, prefill_global=0) -> _Cfg:
+             budget_bp, top_k=0, evict_lag=0, next_step=0, chunk_span=1, prefill_global=0, max_new=0) -> _Cfg:
     return _Cfg(batch, layers, q_heads, kv_heads, head_dim, audio_len, text_len, chunk_len,
-                budget_bp, top_k, evict_lag, next_step, chunk_span, prefill_global)
+                budget_bp, top_k, evict_lag, next_step, chunk_span, prefill_global, max_new)
 
 
 def cfg_from_workload(w, batch=None, **over) -> _Cfg:
@@ -166,6 +167,15 @@ class Oracle:
         if lib().wnwo_keep_mask(self._h, b, l, kv, _ptr(m)):
             raise ValueError("bad head index")
         return m
+
+    def append(self, k_new, v_new):
+        """K, V rows [B][L][H_kv][d] (uint16 bf16) of the token generated at this step."""
+        c = self.cfg
+        k = np.ascontiguousarray(k_new, dtype=np.uint16)
+        v = np.ascontiguousarray(v_new, dtype=np.uint16)
+        assert k.shape == (c.batch, c.layers, c.kv_heads, c.head_dim) and v.shape == k.shape
+        if lib().wnwo_append(self._h, _ptr(k), _ptr(v)):
+            raise ValueError("wnwo_append failed (more than max_new tokens?)")
 
     def step(self, q, forced=None, head_mask=None):
         c = self.cfg

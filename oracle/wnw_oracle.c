@@ -52,7 +52,9 @@
 struct wnwo {
     wnwo_config c;
     int32_t n_chunks, n_seg, span, k, keep_total, delta;
+    int32_t n_gen, tcap;   /* tokens appended so far; rows per head in kc / vc          */
     const uint16_t *kc, *vc;
+    uint16_t *kown, *vown; /* the oracle's copy of the cache when tokens may be appended */
     uint8_t *roles;        /* [L][Hkv]                                               */
     uint8_t *keep;         /* [B][L][Hkv][T_a] prefill keep flags of non-anchor heads */
     int32_t *streak;       /* [B][n_chunks] steps since last selection, capped at delta */
@@ -120,7 +122,7 @@ int wnwo_geometry(const wnwo_config *c, int32_t *n_chunks, int32_t *k, int32_t *
     if (!c || c->batch < 1 || c->layers < 1 || c->kv_heads < 1 || c->head_dim < 1 ||
         c->q_heads < c->kv_heads || c->q_heads % c->kv_heads || c->audio_len < 0 ||
         c->text_len < 0 || c->chunk_len < 1 || c->budget_bp < 0 || c->budget_bp > 10000 ||
-        c->top_k < 0 || c->evict_lag < 0 || c->chunk_span < 0 || c->chunk_span > 2 ||
+        c->top_k < 0 || c->evict_lag < 0 || c->chunk_span < 0 || c->chunk_span > 2 || c->max_new < 0 ||
         (c->chunk_span == 2 && c->chunk_len % 2))
         return -1;
     int32_t nc = chunk_count(c), ns = seg_count(c);
@@ -209,6 +211,7 @@ wnwo *wnwo_create_retention(const wnwo_config *cfg, const uint16_t *k, const uin
     o->delta = cfg->evict_lag ? cfg->evict_lag : 3;
     o->kc = k;
     o->vc = v;
+    o->tcap = cfg->audio_len + cfg->text_len;
     size_t nh = (size_t)cfg->layers * cfg->kv_heads, B = (size_t)cfg->batch;
     o->roles = malloc(nh);
     o->keep = malloc(B * nh * (size_t)(cfg->audio_len ? cfg->audio_len : 1));
@@ -221,6 +224,25 @@ wnwo *wnwo_create_retention(const wnwo_config *cfg, const uint16_t *k, const uin
         return NULL;
     }
     memcpy(o->roles, roles, nh);
+    if (cfg->max_new > 0) {
+        /* room for max_new appended rows after each head's prompt rows */
+        const int32_t T = cfg->audio_len + cfg->text_len, D = cfg->head_dim;
+        o->tcap = T + cfg->max_new;
+        size_t n = B * nh * (size_t)o->tcap * D;
+        o->kown = calloc(n, sizeof(uint16_t));
+        o->vown = calloc(n, sizeof(uint16_t));
+        if (!o->kown || !o->vown) {
+            free(tmp);
+            wnwo_destroy(o);
+            return NULL;
+        }
+        for (size_t i = 0; i < B * nh; ++i) {
+            memcpy(o->kown + i * o->tcap * D, k + i * T * D, (size_t)T * D * sizeof(uint16_t));
+            memcpy(o->vown + i * o->tcap * D, v + i * T * D, (size_t)T * D * sizeof(uint16_t));
+        }
+        o->kc = o->kown;
+        o->vc = o->vown;
+    }
     for (size_t b = 0; b < B; ++b)
         for (size_t h = 0; h < nh; ++h) {
             uint8_t *kp = o->keep + (b * nh + h) * (size_t)cfg->audio_len;
@@ -243,6 +265,8 @@ void wnwo_destroy(wnwo *o)
     free(o->keep);
     free(o->streak);
     free(o->res_prev);
+    free(o->kown);
+    free(o->vown);
     free(o);
 }
 
@@ -347,6 +371,25 @@ int wnwo_prefill_scores(const wnwo_config *c, const uint16_t *k, const uint16_t 
     return 0;
 }
 
+/* ---- decode-time append ----------------------------------------------------------------------- */
+
+/* The K and V rows of the token generated at this step, k_new / v_new [B][L][H_kv][d], join every
+ * head's key set after the prompt text; generated tokens are not audio, so every role keeps them
+ * in full (the remark under Eq. 1). */
+int wnwo_append(wnwo *o, const uint16_t *k_new, const uint16_t *v_new)
+{
+    if (!o || !k_new || !v_new || o->n_gen >= o->c.max_new) return -1;
+    const wnwo_config *c = &o->c;
+    const size_t nh = (size_t)c->layers * c->kv_heads, D = (size_t)c->head_dim;
+    const size_t row = (size_t)c->audio_len + c->text_len + o->n_gen;
+    for (size_t i = 0; i < (size_t)c->batch * nh; ++i) {
+        memcpy(o->kown + (i * o->tcap + row) * D, k_new + i * D, D * sizeof(uint16_t));
+        memcpy(o->vown + (i * o->tcap + row) * D, v_new + i * D, D * sizeof(uint16_t));
+    }
+    o->n_gen++;
+    return 0;
+}
+
 /* ---- one decode step -------------------------------------------------------------------------- */
 
 int wnwo_step(wnwo *o, const uint16_t *q, const int32_t *forced, const uint8_t *head_mask,
@@ -355,8 +398,11 @@ int wnwo_step(wnwo *o, const uint16_t *q, const int32_t *forced, const uint8_t *
     if (!o || !q || !out || !scores || (o->k && !selected)) return -1;
     const wnwo_config *c = &o->c;
     const int32_t L = c->layers, H = c->kv_heads, Hq = c->q_heads, g = Hq / H, D = c->head_dim;
-    const int32_t Ta = c->audio_len, T = Ta + c->text_len, nc = o->n_chunks, ns = o->n_seg, k = o->k, B = c->batch;
-    const size_t nh = (size_t)L * H;
+    /* rows of every key set: audio, prompt text, then the tokens appended so far (kept in full
+     * by every head, like text); a head's rows sit at stride tcap */
+    const int32_t Ta = c->audio_len, T = Ta + c->text_len + o->n_gen, nc = o->n_chunks, ns = o->n_seg, k = o->k,
+                  B = c->batch;
+    const size_t nh = (size_t)L * H, TS = (size_t)o->tcap;
 
     int32_t n_anchor = 0;
     for (size_t h = 0; h < nh; ++h) n_anchor += o->roles[h] == 0;
@@ -392,7 +438,7 @@ int wnwo_step(wnwo *o, const uint16_t *q, const int32_t *forced, const uint8_t *
                 continue;
             }
             for (int32_t t = 0; t < T; ++t) rows[t] = t;
-            size_t hoff = (((size_t)b * L + l) * H + kv) * (size_t)T * D;
+            size_t hoff = (((size_t)b * L + l) * H + kv) * TS * D;
             for (int32_t j = 0; j < g; ++j) {
                 int32_t hq = kv * g + j;
                 const uint16_t *qh = q + (((size_t)b * L + l) * Hq + hq) * D;
@@ -481,7 +527,7 @@ int wnwo_step(wnwo *o, const uint16_t *q, const int32_t *forced, const uint8_t *
                 if (kp[t] || (o->roles[hh] == 1 && ru[sg])) rows[n++] = t;
             }
             for (int32_t t = Ta; t < T; ++t) rows[n++] = t;
-            size_t hoff = (((size_t)b * L + l) * H + kv) * (size_t)T * D;
+            size_t hoff = (((size_t)b * L + l) * H + kv) * TS * D;
             for (int32_t j = 0; j < g; ++j) {
                 int32_t hq = kv * g + j;
                 attend(q + (((size_t)b * L + l) * Hq + hq) * D, o->kc + hoff, o->vc + hoff, rows, n, D, x,

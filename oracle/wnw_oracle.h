@@ -32,6 +32,8 @@ typedef struct {
                                       of chunk_len / 2 positions, one chunk per segment start  */
     int32_t prefill_global;        /* 1: prefill keeps the same number of positions, ranked over
                                       the whole audio of a head instead of per segment          */
+    int32_t max_new;               /* tokens that wnwo_append may add (0: none; the oracle then
+                                      references the caller's cache, else it keeps a copy)     */
 } wnwo_config;
 
 typedef struct wnwo wnwo;
@@ -64,6 +66,11 @@ int wnwo_keep_mask(const wnwo *o, int32_t b, int32_t l, int32_t kv, uint8_t *mas
  *   k       [B][L][H_kv][T_a+T_t][d] bf16
  *   q_text  [B][L][H_q][T_t][d] bf16, the text tokens' queries at prefill */
 int wnwo_prefill_scores(const wnwo_config *cfg, const uint16_t *k, const uint16_t *q_text, double *p);
+
+/* Append the K and V rows [B][L][H_kv][d] bf16 of the token generated at this step: from the
+ * next wnwo_step on they are part of every head's key set, after the text rows.  At most
+ * max_new times. */
+int wnwo_append(wnwo *o, const uint16_t *k_new, const uint16_t *v_new);
 
 /* One decode step.
  *   q         [B][L][H_q][d] bf16

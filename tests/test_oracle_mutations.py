@@ -50,6 +50,11 @@ MUTANTS = {
     "prefill scores from the first q-head only": (
         "        for (int32_t j = 0; j < g; ++j)\n            for (int32_t t = 0; t < Tt; ++t) {",
         "        for (int32_t j = 0; j < 1; ++j)\n            for (int32_t t = 0; t < Tt; ++t) {"),
+    "tidal and fixed heads miss the appended rows": (
+        "for (int32_t t = Ta; t < T; ++t) rows[n++] = t;", "for (int32_t t = Ta; t < Ta + c->text_len; ++t) rows[n++] = t;"),
+    "append overwrites the last prompt row": (
+        "const size_t row = (size_t)c->audio_len + c->text_len + o->n_gen;",
+        "const size_t row = (size_t)c->audio_len + c->text_len + o->n_gen - 1;"),
     "global prefill keeps the last segment's count": (
         "for (int32_t j = 0; j < ns; ++j) total += keep_count_head(",
         "for (int32_t j = 0; j < ns; ++j) total = keep_count_head("),

@@ -539,3 +539,71 @@ def test_prefill_global_keep_is_brute_force_top(oracle_mod):
     s = oracle_mod.Oracle(oracle_mod.make_cfg(1, 1, 3, 3, 8, 14, 2, 16, 4000), k1, v1, roles, pf1)
     for h in range(3):
         assert np.array_equal(a.keep_mask(0, 0, h), s.keep_mask(0, 0, h))
+
+
+# ---- decode-time append: generated tokens join every head's key set, kept in full like text
+
+def test_append_equals_extra_text_rows(oracle_mod):
+    """Appending a token's K/V rows is the same as having them as trailing text rows: after one
+    append the step equals a fresh oracle with one more text row; after a second append (and
+    the same selection history) it equals one with two more, bit for bit."""
+    rng = np.random.default_rng(61)
+    B, L, H, g, D, Ta, Tt, cl = 2, 2, 3, 2, 8, 64, 4, 8
+    roles = np.array([[0, 1, 2], [1, 2, 0]], dtype=np.uint8)
+    k, v = _rand_cache(rng, B, L, H, Ta + Tt + 2, D)
+    pf = rng.random((B, L, H, Ta), dtype=np.float32)
+    q1, q2 = (f32_to_bf16(rng.standard_normal((B, L, H * g, D)).astype(np.float32)) for _ in range(2))
+    mk = lambda tt, mx: oracle_mod.make_cfg(B, L, H * g, H, D, Ta, tt, cl, 2500, max_new=mx)
+    a = oracle_mod.Oracle(mk(Tt, 2), k[:, :, :, : Ta + Tt], v[:, :, :, : Ta + Tt], roles, pf)
+    a.append(k[:, :, :, Ta + Tt], v[:, :, :, Ta + Tt])
+    ra1 = a.step(q1)
+    b1 = oracle_mod.Oracle(mk(Tt + 1, 0), k[:, :, :, : Ta + Tt + 1], v[:, :, :, : Ta + Tt + 1], roles, pf)
+    rb1 = b1.step(q1)
+    for key in ("out", "scores", "selected", "resident"):
+        assert np.array_equal(ra1[key], rb1[key]), key
+    a.append(k[:, :, :, Ta + Tt + 1], v[:, :, :, Ta + Tt + 1])
+    ra2 = a.step(q2)
+    b2 = oracle_mod.Oracle(mk(Tt + 2, 0), k, v, roles, pf)
+    b2.step(q1, forced=ra1["selected"])
+    rb2 = b2.step(q2)
+    for key in ("out", "scores", "selected", "resident"):
+        assert np.array_equal(ra2[key], rb2[key]), key
+    with pytest.raises(ValueError):
+        a.append(k[:, :, :, 0], v[:, :, :, 0])
+
+
+def test_appended_rows_in_every_key_set(oracle_mod):
+    """After appends every head attends over its key set plus the appended rows (SDPA with the
+    mask), and a dominant appended key takes a head's whole weight."""
+    rng = np.random.default_rng(63)
+    B, L, H, g, D, Ta, Tt, cl = 2, 2, 3, 2, 16, 64, 4, 8
+    roles = np.array([[0, 1, 2], [1, 2, 0]], dtype=np.uint8)
+    k, v = _rand_cache(rng, B, L, H, Ta + Tt, D)
+    pf = rng.random((B, L, H, Ta), dtype=np.float32)
+    o = oracle_mod.Oracle(oracle_mod.make_cfg(B, L, H * g, H, D, Ta, Tt, cl, 2500, max_new=3), k, v, roles, pf)
+    kn, vn = [], []
+    for step in range(3):
+        q = f32_to_bf16(rng.standard_normal((B, L, H * g, D)).astype(np.float32))
+        kk = f32_to_bf16(rng.standard_normal((B, L, H, D)).astype(np.float32))
+        if step == 2:
+            kk = f32_to_bf16(bf16_to_f32(q[:, :, ::g]) * 40.0)   # aligned with q-head 0 of each KV-head
+        vv = f32_to_bf16(rng.standard_normal((B, L, H, D)).astype(np.float32))
+        kn.append(kk)
+        vn.append(vv)
+        o.append(kk, vv)
+        r = o.step(q)
+        K = np.concatenate([k, np.stack(kn, axis=3)], axis=3)
+        V = np.concatenate([v, np.stack(vn, axis=3)], axis=3)
+        T = Ta + Tt + step + 1
+        for b, l, hq in itertools.product(range(B), range(L), range(H * g)):
+            h = hq // g
+            mask = np.ones(T, dtype=bool)
+            if roles[l, h] != 0:
+                keep = o.keep_mask(b, l, h).astype(bool)
+                if roles[l, h] == 1:
+                    keep |= np.repeat(r["resident"][b].astype(bool), cl)[:Ta]
+                mask[:Ta] = keep
+            ref = _sdpa(q[b, l, hq], K[b, l, h], V[b, l, h], mask)
+            np.testing.assert_allclose(r["out"][b, l, hq], ref, rtol=0, atol=1e-12)
+            if step == 2 and hq % g == 0:
+                np.testing.assert_allclose(r["out"][b, l, hq], bf16_to_f32(vv[b, l, h]), rtol=0, atol=1e-6)
