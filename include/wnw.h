@@ -107,6 +107,8 @@ typedef struct {
     int32_t top_k;        /* chunks selected per step; 0 = budget-derived            */
     int32_t evict_lag;    /* delta >= 1; 0 = 3                                       */
     uint32_t flags;       /* WNW_F_* bits                                            */
+    int32_t max_new_tokens; /* generated tokens wnw_append_kv may add, >= 0 (device rows
+                               are reserved for them in every head at set-up)           */
 } wnw_config;
 
 typedef struct {
@@ -191,6 +193,15 @@ wnw_status wnw_prefill_scores(wnw_ctx *ctx, const void *q_text_dev, float *score
  * its keep flags.  The same scores give the same tiers as wnw_set_roles.  On failure (or a
  * failure of wnw_set_roles) the context is in the error state and can only be destroyed. */
 wnw_status wnw_set_roles_device(wnw_ctx *ctx, const uint8_t *roles, const float *prefill_scores_dev);
+
+/* Decode-time append: the K and V rows of the token generated at this step join the key set of
+ * every head from the next wnw_decode_step on, after the text rows; a generated token is not
+ * audio, so every role keeps it in full (the remark under Eq. 1).
+ *   k_new_dev, v_new_dev  device bf16 [B][L][H_kv][d]; read by a kernel enqueued on hip_stream
+ *                         (valid until it has run).
+ * Call it before the wnw_decode_step of the token it belongs to, on the same stream.
+ * WNW_ERR_STATE before wnw_set_roles or once max_new_tokens rows have been appended. */
+wnw_status wnw_append_kv(wnw_ctx *ctx, const void *k_new_dev, const void *v_new_dev, void *hip_stream);
 
 /* One decode step (Eq. 2 and "Dynamic Chunk Selection"), enqueued on hip_stream (with
  * WNW_F_SELECT_NEXT_STEP or WNW_F_RECALL_MEMCPY the recall runs on an internal stream, joined by

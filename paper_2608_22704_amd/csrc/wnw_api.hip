@@ -61,6 +61,7 @@ struct wnw_ctx {
     std::vector<HeadRows> hrows;       // [nT + nF]
     std::vector<int32_t> head_keep;    // [nT + nF] kept audio rows
     int64_t keep_sum_t = 0;            // kept audio rows over the tidal heads
+    int64_t static_rows = 0;           // static rows over the tidal and fixed heads at set-up
     std::vector<int32_t> comp_rows;    // [B][nc][nT] complement rows of each unit
     std::vector<int32_t> seg_rows;     // [B][nc] their sum over the tidal heads
 
@@ -68,7 +69,7 @@ struct wnw_ctx {
     StepBuffers s{};
     uint16_t *aK = nullptr, *aV = nullptr, *tK = nullptr, *tV = nullptr, *fK = nullptr, *fV = nullptr;
     uint16_t *slots = nullptr, *host_comp = nullptr;
-    int32_t *d_lk = nullptr, *d_tile_head = nullptr, *d_comp_rows = nullptr, *d_seg_rows = nullptr;
+    int32_t *d_lk = nullptr, *d_tile_head = nullptr, *d_comp_rows = nullptr, *d_seg_rows = nullptr, *d_place = nullptr;
     HeadRows *d_hr = nullptr;
     float *scores_int = nullptr;
     int32_t *sel_int = nullptr;
@@ -80,6 +81,7 @@ struct wnw_ctx {
     int32_t *h_newinfo = nullptr;      // pinned: counts [B][2] then new lists [B][k][2]
 
     std::vector<StepEvents> pending, spare;
+    int n_gen = 0;                     // tokens appended (wnw_append_kv)
     double t_acc[8] = {0};
     int64_t timed_steps = 0, steps = 0;
 };
@@ -170,6 +172,10 @@ wnw_status derive(wnw_ctx *c, const wnw_config &cfg, Geometry &g)
     g.Ta = cfg.audio_len;
     g.Tt = cfg.text_len;
     g.T = g.Ta + g.Tt;
+    if (cfg.max_new_tokens < 0) return fail(c, WNW_ERR_INVALID, "max_new_tokens must be >= 0");
+    g.max_new = cfg.max_new_tokens;
+    g.Tcap = g.T + g.max_new;
+    g.n_gen = 0;
     g.span = span;
     g.cl = cfg.chunk_len / span;   // segment length
     g.budget_bp = cfg.budget_bp;
@@ -192,7 +198,9 @@ wnw_status derive(wnw_ctx *c, const wnw_config &cfg, Geometry &g)
         return fail(c, WNW_ERR_UNSUPPORTED, "%d chunks with %d slots exceed the selection kernel's shared memory", g.nc,
                     g.n_slots);
     g.n_tiles_a = (g.T + TILE_A - 1) / TILE_A;
-    if ((int64_t)g.n_tiles_a * G * 8 > 65536) return fail(c, WNW_ERR_UNSUPPORTED, "cache of %d rows too long", g.T);
+    g.n_tiles_a_cap = (g.Tcap + TILE_A - 1) / TILE_A;
+    if ((int64_t)g.n_tiles_a_cap * G * 8 > 65536)
+        return fail(c, WNW_ERR_UNSUPPORTED, "cache of %d rows (with room for appended tokens) too long", g.Tcap);
     g.maxc = (TILE_A - 1) / g.cl + 2;
     if (g.B > 65535 || (int64_t)g.L * g.Hkv > 65535) return fail(c, WNW_ERR_UNSUPPORTED, "batch or head count too large");
     return WNW_OK;
@@ -221,6 +229,7 @@ wnw_status plan_keep(wnw_ctx *c)
     const int len0 = g.nc ? chunk_len_of(g, 0) : 0, lenl = g.nc ? chunk_len_of(g, g.nc - 1) : 0;
     int64_t rowT = 0, rowF = 0, tiles = 0;
     g.keep_sum = 0;
+    c->static_rows = 0;
     c->keep_sum_t = 0;
     for (int hi = 0; hi < nsub; ++hi) {
         const bool tidal = hi < g.nT;
@@ -231,11 +240,12 @@ wnw_status plan_keep(wnw_ctx *c)
         h.kfull = k0;
         h.klast = kl;
         h.rs = keep + g.Tt;
-        h.nts = (h.rs + TILE_S - 1) / TILE_S;
+        h.nts = (h.rs + g.max_new + TILE_S - 1) / TILE_S;   // room for the appended tokens
         h.tile0 = (int)tiles;
         tiles += h.nts;
         h.srow = (int)(tidal ? rowT : rowF);
-        (tidal ? rowT : rowF) += h.rs;
+        (tidal ? rowT : rowF) += h.rs + g.max_new;
+        c->static_rows += h.rs;
         h.sg = 1;
         if (tidal) c->keep_sum_t += keep;
         c->head_keep[hi] = keep;
@@ -423,7 +433,7 @@ wnw_status harvest_timing(wnw_ctx *c)
 void free_all(wnw_ctx *c)
 {
     void *ptrs[] = {c->aK, c->aV, c->tK, c->tV, c->fK, c->fV, c->slots, c->d_lk, c->d_tile_head, c->d_hr,
-                    c->d_comp_rows, c->d_seg_rows,
+                    c->d_comp_rows, c->d_seg_rows, c->d_place,
                     c->scores_int, c->sel_int,
                     c->s.pa_m, c->s.pa_l, c->s.pa_o, c->s.pa_mass, c->s.mass, c->s.ps_m, c->s.ps_l, c->s.ps_o,
                     c->s.streak, c->s.slot_of, c->s.slot_last, c->s.att, c->s.slot_data, c->s.slot_busy, c->s.slot_since,
@@ -512,8 +522,8 @@ wnw_status build_tiers(wnw_ctx *c, const uint8_t *keep_all)
     // ---- allocations ------------------------------------------------------------------
 #define ALLOC(p, n, what) \
     if ((r = dalloc(c, &(p), (size_t)(n), what)) != WNW_OK) return r
-    ALLOC(c->aK, B * g.nA * g.T * Dz, "anchor K");
-    ALLOC(c->aV, B * g.nA * g.T * Dz, "anchor V");
+    ALLOC(c->aK, B * g.nA * g.Tcap * Dz, "anchor K");
+    ALLOC(c->aV, B * g.nA * g.Tcap * Dz, "anchor V");
     ALLOC(c->tK, B * g.RsT * Dz, "tidal K");
     ALLOC(c->tV, B * g.RsT * Dz, "tidal V");
     ALLOC(c->fK, B * g.RsF * Dz, "fixed K");
@@ -522,15 +532,16 @@ wnw_status build_tiers(wnw_ctx *c, const uint8_t *keep_all)
     ALLOC(c->d_lk, (size_t)nh, "role tables");
     ALLOC(c->d_hr, c->hrows.size(), "head rows");
     ALLOC(c->d_tile_head, (size_t)g.n_static, "static tile table");
+    ALLOC(c->d_place, (size_t)nh, "append table");
     ALLOC(c->d_comp_rows, c->comp_rows.size(), "complement rows");
     ALLOC(c->d_seg_rows, c->seg_rows.size(), "segment rows");
     ALLOC(c->scores_int, B * g.nchk, "scores");
     ALLOC(c->sel_int, B * g.k, "selection");
     StepBuffers &s = c->s;
-    ALLOC(s.pa_m, B * g.nA * g.n_tiles_a * g.G, "anchor partial max");
-    ALLOC(s.pa_l, B * g.nA * g.n_tiles_a * g.G, "anchor partial sum");
-    ALLOC(s.pa_o, B * g.nA * g.n_tiles_a * g.G * Dz, "anchor partial out");
-    ALLOC(s.pa_mass, B * g.nA * g.n_tiles_a * g.G * g.maxc, "anchor partial mass");
+    ALLOC(s.pa_m, B * g.nA * g.n_tiles_a_cap * g.G, "anchor partial max");
+    ALLOC(s.pa_l, B * g.nA * g.n_tiles_a_cap * g.G, "anchor partial sum");
+    ALLOC(s.pa_o, B * g.nA * g.n_tiles_a_cap * g.G * Dz, "anchor partial out");
+    ALLOC(s.pa_mass, B * g.nA * g.n_tiles_a_cap * g.G * g.maxc, "anchor partial mass");
     ALLOC(s.mass, B * g.nA * g.G * g.nc, "chunk mass");
     ALLOC(s.ps_m, B * g.P * g.G, "partial max");
     ALLOC(s.ps_l, B * g.P * g.G, "partial sum");
@@ -586,6 +597,13 @@ wnw_status build_tiers(wnw_ctx *c, const uint8_t *keep_all)
         HIPCHECK(c, hipMemcpy(c->d_seg_rows, c->seg_rows.data(), c->seg_rows.size() * sizeof(int32_t), hipMemcpyHostToDevice));
     c->t.comp_rows = c->d_comp_rows;
     c->s.seg_rows = c->d_seg_rows;
+    {
+        std::vector<int32_t> place(nh);
+        for (int a = 0; a < g.nA; ++a) place[c->anchor_lk[a]] = a;
+        for (int i = 0; i < g.nT; ++i) place[c->tidal_lk[i]] = -(1 + i);
+        for (int i = 0; i < g.nF; ++i) place[c->fixed_lk[i]] = -(1 + g.nT + i);
+        if (nh) HIPCHECK(c, hipMemcpy(c->d_place, place.data(), nh * sizeof(int32_t), hipMemcpyHostToDevice));
+    }
     c->t.hr = c->d_hr;
     c->t.tile_head = c->d_tile_head;
     c->t.anchor_lk = c->d_lk;
@@ -599,7 +617,8 @@ wnw_status build_tiers(wnw_ctx *c, const uint8_t *keep_all)
     // ---- per-sequence tier construction ------------------------------------------------------
     const int nsub = g.nT + g.nF;
     const size_t seq_rows = (size_t)g.L * g.Hkv * g.T;
-    std::vector<int32_t> static_idx((size_t)g.RsT + g.RsF), comp_idx((size_t)g.nc * g.blk_rows);
+    // rows reserved for appended tokens stay zero (index -1) until an append writes them
+    std::vector<int32_t> static_idx((size_t)g.RsT + g.RsF, -1), comp_idx((size_t)g.nc * g.blk_rows);
     int32_t *d_idx = nullptr;
     uint16_t *staging = nullptr;
     const size_t idx_n = std::max(static_idx.size(), comp_idx.size());
@@ -617,7 +636,7 @@ wnw_status build_tiers(wnw_ctx *c, const uint8_t *keep_all)
         const uint16_t *fk = c->full_k + b * seq_rows * D, *fv = c->full_v + b * seq_rows * D;
         // anchors: every row, one contiguous copy per head
         for (int a = 0; a < g.nA; ++a) {
-            const size_t src = (size_t)c->anchor_lk[a] * g.T * D, dst = (((size_t)b * g.nA + a) * g.T) * D;
+            const size_t src = (size_t)c->anchor_lk[a] * g.T * D, dst = (((size_t)b * g.nA + a) * g.Tcap) * D;
             const size_t bytes = (size_t)g.T * D * sizeof(uint16_t);
             hipError_t e1 = hipMemcpyAsync(c->aK + dst, fk + src, bytes, hipMemcpyDeviceToDevice, st);
             hipError_t e2 = hipMemcpyAsync(c->aV + dst, fv + src, bytes, hipMemcpyDeviceToDevice, st);
@@ -781,6 +800,23 @@ wnw_status wnw_set_roles_device(wnw_ctx *c, const uint8_t *roles, const float *p
     return r;
 }
 
+wnw_status wnw_append_kv(wnw_ctx *c, const void *k_new_dev, const void *v_new_dev, void *hip_stream)
+{
+    if (!c) return fail(nullptr, WNW_ERR_INVALID, "ctx is NULL");
+    if (c->state != READY) return fail(c, WNW_ERR_STATE, "wnw_append_kv needs a context after wnw_set_roles");
+    if (!k_new_dev || !v_new_dev) return fail(c, WNW_ERR_INVALID, "k_new_dev and v_new_dev must not be NULL");
+    if (c->n_gen >= c->g.max_new)
+        return fail(c, WNW_ERR_STATE, "all %d rows reserved for appended tokens are used", c->g.max_new);
+    DeviceGuard dg(c->device);
+    Geometry g = c->g;
+    g.n_gen = c->n_gen;
+    g.T += c->n_gen;
+    HIPCHECK(c, launch_append_kv(g, c->d_hr, c->d_place, c->aK, c->aV, c->tK, c->tV, c->fK, c->fV,
+                                 (const uint16_t *)k_new_dev, (const uint16_t *)v_new_dev, (hipStream_t)hip_stream));
+    c->n_gen++;
+    return WNW_OK;
+}
+
 wnw_status wnw_prefill_scores(wnw_ctx *c, const void *q_text_dev, float *scores_dev)
 {
     if (!c) return fail(nullptr, WNW_ERR_INVALID, "ctx is NULL");
@@ -814,7 +850,11 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, float *out, float *sco
                     c->state == FAILED ? c->err.c_str() : "wnw_set_roles has not run");
     if (!q_dev || !out) return fail(c, WNW_ERR_INVALID, "q_dev and out_dev must not be NULL");
     DeviceGuard dg(c->device);
-    const Geometry &g = c->g;
+    // this step's geometry: the prompt rows plus the tokens appended so far
+    Geometry g = c->g;
+    g.n_gen = c->n_gen;
+    g.T += c->n_gen;
+    g.n_tiles_a = (g.T + TILE_A - 1) / TILE_A;
     hipStream_t s0 = (hipStream_t)hip_stream;
     const uint16_t *q = (const uint16_t *)q_dev;
     float *sc = scores ? scores : c->scores_int;
@@ -1006,8 +1046,8 @@ wnw_status wnw_get_stats(wnw_ctx *c, wnw_stats *o)
         o->r_gpu = ((double)g.nA * g.Ta + (double)g.keep_sum + res_rows) / full;
         o->r_gpu_cpu = o->r_gpu + ((double)g.nT * g.Ta - (double)c->keep_sum_t) / full;
     }
-    o->anchor_bytes = (int64_t)g.B * g.nA * g.T * 2 * D * 2;
-    o->static_bytes = (int64_t)g.B * ((int64_t)g.RsT + g.RsF) * 2 * D * 2;
+    o->anchor_bytes = (int64_t)g.B * g.nA * (g.T + c->n_gen) * 2 * D * 2;
+    o->static_bytes = (int64_t)g.B * (c->static_rows + (int64_t)c->n_gen * (g.nT + g.nF)) * 2 * D * 2;
     o->revived_chunks = (int64_t)st[6];
     o->timed_steps = c->timed_steps;
     o->t_anchor_ms = c->t_acc[0];

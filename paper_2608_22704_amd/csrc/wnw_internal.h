@@ -17,7 +17,9 @@ constexpr int SCORE_PARTS = 4;   // fixed ranges of anchor q-heads summed per ch
 // Everything the kernels need to know about the cache and the step, fixed at set-up.
 struct Geometry {
     int B, L, Hq, Hkv, G;
-    int Ta, Tt, T;              // audio, text and total rows of an anchor head
+    int Ta, Tt, T;              // audio, prompt text and current rows of an anchor head (T grows by
+                                // one per appended token)
+    int Tcap, max_new, n_gen;   // anchor row stride (prompt rows + max_new), tokens appended so far
     int cl, budget_bp;          // segment length (the unit of keep sets, masses, residency,
                                 // slots and recall), retention in basis points
     int span;                   // segments per chunk: 1 disjoint chunks, 2 overlapping chunks
@@ -30,7 +32,8 @@ struct Geometry {
                                 // (-1 with per-head retention)
     int n_slots;                // recall slots per sequence
     int nA, nT, nF;             // anchor / tidal / fixed KV-heads over all layers
-    int n_tiles_a, maxc;        // anchor tiles per head, chunk entries per anchor tile
+    int n_tiles_a, maxc;        // anchor tiles per head (current rows), chunk entries per anchor tile
+    int n_tiles_a_cap;          // anchor tiles per head at full capacity (partials are sized for it)
     // Set with the roles (per-head rows, see HeadRows):
     int RsT, RsF;               // rows of a sequence's tidal / fixed static tier
     int n_static;               // static tiles of one sequence (all tidal and fixed heads)
@@ -48,8 +51,9 @@ struct Geometry {
 // kept groups, then one per newly resident segment.
 struct HeadRows {
     int srow;    // first row of the head in its sequence's static tier (tidal or fixed)
-    int rs;      // static rows: kept audio rows (ascending) + text rows
-    int nts;     // static tiles
+    int rs;      // static rows at set-up: kept audio rows (ascending) + text rows; appended tokens
+                 // follow them (rs + n_gen rows, room for max_new)
+    int nts;     // static tiles (room included)
     int tile0;   // first static tile of the head among its sequence's static tiles
     int pbase;   // first partial entry of the head among its sequence's partials
     // tidal heads (0 for fixed heads)
@@ -74,7 +78,7 @@ __host__ __device__ inline int chunk_len_of(const Geometry &g, int c)
 
 struct Tiers {
     const uint16_t *aK, *aV;    // [B][nA][T][D]
-    const uint16_t *tK, *tV;    // [B][RsT][D]: tidal heads one after the other (HeadRows::srow, rs)
+    const uint16_t *tK, *tV;    // [B][RsT][D]: tidal heads one after the other (HeadRows::srow, rs + max_new)
     const uint16_t *fK, *fV;    // [B][RsF][D]: fixed heads likewise
     uint16_t *slots;            // [B][n_slots][blk_rows][D]
     const uint16_t *host_comp;  // device view of pinned [B][nc][blk_rows][D]
@@ -150,6 +154,12 @@ hipError_t launch_prefill_scores(const Geometry &g, const uint16_t *K, const uin
 // score is marked 2.
 hipError_t launch_prefill_keep(const Geometry &g, int n_sub, const int32_t *sub_lk, const int2 *seg_keep, bool global,
                                const float *p, uint8_t *keep, hipStream_t st);
+// Decode-time append of one token's K and V rows [B][L][Hkv][D] to every head's tier at row
+// T (anchors) or rs + n_gen (tidal, fixed); place[l * Hkv + kv] = anchor index, or -(1 + index
+// among the tidal then fixed heads).
+hipError_t launch_append_kv(const Geometry &g, const HeadRows *hr, const int32_t *place, uint16_t *aK, uint16_t *aV,
+                            uint16_t *tK, uint16_t *tV, uint16_t *fK, uint16_t *fV, const uint16_t *k_new,
+                            const uint16_t *v_new, hipStream_t st);
 // Set-up: dst[i] = row idx[i] of src_k (idx >= 0), row -idx[i]-2 of src_v (idx <= -2), or zeros
 // (idx == -1); a row is D bf16.
 hipError_t launch_gather_rows(uint16_t *dst, const uint16_t *src_k, const uint16_t *src_v, const int32_t *idx,

@@ -196,7 +196,7 @@ __device__ inline void anchor_tile(const Geometry &g, const Tiers &t, const Step
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, sub = lane & 15, rg = lane >> 4;
     const int kq = lane >> 4, blk = (lane >> 2) & 3, x4 = lane & 3;
     const int lk = t.anchor_lk[ai], l = lk / g.Hkv, kv = lk - l * g.Hkv;
-    const size_t hrow = ((size_t)b * g.nA + ai) * (size_t)g.T;
+    const size_t hrow = ((size_t)b * g.nA + ai) * (size_t)g.Tcap;
     const uint16_t *__restrict__ K = t.aK + hrow * D;
     const uint16_t *__restrict__ V = t.aV + hrow * D;
     const uint16_t *__restrict__ qh = q + (((size_t)b * g.L + l) * g.Hq + (size_t)kv * G) * D;
@@ -1038,13 +1038,22 @@ __device__ inline void static_tile(const Geometry &g, const Tiers &t, const Step
 {
     const int hi = t.tile_head[j];
     const HeadRows hr = t.hr[hi];
-    const int tile = j - hr.tile0;
+    const int tile = j - hr.tile0, rows = hr.rs + g.n_gen;
+    const size_t p = (size_t)b * g.P + hr.pbase + tile;
+    if (tile * TILE_S >= rows) {
+        // room reserved for tokens not appended yet: an empty partial, which the merge skips
+        if (threadIdx.x < G) {
+            s.ps_m[p * G + threadIdx.x] = -INFINITY;
+            s.ps_l[p * G + threadIdx.x] = 0.f;
+        }
+        for (int i = threadIdx.x; i < G * D; i += NT) s.ps_o[p * G * D + i] = 0.f;
+        return;
+    }
     const bool tidal = hi < g.nT;
     const int lk = tidal ? t.tidal_lk[hi] : t.fixed_lk[hi - g.nT], l = lk / g.Hkv, kv = lk - l * g.Hkv;
     const size_t hb = ((size_t)b * (tidal ? g.RsT : g.RsF) + hr.srow) * D;
-    const StaticRows map{(tidal ? t.tK : t.fK) + hb, (tidal ? t.tV : t.fV) + hb, tile * TILE_S, hr.rs};
+    const StaticRows map{(tidal ? t.tK : t.fK) + hb, (tidal ? t.tV : t.fV) + hb, tile * TILE_S, rows};
     const uint16_t *qh = q + (((size_t)b * g.L + l) * g.Hq + (size_t)kv * G) * D;
-    const size_t p = (size_t)b * g.P + hr.pbase + tile;
     subset_tile<G, RPL_S>(qh, map, s.ps_m + p * G, s.ps_l + p * G, s.ps_o + p * G * D, sm);
 }
 
@@ -1330,6 +1339,34 @@ __global__ void gather_rows_kernel(uint16_t *__restrict__ dst, const uint16_t *_
     ((uint4 *)(dst + row * D))[part] = v;
 }
 
+// Decode-time append: grid (L * Hkv, B), one 64-thread group per head writes the token's K row
+// (lanes 0-15) and V row (lanes 16-31) as sixteen 16-byte pieces each.
+__global__ __launch_bounds__(64) void append_kv_kernel(Geometry g, const HeadRows *__restrict__ hr,
+                                                       const int32_t *__restrict__ place, uint16_t *aK, uint16_t *aV,
+                                                       uint16_t *tK, uint16_t *tV, uint16_t *fK, uint16_t *fV,
+                                                       const uint16_t *__restrict__ k_new,
+                                                       const uint16_t *__restrict__ v_new)
+{
+    const int lk = blockIdx.x, b = blockIdx.y, lane = threadIdx.x;
+    if (lane >= 32) return;
+    const int pl = place[lk], piece = lane & 15;
+    const bool isv = lane >= 16;
+    size_t row;
+    uint16_t *dst;
+    if (pl >= 0) {
+        row = ((size_t)b * g.nA + pl) * g.Tcap + g.T;
+        dst = isv ? aV : aK;
+    } else {
+        const int hi = -pl - 1;
+        const bool tidal = hi < g.nT;
+        const HeadRows h = hr[hi];
+        row = (size_t)b * (tidal ? g.RsT : g.RsF) + h.srow + h.rs + g.n_gen;
+        dst = tidal ? (isv ? tV : tK) : (isv ? fV : fK);
+    }
+    const size_t src = ((size_t)b * g.L * g.Hkv + lk) * D + piece * 8;
+    *(uint4 *)(dst + row * D + piece * 8) = *(const uint4 *)((isv ? v_new : k_new) + src);
+}
+
 // Timing events of a launch that has no work: both recorded on the stream (the interval is empty).
 hipError_t record_pair(hipEvent_t e0, hipEvent_t e1, hipStream_t st)
 {
@@ -1477,6 +1514,15 @@ hipError_t launch_new_slots(const Geometry &g, const Tiers &t, const StepBuffers
 hipError_t launch_subset_combine(const Geometry &g, const Tiers &t, const StepBuffers &s, float *out, hipStream_t st)
 {
     return dispatch_g<CombineL>(g.G, g, t, s, out, st);
+}
+
+hipError_t launch_append_kv(const Geometry &g, const HeadRows *hr, const int32_t *place, uint16_t *aK, uint16_t *aV,
+                            uint16_t *tK, uint16_t *tV, uint16_t *fK, uint16_t *fV, const uint16_t *k_new,
+                            const uint16_t *v_new, hipStream_t st)
+{
+    hipLaunchKernelGGL(append_kv_kernel, dim3(g.L * g.Hkv, g.B), dim3(64), 0, st, g, hr, place, aK, aV, tK, tV, fK, fV,
+                       k_new, v_new);
+    return hipGetLastError();
 }
 
 hipError_t launch_gather_rows(uint16_t *dst, const uint16_t *src_k, const uint16_t *src_v, const int32_t *idx,

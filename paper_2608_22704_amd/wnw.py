@@ -20,7 +20,7 @@ WNW_ANCHOR, WNW_TIDAL, WNW_FIXED = 0, 1, 2
 WNW_F_SELECT_NEXT_STEP, WNW_F_RECALL_MEMCPY, WNW_F_TIMING, WNW_F_OVERLAP_CHUNKS, WNW_F_PREFILL_GLOBAL = 1, 2, 4, 8, 16
 
 EXPORTS = ("wnw_init_cache", "wnw_set_retention", "wnw_set_roles", "wnw_prefill_scores", "wnw_set_roles_device",
-           "wnw_decode_step", "wnw_query_geometry",
+           "wnw_append_kv", "wnw_decode_step", "wnw_query_geometry",
            "wnw_query_segments", "wnw_query_head_keep", "wnw_get_stats",
            "wnw_set_selection_override", "wnw_debug_read_slot", "wnw_debug_read_host_chunk",
            "wnw_debug_read_resident", "wnw_last_error", "wnw_destroy")
@@ -30,7 +30,7 @@ class wnw_config(C.Structure):
     _fields_ = [("batch", C.c_int32), ("layers", C.c_int32), ("q_heads", C.c_int32), ("kv_heads", C.c_int32),
                 ("head_dim", C.c_int32), ("audio_len", C.c_int32), ("text_len", C.c_int32),
                 ("chunk_len", C.c_int32), ("budget_bp", C.c_int32), ("top_k", C.c_int32),
-                ("evict_lag", C.c_int32), ("flags", C.c_uint32)]
+                ("evict_lag", C.c_int32), ("flags", C.c_uint32), ("max_new_tokens", C.c_int32)]
 
 
 class wnw_stats(C.Structure):
@@ -63,6 +63,7 @@ def _load():
         "wnw_set_roles": ([P, P, P], C.c_int),
         "wnw_set_retention": ([P, P, C.c_float], C.c_int),
         "wnw_prefill_scores": ([P, P, P], C.c_int),
+        "wnw_append_kv": ([P, P, P, P], C.c_int),
         "wnw_set_roles_device": ([P, P, P], C.c_int),
         "wnw_query_head_keep": ([P, P], C.c_int),
         "wnw_decode_step": ([P, P, P, P, P, P], C.c_int),
@@ -124,6 +125,10 @@ def wnw_set_retention(ctx, importance, lam):
 
 def wnw_set_roles(ctx, roles, prefill_scores):
     _check(lib.wnw_set_roles(ctx, _ptr(roles), _ptr(prefill_scores)), ctx)
+
+
+def wnw_append_kv(ctx, k_new_dev, v_new_dev, stream=None):
+    _check(lib.wnw_append_kv(ctx, _ptr(k_new_dev), _ptr(v_new_dev), _stream(stream)), ctx)
 
 
 def wnw_prefill_scores(ctx, q_text_dev, scores_dev):
@@ -188,6 +193,6 @@ def wnw_destroy(ctx):
 
 
 def make_config(batch, layers, q_heads, kv_heads, audio_len, text_len, chunk_len, budget_bp,
-                head_dim=128, top_k=0, evict_lag=0, flags=0) -> wnw_config:
+                head_dim=128, top_k=0, evict_lag=0, flags=0, max_new_tokens=0) -> wnw_config:
     return wnw_config(batch, layers, q_heads, kv_heads, head_dim, audio_len, text_len, chunk_len, budget_bp,
-                      top_k, evict_lag, flags)
+                      top_k, evict_lag, flags, max_new_tokens)

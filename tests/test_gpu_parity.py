@@ -690,3 +690,52 @@ def test_prefill_global_device_scores_and_variants():
     _run(w, prefill_device=True, flags=_glob(_next()))
     _run(w, prefill_device=True, flags=_glob(_ovl()))
     _run(w, flags=_glob(_next()), importance=_imp(w, 506, ((0, 1),), ((1, 2),)), lam=1.0)
+
+
+# ---- decode-time append: the generated token's K/V rows join every head's key set before each
+# step (room reserved for w.steps tokens); the oracle appends the same rows.
+
+APP = [
+    _small("app_g2", 601, Tt=9),
+    _small("app_anchor_tile_boundary", 602, Ta=250, Tt=4, cl=32, steps=8),
+    _small("app_static_tile_boundary", 603, Ta=250, Tt=4, cl=32, budget=10000, steps=6),
+    _small("app_no_text", 604, Tt=0),
+    _small("app_budget_zero", 605, budget=0),
+    _small("app_g8_chunk256", 606, Hq=16, Hkv=2, cl=256, Ta=1300, Tt=300),
+    _small("app_text_only", 607, Ta=0, Tt=40),
+]
+
+
+@pytest.mark.parametrize("w", APP, ids=[w.name for w in APP])
+def test_append_lockstep(w):
+    _run(w, append=True)
+    _run(w, append=True, flags=_next())
+
+
+def test_append_with_variants():
+    w = _small("app_variants", 608, L=2, Hq=8, Hkv=4, Ta=480, Tt=5, cl=32, steps=8)
+    _run(w, append=True, flags=_ovl(_next()))
+    _run(w, append=True, flags=_next(), importance=_imp(w, 608, ((0, 1),), ((1, 2),)), lam=1.0)
+    _run(w, append=True, flags=_glob(_next()))
+    from paper_2608_22704_amd import wnw as W
+    _run(w, append=True, flags=_next(W.WNW_F_RECALL_MEMCPY))
+
+
+def test_append_qwen_shaped_all_steps():
+    _run(configs.QWEN_10MIN, append=True, flags=_next())
+
+
+def test_append_beyond_reserved_rows_is_refused():
+    from paper_2608_22704_amd import wnw as W
+    from tests.wnw_harness import Lockstep, log, to_dev
+    w = _small("app_full", 609, steps=2)
+    log("[case] append beyond the reserved rows")
+    h = Lockstep(w, append=True)
+    try:
+        h.step(0)
+        h.step(1)
+        kn, vn = h.new_token(2)
+        with pytest.raises(W.WnwError):
+            W.wnw_append_kv(h.ctx, to_dev(kn), to_dev(vn))
+    finally:
+        h.close()

@@ -107,10 +107,13 @@ class Lockstep:
     all w.batch sequences)."""
 
     def __init__(self, w, flags: int = 0, seqs=None, budget_bp=None, data=None, top_k=0, importance=None, lam=None,
-                 prefill_device=False):
+                 prefill_device=False, append=False):
         """prefill_device: the prefill scores come from wnw_prefill_scores over the synthetic text
         queries, the keep sets from wnw_set_roles_device; the scores are checked against the
-        oracle's (double) and then given to the oracle as its prefill input."""
+        oracle's (double) and then given to the oracle as its prefill input.
+        append: before every step the K/V rows of a synthetic generated token (N(0,1), bf16, seeded
+        by step) are appended on both sides (room for w.steps tokens)."""
+        self.append = append
         import torch
         from paper_2608_22704_amd import wnw as W
         self.W, self.torch = W, torch
@@ -145,7 +148,7 @@ class Lockstep:
         torch.cuda.synchronize()
         log(f"[harness] {w.name}: inputs ready in {time.time() - t0:.1f}s")
         self.cfg = W.make_config(B, L, w.q_heads, H, w.audio_len, w.text_len, w.chunk_len, w.budget_bp,
-                                 top_k=top_k, flags=flags)
+                                 top_k=top_k, flags=flags, max_new_tokens=w.steps if append else 0)
         self.ctx = W.wnw_init_cache(self.cfg, kd, vd)
         if importance is not None:
             W.wnw_set_retention(self.ctx, importance, lam)
@@ -167,7 +170,8 @@ class Lockstep:
         self.next_step = 1 if flags & W.WNW_F_SELECT_NEXT_STEP else 0
         span = 2 if flags & W.WNW_F_OVERLAP_CHUNKS else 1
         ocfg = O.cfg_from_workload(w, batch=len(self.seqs), top_k=top_k, next_step=self.next_step,
-                                   chunk_span=span, prefill_global=1 if flags & W.WNW_F_PREFILL_GLOBAL else 0)
+                                   chunk_span=span, prefill_global=1 if flags & W.WNW_F_PREFILL_GLOBAL else 0,
+                                   max_new=w.steps if append else 0)
         self.ok_ = np.stack([host[b]["k"] for b in self.seqs])
         self.ov_ = np.stack([host[b]["v"] for b in self.seqs])
         self.oracle = O.Oracle(ocfg, self.ok_, self.ov_, self.roles, self.prefill[self.seqs], importance=importance,
@@ -195,7 +199,18 @@ class Lockstep:
         if getattr(self, "oracle", None) is not None:
             self.oracle.close()
 
+    def new_token(self, s: int):
+        """K, V rows [B][L][H_kv][d] (bf16 bit patterns) of the token generated before step s."""
+        w = self.w
+        rng = np.random.default_rng(7000 + s)
+        shape = (w.batch, w.layers, w.kv_heads, w.head_dim)
+        return (gen.f32_to_bf16(rng.standard_normal(shape, dtype=np.float32)),
+                gen.f32_to_bf16(rng.standard_normal(shape, dtype=np.float32)))
+
     def gpu_step(self, s: int):
+        if self.append:
+            kn, vn = self.new_token(s)
+            self.W.wnw_append_kv(self.ctx, to_dev(kn), to_dev(vn))
         qd = to_dev(self.q[s])
         self.W.wnw_decode_step(self.ctx, qd, self.out, self.scores, self.sel)
         self.torch.cuda.synchronize()
@@ -207,6 +222,9 @@ class Lockstep:
     def step(self, s: int, head_mask=None):
         out, sc, sel, res = self.gpu_step(s)
         idx = self.seqs
+        if self.append:
+            kn, vn = self.new_token(s)
+            self.oracle.append(kn[idx], vn[idx])
         r = self.oracle.step(self.q[s][idx], forced=sel[idx] if self.k else None, head_mask=head_mask)
         for j, b in enumerate(idx):
             so = r["scores"][j]
