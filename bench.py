@@ -29,6 +29,7 @@ sys.path.insert(0, ROOT)
 METRIC = "WnW decode steps/sec + achieved HBM GB/s (attn) at 15k audio tokens, 1 GPU"
 PEAK_HBM_GBPS = 8000.0
 PEAK_BF16_TFLOPS = 2500.0      # dense bf16 MFMA
+PEAK_LINK_GBPS = 64.0          # PCIe 5.0 x16, one direction
 
 
 def log(msg):
@@ -284,6 +285,11 @@ def main():
                            "note": "achieved: over the timed steps, the recall's host reads running beside it; "
                                    "achieved_without_recall: selection pinned, no recall"}
     res["recall"] = main_run["recall"]
+    if main_run["recall"].get("GBps"):
+        # the recall is bound by the host link (PCIe 5.0 x16, 64 GB/s per direction)
+        gb = main_run["recall"]["GBps"]
+        res["recall"]["roofline"] = {"bound": "host link", "achieved": gb, "peak": PEAK_LINK_GBPS, "unit": "GB/s",
+                                     "frac": gb / PEAK_LINK_GBPS}
     if main_run.get("sweep"):
         res["overlap_sweep"] = main_run["sweep"]
         # share of the recall hidden behind the step at the workload's own recall load
