@@ -59,6 +59,10 @@ def lib():
         L.wnwo_segments.argtypes = [C.POINTER(_Cfg), C.POINTER(C.c_int32)]
         L.wnwo_prefill_scores.argtypes = [C.POINTER(_Cfg), P, P, P]
         L.wnwo_append.argtypes = [P, P, P]
+        I = C.c_int32
+        L.wnwo_voice_hits.argtypes = [I, I, I, I, I, I, I, P, P, P, I, P]
+        L.wnwo_key_sensitivity.argtypes = [I, I, I, I, I, P, P]
+        L.wnwo_triage.argtypes = [I, I, I, I, P, P, I, P, I, I, P, P, P, P]
         L.wnwo_set_threads.argtypes = [C.c_int]
         L.wnwo_set_threads.restype = C.c_int
         _lib = L
@@ -119,6 +123,46 @@ def prefill_scores(cfg: _Cfg, k, q_text) -> np.ndarray:
     if lib().wnwo_prefill_scores(C.byref(cfg), _ptr(k), _ptr(q), _ptr(p)):
         raise ValueError("wnwo_prefill_scores failed")
     return p
+
+
+def voice_hits(k, q, span, K, audio_len) -> np.ndarray:
+    """k uint16 [L][H_kv][T][d], q uint16 [n_tok][L][H_q][d], span int32 [n_tok][2] ->
+    hits int32 [n_tok][L][H_q]."""
+    k = np.ascontiguousarray(k, dtype=np.uint16)
+    q = np.ascontiguousarray(q, dtype=np.uint16)
+    span = np.ascontiguousarray(span, dtype=np.int32)
+    L, Hkv, T, d = k.shape
+    n_tok, _, Hq, _ = q.shape
+    out = np.empty((n_tok, L, Hq), dtype=np.int32)
+    if lib().wnwo_voice_hits(L, Hq, Hkv, d, T, audio_len, n_tok, _ptr(k), _ptr(q), _ptr(span), K, _ptr(out)):
+        raise ValueError("wnwo_voice_hits failed")
+    return out
+
+
+def key_sensitivity(grad) -> np.ndarray:
+    """grad fp32 [n_tok][L][H_kv][T_a][d] -> sens double [n_tok][L][H_kv]."""
+    g = np.ascontiguousarray(grad, dtype=np.float32)
+    n_tok, L, Hkv, Ta, d = g.shape
+    out = np.empty((n_tok, L, Hkv), dtype=np.float64)
+    if lib().wnwo_key_sensitivity(L, Hkv, d, Ta, n_tok, _ptr(g), _ptr(out)):
+        raise ValueError("wnwo_key_sensitivity failed")
+    return out
+
+
+def triage(hits, K, sens, sample, n_voice, n_anchor):
+    """hits int32 [n][L][H_q], sens [n][L][H_kv], sample int32 [n] -> (roles uint8, vs, hs,
+    importance_norm), each [L][H_kv]."""
+    hits = np.ascontiguousarray(hits, dtype=np.int32)
+    sens = np.ascontiguousarray(sens, dtype=np.float64)
+    sample = np.ascontiguousarray(sample, dtype=np.int32)
+    n, L, Hq = hits.shape
+    Hkv = sens.shape[2]
+    roles = np.empty((L, Hkv), dtype=np.uint8)
+    vs, hs, imp = (np.empty((L, Hkv), dtype=np.float64) for _ in range(3))
+    if lib().wnwo_triage(L, Hkv, Hq // Hkv, n, _ptr(sample), _ptr(hits), K, _ptr(sens), n_voice, n_anchor,
+                         _ptr(roles), _ptr(vs), _ptr(hs), _ptr(imp)):
+        raise ValueError("wnwo_triage failed")
+    return roles, vs, hs, imp
 
 
 def set_threads(n: int) -> int:

@@ -560,3 +560,145 @@ int wnwo_set_threads(int n)
     return 1;
 #endif
 }
+
+/* ---- head triage arithmetic (Method, "Head Functional Triage via Offline Calibration" and the
+ * calibration score details of the appendix) ------------------------------------------------------ */
+
+typedef struct { double s; int32_t pos; } scored_d;
+
+static int by_logit_then_pos(const void *a, const void *b)
+{
+    const scored_d *x = a, *y = b;
+    if (x->s > y->s) return -1;
+    if (x->s < y->s) return 1;
+    return (x->pos > y->pos) - (x->pos < y->pos);
+}
+
+/* Voice-score hits: the K audio positions that answer token t's q-head (l, h) attends to most
+ * (softmax keeps the order of the logits q.k / sqrt(d); ties to the lower position), counted
+ * when inside the token's aligned audio interval [a_t, b_t). */
+int wnwo_voice_hits(int32_t L, int32_t Hq, int32_t Hkv, int32_t d, int32_t T, int32_t Ta, int32_t n_tok,
+                    const uint16_t *k, const uint16_t *q, const int32_t *span, int32_t K, int32_t *hits)
+{
+    if (L < 1 || Hkv < 1 || Hq < Hkv || Hq % Hkv || d < 1 || Ta < 0 || T < Ta || n_tok < 0 || K < 1 || K > Ta ||
+        !k || !q || !span || !hits)
+        return -1;
+    const int32_t g = Hq / Hkv;
+    const int64_t n = (int64_t)n_tok * L * Hq;
+    int status = 0;
+#pragma omp parallel for schedule(dynamic)
+    for (int64_t i = 0; i < n; ++i) {
+        const int32_t t = (int32_t)(i / ((int64_t)L * Hq)), l = (int32_t)(i / Hq % L), h = (int32_t)(i % Hq);
+        const uint16_t *qv = q + (size_t)i * d;
+        const uint16_t *K0 = k + ((size_t)l * Hkv + h / g) * (size_t)T * d;
+        scored_d *x = malloc((size_t)Ta * sizeof *x);
+        if (!x) {
+#pragma omp atomic write
+            status = -2;
+            continue;
+        }
+        for (int32_t tau = 0; tau < Ta; ++tau) {
+            double acc = 0.0;
+            for (int32_t j = 0; j < d; ++j) acc += bf16(qv[j]) * bf16(K0[(size_t)tau * d + j]);
+            x[tau].s = acc / sqrt((double)d);
+            x[tau].pos = tau;
+        }
+        qsort(x, (size_t)Ta, sizeof *x, by_logit_then_pos);
+        int32_t c = 0;
+        for (int32_t r = 0; r < K; ++r) c += x[r].pos >= span[2 * t] && x[r].pos < span[2 * t + 1];
+        hits[i] = c;
+        free(x);
+    }
+    return status;
+}
+
+/* Key sensitivity of each answer token and KV-head: the mean over audio positions of the L2
+ * norm of the loss gradient with respect to the position's key vector. */
+int wnwo_key_sensitivity(int32_t L, int32_t Hkv, int32_t d, int32_t Ta, int32_t n_tok, const float *grad, double *sens)
+{
+    if (L < 1 || Hkv < 1 || d < 1 || Ta < 1 || n_tok < 0 || !grad || !sens) return -1;
+    const int64_t n = (int64_t)n_tok * L * Hkv;
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; ++i) {
+        double acc = 0.0;
+        for (int32_t tau = 0; tau < Ta; ++tau) {
+            const float *gv = grad + ((size_t)i * Ta + tau) * d;
+            double s2 = 0.0;
+            for (int32_t j = 0; j < d; ++j) s2 += (double)gv[j] * (double)gv[j];
+            acc += sqrt(s2);
+        }
+        sens[i] = acc / Ta;
+    }
+    return 0;
+}
+
+/* Mean over calibration samples of the per-sample mean over its rows of v[row][m] (m < M). */
+static void sample_mean(int32_t n, const int32_t *sample, int32_t M, const double *v, double *out)
+{
+    int32_t ns = 0;
+    for (int32_t i = 0; i < n; ++i) if (sample[i] + 1 > ns) ns = sample[i] + 1;
+    double *sum = calloc((size_t)(ns ? ns : 1) * M, sizeof(double));
+    int32_t *cnt = calloc((size_t)(ns ? ns : 1), sizeof(int32_t));
+    for (int32_t i = 0; i < n; ++i) {
+        cnt[sample[i]]++;
+        for (int32_t m = 0; m < M; ++m) sum[(size_t)sample[i] * M + m] += v[(size_t)i * M + m];
+    }
+    int32_t used = 0;
+    for (int32_t m = 0; m < M; ++m) out[m] = 0.0;
+    for (int32_t s = 0; s < ns; ++s) {
+        if (!cnt[s]) continue;
+        ++used;
+        for (int32_t m = 0; m < M; ++m) out[m] += sum[(size_t)s * M + m] / cnt[s];
+    }
+    for (int32_t m = 0; m < M; ++m) out[m] = used ? out[m] / used : 0.0;
+    free(sum);
+    free(cnt);
+}
+
+typedef struct { double s; int32_t id; } ranked_h;
+
+static int by_importance_then_head(const void *a, const void *b)
+{
+    const ranked_h *x = a, *y = b;
+    if (x->s > y->s) return -1;
+    if (x->s < y->s) return 1;
+    return (x->id > y->id) - (x->id < y->id);
+}
+
+/* Three-way classification from the scores of n answer tokens (sample[i] >= 0 names the
+ * calibration sample of row i): VS is the per-sample mean of hits / K, averaged over samples and
+ * then over the g q-heads of each KV-head; HS the per-sample mean of sens averaged over samples;
+ * the importance VS * HS ranks the heads (ties to the lower head index l * H_kv + kv).  The
+ * first n_voice are voice heads: their first n_anchor are anchors, the rest tidal; the others are
+ * fixed.  The normalised importance divides by the largest importance (all zero if it is 0). */
+int wnwo_triage(int32_t L, int32_t Hkv, int32_t g, int32_t n, const int32_t *sample, const int32_t *hits, int32_t K,
+                const double *sens, int32_t n_voice, int32_t n_anchor, uint8_t *roles, double *vs, double *hs,
+                double *importance_norm)
+{
+    const int32_t nh = L * Hkv, nq = nh * g;
+    if (L < 1 || Hkv < 1 || g < 1 || n < 1 || K < 1 || n_voice < 0 || n_voice > nh || n_anchor < 0 ||
+        n_anchor > n_voice || !sample || !hits || !sens || !roles || !vs || !hs || !importance_norm)
+        return -1;
+    for (int32_t i = 0; i < n; ++i) if (sample[i] < 0) return -1;
+    double *hr = malloc((size_t)n * nq * sizeof(double)), *hq = malloc((size_t)nq * sizeof(double));
+    ranked_h *rk = malloc((size_t)nh * sizeof *rk);
+    for (size_t i = 0; i < (size_t)n * nq; ++i) hr[i] = (double)hits[i] / K;
+    sample_mean(n, sample, nq, hr, hq);
+    sample_mean(n, sample, nh, sens, hs);
+    double mx = 0.0;
+    for (int32_t h = 0; h < nh; ++h) {
+        double a = 0.0;
+        for (int32_t j = 0; j < g; ++j) a += hq[(size_t)h * g + j];
+        vs[h] = a / g;
+        rk[h].s = vs[h] * hs[h];
+        rk[h].id = h;
+        if (rk[h].s > mx) mx = rk[h].s;
+    }
+    for (int32_t h = 0; h < nh; ++h) importance_norm[h] = mx > 0.0 ? rk[h].s / mx : 0.0;
+    qsort(rk, (size_t)nh, sizeof *rk, by_importance_then_head);
+    for (int32_t r = 0; r < nh; ++r) roles[rk[r].id] = r < n_anchor ? 0 : r < n_voice ? 1 : 2;
+    free(hr);
+    free(hq);
+    free(rk);
+    return 0;
+}

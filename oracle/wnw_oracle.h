@@ -87,6 +87,30 @@ int wnwo_append(wnwo *o, const uint16_t *k_new, const uint16_t *v_new);
 int wnwo_step(wnwo *o, const uint16_t *q, const int32_t *forced, const uint8_t *head_mask,
               double *out, double *scores, int32_t *selected, double *mass, uint8_t *resident);
 
+/* Head triage arithmetic (Method, "Head Functional Triage via Offline Calibration"; the
+ * calibration score details of the appendix), on given inputs (no model, alignment or autograd).
+ *
+ * Voice-score hits of answer token t and q-head (l, h): how many of the K audio positions with
+ * the largest logit q.k / sqrt(d) (ties to the lower position) lie in [span[t][0], span[t][1]).
+ *   k     [L][H_kv][T][d] bf16 of one calibration sample (audio rows first)
+ *   q     [n_tok][L][H_q][d] bf16 answer-token queries;  span [n_tok][2] int32
+ *   hits  [n_tok][L][H_q] int32 in 0..K */
+int wnwo_voice_hits(int32_t L, int32_t Hq, int32_t Hkv, int32_t d, int32_t T, int32_t Ta, int32_t n_tok,
+                    const uint16_t *k, const uint16_t *q, const int32_t *span, int32_t K, int32_t *hits);
+
+/* Key sensitivity: sens[t][l][kv] = mean over audio positions of the L2 norm of the loss
+ * gradient grad [n_tok][L][H_kv][T_a][d] (fp32) at that position's key. */
+int wnwo_key_sensitivity(int32_t L, int32_t Hkv, int32_t d, int32_t Ta, int32_t n_tok, const float *grad, double *sens);
+
+/* Roles from n answer-token rows (sample[i] = calibration sample of row i): VS = mean over
+ * samples of the per-sample mean of hits / K, then over the g q-heads of a KV-head; HS = mean
+ * over samples of the per-sample mean of sens; VS * HS ranked descending (ties to the lower
+ * head index): the first n_anchor heads are anchors, the next up to n_voice tidal, the rest
+ * fixed; importance_norm = VS * HS / max (0 if the max is 0).  Outputs [L][H_kv]. */
+int wnwo_triage(int32_t L, int32_t Hkv, int32_t g, int32_t n, const int32_t *sample, const int32_t *hits, int32_t K,
+                const double *sens, int32_t n_voice, int32_t n_anchor, uint8_t *roles, double *vs, double *hs,
+                double *importance_norm);
+
 /* Top-k of n scores ordered by (score descending, id ascending); ids returned ascending. */
 int wnwo_topk(const float *scores, int32_t n, int32_t k, int32_t *sel);
 

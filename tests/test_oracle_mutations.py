@@ -20,7 +20,8 @@ MUTANTS = {
         "attend(qh, o->kc + hoff, o->vc + hoff, rows, T, D, x, oh, p);",
         "attend(qh, o->kc + hoff, o->vc + hoff, rows, Ta, D, x, oh, p);"),
     "chunk ties prefer the higher id": (
-        "return (x->id > y->id) - (x->id < y->id);", "return (x->id < y->id) - (x->id > y->id);"),
+        "return (x->id > y->id) - (x->id < y->id);\n}\n\nstatic int by_int",
+        "return (x->id < y->id) - (x->id > y->id);\n}\n\nstatic int by_int"),
     "eviction lag one step too long": (
         "            if (st[ch] < o->delta)\n", "            if (st[ch] <= o->delta)\n"),
     "keep count rounds up": (
@@ -55,6 +56,16 @@ MUTANTS = {
     "append overwrites the last prompt row": (
         "const size_t row = (size_t)c->audio_len + c->text_len + o->n_gen;",
         "const size_t row = (size_t)c->audio_len + c->text_len + o->n_gen - 1;"),
+    "voice hits count the span's end": (
+        "c += x[r].pos >= span[2 * t] && x[r].pos < span[2 * t + 1];",
+        "c += x[r].pos >= span[2 * t] && x[r].pos <= span[2 * t + 1];"),
+    "voice scores pooled over tokens instead of per sample": (
+        "out[m] += sum[(size_t)s * M + m] / cnt[s];", "out[m] += sum[(size_t)s * M + m] * used / n;"),
+    "head ranking ties to the higher head": (
+        "    return (x->id > y->id) - (x->id < y->id);\n}\n\n/* Three-way",
+        "    return (x->id < y->id) - (x->id > y->id);\n}\n\n/* Three-way"),
+    "importance normalised by its sum": (
+        "if (rk[h].s > mx) mx = rk[h].s;", "mx += rk[h].s;"),
     "global prefill keeps the last segment's count": (
         "for (int32_t j = 0; j < ns; ++j) total += keep_count_head(",
         "for (int32_t j = 0; j < ns; ++j) total = keep_count_head("),

@@ -607,3 +607,84 @@ def test_appended_rows_in_every_key_set(oracle_mod):
             np.testing.assert_allclose(r["out"][b, l, hq], ref, rtol=0, atol=1e-12)
             if step == 2 and hq % g == 0:
                 np.testing.assert_allclose(r["out"][b, l, hq], bf16_to_f32(vv[b, l, h]), rtol=0, atol=1e-6)
+
+
+# ---- head triage arithmetic: voice-score hits, key sensitivity, VS x HS roles
+
+def _basis_keys(L, H, T, d, mags):
+    """Key tau = mags[tau] * e_(tau mod d) (exact in bf16 for the magnitudes used)."""
+    k = np.zeros((L, H, T, d), dtype=np.float32)
+    for tau in range(T):
+        k[:, :, tau, tau % d] = mags[tau]
+    return f32_to_bf16(k)
+
+
+def test_voice_hits_planted_top_positions(oracle_mod):
+    """Keys are scaled basis vectors, so a query's logits are known in closed form: the query
+    e_j weights position tau by mags[tau] when tau = j (mod d) and 0 otherwise.  The top-K are then
+    the K largest magnitudes on residue j (ties to the lower position), and hits count those inside
+    the span; K = T_a ranks every position, a span over all audio gives K hits."""
+    L, H, g, d, Ta, Tt = 1, 2, 2, 8, 40, 3
+    mags = np.array([1 + (tau * 7) % 11 for tau in range(Ta + Tt)], dtype=np.float32)
+    mags[[3, 11]] = 12.0                       # a tie on residue 3: position 3 ranks before 11
+    k = _basis_keys(L, H, Ta + Tt, d, mags)
+    q = np.zeros((4, L, H * g, d), dtype=np.float32)
+    resid = [3, 5, 0, 7]
+    for t, j in enumerate(resid):
+        q[t, :, :, j] = 1.0
+    q = f32_to_bf16(q)
+    span = np.array([[0, 10], [20, 40], [0, 40], [39, 40]], dtype=np.int32)
+    for K in (1, 3, 5):
+        hits = oracle_mod.voice_hits(k, q, span, K, Ta)
+        for t, j in enumerate(resid):
+            cand = sorted([tau for tau in range(Ta) if tau % d == j], key=lambda tau: (-mags[tau], tau))
+            top = cand[:K] + [tau for tau in range(Ta) if tau % d != j][: max(0, K - len(cand))]
+            want = sum(span[t, 0] <= tau < span[t, 1] for tau in top)
+            assert (hits[t] == want).all(), (K, t)
+    assert (oracle_mod.voice_hits(k, q, np.array([[0, Ta]] * 4, np.int32), 5, Ta) == 5).all()
+    full = oracle_mod.voice_hits(k, q, span, Ta, Ta)
+    assert (full[:, 0, 0] == np.minimum(span[:, 1], Ta) - span[:, 0]).all()
+    one = oracle_mod.voice_hits(k, q[:1], np.array([[11, 12]], np.int32), 1, Ta)
+    assert (one == 0).all()                    # the tie went to position 3
+
+
+def test_key_sensitivity_closed_forms(oracle_mod):
+    """A gradient of constant entries c has norm |c| sqrt(d) at every position; the measure is
+    linear in the gradient's scale and the mean over positions of per-position norms."""
+    n, L, H, Ta, d = 2, 2, 3, 5, 16
+    grad = np.zeros((n, L, H, Ta, d), dtype=np.float32)
+    c = np.arange(1, n * L * H + 1, dtype=np.float32).reshape(n, L, H)
+    grad += c[..., None, None]
+    np.testing.assert_allclose(oracle_mod.key_sensitivity(grad), c * np.sqrt(d), rtol=1e-14)
+    grad2 = np.zeros_like(grad)
+    grad2[:, :, :, 0, 0] = 3.0
+    grad2[:, :, :, 1, :2] = 4.0 / np.sqrt(2.0)                    # norm 4
+    np.testing.assert_allclose(oracle_mod.key_sensitivity(grad2), (3.0 + 4.0) / Ta, rtol=1e-6)
+    np.testing.assert_allclose(oracle_mod.key_sensitivity(-2.5 * grad2), 2.5 * (3.0 + 4.0) / Ta, rtol=1e-6)
+
+
+def test_triage_hand_worked_example(oracle_mod):
+    with open(os.path.join(GOLD, "triage_example.json")) as f:
+        ex = json.load(f)
+    roles, vs, hs, imp = oracle_mod.triage(np.array(ex["hits"]), ex["K"], np.array(ex["sens"]), np.array(ex["sample"]),
+                                           ex["n_voice"], ex["n_anchor"])
+    np.testing.assert_allclose(vs, ex["vs"], rtol=0, atol=1e-15)
+    np.testing.assert_allclose(hs, ex["hs"], rtol=0, atol=1e-15)
+    assert roles.tolist() == ex["roles"]
+    np.testing.assert_allclose(imp, ex["importance_norm"], rtol=0, atol=1e-15)
+
+
+def test_triage_ranking_counts_and_normalisation(oracle_mod):
+    """Random scores: exactly n_anchor anchors and n_voice - n_anchor tidal heads, every anchor
+    outranks every tidal head, which outranks every fixed head by VS * HS; the normalised
+    importance peaks at 1 on the best head."""
+    rng = np.random.default_rng(71)
+    n, L, H, g = 6, 3, 4, 2
+    hits = rng.integers(0, 5, size=(n, L, H * g)).astype(np.int32)
+    sens = rng.random((n, L, H))
+    sample = np.array([0, 0, 1, 1, 1, 2], dtype=np.int32)
+    roles, vs, hs, imp = oracle_mod.triage(hits, 4, sens, sample, 7, 2)
+    assert (roles == 0).sum() == 2 and (roles == 1).sum() == 5 and (roles == 2).sum() == L * H - 7
+    prod = vs * hs
+    assert prod[roles == 0].min() >= prod[roles == 1].max() >= prod[roles == 2].max() - 0.0
+    assert abs(imp.max() - 1.0) < 1e-15 and np.argmax(imp) == np.argmax(prod)
