@@ -30,6 +30,7 @@ METRIC = "WnW decode steps/sec + achieved HBM GB/s (attn) at 15k audio tokens, 1
 PEAK_HBM_GBPS = 8000.0
 PEAK_BF16_TFLOPS = 2500.0      # dense bf16 MFMA
 PEAK_LINK_GBPS = 64.0          # PCIe 5.0 x16, one direction
+PEAK_FP64_TFLOPS = 78.6        # fp64 vector
 
 
 def log(msg):
@@ -203,7 +204,8 @@ def main():
                          "lambda, 1) per head with seeded U(0,1) importance")
     ap.add_argument("--lam", type=float, default=0.4, help="lambda of the per-head retention (0.4: mean 20 %%)")
     ap.add_argument("--no-other-retention", action="store_true", help="skip the run with the other retention")
-    ap.add_argument("--no-prefill", action="store_true", help="skip the prefill-compression measurement")
+    ap.add_argument("--no-prefill", action="store_true",
+                    help="skip the set-up measurements (prefill compression, head triage arithmetic)")
     ap.add_argument("--no-sweep", dest="sweep", action="store_false",
                     help="skip the overlap sweep (forced 1..24 newly resident chunks per step)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU oracle sample (0 = skip)")
@@ -258,6 +260,7 @@ def main():
         other_ret = run_timing(W, torch, w, args.timing, args.recall, kd, vd, qd, roles, prefill, args_other,
                                args.chunks, other_retention)
     prefill_res = None if args.no_prefill else prefill_bench(W, torch, w, kd, vd, roles)
+    triage_res = None if args.no_prefill else triage_bench(W, torch, w, kd)
     del kd, vd
     torch.cuda.empty_cache()
 
@@ -322,6 +325,8 @@ def main():
 
     if prefill_res is not None:
         res["prefill"] = prefill_res
+    if triage_res is not None:
+        res["triage"] = triage_res
     if args.cpu_seconds > 0:
         res["cpu_baseline"] = cpu_baseline(w, roles, prefill, args.cpu_seconds)
     print(json.dumps(res), flush=True)
@@ -400,6 +405,47 @@ def prefill_bench(W, torch, w, kd, vd, roles, reps=5):
     return {"scores_ms": avg, "flop": flop, "achieved_tflops": tf, "peak_tflops": PEAK_BF16_TFLOPS,
             "frac": tf / PEAK_BF16_TFLOPS, "set_roles_device_s": t_dev, "set_roles_host_s": t_host,
             "note": "one-time set-up, outside the decode step; scores_ms over both MFMA passes (HIP events)"}
+
+
+def triage_bench(W, torch, w, kd, n_tok=64, reps=5):
+    """Head triage arithmetic at the workload's shapes (one calibration sample): voice-score hits
+    of n_tok answer tokens (fp64 dot products over every audio key: 2 d flops per token, q-head
+    and audio key), and the key sensitivity of one answer token (a read of its fp32 key gradients:
+    L * H_kv * T_a * d * 4 bytes).  Synthetic inputs; calibration itself is offline."""
+    L, Hq, H, D, Ta, T = w.layers, w.q_heads, w.kv_heads, w.head_dim, w.audio_len, w.total_len
+    g = torch.Generator(device="cuda").manual_seed(5)
+    q = torch.randn((n_tok, L, Hq, D), device="cuda", generator=g).to(torch.bfloat16).view(torch.int16)
+    a = torch.randint(0, max(Ta - 8, 1), (n_tok,), device="cuda", generator=g)
+    span = torch.stack([a, a + 8], dim=1).to(torch.int32).contiguous()
+    hits = torch.empty((n_tok, L, Hq), dtype=torch.int32, device="cuda")
+    k0 = kd[0].contiguous()
+    grad = torch.randn((1, L, H, Ta, D), device="cuda", generator=g, dtype=torch.float32)
+    sens = torch.empty((1, L, H), dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def timed(fn):
+        fn()
+        ms = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            e1.synchronize()
+            ms.append(e0.elapsed_time(e1))
+        return sum(ms) / len(ms)
+
+    vh = timed(lambda: W.wnw_voice_hits(k0, q, span, 4, Ta, hits))
+    ks = timed(lambda: W.wnw_key_sensitivity(grad, sens))
+    flop = 2.0 * D * n_tok * L * Hq * Ta
+    nbytes = float(L * H * Ta * D * 4)
+    del grad
+    log(f"[bench] triage: voice hits {vh:.3f} ms, key sensitivity {ks:.3f} ms")
+    return {"voice_hits_ms": vh, "voice_hits_tokens": n_tok, "voice_hits_tflops": flop / (vh * 1e-3) / 1e12,
+            "voice_hits_frac": flop / (vh * 1e-3) / 1e12 / PEAK_FP64_TFLOPS, "voice_hits_bound": "fp64 alu",
+            "key_sensitivity_ms": ks, "key_sensitivity_GBps": nbytes / (ks * 1e-3) / 1e9,
+            "key_sensitivity_frac": nbytes / (ks * 1e-3) / 1e9 / PEAK_HBM_GBPS,
+            "note": "offline calibration arithmetic on synthetic inputs; one sample, K = 4"}
 
 
 def cpu_baseline(w, roles, prefill, budget_s):

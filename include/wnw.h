@@ -262,6 +262,48 @@ const char *wnw_last_error(const wnw_ctx *ctx);
 /* Free every device, pinned and stream resource of ctx (waits for its work).  NULL is a no-op. */
 void wnw_destroy(wnw_ctx *ctx);
 
+/* ---- head triage arithmetic (Method, "Head Functional Triage via Offline Calibration"; the
+ * calibration score details of the appendix).  These calls need no context: they turn the
+ * calibration inputs (answer-token queries and a sample's keys, aligned audio intervals, key
+ * gradients) into the roles and normalised importance that wnw_set_roles / wnw_set_retention
+ * take.  Producing those inputs (model, forced alignment, autograd) is outside the library.
+ * Errors: WNW_ERR_INVALID / _UNSUPPORTED / _HIP, message from wnw_triage_last_error(). */
+
+/* Voice-score hits.  For every answer token t and q-head (l, h): the top_k audio positions with
+ * the largest logit q . k (the softmax keeps that order; ties to the lower position), and how
+ * many lie in [span[t][0], span[t][1]).  Logits are exact bf16 products summed in double.
+ *   k_dev     device bf16 [L][H_kv][rows][d] of one calibration sample, audio rows first
+ *   q_dev     device bf16 [n_tok][L][H_q][d], the answer tokens' queries
+ *   span_dev  device int32 [n_tok][2], audio-token interval [a, b) of each answer token
+ *   hits_dev  device int32 [n_tok][L][H_q], written (0..top_k)
+ * top_k in 1..8 and <= audio_len; d = 128.  Enqueued on hip_stream. */
+wnw_status wnw_voice_hits(int32_t layers, int32_t q_heads, int32_t kv_heads, int32_t rows, int32_t audio_len,
+                          int32_t n_tok, const void *k_dev, const void *q_dev, const int32_t *span_dev, int32_t top_k,
+                          int32_t *hits_dev, void *hip_stream);
+
+/* Key sensitivity.  sens[t][l][kv] = mean over the audio positions of the L2 norm of the loss
+ * gradient at that position's key.
+ *   grad_dev  device fp32 [n_tok][L][H_kv][audio_len][d]
+ *   sens_dev  device fp32 [n_tok][L][H_kv], written
+ * Enqueued on hip_stream. */
+wnw_status wnw_key_sensitivity(int32_t layers, int32_t kv_heads, int32_t audio_len, int32_t n_tok, const float *grad_dev,
+                               float *sens_dev, void *hip_stream);
+
+/* Three-way classification (host).  Rows i = 0..n-1 are answer tokens of calibration samples
+ * sample[i] >= 0.  VS = per-sample mean of hits / top_k, averaged over the samples, then over the
+ * group q-heads of each KV-head; HS = per-sample mean of sens averaged over the samples.  Heads
+ * are ranked by VS * HS (ties to the lower index l * H_kv + kv): the first n_anchor are anchors,
+ * the next ones up to n_voice tidal, the rest fixed.  importance = VS * HS / its maximum (all 0
+ * when the maximum is 0), the normalised importance of the retention equation (Eq. 1).
+ *   hits [n][L][H_kv * group], sens [n][L][H_kv]; outputs [L][H_kv]: roles (wnw_role),
+ *   importance; vs_out, hs_out (may be NULL). */
+wnw_status wnw_triage(int32_t layers, int32_t kv_heads, int32_t group, int32_t n, const int32_t *sample,
+                      const int32_t *hits, int32_t top_k, const float *sens, int32_t n_voice, int32_t n_anchor,
+                      uint8_t *roles, float *importance, double *vs_out, double *hs_out);
+
+/* Message of the last failed triage call of this thread. */
+const char *wnw_triage_last_error(void);
+
 #ifdef __cplusplus
 }
 #endif

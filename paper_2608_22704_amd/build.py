@@ -10,7 +10,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libwnw.so")
-SOURCES = ["wnw_kernels.hip", "wnw_prefill.hip", "wnw_api.hip"]
+SOURCES = ["wnw_kernels.hip", "wnw_prefill.hip", "wnw_triage.hip", "wnw_api.hip"]
 ARCH = "gfx950"
 
 

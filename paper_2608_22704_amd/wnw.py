@@ -23,7 +23,8 @@ EXPORTS = ("wnw_init_cache", "wnw_set_retention", "wnw_set_roles", "wnw_prefill_
            "wnw_append_kv", "wnw_decode_step", "wnw_query_geometry",
            "wnw_query_segments", "wnw_query_head_keep", "wnw_get_stats",
            "wnw_set_selection_override", "wnw_debug_read_slot", "wnw_debug_read_host_chunk",
-           "wnw_debug_read_resident", "wnw_last_error", "wnw_destroy")
+           "wnw_debug_read_resident", "wnw_last_error", "wnw_destroy", "wnw_voice_hits", "wnw_key_sensitivity",
+           "wnw_triage", "wnw_triage_last_error")
 
 
 class wnw_config(C.Structure):
@@ -64,6 +65,10 @@ def _load():
         "wnw_set_retention": ([P, P, C.c_float], C.c_int),
         "wnw_prefill_scores": ([P, P, P], C.c_int),
         "wnw_append_kv": ([P, P, P, P], C.c_int),
+        "wnw_voice_hits": ([I32, I32, I32, I32, I32, I32, P, P, P, I32, P, P], C.c_int),
+        "wnw_key_sensitivity": ([I32, I32, I32, I32, P, P, P], C.c_int),
+        "wnw_triage": ([I32, I32, I32, I32, P, P, I32, P, I32, I32, P, P, P, P], C.c_int),
+        "wnw_triage_last_error": ([], C.c_char_p),
         "wnw_set_roles_device": ([P, P, P], C.c_int),
         "wnw_query_head_keep": ([P, P], C.c_int),
         "wnw_decode_step": ([P, P, P, P, P, P], C.c_int),
@@ -125,6 +130,42 @@ def wnw_set_retention(ctx, importance, lam):
 
 def wnw_set_roles(ctx, roles, prefill_scores):
     _check(lib.wnw_set_roles(ctx, _ptr(roles), _ptr(prefill_scores)), ctx)
+
+
+def _tcheck(status):
+    if status != WNW_OK:
+        raise WnwError(status, lib.wnw_triage_last_error().decode())
+
+
+def wnw_voice_hits(k_dev, q_dev, span_dev, top_k, audio_len, hits_dev, stream=None):
+    """k_dev [L][H_kv][rows][d] bf16, q_dev [n_tok][L][H_q][d] bf16, span_dev int32 [n_tok][2] ->
+    hits_dev int32 [n_tok][L][H_q] (tensors on the device)."""
+    L, Hkv, rows, _ = k_dev.shape
+    n_tok, _, Hq, _ = q_dev.shape
+    _tcheck(lib.wnw_voice_hits(L, Hq, Hkv, rows, audio_len, n_tok, _ptr(k_dev), _ptr(q_dev), _ptr(span_dev), top_k,
+                               _ptr(hits_dev), _stream(stream)))
+
+
+def wnw_key_sensitivity(grad_dev, sens_dev, stream=None):
+    """grad_dev fp32 [n_tok][L][H_kv][T_a][d] -> sens_dev fp32 [n_tok][L][H_kv]."""
+    n_tok, L, Hkv, Ta, _ = grad_dev.shape
+    _tcheck(lib.wnw_key_sensitivity(L, Hkv, Ta, n_tok, _ptr(grad_dev), _ptr(sens_dev), _stream(stream)))
+
+
+def wnw_triage(hits, top_k, sens, sample, n_voice, n_anchor):
+    """Host arrays hits int32 [n][L][H_q], sens fp32 [n][L][H_kv], sample int32 [n] ->
+    (roles uint8, importance fp32, vs, hs) each [L][H_kv]."""
+    hits = np.ascontiguousarray(hits, dtype=np.int32)
+    sens = np.ascontiguousarray(sens, dtype=np.float32)
+    sample = np.ascontiguousarray(sample, dtype=np.int32)
+    n, L, Hq = hits.shape
+    Hkv = sens.shape[2]
+    roles = np.empty((L, Hkv), dtype=np.uint8)
+    imp = np.empty((L, Hkv), dtype=np.float32)
+    vs, hs = np.empty((L, Hkv)), np.empty((L, Hkv))
+    _tcheck(lib.wnw_triage(L, Hkv, Hq // Hkv, n, _ptr(sample), _ptr(hits), top_k, _ptr(sens), n_voice, n_anchor,
+                           _ptr(roles), _ptr(imp), _ptr(vs), _ptr(hs)))
+    return roles, imp, vs, hs
 
 
 def wnw_append_kv(ctx, k_new_dev, v_new_dev, stream=None):

@@ -69,3 +69,34 @@ def test_validation_without_gpu(W):
     assert W.lib.wnw_set_roles(None, None, None) == W.WNW_ERR_INVALID
     assert W.lib.wnw_decode_step(None, None, None, None, None, None) == W.WNW_ERR_INVALID
     W.wnw_destroy(None)
+
+
+def test_triage_host_ranking_matches_oracle():
+    """wnw_triage (host code of the library, no GPU) on the hand-worked example and on random
+    scores against the oracle's triage."""
+    import json
+    import os
+    import numpy as np
+    from oracle import oracle as O
+    from paper_2608_22704_amd import wnw as W
+    ex = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "triage_example.json")))
+    roles, imp, vs, hs = W.wnw_triage(np.array(ex["hits"]), ex["K"], np.array(ex["sens"]), np.array(ex["sample"]),
+                                      ex["n_voice"], ex["n_anchor"])
+    assert roles.tolist() == ex["roles"]
+    np.testing.assert_allclose(vs, ex["vs"], rtol=0, atol=1e-15)
+    np.testing.assert_allclose(hs, ex["hs"], rtol=0, atol=1e-15)
+    np.testing.assert_allclose(imp, ex["importance_norm"], rtol=0, atol=0)
+    rng = np.random.default_rng(5)
+    for trial in range(20):
+        n, L, H, g = int(rng.integers(1, 9)), int(rng.integers(1, 5)), int(rng.integers(1, 9)), int(rng.choice([1, 2, 4]))
+        hits = rng.integers(0, 5, size=(n, L, H * g)).astype(np.int32)
+        sens = (rng.integers(0, 4, size=(n, L, H)) / 4).astype(np.float32)   # ties in the ranking
+        sample = np.sort(rng.integers(0, 3, size=n)).astype(np.int32)
+        nv = int(rng.integers(0, L * H + 1))
+        na = int(rng.integers(0, nv + 1))
+        r1, i1, v1, h1 = W.wnw_triage(hits, 4, sens, sample, nv, na)
+        r2, v2, h2, i2 = O.triage(hits, 4, sens.astype(np.float64), sample, nv, na)
+        assert np.array_equal(r1, r2), trial
+        np.testing.assert_allclose(v1, v2, rtol=1e-15, atol=1e-15)
+        np.testing.assert_allclose(h1, h2, rtol=1e-15, atol=1e-15)
+        np.testing.assert_allclose(i1, i2.astype(np.float32), rtol=0, atol=0)

@@ -739,3 +739,63 @@ def test_append_beyond_reserved_rows_is_refused():
             W.wnw_append_kv(h.ctx, to_dev(kn), to_dev(vn))
     finally:
         h.close()
+
+
+# ---- head triage arithmetic on the device: voice-score hits (exact against the oracle) and key
+# sensitivity (fp32 squares, double sums; 1e-5 relative), then the roles.
+
+VH = [  # (L, H_q, H_kv, T_a, T_t, n_tok, K)
+    (1, 8, 2, 300, 5, 7, 4),
+    (2, 8, 8, 97, 0, 64, 8),
+    (2, 12, 4, 517, 9, 22, 1),
+    (1, 24, 3, 1000, 3, 17, 4),
+    (1, 16, 2, 64, 1, 9, 8),
+]
+
+
+@pytest.mark.parametrize("shape", VH, ids=[f"L{s[0]}_q{s[1]}_kv{s[2]}_Ta{s[3]}_tok{s[5]}_K{s[6]}" for s in VH])
+def test_voice_hits_match_oracle(shape):
+    import torch
+    from oracle import oracle as O
+    from paper_2608_22704_amd import wnw as W
+    from tests.wnw_harness import log, to_dev
+    L, Hq, Hkv, Ta, Tt, n_tok, K = shape
+    log(f"[case] voice hits {shape}")
+    rng = np.random.default_rng(sum(shape))
+    k = gen.f32_to_bf16(rng.standard_normal((L, Hkv, Ta + Tt, 128), dtype=np.float32))
+    k[:, :, 5] = k[:, :, 2]                      # duplicate keys: ties go to the lower position
+    q = gen.f32_to_bf16(rng.standard_normal((n_tok, L, Hq, 128), dtype=np.float32))
+    a = rng.integers(0, Ta, size=n_tok)
+    span = np.stack([a, np.minimum(a + rng.integers(1, 12, size=n_tok), Ta)], axis=1).astype(np.int32)
+    span[0] = (2, 3)
+    hits = torch.empty((n_tok, L, Hq), dtype=torch.int32, device="cuda")
+    W.wnw_voice_hits(to_dev(k), to_dev(q), torch.from_numpy(span).cuda(), K, Ta, hits)
+    torch.cuda.synchronize()
+    want = O.voice_hits(k, q, span, K, Ta)
+    assert np.array_equal(hits.cpu().numpy(), want)
+
+
+def test_key_sensitivity_and_roles_match_oracle():
+    import torch
+    from oracle import oracle as O
+    from paper_2608_22704_amd import wnw as W
+    from tests.wnw_harness import log
+    log("[case] key sensitivity and roles")
+    rng = np.random.default_rng(3)
+    n_tok, L, Hkv, Ta = 5, 3, 4, 333
+    grad = (rng.standard_normal((n_tok, L, Hkv, Ta, 128), dtype=np.float32)
+            * rng.random((n_tok, L, Hkv, 1, 1), dtype=np.float32))
+    sens = torch.empty((n_tok, L, Hkv), dtype=torch.float32, device="cuda")
+    W.wnw_key_sensitivity(torch.from_numpy(grad).cuda(), sens)
+    torch.cuda.synchronize()
+    got = sens.cpu().numpy()
+    want = O.key_sensitivity(grad)
+    rel = np.abs(got - want) / want
+    log(f"[triage] key sensitivity max rel err {rel.max():.3g}")
+    assert (rel <= 1e-5).all()
+    hits = rng.integers(0, 5, size=(n_tok, L, Hkv * 2)).astype(np.int32)
+    sample = np.array([0, 0, 1, 1, 1], dtype=np.int32)
+    r1, i1, _, _ = W.wnw_triage(hits, 4, got, sample, 6, 2)
+    r2, _, _, i2 = O.triage(hits, 4, got.astype(np.float64), sample, 6, 2)
+    assert np.array_equal(r1, r2)
+    np.testing.assert_allclose(i1, i2, rtol=1e-6)
