@@ -808,12 +808,19 @@ __device__ inline void subset_tile(const uint16_t *__restrict__ qh, const RowMap
     for (int i = 0; i < RPL; ++i) {
         const RowPtr rp = map.row(wave * NR + i * 4 + rg);
         ok[i] = rp.k != nullptr;
-        kr[i] = ok[i] ? *(const uint4 *)(rp.k + sub * 8) : make_uint4(0, 0, 0, 0);
+        // device rows stream once (nontemporal); host rows keep plain loads
+        if constexpr (RowMap::copies)
+            kr[i] = ok[i] ? *(const uint4 *)(rp.k + sub * 8) : make_uint4(0, 0, 0, 0);
+        else
+            kr[i] = ok[i] ? load_nt(rp.k + sub * 8) : make_uint4(0, 0, 0, 0);
     }
 #pragma unroll
     for (int i = 0; i < RPL; ++i) {
         const RowPtr rp = map.row(wave * NR + i * 4 + rg);
-        vr[i] = ok[i] ? *(const uint4 *)(rp.v + sub * 8) : make_uint4(0, 0, 0, 0);
+        if constexpr (RowMap::copies)
+            vr[i] = ok[i] ? *(const uint4 *)(rp.v + sub * 8) : make_uint4(0, 0, 0, 0);
+        else
+            vr[i] = ok[i] ? load_nt(rp.v + sub * 8) : make_uint4(0, 0, 0, 0);
     }
     if constexpr (RowMap::copies) {
         // rows read from host memory are also written to their device slot on the way
