@@ -799,3 +799,28 @@ def test_key_sensitivity_and_roles_match_oracle():
     r2, _, _, i2 = O.triage(hits, 4, got.astype(np.float64), sample, 6, 2)
     assert np.array_equal(r1, r2)
     np.testing.assert_allclose(i1, i2, rtol=1e-6)
+
+
+# ---- feature combinations: every option of the step together, batch 3
+
+COMBOS = [
+    dict(flags=("ovl", "next"), importance=True, append=True, prefill_device=True),
+    dict(flags=("ovl", "glob"), importance=True, append=True),
+    dict(flags=("next", "glob", "memcpy"), append=True, prefill_device=True),
+    dict(flags=("ovl", "next", "memcpy"), importance=True),
+]
+
+
+@pytest.mark.parametrize("combo", COMBOS, ids=["+".join(c["flags"]) + ("+imp" if c.get("importance") else "") +
+                                                ("+app" if c.get("append") else "") +
+                                                ("+dev" if c.get("prefill_device") else "") for c in COMBOS])
+def test_feature_combinations(combo):
+    from paper_2608_22704_amd import wnw as W
+    bits = {"ovl": W.WNW_F_OVERLAP_CHUNKS, "next": W.WNW_F_SELECT_NEXT_STEP, "glob": W.WNW_F_PREFILL_GLOBAL,
+            "memcpy": W.WNW_F_RECALL_MEMCPY}
+    w = _small("combo", 701, B=3, L=2, Hq=12, Hkv=4, Ta=611, Tt=17, cl=34, budget=2500, steps=7)
+    kw = dict(flags=sum(bits[f] for f in combo["flags"]), append=combo.get("append", False),
+              prefill_device=combo.get("prefill_device", False))
+    if combo.get("importance"):
+        kw.update(importance=_imp(w, 701, ((0, 1),), ((1, 3),)), lam=0.9)
+    _run(w, **kw)
