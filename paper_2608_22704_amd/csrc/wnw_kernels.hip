@@ -558,6 +558,7 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
     int *since = sdata + ns;                          // [ns] step at which the slot was freed
     int *skey = since + ns;                           // [ns] ordering key of free slots
     int *freelist = skey + ns;                        // [ns] free slots in order
+    int *frank = freelist + ns;                       // [ns] rank of a free slot among the free ones
     __shared__ int wsum[SEL_THREADS / 64 + 1];
     __shared__ int ndrop, nrows, nrev, nfree;
 
@@ -674,19 +675,37 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
 
     // free slots ordered by (holds data, freed at step, slot id): never-used first, then the
     // least recently freed.  Key: -1 for slots not free, else (holds data) * 2^30 + freed-at step.
-    for (int i = tid; i < ns; i += nthr) skey[i] = busy[i] ? -1 : ((sdata[i] >= 0 ? 1 : 0) << 30) + since[i];
-    __syncthreads();
-    for (int i = tid; i < ns; i += nthr) {
-        const int ki = skey[i];
-        if (ki < 0) continue;
-        int r = 0;
-        for (int j = 0; j < ns; ++j) {
-            const int kj = skey[j];
-            r += kj >= 0 && (kj < ki || (kj == ki && j < i));
+    for (int i0 = 0; i0 < ns; i0 += nthr) {
+        const int i = i0 + tid;
+        const bool fr = i < ns && !busy[i];
+        if (i < ns) {
+            skey[i] = fr ? ((sdata[i] >= 0 ? 1 : 0) << 30) + since[i] : -1;
+            frank[i] = 0;
         }
-        freelist[r] = i;   // the ranks of the free slots are 0 .. nfree-1, each once
-        atomicAdd(&nfree, 1);
+        const unsigned long long bal = __ballot(fr);   // free slots: one count per wavefront
+        if ((tid & 63) == 0 && bal) atomicAdd(&nfree, __popcll(bal));
     }
+    __syncthreads();
+    {
+        // every free slot counts the free slots ordered before it; the comparisons of one slot are
+        // split over `split` threads that add their counts (integer sums: any order)
+        const int split = max(1, nthr / max(ns, 1)), span_j = (ns + split - 1) / split;
+        for (int w = tid; w < ns * split; w += nthr) {
+            const int i = w % ns, part = w / ns;
+            const int ki = skey[i];
+            if (ki < 0) continue;
+            int r = 0;
+#pragma unroll 8
+            for (int j = part * span_j, je = min(ns, (part + 1) * span_j); j < je; ++j) {
+                const int kj = skey[j];
+                r += kj >= 0 && (kj < ki || (kj == ki && j < i));
+            }
+            if (r) atomicAdd(&frank[i], r);
+        }
+    }
+    __syncthreads();
+    for (int i = tid; i < ns; i += nthr)
+        if (skey[i] >= 0) freelist[frank[i]] = i;   // the ranks of the free slots are 0 .. nfree-1, each once
     __syncthreads();
 
     // kept list first (it needs the slots of segments dropped now under next-step timing)
