@@ -190,7 +190,11 @@ def main():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=16)
     ap.add_argument("--workload", default=None, help="workload name from synth.configs (default: the 15k-audio one)")
-    ap.add_argument("--recall", choices=("kernel", "memcpy"), default="kernel")
+    ap.add_argument("--recall", choices=("auto", "kernel", "memcpy"), default="auto",
+                    help="recall path: copy-engine transfers issued by the host after each selection (memcpy), or "
+                         "work-groups reading mapped pinned memory (kernel); auto = memcpy with next-step timing "
+                         "(the transfers leave the compute units to the attention launch beside them), kernel with "
+                         "same-step timing (the recall is attended in the same pass, no host wait)")
     ap.add_argument("--timing", choices=("next", "same"), default="next",
                     help="selection timing of the headline run: the selection made after step s serves step s+1 "
                          "(the paper's timing; the recall overlaps the step) or step s itself")
@@ -242,23 +246,28 @@ def main():
     torch.cuda.synchronize()
     log(f"[bench] inputs resident in HBM after {time.time() - t0:.1f}s")
 
-    main_run = run_timing(W, torch, w, args.timing, args.recall, kd, vd, qd, roles, prefill, args, args.chunks,
-                          args.retention)
+    def recall_for(timing):
+        if args.recall != "auto":
+            return args.recall
+        return "memcpy" if timing == "next" else "kernel"
+
+    main_run = run_timing(W, torch, w, args.timing, recall_for(args.timing), kd, vd, qd, roles, prefill, args,
+                          args.chunks, args.retention)
     other = other_ch = None
     args_other = argparse.Namespace(**{**vars(args), "calibrate_copy": False, "sweep": False})
     if not args.no_other_timing:
         other_timing = "same" if args.timing == "next" else "next"
-        other = run_timing(W, torch, w, other_timing, args.recall, kd, vd, qd, roles, prefill, args_other, args.chunks,
-                           args.retention)
+        other = run_timing(W, torch, w, other_timing, recall_for(other_timing), kd, vd, qd, roles, prefill, args_other,
+                           args.chunks, args.retention)
     other_chunks = "overlap" if args.chunks == "disjoint" else "disjoint"
     if not args.no_other_chunks:
-        other_ch = run_timing(W, torch, w, args.timing, args.recall, kd, vd, qd, roles, prefill, args_other,
-                              other_chunks, args.retention)
+        other_ch = run_timing(W, torch, w, args.timing, recall_for(args.timing), kd, vd, qd, roles, prefill,
+                              args_other, other_chunks, args.retention)
     other_retention = "per-head" if args.retention == "uniform" else "uniform"
     other_ret = None
     if not args.no_other_retention:
-        other_ret = run_timing(W, torch, w, args.timing, args.recall, kd, vd, qd, roles, prefill, args_other,
-                               args.chunks, other_retention)
+        other_ret = run_timing(W, torch, w, args.timing, recall_for(args.timing), kd, vd, qd, roles, prefill,
+                               args_other, args.chunks, other_retention)
     prefill_res = None if args.no_prefill else prefill_bench(W, torch, w, kd, vd, roles)
     triage_res = None if args.no_prefill else triage_bench(W, torch, w, kd)
     del kd, vd
@@ -273,7 +282,7 @@ def main():
         "config": {"workload": w.name, "batch": B, "layers": L, "q_heads": w.q_heads, "kv_heads": H,
                    "head_dim": D, "audio_len": w.audio_len, "text_len": w.text_len, "chunk_len": w.chunk_len,
                    "budget_bp": w.budget_bp, "roles": [w.n_anchor, w.n_tidal, w.n_fixed], "kv_storage": "bf16",
-                   "selection_timing": args.timing, "recall": args.recall, "chunks": args.chunks,
+                   "selection_timing": args.timing, "recall": recall_for(args.timing), "chunks": args.chunks,
                    "retention": args.retention if args.retention == "uniform" else f"per-head, lambda {args.lam}"},
     }
     if "kernels" in main_run:
@@ -285,7 +294,7 @@ def main():
                            "unit": "GB/s", "frac": a["GBps"] / PEAK_HBM_GBPS,
                            "traffic": measured_traffic(first, w.name),
                            "achieved_without_recall": k[first + "_pinned_selection"]["GBps"],
-                           "note": "achieved: over the timed steps, the recall's host reads running beside it; "
+                           "note": "achieved: over the timed steps, the recall running beside it; "
                                    "achieved_without_recall: selection pinned, no recall"}
     res["recall"] = main_run["recall"]
     if main_run["recall"].get("GBps"):
@@ -302,7 +311,7 @@ def main():
     res["r_gpu"] = st1["r_gpu"]
     res["r_gpu_cpu"] = st1["r_gpu_cpu"]
     if other is not None:
-        o = {"selection_timing": "same" if args.timing == "next" else "next", "value": other["value"],
+        o = {"selection_timing": other_timing, "recall": recall_for(other_timing), "value": other["value"],
              "unit": "steps/s", "ms_per_step": other["ms_per_step"], "recall": other["recall"]}
         if "kernels" in other:
             o["kernels"] = other["kernels"]

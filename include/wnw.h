@@ -72,9 +72,14 @@ enum {
      * side stream, overlapped with the rest of step s and the anchor attention of step s+1;
      * a dropped chunk keeps its slot one step longer, so n_slots = (delta + 1) * k. */
     WNW_F_SELECT_NEXT_STEP = 1u,
-    /* Recall with hipMemcpyAsync on a side stream after one host wait per step, instead of
-     * the default: work-groups of the tidal/fixed launch read the complements from mapped
-     * pinned memory, copy them to their slots and attend to them in the same pass. */
+    /* Recall with copy-engine transfers (hipMemcpyAsync from the pinned complement, spread over
+     * four internal streams) that the host issues as soon as the step's selection has run; the
+     * call polls for that point, so it returns only after the selection.  Without this flag
+     * work-groups read the complements from mapped pinned memory (same-step timing: in the
+     * tidal/fixed launch, which also attends to them; next-step timing: a copy kernel on a side
+     * stream) and the call never waits.  The transfers occupy no compute units: with next-step
+     * timing they disturb the attention launch beside them far less than work-groups holding
+     * host reads, and they keep the link as busy. */
     WNW_F_RECALL_MEMCPY = 2u,
     /* Record HIP events around the kernels of every step; wnw_get_stats reports the times. */
     WNW_F_TIMING = 4u,
@@ -142,7 +147,9 @@ typedef struct {
     double t_step_ms;          /* whole step on the caller's stream                             */
     double t_recall_ms;        /* the recall: the launch that carries it (same-step timing), the
                                   copy kernel on the side stream (next-step timing) or the
-                                  host-issued copies (WNW_F_RECALL_MEMCPY)                      */
+                                  host-issued copies (WNW_F_RECALL_MEMCPY: from the first copy
+                                  stream's start to the last copy's end, less the part spent
+                                  behind the previous step's copies)                            */
 } wnw_stats;
 
 /* Create a context for one batch of caches.
@@ -204,7 +211,7 @@ wnw_status wnw_set_roles_device(wnw_ctx *ctx, const uint8_t *roles, const float 
 wnw_status wnw_append_kv(wnw_ctx *ctx, const void *k_new_dev, const void *v_new_dev, void *hip_stream);
 
 /* One decode step (Eq. 2 and "Dynamic Chunk Selection"), enqueued on hip_stream (with
- * WNW_F_SELECT_NEXT_STEP or WNW_F_RECALL_MEMCPY the recall runs on an internal stream, joined by
+ * WNW_F_SELECT_NEXT_STEP or WNW_F_RECALL_MEMCPY the recall runs on internal streams, joined by
  * events).
  *   q_dev             device bf16 [B][L][H_q][d]
  *   out_dev           device fp32 [B][L][H_q][d]     attention output of every q-head
@@ -213,7 +220,7 @@ wnw_status wnw_append_kv(wnw_ctx *ctx, const void *k_new_dev, const void *v_new_
  *   hip_stream        caller's stream (NULL = null stream); outputs are valid once it has
  *                     completed.  Buffers must stay valid until then.
  * The default recall path does not block the host.  With WNW_F_RECALL_MEMCPY the call waits
- * once, mid-step, for the selection before issuing the copies. */
+ * once, mid-step (busy polling), for the selection before issuing the copies. */
 wnw_status wnw_decode_step(wnw_ctx *ctx, const void *q_dev, float *out_dev,
                            float *chunk_scores_dev, int32_t *selected_dev, void *hip_stream);
 

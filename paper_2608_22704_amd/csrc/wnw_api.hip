@@ -40,9 +40,19 @@ enum State { CREATED = 0, READY = 1, FAILED = 2 };
 // 2 after merge + selection, 3 after the tidal/fixed kernel, 4 once the complements recalled
 // this step have been attended to (same-step timing), 5 after the final merge.  r[] on the side
 // stream around the recall.
+// Streams that share the host-issued copies of one step: copy-engine transfers queued on one
+// stream leave a gap between transfers (3 MB copies reach ~49 of ~57 GB/s on one stream, ~56
+// on four).
+constexpr int N_COPY_STREAMS = 4;
+
 struct StepEvents {
     hipEvent_t e[6];
     hipEvent_t r[2];
+    // next-step timing with host-issued copies: the end of each copy stream's share (the recall
+    // ends with the last of them; joining the streams for one end marker would stall the next
+    // step's copies behind the slowest stream)
+    hipEvent_t rc[N_COPY_STREAMS];
+    bool split;
 };
 
 }  // namespace
@@ -76,9 +86,14 @@ struct wnw_ctx {
     const int32_t *override_sel = nullptr;
 
     hipStream_t side = nullptr;
-    hipEvent_t ev_sel = nullptr, ev_rec = nullptr, ev_nl = nullptr;
+    // host-issued recall: the copies of one step go round-robin to `side` and these streams,
+    // which are joined back into `side` (one stream queues copies with a gap between them)
+    hipStream_t copy_st[N_COPY_STREAMS - 1] = {};
+    hipEvent_t ev_copy[N_COPY_STREAMS] = {};   // end of each stream's copies of the last recall
+    hipEvent_t ev_sel = nullptr, ev_rec = nullptr;
     bool rec_pending = false;          // next-step timing: a recall issued on `side` not yet joined
     int32_t *h_newinfo = nullptr;      // pinned: counts [B][2] then new lists [B][k][2]
+    int32_t *d_newinfo = nullptr;      // the same memory as the device addresses it
 
     std::vector<StepEvents> pending, spare;
     int n_gen = 0;                     // tokens appended (wnw_append_kv)
@@ -383,13 +398,27 @@ void parallel_for(int n, const std::function<void(int)> &fn)
     for (auto &x : th) x.join();
 }
 
+// Waits on the host for an event by polling it: a sleeping wait wakes tens to hundreds of
+// microseconds late, and with host-issued copies the link idles for that long.
+hipError_t poll_event(hipEvent_t e)
+{
+    hipError_t r;
+    while ((r = hipEventQuery(e)) == hipErrorNotReady) {
+    }
+    return r;
+}
+
 // Host-issued recall: one hipMemcpyAsync per run of consecutive chunks landing in consecutive
 // slots, from the counts and new lists staged in h_newinfo (already complete on the host).
+// The runs go round-robin to `st` and the extra copy streams; ev_copy[i] marks the end of each
+// stream's share.  The caller has seen ev_sel complete on the host, so every earlier reader of
+// the target slots has finished and the copies need no device-side wait.
 wnw_status issue_copies(wnw_ctx *c, hipStream_t st)
 {
     const Geometry &g = c->g;
     const int32_t *cnt = c->h_newinfo, *nl = c->h_newinfo + g.B * 2;
     const size_t cb = (size_t)g.chunk_elems * sizeof(uint16_t);
+    int n_runs = 0;
     for (int b = 0; b < g.B && cb; ++b) {
         const int n = cnt[b * 2 + 1];
         for (int i = 0; i < n;) {
@@ -400,17 +429,29 @@ wnw_status issue_copies(wnw_ctx *c, hipStream_t st)
                 if (ej[0] != e0[0] + (j - i) || ej[1] != e0[1] + (j - i)) break;
                 ++j;
             }
+            const int w = n_runs++ % N_COPY_STREAMS;
             HIPCHECK(c, hipMemcpyAsync(c->slots + ((size_t)b * g.n_slots + e0[1]) * g.chunk_elems,
                                        c->host_comp + ((size_t)b * g.nc + e0[0]) * g.chunk_elems, cb * (j - i),
-                                       hipMemcpyHostToDevice, st));
+                                       hipMemcpyHostToDevice, w == 0 ? st : c->copy_st[w - 1]));
             i = j;
         }
     }
+    for (int i = 0; i < N_COPY_STREAMS; ++i)
+        HIPCHECK(c, hipEventRecord(c->ev_copy[i], i == 0 ? st : c->copy_st[i - 1]));
+    return WNW_OK;
+}
+
+// `s` waits for every copy of the last host-issued recall (one hop per copy stream).
+wnw_status wait_copies(wnw_ctx *c, hipStream_t s)
+{
+    for (int i = 0; i < N_COPY_STREAMS; ++i) HIPCHECK(c, hipStreamWaitEvent(s, c->ev_copy[i], 0));
     return WNW_OK;
 }
 
 wnw_status harvest_timing(wnw_ctx *c)
 {
+    const StepEvents *prev = nullptr;
+    int prev_last = 0;
     for (auto &ev : c->pending) {
         float ms;
         HIPCHECK(c, hipEventSynchronize(ev.e[5]));
@@ -420,9 +461,28 @@ wnw_status harvest_timing(wnw_ctx *c)
             HIPCHECK(c, hipEventElapsedTime(&ms, ev.e[from[i]], ev.e[to[i]]));
             c->t_acc[i] += ms;
         }
-        HIPCHECK(c, hipEventSynchronize(ev.r[1]));
-        HIPCHECK(c, hipEventElapsedTime(&ms, ev.r[0], ev.r[1]));
-        c->t_acc[6] += ms;
+        if (ev.split) {
+            float t = 0.f;
+            int last = 0;
+            for (int i = 0; i < N_COPY_STREAMS; ++i) {
+                HIPCHECK(c, hipEventSynchronize(ev.rc[i]));
+                HIPCHECK(c, hipEventElapsedTime(&ms, ev.r[0], ev.rc[i]));
+                if (i == 0 || ms > t) t = ms, last = i;
+            }
+            // this step's copies queue behind the previous step's on each stream: the time
+            // before the previous step's last copy ended is counted there
+            if (prev && prev->split) {
+                HIPCHECK(c, hipEventElapsedTime(&ms, ev.r[0], prev->rc[prev_last]));
+                if (ms > 0.f) t -= ms;
+            }
+            c->t_acc[6] += t > 0.f ? t : 0.f;
+            prev_last = last;
+        } else {
+            HIPCHECK(c, hipEventSynchronize(ev.r[1]));
+            HIPCHECK(c, hipEventElapsedTime(&ms, ev.r[0], ev.r[1]));
+            c->t_acc[6] += ms;
+        }
+        prev = &ev;
         c->timed_steps++;
         c->spare.push_back(ev);
     }
@@ -444,13 +504,17 @@ void free_all(wnw_ctx *c)
     if (c->h_newinfo) (void)hipHostFree(c->h_newinfo);
     if (c->ev_sel) (void)hipEventDestroy(c->ev_sel);
     if (c->ev_rec) (void)hipEventDestroy(c->ev_rec);
-    if (c->ev_nl) (void)hipEventDestroy(c->ev_nl);
     for (auto *v : {&c->pending, &c->spare})
         for (auto &ev : *v) {
             for (auto e : ev.e) (void)hipEventDestroy(e);
             for (auto e : ev.r) (void)hipEventDestroy(e);
+            for (auto e : ev.rc) (void)hipEventDestroy(e);
         }
     if (c->side) (void)hipStreamDestroy(c->side);
+    for (int i = 0; i < N_COPY_STREAMS - 1; ++i)
+        if (c->copy_st[i]) (void)hipStreamDestroy(c->copy_st[i]);
+    for (int i = 0; i < N_COPY_STREAMS; ++i)
+        if (c->ev_copy[i]) (void)hipEventDestroy(c->ev_copy[i]);
 }
 
 }  // namespace
@@ -572,10 +636,20 @@ wnw_status build_tiers(wnw_ctx *c, const uint8_t *keep_all)
         c->t.host_comp = (const uint16_t *)dp;
     }
     HIPCHECK(c, hipHostMalloc((void **)&c->h_newinfo, (B * 2 + B * g.knew * 2 + 1) * sizeof(int32_t), hipHostMallocDefault));
+    {
+        void *dp = nullptr;
+        HIPCHECK(c, hipHostGetDevicePointer(&dp, c->h_newinfo, 0));
+        c->d_newinfo = (int32_t *)dp;
+    }
     HIPCHECK(c, hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking));
+    if (c->cfg.flags & WNW_F_RECALL_MEMCPY) {
+        for (int i = 0; i < N_COPY_STREAMS - 1; ++i)
+            HIPCHECK(c, hipStreamCreateWithFlags(&c->copy_st[i], hipStreamNonBlocking));
+        for (int i = 0; i < N_COPY_STREAMS; ++i)
+            HIPCHECK(c, hipEventCreateWithFlags(&c->ev_copy[i], hipEventDisableTiming));
+    }
     HIPCHECK(c, hipEventCreateWithFlags(&c->ev_sel, hipEventDisableTiming));
     HIPCHECK(c, hipEventCreateWithFlags(&c->ev_rec, hipEventDisableTiming));
-    HIPCHECK(c, hipEventCreateWithFlags(&c->ev_nl, hipEventDisableTiming));
 
     std::vector<int32_t> lk;
     lk.insert(lk.end(), c->anchor_lk.begin(), c->anchor_lk.end());
@@ -870,7 +944,9 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, float *out, float *sco
             // which would slow the kernels that follow and blur the measurement
             for (auto &e : ev.e) HIPCHECK(c, hipEventCreateWithFlags(&e, hipEventDisableSystemFence));
             for (auto &e : ev.r) HIPCHECK(c, hipEventCreateWithFlags(&e, hipEventDisableSystemFence));
+            for (auto &e : ev.rc) HIPCHECK(c, hipEventCreateWithFlags(&e, hipEventDisableSystemFence));
         }
+        ev.split = false;
     }
 #define MARK(i) \
     if (timing) HIPCHECK(c, hipEventRecord(ev.e[i], s0))
@@ -893,6 +969,9 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, float *out, float *sco
     HIPCHECK(c, launch_anchor_combine(g, c->t, sb, out, s0));
     HIPCHECK(c, launch_select(g, sb, sc, c->override_sel, sel, s0));
     const bool memcpy_path = c->cfg.flags & WNW_F_RECALL_MEMCPY;
+    // host-issued copies: the counts and new lists go to mapped pinned memory right after the
+    // selection, on s0, so the host never waits behind copies still running on the side stream
+    if (memcpy_path) HIPCHECK(c, launch_publish_new(g, sb, c->d_newinfo, s0));
     if (g.next_step) {
         // Next-step timing: the chunks that became resident now are copied on the side stream,
         // back to back with the previous step's copies, while this step's tidal heads read only
@@ -901,27 +980,32 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, float *out, float *sco
         HIPCHECK(c, hipEventRecord(c->ev_sel, s0));
         HIPCHECK(c, hipStreamWaitEvent(c->side, c->ev_sel, 0));
         if (timing) HIPCHECK(c, hipEventRecord(ev.r[0], c->side));
-        if (!memcpy_path) {
-            HIPCHECK(c, launch_recall(g, c->t, sb, c->side));
-        } else {
-            HIPCHECK(c, hipMemcpyAsync(c->h_newinfo, sb.counts, g.B * 2 * sizeof(int32_t), hipMemcpyDeviceToHost, c->side));
-            if (g.knew)
-                HIPCHECK(c, hipMemcpyAsync(c->h_newinfo + g.B * 2, sb.new_list, (size_t)g.B * g.knew * 2 * sizeof(int32_t),
-                                           hipMemcpyDeviceToHost, c->side));
-            HIPCHECK(c, hipEventRecord(c->ev_nl, c->side));
-        }
+        if (!memcpy_path) HIPCHECK(c, launch_recall(g, c->t, sb, c->side));
         // this step's tidal heads read the complements the previous step recalled
-        if (c->rec_pending) HIPCHECK(c, hipStreamWaitEvent(s0, c->ev_rec, 0));
+        if (c->rec_pending) {
+            if (memcpy_path) {
+                wnw_status r = wait_copies(c, s0);
+                if (r != WNW_OK) return r;
+            } else {
+                HIPCHECK(c, hipStreamWaitEvent(s0, c->ev_rec, 0));
+            }
+        }
         MARK(2);
         HIPCHECK(c, launch_tidal_fixed(g, c->t, sb, q, false, false, s0));
         MARK(3);
         MARK(4);
         if (memcpy_path) {
-            HIPCHECK(c, hipEventSynchronize(c->ev_nl));
+            // the copy engines queue these behind the previous step's copies: the link stays busy
+            HIPCHECK(c, poll_event(c->ev_sel));
             wnw_status r = issue_copies(c, c->side);
             if (r != WNW_OK) return r;
+            if (timing) {
+                for (int i = 0; i < N_COPY_STREAMS; ++i)
+                    HIPCHECK(c, hipEventRecord(ev.rc[i], i == 0 ? c->side : c->copy_st[i - 1]));
+                ev.split = true;
+            }
         }
-        if (timing) HIPCHECK(c, hipEventRecord(ev.r[1], c->side));
+        if (timing && !memcpy_path) HIPCHECK(c, hipEventRecord(ev.r[1], c->side));
         HIPCHECK(c, hipEventRecord(c->ev_rec, c->side));
         c->rec_pending = true;
     } else if (!memcpy_path) {
@@ -937,10 +1021,6 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, float *out, float *sco
         MARK(3);
         MARK(4);
     } else {
-        HIPCHECK(c, hipMemcpyAsync(c->h_newinfo, sb.counts, g.B * 2 * sizeof(int32_t), hipMemcpyDeviceToHost, s0));
-        if (g.knew)
-            HIPCHECK(c, hipMemcpyAsync(c->h_newinfo + g.B * 2, sb.new_list, (size_t)g.B * g.knew * 2 * sizeof(int32_t),
-                                       hipMemcpyDeviceToHost, s0));
         HIPCHECK(c, hipEventRecord(c->ev_sel, s0));
         MARK(2);
         // (4a) device-resident rows while the host waits for the selection and issues the copies
@@ -950,12 +1030,16 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, float *out, float *sco
         // kernel, which follows every earlier reader on s0; the copies start after ev_sel.
         HIPCHECK(c, hipStreamWaitEvent(c->side, c->ev_sel, 0));
         if (timing) HIPCHECK(c, hipEventRecord(ev.r[0], c->side));
-        HIPCHECK(c, hipEventSynchronize(c->ev_sel));
+        HIPCHECK(c, poll_event(c->ev_sel));
         wnw_status r = issue_copies(c, c->side);
         if (r != WNW_OK) return r;
-        if (timing) HIPCHECK(c, hipEventRecord(ev.r[1], c->side));
-        HIPCHECK(c, hipEventRecord(c->ev_rec, c->side));
-        HIPCHECK(c, hipStreamWaitEvent(s0, c->ev_rec, 0));
+        if (timing) {
+            r = wait_copies(c, c->side);
+            if (r != WNW_OK) return r;
+            HIPCHECK(c, hipEventRecord(ev.r[1], c->side));
+        }
+        r = wait_copies(c, s0);
+        if (r != WNW_OK) return r;
         // (4b) the complements copied this step
         HIPCHECK(c, launch_new_slots(g, c->t, sb, q, s0));
         MARK(4);

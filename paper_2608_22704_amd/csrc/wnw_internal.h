@@ -140,6 +140,8 @@ hipError_t launch_attention(const Geometry &g, const Tiers &t, const StepBuffers
 // Next-step timing: copy of the complements listed for recall from mapped pinned memory into
 // their slots, no attention (they are attended from the next step on).
 hipError_t launch_recall(const Geometry &g, const Tiers &t, const StepBuffers &s, hipStream_t st);
+// counts [B][2] then new lists [B][knew][2] of the step, into mapped pinned memory `host`
+hipError_t launch_publish_new(const Geometry &g, const StepBuffers &s, int32_t *host, hipStream_t st);
 // Complements already copied to their slots by the host-waited recall path.
 hipError_t launch_new_slots(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st);
 hipError_t launch_subset_combine(const Geometry &g, const Tiers &t, const StepBuffers &s, float *out,
