@@ -586,12 +586,21 @@ wnw_status build_tiers(wnw_ctx *c, const uint8_t *keep_all)
     // ---- allocations ------------------------------------------------------------------
 #define ALLOC(p, n, what) \
     if ((r = dalloc(c, &(p), (size_t)(n), what)) != WNW_OK) return r
-    ALLOC(c->aK, B * g.nA * g.Tcap * Dz, "anchor K");
-    ALLOC(c->aV, B * g.nA * g.Tcap * Dz, "anchor V");
-    ALLOC(c->tK, B * g.RsT * Dz, "tidal K");
-    ALLOC(c->tV, B * g.RsT * Dz, "tidal V");
-    ALLOC(c->fK, B * g.RsF * Dz, "fixed K");
-    ALLOC(c->fV, B * g.RsF * Dz, "fixed V");
+    // K/V tiers, each with one zeroed tile of padding rows at the end (the tiles' buffer loads)
+    const size_t pad = (size_t)std::max(TILE_A, TILE_S) * Dz;
+    ALLOC(c->aK, B * g.nA * g.Tcap * Dz + pad, "anchor K");
+    ALLOC(c->aV, B * g.nA * g.Tcap * Dz + pad, "anchor V");
+    ALLOC(c->tK, B * g.RsT * Dz + pad, "tidal K");
+    ALLOC(c->tV, B * g.RsT * Dz + pad, "tidal V");
+    ALLOC(c->fK, B * g.RsF * Dz + pad, "fixed K");
+    ALLOC(c->fV, B * g.RsF * Dz + pad, "fixed V");
+    // anchor rows reserved for appended tokens and every padding tile start out zero
+    HIPCHECK(c, hipMemsetAsync(c->aK, 0, (B * g.nA * g.Tcap * Dz + pad) * sizeof(uint16_t), st));
+    HIPCHECK(c, hipMemsetAsync(c->aV, 0, (B * g.nA * g.Tcap * Dz + pad) * sizeof(uint16_t), st));
+    HIPCHECK(c, hipMemsetAsync(c->tK + B * g.RsT * Dz, 0, pad * sizeof(uint16_t), st));
+    HIPCHECK(c, hipMemsetAsync(c->tV + B * g.RsT * Dz, 0, pad * sizeof(uint16_t), st));
+    HIPCHECK(c, hipMemsetAsync(c->fK + B * g.RsF * Dz, 0, pad * sizeof(uint16_t), st));
+    HIPCHECK(c, hipMemsetAsync(c->fV + B * g.RsF * Dz, 0, pad * sizeof(uint16_t), st));
     ALLOC(c->slots, B * g.n_slots * g.chunk_elems, "recall slots");
     ALLOC(c->d_lk, (size_t)nh, "role tables");
     ALLOC(c->d_hr, c->hrows.size(), "head rows");

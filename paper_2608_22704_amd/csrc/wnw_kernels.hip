@@ -161,6 +161,25 @@ __device__ inline uint4 load_nt(const uint16_t *p)
     return make_uint4(a.x, a.y, a.z, a.w);
 }
 
+// Raw buffer loads for the streamed K/V tiles: the base and the byte count of a head's valid rows
+// sit in scalar registers and each lane adds one 32-bit offset (the row offsets fold into the
+// instruction's immediate), which saves the per-load 64-bit address arithmetic and the zeroing of
+// registers that a conditional load needs; offsets at or past the byte count read zeros.  The
+// K/V arrays also carry zeroed rows past every head's valid rows (reserved rows, a padding tile
+// at the end), so a tile's tail reads finite data inside the allocation in any case.
+// aux 2 = nontemporal (every byte is read once per step).
+__device__ inline __amdgpu_buffer_rsrc_t buf_rsrc(const void *base, unsigned bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+__device__ inline uint4 buf_load_nt(__amdgpu_buffer_rsrc_t r, unsigned off)
+{
+    typedef unsigned v4u __attribute__((ext_vector_type(4)));
+    const v4u a = __builtin_bit_cast(v4u, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 2));
+    return make_uint4(a.x, a.y, a.z, a.w);
+}
+
 // exp(y) for y <= 0 (see above); 0 below 2^-1022
 __device__ inline double exp_nonpos(double y)
 {
@@ -217,15 +236,14 @@ __device__ inline void anchor_tile(const Geometry &g, const Tiers &t, const Step
     for (int u = 0; u < 4; ++u)
         qr[u] = hB < G ? *(const uint4 *)(qh + hB * D + kq * 32 + u * 8) : make_uint4(0, 0, 0, 0);
     uint4 kr[RPL], vr[RPL];
+    {
+        // rows at or past T read zeros
+        const __amdgpu_buffer_rsrc_t rk = buf_rsrc(K, (unsigned)g.T * (D * 2)), rv = buf_rsrc(V, (unsigned)g.T * (D * 2));
+        const unsigned o0 = (unsigned)(t0 + wave * RW + rg) * (D * 2) + sub * 16;
 #pragma unroll
-    for (int i = 0; i < RPL; ++i) {
-        const int row = t0 + wave * RW + i * 4 + rg;
-        kr[i] = row < g.T ? load_nt(K + (size_t)row * D + sub * 8) : make_uint4(0, 0, 0, 0);
-    }
+        for (int i = 0; i < RPL; ++i) kr[i] = buf_load_nt(rk, o0 + i * (4 * D * 2));
 #pragma unroll
-    for (int i = 0; i < RPL; ++i) {
-        const int row = t0 + wave * RW + i * 4 + rg;
-        vr[i] = row < g.T ? load_nt(V + (size_t)row * D + sub * 8) : make_uint4(0, 0, 0, 0);
+        for (int i = 0; i < RPL; ++i) vr[i] = buf_load_nt(rv, o0 + i * (4 * D * 2));
     }
 #pragma unroll
     for (int i = 0; i < RPL; ++i) {
@@ -823,23 +841,36 @@ __device__ inline void subset_tile(const uint16_t *__restrict__ qh, const RowMap
     }
     uint4 kr[RPL], vr[RPL];
     bool ok[RPL];
+    if constexpr (RowMap::contiguous) {
+        // consecutive rows of one head: buffer loads, rows at or past R read zeros
+        const __amdgpu_buffer_rsrc_t rk = buf_rsrc(map.K, (unsigned)map.R * (D * 2));
+        const __amdgpu_buffer_rsrc_t rv = buf_rsrc(map.V, (unsigned)map.R * (D * 2));
+        const unsigned o0 = (unsigned)(map.t0 + wave * NR + rg) * (D * 2) + sub * 16;
 #pragma unroll
-    for (int i = 0; i < RPL; ++i) {
-        const RowPtr rp = map.row(wave * NR + i * 4 + rg);
-        ok[i] = rp.k != nullptr;
-        // device rows stream once (nontemporal); host rows keep plain loads
-        if constexpr (RowMap::copies)
-            kr[i] = ok[i] ? *(const uint4 *)(rp.k + sub * 8) : make_uint4(0, 0, 0, 0);
-        else
-            kr[i] = ok[i] ? load_nt(rp.k + sub * 8) : make_uint4(0, 0, 0, 0);
-    }
+        for (int i = 0; i < RPL; ++i) kr[i] = buf_load_nt(rk, o0 + i * (4 * D * 2));
 #pragma unroll
-    for (int i = 0; i < RPL; ++i) {
-        const RowPtr rp = map.row(wave * NR + i * 4 + rg);
-        if constexpr (RowMap::copies)
-            vr[i] = ok[i] ? *(const uint4 *)(rp.v + sub * 8) : make_uint4(0, 0, 0, 0);
-        else
-            vr[i] = ok[i] ? load_nt(rp.v + sub * 8) : make_uint4(0, 0, 0, 0);
+        for (int i = 0; i < RPL; ++i) vr[i] = buf_load_nt(rv, o0 + i * (4 * D * 2));
+#pragma unroll
+        for (int i = 0; i < RPL; ++i) ok[i] = map.t0 + wave * NR + i * 4 + rg < map.R;
+    } else {
+#pragma unroll
+        for (int i = 0; i < RPL; ++i) {
+            const RowPtr rp = map.row(wave * NR + i * 4 + rg);
+            ok[i] = rp.k != nullptr;
+            // device rows stream once (nontemporal); host rows keep plain loads
+            if constexpr (RowMap::copies)
+                kr[i] = ok[i] ? *(const uint4 *)(rp.k + sub * 8) : make_uint4(0, 0, 0, 0);
+            else
+                kr[i] = ok[i] ? load_nt(rp.k + sub * 8) : make_uint4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < RPL; ++i) {
+            const RowPtr rp = map.row(wave * NR + i * 4 + rg);
+            if constexpr (RowMap::copies)
+                vr[i] = ok[i] ? *(const uint4 *)(rp.v + sub * 8) : make_uint4(0, 0, 0, 0);
+            else
+                vr[i] = ok[i] ? load_nt(rp.v + sub * 8) : make_uint4(0, 0, 0, 0);
+        }
     }
     if constexpr (RowMap::copies) {
         // rows read from host memory are also written to their device slot on the way
@@ -1009,7 +1040,7 @@ __device__ inline void subset_tile(const uint16_t *__restrict__ qh, const RowMap
 }
 
 struct StaticRows {
-    static constexpr bool copies = false;
+    static constexpr bool copies = false, contiguous = true;
     const uint16_t *K, *V;
     int t0, R;
     __device__ RowPtr row(int r) const
@@ -1023,7 +1054,7 @@ struct StaticRows {
 // Rows of a group of resident complements.  The group's entries are staged in shared memory as
 // (K row base, valid rows) so that the row map needs no global load.
 struct SlotRows {
-    static constexpr bool copies = false;
+    static constexpr bool copies = false, contiguous = false;
     const uint16_t *const *kbase;   // [sg] first K row of the tidal head in the entry's slot
     const int *nrows;               // [sg] valid rows of the entry (complement length)
     int n_entries, comp_max;
@@ -1040,7 +1071,7 @@ struct SlotRows {
 // then comp_max V rows, of which the first nrows are valid.  They are read from the mapped pinned
 // host block and copied through to the device slot on the way.
 struct RecallRows {
-    static constexpr bool copies = true;
+    static constexpr bool copies = true, contiguous = false;
     const uint16_t *src;     // host block
     uint16_t *dst;           // device slot block, same layout
     int nrows, comp_max;
