@@ -976,11 +976,12 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, float *out, float *sco
     else
         HIPCHECK(c, launch_anchor(g, c->t, sb, q, s0, e0, e1));
     HIPCHECK(c, launch_anchor_combine(g, c->t, sb, out, s0));
-    HIPCHECK(c, launch_select(g, sb, sc, c->override_sel, sel, s0));
     const bool memcpy_path = c->cfg.flags & WNW_F_RECALL_MEMCPY;
-    // host-issued copies: the counts and new lists go to mapped pinned memory right after the
-    // selection, on s0, so the host never waits behind copies still running on the side stream
-    if (memcpy_path) HIPCHECK(c, launch_publish_new(g, sb, c->d_newinfo, s0));
+    // host-issued copies: the select kernel also writes the counts and new lists to mapped pinned
+    // memory, so the host reads them once the selection is done, never behind copies still
+    // running on the side streams
+    sb.pub = memcpy_path ? c->d_newinfo : nullptr;
+    HIPCHECK(c, launch_select(g, sb, sc, c->override_sel, sel, s0));
     if (g.next_step) {
         // Next-step timing: the chunks that became resident now are copied on the side stream,
         // back to back with the previous step's copies, while this step's tidal heads read only

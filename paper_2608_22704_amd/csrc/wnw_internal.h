@@ -109,6 +109,8 @@ struct StepBuffers {
     int32_t *kept_list;         // [B][n_slots][2] (segment, slot) attended from a filled slot
     int32_t *new_list;          // [B][knew][2]    (segment, slot) newly resident this step
     int32_t *counts;            // [B][2] kept, new
+    int32_t *pub;               // host-issued recall: mapped pinned mirror of counts [B][2] and new
+                                // lists [B][knew][2], written by the select kernel; else null
     unsigned long long *stats;  // [8] recalled, dropped, resident, slot_rows, peak, exhausted, revived
     const int32_t *seg_rows;    // [B][nc] complement rows of a segment over the tidal heads
 };
@@ -140,8 +142,6 @@ hipError_t launch_attention(const Geometry &g, const Tiers &t, const StepBuffers
 // Next-step timing: copy of the complements listed for recall from mapped pinned memory into
 // their slots, no attention (they are attended from the next step on).
 hipError_t launch_recall(const Geometry &g, const Tiers &t, const StepBuffers &s, hipStream_t st);
-// counts [B][2] then new lists [B][knew][2] of the step, into mapped pinned memory `host`
-hipError_t launch_publish_new(const Geometry &g, const StepBuffers &s, int32_t *host, hipStream_t st);
 // Complements already copied to their slots by the host-waited recall path.
 hipError_t launch_new_slots(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st);
 hipError_t launch_subset_combine(const Geometry &g, const Tiers &t, const StepBuffers &s, float *out,

@@ -754,6 +754,12 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
             sdata[slot] = u;
             nl[rank[u] * 2] = u;
             nl[rank[u] * 2 + 1] = slot;
+            if (s.pub) {
+                // the host reads this mirror once the step's selection event has completed
+                int32_t *hl = s.pub + g.B * 2 + (size_t)b * g.knew * 2;
+                hl[rank[u] * 2] = u;
+                hl[rank[u] * 2 + 1] = slot;
+            }
         }
     __syncthreads();
 
@@ -772,6 +778,10 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
         const int nn = min(nnew, min(nfree, g.knew));
         s.counts[b * 2] = nkept;
         s.counts[b * 2 + 1] = nn;
+        if (s.pub) {
+            s.pub[b * 2] = nkept;
+            s.pub[b * 2 + 1] = nn;
+        }
         s.step[b] = step + 1;
         atomicAdd(&s.stats[0], (unsigned long long)nn);
         atomicAdd(&s.stats[1], (unsigned long long)ndrop);
@@ -1272,18 +1282,6 @@ __global__ __launch_bounds__(NT) void recall_copy_kernel(Geometry g, Tiers t, St
     }
 }
 
-// Host-issued recall: the step's counts and new lists, written into mapped pinned memory by
-// plain vector stores, so the host can read them as soon as the selection is done without a
-// copy-engine transfer queued behind the previous step's recall.
-__global__ __launch_bounds__(256) void publish_new_kernel(const int32_t *__restrict__ counts,
-                                                          const int32_t *__restrict__ new_list, int32_t *host,
-                                                          int n_counts, int n_list)
-{
-    for (int i = threadIdx.x; i < n_counts + n_list; i += blockDim.x)
-        host[i] = i < n_counts ? counts[i] : new_list[i - n_counts];
-    __threadfence_system();
-}
-
 // Complements copied by hipMemcpyAsync (host-waited recall path): one entry per work-group.
 template <int G, int RPL>
 __global__ __launch_bounds__(NT, RPL == RPL_S ? 4 : 2) void new_slots_kernel(Geometry g, Tiers t, StepBuffers s, const uint16_t *__restrict__ q)
@@ -1572,13 +1570,6 @@ hipError_t launch_recall(const Geometry &g, const Tiers &t, const StepBuffers &s
 {
     if (g.nT == 0 || g.k == 0 || g.comp_max == 0) return hipSuccess;
     hipLaunchKernelGGL(recall_copy_kernel, dim3(RECALL_WGS), dim3(NT), 0, st, g, t, s);
-    return hipGetLastError();
-}
-
-hipError_t launch_publish_new(const Geometry &g, const StepBuffers &s, int32_t *host, hipStream_t st)
-{
-    hipLaunchKernelGGL(publish_new_kernel, dim3(1), dim3(256), 0, st, s.counts, s.new_list, host, g.B * 2,
-                       g.B * g.knew * 2);
     return hipGetLastError();
 }
 
