@@ -862,6 +862,23 @@ __device__ inline void subset_tile(const uint16_t *__restrict__ qh, const RowMap
         for (int i = 0; i < RPL; ++i) vr[i] = buf_load_nt(rv, o0 + i * (4 * D * 2));
 #pragma unroll
         for (int i = 0; i < RPL; ++i) ok[i] = map.t0 + wave * NR + i * 4 + rg < map.R;
+    } else if constexpr (RowMap::offsets) {
+        // rows of several slot entries: offsets in the sequence's slot region; each lane walks
+        // its rows (stride 4) through the entries with one division.  Rows past the group's
+        // entries or past an entry's valid rows read the first row of entry 0 (finite, masked).
+        const __amdgpu_buffer_rsrc_t rs = buf_rsrc(map.base, map.bytes);
+        const int cm = map.comp_max;
+        const unsigned vd = (unsigned)cm * (D * 2);   // an entry's V rows follow its K rows
+        int e = (wave * NR + rg) / cm, rr = wave * NR + rg - e * cm;
+#pragma unroll
+        for (int i = 0; i < RPL; ++i) {
+            ok[i] = e < map.n_entries && rr < map.nrows[e < map.n_entries ? e : 0];
+            const unsigned o = (ok[i] ? map.koff[e] + (unsigned)rr * (D * 2) : map.koff[0]) + sub * 16;
+            kr[i] = buf_load_nt(rs, o);
+            vr[i] = buf_load_nt(rs, o + vd);
+            rr += 4;
+            while (rr >= cm) rr -= cm, ++e;
+        }
     } else {
 #pragma unroll
         for (int i = 0; i < RPL; ++i) {
@@ -881,6 +898,13 @@ __device__ inline void subset_tile(const uint16_t *__restrict__ qh, const RowMap
             else
                 vr[i] = ok[i] ? load_nt(rp.v + sub * 8) : make_uint4(0, 0, 0, 0);
         }
+    }
+    // valid rows of this wavefront as a mask (bit i * 4 + rg), for the logits
+    unsigned long long rowmask = 0;
+#pragma unroll
+    for (int i = 0; i < RPL; ++i) {
+        const unsigned long long bal = __ballot(ok[i]);   // lane rg * 16 + sub; a row's lanes agree
+        rowmask |= ((bal & 1ull) | ((bal >> 15) & 2ull) | ((bal >> 30) & 4ull) | ((bal >> 45) & 8ull)) << (i * 4);
     }
     if constexpr (RowMap::copies) {
         // rows read from host memory are also written to their device slot on the way
@@ -939,8 +963,8 @@ __device__ inline void subset_tile(const uint16_t *__restrict__ qh, const RowMap
             for (int i = 0; i < 4; ++i) {
                 float x = lg[sb][hs][i];
                 x += __shfl_xor(x, 32);
-                const int r = wave * NR + sb * 32 + 4 * kb + i;
-                x = (hv && map.row(r).k != nullptr) ? x * SCALE_F : -INFINITY;
+                const int r = sb * 32 + 4 * kb + i;   // row of this wavefront
+                x = (hv && ((rowmask >> r) & 1ull)) ? x * SCALE_F : -INFINITY;
                 lg[sb][hs][i] = x;
                 mm = fmaxf(mm, x);
             }
@@ -1050,7 +1074,7 @@ __device__ inline void subset_tile(const uint16_t *__restrict__ qh, const RowMap
 }
 
 struct StaticRows {
-    static constexpr bool copies = false, contiguous = true;
+    static constexpr bool copies = false, contiguous = true, offsets = false;
     const uint16_t *K, *V;
     int t0, R;
     __device__ RowPtr row(int r) const
@@ -1064,7 +1088,7 @@ struct StaticRows {
 // Rows of a group of resident complements.  The group's entries are staged in shared memory as
 // (K row base, valid rows) so that the row map needs no global load.
 struct SlotRows {
-    static constexpr bool copies = false, contiguous = false;
+    static constexpr bool copies = false, contiguous = false, offsets = false;
     const uint16_t *const *kbase;   // [sg] first K row of the tidal head in the entry's slot
     const int *nrows;               // [sg] valid rows of the entry (complement length)
     int n_entries, comp_max;
@@ -1077,11 +1101,22 @@ struct SlotRows {
     }
 };
 
+// The same rows as byte offsets in the sequence's slot region (buffer loads; used while the
+// region stays below 4 GB).
+struct SlotRowsOff {
+    static constexpr bool copies = false, contiguous = false, offsets = true;
+    const uint16_t *base;           // the sequence's first slot
+    unsigned bytes;                 // its slot region
+    const unsigned *koff;           // [sg] byte offset of the entry's first K row of the tidal head
+    const int *nrows;               // [sg] valid rows of the entry (complement length)
+    int n_entries, comp_max;
+};
+
 // Rows of one recalled complement block (a tidal head's complement of one chunk): comp_max K rows,
 // then comp_max V rows, of which the first nrows are valid.  They are read from the mapped pinned
 // host block and copied through to the device slot on the way.
 struct RecallRows {
-    static constexpr bool copies = true, contiguous = false;
+    static constexpr bool copies = true, contiguous = false, offsets = false;
     const uint16_t *src;     // host block
     uint16_t *dst;           // device slot block, same layout
     int nrows, comp_max;
@@ -1135,21 +1170,32 @@ __device__ inline void slot_group(const Geometry &g, const Tiers &t, const StepB
     if (hr.cfull == 0 || (!which && grp >= hr.ngk) || grp * epg >= cnt) return;
     constexpr int MAXE = 4 * RPL * WAVES;   // entries of one group never exceed its rows
     __shared__ const uint16_t *kbase[MAXE];
+    __shared__ unsigned koff[MAXE];
     __shared__ int nrows[MAXE];
     const int n_entries = min(epg, cnt - grp * epg);
     const int32_t *list = (which ? s.new_list + (size_t)b * g.knew * 2 : s.kept_list + (size_t)b * g.n_slots * 2) +
                           (size_t)grp * epg * 2;
+    const uint16_t *region = t.slots + (size_t)b * g.n_slots * g.chunk_elems;
+    const size_t region_bytes = (size_t)g.n_slots * g.chunk_elems * sizeof(uint16_t);
+    const bool by_offset = region_bytes < 0xffffffffull;
     for (int e = threadIdx.x; e < n_entries; e += NT) {
         const int c = list[e * 2], slot = list[e * 2 + 1];
-        kbase[e] = t.slots + ((size_t)b * g.n_slots + slot) * g.chunk_elems + (size_t)hr.coff * D;
+        const size_t o = (size_t)slot * g.chunk_elems + (size_t)hr.coff * D;
+        kbase[e] = region + o;
+        koff[e] = (unsigned)(o * sizeof(uint16_t));
         nrows[e] = t.comp_rows[((size_t)b * g.nc + c) * g.nT + ti];
     }
     __syncthreads();
     const int lk = t.tidal_lk[ti], l = lk / g.Hkv, kv = lk - l * g.Hkv;
-    const SlotRows map{kbase, nrows, n_entries, hr.cfull};
     const uint16_t *qh = q + (((size_t)b * g.L + l) * g.Hq + (size_t)kv * G) * D;
     const size_t p = (size_t)b * g.P + hr.pbase + hr.nts + (which ? hr.ngk : 0) + grp;
-    subset_tile<G, RPL>(qh, map, s.ps_m + p * G, s.ps_l + p * G, s.ps_o + p * G * D, sm);
+    if (by_offset) {
+        const SlotRowsOff map{region, (unsigned)region_bytes, koff, nrows, n_entries, hr.cfull};
+        subset_tile<G, RPL>(qh, map, s.ps_m + p * G, s.ps_l + p * G, s.ps_o + p * G * D, sm);
+    } else {
+        const SlotRows map{kbase, nrows, n_entries, hr.cfull};
+        subset_tile<G, RPL>(qh, map, s.ps_m + p * G, s.ps_l + p * G, s.ps_o + p * G * D, sm);
+    }
 }
 
 // Recall work-group w of nw: walks the units (sequence, new entry, tidal head); each unit's
