@@ -263,6 +263,13 @@ wnw_status wnw_debug_read_host_chunk(wnw_ctx *ctx, int32_t b, int32_t chunk, voi
  * WNW_F_SELECT_NEXT_STEP (waits for the device). */
 wnw_status wnw_debug_read_resident(wnw_ctx *ctx, uint8_t *host_dst);
 
+/* Slot groups of a sequence whose slot region (n_slots * chunk_bytes) has `bytes` or more read
+ * their rows through per-row pointers instead of 32-bit buffer offsets.  The default,
+ * 4294967295, is the largest region buffer offsets can address; 0 forces the pointer path
+ * everywhere.  Both paths compute the same results.  Takes effect from the next step;
+ * WNW_ERR_INVALID for a negative value. */
+wnw_status wnw_debug_set_slot_offset_limit(wnw_ctx *ctx, int64_t bytes);
+
 /* Message of the last failure on ctx (or of this thread when ctx is NULL).  Never NULL. */
 const char *wnw_last_error(const wnw_ctx *ctx);
 

@@ -179,6 +179,7 @@ wnw_status derive(wnw_ctx *c, const wnw_config &cfg, Geometry &g)
         return fail(c, WNW_ERR_UNSUPPORTED, "segments of %d positions > %d", cfg.chunk_len / span, MAX_CHUNK);
 
     g = Geometry{};
+    g.slot_off_max = 0xffffffffll;
     g.B = cfg.batch;
     g.L = cfg.layers;
     g.Hq = cfg.q_heads;
@@ -1158,6 +1159,14 @@ wnw_status wnw_set_selection_override(wnw_ctx *c, const int32_t *sel_dev)
 {
     if (!c) return fail(nullptr, WNW_ERR_INVALID, "ctx is NULL");
     c->override_sel = sel_dev;
+    return WNW_OK;
+}
+
+wnw_status wnw_debug_set_slot_offset_limit(wnw_ctx *c, int64_t bytes)
+{
+    if (!c) return fail(nullptr, WNW_ERR_INVALID, "ctx is NULL");
+    if (bytes < 0) return fail(c, WNW_ERR_INVALID, "slot offset limit must be >= 0");
+    c->g.slot_off_max = std::min<int64_t>(bytes, 0xffffffffll);
     return WNW_OK;
 }
 

@@ -44,6 +44,7 @@ struct Geometry {
     int slot_tile;              // rows of one slot-group work-group (TILE_S or 2 * TILE_S)
     int ng_kept;                // kept-slot groups of the head with the most
     int64_t chunk_elems;        // bf16 elements of one segment's complement block (blk_rows * D)
+    int64_t slot_off_max;       // slot regions below this many bytes use buffer offsets
 };
 
 // Rows of one non-anchor head (tidal heads 0..nT-1, then fixed heads), whose audio retention

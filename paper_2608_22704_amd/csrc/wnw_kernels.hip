@@ -1177,7 +1177,7 @@ __device__ inline void slot_group(const Geometry &g, const Tiers &t, const StepB
                           (size_t)grp * epg * 2;
     const uint16_t *region = t.slots + (size_t)b * g.n_slots * g.chunk_elems;
     const size_t region_bytes = (size_t)g.n_slots * g.chunk_elems * sizeof(uint16_t);
-    const bool by_offset = region_bytes < 0xffffffffull;
+    const bool by_offset = (long long)region_bytes < g.slot_off_max;   // at most 4294967295
     for (int e = threadIdx.x; e < n_entries; e += NT) {
         const int c = list[e * 2], slot = list[e * 2 + 1];
         const size_t o = (size_t)slot * g.chunk_elems + (size_t)hr.coff * D;

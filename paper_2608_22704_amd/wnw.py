@@ -23,6 +23,7 @@ EXPORTS = ("wnw_init_cache", "wnw_set_retention", "wnw_set_roles", "wnw_prefill_
            "wnw_append_kv", "wnw_decode_step", "wnw_query_geometry",
            "wnw_query_segments", "wnw_query_head_keep", "wnw_get_stats",
            "wnw_set_selection_override", "wnw_debug_read_slot", "wnw_debug_read_host_chunk",
+           "wnw_debug_set_slot_offset_limit",
            "wnw_debug_read_resident", "wnw_last_error", "wnw_destroy", "wnw_voice_hits", "wnw_key_sensitivity",
            "wnw_triage", "wnw_triage_last_error")
 
@@ -79,6 +80,7 @@ def _load():
         "wnw_debug_read_slot": ([P, I32, I32, P, SZ], C.c_int),
         "wnw_debug_read_host_chunk": ([P, I32, I32, P, SZ], C.c_int),
         "wnw_debug_read_resident": ([P, P], C.c_int),
+        "wnw_debug_set_slot_offset_limit": ([P, I64], C.c_int),
         "wnw_last_error": ([P], C.c_char_p),
         "wnw_destroy": ([P], None),
     }
@@ -211,6 +213,10 @@ def wnw_get_stats(ctx) -> dict:
 
 def wnw_set_selection_override(ctx, sel_dev):
     _check(lib.wnw_set_selection_override(ctx, _ptr(sel_dev)), ctx)
+
+
+def wnw_debug_set_slot_offset_limit(ctx, nbytes: int):
+    _check(lib.wnw_debug_set_slot_offset_limit(ctx, nbytes), ctx)
 
 
 def wnw_debug_read_slot(ctx, b: int, chunk: int, host_dst, nbytes: int):

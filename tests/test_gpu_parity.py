@@ -291,6 +291,29 @@ def test_next_step_memcpy_recall_path():
          flags=_next(W.WNW_F_RECALL_MEMCPY))
 
 
+@pytest.mark.parametrize("timing", ["same", "next"])
+def test_slot_rows_pointer_path(timing):
+    """Slot groups read through per-row pointers (forced by a zero slot offset limit; the default
+    takes buffer offsets below 4 GB of slots) match the oracle and, bit for bit, the offset path
+    on the same steps."""
+    from paper_2608_22704_amd import wnw as W
+    from tests.wnw_harness import Lockstep, log
+    w = _small(f"slot_ptr_{timing}", 190 if timing == "same" else 191, L=2, Hq=8, Hkv=4, Ta=480, Tt=5, cl=16,
+               steps=10)
+    flags = _next() if timing == "next" else 0
+    log(f"[case] slot rows through pointers vs buffer offsets, {timing}-step timing")
+    h, h2 = Lockstep(w, flags=flags), Lockstep(w, flags=flags)
+    try:
+        W.wnw_debug_set_slot_offset_limit(h.ctx, 0)
+        for s in range(w.steps):
+            h.step(s)
+            ref = h2.gpu_step(s)[0]
+            assert np.array_equal(h.out.cpu().numpy(), ref), f"step {s}: pointer and offset paths differ"
+    finally:
+        h.close()
+        h2.close()
+
+
 def test_next_step_qwen_shaped_all_steps():
     _run(configs.QWEN_10MIN, flags=_next())
 
