@@ -1016,8 +1016,10 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, float *out, float *sco
                 ev.split = true;
             }
         }
-        if (timing && !memcpy_path) HIPCHECK(c, hipEventRecord(ev.r[1], c->side));
-        HIPCHECK(c, hipEventRecord(c->ev_rec, c->side));
+        if (!memcpy_path) {
+            if (timing) HIPCHECK(c, hipEventRecord(ev.r[1], c->side));
+            HIPCHECK(c, hipEventRecord(c->ev_rec, c->side));   // host-issued copies: ev_copy[] instead
+        }
         c->rec_pending = true;
     } else if (!memcpy_path) {
         MARK(2);
