@@ -32,6 +32,13 @@ constexpr int CS_KEYS = 128;                          // audio keys per pass-2 w
 constexpr int TILE = 64;                              // rows staged in LDS per iteration
 constexpr int PADU = D / 8 + 1;                       // uint4 per staged row: 16 + 1 of padding
 
+// 2^x by the hardware instruction alone: outputs below 2^-126 flush to zero (exp2f adds a
+// range fix-up of ~3 instructions per call for them).
+__device__ inline float exp2_hw(float x)
+{
+    return __builtin_amdgcn_exp2f(x);
+}
+
 __device__ inline bf16x8_t as_bf8(uint4 u)
 {
     return __builtin_bit_cast(bf16x8_t, u);
@@ -140,12 +147,29 @@ __global__ __launch_bounds__(NT) void prefill_rowstats_kernel(Geometry g, const 
                 f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int kk = 0; kk < 4; ++kk) acc = mfma16(qf[rb][kk], kf[kk], acc);
-                x[rb][kb] = acc * C2;
+                x[rb][kb] = acc;   // unscaled; the scale folds into the exponent's FMA
             }
         }
-        // keys past a row's causal limit (text rows after its token, rows past the end, keys
-        // past the cache) drop out; tiles entirely inside the audio need no mask
-        if (k0 + TILE > g.Ta) {
+        // One rescale per row and tile (the lane's four keys of the tile at once).  Statistics
+        // are base 2 and scaled; every row sum holds its maximum term 2^0, so exponentials that
+        // flush below 2^-126 change nothing.
+        if (k0 + TILE <= g.Ta) {
+            // audio tile: every key visible to every row, no mask; m is finite after it
+#pragma unroll
+            for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float mt = fmaxf(fmaxf(x[rb][0][i], x[rb][1][i]), fmaxf(x[rb][2][i], x[rb][3][i]));
+                    const float mn = fmaxf(m[rb][i], mt * C2);
+                    float acc = s[rb][i] * exp2_hw(m[rb][i] - mn);   // 0 before the first tile
+#pragma unroll
+                    for (int kb = 0; kb < TILE / 16; ++kb) acc += exp2_hw(fmaf(x[rb][kb][i], C2, -mn));
+                    s[rb][i] = acc;
+                    m[rb][i] = mn;
+                }
+        } else {
+            // keys past a row's causal limit (text rows after its token, rows past the end, keys
+            // past the cache) drop out
 #pragma unroll
             for (int kb = 0; kb < TILE / 16; ++kb) {
                 const int key = k0 + kb * 16 + col;
@@ -155,23 +179,22 @@ __global__ __launch_bounds__(NT) void prefill_rowstats_kernel(Geometry g, const 
                     for (int i = 0; i < 4; ++i)
                         if (key > lim[rb][i]) x[rb][kb][i] = -INFINITY;
             }
+#pragma unroll
+            for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    float mt = x[rb][0][i];
+#pragma unroll
+                    for (int kb = 1; kb < TILE / 16; ++kb) mt = fmaxf(mt, x[rb][kb][i]);
+                    if (mt == -INFINITY) continue;   // every key of the tile masked for this row
+                    const float mn = fmaxf(m[rb][i], mt * C2);
+                    float acc = s[rb][i] * exp2_hw(m[rb][i] - mn);   // exp2(-inf) = 0 for an empty row
+#pragma unroll
+                    for (int kb = 0; kb < TILE / 16; ++kb) acc += exp2_hw(fmaf(x[rb][kb][i], C2, -mn));
+                    s[rb][i] = acc;
+                    m[rb][i] = mn;
+                }
         }
-        // one rescale per row and tile: the lane's four keys of the tile at once
-#pragma unroll
-        for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                float mt = x[rb][0][i];
-#pragma unroll
-                for (int kb = 1; kb < TILE / 16; ++kb) mt = fmaxf(mt, x[rb][kb][i]);
-                if (mt == -INFINITY) continue;   // every key of the tile masked for this row
-                const float mn = fmaxf(m[rb][i], mt);
-                float acc = s[rb][i] * exp2f(m[rb][i] - mn);   // exp2(-inf) = 0 for an empty row
-#pragma unroll
-                for (int kb = 0; kb < TILE / 16; ++kb) acc += exp2f(x[rb][kb][i] - mn);
-                s[rb][i] = acc;
-                m[rb][i] = mn;
-            }
         if (more) tile_store(kbuf[(it + 1) & 1], pre);
         __syncthreads();
     }
@@ -227,8 +250,11 @@ __global__ __launch_bounds__(NT) void prefill_colsum_kernel(Geometry g, const ui
     __shared__ float sbuf[2][TILE];
     uint4 pre[SPT];
     float pl = 0.f;
-    // a padding row adds exp2(-inf) = 0
-    auto lse_of = [&](int r) { return r < R ? lse[qbase + r] : INFINITY; };
+    // Terms are taken as 2^(x - lse + 64) and the sum scaled by 2^-64 at the end, so that terms
+    // below 2^-126 still count without the exponential's range fix-up (terms are at most 1 and
+    // sums of at most R of them stay far below the fp32 range).  sbuf holds 64 - lse; a padding
+    // row holds -inf and adds 0.
+    auto lse_of = [&](int r) { return r < R ? 64.f - lse[qbase + r] : -INFINITY; };
     tile_load(pre, Qh, 0, R);
     tile_store(qbuf[0], pre);
     if (threadIdx.x < TILE) sbuf[0][threadIdx.x] = lse_of(threadIdx.x);
@@ -255,7 +281,7 @@ __global__ __launch_bounds__(NT) void prefill_colsum_kernel(Geometry g, const ui
 #pragma unroll
                 for (int kk = 0; kk < 4; ++kk) sc = mfma16(qf[kk], kf[kb][kk], sc);
 #pragma unroll
-                for (int i = 0; i < 4; ++i) acc[kb] += exp2f(fmaf(sc[i], C2, -st[i]));
+                for (int i = 0; i < 4; ++i) acc[kb] += exp2_hw(fmaf(sc[i], C2, st[i]));
             }
         }
         if (more) {
@@ -273,7 +299,7 @@ __global__ __launch_bounds__(NT) void prefill_colsum_kernel(Geometry g, const ui
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
             const int key = kw + kb * 16 + col;
-            if (key < g.Ta) p[(size_t)hd * g.Ta + key] = acc[kb];
+            if (key < g.Ta) p[(size_t)hd * g.Ta + key] = ldexpf(acc[kb], -64);
         }
 }
 
