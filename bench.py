@@ -30,7 +30,7 @@ METRIC = "WnW decode steps/sec + achieved HBM GB/s (attn) at 15k audio tokens, 1
 PEAK_HBM_GBPS = 8000.0
 PEAK_BF16_TFLOPS = 2500.0      # dense bf16 MFMA
 PEAK_LINK_GBPS = 64.0          # PCIe 5.0 x16, one direction
-PEAK_FP64_TFLOPS = 78.6        # fp64 vector
+PEAK_FP64_TFLOPS = 78.6        # fp64, matrix cores (the vector rate is the same)
 
 
 def log(msg):
@@ -451,7 +451,7 @@ def triage_bench(W, torch, w, kd, n_tok=64, reps=5):
     del grad
     log(f"[bench] triage: voice hits {vh:.3f} ms, key sensitivity {ks:.3f} ms")
     return {"voice_hits_ms": vh, "voice_hits_tokens": n_tok, "voice_hits_tflops": flop / (vh * 1e-3) / 1e12,
-            "voice_hits_frac": flop / (vh * 1e-3) / 1e12 / PEAK_FP64_TFLOPS, "voice_hits_bound": "fp64 alu",
+            "voice_hits_frac": flop / (vh * 1e-3) / 1e12 / PEAK_FP64_TFLOPS, "voice_hits_bound": "fp64 mfma",
             "key_sensitivity_ms": ks, "key_sensitivity_GBps": nbytes / (ks * 1e-3) / 1e9,
             "key_sensitivity_frac": nbytes / (ks * 1e-3) / 1e9 / PEAK_HBM_GBPS,
             "note": "offline calibration arithmetic on synthetic inputs; one sample, K = 4"}

@@ -24,11 +24,9 @@ namespace wnw {
 
 namespace {
 
-constexpr int VH_ROWS = 64;   // (token, q-head) rows per work-group
-constexpr int VH_SPLIT = 4;   // threads per row; key tau goes to thread tau % 4 of its tile
-constexpr int VH_TILE = 64;   // keys staged in LDS per iteration
+constexpr int VH_ROWS = 64;   // (token, q-head) rows per work-group (16 per wavefront)
+constexpr int VH_TILE = 32;   // keys staged in LDS per iteration (as doubles)
 constexpr int VH_KMAX = 8;    // largest K (the paper uses 4 and 8)
-constexpr int PADU = D / 8 + 1;
 
 __device__ inline void bf16x2(uint32_t u, double &lo, double &hi)
 {
@@ -36,28 +34,45 @@ __device__ inline void bf16x2(uint32_t u, double &lo, double &hi)
     hi = (double)__uint_as_float(u & 0xffff0000u);
 }
 
-// Grid (ceil(n_tok / tpb), L * Hkv), tpb = VH_ROWS / g tokens per work-group.  Thread (row r,
-// split s): row r = token tt * g + q-head j; the thread scans the keys s, s + 4, ... of each tile
-// and keeps its best eight (value descending; equal values keep the earlier, lower, position).
-// The four lists of a row are merged at the end.
-__global__ __launch_bounds__(NT) void voice_hits_kernel(int L, int Hq, int Hkv, int T, int Ta, int n_tok, int K,
+// Work-groups: ceil(n_tok * g / VH_ROWS) row blocks per KV-head (row = answer token * g + q-head
+// of the group), in XCD order so that the row blocks of one KV-head read its keys through one L2.
+// Wavefront w owns 16 rows of the block.  The logits run on v_mfma_f64_4x4x4f64 (four 4x4x4
+// blocks; lane l = 16k + 4*blk + x holds A_blk[x][k] and B_blk[k][x], and D_blk[i][j] lands in
+// lane 16i + 4*blk + j): A holds the query rows (row 4*blk + x, converted to double once), B four
+// keys shared by the four blocks, and lane k feeds dimension 32k + s to step s, so one key's
+// 64 contiguous bytes per lane come from the staged tile.  Each lane ends a key group holding one
+// logit (row 4*blk + i, key j) and keeps the best eight of the keys it sees (value descending;
+// equal values keep the earlier, lower, position); the four lists of a row are merged at the end.
+// Products of bf16 values are exact in double; two dimension halves and two key groups make four
+// independent accumulation chains.
+__device__ inline int vh_xcd_order(int w, int n)
+{
+    const int q = n / 8, r = n % 8, x = w % 8;
+    return x * q + min(x, r) + w / 8;
+}
+
+__global__ __launch_bounds__(NT, 4) void voice_hits_kernel(int L, int Hq, int Hkv, int T, int Ta, int n_tok, int K,
                                                        const uint16_t *__restrict__ k, const uint16_t *__restrict__ q,
                                                        const int32_t *__restrict__ span, int32_t *__restrict__ hits)
 {
-    const int g = Hq / Hkv, tpb = VH_ROWS / g, lk = blockIdx.y, l = lk / Hkv, kv = lk - l * Hkv;
-    const int tid = threadIdx.x, r = tid / VH_SPLIT, sp = tid % VH_SPLIT;
-    const int tt = r / g, j = r - tt * g, t = blockIdx.x * tpb + tt;
-    const bool active = tt < tpb && t < n_tok;
-    uint32_t qv[D / 2];
+    const int g = Hq / Hkv, R = n_tok * g, nrb = (R + VH_ROWS - 1) / VH_ROWS;
+    const int v = vh_xcd_order(blockIdx.x, gridDim.x), lk = v / nrb, rblk = v - lk * nrb;
+    const int l = lk / Hkv, kv = lk - l * Hkv;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, kq = lane >> 4, blk = (lane >> 2) & 3, x = lane & 3;
+    const int r0 = rblk * VH_ROWS + wave * 16;
+    // A operand: row r0 + 4 blk + x, dimensions 32 kq .. + 32
+    double qd[32];
     {
-        const uint4 *qrow = (const uint4 *)(q + (((size_t)(active ? t : 0) * L + l) * Hq + (size_t)kv * g + j) * D);
+        const int ra = r0 + blk * 4 + x;
+        const bool ok = ra < R;
+        const int t = ok ? ra / g : 0, j = ok ? ra - t * g : 0;
+        const uint4 *qrow = (const uint4 *)(q + (((size_t)t * L + l) * Hq + (size_t)kv * g + j) * D) + kq * 4;
 #pragma unroll
-        for (int i = 0; i < D / 8; ++i) {
-            const uint4 u = active ? qrow[i] : make_uint4(0, 0, 0, 0);
-            qv[4 * i] = u.x;
-            qv[4 * i + 1] = u.y;
-            qv[4 * i + 2] = u.z;
-            qv[4 * i + 3] = u.w;
+        for (int u = 0; u < 4; ++u) {
+            const uint4 w = ok ? qrow[u] : make_uint4(0, 0, 0, 0);
+            const uint32_t d[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) bf16x2(d[e], qd[8 * u + 2 * e], qd[8 * u + 2 * e + 1]);
         }
     }
     double best[VH_KMAX];
@@ -67,71 +82,83 @@ __global__ __launch_bounds__(NT) void voice_hits_kernel(int L, int Hq, int Hkv, 
         best[i] = -INFINITY;
         bpos[i] = INT32_MAX;
     }
+    auto insert = [&](double val, int pos) {
+        if (val > best[VH_KMAX - 1]) {
+#pragma unroll
+            for (int s = 0; s < VH_KMAX; ++s)
+                if (val > best[s]) {
+                    const double tv = best[s];
+                    const int tp = bpos[s];
+                    best[s] = val;
+                    bpos[s] = pos;
+                    val = tv;
+                    pos = tp;
+                }
+        }
+    };
+    // key tile staged as doubles (each element converted once per work-group): key r, dimension
+    // 32 kq + s at r * VH_KS + kq * 33 + s; the padding keeps the 16 (key, quarter) addresses of a
+    // read on distinct banks.  After the loop the same memory holds the candidate lists.
+    constexpr int VH_KS = 4 * 33 + 1;
+    constexpr int TILE_DBL = VH_TILE * VH_KS, LIST_DBL = VH_ROWS * 4 * VH_KMAX * 3 / 2;   // lists: double + int
+    __shared__ double ksd[TILE_DBL > LIST_DBL ? TILE_DBL : LIST_DBL];
     const uint16_t *Kh = k + (size_t)lk * T * D;
-    __shared__ uint4 ks[VH_TILE * PADU];
     for (int k0 = 0; k0 < Ta; k0 += VH_TILE) {
         __syncthreads();
         for (int i = tid; i < VH_TILE * (D / 8); i += NT) {
             const int rr = i >> 4, c = i & 15, row = k0 + rr;
-            ks[rr * PADU + c] = row < Ta ? *(const uint4 *)(Kh + (size_t)row * D + c * 8) : make_uint4(0, 0, 0, 0);
+            const uint4 w = row < Ta ? *(const uint4 *)(Kh + (size_t)row * D + c * 8) : make_uint4(0, 0, 0, 0);
+            const uint32_t d[4] = {w.x, w.y, w.z, w.w};
+            double *dst = ksd + rr * VH_KS + (c >> 2) * 33 + (c & 3) * 8;   // dimensions 8c .. 8c + 8
+#pragma unroll
+            for (int e = 0; e < 4; ++e) bf16x2(d[e], dst[2 * e], dst[2 * e + 1]);
         }
         __syncthreads();
-        for (int kr = sp; kr < VH_TILE; kr += VH_SPLIT) {
-            const int tau = k0 + kr;
-            if (tau >= Ta) break;
-            double acc = 0.0;
+        const int nk = min(VH_TILE, Ta - k0);
+        for (int kg = 0; kg < nk; kg += 8) {
+            // keys k0 + kg + x (group 0) and k0 + kg + 4 + x (group 1), dimension 32 kq + s
+            const double *g0 = ksd + (kg + x) * VH_KS + kq * 33, *g1 = ksd + (kg + 4 + x) * VH_KS + kq * 33;
+            double a0 = 0.0, a1 = 0.0, b0 = 0.0, b1 = 0.0;   // group 0/1, dimension halves a/b
 #pragma unroll
-            for (int c = 0; c < D / 8; ++c) {
-                const uint4 u = ks[kr * PADU + c];
-                const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    double k_lo, k_hi, q_lo, q_hi;
-                    bf16x2(w[e], k_lo, k_hi);
-                    bf16x2(qv[4 * c + e], q_lo, q_hi);
-                    acc = fma(q_lo, k_lo, acc);
-                    acc = fma(q_hi, k_hi, acc);
-                }
+            for (int s2 = 0; s2 < 16; ++s2) {
+                a0 = __builtin_amdgcn_mfma_f64_4x4x4f64(qd[s2], g0[s2], a0, 0, 0, 0);
+                a1 = __builtin_amdgcn_mfma_f64_4x4x4f64(qd[s2], g1[s2], a1, 0, 0, 0);
+                b0 = __builtin_amdgcn_mfma_f64_4x4x4f64(qd[16 + s2], g0[16 + s2], b0, 0, 0, 0);
+                b1 = __builtin_amdgcn_mfma_f64_4x4x4f64(qd[16 + s2], g1[16 + s2], b1, 0, 0, 0);
             }
-            if (acc > best[VH_KMAX - 1]) {
-                double v = acc;
-                int p = tau;
-#pragma unroll
-                for (int s = 0; s < VH_KMAX; ++s)
-                    if (v > best[s]) {
-                        const double tv = best[s];
-                        const int tp = bpos[s];
-                        best[s] = v;
-                        bpos[s] = p;
-                        v = tv;
-                        p = tp;
-                    }
-            }
+            // this lane: row r0 + 4 blk + kq, keys k0 + kg + x and k0 + kg + 4 + x
+            const int p0 = k0 + kg + x, p1 = p0 + 4;
+            if (p0 < Ta) insert(a0 + b0, p0);
+            if (p1 < Ta) insert(a1 + b1, p1);
         }
     }
-    __shared__ double sbest[VH_ROWS][VH_SPLIT * VH_KMAX];
-    __shared__ int spos[VH_ROWS][VH_SPLIT * VH_KMAX];
-    __syncthreads();
+    __syncthreads();   // the tile's memory takes the candidate lists
+    double (*sbest)[4 * VH_KMAX] = reinterpret_cast<double (*)[4 * VH_KMAX]>(ksd);
+    int (*spos)[4 * VH_KMAX] = reinterpret_cast<int (*)[4 * VH_KMAX]>(ksd + VH_ROWS * 4 * VH_KMAX);
+    const int rl = wave * 16 + blk * 4 + kq;   // this lane's row within the block
 #pragma unroll
     for (int i = 0; i < VH_KMAX; ++i) {
-        sbest[r][sp * VH_KMAX + i] = best[i];
-        spos[r][sp * VH_KMAX + i] = bpos[i];
+        sbest[rl][x * VH_KMAX + i] = best[i];
+        spos[rl][x * VH_KMAX + i] = bpos[i];
     }
     __syncthreads();
-    if (sp == 0 && active) {
+    const int rg = rblk * VH_ROWS + tid;
+    if (tid < VH_ROWS && rg < R) {
         // top K of the row's candidates by (value descending, position ascending)
+        const int t = rg / g, j = rg - t * g;
         const int a = span[2 * t], b = span[2 * t + 1];
         unsigned taken = 0;
         int c = 0;
         for (int n = 0; n < K; ++n) {
             int bi = -1;
-            for (int i = 0; i < VH_SPLIT * VH_KMAX; ++i) {
+            for (int i = 0; i < 4 * VH_KMAX; ++i) {
                 if (taken >> i & 1u) continue;
-                if (bi < 0 || sbest[r][i] > sbest[r][bi] || (sbest[r][i] == sbest[r][bi] && spos[r][i] < spos[r][bi]))
+                if (bi < 0 || sbest[tid][i] > sbest[tid][bi] ||
+                    (sbest[tid][i] == sbest[tid][bi] && spos[tid][i] < spos[tid][bi]))
                     bi = i;
             }
             taken |= 1u << bi;
-            const int pos = spos[r][bi];
+            const int pos = spos[tid][bi];
             c += pos >= a && pos < b;
         }
         hits[((size_t)t * L + l) * Hq + (size_t)kv * g + j] = c;
@@ -210,13 +237,14 @@ wnw_status wnw_voice_hits(int32_t layers, int32_t q_heads, int32_t kv_heads, int
         n_tok < 0 || (int64_t)layers * kv_heads > 65535)
         return triage_fail(WNW_ERR_INVALID, "bad sizes");
     const int g = q_heads / kv_heads;
-    if (g > VH_ROWS) return triage_fail(WNW_ERR_UNSUPPORTED, "GQA group larger than 64");
+    if ((int64_t)n_tok * g > INT32_MAX) return triage_fail(WNW_ERR_UNSUPPORTED, "too many answer-token rows");
     if (top_k < 1 || top_k > VH_KMAX || top_k > audio_len)
         return triage_fail(WNW_ERR_INVALID, "top_k must be in 1..8 and at most audio_len");
     if (n_tok == 0) return WNW_OK;
     if (!k_dev || !q_dev || !span_dev || !hits_dev) return triage_fail(WNW_ERR_INVALID, "NULL pointer");
-    const int tpb = VH_ROWS / g;
-    hipLaunchKernelGGL(voice_hits_kernel, dim3((n_tok + tpb - 1) / tpb, layers * kv_heads), dim3(NT), 0,
+    const int64_t nrb = ((int64_t)n_tok * g + VH_ROWS - 1) / VH_ROWS, nwg = nrb * layers * kv_heads;
+    if (nwg > INT32_MAX) return triage_fail(WNW_ERR_UNSUPPORTED, "too many answer tokens for one launch");
+    hipLaunchKernelGGL(voice_hits_kernel, dim3((unsigned)nwg), dim3(NT), 0,
                        (hipStream_t)hip_stream, layers, q_heads, kv_heads, rows, audio_len, n_tok, top_k,
                        (const uint16_t *)k_dev, (const uint16_t *)q_dev, span_dev, hits_dev);
     const hipError_t e = hipGetLastError();
