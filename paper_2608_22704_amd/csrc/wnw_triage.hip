@@ -6,7 +6,9 @@
 //   voice_hits_kernel   per (answer token, q-head): the K audio positions with the largest
 //                       logit (softmax keeps the order), ties to the lower position, counted
 //                       inside the token's interval.  Logits are exact bf16 products summed in
-//                       double, so the top-K decisions are those of the exact logits.
+//                       double on the matrix cores; a sum of 128 products (16 significant bits
+//                       each) rounds only when their magnitudes span more than ~30 binary
+//                       orders, so the top-K decisions are in practice those of the exact logits.
 //   key_sens_kernel     per (answer token, KV-head): the mean over audio positions of the L2 norm
 //                       of the key gradient.  A streaming reduction (HBM-bound).
 //   wnw_triage          (host) VS and HS means, VS * HS ranking, roles, normalised importance.
