@@ -807,7 +807,11 @@ struct RowPtr {
 
 // One work-group = 4 wavefronts; wavefront w owns rows [w * 4 * RPL, (w + 1) * 4 * RPL) of the
 // tile's row map, in sub-tiles of 32 rows (RPL = 8 or 16).  Rows are loaded fully coalesced
-// (16 lanes per 256-byte row).
+// (16 lanes per 256-byte row), by one of three paths chosen by the row map: consecutive rows of
+// one head (`contiguous`: buffer loads, one lane offset), rows of several slot entries
+// (`offsets`: buffer loads over the sequence's slot region, each lane walking its rows through
+// the entries), or one pointer per row (the recall path, and slot regions of 4 GB or more).  The
+// rows' validity becomes a per-wavefront mask (a ballot per load), which the logits read.
 //
 // Logits (fp32, exact bf16 products) on v_mfma_f32_4x4x4_16b_bf16: lane l = 4*blk + i feeds
 // A_blk[i][0..3] and B_blk[0..3][i], and D_blk[i][j] lands in lane 4*blk + j, register i.
@@ -1073,16 +1077,12 @@ __device__ inline void subset_tile(const uint16_t *__restrict__ qh, const RowMap
     __syncthreads();   // the shared buffers may be reused by the next tile of this work-group
 }
 
+// Consecutive rows of one head: rows t0 .. of the head starting at K / V, R of them valid (read
+// by buffer loads, see subset_tile).
 struct StaticRows {
     static constexpr bool copies = false, contiguous = true, offsets = false;
     const uint16_t *K, *V;
     int t0, R;
-    __device__ RowPtr row(int r) const
-    {
-        if (t0 + r >= R) return {nullptr, nullptr};
-        const size_t o = (size_t)(t0 + r) * D;
-        return {K + o, V + o};
-    }
 };
 
 // Rows of a group of resident complements.  The group's entries are staged in shared memory as
