@@ -68,6 +68,9 @@ def test_validation_without_gpu(W):
     # NULL context everywhere
     assert W.lib.wnw_set_roles(None, None, None) == W.WNW_ERR_INVALID
     assert W.lib.wnw_decode_step(None, None, None, None, None, None) == W.WNW_ERR_INVALID
+    assert W.lib.wnw_append_kv(None, None, None, None) == W.WNW_ERR_INVALID
+    assert W.lib.wnw_set_selection_override(None, None) == W.WNW_ERR_INVALID
+    assert W.lib.wnw_debug_set_slot_offset_limit(None, 0) == W.WNW_ERR_INVALID
     W.wnw_destroy(None)
 
 

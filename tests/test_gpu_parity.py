@@ -304,6 +304,9 @@ def test_slot_rows_pointer_path(timing):
     log(f"[case] slot rows through pointers vs buffer offsets, {timing}-step timing")
     h, h2 = Lockstep(w, flags=flags), Lockstep(w, flags=flags)
     try:
+        with pytest.raises(W.WnwError) as e:
+            W.wnw_debug_set_slot_offset_limit(h.ctx, -1)
+        assert e.value.status == W.WNW_ERR_INVALID
         W.wnw_debug_set_slot_offset_limit(h.ctx, 0)
         for s in range(w.steps):
             h.step(s)
