@@ -28,6 +28,7 @@ namespace {
 
 constexpr int VH_ROWS = 64;   // (token, q-head) rows per work-group (16 per wavefront)
 constexpr int VH_TILE = 32;   // keys staged in LDS per iteration (as doubles)
+static_assert(VH_TILE * (D / 8) % NT == 0, "whole 16-byte pieces per thread");
 constexpr int VH_KMAX = 8;    // largest K (the paper uses 4 and 8)
 
 __device__ inline void bf16x2(uint32_t u, double &lo, double &hi)
@@ -105,17 +106,30 @@ __global__ __launch_bounds__(NT, 4) void voice_hits_kernel(int L, int Hq, int Hk
     constexpr int TILE_DBL = VH_TILE * VH_KS, LIST_DBL = VH_ROWS * 4 * VH_KMAX * 3 / 2;   // lists: double + int
     __shared__ double ksd[TILE_DBL > LIST_DBL ? TILE_DBL : LIST_DBL];
     const uint16_t *Kh = k + (size_t)lk * T * D;
+    // The next tile's keys are loaded into registers while the current tile is computed (each
+    // thread holds VH_PF 16-byte pieces), then converted into the single shared buffer.
+    constexpr int VH_PF = VH_TILE * (D / 8) / NT;
+    uint4 pf[VH_PF];
+    auto fetch = [&](int k0) {
+#pragma unroll
+        for (int j = 0; j < VH_PF; ++j) {
+            const int i = tid + j * NT, row = k0 + (i >> 4);
+            pf[j] = row < Ta ? *(const uint4 *)(Kh + (size_t)row * D + (i & 15) * 8) : make_uint4(0, 0, 0, 0);
+        }
+    };
+    fetch(0);
     for (int k0 = 0; k0 < Ta; k0 += VH_TILE) {
-        __syncthreads();
-        for (int i = tid; i < VH_TILE * (D / 8); i += NT) {
-            const int rr = i >> 4, c = i & 15, row = k0 + rr;
-            const uint4 w = row < Ta ? *(const uint4 *)(Kh + (size_t)row * D + c * 8) : make_uint4(0, 0, 0, 0);
-            const uint32_t d[4] = {w.x, w.y, w.z, w.w};
+        __syncthreads();   // every wavefront is done with the previous tile
+#pragma unroll
+        for (int j = 0; j < VH_PF; ++j) {
+            const int i = tid + j * NT, rr = i >> 4, c = i & 15;
+            const uint32_t d[4] = {pf[j].x, pf[j].y, pf[j].z, pf[j].w};
             double *dst = ksd + rr * VH_KS + (c >> 2) * 33 + (c & 3) * 8;   // dimensions 8c .. 8c + 8
 #pragma unroll
             for (int e = 0; e < 4; ++e) bf16x2(d[e], dst[2 * e], dst[2 * e + 1]);
         }
         __syncthreads();
+        if (k0 + VH_TILE < Ta) fetch(k0 + VH_TILE);
         const int nk = min(VH_TILE, Ta - k0);
         for (int kg = 0; kg < nk; kg += 8) {
             // keys k0 + kg + x (group 0) and k0 + kg + 4 + x (group 1), dimension 32 kq + s
