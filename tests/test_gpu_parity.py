@@ -268,6 +268,24 @@ def test_voxtral_60min_b4_full_size_sampled(w):
     _run(w, steps=24, head_mask_fn=_sampled(6), seqs=[2])
 
 
+def test_headline_config_full_size_sampled():
+    """The benchmark's launch configuration at full size: the 15k-audio cache with the paper's
+    next-step timing and copy-engine recall, all 256 steps; selection, residency, scores and
+    anchor outputs at every step, sampled non-anchor heads."""
+    from paper_2608_22704_amd import wnw as W
+    _run(configs.VOXTRAL_10MIN, head_mask_fn=_sampled(8),
+         flags=W.WNW_F_SELECT_NEXT_STEP | W.WNW_F_RECALL_MEMCPY)
+
+
+def test_b16_next_step_copy_engines_full_size_sampled():
+    """Batch 16 of the 15k-audio cache with next-step timing and copy-engine recall (every
+    sequence's new complements in one step's transfers): sequences 3 and 12 against the oracle
+    for 48 steps, sampled heads."""
+    from paper_2608_22704_amd import wnw as W
+    _run(configs.VOXTRAL_10MIN_B16, steps=48, head_mask_fn=_sampled(6), seqs=[3, 12],
+         flags=W.WNW_F_SELECT_NEXT_STEP | W.WNW_F_RECALL_MEMCPY)
+
+
 # ---- next-step selection timing: the tidal heads of step s attend over the resident set left
 # by step s-1; the oracle runs the same timing (its next_step mode).
 
