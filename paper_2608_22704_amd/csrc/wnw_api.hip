@@ -984,10 +984,11 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, float *out, float *sco
     sb.pub = memcpy_path ? c->d_newinfo : nullptr;
     HIPCHECK(c, launch_select(g, sb, sc, c->override_sel, sel, s0));
     if (g.next_step) {
-        // Next-step timing: the chunks that became resident now are copied on the side stream,
-        // back to back with the previous step's copies, while this step's tidal heads read only
-        // slots filled before it.  The target slots were free at this step's selection, which
-        // follows on s0 every reader of them (up to the previous step's tidal kernel).
+        // Next-step timing: the chunks that became resident now are copied on the side stream
+        // (host-issued: over the copy streams, of which the side stream is the first), back to
+        // back with the previous step's copies, while this step's tidal heads read only slots
+        // filled before it.  The target slots were free at this step's selection, which follows
+        // on s0 every reader of them (up to the previous step's tidal kernel).
         HIPCHECK(c, hipEventRecord(c->ev_sel, s0));
         HIPCHECK(c, hipStreamWaitEvent(c->side, c->ev_sel, 0));
         if (timing) HIPCHECK(c, hipEventRecord(ev.r[0], c->side));
