@@ -115,14 +115,14 @@ __global__ __launch_bounds__(NT) void prefill_rowstats_kernel(Geometry g, const 
     }
     // causal limit (last visible key) of the rows this lane holds in the result layout
     int lim[2][4];
-    float m[2][4], s[2][4];
+    float nm[2][4], s[2][4];
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int r = rw + rb * 16 + 4 * grp + i;
             lim[rb][i] = r < R ? g.Ta + r % g.Tt : -1;
-            m[rb][i] = -INFINITY;
+            nm[rb][i] = INFINITY;
             s[rb][i] = 0.f;
         }
 
@@ -150,23 +150,44 @@ __global__ __launch_bounds__(NT) void prefill_rowstats_kernel(Geometry g, const 
                 x[rb][kb] = acc;   // unscaled; the scale folds into the exponent's FMA
             }
         }
-        // One rescale per row and tile (the lane's four keys of the tile at once).  Statistics
-        // are base 2 and scaled; every row sum holds its maximum term 2^0, so exponentials that
-        // flush below 2^-126 change nothing.
+        // Statistics are base 2 and scaled, the running maximum kept negated (nm = -m) for the
+        // exponent's FMA.  Every row sum holds a term of at least 2^0, so exponentials that flush
+        // below 2^-126 change nothing.
         if (k0 + TILE <= g.Ta) {
-            // audio tile: every key visible to every row, no mask; m is finite after it
+            // audio tile: every key visible to every row, no mask.  The terms are first taken
+            // against the running maximum as it stands; only when a row's terms add up to more
+            // than 2^20 (or its maximum is still -inf, which gives +inf) does the wavefront raise
+            // the maxima and take the tile again.  Sums stay far inside fp32's range either way.
+            float t[2][4], tall = 0.f;
 #pragma unroll
             for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const float mt = fmaxf(fmaxf(x[rb][0][i], x[rb][1][i]), fmaxf(x[rb][2][i], x[rb][3][i]));
-                    const float mn = fmaxf(m[rb][i], mt * C2);
-                    float acc = s[rb][i] * exp2_hw(m[rb][i] - mn);   // 0 before the first tile
+                    float acc = exp2_hw(fmaf(x[rb][0][i], C2, nm[rb][i]));
 #pragma unroll
-                    for (int kb = 0; kb < TILE / 16; ++kb) acc += exp2_hw(fmaf(x[rb][kb][i], C2, -mn));
-                    s[rb][i] = acc;
-                    m[rb][i] = mn;
+                    for (int kb = 1; kb < TILE / 16; ++kb) acc += exp2_hw(fmaf(x[rb][kb][i], C2, nm[rb][i]));
+                    t[rb][i] = acc;
+                    tall += acc;
                 }
+            if (__any(tall > 0x1p20f)) {
+#pragma unroll
+                for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const float mt = fmaxf(fmaxf(x[rb][0][i], x[rb][1][i]), fmaxf(x[rb][2][i], x[rb][3][i]));
+                        const float mn = fmaxf(-nm[rb][i], mt * C2);
+                        float acc = s[rb][i] * exp2_hw(-nm[rb][i] - mn);   // 0 before the first tile
+#pragma unroll
+                        for (int kb = 0; kb < TILE / 16; ++kb) acc += exp2_hw(fmaf(x[rb][kb][i], C2, -mn));
+                        s[rb][i] = acc;
+                        nm[rb][i] = -mn;
+                    }
+            } else {
+#pragma unroll
+                for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) s[rb][i] += t[rb][i];
+            }
         } else {
             // keys past a row's causal limit (text rows after its token, rows past the end, keys
             // past the cache) drop out
@@ -187,12 +208,12 @@ __global__ __launch_bounds__(NT) void prefill_rowstats_kernel(Geometry g, const 
 #pragma unroll
                     for (int kb = 1; kb < TILE / 16; ++kb) mt = fmaxf(mt, x[rb][kb][i]);
                     if (mt == -INFINITY) continue;   // every key of the tile masked for this row
-                    const float mn = fmaxf(m[rb][i], mt * C2);
-                    float acc = s[rb][i] * exp2_hw(m[rb][i] - mn);   // exp2(-inf) = 0 for an empty row
+                    const float mn = fmaxf(-nm[rb][i], mt * C2);
+                    float acc = s[rb][i] * exp2_hw(-nm[rb][i] - mn);   // exp2(-inf) = 0 for an empty row
 #pragma unroll
                     for (int kb = 0; kb < TILE / 16; ++kb) acc += exp2_hw(fmaf(x[rb][kb][i], C2, -mn));
                     s[rb][i] = acc;
-                    m[rb][i] = mn;
+                    nm[rb][i] = -mn;
                 }
         }
         if (more) tile_store(kbuf[(it + 1) & 1], pre);
@@ -202,20 +223,16 @@ __global__ __launch_bounds__(NT) void prefill_rowstats_kernel(Geometry g, const 
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < 4; ++i) {
+            float m = -nm[rb][i], l = s[rb][i];
 #pragma unroll
             for (int o = 1; o < 16; o <<= 1) {
-                const float m2 = __shfl_xor(m[rb][i], o), s2 = __shfl_xor(s[rb][i], o);
-                merge_ms(m[rb][i], s[rb][i], m2, s2);
+                const float m2 = __shfl_xor(m, o), l2 = __shfl_xor(l, o);
+                merge_ms(m, l, m2, l2);
             }
-    if (col == 0)
-#pragma unroll
-        for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int r = rw + rb * 16 + 4 * grp + i;
-                if (r < R) lse[qbase + r] = m[rb][i] + log2f(s[rb][i]);
-            }
+            const int r = rw + rb * 16 + 4 * grp + i;
+            if (col == 0 && r < R) lse[qbase + r] = m + log2f(l);
+        }
 }
 
 // Pass 2.  Grid: ceil(T_a / CS_KEYS) key blocks for each of the B * L * H_kv KV-heads, in XCD
