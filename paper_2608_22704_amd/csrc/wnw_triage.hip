@@ -27,9 +27,11 @@ namespace wnw {
 namespace {
 
 constexpr int VH_ROWS = 64;   // (token, q-head) rows per work-group (16 per wavefront)
-constexpr int VH_TILE = 32;   // keys staged in LDS per iteration (as doubles)
+constexpr int VH_TILE = 16;   // keys staged in LDS per iteration (as doubles): one MFMA key block
 static_assert(VH_TILE * (D / 8) % NT == 0, "whole 16-byte pieces per thread");
 constexpr int VH_KMAX = 8;    // largest K (the paper uses 4 and 8)
+static_assert(VH_TILE % 16 == 0, "whole 16-key blocks per tile");
+typedef double v4d __attribute__((ext_vector_type(4)));
 
 __device__ inline void bf16x2(uint32_t u, double &lo, double &hi)
 {
@@ -39,15 +41,14 @@ __device__ inline void bf16x2(uint32_t u, double &lo, double &hi)
 
 // Work-groups: ceil(n_tok * g / VH_ROWS) row blocks per KV-head (row = answer token * g + q-head
 // of the group), in XCD order so that the row blocks of one KV-head read its keys through one L2.
-// Wavefront w owns 16 rows of the block.  The logits run on v_mfma_f64_4x4x4f64 (four 4x4x4
-// blocks; lane l = 16k + 4*blk + x holds A_blk[x][k] and B_blk[k][x], and D_blk[i][j] lands in
-// lane 16i + 4*blk + j): A holds the query rows (row 4*blk + x, converted to double once), B four
-// keys shared by the four blocks, and lane k feeds dimension 32k + s to step s, so one key's
-// 64 contiguous bytes per lane come from the staged tile.  Each lane ends a key group holding one
-// logit (row 4*blk + i, key j) and keeps the best eight of the keys it sees (value descending;
-// equal values keep the earlier, lower, position); the four lists of a row are merged at the end.
-// Products of bf16 values are exact in double; two dimension halves and two key groups make four
-// independent accumulation chains.
+// Wavefront w owns 16 rows of the block.  The logits run on v_mfma_f64_16x16x4f64 (lane
+// l = i + 16k supplies A[i][k] and B[k][i]; D[i][j] lands in lane j + 16 (i % 4), element i / 4):
+// A is a block of 16 keys from the staged tile, B the wavefront's 16 query rows (converted to
+// double once and held in registers), and lane group k feeds dimension 32k + s at step s.  Every
+// key element is read from shared memory once per wavefront.  A lane ends a key block holding
+// four logits of its row (keys k + 4v) and keeps the best eight of the keys it sees (value
+// descending; equal values keep the earlier, lower, position); the four lists of a row (one per
+// lane group) are merged at the end.  Products of bf16 values are exact in double.
 __device__ inline int vh_xcd_order(int w, int n)
 {
     const int q = n / 8, r = n % 8, x = w % 8;
@@ -61,12 +62,12 @@ __global__ __launch_bounds__(NT, 4) void voice_hits_kernel(int L, int Hq, int Hk
     const int g = Hq / Hkv, R = n_tok * g, nrb = (R + VH_ROWS - 1) / VH_ROWS;
     const int v = vh_xcd_order(blockIdx.x, gridDim.x), lk = v / nrb, rblk = v - lk * nrb;
     const int l = lk / Hkv, kv = lk - l * Hkv;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, kq = lane >> 4, blk = (lane >> 2) & 3, x = lane & 3;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, kq = lane >> 4, li = lane & 15;
     const int r0 = rblk * VH_ROWS + wave * 16;
-    // A operand: row r0 + 4 blk + x, dimensions 32 kq .. + 32
+    // B operand: row r0 + li, dimensions 32 kq .. + 32
     double qd[32];
     {
-        const int ra = r0 + blk * 4 + x;
+        const int ra = r0 + li;
         const bool ok = ra < R;
         const int t = ok ? ra / g : 0, j = ok ? ra - t * g : 0;
         const uint4 *qrow = (const uint4 *)(q + (((size_t)t * L + l) * Hq + (size_t)kv * g + j) * D) + kq * 4;
@@ -100,8 +101,8 @@ __global__ __launch_bounds__(NT, 4) void voice_hits_kernel(int L, int Hq, int Hk
         }
     };
     // key tile staged as doubles (each element converted once per work-group): key r, dimension
-    // 32 kq + s at r * VH_KS + kq * 33 + s; the padding keeps the 16 (key, quarter) addresses of a
-    // read on distinct banks.  After the loop the same memory holds the candidate lists.
+    // 32 kq + s at r * VH_KS + kq * 33 + s; the padding puts the 16 keys that one lane group reads
+    // at a step on distinct banks.  After the loop the same memory holds the candidate lists.
     constexpr int VH_KS = 4 * 33 + 1;
     constexpr int TILE_DBL = VH_TILE * VH_KS, LIST_DBL = VH_ROWS * 4 * VH_KMAX * 3 / 2;   // lists: double + int
     __shared__ double ksd[TILE_DBL > LIST_DBL ? TILE_DBL : LIST_DBL];
@@ -131,31 +132,28 @@ __global__ __launch_bounds__(NT, 4) void voice_hits_kernel(int L, int Hq, int Hk
         __syncthreads();
         if (k0 + VH_TILE < Ta) fetch(k0 + VH_TILE);
         const int nk = min(VH_TILE, Ta - k0);
-        for (int kg = 0; kg < nk; kg += 8) {
-            // keys k0 + kg + x (group 0) and k0 + kg + 4 + x (group 1), dimension 32 kq + s
-            const double *g0 = ksd + (kg + x) * VH_KS + kq * 33, *g1 = ksd + (kg + 4 + x) * VH_KS + kq * 33;
-            double a0 = 0.0, a1 = 0.0, b0 = 0.0, b1 = 0.0;   // group 0/1, dimension halves a/b
+        for (int kb = 0; kb < nk; kb += 16) {
+            // A: key k0 + kb + li, dimension 32 kq + s
+            const double *ga = ksd + (kb + li) * VH_KS + kq * 33;
+            v4d acc = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-            for (int s2 = 0; s2 < 16; ++s2) {
-                a0 = __builtin_amdgcn_mfma_f64_4x4x4f64(qd[s2], g0[s2], a0, 0, 0, 0);
-                a1 = __builtin_amdgcn_mfma_f64_4x4x4f64(qd[s2], g1[s2], a1, 0, 0, 0);
-                b0 = __builtin_amdgcn_mfma_f64_4x4x4f64(qd[16 + s2], g0[16 + s2], b0, 0, 0, 0);
-                b1 = __builtin_amdgcn_mfma_f64_4x4x4f64(qd[16 + s2], g1[16 + s2], b1, 0, 0, 0);
+            for (int s2 = 0; s2 < 32; ++s2) acc = __builtin_amdgcn_mfma_f64_16x16x4f64(ga[s2], qd[s2], acc, 0, 0, 0);
+            // this lane: row r0 + li, keys k0 + kb + kq + 4 e
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int p = k0 + kb + kq + 4 * e;
+                if (p < Ta) insert(acc[e], p);
             }
-            // this lane: row r0 + 4 blk + kq, keys k0 + kg + x and k0 + kg + 4 + x
-            const int p0 = k0 + kg + x, p1 = p0 + 4;
-            if (p0 < Ta) insert(a0 + b0, p0);
-            if (p1 < Ta) insert(a1 + b1, p1);
         }
     }
     __syncthreads();   // the tile's memory takes the candidate lists
     double (*sbest)[4 * VH_KMAX] = reinterpret_cast<double (*)[4 * VH_KMAX]>(ksd);
     int (*spos)[4 * VH_KMAX] = reinterpret_cast<int (*)[4 * VH_KMAX]>(ksd + VH_ROWS * 4 * VH_KMAX);
-    const int rl = wave * 16 + blk * 4 + kq;   // this lane's row within the block
+    const int rl = wave * 16 + li;   // this lane's row within the block
 #pragma unroll
     for (int i = 0; i < VH_KMAX; ++i) {
-        sbest[rl][x * VH_KMAX + i] = best[i];
-        spos[rl][x * VH_KMAX + i] = bpos[i];
+        sbest[rl][kq * VH_KMAX + i] = best[i];
+        spos[rl][kq * VH_KMAX + i] = bpos[i];
     }
     __syncthreads();
     const int rg = rblk * VH_ROWS + tid;
