@@ -28,7 +28,8 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 constexpr float LOG2E = 1.4426950408889634f;
 constexpr float C2 = 0.08838834764831845f * LOG2E;   // logit scale 1 / sqrt(128), base 2
 constexpr int RS_ROWS = 128;                          // query rows per pass-1 work-group (32 per wave)
-constexpr int CS_KEYS = 128;                          // audio keys per pass-2 work-group (32 per wave)
+constexpr int CS_KB = 3;                              // 16-key blocks per pass-2 wavefront
+constexpr int CS_KEYS = 4 * 16 * CS_KB;               // audio keys per pass-2 work-group (48 per wave)
 constexpr int TILE = 64;                              // rows staged in LDS per iteration
 constexpr int PADU = D / 8 + 1;                       // uint4 per staged row: 16 + 1 of padding
 
@@ -236,11 +237,11 @@ __global__ __launch_bounds__(NT) void prefill_rowstats_kernel(Geometry g, const 
 }
 
 // Pass 2.  Grid: ceil(T_a / CS_KEYS) key blocks for each of the B * L * H_kv KV-heads, in XCD
-// order.  Wave w owns audio keys k0 + 32 w .. + 32
-// (two 16-key blocks, their K fragments held in registers); the work-group walks every query row
-// of the KV-head in tiles of TILE rows staged in LDS with their log-sum-exp, and each lane adds
-// exp2(s * C2 - lse) over the rows it holds for its key column.
-__global__ __launch_bounds__(NT) void prefill_colsum_kernel(Geometry g, const uint16_t *__restrict__ K,
+// order.  Wave w owns audio keys k0 + 48 w .. + 48 (three 16-key blocks, their K fragments held
+// in registers, so each query fragment read from LDS feeds three MFMA chains); the work-group
+// walks every query row of the KV-head in tiles of TILE rows staged in LDS with their
+// log-sum-exp, and each lane adds exp2(s * C2 - lse) over the rows it holds for its key column.
+__global__ __launch_bounds__(NT, 3) void prefill_colsum_kernel(Geometry g, const uint16_t *__restrict__ K,
                                                            const uint16_t *__restrict__ qt,
                                                            const float *__restrict__ lse, float *__restrict__ p)
 {
@@ -251,18 +252,18 @@ __global__ __launch_bounds__(NT) void prefill_colsum_kernel(Geometry g, const ui
     const uint16_t *Kh = K + (size_t)hd * g.T * D;
     const size_t qbase = (((size_t)b * g.L + l) * g.Hq + (size_t)kv * g.G) * g.Tt;
     const uint16_t *Qh = qt + qbase * D;
-    const int kw = kblk * CS_KEYS + wave * 32;
+    const int kw = kblk * CS_KEYS + wave * 16 * CS_KB;
 
-    bf16x8_t kf[2][4];
+    bf16x8_t kf[CS_KB][4];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int kb = 0; kb < CS_KB; ++kb) {
         const int key = kw + kb * 16 + col;
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk)
             kf[kb][kk] = as_bf8(key < g.Ta ? *(const uint4 *)(Kh + (size_t)key * D + grp * 8 + 32 * kk)
                                            : make_uint4(0, 0, 0, 0));
     }
-    float acc[2] = {0.f, 0.f};
+    float acc[CS_KB] = {};
     __shared__ uint4 qbuf[2][TILE * PADU];
     __shared__ float sbuf[2][TILE];
     uint4 pre[SPT];
@@ -293,7 +294,7 @@ __global__ __launch_bounds__(NT) void prefill_colsum_kernel(Geometry g, const ui
 #pragma unroll
             for (int i = 0; i < 4; ++i) st[i] = sst[rb * 16 + 4 * grp + i];
 #pragma unroll
-            for (int kb = 0; kb < 2; ++kb) {
+            for (int kb = 0; kb < CS_KB; ++kb) {
                 f32x4_t sc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int kk = 0; kk < 4; ++kk) sc = mfma16(qf[kk], kf[kb][kk], sc);
@@ -308,13 +309,13 @@ __global__ __launch_bounds__(NT) void prefill_colsum_kernel(Geometry g, const ui
         __syncthreads();
     }
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int kb = 0; kb < CS_KB; ++kb) {
         acc[kb] += __shfl_xor(acc[kb], 16);
         acc[kb] += __shfl_xor(acc[kb], 32);
     }
     if (grp == 0)
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
+        for (int kb = 0; kb < CS_KB; ++kb) {
             const int key = kw + kb * 16 + col;
             if (key < g.Ta) p[(size_t)hd * g.Ta + key] = ldexpf(acc[kb], -64);
         }
