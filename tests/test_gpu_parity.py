@@ -609,6 +609,7 @@ PRE = [
     _small("pre_g6", 405, Hq=12, Hkv=2, Tt=3, Ta=1111, cl=100),
     _small("pre_no_text", 406, Tt=0),
     _small("pre_batch3", 407, B=3, Ta=777, Tt=65, cl=37, steps=4),
+    _small("pre_short_audio", 419, Ta=40, Tt=70, cl=16),   # fewer audio keys than one wavefront's
 ]
 
 
@@ -794,6 +795,9 @@ VH = [  # (L, H_q, H_kv, T_a, T_t, n_tok, K)
     (2, 12, 4, 517, 9, 22, 1),
     (1, 24, 3, 1000, 3, 17, 4),
     (1, 16, 2, 64, 1, 9, 8),
+    (1, 8, 2, 5, 2, 3, 4),        # fewer audio keys than one 16-key block
+    (1, 4, 1, 16, 0, 16, 8),      # exactly one key tile and one 64-row work-group
+    (1, 8, 1, 33, 2, 40, 4),      # five work-groups, a ragged key tail
 ]
 
 
