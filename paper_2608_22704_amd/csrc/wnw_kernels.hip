@@ -1261,7 +1261,9 @@ __global__ __launch_bounds__(NT, REC ? (RPLK == RPL_S ? 2 : 1) : (RPLK == RPL_S 
         return;
     }
     bid -= n_static;
-    const int grp = bid % g.ng_kept, rest = bid / g.ng_kept;
+    // group-major: the grid holds room for the most kept groups a head can have, and the groups
+    // past this step's count return at once; this order puts them at the end of the dispatch
+    const int nh = g.nT * g.B, grp = bid / nh, rest = bid - grp * nh;
     slot_group<G, RPLK>(g, t, s, q, grp, rest % g.nT, rest / g.nT, 0, sm.sl);
 }
 
