@@ -94,7 +94,10 @@ enum {
      * positions (the sum of its per-segment counts), the best over its whole audio; a segment
      * may then be kept whole or not at all, and complements differ in size from segment to
      * segment.  Default: per segment. */
-    WNW_F_PREFILL_GLOBAL = 16u
+    WNW_F_PREFILL_GLOBAL = 16u,
+    /* wnw_decode_step writes out_dev as bf16 (each fp32 result rounded to nearest, ties to
+     * even) instead of fp32; the arithmetic is unchanged. */
+    WNW_F_OUT_BF16 = 32u
 };
 
 typedef struct wnw_ctx wnw_ctx;
@@ -215,13 +218,14 @@ wnw_status wnw_append_kv(wnw_ctx *ctx, const void *k_new_dev, const void *v_new_
  * events).
  *   q_dev             device bf16 [B][L][H_q][d]
  *   out_dev           device fp32 [B][L][H_q][d]     attention output of every q-head
+ *                     (bf16, same layout, with WNW_F_OUT_BF16)
  *   chunk_scores_dev  device fp32 [B][n_chunks]      this step's chunk scores
  *   selected_dev      device int32 [B][k]            selected chunk ids, ascending
  *   hip_stream        caller's stream (NULL = null stream); outputs are valid once it has
  *                     completed.  Buffers must stay valid until then.
  * The default recall path does not block the host.  With WNW_F_RECALL_MEMCPY the call waits
  * once, mid-step (busy polling), for the selection before issuing the copies. */
-wnw_status wnw_decode_step(wnw_ctx *ctx, const void *q_dev, float *out_dev,
+wnw_status wnw_decode_step(wnw_ctx *ctx, const void *q_dev, void *out_dev,
                            float *chunk_scores_dev, int32_t *selected_dev, void *hip_stream);
 
 /* Derived sizes: chunks (the selection's candidates), k, kept audio rows per tidal/fixed head

@@ -166,7 +166,7 @@ wnw_status derive(wnw_ctx *c, const wnw_config &cfg, Geometry &g)
     if (cfg.budget_bp < 0 || cfg.budget_bp > 10000) return fail(c, WNW_ERR_INVALID, "budget_bp must be in 0..10000");
     if (cfg.top_k < 0 || cfg.evict_lag < 0) return fail(c, WNW_ERR_INVALID, "top_k and evict_lag must be >= 0");
     if (cfg.flags & ~(uint32_t)(WNW_F_SELECT_NEXT_STEP | WNW_F_RECALL_MEMCPY | WNW_F_TIMING | WNW_F_OVERLAP_CHUNKS |
-                                WNW_F_PREFILL_GLOBAL))
+                                WNW_F_PREFILL_GLOBAL | WNW_F_OUT_BF16))
         return fail(c, WNW_ERR_INVALID, "unknown flag bits 0x%x", cfg.flags);
     const int span = (cfg.flags & WNW_F_OVERLAP_CHUNKS) ? 2 : 1;
     if (span == 2 && cfg.chunk_len % 2)
@@ -202,6 +202,7 @@ wnw_status derive(wnw_ctx *c, const wnw_config &cfg, Geometry &g)
     g.knew = std::min(g.nc, span * g.k);
     g.delta = cfg.evict_lag ? cfg.evict_lag : 3;
     g.next_step = (cfg.flags & WNW_F_SELECT_NEXT_STEP) ? 1 : 0;
+    g.out_bf16 = (cfg.flags & WNW_F_OUT_BF16) ? 1 : 0;
     g.keep_total = 0;
     for (int ch = 0; ch < g.nc; ++ch) g.keep_total += keep_of_len(g.budget_bp, chunk_len_of(g, ch));
     // Slots: the resident set holds at most delta * k chunks, i.e. span * delta * k segments.
@@ -926,7 +927,7 @@ wnw_status wnw_prefill_scores(wnw_ctx *c, const void *q_text_dev, float *scores_
     return WNW_OK;
 }
 
-wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, float *out, float *scores, int32_t *selected, void *hip_stream)
+wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, void *out, float *scores, int32_t *selected, void *hip_stream)
 {
     if (!c) return fail(nullptr, WNW_ERR_INVALID, "ctx is NULL");
     if (c->state != READY)

@@ -45,6 +45,7 @@ struct Geometry {
     int ng_kept;                // kept-slot groups of the head with the most
     int64_t chunk_elems;        // bf16 elements of one segment's complement block (blk_rows * D)
     int64_t slot_off_max;       // slot regions below this many bytes use buffer offsets
+    int out_bf16;               // decode-step output written as bf16
 };
 
 // Rows of one non-anchor head (tidal heads 0..nT-1, then fixed heads), whose audio retention
@@ -121,7 +122,7 @@ struct StepBuffers {
 // and end times (hipExtLaunchKernel), or are recorded back to back when there is nothing to launch.
 hipError_t launch_anchor(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q,
                          hipStream_t st, hipEvent_t e0, hipEvent_t e1);
-hipError_t launch_anchor_combine(const Geometry &g, const Tiers &t, const StepBuffers &s, float *out,
+hipError_t launch_anchor_combine(const Geometry &g, const Tiers &t, const StepBuffers &s, void *out,
                                  hipStream_t st);
 // Scores, selection, residency and slot bookkeeping (writes scores[B][nc] and selected[B][k]).
 hipError_t launch_select(const Geometry &g, const StepBuffers &s, float *scores, const int32_t *override_sel,
@@ -145,7 +146,7 @@ hipError_t launch_attention(const Geometry &g, const Tiers &t, const StepBuffers
 hipError_t launch_recall(const Geometry &g, const Tiers &t, const StepBuffers &s, hipStream_t st);
 // Complements already copied to their slots by the host-waited recall path.
 hipError_t launch_new_slots(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st);
-hipError_t launch_subset_combine(const Geometry &g, const Tiers &t, const StepBuffers &s, float *out,
+hipError_t launch_subset_combine(const Geometry &g, const Tiers &t, const StepBuffers &s, void *out,
                                  hipStream_t st);
 // Prefill scores (wnw_prefill.hip): p [B][L][Hkv][Ta] fp32 from the full K cache
 // [B][L][Hkv][T][D] and the text queries [B][L][Hq][Tt][D]; lse [B][L][Hq][Tt] is scratch.

@@ -450,8 +450,20 @@ __device__ inline T block_sum1(T v, T *red)
 constexpr int COMBINE_THREADS = 1024;
 constexpr int CGROUPS = COMBINE_THREADS / D;
 
+// One output element: fp32, or bf16 rounded to nearest (ties to even; NaN stays a quiet NaN).
+__device__ inline void store_out(void *out, size_t i, float v, bool bf16)
+{
+    if (!bf16) {
+        static_cast<float *>(out)[i] = v;
+        return;
+    }
+    const unsigned u = __float_as_uint(v);
+    const unsigned r = (u & 0x7fffffffu) > 0x7f800000u ? 0x7fc0u : (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+    static_cast<uint16_t *>(out)[i] = (uint16_t)r;
+}
+
 template <int G>
-__global__ __launch_bounds__(COMBINE_THREADS) void anchor_combine_kernel(Geometry g, Tiers t, StepBuffers s, float *out)
+__global__ __launch_bounds__(COMBINE_THREADS) void anchor_combine_kernel(Geometry g, Tiers t, StepBuffers s, void *out)
 {
     const int ai = blockIdx.x, h = blockIdx.y, b = blockIdx.z, tid = threadIdx.x;
     extern __shared__ double fac[];      // [n_tiles_a]
@@ -483,7 +495,7 @@ __global__ __launch_bounds__(COMBINE_THREADS) void anchor_combine_kernel(Geometr
 #pragma unroll
             for (int j = 1; j < CGROUPS; ++j) acc += ocol[j][d];
             const int lk = t.anchor_lk[ai], ll = lk / g.Hkv, kv = lk - ll * g.Hkv;
-            out[(((size_t)b * g.L + ll) * g.Hq + (size_t)kv * G + h) * D + d] = (float)(acc * inv);
+            store_out(out, (((size_t)b * g.L + ll) * g.Hq + (size_t)kv * G + h) * D + d, (float)(acc * inv), g.out_bf16);
         }
     }
     double *mass = s.mass + (((size_t)b * g.nA + ai) * G + h) * (size_t)g.nc;
@@ -1342,7 +1354,7 @@ __global__ __launch_bounds__(NT, RPL == RPL_S ? 4 : 2) void new_slots_kernel(Geo
 // COMBINE_THREADS threads; the partials of every output column are split over groups of
 // threads and summed in a fixed order.
 template <int G>
-__global__ __launch_bounds__(COMBINE_THREADS) void subset_combine_kernel(Geometry g, Tiers t, StepBuffers s, float *out)
+__global__ __launch_bounds__(COMBINE_THREADS) void subset_combine_kernel(Geometry g, Tiers t, StepBuffers s, void *out)
 {
     const int hi = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
     const bool tidal = hi < g.nT;
@@ -1407,7 +1419,7 @@ __global__ __launch_bounds__(COMBINE_THREADS) void subset_combine_kernel(Geometr
     }
     __syncthreads();
     const int lk = tidal ? t.tidal_lk[hi] : t.fixed_lk[hi - g.nT], l = lk / g.Hkv, kv = lk - l * g.Hkv;
-    float *oh = out + (((size_t)b * g.L + l) * g.Hq + (size_t)kv * G) * D;
+    const size_t ob = (((size_t)b * g.L + l) * g.Hq + (size_t)kv * G) * D;
     if constexpr (OG > 1) {
         // threads beyond OG * G * D (when G * D does not divide the block) only join the barrier
         const int idx = tid % (G * D), grp = tid / (G * D), h = idx / D;
@@ -1423,7 +1435,7 @@ __global__ __launch_bounds__(COMBINE_THREADS) void subset_combine_kernel(Geometr
         if (grp == 0) {
 #pragma unroll
             for (int q2 = 1; q2 < OG; ++q2) acc += opart[q2][idx];
-            oh[idx] = acc * Linv[h];
+            store_out(out, ob + idx, acc * Linv[h], g.out_bf16);
         }
     } else {
         for (int idx = tid; idx < G * D; idx += COMBINE_THREADS) {
@@ -1431,7 +1443,7 @@ __global__ __launch_bounds__(COMBINE_THREADS) void subset_combine_kernel(Geometr
             float acc = 0.f;
 #pragma unroll 8
             for (int j = 0; j < nvalid; ++j) acc += s.ps_o[(base + part(j)) * G * D + idx] * sfac[j * G + h];
-            oh[idx] = acc * Linv[h];
+            store_out(out, ob + idx, acc * Linv[h], g.out_bf16);
         }
     }
 }
@@ -1518,7 +1530,7 @@ struct AnchorL {
 };
 template <int G>
 struct AnchorCombineL {
-    static hipError_t run(const Geometry &g, const Tiers &t, const StepBuffers &s, float *out, hipStream_t st)
+    static hipError_t run(const Geometry &g, const Tiers &t, const StepBuffers &s, void *out, hipStream_t st)
     {
         if (g.nA == 0) return hipSuccess;
         const size_t shm = (size_t)g.n_tiles_a * sizeof(double);
@@ -1572,7 +1584,7 @@ struct NewSlotsL {
 };
 template <int G>
 struct CombineL {
-    static hipError_t run(const Geometry &g, const Tiers &t, const StepBuffers &s, float *out, hipStream_t st)
+    static hipError_t run(const Geometry &g, const Tiers &t, const StepBuffers &s, void *out, hipStream_t st)
     {
         if (g.nT + g.nF == 0) return hipSuccess;
         const size_t shm = (size_t)(g.np_max ? g.np_max : 1) * G * sizeof(float);
@@ -1589,7 +1601,7 @@ hipError_t launch_anchor(const Geometry &g, const Tiers &t, const StepBuffers &s
     return dispatch_g<AnchorL>(g.G, g, t, s, q, st, e0, e1);
 }
 
-hipError_t launch_anchor_combine(const Geometry &g, const Tiers &t, const StepBuffers &s, float *out, hipStream_t st)
+hipError_t launch_anchor_combine(const Geometry &g, const Tiers &t, const StepBuffers &s, void *out, hipStream_t st)
 {
     return dispatch_g<AnchorCombineL>(g.G, g, t, s, out, st);
 }
@@ -1626,7 +1638,7 @@ hipError_t launch_new_slots(const Geometry &g, const Tiers &t, const StepBuffers
     return dispatch_g<NewSlotsL>(g.G, g, t, s, q, st);
 }
 
-hipError_t launch_subset_combine(const Geometry &g, const Tiers &t, const StepBuffers &s, float *out, hipStream_t st)
+hipError_t launch_subset_combine(const Geometry &g, const Tiers &t, const StepBuffers &s, void *out, hipStream_t st)
 {
     return dispatch_g<CombineL>(g.G, g, t, s, out, st);
 }

@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(PKG, "libwnw.so")
 WNW_OK, WNW_ERR_INVALID, WNW_ERR_OOM, WNW_ERR_HIP, WNW_ERR_STATE, WNW_ERR_UNSUPPORTED = 0, -1, -2, -3, -4, -5
 WNW_ANCHOR, WNW_TIDAL, WNW_FIXED = 0, 1, 2
 WNW_F_SELECT_NEXT_STEP, WNW_F_RECALL_MEMCPY, WNW_F_TIMING, WNW_F_OVERLAP_CHUNKS, WNW_F_PREFILL_GLOBAL = 1, 2, 4, 8, 16
+WNW_F_OUT_BF16 = 32
 
 EXPORTS = ("wnw_init_cache", "wnw_set_retention", "wnw_set_roles", "wnw_prefill_scores", "wnw_set_roles_device",
            "wnw_append_kv", "wnw_decode_step", "wnw_query_geometry",

@@ -33,6 +33,14 @@ def test_every_declared_symbol_is_exported(W):
     assert set(names) <= exported
 
 
+def test_flag_and_status_values_match_the_header(W):
+    src = open(HEADER).read()
+    values = {m.group(1): int(m.group(2), 0) for m in re.finditer(r"\b(WNW_(?:F|ERR)_[A-Z0-9_]+)\s*=\s*(-?(?:0x)?[0-9a-fA-F]+)u?", src)}
+    assert {k for k in values if k.startswith("WNW_F_")} >= {"WNW_F_SELECT_NEXT_STEP", "WNW_F_OUT_BF16"}
+    for name, v in values.items():
+        assert getattr(W, name) == v, name
+
+
 @pytest.mark.parametrize("cmd", [["gcc", "-std=c99", "-Wall", "-Wextra", "-pedantic", "-x", "c"],
                                  ["g++", "-std=c++17", "-Wall", "-Wextra", "-pedantic", "-x", "c++"]])
 def test_header_compiles(cmd, tmp_path):

@@ -335,6 +335,30 @@ def test_slot_rows_pointer_path(timing):
         h2.close()
 
 
+@pytest.mark.parametrize("timing", ["same", "next"])
+def test_out_bf16(timing):
+    """WNW_F_OUT_BF16: every step's bf16 output is, bit for bit, the fp32 output of a context
+    without the flag rounded to nearest (ties to even), and the fp32 run matches the oracle."""
+    import torch
+    from paper_2608_22704_amd import wnw as W
+    from tests.wnw_harness import Lockstep, log
+    w = _small(f"out_bf16_{timing}", 192 if timing == "same" else 193, L=2, Hq=8, Hkv=4, Ta=480, Tt=5, cl=16,
+               steps=8)
+    flags = _next(W.WNW_F_RECALL_MEMCPY) if timing == "next" else 0
+    log(f"[case] bf16 output, {timing}-step timing")
+    h, h2 = Lockstep(w, flags=flags), Lockstep(w, flags=flags | W.WNW_F_OUT_BF16)
+    try:
+        h2.out = torch.empty(h.out.shape, dtype=torch.int16, device="cuda")
+        for s in range(w.steps):
+            h.step(s)
+            got = h2.gpu_step(s)[0].view(np.uint16)
+            want = gen.f32_to_bf16(h.out.cpu().numpy())
+            assert np.array_equal(got, want), f"step {s}: bf16 output is not the rounded fp32 output"
+    finally:
+        h.close()
+        h2.close()
+
+
 def test_next_step_qwen_shaped_all_steps():
     _run(configs.QWEN_10MIN, flags=_next())
 
