@@ -43,6 +43,11 @@
  *
  * Threading: a context is not thread-safe.  Calls on one GPU that share a context must be
  * serialised by the caller.
+ *
+ * Environment: WNW_LOG=1 prints one trace line per decode step on stderr (what the call
+ * enqueued; with WNW_F_RECALL_MEMCPY the segments it copied and the host's wait).
+ * WNW_TEST_PINNED_LIMIT=<bytes> makes pinned allocations above that size fail with WNW_ERR_OOM
+ * (a test hook for the failure path of wnw_set_roles).
  */
 #ifndef WNW_H
 #define WNW_H
@@ -140,7 +145,8 @@ typedef struct {
      * around the step's launches, and the number of timed steps. */
     int64_t timed_steps;
     double t_anchor_ms;        /* anchor attention + chunk mass                                 */
-    double t_select_ms;        /* anchor merge, chunk scores, top-k, residency, slots           */
+    double t_select_ms;        /* anchor merge, chunk scores, top-k, residency, slots (up to the
+                                  end of the select kernel)                                     */
     double t_tidal_fixed_ms;   /* fixed heads, tidal kept rows, complements already on the device;
                                   with same-step timing (default recall) also the recall and the
                                   attention over the recalled complements, in the same launch   */
@@ -153,9 +159,19 @@ typedef struct {
                                   host-issued copies (WNW_F_RECALL_MEMCPY: from the first copy
                                   stream's start to the last copy's end, less the part spent
                                   behind the previous step's copies)                            */
+    int64_t slot_exhausted;    /* steps that found no free recall slot; never expected (the
+                                  slot count bounds the resident set).  When it happens the
+                                  context fails: wnw_get_stats and the next wnw_decode_step
+                                  return WNW_ERR_STATE with a message                            */
+    double t_host_wait_ms;     /* WNW_F_RECALL_MEMCPY: host time spent polling for the step's
+                                  selection before issuing the copies, summed over steps         */
+    double t_recall_wait_ms;   /* WNW_F_TIMING: on the caller's stream, from the end of the
+                                  select kernel to the start of the tidal/fixed launch: with
+                                  WNW_F_SELECT_NEXT_STEP the wait for the previous step's recall */
 } wnw_stats;
 
-/* Create a context for one batch of caches.
+/* Create a context for one batch of caches: the full KV cache as prefill leaves it, before any
+ * compression (the starting point of Method, "Prefill Compression and Decode-Time Chunk Swap").
  *   cfg        copied; validated here (WNW_ERR_INVALID / WNW_ERR_UNSUPPORTED).
  *   k_dev/v_dev  device bf16 [B][L][H_kv][T_a+T_t][d], owned by the caller, read only by
  *              wnw_set_roles; they may be freed once it has returned.
@@ -228,30 +244,38 @@ wnw_status wnw_append_kv(wnw_ctx *ctx, const void *k_new_dev, const void *v_new_
 wnw_status wnw_decode_step(wnw_ctx *ctx, const void *q_dev, void *out_dev,
                            float *chunk_scores_dev, int32_t *selected_dev, void *hip_stream);
 
-/* Derived sizes: chunks (the selection's candidates), k, kept audio rows per tidal/fixed head
+/* Derived sizes (Method, "Chunk Structure" and "Dynamic Chunk Selection"; k as the budget
+ * gives it, see the file header): chunks (the selection's candidates), k, kept audio rows per tidal/fixed head
  * (-1 after wnw_set_retention: see wnw_query_head_keep), recall slots per sequence, and bytes of
  * one recalled segment of one sequence (all tidal heads; a segment is a chunk unless
  * WNW_F_OVERLAP_CHUNKS; known after wnw_set_roles).  Any pointer may be NULL. */
 wnw_status wnw_query_geometry(const wnw_ctx *ctx, int32_t *n_chunks, int32_t *k,
                               int32_t *keep_total, int32_t *n_slots, int64_t *chunk_bytes);
 
-/* Number of segments (the unit of residency and recall; equal to n_chunks unless
+/* Number of segments (Method, "Chunk Structure"; the unit of residency and recall; equal to n_chunks unless
  * WNW_F_OVERLAP_CHUNKS, then n_chunks + 1).  The pointer may be NULL. */
 wnw_status wnw_query_segments(const wnw_ctx *ctx, int32_t *n_segments);
 
-/* Kept audio rows of every head, host int32 [L][H_kv] (T_a for anchors).  After wnw_set_roles. */
+/* Kept audio rows of every head (Method, "Prefill Compression"; Eq. 1 with per-head retention),
+ * host int32 [L][H_kv] (T_a for anchors).  After wnw_set_roles. */
 wnw_status wnw_query_head_keep(const wnw_ctx *ctx, int32_t *keep);
 
-/* Counters and (with WNW_F_TIMING) kernel times; waits for the device. */
+/* Counters and (with WNW_F_TIMING) kernel times; waits for the device.  r_gpu and r_gpu_cpu are
+ * the paper's audio KV retention ratios (Experiments, "Audio KV Retention and WnW Configuration");
+ * recalled_bytes is the CPU-to-GPU volume of the runtime table (Experiments, "Efficiency and
+ * Runtime Analysis"); the other fields are instrumentation with no passage behind them.
+ * WNW_ERR_STATE (context failed) if a step ran out of recall slots. */
 wnw_status wnw_get_stats(wnw_ctx *ctx, wnw_stats *out);
 
-/* Replace the top-k of the following steps by the ids in sel_dev (device int32 [B][k], read
+/* Test and benchmark support, no passage behind it.
+ * Replace the top-k of the following steps by the ids in sel_dev (device int32 [B][k], read
  * when each step runs; -1 = no chunk; ids distinct, < n_chunks).  NULL restores the top-k.
  * Scores are still computed.  Used to keep two implementations on one trajectory and to force
  * a recall load. */
 wnw_status wnw_set_selection_override(wnw_ctx *ctx, const int32_t *sel_dev);
 
-/* Copy the device slot holding the recalled complement of (b, segment) to host_dst (waits for
+/* Test support (the byte identity of a recalled chunk with its host copy), no passage behind it.
+ * Copy the device slot holding the recalled complement of (b, segment) to host_dst (waits for
  * the device).  Valid for segments resident after the last step (with WNW_F_SELECT_NEXT_STEP,
  * also those recalled during it).  Layout: per tidal head in role order (roles scanned in
  * [L][H_kv] order), its complement K rows then V rows, c rows each, where c is that head's
@@ -259,25 +283,30 @@ wnw_status wnw_set_selection_override(wnw_ctx *ctx, const int32_t *sel_dev);
  * equal chunk_bytes.  WNW_ERR_INVALID if that segment is not resident. */
 wnw_status wnw_debug_read_slot(wnw_ctx *ctx, int32_t b, int32_t chunk, void *host_dst, size_t bytes);
 
-/* Copy the host (pinned) complement of (b, segment) in the same layout as wnw_debug_read_slot. */
+/* Test support, no passage behind it.
+ * Copy the host (pinned) complement of (b, segment) in the same layout as wnw_debug_read_slot. */
 wnw_status wnw_debug_read_host_chunk(wnw_ctx *ctx, int32_t b, int32_t chunk, void *host_dst, size_t bytes);
 
-/* Flags [B][n_segments] (uint8) of the segment complements the last step's tidal heads
+/* Test support, no passage behind it (the resident set is the one "Dynamic Chunk Selection"
+ * defines).  Flags [B][n_segments] (uint8) of the segment complements the last step's tidal heads
  * attended: the resident set of that step, or of the step before it with
  * WNW_F_SELECT_NEXT_STEP (waits for the device). */
 wnw_status wnw_debug_read_resident(wnw_ctx *ctx, uint8_t *host_dst);
 
-/* Slot groups of a sequence whose slot region (n_slots * chunk_bytes) has `bytes` or more read
+/* Test support, no passage behind it.
+ * Slot groups of a sequence whose slot region (n_slots * chunk_bytes) has `bytes` or more read
  * their rows through per-row pointers instead of 32-bit buffer offsets.  The default,
  * 4294967295, is the largest region buffer offsets can address; 0 forces the pointer path
  * everywhere.  Both paths compute the same results.  Takes effect from the next step;
  * WNW_ERR_INVALID for a negative value. */
 wnw_status wnw_debug_set_slot_offset_limit(wnw_ctx *ctx, int64_t bytes);
 
-/* Message of the last failure on ctx (or of this thread when ctx is NULL).  Never NULL. */
+/* Error reporting, no passage behind it.
+ * Message of the last failure on ctx (or of this thread when ctx is NULL).  Never NULL. */
 const char *wnw_last_error(const wnw_ctx *ctx);
 
-/* Free every device, pinned and stream resource of ctx (waits for its work).  NULL is a no-op. */
+/* Resource management, no passage behind it.
+ * Free every device, pinned and stream resource of ctx (waits for its work).  NULL is a no-op. */
 void wnw_destroy(wnw_ctx *ctx);
 
 /* ---- head triage arithmetic (Method, "Head Functional Triage via Offline Calibration"; the
@@ -319,7 +348,7 @@ wnw_status wnw_triage(int32_t layers, int32_t kv_heads, int32_t group, int32_t n
                       const int32_t *hits, int32_t top_k, const float *sens, int32_t n_voice, int32_t n_anchor,
                       uint8_t *roles, float *importance, double *vs_out, double *hs_out);
 
-/* Message of the last failed triage call of this thread. */
+/* Error reporting, no passage behind it.  Message of the last failed triage call of this thread. */
 const char *wnw_triage_last_error(void);
 
 #ifdef __cplusplus

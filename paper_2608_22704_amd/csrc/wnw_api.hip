@@ -18,7 +18,9 @@
 #include "wnw_internal.h"
 
 #include <algorithm>
+#include <chrono>
 #include <cmath>
+#include <cstdlib>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -36,17 +38,19 @@ thread_local std::string t_err = "no error";
 
 enum State { CREATED = 0, READY = 1, FAILED = 2 };
 
-// Timing events of one step.  e[] on the caller's stream: 0 start, 1 after anchor attention,
-// 2 after merge + selection, 3 after the tidal/fixed kernel, 4 once the complements recalled
-// this step have been attended to (same-step timing), 5 after the final merge.  r[] on the side
-// stream around the recall.
+// Timing events of one step.  e[] on the caller's stream: 0 and 1 the first launch's own start
+// and end, 6 after the anchor merge and the selection, 2 before the tidal/fixed launch (after any
+// wait for the previous step's recall), 3 after it, 4 once the complements copied this step have
+// been attended to (copy-engine recall with same-step timing only: has_new), 5 after the final
+// merge.  r[] on the side stream around the recall.
 // Streams that share the host-issued copies of one step: copy-engine transfers queued on one
 // stream leave a gap between transfers (3 MB copies reach ~49 of ~57 GB/s on one stream, ~56
 // on four).
 constexpr int N_COPY_STREAMS = 4;
 
 struct StepEvents {
-    hipEvent_t e[6];
+    hipEvent_t e[7];
+    bool has_new;
     hipEvent_t r[2];
     // next-step timing with host-issued copies: the end of each copy stream's share (the recall
     // ends with the last of them; joining the streams for one end marker would stall the next
@@ -94,10 +98,14 @@ struct wnw_ctx {
     bool rec_pending = false;          // next-step timing: a recall issued on `side` not yet joined
     int32_t *h_newinfo = nullptr;      // pinned: counts [B][2] then new lists [B][k][2]
     int32_t *d_newinfo = nullptr;      // the same memory as the device addresses it
+    int32_t *h_flag = nullptr;         // pinned, mapped: [0] slot exhaustion seen by a select kernel
+    int32_t *d_flag = nullptr;         // the same memory as the device addresses it
+    double host_wait_ms = 0.0;         // host time spent waiting for selections (copy-engine recall)
+    bool log = false;                  // WNW_LOG set: one trace line per step on stderr
 
     std::vector<StepEvents> pending, spare;
     int n_gen = 0;                     // tokens appended (wnw_append_kv)
-    double t_acc[8] = {0};
+    double t_acc[8] = {0};             // anchor, select, tidal/fixed, new, combine, step, recall, recall wait
     int64_t timed_steps = 0, steps = 0;
 };
 
@@ -151,6 +159,25 @@ wnw_status dalloc(wnw_ctx *c, T **p, size_t n, const char *what)
         *p = nullptr;
         return fail(c, e == hipErrorOutOfMemory ? WNW_ERR_OOM : WNW_ERR_HIP, "hipMalloc of %s (%zu bytes): %s", what,
                     n * sizeof(T), hipGetErrorString(e));
+    }
+    return WNW_OK;
+}
+
+// Pinned host memory (hipHostMalloc).  WNW_TEST_PINNED_LIMIT=<bytes> makes every request above
+// that size fail as if the host were out of pinned memory (a test hook for the failure path).
+wnw_status palloc(wnw_ctx *c, void **p, size_t bytes, const char *what)
+{
+    *p = nullptr;
+    if (const char *lim = std::getenv("WNW_TEST_PINNED_LIMIT")) {
+        const long long cap = std::atoll(lim);
+        if (cap >= 0 && bytes > (size_t)cap)
+            return fail(c, WNW_ERR_OOM, "pinned %s of %zu bytes: above WNW_TEST_PINNED_LIMIT (%lld)", what, bytes, cap);
+    }
+    hipError_t e = hipHostMalloc(p, bytes, hipHostMallocDefault);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        *p = nullptr;
+        return fail(c, WNW_ERR_OOM, "pinned %s of %zu bytes: %s", what, bytes, hipGetErrorString(e));
     }
     return WNW_OK;
 }
@@ -263,7 +290,6 @@ wnw_status plan_keep(wnw_ctx *c)
         h.srow = (int)(tidal ? rowT : rowF);
         (tidal ? rowT : rowF) += h.rs + g.max_new;
         c->static_rows += h.rs;
-        h.sg = 1;
         if (tidal) c->keep_sum_t += keep;
         c->head_keep[hi] = keep;
         g.keep_sum += keep;
@@ -309,16 +335,14 @@ wnw_status plan_comp(wnw_ctx *c, const uint8_t *flags)
     g.blk_rows = (int)coff;
     g.chunk_elems = coff * D;
     g.slot_tile = g.comp_max <= TILE_S ? TILE_S : 2 * TILE_S;
-    // the kept list holds at most the resident segments (span * delta * k) in both timings
+    // the kept list holds at most the resident segments (span * delta * k) in both timings; a
+    // head's kept items cut the run of its kept complements into TILE_S-row pieces
     const int kept_max = (int)std::min<int64_t>(g.nc, (int64_t)g.delta * g.span * g.k);
     int64_t P = 0;
     g.ng_kept = g.np_max = 0;
     for (int hi = 0; hi < nsub; ++hi) {
         HeadRows &h = c->hrows[hi];
-        if (h.cfull > 0) {
-            h.sg = g.slot_tile / h.cfull;
-            h.ngk = (kept_max + h.sg - 1) / h.sg;
-        }
+        if (h.cfull > 0) h.ngk = (int)(((int64_t)kept_max * h.cfull + TILE_S - 1) / TILE_S);
         g.ng_kept = std::max(g.ng_kept, h.ngk);
         h.pbase = (int)P;
         const int np = h.nts + (h.cfull > 0 ? h.ngk + g.knew : 0);
@@ -450,6 +474,18 @@ wnw_status wait_copies(wnw_ctx *c, hipStream_t s)
     return WNW_OK;
 }
 
+// Slot exhaustion reported by a select kernel (mapped pinned flag): the context fails, since
+// tidal heads of that step missed a resident segment.  Reads host memory only (no wait).
+wnw_status check_exhaustion(wnw_ctx *c)
+{
+    if (c->h_flag && *(volatile int32_t *)c->h_flag) {
+        c->state = FAILED;
+        return fail(c, WNW_ERR_STATE, "a decode step found no free recall slot for a newly resident segment "
+                                      "(slot pool of %d per sequence exhausted)", c->g.n_slots);
+    }
+    return WNW_OK;
+}
+
 wnw_status harvest_timing(wnw_ctx *c)
 {
     const StepEvents *prev = nullptr;
@@ -457,9 +493,11 @@ wnw_status harvest_timing(wnw_ctx *c)
     for (auto &ev : c->pending) {
         float ms;
         HIPCHECK(c, hipEventSynchronize(ev.e[5]));
-        // anchor, select, tidal/fixed, new, combine, step
-        const int from[6] = {0, 1, 2, 3, 4, 0}, to[6] = {1, 2, 3, 4, 5, 5};
-        for (int i = 0; i < 6; ++i) {
+        // anchor, select, tidal/fixed, new, combine, step, -, recall wait
+        const int m = ev.has_new ? 4 : 3;
+        const int from[8] = {0, 1, 2, 3, m, 0, -1, 6}, to[8] = {1, 6, 3, 4, 5, 5, -1, 2};
+        for (int i = 0; i < 8; ++i) {
+            if (from[i] < 0 || (i == 3 && !ev.has_new)) continue;
             HIPCHECK(c, hipEventElapsedTime(&ms, ev.e[from[i]], ev.e[to[i]]));
             c->t_acc[i] += ms;
         }
@@ -504,6 +542,7 @@ void free_all(wnw_ctx *c)
         if (p) (void)hipFree(p);
     if (c->host_comp) (void)hipHostFree(c->host_comp);
     if (c->h_newinfo) (void)hipHostFree(c->h_newinfo);
+    if (c->h_flag) (void)hipHostFree(c->h_flag);
     if (c->ev_sel) (void)hipEventDestroy(c->ev_sel);
     if (c->ev_rec) (void)hipEventDestroy(c->ev_rec);
     for (auto *v : {&c->pending, &c->spare})
@@ -543,10 +582,16 @@ wnw_status wnw_init_cache(const wnw_config *cfg, const void *k_dev, const void *
     if (!c) return fail(nullptr, WNW_ERR_OOM, "context allocation failed");
     c->cfg = *cfg;
     c->g = g;
+    if (hipDeviceGetAttribute(&c->g.n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || c->g.n_cu < 1) {
+        (void)hipGetLastError();
+        c->g.n_cu = 1;
+    }
     c->device = dev;
     c->setup_stream = (hipStream_t)hip_stream;
     c->full_k = (const uint16_t *)k_dev;
     c->full_v = (const uint16_t *)v_dev;
+    const char *lg = std::getenv("WNW_LOG");
+    c->log = lg && *lg && strcmp(lg, "0") != 0;
     *out = c;
     return WNW_OK;
 }
@@ -636,21 +681,25 @@ wnw_status build_tiers(wnw_ctx *c, const uint8_t *keep_all)
 #undef ALLOC
     const size_t host_bytes = B * g.nc * (size_t)g.chunk_elems * sizeof(uint16_t);
     if (host_bytes) {
-        hipError_t e = hipHostMalloc((void **)&c->host_comp, host_bytes, hipHostMallocDefault);
-        if (e != hipSuccess) {
-            (void)hipGetLastError();
-            c->host_comp = nullptr;
-            return fail(c, WNW_ERR_OOM, "pinned complement of %zu bytes: %s", host_bytes, hipGetErrorString(e));
-        }
+        if ((r = palloc(c, (void **)&c->host_comp, host_bytes, "complement")) != WNW_OK) return r;
         void *dp = nullptr;
         HIPCHECK(c, hipHostGetDevicePointer(&dp, c->host_comp, 0));
         c->t.host_comp = (const uint16_t *)dp;
     }
-    HIPCHECK(c, hipHostMalloc((void **)&c->h_newinfo, (B * 2 + B * g.knew * 2 + 1) * sizeof(int32_t), hipHostMallocDefault));
+    if ((r = palloc(c, (void **)&c->h_newinfo, (B * 2 + B * g.knew * 2 + 1) * sizeof(int32_t), "recall lists")) != WNW_OK)
+        return r;
     {
         void *dp = nullptr;
         HIPCHECK(c, hipHostGetDevicePointer(&dp, c->h_newinfo, 0));
         c->d_newinfo = (int32_t *)dp;
+    }
+    if ((r = palloc(c, (void **)&c->h_flag, 4 * sizeof(int32_t), "status flags")) != WNW_OK) return r;
+    {
+        memset(c->h_flag, 0, 4 * sizeof(int32_t));
+        void *dp = nullptr;
+        HIPCHECK(c, hipHostGetDevicePointer(&dp, c->h_flag, 0));
+        c->d_flag = (int32_t *)dp;
+        c->s.exhausted = c->d_flag;
     }
     HIPCHECK(c, hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking));
     if (c->cfg.flags & WNW_F_RECALL_MEMCPY) {
@@ -934,6 +983,10 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, void *out, float *scor
         return fail(c, WNW_ERR_STATE, c->state == FAILED ? "context is in the error state: %s" : "%s",
                     c->state == FAILED ? c->err.c_str() : "wnw_set_roles has not run");
     if (!q_dev || !out) return fail(c, WNW_ERR_INVALID, "q_dev and out_dev must not be NULL");
+    {
+        wnw_status r = check_exhaustion(c);
+        if (r != WNW_OK) return r;
+    }
     DeviceGuard dg(c->device);
     // this step's geometry: the prompt rows plus the tokens appended so far
     Geometry g = c->g;
@@ -958,6 +1011,7 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, void *out, float *scor
             for (auto &e : ev.rc) HIPCHECK(c, hipEventCreateWithFlags(&e, hipEventDisableSystemFence));
         }
         ev.split = false;
+        ev.has_new = false;
     }
 #define MARK(i) \
     if (timing) HIPCHECK(c, hipEventRecord(ev.e[i], s0))
@@ -984,6 +1038,7 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, void *out, float *scor
     // running on the side streams
     sb.pub = memcpy_path ? c->d_newinfo : nullptr;
     HIPCHECK(c, launch_select(g, sb, sc, c->override_sel, sel, s0));
+    MARK(6);
     if (g.next_step) {
         // Next-step timing: the chunks that became resident now are copied on the side stream
         // (host-issued: over the copy streams, of which the side stream is the first), back to
@@ -1003,14 +1058,17 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, void *out, float *scor
                 HIPCHECK(c, hipStreamWaitEvent(s0, c->ev_rec, 0));
             }
         }
-        MARK(2);
-        HIPCHECK(c, launch_tidal_fixed(g, c->t, sb, q, false, false, s0));
-        MARK(3);
-        MARK(4);
+        // markers 2 and 3: the tidal launch's own start and end
+        HIPCHECK(c, launch_tidal_fixed(g, c->t, sb, q, false, false, s0, timing ? ev.e[2] : nullptr,
+                                       timing ? ev.e[3] : nullptr));
         if (memcpy_path) {
             // the copy engines queue these behind the previous step's copies: the link stays busy
+            const auto w0 = std::chrono::steady_clock::now();
             HIPCHECK(c, poll_event(c->ev_sel));
-            wnw_status r = issue_copies(c, c->side);
+            c->host_wait_ms += std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - w0).count();
+            wnw_status r = check_exhaustion(c);
+            if (r != WNW_OK) return r;
+            r = issue_copies(c, c->side);
             if (r != WNW_OK) return r;
             if (timing) {
                 for (int i = 0; i < N_COPY_STREAMS; ++i)
@@ -1034,7 +1092,6 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, void *out, float *scor
         HIPCHECK(c, launch_tidal_fixed(g, c->t, sb, q, true, true, s0));
         if (timing) HIPCHECK(c, hipEventRecord(ev.r[1], s0));
         MARK(3);
-        MARK(4);
     } else {
         HIPCHECK(c, hipEventRecord(c->ev_sel, s0));
         MARK(2);
@@ -1045,8 +1102,12 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, void *out, float *scor
         // kernel, which follows every earlier reader on s0; the copies start after ev_sel.
         HIPCHECK(c, hipStreamWaitEvent(c->side, c->ev_sel, 0));
         if (timing) HIPCHECK(c, hipEventRecord(ev.r[0], c->side));
+        const auto w0 = std::chrono::steady_clock::now();
         HIPCHECK(c, poll_event(c->ev_sel));
-        wnw_status r = issue_copies(c, c->side);
+        c->host_wait_ms += std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - w0).count();
+        wnw_status r = check_exhaustion(c);
+        if (r != WNW_OK) return r;
+        r = issue_copies(c, c->side);
         if (r != WNW_OK) return r;
         if (timing) {
             r = wait_copies(c, c->side);
@@ -1058,11 +1119,21 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, void *out, float *scor
         // (4b) the complements copied this step
         HIPCHECK(c, launch_new_slots(g, c->t, sb, q, s0));
         MARK(4);
+        ev.has_new = timing;
     }
     HIPCHECK(c, launch_subset_combine(g, c->t, sb, out, s0));
     MARK(5);
 #undef MARK
     if (timing) c->pending.push_back(ev);
+    if (c->log) {
+        // host-side trace: what this call enqueued and, with host-issued copies, what it copied
+        int n_new = -1;
+        if (memcpy_path)
+            for (int b = n_new = 0; b < g.B; ++b) n_new += c->h_newinfo[b * 2 + 1];
+        fprintf(stderr, "[wnw] step %lld: %s timing, %s recall, %d sequences, new segments copied %d, host wait %.3f ms total\n",
+                (long long)c->steps, g.next_step ? "next-step" : "same-step",
+                memcpy_path ? "copy-engine" : "work-group", g.B, n_new, c->host_wait_ms);
+    }
     c->steps++;
     return WNW_OK;
 }
@@ -1128,6 +1199,11 @@ wnw_status wnw_get_stats(wnw_ctx *c, wnw_stats *o)
     if (r != WNW_OK) return r;
     unsigned long long st[8];
     HIPCHECK(c, hipMemcpy(st, c->s.stats, sizeof st, hipMemcpyDeviceToHost));
+    if (st[5]) {
+        c->state = FAILED;
+        return fail(c, WNW_ERR_STATE, "%llu decode step(s) found no free recall slot (slot pool of %d per sequence)",
+                    st[5], c->g.n_slots);
+    }
     const Geometry &g = c->g;
     *o = wnw_stats{};
     o->steps = c->steps;
@@ -1156,6 +1232,9 @@ wnw_status wnw_get_stats(wnw_ctx *c, wnw_stats *o)
     o->t_combine_ms = c->t_acc[4];
     o->t_step_ms = c->t_acc[5];
     o->t_recall_ms = c->t_acc[6];
+    o->slot_exhausted = (int64_t)st[5];
+    o->t_host_wait_ms = c->host_wait_ms;
+    o->t_recall_wait_ms = c->t_acc[7];
     return WNW_OK;
 }
 

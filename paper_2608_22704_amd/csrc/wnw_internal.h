@@ -41,8 +41,11 @@ struct Geometry {
     int comp_max;               // largest complement of one segment of one tidal head
     int blk_rows;               // rows of one segment's complement block (every tidal head, K and V)
     int64_t keep_sum;           // kept audio rows over all non-anchor heads
-    int slot_tile;              // rows of one slot-group work-group (TILE_S or 2 * TILE_S)
-    int ng_kept;                // kept-slot groups of the head with the most
+    int slot_tile;              // rows of one recall unit's work-group (TILE_S, or 2 * TILE_S when a
+                                // complement exceeds TILE_S rows)
+    int ng_kept;                // kept items (TILE_S rows of resident complements) of the head with
+                                // the most
+    int n_cu;                   // compute units of the device (grid-stride launches)
     int64_t chunk_elems;        // bf16 elements of one segment's complement block (blk_rows * D)
     int64_t slot_off_max;       // slot regions below this many bytes use buffer offsets
     int out_bf16;               // decode-step output written as bf16
@@ -61,8 +64,7 @@ struct HeadRows {
     // tidal heads (0 for fixed heads)
     int cfull;   // block stride: the head's largest complement of one segment over the batch
     int coff;    // first row of the head in a segment's complement block: cfull K rows, cfull V rows
-    int sg;      // kept slots per slot-group work-group (>= 1)
-    int ngk;     // kept-slot groups
+    int ngk;     // kept items: TILE_S-row pieces of the head's resident complements at most
     int kfull;   // kept positions of a full segment (set-up)
     int klast;   // kept positions of the last segment (set-up)
 };
@@ -114,6 +116,8 @@ struct StepBuffers {
     int32_t *pub;               // host-issued recall: mapped pinned mirror of counts [B][2] and new
                                 // lists [B][knew][2], written by the select kernel; else null
     unsigned long long *stats;  // [8] recalled, dropped, resident, slot_rows, peak, exhausted, revived
+    int32_t *exhausted;         // mapped pinned flag, set to 1 by a step that found no free slot for a
+                                // newly resident segment (the host fails the context on it)
     const int32_t *seg_rows;    // [B][nc] complement rows of a segment over the tidal heads
 };
 
@@ -137,7 +141,7 @@ inline size_t select_shared_bytes(const Geometry &g)
 // (same-step timing), also the copy of the complements listed for recall from mapped pinned
 // memory into their slots and the attention over them.
 hipError_t launch_tidal_fixed(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, bool recall,
-                              bool with_static, hipStream_t st);
+                              bool with_static, hipStream_t st, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 // Anchor attention + chunk mass together with the static tidal/fixed tiles (next-step timing).
 hipError_t launch_attention(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st,
                             hipEvent_t e0, hipEvent_t e1);

@@ -30,6 +30,7 @@
 #include <math.h>
 
 #include <algorithm>
+#include <atomic>
 
 namespace wnw {
 
@@ -189,6 +190,16 @@ __device__ inline double exp_nonpos(double y)
     return tt < -1022.0 ? 0.0 : ldexp((double)e, (int)n);
 }
 
+// Thread index as a value the compiler may not treat as loop-invariant: tiles run inside
+// grid-stride loops, and hoisting every lane-dependent index out of the loop would keep them all
+// live across the tile and spill registers.
+__device__ inline int lane_id_opaque()
+{
+    int tid = threadIdx.x;
+    __asm__ volatile("" : "+v"(tid));
+    return tid;
+}
+
 // Shared memory of one anchor tile.
 template <int G>
 struct AnchorSmem {
@@ -212,7 +223,7 @@ __device__ inline void anchor_tile(const Geometry &g, const Tiers &t, const Step
     constexpr int OGR = G <= 4 ? 4 : 2;       // row groups kept in the P.V partial store
     constexpr int HS = (G + 3) / 4;           // sets of 4 heads for P.V
     static_assert(NKG % 2 == 0, "key groups are processed in pairs");
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, sub = lane & 15, rg = lane >> 4;
+    const int tid = lane_id_opaque(), lane = tid & 63, wave = tid >> 6, sub = lane & 15, rg = lane >> 4;
     const int kq = lane >> 4, blk = (lane >> 2) & 3, x4 = lane & 3;
     const int lk = t.anchor_lk[ai], l = lk / g.Hkv, kv = lk - l * g.Hkv;
     const size_t hrow = ((size_t)b * g.nA + ai) * (size_t)g.Tcap;
@@ -742,11 +753,13 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
     for (int u = tid; u < nu; u += nthr) rank[u] = fkept[u];
     __syncthreads();
     const int nkept = block_scan_excl(rank, nu, wsum);
+    // bit 30 of a kept entry's slot: every tidal head's complement of the segment has its full
+    // stride of rows (the tiles then skip the per-head row count)
     int32_t *kl = s.kept_list + (size_t)b * ns * 2;
     for (int u = tid; u < nu; u += nthr)
         if (fkept[u]) {
             kl[rank[u] * 2] = u;
-            kl[rank[u] * 2 + 1] = sof[u];
+            kl[rank[u] * 2 + 1] = sof[u] | (s.seg_rows[(size_t)b * nu + u] * 2 == g.blk_rows ? 1 << 30 : 0);
         }
     __syncthreads();
     for (int u = tid; u < nu; u += nthr)
@@ -802,7 +815,13 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
         atomicAdd(&s.stats[2], (unsigned long long)nres);
         atomicAdd(&s.stats[3], (unsigned long long)nrows);
         atomicMax(&s.stats[4], (unsigned long long)nres);
-        if (nnew > nn) atomicAdd(&s.stats[5], 1ull);   // slot exhaustion (never expected)
+        if (nnew > nn) {
+            // no free slot for a newly resident segment: the slot count bounds the resident set,
+            // so this never happens; if it did, tidal heads would miss a resident segment, so the
+            // host is told (vector store to mapped pinned memory) and fails the context
+            atomicAdd(&s.stats[5], 1ull);
+            if (s.exhausted) *(volatile int32_t *)s.exhausted = 1;
+        }
         atomicAdd(&s.stats[6], (unsigned long long)nrev);
     }
 }
@@ -854,7 +873,7 @@ __device__ inline void subset_tile(const uint16_t *__restrict__ qh, const RowMap
     constexpr int OGR = G <= 4 ? 4 : 2;       // row groups kept in the P.V partial store
     constexpr int QS = 136;                   // padded q row, in uint16
     static_assert(NR % 32 == 0, "wavefront rows come in 32-row sub-tiles");
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, sub = lane & 15, rg = lane >> 4;
+    const int tid = lane_id_opaque(), lane = tid & 63, wave = tid >> 6, sub = lane & 15, rg = lane >> 4;
     const int j4 = lane & 3, kb = (lane >> 2) & 7, dh = lane >> 5;
     auto &kst = sm.kst;
     uint16_t *qs = sm.qs;
@@ -885,7 +904,8 @@ __device__ inline void subset_tile(const uint16_t *__restrict__ qh, const RowMap
         const __amdgpu_buffer_rsrc_t rs = buf_rsrc(map.base, map.bytes);
         const int cm = map.comp_max;
         const unsigned vd = (unsigned)cm * (D * 2);   // an entry's V rows follow its K rows
-        int e = (wave * NR + rg) / cm, rr = wave * NR + rg - e * cm;
+        const int v0 = map.first + wave * NR + rg;     // row within the entries, from entry 0's first
+        int e = v0 / cm, rr = v0 - e * cm;
 #pragma unroll
         for (int i = 0; i < RPL; ++i) {
             ok[i] = e < map.n_entries && rr < map.nrows[e < map.n_entries ? e : 0];
@@ -1097,16 +1117,18 @@ struct StaticRows {
     int t0, R;
 };
 
-// Rows of a group of resident complements.  The group's entries are staged in shared memory as
-// (K row base, valid rows) so that the row map needs no global load.
+// Rows of a run of resident complements of one tidal head: the entries' rows one after the
+// other (comp_max per entry, of which the first nrows are valid), starting at row `first` of the
+// first entry.  The entries are staged in shared memory as (K row base, valid rows) so that the
+// row map needs no global load.
 struct SlotRows {
     static constexpr bool copies = false, contiguous = false, offsets = false;
-    const uint16_t *const *kbase;   // [sg] first K row of the tidal head in the entry's slot
-    const int *nrows;               // [sg] valid rows of the entry (complement length)
-    int n_entries, comp_max;
+    const uint16_t *const *kbase;   // [n_entries] first K row of the tidal head in the entry's slot
+    const int *nrows;               // [n_entries] valid rows of the entry (complement length)
+    int n_entries, comp_max, first;
     __device__ RowPtr row(int r) const
     {
-        const int e = r / comp_max, rr = r - e * comp_max;
+        const int v = first + r, e = v / comp_max, rr = v - e * comp_max;
         if (e >= n_entries || rr >= nrows[e]) return {nullptr, nullptr};
         const uint16_t *k = kbase[e] + (size_t)rr * D;
         return {k, k + (size_t)comp_max * D};
@@ -1119,9 +1141,9 @@ struct SlotRowsOff {
     static constexpr bool copies = false, contiguous = false, offsets = true;
     const uint16_t *base;           // the sequence's first slot
     unsigned bytes;                 // its slot region
-    const unsigned *koff;           // [sg] byte offset of the entry's first K row of the tidal head
-    const int *nrows;               // [sg] valid rows of the entry (complement length)
-    int n_entries, comp_max;
+    const unsigned *koff;           // [n_entries] byte offset of the entry's first K row of the tidal head
+    const int *nrows;               // [n_entries] valid rows of the entry (complement length)
+    int n_entries, comp_max, first;
 };
 
 // Rows of one recalled complement block (a tidal head's complement of one chunk): comp_max K rows,
@@ -1171,43 +1193,72 @@ __device__ inline void static_tile(const Geometry &g, const Tiers &t, const Step
     subset_tile<G, RPL_S>(qh, map, s.ps_m + p * G, s.ps_l + p * G, s.ps_o + p * G * D, sm);
 }
 
-// Slot group `grp` of list `which` (0 kept: the head's sg entries per group; 1 new: one entry)
-// of tidal head ti.
+// Rows of the listed resident complements of tidal head ti, sequence b, as a run of entries
+// (see SlotRows) starting at row `first` of entry e0: n_entries entries from `list` ((segment,
+// slot) pairs; bit 30 of the slot marks a segment whose complement has the full stride in every
+// tidal head, so its row count needs no lookup), attended as one tile into partial p.
 template <int G, int RPL>
-__device__ inline void slot_group(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, int grp,
-                                  int ti, int b, int which, SubsetSmem<G, RPL> &sm)
+__device__ inline void slot_rows_tile(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q,
+                                      const int32_t *list, int e0, int n_entries, int first, int ti, int b, size_t p,
+                                      SubsetSmem<G, RPL> &sm)
 {
-    const HeadRows hr = t.hr[ti];
-    const int cnt = s.counts[b * 2 + which], epg = which ? 1 : hr.sg;
-    if (hr.cfull == 0 || (!which && grp >= hr.ngk) || grp * epg >= cnt) return;
-    constexpr int MAXE = 4 * RPL * WAVES;   // entries of one group never exceed its rows
+    constexpr int MAXE = 4 * RPL * WAVES;   // entries of one tile never exceed its rows
     __shared__ const uint16_t *kbase[MAXE];
     __shared__ unsigned koff[MAXE];
     __shared__ int nrows[MAXE];
-    const int n_entries = min(epg, cnt - grp * epg);
-    const int32_t *list = (which ? s.new_list + (size_t)b * g.knew * 2 : s.kept_list + (size_t)b * g.n_slots * 2) +
-                          (size_t)grp * epg * 2;
+    const HeadRows hr = t.hr[ti];
     const uint16_t *region = t.slots + (size_t)b * g.n_slots * g.chunk_elems;
     const size_t region_bytes = (size_t)g.n_slots * g.chunk_elems * sizeof(uint16_t);
     const bool by_offset = (long long)region_bytes < g.slot_off_max;   // at most 4294967295
     for (int e = threadIdx.x; e < n_entries; e += NT) {
-        const int c = list[e * 2], slot = list[e * 2 + 1];
+        const int c = list[(e0 + e) * 2], sf = list[(e0 + e) * 2 + 1], slot = sf & 0xffff;
         const size_t o = (size_t)slot * g.chunk_elems + (size_t)hr.coff * D;
         kbase[e] = region + o;
         koff[e] = (unsigned)(o * sizeof(uint16_t));
-        nrows[e] = t.comp_rows[((size_t)b * g.nc + c) * g.nT + ti];
+        nrows[e] = (sf >> 30) & 1 ? hr.cfull : t.comp_rows[((size_t)b * g.nc + c) * g.nT + ti];
     }
     __syncthreads();
     const int lk = t.tidal_lk[ti], l = lk / g.Hkv, kv = lk - l * g.Hkv;
     const uint16_t *qh = q + (((size_t)b * g.L + l) * g.Hq + (size_t)kv * G) * D;
-    const size_t p = (size_t)b * g.P + hr.pbase + hr.nts + (which ? hr.ngk : 0) + grp;
     if (by_offset) {
-        const SlotRowsOff map{region, (unsigned)region_bytes, koff, nrows, n_entries, hr.cfull};
+        const SlotRowsOff map{region, (unsigned)region_bytes, koff, nrows, n_entries, hr.cfull, first};
         subset_tile<G, RPL>(qh, map, s.ps_m + p * G, s.ps_l + p * G, s.ps_o + p * G * D, sm);
     } else {
-        const SlotRows map{kbase, nrows, n_entries, hr.cfull};
+        const SlotRows map{kbase, nrows, n_entries, hr.cfull, first};
         subset_tile<G, RPL>(qh, map, s.ps_m + p * G, s.ps_l + p * G, s.ps_o + p * G * D, sm);
     }
+}
+
+// Kept item j of tidal head ti, sequence b: the head's complements in the kept list, taken as
+// one run of rows (kept entries one after the other, cfull rows each), cut into TILE_S-row items;
+// item j is rows [j * TILE_S, (j + 1) * TILE_S) of that run.  An item may start or end inside an
+// entry, so every work-group streams a full tile whatever the complement length.  Returns at
+// once when the head has fewer items this step.
+template <int G>
+__device__ inline void kept_item(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, int j,
+                                 int ti, int b, SubsetSmem<G, RPL_S> &sm)
+{
+    const HeadRows hr = t.hr[ti];
+    const int cm = hr.cfull, cnt = s.counts[b * 2];
+    const long long v0 = (long long)j * TILE_S;
+    if (cm == 0 || j >= hr.ngk || v0 >= (long long)cnt * cm) return;
+    const int e0 = (int)(v0 / cm), e1 = (int)min((long long)cnt - 1, (v0 + TILE_S - 1) / cm);
+    const int32_t *list = s.kept_list + (size_t)b * g.n_slots * 2;
+    const size_t p = (size_t)b * g.P + hr.pbase + hr.nts + j;
+    slot_rows_tile<G, RPL_S>(g, t, s, q, list, e0, e1 - e0 + 1, (int)(v0 - (long long)e0 * cm), ti, b, p, sm);
+}
+
+// New entry e of tidal head ti, sequence b (complements copied by the host-issued recall with
+// same-step timing): the whole entry in one tile.
+template <int G, int RPL>
+__device__ inline void new_entry(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, int e,
+                                 int ti, int b, SubsetSmem<G, RPL> &sm)
+{
+    const HeadRows hr = t.hr[ti];
+    if (hr.cfull == 0 || e >= s.counts[b * 2 + 1]) return;
+    const int32_t *list = s.new_list + (size_t)b * g.knew * 2;
+    const size_t p = (size_t)b * g.P + hr.pbase + hr.nts + hr.ngk + e;
+    slot_rows_tile<G, RPL>(g, t, s, q, list, e, 1, 0, ti, b, p, sm);
 }
 
 // Recall work-group w of nw: walks the units (sequence, new entry, tidal head); each unit's
@@ -1246,12 +1297,14 @@ __device__ inline void recall_units(const Geometry &g, const Tiers &t, const Ste
 }
 
 // Fixed heads, tidal kept rows and tidal complements already in their slots: static tiles
-// first (unless the attention launch ran them), then groups of kept entries.  With REC (same-step timing), the first RECALL_WGS
-// work-groups also copy the complements listed for recall from mapped pinned memory into their
-// slots and attend to them: the step is bound by the host link then, and the copies start with
-// the launch.  Without REC the kernel keeps to its lean register budget.
+// first (unless the attention launch ran them), then the kept items (kept_item).  The
+// work-groups loop over those tiles with the grid's stride, so the launch holds about as many
+// work-groups as the compute units keep resident and none of them is spent on an item that
+// this step does not have.  With REC (same-step timing), the first RECALL_WGS work-groups copy
+// the complements listed for recall from mapped pinned memory into their slots and attend to
+// them: the step is bound by the host link then, and the copies start with the launch.
 template <int G, int RPLK, bool REC>
-__global__ __launch_bounds__(NT, REC ? (RPLK == RPL_S ? 2 : 1) : (RPLK == RPL_S ? (G <= 4 ? 4 : 3) : 2)) void tidal_fixed_kernel(
+__global__ __launch_bounds__(NT, REC ? (RPLK == RPL_S ? 2 : 1) : (G <= 4 ? 4 : 3)) void tidal_fixed_kernel(
     Geometry g, Tiers t, StepBuffers s, const uint16_t *__restrict__ q, int with_static)
 {
     union Smem {
@@ -1259,24 +1312,30 @@ __global__ __launch_bounds__(NT, REC ? (RPLK == RPL_S ? 2 : 1) : (RPLK == RPL_S 
         SubsetSmem<G, RPLK> sl;
     };
     __shared__ Smem sm;   // one block for whichever path this work-group runs
-    int bid = blockIdx.x;
+    int w = blockIdx.x, nw = gridDim.x;
     if constexpr (REC) {
-        if (bid < RECALL_WGS) {
-            recall_units<G, RPLK>(g, t, s, q, bid, RECALL_WGS, sm.sl);
+        if (w < RECALL_WGS) {
+            recall_units<G, RPLK>(g, t, s, q, w, RECALL_WGS, sm.sl);
             return;
         }
-        bid -= RECALL_WGS;
+        w -= RECALL_WGS;
+        nw -= RECALL_WGS;
     }
-    const int n_static = with_static ? g.n_static * g.B : 0;
-    if (bid < n_static) {
-        static_tile<G>(g, t, s, q, bid % g.n_static, bid / g.n_static, sm.st);
-        return;
+    const long long n_static = with_static ? (long long)g.n_static * g.B : 0;
+    // kept items in item-major order over (sequence, tidal head); the loop ends after the last
+    // item any head has this step (a head with fewer returns at once from the ones past its own)
+    int kmax = 0;
+    for (int b = 0; b < g.B; ++b) kmax = max(kmax, s.counts[b * 2]);
+    const long long n_items = min((long long)g.ng_kept, ((long long)kmax * g.comp_max + TILE_S - 1) / TILE_S);
+    const long long nh = (long long)g.nT * g.B, total = n_static + n_items * nh;
+    for (long long it = w; it < total; it += nw) {
+        if (it < n_static) {
+            static_tile<G>(g, t, s, q, (int)(it % g.n_static), (int)(it / g.n_static), sm.st);
+        } else {
+            const long long i2 = it - n_static, j = i2 / nh, rest = i2 - j * nh;
+            kept_item<G>(g, t, s, q, (int)j, (int)(rest % g.nT), (int)(rest / g.nT), sm.st);
+        }
     }
-    bid -= n_static;
-    // group-major: the grid holds room for the most kept groups a head can have, and the groups
-    // past this step's count return at once; this order puts them at the end of the dispatch
-    const int nh = g.nT * g.B, grp = bid / nh, rest = bid - grp * nh;
-    slot_group<G, RPLK>(g, t, s, q, grp, rest % g.nT, rest / g.nT, 0, sm.sl);
 }
 
 // Anchor tiles and the static tidal/fixed tiles (kept rows + text, which no selection changes)
@@ -1292,6 +1351,8 @@ __global__ __launch_bounds__(NT, G <= 4 ? 4 : 2) void attention_kernel(Geometry 
         SubsetSmem<G, RPL_S> st;
     };
     __shared__ Smem sm;
+    // one tile per work-group (the hardware's dynamic dispatch balances the slower anchor tiles
+    // against the static ones better than a grid-stride loop: measured 98 vs 107 us)
     const long long na = (long long)g.n_tiles_a * g.nA * g.B;
     const long long n = na + (long long)g.n_static * g.B;
     const long long p = blockIdx.x, a0 = p * na / n, a1 = (p + 1) * na / n;
@@ -1347,7 +1408,7 @@ template <int G, int RPL>
 __global__ __launch_bounds__(NT, RPL == RPL_S ? 4 : 2) void new_slots_kernel(Geometry g, Tiers t, StepBuffers s, const uint16_t *__restrict__ q)
 {
     __shared__ SubsetSmem<G, RPL> sm;
-    slot_group<G, RPL>(g, t, s, q, blockIdx.x, blockIdx.y, blockIdx.z, 1, sm);
+    new_entry<G, RPL>(g, t, s, q, blockIdx.x, blockIdx.y, blockIdx.z, sm);
 }
 
 // Merge of one tidal/fixed KV-head's partials (static tiles, kept groups, new groups):
@@ -1366,7 +1427,7 @@ __global__ __launch_bounds__(COMBINE_THREADS) void subset_combine_kernel(Geometr
     __shared__ float opart[OG > 1 ? OG : 1][G * D > COMBINE_THREADS ? 1 : G * D];
     const HeadRows hr = t.hr[hi];
     const bool recalls = tidal && hr.cfull > 0;   // no complement at retention 1
-    const int nk = recalls ? min((s.counts[b * 2] + hr.sg - 1) / hr.sg, hr.ngk) : 0;
+    const int nk = recalls ? (int)min(((long long)s.counts[b * 2] * hr.cfull + TILE_S - 1) / TILE_S, (long long)hr.ngk) : 0;
     // one partial per new entry (same-step timing)
     const int nn = (recalls && !g.next_step) ? min(s.counts[b * 2 + 1], g.knew) : 0;
     const int nts = hr.nts, ngk = hr.ngk, nvalid = nts + nk + nn;
@@ -1538,23 +1599,45 @@ struct AnchorCombineL {
         return hipGetLastError();
     }
 };
+// Work-groups of a grid-stride launch: the tiles, at most as many as the compute units keep
+// resident at once (the kernel's occupancy, queried once and kept in `cache`).
+template <typename K>
+long long resident_grid(K kernel, std::atomic<int> &cache, const Geometry &g, long long tiles)
+{
+    int per_cu = cache.load(std::memory_order_relaxed);
+    if (per_cu == 0) {
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, NT, 0) != hipSuccess || per_cu < 1) {
+            (void)hipGetLastError();
+            per_cu = 1;
+        }
+        cache.store(per_cu, std::memory_order_relaxed);
+    }
+    return std::min<long long>(tiles, (long long)per_cu * std::max(g.n_cu, 1));
+}
+
 template <int G>
 struct TidalFixedL {
     static hipError_t run(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, bool recall,
-                          bool with_static, hipStream_t st)
+                          bool with_static, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
     {
         recall = recall && g.nT > 0 && g.k > 0 && g.comp_max > 0;
-        const long long n = (recall ? RECALL_WGS : 0) + (with_static ? (long long)g.n_static * g.B : 0) +
-                            (long long)g.ng_kept * g.nT * g.B;
-        if (n == 0) return hipSuccess;
-        const dim3 grid((unsigned)n), block(NT);
+        const long long tiles = (with_static ? (long long)g.n_static * g.B : 0) + (long long)g.ng_kept * g.nT * g.B;
+        if (tiles == 0 && !recall) return record_pair(e0, e1, st);
+        const dim3 block(NT);
         const int ws = with_static ? 1 : 0;
-        if (g.slot_tile == TILE_S) {
-            if (recall) hipLaunchKernelGGL((tidal_fixed_kernel<G, TILE_S / 16, true>), grid, block, 0, st, g, t, s, q, ws);
-            else hipLaunchKernelGGL((tidal_fixed_kernel<G, TILE_S / 16, false>), grid, block, 0, st, g, t, s, q, ws);
+        static std::atomic<int> occ[3];
+        if (!recall) {
+            auto k = tidal_fixed_kernel<G, RPL_S, false>;
+            const dim3 grid((unsigned)resident_grid(k, occ[0], g, tiles));
+            hipExtLaunchKernelGGL(k, grid, block, 0, st, e0, e1, 0, g, t, s, q, ws);
+        } else if (g.slot_tile == TILE_S) {
+            auto k = tidal_fixed_kernel<G, RPL_S, true>;
+            const dim3 grid((unsigned)(RECALL_WGS + std::max(1LL, resident_grid(k, occ[1], g, tiles))));
+            hipExtLaunchKernelGGL(k, grid, block, 0, st, e0, e1, 0, g, t, s, q, ws);
         } else {
-            if (recall) hipLaunchKernelGGL((tidal_fixed_kernel<G, TILE_S / 8, true>), grid, block, 0, st, g, t, s, q, ws);
-            else hipLaunchKernelGGL((tidal_fixed_kernel<G, TILE_S / 8, false>), grid, block, 0, st, g, t, s, q, ws);
+            auto k = tidal_fixed_kernel<G, 2 * RPL_S, true>;
+            const dim3 grid((unsigned)(RECALL_WGS + std::max(1LL, resident_grid(k, occ[2], g, tiles))));
+            hipExtLaunchKernelGGL(k, grid, block, 0, st, e0, e1, 0, g, t, s, q, ws);
         }
         return hipGetLastError();
     }
@@ -1615,9 +1698,9 @@ hipError_t launch_select(const Geometry &g, const StepBuffers &s, float *scores,
 }
 
 hipError_t launch_tidal_fixed(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, bool recall,
-                              bool with_static, hipStream_t st)
+                              bool with_static, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
 {
-    return dispatch_g<TidalFixedL>(g.G, g, t, s, q, recall, with_static, st);
+    return dispatch_g<TidalFixedL>(g.G, g, t, s, q, recall, with_static, st, e0, e1);
 }
 
 hipError_t launch_attention(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st,

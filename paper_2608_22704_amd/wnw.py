@@ -44,7 +44,8 @@ class wnw_stats(C.Structure):
                 ("anchor_bytes", C.c_int64), ("static_bytes", C.c_int64), ("slot_rows", C.c_int64),
                 ("timed_steps", C.c_int64), ("t_anchor_ms", C.c_double), ("t_select_ms", C.c_double),
                 ("t_tidal_fixed_ms", C.c_double), ("t_new_ms", C.c_double), ("t_combine_ms", C.c_double),
-                ("t_step_ms", C.c_double), ("t_recall_ms", C.c_double)]
+                ("t_step_ms", C.c_double), ("t_recall_ms", C.c_double), ("slot_exhausted", C.c_int64),
+                ("t_host_wait_ms", C.c_double), ("t_recall_wait_ms", C.c_double)]
 
     def as_dict(self) -> dict:
         return {name: getattr(self, name) for name, _ in self._fields_}
@@ -110,6 +111,49 @@ def _ptr(t):
     return t.ctypes.data
 
 
+# element sizes the library reads or writes: bf16 bit patterns (any 2-byte dtype), fp32, int32
+_BF16, _F32, _I32 = "bf16", "f32", "i32"
+
+
+def _dev(t, kind, numel=None, what="tensor"):
+    """Address of a device tensor after checking it holds at least `numel` contiguous elements
+    of the kind the library expects (no conversion: the library reads the raw buffer)."""
+    if t is None or isinstance(t, int):
+        return t
+    if not hasattr(t, "data_ptr"):
+        raise TypeError(f"{what} must be a device tensor")
+    import torch
+    ok = {_BF16: t.element_size() == 2 and not t.dtype.is_complex,
+          _F32: t.dtype == torch.float32, _I32: t.dtype == torch.int32}[kind]
+    if not ok:
+        raise TypeError(f"{what}: expected {kind} elements, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+    if numel is not None and t.numel() < numel:
+        raise ValueError(f"{what}: needs {numel} elements, got {t.numel()}")
+    return t.data_ptr()
+
+
+def _host_in(a, dtype, numel=None, what="array"):
+    """A contiguous host copy (or view) of `a` with the given numpy dtype, size checked."""
+    a = np.ascontiguousarray(a, dtype=dtype)
+    if numel is not None and a.size != numel:
+        raise ValueError(f"{what}: expected {numel} elements, got {a.size}")
+    return a
+
+
+def _host_out(a, nbytes, what="host_dst"):
+    """Address of a writable, contiguous host array of exactly nbytes."""
+    if not isinstance(a, np.ndarray) or not a.flags.c_contiguous or not a.flags.writeable:
+        raise TypeError(f"{what} must be a writable C-contiguous numpy array")
+    if a.nbytes != nbytes:
+        raise ValueError(f"{what}: expected {nbytes} bytes, got {a.nbytes}")
+    return a.ctypes.data
+
+
+_CFG = {}   # handle value -> wnw_config, for the size checks of later calls
+
+
 def _stream(stream):
     if stream is None:
         import torch
@@ -119,20 +163,36 @@ def _stream(stream):
 
 # ---- the C ABI, one wrapper per entry point -------------------------------------------------
 
+def _cache_numel(cfg):
+    return cfg.batch * cfg.layers * cfg.kv_heads * (cfg.audio_len + cfg.text_len) * cfg.head_dim
+
+
 def wnw_init_cache(cfg: wnw_config, k_dev, v_dev, stream=None):
+    n = _cache_numel(cfg)
     h = C.c_void_p()
-    _check(lib.wnw_init_cache(C.byref(cfg), _ptr(k_dev), _ptr(v_dev), _stream(stream), C.byref(h)))
+    _check(lib.wnw_init_cache(C.byref(cfg), _dev(k_dev, _BF16, n, "k_dev"), _dev(v_dev, _BF16, n, "v_dev"),
+                              _stream(stream), C.byref(h)))
+    _CFG[h.value] = wnw_config.from_buffer_copy(cfg)
     return h
+
+
+def _cfg(ctx):
+    return _CFG.get(getattr(ctx, "value", ctx))
 
 
 def wnw_set_retention(ctx, importance, lam):
     """importance: host fp32 [L][H_kv] (or None for the uniform budget); lam: the scale."""
-    imp = None if importance is None else np.ascontiguousarray(importance, dtype=np.float32)
+    c = _cfg(ctx)
+    imp = None if importance is None else _host_in(importance, np.float32, c and c.layers * c.kv_heads, "importance")
     _check(lib.wnw_set_retention(ctx, _ptr(imp), float(lam)), ctx)
 
 
 def wnw_set_roles(ctx, roles, prefill_scores):
-    _check(lib.wnw_set_roles(ctx, _ptr(roles), _ptr(prefill_scores)), ctx)
+    """roles: host uint8 [L][H_kv]; prefill_scores: host fp32 [B][L][H_kv][T_a]."""
+    c = _cfg(ctx)
+    r = _host_in(roles, np.uint8, c and c.layers * c.kv_heads, "roles")
+    p = _host_in(prefill_scores, np.float32, c and c.batch * c.layers * c.kv_heads * c.audio_len, "prefill_scores")
+    _check(lib.wnw_set_roles(ctx, _ptr(r), _ptr(p)), ctx)
 
 
 def _tcheck(status):
@@ -143,16 +203,18 @@ def _tcheck(status):
 def wnw_voice_hits(k_dev, q_dev, span_dev, top_k, audio_len, hits_dev, stream=None):
     """k_dev [L][H_kv][rows][d] bf16, q_dev [n_tok][L][H_q][d] bf16, span_dev int32 [n_tok][2] ->
     hits_dev int32 [n_tok][L][H_q] (tensors on the device)."""
-    L, Hkv, rows, _ = k_dev.shape
+    L, Hkv, rows, D = k_dev.shape
     n_tok, _, Hq, _ = q_dev.shape
-    _tcheck(lib.wnw_voice_hits(L, Hq, Hkv, rows, audio_len, n_tok, _ptr(k_dev), _ptr(q_dev), _ptr(span_dev), top_k,
-                               _ptr(hits_dev), _stream(stream)))
+    _tcheck(lib.wnw_voice_hits(L, Hq, Hkv, rows, audio_len, n_tok, _dev(k_dev, _BF16, None, "k_dev"),
+                               _dev(q_dev, _BF16, n_tok * L * Hq * D, "q_dev"), _dev(span_dev, _I32, n_tok * 2, "span_dev"),
+                               top_k, _dev(hits_dev, _I32, n_tok * L * Hq, "hits_dev"), _stream(stream)))
 
 
 def wnw_key_sensitivity(grad_dev, sens_dev, stream=None):
     """grad_dev fp32 [n_tok][L][H_kv][T_a][d] -> sens_dev fp32 [n_tok][L][H_kv]."""
     n_tok, L, Hkv, Ta, _ = grad_dev.shape
-    _tcheck(lib.wnw_key_sensitivity(L, Hkv, Ta, n_tok, _ptr(grad_dev), _ptr(sens_dev), _stream(stream)))
+    _tcheck(lib.wnw_key_sensitivity(L, Hkv, Ta, n_tok, _dev(grad_dev, _F32, None, "grad_dev"),
+                                    _dev(sens_dev, _F32, n_tok * L * Hkv, "sens_dev"), _stream(stream)))
 
 
 def wnw_triage(hits, top_k, sens, sample, n_voice, n_anchor):
@@ -172,15 +234,25 @@ def wnw_triage(hits, top_k, sens, sample, n_voice, n_anchor):
 
 
 def wnw_append_kv(ctx, k_new_dev, v_new_dev, stream=None):
-    _check(lib.wnw_append_kv(ctx, _ptr(k_new_dev), _ptr(v_new_dev), _stream(stream)), ctx)
+    c = _cfg(ctx)
+    n = c and c.batch * c.layers * c.kv_heads * c.head_dim
+    _check(lib.wnw_append_kv(ctx, _dev(k_new_dev, _BF16, n, "k_new_dev"), _dev(v_new_dev, _BF16, n, "v_new_dev"),
+                             _stream(stream)), ctx)
 
 
 def wnw_prefill_scores(ctx, q_text_dev, scores_dev):
-    _check(lib.wnw_prefill_scores(ctx, _ptr(q_text_dev), _ptr(scores_dev)), ctx)
+    c = _cfg(ctx)
+    nq = c and c.batch * c.layers * c.q_heads * c.text_len * c.head_dim
+    ns = c and c.batch * c.layers * c.kv_heads * c.audio_len
+    _check(lib.wnw_prefill_scores(ctx, _dev(q_text_dev, _BF16, nq, "q_text_dev"), _dev(scores_dev, _F32, ns, "scores_dev")),
+           ctx)
 
 
 def wnw_set_roles_device(ctx, roles, prefill_scores_dev):
-    _check(lib.wnw_set_roles_device(ctx, _ptr(roles), _ptr(prefill_scores_dev)), ctx)
+    c = _cfg(ctx)
+    r = _host_in(roles, np.uint8, c and c.layers * c.kv_heads, "roles")
+    ns = c and c.batch * c.layers * c.kv_heads * c.audio_len
+    _check(lib.wnw_set_roles_device(ctx, _ptr(r), _dev(prefill_scores_dev, _F32, ns, "prefill_scores_dev")), ctx)
 
 
 def wnw_query_head_keep(ctx, layers, kv_heads) -> np.ndarray:
@@ -190,8 +262,12 @@ def wnw_query_head_keep(ctx, layers, kv_heads) -> np.ndarray:
 
 
 def wnw_decode_step(ctx, q_dev, out_dev, chunk_scores_dev=None, selected_dev=None, stream=None):
-    _check(lib.wnw_decode_step(ctx, _ptr(q_dev), _ptr(out_dev), _ptr(chunk_scores_dev), _ptr(selected_dev),
-                               _stream(stream)), ctx)
+    c = _cfg(ctx)
+    nq = c and c.batch * c.layers * c.q_heads * c.head_dim
+    okind = _BF16 if c and c.flags & WNW_F_OUT_BF16 else _F32
+    _check(lib.wnw_decode_step(ctx, _dev(q_dev, _BF16, nq, "q_dev"), _dev(out_dev, okind, nq, "out_dev"),
+                               _dev(chunk_scores_dev, _F32, None, "chunk_scores_dev"),
+                               _dev(selected_dev, _I32, None, "selected_dev"), _stream(stream)), ctx)
 
 
 def wnw_query_geometry(ctx) -> dict:
@@ -213,7 +289,7 @@ def wnw_get_stats(ctx) -> dict:
 
 
 def wnw_set_selection_override(ctx, sel_dev):
-    _check(lib.wnw_set_selection_override(ctx, _ptr(sel_dev)), ctx)
+    _check(lib.wnw_set_selection_override(ctx, _dev(sel_dev, _I32, None, "sel_dev")), ctx)
 
 
 def wnw_debug_set_slot_offset_limit(ctx, nbytes: int):
@@ -221,14 +297,22 @@ def wnw_debug_set_slot_offset_limit(ctx, nbytes: int):
 
 
 def wnw_debug_read_slot(ctx, b: int, chunk: int, host_dst, nbytes: int):
-    _check(lib.wnw_debug_read_slot(ctx, b, chunk, _ptr(host_dst), nbytes), ctx)
+    _check(lib.wnw_debug_read_slot(ctx, b, chunk, _host_out(host_dst, nbytes), nbytes), ctx)
 
 
 def wnw_debug_read_host_chunk(ctx, b: int, chunk: int, host_dst, nbytes: int):
-    _check(lib.wnw_debug_read_host_chunk(ctx, b, chunk, _ptr(host_dst), nbytes), ctx)
+    _check(lib.wnw_debug_read_host_chunk(ctx, b, chunk, _host_out(host_dst, nbytes), nbytes), ctx)
 
 
 def wnw_debug_read_resident(ctx, host_dst):
+    """host_dst: writable uint8 [B][n_segments]."""
+    seg = C.c_int32()
+    _check(lib.wnw_query_segments(ctx, C.byref(seg)), ctx)
+    c = _cfg(ctx)
+    need = c.batch * seg.value if c is not None else 0
+    if not isinstance(host_dst, np.ndarray) or not host_dst.flags.c_contiguous or not host_dst.flags.writeable \
+            or host_dst.dtype != np.uint8 or host_dst.nbytes < need:
+        raise ValueError(f"host_dst must be a writable contiguous uint8 array of at least {need} elements")
     _check(lib.wnw_debug_read_resident(ctx, _ptr(host_dst)), ctx)
 
 
@@ -237,6 +321,7 @@ def wnw_last_error(ctx=None) -> str:
 
 
 def wnw_destroy(ctx):
+    _CFG.pop(getattr(ctx, "value", ctx), None)
     lib.wnw_destroy(ctx)
 
 

@@ -111,3 +111,35 @@ def test_triage_host_ranking_matches_oracle():
         np.testing.assert_allclose(v1, v2, rtol=1e-15, atol=1e-15)
         np.testing.assert_allclose(h1, h2, rtol=1e-15, atol=1e-15)
         np.testing.assert_allclose(i1, i2.astype(np.float32), rtol=0, atol=0)
+
+
+def test_binding_checks_buffers_before_passing_them():
+    """The binding refuses buffers the library would misread: wrong element type, a
+    non-contiguous view, too few elements; host inputs are converted to the library's types."""
+    import numpy as np
+    import torch
+    from paper_2608_22704_amd import wnw as W
+    x = torch.zeros(64, dtype=torch.int16)
+    assert W._dev(x, W._BF16, 64) == x.data_ptr()
+    assert W._dev(torch.zeros(8, dtype=torch.bfloat16), W._BF16, 8)
+    with pytest.raises(TypeError):
+        W._dev(torch.zeros(64, dtype=torch.float32), W._BF16, 64)
+    with pytest.raises(TypeError):
+        W._dev(torch.zeros(64, dtype=torch.int64), W._I32, 64)
+    with pytest.raises(ValueError):
+        W._dev(torch.zeros(8, 8, dtype=torch.float32).t(), W._F32, 64)
+    with pytest.raises(ValueError):
+        W._dev(torch.zeros(63, dtype=torch.float32), W._F32, 64)
+    assert W._dev(None, W._F32, 64) is None
+    r = W._host_in(np.array([[0, 1], [2, 1]], dtype=np.int64), np.uint8, 4, "roles")
+    assert r.dtype == np.uint8 and r.flags.c_contiguous and r.tolist() == [[0, 1], [2, 1]]
+    p = W._host_in(np.zeros((3, 4), dtype=np.float64)[:, ::2], np.float32, 6)
+    assert p.dtype == np.float32 and p.flags.c_contiguous
+    with pytest.raises(ValueError):
+        W._host_in(np.zeros(5), np.uint8, 4)
+    buf = np.empty(16, dtype=np.uint16)
+    assert W._host_out(buf, 32) == buf.ctypes.data
+    with pytest.raises(ValueError):
+        W._host_out(buf, 30)
+    with pytest.raises(TypeError):
+        W._host_out(np.empty(32, dtype=np.uint8)[::2], 16)

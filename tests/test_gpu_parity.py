@@ -262,10 +262,72 @@ def test_voxtral_b16_full_size_sampled():
 @pytest.mark.parametrize("w", [configs.VOXTRAL_60MIN_B4_20, configs.VOXTRAL_60MIN_B4_10],
                          ids=["budget20", "budget10"])
 def test_voxtral_60min_b4_full_size_sampled(w):
-    """Batch 4 of 90k audio + 1k text positions, chunk 128: the first 24 of 512 steps, sequence 2
+    """Batch 4 of 90k audio + 1k text positions, chunk 128: the first 64 of 512 steps, sequence 2
     against the oracle with sampled heads (the oracle's anchor pass alone is ~2 G multiply-adds
-    per step per sequence)."""
-    _run(w, steps=24, head_mask_fn=_sampled(6), seqs=[2])
+    per step per sequence); the slot pool (3 k slots) is reused many times over."""
+    h = _run(w, steps=64, head_mask_fn=_sampled(6), seqs=[2])
+    assert h.recalled_total > h.geo["n_slots"], "the slot pool was not wrapped"
+
+
+@pytest.mark.parametrize("w", [configs.VOXTRAL_60MIN_B4_20, configs.VOXTRAL_60MIN_B4_10],
+                         ids=["budget20", "budget10"])
+def test_voxtral_60min_b4_benchmark_mode_full_size_sampled(w):
+    """The 60-minute batch-4 caches in the benchmark's launch configuration (the paper's
+    next-step timing, copy-engine recall from the pinned complement): 64 of 512 steps, sequence
+    1 against the oracle at every step (scores, selection, residency, anchor outputs, sampled
+    non-anchor heads), no slot ever exhausted, and more complements copied than there are slots
+    (4 k per sequence), so freed slots are refilled many times."""
+    from paper_2608_22704_amd import wnw as W
+    h = _run(w, steps=64, head_mask_fn=_sampled(6), seqs=[1], flags=W.WNW_F_SELECT_NEXT_STEP | W.WNW_F_RECALL_MEMCPY)
+    assert h.recalled_total > h.geo["n_slots"] * w.batch, "the slot pool was not wrapped"
+
+
+@pytest.mark.parametrize("nxt", [0, 1], ids=["same_step", "next_step"])
+def test_selection_state_above_64k_of_shared_memory(nxt):
+    """1 250 segments of 16 positions and k = 250 (up to 1 000 slots): the select kernel's
+    state needs ~103-109 KB of shared memory, above the 64 KB of a default launch."""
+    from paper_2608_22704_amd import wnw as W
+    w = _small("select_lds_109k", 170, L=1, Hq=8, Hkv=4, Ta=20000, Tt=16, cl=16, budget=2000, steps=6, roles=(1, 2, 1),
+               B=1)
+    _run(w, flags=W.WNW_F_SELECT_NEXT_STEP | W.WNW_F_RECALL_MEMCPY if nxt else 0)
+
+
+def test_pinned_allocation_failure_is_reported():
+    """Set-up with pinned memory refused (WNW_TEST_PINNED_LIMIT): wnw_set_roles returns
+    WNW_ERR_OOM, the context is failed (later steps return WNW_ERR_STATE) and destroys cleanly;
+    a context made afterwards works."""
+    import os
+    import torch
+    from paper_2608_22704_amd import wnw as W
+    from tests.wnw_harness import log, to_dev
+    w = configs.TINY
+    log("[case] pinned allocation failure")
+    seq = gen.sequence(w, 0)
+    kd, vd = to_dev(seq["k"][None]), to_dev(seq["v"][None])
+    cfg = W.make_config(1, w.layers, w.q_heads, w.kv_heads, w.audio_len, w.text_len, w.chunk_len, w.budget_bp)
+    ctx = W.wnw_init_cache(cfg, kd, vd)
+    os.environ["WNW_TEST_PINNED_LIMIT"] = "4096"
+    try:
+        with pytest.raises(W.WnwError) as e:
+            W.wnw_set_roles(ctx, gen.roles(w), seq["prefill"][None])
+        assert e.value.status == W.WNW_ERR_OOM and "WNW_TEST_PINNED_LIMIT" in str(e.value)
+    finally:
+        del os.environ["WNW_TEST_PINNED_LIMIT"]
+    try:
+        out = torch.empty((1, w.layers, w.q_heads, w.head_dim), dtype=torch.float32, device="cuda")
+        with pytest.raises(W.WnwError) as e:
+            W.wnw_decode_step(ctx, to_dev(seq["q"][0][None]), out)
+        assert e.value.status == W.WNW_ERR_STATE
+    finally:
+        W.wnw_destroy(ctx)
+    ctx = W.wnw_init_cache(cfg, kd, vd)
+    try:
+        W.wnw_set_roles(ctx, gen.roles(w), seq["prefill"][None])
+        W.wnw_decode_step(ctx, to_dev(seq["q"][0][None]), out)
+        torch.cuda.synchronize()
+        assert np.isfinite(out.cpu().numpy()).all()
+    finally:
+        W.wnw_destroy(ctx)
 
 
 def test_headline_config_full_size_sampled():

@@ -194,8 +194,15 @@ class Lockstep:
 
     def close(self):
         if getattr(self, "ctx", None) is not None:
-            self.W.wnw_destroy(self.ctx)
-            self.ctx = None
+            try:
+                # a step that ran out of recall slots fails the context: get_stats raises then
+                st = self.W.wnw_get_stats(self.ctx)
+                assert st["slot_exhausted"] == 0
+                self.final_stats = st
+                self.recalled_total = st["recalled_chunks"]
+            finally:
+                self.W.wnw_destroy(self.ctx)
+                self.ctx = None
         if getattr(self, "oracle", None) is not None:
             self.oracle.close()
 
