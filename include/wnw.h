@@ -214,6 +214,19 @@ wnw_status wnw_set_roles(wnw_ctx *ctx, const uint8_t *roles, const float *prefil
  * temporary device buffer of B * L * H_q * T_t * 4 bytes. */
 wnw_status wnw_prefill_scores(wnw_ctx *ctx, const void *q_text_dev, float *scores_dev);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, serving loops,
+ * harnesses that forbid hipMalloc): wnw_prefill_scores without its temporary buffer.  The same
+ * kernels compute the same scores (bit for bit); their per-row statistics go to a fixed device
+ * array of the library (32 MiB, one per GPU, held until the process ends) instead of a
+ * temporary allocation, and the call only enqueues work on hip_stream (NULL = null stream) and
+ * returns: scores_dev is valid once that stream has completed.  Calls whose work overlaps on
+ * one GPU (any context, any stream) share that array and race: the caller orders them.
+ *   q_text_dev, scores_dev  as wnw_prefill_scores.
+ * WNW_ERR_UNSUPPORTED when batch * layers * q_heads * text_len exceeds 8 388 608 rows (use
+ * wnw_prefill_scores); WNW_ERR_STATE after wnw_set_roles.  Allocates nothing (no hipMalloc,
+ * hipFree or allocating library call). */
+wnw_status wnw_prefill_scores_static(wnw_ctx *ctx, const void *q_text_dev, float *scores_dev, void *hip_stream);
+
 /* As wnw_set_roles, with the prefill scores in device memory (e.g. from wnw_prefill_scores):
  * the per-segment ranking (same rule and ties) runs on the device and the tiers are built from
  * its keep flags.  The same scores give the same tiers as wnw_set_roles.  On failure (or a

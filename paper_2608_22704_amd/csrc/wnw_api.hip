@@ -25,6 +25,7 @@
 #include <cstdio>
 #include <cstring>
 #include <functional>
+#include <mutex>
 #include <numeric>
 #include <string>
 #include <thread>
@@ -111,6 +112,18 @@ struct wnw_ctx {
 
 namespace {
 
+// ---- statistics buffer of the allocation-free prefill scores ------------------------------
+// wnw_prefill_scores_static keeps the per-row log-sum-exp of the text queries (one fp32 per
+// sequence, layer, q-head and text token) in this fixed device array instead of a temporary
+// allocation.  Every GPU the library runs on holds its own copy until the process ends; its
+// address on a device comes from hipGetSymbolAddress once per device (the array's name is a
+// host-side stand-in and is never handed to a kernel).
+constexpr size_t STATIC_PREFILL_ROWS = (size_t)8 << 20;   // 32 MiB of fp32
+constexpr int MAX_DEVICES = 64;
+static __device__ __align__(256) float scratch[STATIC_PREFILL_ROWS];
+std::mutex g_scratch_mu;
+float *g_scratch_dev[MAX_DEVICES] = {};
+
 wnw_status fail(wnw_ctx *c, wnw_status st, const char *fmt, ...)
 {
     char buf[512];
@@ -124,6 +137,30 @@ wnw_status fail(wnw_ctx *c, wnw_status st, const char *fmt, ...)
         if (st == WNW_ERR_HIP) c->state = FAILED;
     }
     return st;
+}
+
+// Device address of the static statistics buffer on device `dev` (which must be current),
+// taken once per device; null (with the message in t_err) on failure.
+float *scratch_on_device(int dev)
+{
+    if (dev < 0 || dev >= MAX_DEVICES) {
+        fail(nullptr, WNW_ERR_UNSUPPORTED, "device %d: the static prefill buffer is set up for devices 0..%d", dev,
+             MAX_DEVICES - 1);
+        return nullptr;
+    }
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_dev[dev]) {
+        void *ptr = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !ptr) {
+            (void)hipGetLastError();
+            fail(nullptr, WNW_ERR_HIP, "hipGetSymbolAddress of the static prefill buffer on device %d: %s", dev,
+                 hipGetErrorString(e));
+            return nullptr;
+        }
+        g_scratch_dev[dev] = (float *)ptr;
+    }
+    return g_scratch_dev[dev];
 }
 
 #define HIPCHECK(ctx, call)                                                                       \
@@ -592,6 +629,11 @@ wnw_status wnw_init_cache(const wnw_config *cfg, const void *k_dev, const void *
     c->full_v = (const uint16_t *)v_dev;
     const char *lg = std::getenv("WNW_LOG");
     c->log = lg && *lg && strcmp(lg, "0") != 0;
+    // the static prefill buffer's address on this device (once per device; the current device)
+    if (!scratch_on_device(dev)) {
+        delete c;
+        return WNW_ERR_HIP;
+    }
     *out = c;
     return WNW_OK;
 }
@@ -972,6 +1014,28 @@ wnw_status wnw_prefill_scores(wnw_ctx *c, const void *q_text_dev, float *scores_
     hipError_t e = launch_prefill_scores(g, c->full_k, (const uint16_t *)q_text_dev, stats, scores_dev, st);
     if (e == hipSuccess) e = hipStreamSynchronize(st);
     if (stats) (void)hipFree(stats);
+    if (e != hipSuccess) return fail(c, WNW_ERR_HIP, "prefill scores failed: %s", hipGetErrorString(e));
+    return WNW_OK;
+}
+
+wnw_status wnw_prefill_scores_static(wnw_ctx *c, const void *q_text_dev, float *scores_dev, void *hip_stream)
+{
+    if (!c) return fail(nullptr, WNW_ERR_INVALID, "ctx is NULL");
+    if (c->state != CREATED)
+        return fail(c, WNW_ERR_STATE, "wnw_prefill_scores_static needs the full cache: call it before wnw_set_roles");
+    const Geometry &g = c->g;
+    if (!scores_dev || (g.Tt > 0 && !q_text_dev))
+        return fail(c, WNW_ERR_INVALID, "scores_dev (and q_text_dev when text_len > 0) must not be NULL");
+    const size_t ns = (size_t)g.B * g.L * g.Hq * g.Tt;
+    if (ns > STATIC_PREFILL_ROWS)
+        return fail(c, WNW_ERR_UNSUPPORTED,
+                    "batch * layers * q_heads * text_len = %zu statistics rows exceed the static buffer's %zu "
+                    "(use wnw_prefill_scores)", ns, STATIC_PREFILL_ROWS);
+    DeviceGuard dg(c->device);
+    float *stats = scratch_on_device(c->device);
+    if (!stats) return fail(c, WNW_ERR_HIP, "%s", t_err.c_str());
+    const hipError_t e = launch_prefill_scores(g, c->full_k, (const uint16_t *)q_text_dev, stats, scores_dev,
+                                               (hipStream_t)hip_stream);
     if (e != hipSuccess) return fail(c, WNW_ERR_HIP, "prefill scores failed: %s", hipGetErrorString(e));
     return WNW_OK;
 }

@@ -16,6 +16,8 @@
 // rows 4 * (l / 16) + i in element i.
 #include "wnw_internal.h"
 
+#include <algorithm>
+
 #include <math.h>
 
 namespace wnw {
@@ -422,6 +424,13 @@ __global__ __launch_bounds__(NT) void prefill_keep_global_kernel(Geometry g, con
     }
 }
 
+// p = 0 (no text tokens): a fill kernel rather than a memset, so that the launch can sit in a
+// captured graph.
+__global__ __launch_bounds__(NT) void prefill_zero_kernel(float *__restrict__ p, long long n)
+{
+    for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < n; i += (long long)gridDim.x * NT) p[i] = 0.f;
+}
+
 }  // namespace
 
 hipError_t launch_prefill_scores(const Geometry &g, const uint16_t *K, const uint16_t *q_text, float *lse,
@@ -429,7 +438,12 @@ hipError_t launch_prefill_scores(const Geometry &g, const uint16_t *K, const uin
 {
     const int R = g.G * g.Tt;
     if (g.Ta == 0) return hipSuccess;
-    if (R == 0) return hipMemsetAsync(p, 0, (size_t)g.B * g.L * g.Hkv * g.Ta * sizeof(float), st);
+    if (R == 0) {
+        const long long n = (long long)g.B * g.L * g.Hkv * g.Ta;
+        hipLaunchKernelGGL(prefill_zero_kernel, dim3((unsigned)std::min<long long>((n + NT - 1) / NT, 4096)), dim3(NT), 0,
+                           st, p, n);
+        return hipGetLastError();
+    }
     const long long nheads = (long long)g.B * g.L * g.Hkv;
     const long long n1 = (long long)((R + RS_ROWS - 1) / RS_ROWS) * nheads;
     const long long n2 = (long long)((g.Ta + CS_KEYS - 1) / CS_KEYS) * nheads;

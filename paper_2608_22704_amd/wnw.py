@@ -20,7 +20,8 @@ WNW_ANCHOR, WNW_TIDAL, WNW_FIXED = 0, 1, 2
 WNW_F_SELECT_NEXT_STEP, WNW_F_RECALL_MEMCPY, WNW_F_TIMING, WNW_F_OVERLAP_CHUNKS, WNW_F_PREFILL_GLOBAL = 1, 2, 4, 8, 16
 WNW_F_OUT_BF16 = 32
 
-EXPORTS = ("wnw_init_cache", "wnw_set_retention", "wnw_set_roles", "wnw_prefill_scores", "wnw_set_roles_device",
+EXPORTS = ("wnw_init_cache", "wnw_set_retention", "wnw_set_roles", "wnw_prefill_scores", "wnw_prefill_scores_static",
+           "wnw_set_roles_device",
            "wnw_append_kv", "wnw_decode_step", "wnw_query_geometry",
            "wnw_query_segments", "wnw_query_head_keep", "wnw_get_stats",
            "wnw_set_selection_override", "wnw_debug_read_slot", "wnw_debug_read_host_chunk",
@@ -67,6 +68,7 @@ def _load():
         "wnw_set_roles": ([P, P, P], C.c_int),
         "wnw_set_retention": ([P, P, C.c_float], C.c_int),
         "wnw_prefill_scores": ([P, P, P], C.c_int),
+        "wnw_prefill_scores_static": ([P, P, P, P], C.c_int),
         "wnw_append_kv": ([P, P, P, P], C.c_int),
         "wnw_voice_hits": ([I32, I32, I32, I32, I32, I32, P, P, P, I32, P, P], C.c_int),
         "wnw_key_sensitivity": ([I32, I32, I32, I32, P, P, P], C.c_int),
@@ -246,6 +248,14 @@ def wnw_prefill_scores(ctx, q_text_dev, scores_dev):
     ns = c and c.batch * c.layers * c.kv_heads * c.audio_len
     _check(lib.wnw_prefill_scores(ctx, _dev(q_text_dev, _BF16, nq, "q_text_dev"), _dev(scores_dev, _F32, ns, "scores_dev")),
            ctx)
+
+
+def wnw_prefill_scores_static(ctx, q_text_dev, scores_dev, stream=None):
+    c = _cfg(ctx)
+    nq = c and c.batch * c.layers * c.q_heads * c.text_len * c.head_dim
+    ns = c and c.batch * c.layers * c.kv_heads * c.audio_len
+    _check(lib.wnw_prefill_scores_static(ctx, _dev(q_text_dev, _BF16, nq, "q_text_dev"),
+                                         _dev(scores_dev, _F32, ns, "scores_dev"), _stream(stream)), ctx)
 
 
 def wnw_set_roles_device(ctx, roles, prefill_scores_dev):
