@@ -168,23 +168,29 @@ def run_timing(W, torch, w, timing, recall, kd, vd, qd, roles, prefill, args, ch
         res["sweep"] = sweep
         n, n2 = d["timed_steps"], d2["timed_steps"]
         row_bytes = 2 * D * 2                      # K + V of one position, bf16
-        # with next-step timing the first launch also carries the static tidal/fixed tiles
-        first_bytes = st1["anchor_bytes"] + (st1["static_bytes"] if timing == "next" else 0)
+        # slot_rows: complement rows attended, summed over steps, sequences and tidal heads.  With
+        # next-step timing the first launch carries the static tidal/fixed tiles, the tidal launch
+        # every resident complement
         first = "attention" if timing == "next" else "anchor_attn"
-        static_in_tf = st1["static_bytes"] if timing == "same" else 0
-        # slot_rows: complement rows attended, summed over steps, sequences and tidal heads
-        tf_bytes = static_in_tf + d["slot_rows"] / K * row_bytes
-        tf2_bytes = static_in_tf + d2["slot_rows"] / nr * row_bytes
+        if timing == "next":
+            first_bytes = first2_bytes = st1["anchor_bytes"] + st1["static_bytes"]
+            tf_bytes = d["slot_rows"] / K * row_bytes
+            tf2_bytes = d2["slot_rows"] / nr * row_bytes
+        else:
+            first_bytes = first2_bytes = st1["anchor_bytes"]
+            tf_bytes = st1["static_bytes"] + d["slot_rows"] / K * row_bytes
+            tf2_bytes = st1["static_bytes"] + d2["slot_rows"] / nr * row_bytes
         a_ms, a2_ms = d["t_anchor_ms"] / n, d2["t_anchor_ms"] / n2
         tf_ms, tf2_ms = d["t_tidal_fixed_ms"] / n, d2["t_tidal_fixed_ms"] / n2
         res["first"] = first
         res["kernels"] = {
             first: {"avg_ms": a_ms, "bytes": first_bytes, "GBps": first_bytes / a_ms / 1e6},
-            first + "_pinned_selection": {"avg_ms": a2_ms, "bytes": first_bytes, "GBps": first_bytes / a2_ms / 1e6},
+            first + "_pinned_selection": {"avg_ms": a2_ms, "bytes": first2_bytes, "GBps": first2_bytes / a2_ms / 1e6},
             "merge_select": {"avg_ms": d["t_select_ms"] / n},
             "recall_wait": {"avg_ms": d["t_recall_wait_ms"] / n},
-            "tidal_fixed": {"avg_ms": tf_ms, "bytes": tf_bytes, "GBps": tf_bytes / tf_ms / 1e6},
-            "tidal_fixed_pinned_selection": {"avg_ms": tf2_ms, "bytes": tf2_bytes, "GBps": tf2_bytes / tf2_ms / 1e6},
+            "tidal_fixed": {"avg_ms": tf_ms, "bytes": tf_bytes, "GBps": tf_bytes / tf_ms / 1e6 if tf_ms > 0 else None},
+            "tidal_fixed_pinned_selection": {"avg_ms": tf2_ms, "bytes": tf2_bytes,
+                                             "GBps": tf2_bytes / tf2_ms / 1e6 if tf2_ms > 0 else None},
             "combine": {"avg_ms": d["t_combine_ms"] / n},
             "step_gpu": {"avg_ms": d["t_step_ms"] / n},
         }
@@ -376,8 +382,10 @@ def attention_roofline(k, first, workload):
     per = {}
     for name in (first, "tidal_fixed"):
         e = k[name]
-        per[name] = {"kernel": PROFILE_NAMES.get(name, name), "achieved": e["GBps"], "avg_ms": e["avg_ms"],
-                     "bytes": e["bytes"], "frac": e["GBps"] / PEAK_HBM_GBPS, "traffic": measured_traffic(name, workload),
+        gb = e["GBps"]
+        per[name] = {"kernel": PROFILE_NAMES.get(name, name), "achieved": gb, "avg_ms": e["avg_ms"],
+                     "bytes": e["bytes"], "frac": gb / PEAK_HBM_GBPS if gb else None,
+                     "traffic": measured_traffic(name, workload),
                      "achieved_without_recall": k[name + "_pinned_selection"]["GBps"]}
     tot_b = sum(p["bytes"] for p in per.values())
     tot_ms = sum(p["avg_ms"] for p in per.values())

@@ -78,8 +78,10 @@ enum {
      * a dropped chunk keeps its slot one step longer, so n_slots = (delta + 1) * k. */
     WNW_F_SELECT_NEXT_STEP = 1u,
     /* Recall with copy-engine transfers (hipMemcpyAsync from the pinned complement, spread over
-     * four internal streams) that the host issues as soon as the step's selection has run; the
-     * call polls for that point, so it returns only after the selection.  Without this flag
+     * four internal streams) that the host issues as soon as the step's selection has run: with
+     * same-step timing the call polls for that point, so it returns only after the selection;
+     * with WNW_F_SELECT_NEXT_STEP a library thread polls and issues them, and the call returns
+     * once its own work is enqueued (see wnw_decode_step).  Without this flag
      * work-groups read the complements from mapped pinned memory (same-step timing: in the
      * tidal/fixed launch, which also attends to them; next-step timing: a copy kernel on a side
      * stream) and the call never waits.  The transfers occupy no compute units: with next-step
@@ -144,12 +146,17 @@ typedef struct {
     /* WNW_F_TIMING only: summed times (ms) between HIP events recorded on the caller's stream
      * around the step's launches, and the number of timed steps. */
     int64_t timed_steps;
-    double t_anchor_ms;        /* anchor attention + chunk mass                                 */
+    double t_anchor_ms;        /* the first launch: anchor attention + chunk mass (with
+                                  WNW_F_SELECT_NEXT_STEP also the fixed heads and the tidal kept
+                                  rows)                                                         */
     double t_select_ms;        /* anchor merge, chunk scores, top-k, residency, slots (up to the
                                   end of the select kernel)                                     */
-    double t_tidal_fixed_ms;   /* fixed heads, tidal kept rows, complements already on the device;
-                                  with same-step timing (default recall) also the recall and the
-                                  attention over the recalled complements, in the same launch   */
+    double t_tidal_fixed_ms;   /* the tidal/fixed launch after the selection.  Same-step timing:
+                                  fixed heads, tidal kept rows, complements already on the
+                                  device (default recall: also the recall and the attention over
+                                  the recalled complements).  WNW_F_SELECT_NEXT_STEP: every
+                                  resident complement (after the wait for the previous step's
+                                  recall)                                                       */
     double t_new_ms;           /* WNW_F_RECALL_MEMCPY with same-step timing: attention over the
                                   complements copied this step                                  */
     double t_combine_ms;       /* merge of the tidal/fixed partial results                      */
@@ -168,6 +175,10 @@ typedef struct {
     double t_recall_wait_ms;   /* WNW_F_TIMING: on the caller's stream, from the end of the
                                   select kernel to the start of the tidal/fixed launch: with
                                   WNW_F_SELECT_NEXT_STEP the wait for the previous step's recall */
+    int64_t kept_rows;         /* complement rows of the kept lists (segments whose bytes were
+                                  on the device before the step's recall), summed over steps,
+                                  sequences and tidal heads; the rest of slot_rows were recalled
+                                  by the step before (WNW_F_SELECT_NEXT_STEP) or the step itself */
 } wnw_stats;
 
 /* Create a context for one batch of caches: the full KV cache as prefill leaves it, before any
@@ -244,7 +255,7 @@ wnw_status wnw_append_kv(wnw_ctx *ctx, const void *k_new_dev, const void *v_new_
 
 /* One decode step (Eq. 2 and "Dynamic Chunk Selection"), enqueued on hip_stream (with
  * WNW_F_SELECT_NEXT_STEP or WNW_F_RECALL_MEMCPY the recall runs on internal streams, joined by
- * events).
+ * events; with both, a library thread issues each step's copies once its selection is done).
  *   q_dev             device bf16 [B][L][H_q][d]
  *   out_dev           device fp32 [B][L][H_q][d]     attention output of every q-head
  *                     (bf16, same layout, with WNW_F_OUT_BF16)
@@ -252,8 +263,12 @@ wnw_status wnw_append_kv(wnw_ctx *ctx, const void *k_new_dev, const void *v_new_
  *   selected_dev      device int32 [B][k]            selected chunk ids, ascending
  *   hip_stream        caller's stream (NULL = null stream); outputs are valid once it has
  *                     completed.  Buffers must stay valid until then.
- * The default recall path does not block the host.  With WNW_F_RECALL_MEMCPY the call waits
- * once, mid-step (busy polling), for the selection before issuing the copies. */
+ * The default recall path does not block the host.  With WNW_F_RECALL_MEMCPY and same-step
+ * timing the call waits once, mid-step (busy polling), for the selection before issuing the
+ * copies.  With WNW_F_RECALL_MEMCPY and WNW_F_SELECT_NEXT_STEP the call returns once its work is
+ * enqueued; before enqueueing the launch that reads the previous step's recall it waits until
+ * the library's recall thread has issued that recall (that is, until the previous step's
+ * selection has run on the device), so the caller runs at most about one step ahead. */
 wnw_status wnw_decode_step(wnw_ctx *ctx, const void *q_dev, void *out_dev,
                            float *chunk_scores_dev, int32_t *selected_dev, void *hip_stream);
 
@@ -305,6 +320,14 @@ wnw_status wnw_debug_read_host_chunk(wnw_ctx *ctx, int32_t b, int32_t chunk, voi
  * attended: the resident set of that step, or of the step before it with
  * WNW_F_SELECT_NEXT_STEP (waits for the device). */
 wnw_status wnw_debug_read_resident(wnw_ctx *ctx, uint8_t *host_dst);
+
+/* Test support, no passage behind it (the stream ordering of the recall, which the paper leaves
+ * to future work).  From the next recall on, every recall is delayed by `us` microseconds: the
+ * host waits that long before issuing host-issued copies, and a host function sleeping as long is
+ * queued ahead of the copies on each copy stream (ahead of the copy kernel on the side stream
+ * without WNW_F_RECALL_MEMCPY).  Results must not change: every reader of a recalled slot waits
+ * for the recall.  0 = no delay (default); WNW_ERR_INVALID outside 0..1000000. */
+wnw_status wnw_debug_set_recall_delay(wnw_ctx *ctx, int32_t us);
 
 /* Test support, no passage behind it.
  * Slot groups of a sequence whose slot region (n_slots * chunk_bytes) has `bytes` or more read

@@ -24,6 +24,8 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <condition_variable>
+#include <deque>
 #include <functional>
 #include <mutex>
 #include <numeric>
@@ -94,11 +96,35 @@ struct wnw_ctx {
     // host-issued recall: the copies of one step go round-robin to `side` and these streams,
     // which are joined back into `side` (one stream queues copies with a gap between them)
     hipStream_t copy_st[N_COPY_STREAMS - 1] = {};
-    hipEvent_t ev_copy[N_COPY_STREAMS] = {};   // end of each stream's copies of the last recall
-    hipEvent_t ev_sel = nullptr, ev_rec = nullptr;
+    // by step parity: the end of each copy stream's share of that step's host-issued recall, and
+    // the end of that step's select kernel
+    hipEvent_t ev_copy[2][N_COPY_STREAMS] = {};
+    hipEvent_t ev_sel[2] = {}, ev_rec = nullptr;
     bool rec_pending = false;          // next-step timing: a recall issued on `side` not yet joined
-    int32_t *h_newinfo = nullptr;      // pinned: counts [B][2] then new lists [B][k][2]
+    int32_t *h_newinfo = nullptr;      // pinned, two mirrors by step parity: counts [B][2] then new
+                                       // lists [B][knew][2]
     int32_t *d_newinfo = nullptr;      // the same memory as the device addresses it
+    size_t mirror_ints = 0;            // int32 entries of one mirror
+    unsigned copy_mask[2] = {0, 0};    // by step parity: copy streams that received a copy
+
+    // Recall thread (next-step timing with host-issued copies): for each step it waits for the
+    // step's selection, then issues the step's copies and records their end events, so that
+    // wnw_decode_step returns once it has enqueued its own work.  A step waits (on the host) for
+    // the previous step's copies to be issued before it enqueues the launch that reads them.
+    struct RecallJob {
+        int64_t step;
+        bool timed;
+        hipEvent_t r0, rc[N_COPY_STREAMS];
+    };
+    std::thread rthread;
+    std::mutex rmu;
+    std::condition_variable rcv;
+    std::deque<RecallJob> rjobs;
+    int64_t rissued = -1;              // last step whose copies are issued
+    bool rstop = false;
+    hipError_t rerr = hipSuccess;      // first failure of the recall thread
+    std::string rerr_msg;
+    int32_t delay_us = 0;              // test hook: delay before every recall (wnw_debug_set_recall_delay)
     int32_t *h_flag = nullptr;         // pinned, mapped: [0] slot exhaustion seen by a select kernel
     int32_t *d_flag = nullptr;         // the same memory as the device addresses it
     double host_wait_ms = 0.0;         // host time spent waiting for selections (copy-engine recall)
@@ -376,20 +402,24 @@ wnw_status plan_comp(wnw_ctx *c, const uint8_t *flags)
     // head's kept items cut the run of its kept complements into TILE_S-row pieces
     const int kept_max = (int)std::min<int64_t>(g.nc, (int64_t)g.delta * g.span * g.k);
     int64_t P = 0;
-    g.ng_kept = g.np_max = 0;
+    g.ng_kept = g.ng_new = g.np_max = 0;
     for (int hi = 0; hi < nsub; ++hi) {
         HeadRows &h = c->hrows[hi];
-        if (h.cfull > 0) h.ngk = (int)(((int64_t)kept_max * h.cfull + TILE_S - 1) / TILE_S);
+        if (h.cfull > 0) {
+            h.ngk = (int)(((int64_t)kept_max * h.cfull + TILE_S - 1) / TILE_S);
+            h.ngn = (int)std::max<int64_t>(g.knew, ((int64_t)g.knew * h.cfull + TILE_S - 1) / TILE_S);
+        }
         g.ng_kept = std::max(g.ng_kept, h.ngk);
+        g.ng_new = std::max(g.ng_new, h.ngn);
         h.pbase = (int)P;
-        const int np = h.nts + (h.cfull > 0 ? h.ngk + g.knew : 0);
+        const int np = h.nts + (h.cfull > 0 ? h.ngk + h.ngn : 0);
         P += np;
         g.np_max = std::max(g.np_max, np);
     }
     if ((int64_t)g.np_max * g.G * 4 > 65536) return fail(c, WNW_ERR_UNSUPPORTED, "too many partial tiles per head");
     if (P * g.B > INT32_MAX / 2) return fail(c, WNW_ERR_UNSUPPORTED, "too many partial tiles");
-    const int64_t grid_max = std::max((int64_t)g.n_tiles_a * g.nA * g.B + (int64_t)g.n_static * g.B,
-                                      1024 + (int64_t)g.n_static * g.B + (int64_t)g.ng_kept * g.nT * g.B);
+    const int64_t grid_max = (int64_t)g.n_tiles_a_cap * g.nA * g.B + (int64_t)g.n_static * g.B +
+                             (int64_t)g.ng_kept * g.nT * g.B;
     if (grid_max > INT32_MAX) return fail(c, WNW_ERR_UNSUPPORTED, "launch grid too large");
     g.P = (int)P;
     return WNW_OK;
@@ -471,20 +501,35 @@ hipError_t poll_event(hipEvent_t e)
     return r;
 }
 
-// Host-issued recall: one hipMemcpyAsync per run of consecutive chunks landing in consecutive
-// slots, from the counts and new lists staged in h_newinfo (already complete on the host).
-// The runs go round-robin to `st` and the extra copy streams; ev_copy[i] marks the end of each
-// stream's share.  The caller has seen ev_sel complete on the host, so every earlier reader of
-// the target slots has finished and the copies need no device-side wait.
-wnw_status issue_copies(wnw_ctx *c, hipStream_t st)
+// Test hook: a host function that sleeps `us` microseconds, queued ahead of a recall on its
+// streams (the recall's readers must still see its bytes: tests compare against an undelayed run).
+void delay_fn(void *us)
+{
+    std::this_thread::sleep_for(std::chrono::microseconds(*(const int32_t *)us));
+}
+
+// Host-issued recall of the step of parity `par`: one hipMemcpyAsync per run of consecutive
+// chunks landing in consecutive slots, from the counts and new lists that step's select kernel
+// mirrored to pinned memory (already complete on the host).  The runs go round-robin to `st` and
+// the extra copy streams; ev_copy[par][i] marks the end of each stream's share.  The caller has
+// seen the step's selection complete on the host, so every earlier reader of the target slots
+// has finished and the copies need no device-side wait.  Returns the first failing call's status.
+hipError_t issue_copies_raw(wnw_ctx *c, int par, hipStream_t st, const char **what)
 {
     const Geometry &g = c->g;
-    const int32_t *cnt = c->h_newinfo, *nl = c->h_newinfo + g.B * 2;
+    const int32_t *cnt = c->h_newinfo + par * c->mirror_ints, *nl = cnt + g.B * 2;
     const size_t cb = (size_t)g.chunk_elems * sizeof(uint16_t);
+    hipError_t e = hipSuccess;
+    unsigned mask = 0;
+    if (c->delay_us > 0) {
+        for (int i = 0; i < N_COPY_STREAMS && e == hipSuccess; ++i)
+            e = hipLaunchHostFunc(i == 0 ? st : c->copy_st[i - 1], delay_fn, &c->delay_us);
+        mask = (1u << N_COPY_STREAMS) - 1;   // every stream holds a delay
+    }
     int n_runs = 0;
-    for (int b = 0; b < g.B && cb; ++b) {
+    for (int b = 0; b < g.B && cb && e == hipSuccess; ++b) {
         const int n = cnt[b * 2 + 1];
-        for (int i = 0; i < n;) {
+        for (int i = 0; i < n && e == hipSuccess;) {
             int j = i + 1;
             const int32_t *e0 = nl + ((size_t)b * g.knew + i) * 2;
             while (j < n) {
@@ -493,22 +538,121 @@ wnw_status issue_copies(wnw_ctx *c, hipStream_t st)
                 ++j;
             }
             const int w = n_runs++ % N_COPY_STREAMS;
-            HIPCHECK(c, hipMemcpyAsync(c->slots + ((size_t)b * g.n_slots + e0[1]) * g.chunk_elems,
-                                       c->host_comp + ((size_t)b * g.nc + e0[0]) * g.chunk_elems, cb * (j - i),
-                                       hipMemcpyHostToDevice, w == 0 ? st : c->copy_st[w - 1]));
+            mask |= 1u << w;
+            e = hipMemcpyAsync(c->slots + ((size_t)b * g.n_slots + e0[1]) * g.chunk_elems,
+                               c->host_comp + ((size_t)b * g.nc + e0[0]) * g.chunk_elems, cb * (j - i),
+                               hipMemcpyHostToDevice, w == 0 ? st : c->copy_st[w - 1]);
             i = j;
         }
     }
-    for (int i = 0; i < N_COPY_STREAMS; ++i)
-        HIPCHECK(c, hipEventRecord(c->ev_copy[i], i == 0 ? st : c->copy_st[i - 1]));
+    if (e != hipSuccess) {
+        *what = "hipMemcpyAsync of a recall";
+        return e;
+    }
+    // the readers wait only for the streams that received work (an empty wait still costs a
+    // cross-stream synchronisation on the device)
+    for (int i = 0; i < N_COPY_STREAMS; ++i) {
+        if (!(mask >> i & 1)) continue;
+        e = hipEventRecord(c->ev_copy[par][i], i == 0 ? st : c->copy_st[i - 1]);
+        if (e != hipSuccess) {
+            *what = "hipEventRecord after a recall";
+            return e;
+        }
+    }
+    c->copy_mask[par] = mask;
+    return hipSuccess;
+}
+
+wnw_status issue_copies(wnw_ctx *c, int par, hipStream_t st)
+{
+    const char *what = "";
+    const hipError_t e = issue_copies_raw(c, par, st, &what);
+    if (e != hipSuccess) return fail(c, WNW_ERR_HIP, "%s failed: %s", what, hipGetErrorString(e));
     return WNW_OK;
 }
 
-// `s` waits for every copy of the last host-issued recall (one hop per copy stream).
-wnw_status wait_copies(wnw_ctx *c, hipStream_t s)
+// `s` waits for every copy of the host-issued recall of the step of parity `par` (one hop per
+// copy stream).
+wnw_status wait_copies(wnw_ctx *c, int par, hipStream_t s)
 {
-    for (int i = 0; i < N_COPY_STREAMS; ++i) HIPCHECK(c, hipStreamWaitEvent(s, c->ev_copy[i], 0));
+    for (int i = 0; i < N_COPY_STREAMS; ++i)
+        if (c->copy_mask[par] >> i & 1) HIPCHECK(c, hipStreamWaitEvent(s, c->ev_copy[par][i], 0));
     return WNW_OK;
+}
+
+// The recall thread's loop (see wnw_ctx::RecallJob).
+void recall_thread(wnw_ctx *c)
+{
+    (void)hipSetDevice(c->device);
+    for (;;) {
+        wnw_ctx::RecallJob job;
+        {
+            std::unique_lock<std::mutex> lk(c->rmu);
+            c->rcv.wait(lk, [&] { return c->rstop || !c->rjobs.empty(); });
+            if (c->rjobs.empty()) return;   // stopping, nothing left
+            job = c->rjobs.front();
+        }
+        const int par = (int)(job.step & 1);
+        hipError_t e = hipSuccess;
+        const char *what = "";
+        if (c->rerr == hipSuccess) {
+            const auto w0 = std::chrono::steady_clock::now();
+            // a sleeping wait wakes tens to hundreds of microseconds late: poll
+            while ((e = hipEventQuery(c->ev_sel[par])) == hipErrorNotReady) {
+            }
+            const double waited = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - w0).count();
+            if (e != hipSuccess) what = "hipEventQuery of a selection";
+            if (e == hipSuccess && c->delay_us > 0) std::this_thread::sleep_for(std::chrono::microseconds(c->delay_us));
+            if (e == hipSuccess && job.timed) {
+                e = hipEventRecord(job.r0, c->side);
+                if (e != hipSuccess) what = "hipEventRecord of a recall start";
+            }
+            if (e == hipSuccess) e = issue_copies_raw(c, par, c->side, &what);
+            for (int i = 0; i < N_COPY_STREAMS && e == hipSuccess && job.timed; ++i) {
+                e = hipEventRecord(job.rc[i], i == 0 ? c->side : c->copy_st[i - 1]);
+                if (e != hipSuccess) what = "hipEventRecord of a recall end";
+            }
+            std::lock_guard<std::mutex> lk(c->rmu);
+            c->host_wait_ms += waited;
+        }
+        {
+            // a failure is kept for the caller's thread; the step still counts as issued so that
+            // no one waits for it
+            std::lock_guard<std::mutex> lk(c->rmu);
+            if (e != hipSuccess && c->rerr == hipSuccess) {
+                c->rerr = e;
+                c->rerr_msg = std::string(what) + " failed: " + hipGetErrorString(e);
+            }
+            c->rjobs.pop_front();
+            c->rissued = job.step;
+        }
+        c->rcv.notify_all();
+    }
+}
+
+// Waits until the recall thread has issued the copies of every step up to `step` (all queued
+// ones when step < 0); a failure of the thread fails the context.
+wnw_status recall_wait_issued(wnw_ctx *c, int64_t step)
+{
+    if (!c->rthread.joinable()) return WNW_OK;
+    std::unique_lock<std::mutex> lk(c->rmu);
+    c->rcv.wait(lk, [&] { return step < 0 ? c->rjobs.empty() : c->rissued >= step; });
+    if (c->rerr != hipSuccess) {
+        c->state = FAILED;
+        return fail(c, WNW_ERR_HIP, "recall thread: %s", c->rerr_msg.c_str());
+    }
+    return WNW_OK;
+}
+
+void recall_stop(wnw_ctx *c)
+{
+    if (!c->rthread.joinable()) return;
+    {
+        std::lock_guard<std::mutex> lk(c->rmu);
+        c->rstop = true;
+    }
+    c->rcv.notify_all();
+    c->rthread.join();
 }
 
 // Slot exhaustion reported by a select kernel (mapped pinned flag): the context fails, since
@@ -572,15 +716,16 @@ void free_all(wnw_ctx *c)
     void *ptrs[] = {c->aK, c->aV, c->tK, c->tV, c->fK, c->fV, c->slots, c->d_lk, c->d_tile_head, c->d_hr,
                     c->d_comp_rows, c->d_seg_rows, c->d_place,
                     c->scores_int, c->sel_int,
-                    c->s.pa_m, c->s.pa_l, c->s.pa_o, c->s.pa_mass, c->s.mass, c->s.ps_m, c->s.ps_l, c->s.ps_o,
+                    c->s.pa_m, c->s.pa_l, c->s.pa_o, c->s.pa_mass, c->s.mass, c->s.a_stat, c->s.ps_m, c->s.ps_l, c->s.ps_o,
                     c->s.streak, c->s.slot_of, c->s.slot_last, c->s.att, c->s.slot_data, c->s.slot_busy, c->s.slot_since,
-                    c->s.step, c->s.kept_list, c->s.new_list, c->s.counts, c->s.stats};
+                    c->s.step, c->s.kept_list, c->s.new_list, c->s.counts, c->s.items, c->s.stats};
     for (void *p : ptrs)
         if (p) (void)hipFree(p);
     if (c->host_comp) (void)hipHostFree(c->host_comp);
     if (c->h_newinfo) (void)hipHostFree(c->h_newinfo);
     if (c->h_flag) (void)hipHostFree(c->h_flag);
-    if (c->ev_sel) (void)hipEventDestroy(c->ev_sel);
+    for (auto e : c->ev_sel)
+        if (e) (void)hipEventDestroy(e);
     if (c->ev_rec) (void)hipEventDestroy(c->ev_rec);
     for (auto *v : {&c->pending, &c->spare})
         for (auto &ev : *v) {
@@ -591,8 +736,9 @@ void free_all(wnw_ctx *c)
     if (c->side) (void)hipStreamDestroy(c->side);
     for (int i = 0; i < N_COPY_STREAMS - 1; ++i)
         if (c->copy_st[i]) (void)hipStreamDestroy(c->copy_st[i]);
-    for (int i = 0; i < N_COPY_STREAMS; ++i)
-        if (c->ev_copy[i]) (void)hipEventDestroy(c->ev_copy[i]);
+    for (auto &par : c->ev_copy)
+        for (auto e : par)
+            if (e) (void)hipEventDestroy(e);
 }
 
 }  // namespace
@@ -704,7 +850,8 @@ wnw_status build_tiers(wnw_ctx *c, const uint8_t *keep_all)
     ALLOC(s.pa_l, B * g.nA * g.n_tiles_a_cap * g.G, "anchor partial sum");
     ALLOC(s.pa_o, B * g.nA * g.n_tiles_a_cap * g.G * Dz, "anchor partial out");
     ALLOC(s.pa_mass, B * g.nA * g.n_tiles_a_cap * g.G * g.maxc, "anchor partial mass");
-    ALLOC(s.mass, B * g.nA * g.G * g.nc, "chunk mass");
+    ALLOC(s.mass, B * g.nA * g.nc, "chunk mass");
+    ALLOC(s.a_stat, B * g.nA * g.G * 2, "anchor normalisers");
     ALLOC(s.ps_m, B * g.P * g.G, "partial max");
     ALLOC(s.ps_l, B * g.P * g.G, "partial sum");
     ALLOC(s.ps_o, B * g.P * g.G * Dz, "partial out");
@@ -716,9 +863,10 @@ wnw_status build_tiers(wnw_ctx *c, const uint8_t *keep_all)
     ALLOC(s.slot_busy, B * g.n_slots, "slot owners");
     ALLOC(s.slot_since, B * g.n_slots, "slot ages");
     ALLOC(s.step, B, "step counters");
-    ALLOC(s.kept_list, B * g.n_slots * 2, "kept list");
-    ALLOC(s.new_list, 2 * B * g.knew * 2, "new lists");   // two, alternating by step
+    ALLOC(s.kept_list, 2 * B * g.n_slots * 2, "kept lists");   // two of each, alternating by step
+    ALLOC(s.new_list, 2 * B * g.knew * 2, "new lists");
     ALLOC(s.counts, 2 * B * 2, "counts");
+    ALLOC(s.items, 4, "list items");
     ALLOC(s.stats, 8, "stats");
 #undef ALLOC
     const size_t host_bytes = B * g.nc * (size_t)g.chunk_elems * sizeof(uint16_t);
@@ -728,7 +876,8 @@ wnw_status build_tiers(wnw_ctx *c, const uint8_t *keep_all)
         HIPCHECK(c, hipHostGetDevicePointer(&dp, c->host_comp, 0));
         c->t.host_comp = (const uint16_t *)dp;
     }
-    if ((r = palloc(c, (void **)&c->h_newinfo, (B * 2 + B * g.knew * 2 + 1) * sizeof(int32_t), "recall lists")) != WNW_OK)
+    c->mirror_ints = B * 2 + B * g.knew * 2 + 1;
+    if ((r = palloc(c, (void **)&c->h_newinfo, 2 * c->mirror_ints * sizeof(int32_t), "recall lists")) != WNW_OK)
         return r;
     {
         void *dp = nullptr;
@@ -747,10 +896,10 @@ wnw_status build_tiers(wnw_ctx *c, const uint8_t *keep_all)
     if (c->cfg.flags & WNW_F_RECALL_MEMCPY) {
         for (int i = 0; i < N_COPY_STREAMS - 1; ++i)
             HIPCHECK(c, hipStreamCreateWithFlags(&c->copy_st[i], hipStreamNonBlocking));
-        for (int i = 0; i < N_COPY_STREAMS; ++i)
-            HIPCHECK(c, hipEventCreateWithFlags(&c->ev_copy[i], hipEventDisableTiming));
+        for (auto &par : c->ev_copy)
+            for (auto &e : par) HIPCHECK(c, hipEventCreateWithFlags(&e, hipEventDisableTiming));
     }
-    HIPCHECK(c, hipEventCreateWithFlags(&c->ev_sel, hipEventDisableTiming));
+    for (auto &e : c->ev_sel) HIPCHECK(c, hipEventCreateWithFlags(&e, hipEventDisableTiming));
     HIPCHECK(c, hipEventCreateWithFlags(&c->ev_rec, hipEventDisableTiming));
 
     std::vector<int32_t> lk;
@@ -893,9 +1042,17 @@ wnw_status build_tiers(wnw_ctx *c, const uint8_t *keep_all)
     }
     HIPCHECK(c, hipMemset(s.step, 0, B * sizeof(int32_t)));
     HIPCHECK(c, hipMemset(s.counts, 0, 2 * B * 2 * sizeof(int32_t)));
+    HIPCHECK(c, hipMemset(s.items, 0, 4 * sizeof(int32_t)));
     HIPCHECK(c, hipMemset(s.stats, 0, 8 * sizeof(unsigned long long)));
     HIPCHECK(c, hipDeviceSynchronize());
     c->full_k = c->full_v = nullptr;
+    if (g.next_step && (c->cfg.flags & WNW_F_RECALL_MEMCPY)) {
+        try {
+            c->rthread = std::thread(recall_thread, c);
+        } catch (...) {
+            return fail(c, WNW_ERR_OOM, "could not start the recall thread");
+        }
+    }
     c->state = READY;
     return WNW_OK;
 }
@@ -1050,6 +1207,11 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, void *out, float *scor
     {
         wnw_status r = check_exhaustion(c);
         if (r != WNW_OK) return r;
+        std::lock_guard<std::mutex> lk(c->rmu);
+        if (c->rerr != hipSuccess) {
+            c->state = FAILED;
+            return fail(c, WNW_ERR_HIP, "recall thread: %s", c->rerr_msg.c_str());
+        }
     }
     DeviceGuard dg(c->device);
     // this step's geometry: the prompt rows plus the tokens appended so far
@@ -1080,65 +1242,90 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, void *out, float *scor
 #define MARK(i) \
     if (timing) HIPCHECK(c, hipEventRecord(ev.e[i], s0))
 
-    // The counts and new lists alternate between two buffers by step, so that the next step's
-    // select kernel never rewrites the list a recall still reads (next-step timing).
-    StepBuffers sb = c->s;
-    const int par = (int)(c->steps & 1);
-    sb.counts += (size_t)par * g.B * 2;
-    sb.new_list += (size_t)par * g.B * g.knew * 2;
+    // Lists (kept, new, their counts and item counts) alternate between two buffers by step.
+    // Same-step timing: the select kernel of step s fills buffer s & 1 and step s reads it.
+    // Next-step timing: the select kernel of step s fills buffer (s + 1) & 1 for step s + 1, and
+    // step s reads buffer s & 1, filled by step s - 1: its tidal launch streams the kept list's
+    // complements (on the device before step s - 1's recall) and the new list's (the complements
+    // step s - 1 recalled, once their copies have landed).  Neither select kernel ever rewrites
+    // a list a launch or a recall still reads.  (The kept complements could join the attention
+    // launch, which runs before the wait for the copies; measured, that launch then streams
+    // slower than the two launches apart.)
+    const int par = (int)(c->steps & 1), nxt = (int)((c->steps + 1) & 1);
+    auto lists_of = [&](StepBuffers b, int i) {
+        b.counts += (size_t)i * g.B * 2;
+        b.new_list += (size_t)i * g.B * g.knew * 2;
+        b.kept_list += (size_t)i * g.B * g.n_slots * 2;
+        b.items = g.next_step ? c->s.items + 2 * i : nullptr;
+        b.items_clear = nullptr;
+        return b;
+    };
+    StepBuffers sb = lists_of(c->s, par);                         // what this step reads
+    StepBuffers sn = g.next_step ? lists_of(c->s, nxt) : sb;      // what its select kernel writes
+    if (g.next_step) sb.items_clear = sn.items;                   // zeroed before the select kernel
 
     // (1) anchor attention + chunk mass, (2) scores, top-k and residency.  With next-step
-    // timing the static tidal/fixed tiles (kept rows + text) join the anchor launch.
+    // timing the static tidal/fixed tiles (kept rows + text) and the kept list's complements
+    // join the anchor launch.
     // markers 0 and 1 are the first launch's own start and end (its dispatch excluded)
     hipEvent_t e0 = timing ? ev.e[0] : nullptr, e1 = timing ? ev.e[1] : nullptr;
     if (g.next_step)
         HIPCHECK(c, launch_attention(g, c->t, sb, q, s0, e0, e1));
     else
         HIPCHECK(c, launch_anchor(g, c->t, sb, q, s0, e0, e1));
-    HIPCHECK(c, launch_anchor_combine(g, c->t, sb, out, s0));
+    HIPCHECK(c, launch_anchor_mass(g, sb, s0));
     const bool memcpy_path = c->cfg.flags & WNW_F_RECALL_MEMCPY;
     // host-issued copies: the select kernel also writes the counts and new lists to mapped pinned
-    // memory, so the host reads them once the selection is done, never behind copies still
-    // running on the side streams
-    sb.pub = memcpy_path ? c->d_newinfo : nullptr;
-    HIPCHECK(c, launch_select(g, sb, sc, c->override_sel, sel, s0));
+    // memory (one mirror per step parity), so the host reads them once the selection is done,
+    // never behind copies still running on the side streams
+    sn.pub = memcpy_path ? c->d_newinfo + (size_t)par * c->mirror_ints : nullptr;
+    HIPCHECK(c, launch_select(g, sn, sc, c->override_sel, sel, s0));
     MARK(6);
+    HIPCHECK(c, hipEventRecord(c->ev_sel[par], s0));
+    bool combined = false;
     if (g.next_step) {
         // Next-step timing: the chunks that became resident now are copied on the side stream
-        // (host-issued: over the copy streams, of which the side stream is the first), back to
-        // back with the previous step's copies, while this step's tidal heads read only slots
-        // filled before it.  The target slots were free at this step's selection, which follows
-        // on s0 every reader of them (up to the previous step's tidal kernel).
-        HIPCHECK(c, hipEventRecord(c->ev_sel, s0));
-        HIPCHECK(c, hipStreamWaitEvent(c->side, c->ev_sel, 0));
-        if (timing) HIPCHECK(c, hipEventRecord(ev.r[0], c->side));
-        if (!memcpy_path) HIPCHECK(c, launch_recall(g, c->t, sb, c->side));
-        // this step's tidal heads read the complements the previous step recalled
+        // (host-issued: by the recall thread, over the copy streams, of which the side stream is
+        // the first), back to back with the previous step's copies.  The target slots were free
+        // at this step's selection, which follows on s0 every reader of them (up to the previous
+        // step's last tidal launch; a slot dropped now stays busy until the next selection, since
+        // this step's last launch may still read it).
+        if (!memcpy_path) {
+            HIPCHECK(c, hipStreamWaitEvent(c->side, c->ev_sel[par], 0));
+            if (timing) HIPCHECK(c, hipEventRecord(ev.r[0], c->side));
+            if (c->delay_us > 0) HIPCHECK(c, hipLaunchHostFunc(c->side, delay_fn, &c->delay_us));
+            HIPCHECK(c, launch_recall(g, c->t, sn, c->side));
+        }
+        // this step's last tidal launch reads the complements the previous step recalled
         if (c->rec_pending) {
             if (memcpy_path) {
-                wnw_status r = wait_copies(c, s0);
+                wnw_status r = recall_wait_issued(c, (int64_t)c->steps - 1);
+                if (r == WNW_OK) r = wait_copies(c, nxt, s0);
                 if (r != WNW_OK) return r;
             } else {
                 HIPCHECK(c, hipStreamWaitEvent(s0, c->ev_rec, 0));
             }
         }
-        // markers 2 and 3: the tidal launch's own start and end
-        HIPCHECK(c, launch_tidal_fixed(g, c->t, sb, q, false, false, s0, timing ? ev.e[2] : nullptr,
+        // markers 2 and 3: the launch's own start and end
+        HIPCHECK(c, launch_tidal_fixed(g, c->t, sb, q, false, false, 2, s0, timing ? ev.e[2] : nullptr,
                                        timing ? ev.e[3] : nullptr));
+        // the final merge is queued before the host waits for the selection below, so that the
+        // device never idles behind that wait
+        HIPCHECK(c, launch_subset_combine(g, c->t, sb, out, s0));
+        MARK(5);
+        combined = true;
         if (memcpy_path) {
-            // the copy engines queue these behind the previous step's copies: the link stays busy
-            const auto w0 = std::chrono::steady_clock::now();
-            HIPCHECK(c, poll_event(c->ev_sel));
-            c->host_wait_ms += std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - w0).count();
-            wnw_status r = check_exhaustion(c);
-            if (r != WNW_OK) return r;
-            r = issue_copies(c, c->side);
-            if (r != WNW_OK) return r;
-            if (timing) {
-                for (int i = 0; i < N_COPY_STREAMS; ++i)
-                    HIPCHECK(c, hipEventRecord(ev.rc[i], i == 0 ? c->side : c->copy_st[i - 1]));
-                ev.split = true;
+            // the recall thread issues this step's copies once its selection is done; the copy
+            // engines queue them behind the previous step's copies, so the link stays busy
+            wnw_ctx::RecallJob job{(int64_t)c->steps, timing, timing ? ev.r[0] : nullptr, {}};
+            if (timing)
+                for (int i = 0; i < N_COPY_STREAMS; ++i) job.rc[i] = ev.rc[i];
+            ev.split = timing;
+            {
+                std::lock_guard<std::mutex> lk(c->rmu);
+                c->rjobs.push_back(job);
             }
+            c->rcv.notify_all();
         }
         if (!memcpy_path) {
             if (timing) HIPCHECK(c, hipEventRecord(ev.r[1], c->side));
@@ -1153,47 +1340,48 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, void *out, float *scor
         // this step's select kernel; every kernel that could still read them (the previous
         // step's) precedes it on this stream.
         if (timing) HIPCHECK(c, hipEventRecord(ev.r[0], s0));
-        HIPCHECK(c, launch_tidal_fixed(g, c->t, sb, q, true, true, s0));
+        HIPCHECK(c, launch_tidal_fixed(g, c->t, sb, q, true, true, 0, s0));
         if (timing) HIPCHECK(c, hipEventRecord(ev.r[1], s0));
         MARK(3);
     } else {
-        HIPCHECK(c, hipEventRecord(c->ev_sel, s0));
         MARK(2);
         // (4a) device-resident rows while the host waits for the selection and issues the copies
-        HIPCHECK(c, launch_tidal_fixed(g, c->t, sb, q, false, true, s0));
+        HIPCHECK(c, launch_tidal_fixed(g, c->t, sb, q, false, true, 0, s0));
         MARK(3);
         // (3) copies on the side stream.  The target slots were freed by this step's select
         // kernel, which follows every earlier reader on s0; the copies start after ev_sel.
-        HIPCHECK(c, hipStreamWaitEvent(c->side, c->ev_sel, 0));
+        HIPCHECK(c, hipStreamWaitEvent(c->side, c->ev_sel[par], 0));
         if (timing) HIPCHECK(c, hipEventRecord(ev.r[0], c->side));
         const auto w0 = std::chrono::steady_clock::now();
-        HIPCHECK(c, poll_event(c->ev_sel));
+        HIPCHECK(c, poll_event(c->ev_sel[par]));
         c->host_wait_ms += std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - w0).count();
         wnw_status r = check_exhaustion(c);
         if (r != WNW_OK) return r;
-        r = issue_copies(c, c->side);
+        r = issue_copies(c, par, c->side);
         if (r != WNW_OK) return r;
         if (timing) {
-            r = wait_copies(c, c->side);
+            r = wait_copies(c, par, c->side);
             if (r != WNW_OK) return r;
             HIPCHECK(c, hipEventRecord(ev.r[1], c->side));
         }
-        r = wait_copies(c, s0);
+        r = wait_copies(c, par, s0);
         if (r != WNW_OK) return r;
         // (4b) the complements copied this step
         HIPCHECK(c, launch_new_slots(g, c->t, sb, q, s0));
         MARK(4);
         ev.has_new = timing;
     }
-    HIPCHECK(c, launch_subset_combine(g, c->t, sb, out, s0));
-    MARK(5);
+    if (!combined) {
+        HIPCHECK(c, launch_subset_combine(g, c->t, sb, out, s0));
+        MARK(5);
+    }
 #undef MARK
     if (timing) c->pending.push_back(ev);
     if (c->log) {
         // host-side trace: what this call enqueued and, with host-issued copies, what it copied
         int n_new = -1;
-        if (memcpy_path)
-            for (int b = n_new = 0; b < g.B; ++b) n_new += c->h_newinfo[b * 2 + 1];
+        if (memcpy_path && !g.next_step)
+            for (int b = n_new = 0; b < g.B; ++b) n_new += c->h_newinfo[par * c->mirror_ints + b * 2 + 1];
         fprintf(stderr, "[wnw] step %lld: %s timing, %s recall, %d sequences, new segments copied %d, host wait %.3f ms total\n",
                 (long long)c->steps, g.next_step ? "next-step" : "same-step",
                 memcpy_path ? "copy-engine" : "work-group", g.B, n_new, c->host_wait_ms);
@@ -1258,8 +1446,10 @@ wnw_status wnw_get_stats(wnw_ctx *c, wnw_stats *o)
     if (!c || !o) return fail(c, WNW_ERR_INVALID, "ctx and out must not be NULL");
     if (c->state != READY) return fail(c, WNW_ERR_STATE, "context not ready");
     DeviceGuard dg(c->device);
+    wnw_status r = recall_wait_issued(c, -1);
+    if (r != WNW_OK) return r;
     HIPCHECK(c, hipDeviceSynchronize());
-    wnw_status r = harvest_timing(c);
+    r = harvest_timing(c);
     if (r != WNW_OK) return r;
     unsigned long long st[8];
     HIPCHECK(c, hipMemcpy(st, c->s.stats, sizeof st, hipMemcpyDeviceToHost));
@@ -1297,8 +1487,12 @@ wnw_status wnw_get_stats(wnw_ctx *c, wnw_stats *o)
     o->t_step_ms = c->t_acc[5];
     o->t_recall_ms = c->t_acc[6];
     o->slot_exhausted = (int64_t)st[5];
-    o->t_host_wait_ms = c->host_wait_ms;
+    {
+        std::lock_guard<std::mutex> lk(c->rmu);
+        o->t_host_wait_ms = c->host_wait_ms;
+    }
     o->t_recall_wait_ms = c->t_acc[7];
+    o->kept_rows = (int64_t)st[7];
     return WNW_OK;
 }
 
@@ -1306,6 +1500,16 @@ wnw_status wnw_set_selection_override(wnw_ctx *c, const int32_t *sel_dev)
 {
     if (!c) return fail(nullptr, WNW_ERR_INVALID, "ctx is NULL");
     c->override_sel = sel_dev;
+    return WNW_OK;
+}
+
+wnw_status wnw_debug_set_recall_delay(wnw_ctx *c, int32_t us)
+{
+    if (!c) return fail(nullptr, WNW_ERR_INVALID, "ctx is NULL");
+    if (us < 0 || us > 1000000) return fail(c, WNW_ERR_INVALID, "recall delay must be in 0..1000000 us");
+    wnw_status r = recall_wait_issued(c, -1);   // no recall in flight reads the old value
+    if (r != WNW_OK) return r;
+    c->delay_us = us;
     return WNW_OK;
 }
 
@@ -1325,6 +1529,8 @@ wnw_status wnw_debug_read_slot(wnw_ctx *c, int32_t b, int32_t chunk, void *dst, 
     if (b < 0 || b >= g.B || chunk < 0 || chunk >= g.nc) return fail(c, WNW_ERR_INVALID, "(b, segment) out of range");
     if (bytes != (size_t)g.chunk_elems * sizeof(uint16_t)) return fail(c, WNW_ERR_INVALID, "bytes must equal chunk_bytes");
     DeviceGuard dg(c->device);
+    wnw_status r = recall_wait_issued(c, -1);
+    if (r != WNW_OK) return r;
     HIPCHECK(c, hipDeviceSynchronize());
     int32_t slot = -1;
     HIPCHECK(c, hipMemcpy(&slot, c->s.slot_of + (size_t)b * g.nc + chunk, sizeof slot, hipMemcpyDeviceToHost));
@@ -1350,6 +1556,8 @@ wnw_status wnw_debug_read_resident(wnw_ctx *c, uint8_t *dst)
     if (c->state != READY) return fail(c, WNW_ERR_STATE, "context not ready");
     const Geometry &g = c->g;
     DeviceGuard dg(c->device);
+    wnw_status r = recall_wait_issued(c, -1);
+    if (r != WNW_OK) return r;
     HIPCHECK(c, hipDeviceSynchronize());
     std::vector<int32_t> att((size_t)g.B * g.nc);
     if (!att.empty()) HIPCHECK(c, hipMemcpy(att.data(), c->s.att, att.size() * sizeof(int32_t), hipMemcpyDeviceToHost));
@@ -1361,6 +1569,7 @@ void wnw_destroy(wnw_ctx *c)
 {
     if (!c) return;
     DeviceGuard dg(c->device);
+    recall_stop(c);   // issues every queued recall first
     (void)hipDeviceSynchronize();
     free_all(c);
     delete c;

@@ -45,6 +45,8 @@ struct Geometry {
                                 // complement exceeds TILE_S rows)
     int ng_kept;                // kept items (TILE_S rows of resident complements) of the head with
                                 // the most
+    int ng_new;                 // partial entries for newly resident complements of the head with
+                                // the most (packed items or one per entry)
     int n_cu;                   // compute units of the device (grid-stride launches)
     int64_t chunk_elems;        // bf16 elements of one segment's complement block (blk_rows * D)
     int64_t slot_off_max;       // slot regions below this many bytes use buffer offsets
@@ -65,6 +67,8 @@ struct HeadRows {
     int cfull;   // block stride: the head's largest complement of one segment over the batch
     int coff;    // first row of the head in a segment's complement block: cfull K rows, cfull V rows
     int ngk;     // kept items: TILE_S-row pieces of the head's resident complements at most
+    int ngn;     // partials for newly resident complements: TILE_S-row pieces (next-step timing)
+                 // or one per entry (same-step timing), whichever is more
     int kfull;   // kept positions of a full segment (set-up)
     int klast;   // kept positions of the last segment (set-up)
 };
@@ -97,7 +101,8 @@ struct StepBuffers {
     double *pa_m, *pa_l;        // [B][nA][n_tiles_a][G]
     float *pa_o;                // [B][nA][n_tiles_a][G][D]
     double *pa_mass;            // [B][nA][n_tiles_a][G][maxc]
-    double *mass;               // [B][nA*G][nc]
+    double *mass;               // [B][nA][nc] normalised chunk mass, summed over the head's q-heads
+    double *a_stat;             // [B][nA][G][2] log-sum-exp maximum and 1 / sum of each anchor q-head
     // tidal/fixed partials, head index = tidal 0..nT-1 then fixed nT..nT+nF-1
     float *ps_m, *ps_l;         // [B][P][G]    (HeadRows::pbase + entry)
     float *ps_o;                // [B][P][G][D]
@@ -110,12 +115,21 @@ struct StepBuffers {
     int32_t *slot_since;        // [B][n_slots] step at which the slot was last freed
     int32_t *step;              // [B] steps run
     int32_t *att;               // [B][nc]  segment complements attended by the last step
-    int32_t *kept_list;         // [B][n_slots][2] (segment, slot) attended from a filled slot
-    int32_t *new_list;          // [B][knew][2]    (segment, slot) newly resident this step
+    // Lists of a step (two of each, alternating by step; see wnw_decode_step for which step
+    // reads which): kept = resident segments whose bytes are on the device already, new =
+    // segments to recall.
+    int32_t *kept_list;         // [B][n_slots][2] (segment, slot | full-stride bit 30)
+    int32_t *new_list;          // [B][knew][2]    (segment, slot)
     int32_t *counts;            // [B][2] kept, new
+    int32_t *items;             // [2] most kept / new items (TILE_S-row pieces of one head's listed
+                                // complements) over the sequences: written by the select kernel
+                                // (next-step timing), read by the next step's launches; else null
+    int32_t *items_clear;       // [2] the other step's items, zeroed by the attention launch for the
+                                // select kernel that follows it; else null
     int32_t *pub;               // host-issued recall: mapped pinned mirror of counts [B][2] and new
                                 // lists [B][knew][2], written by the select kernel; else null
-    unsigned long long *stats;  // [8] recalled, dropped, resident, slot_rows, peak, exhausted, revived
+    unsigned long long *stats;  // [8] recalled, dropped, resident, slot_rows, peak, exhausted, revived,
+                                // kept-list rows
     int32_t *exhausted;         // mapped pinned flag, set to 1 by a step that found no free slot for a
                                 // newly resident segment (the host fails the context on it)
     const int32_t *seg_rows;    // [B][nc] complement rows of a segment over the tidal heads
@@ -126,22 +140,26 @@ struct StepBuffers {
 // and end times (hipExtLaunchKernel), or are recorded back to back when there is nothing to launch.
 hipError_t launch_anchor(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q,
                          hipStream_t st, hipEvent_t e0, hipEvent_t e1);
-hipError_t launch_anchor_combine(const Geometry &g, const Tiers &t, const StepBuffers &s, void *out,
-                                 hipStream_t st);
+// Anchor normalisers and chunk masses (the selection's input); the anchor output rows are merged
+// by launch_subset_combine at the end of the step.
+hipError_t launch_anchor_mass(const Geometry &g, const StepBuffers &s, hipStream_t st);
 // Scores, selection, residency and slot bookkeeping (writes scores[B][nc] and selected[B][k]).
 hipError_t launch_select(const Geometry &g, const StepBuffers &s, float *scores, const int32_t *override_sel,
                          int32_t *selected, hipStream_t st);
 // Shared memory of the select kernel (bounded at set-up).
 inline size_t select_shared_bytes(const Geometry &g)
 {
-    return (size_t)g.nc * (SCORE_PARTS * 8 + 4 + 8 * 4) + (size_t)g.n_slots * 6 * 4;
+    return (size_t)g.nc * (SCORE_PARTS * 8 + 4 + 9 * 4) + (size_t)g.n_slots * 6 * 4;
 }
 // Fixed heads (with `with_static`), tidal kept rows and the tidal complements already in their
 // slots; with `recall`
 // (same-step timing), also the copy of the complements listed for recall from mapped pinned
 // memory into their slots and the attention over them.
+// `which`: 0 the kept list's items (after the static tiles when with_static), 1 the new list's
+// items (next-step timing: the complements the previous step copied), 2 both.
 hipError_t launch_tidal_fixed(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, bool recall,
-                              bool with_static, hipStream_t st, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
+                              bool with_static, int which, hipStream_t st, hipEvent_t e0 = nullptr,
+                              hipEvent_t e1 = nullptr);
 // Anchor attention + chunk mass together with the static tidal/fixed tiles (next-step timing).
 hipError_t launch_attention(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st,
                             hipEvent_t e0, hipEvent_t e1);
@@ -150,6 +168,7 @@ hipError_t launch_attention(const Geometry &g, const Tiers &t, const StepBuffers
 hipError_t launch_recall(const Geometry &g, const Tiers &t, const StepBuffers &s, hipStream_t st);
 // Complements already copied to their slots by the host-waited recall path.
 hipError_t launch_new_slots(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st);
+// Final merge: tidal/fixed heads' partials and anchor heads' tiles into the output rows.
 hipError_t launch_subset_combine(const Geometry &g, const Tiers &t, const StepBuffers &s, void *out,
                                  hipStream_t st);
 // Prefill scores (wnw_prefill.hip): p [B][L][Hkv][Ta] fp32 from the full K cache

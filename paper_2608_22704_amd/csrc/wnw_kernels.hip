@@ -7,8 +7,8 @@
 //                   the unnormalised P.V partial.  Logits and masses are kept in double: the
 //                   chunk ranking must agree with an fp64 reference to well under 1e-6.
 //   attention       (next-step timing) anchor tiles and the static tidal/fixed tiles in one launch.
-//   anchor_combine  log-sum-exp merge of the tiles of one anchor head -> its outputs and its
-//                   normalised chunk masses.
+//   anchor_mass     log-sum-exp normalisers of one anchor head's tiles and its normalised
+//                   chunk masses (summed over its q-heads), for the selection.
 //   scores          per chunk: fixed-order sum over anchor q-heads / chunk length (mean).
 //   select          one work-group per sequence: top-k by (score desc, id asc), streaks,
 //                   residency, slot assignment, kept/new lists.
@@ -17,7 +17,8 @@
 //                   With same-step timing its first work-groups recall: they copy newly resident
 //                   complements from mapped pinned host memory into their slots and attend to them.
 //   recall_copy     next-step recall (side stream): the copy only.
-//   subset_combine  merge of a tidal/fixed head's partials.
+//   subset_combine  final merge: a tidal/fixed head's partials, or an anchor head's tiles, into
+//                   output rows.
 //
 // Layout inside a tile: 16 lanes share one 256-byte key row (8 bf16 = 16 bytes each), so one
 // wavefront load moves 4 rows (1 KiB) fully coalesced.  A wavefront owns RPL such 4-row steps
@@ -428,38 +429,7 @@ __global__ __launch_bounds__(NT, G <= 4 ? 4 : 2) void anchor_attn_kernel(Geometr
     anchor_tile<G>(g, t, s, q, blockIdx.x, blockIdx.y, blockIdx.z, sm);
 }
 
-template <typename T>
-__device__ inline T block_max1(T v, T *red)
-{
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
-    v = wave_max(v);
-    if (lane == 0) red[wave] = v;
-    __syncthreads();
-    T m = red[0];
-    for (int w = 1; w < nw; ++w) m = fmax(m, red[w]);
-    __syncthreads();
-    return m;
-}
-
-template <typename T>
-__device__ inline T block_sum1(T v, T *red)
-{
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
-    v = wave_sum(v);
-    if (lane == 0) red[wave] = v;
-    __syncthreads();
-    T m = red[0];
-    for (int w = 1; w < nw; ++w) m += red[w];
-    __syncthreads();
-    return m;
-}
-
-// Log-sum-exp merge of the tiles of one (anchor KV-head, q-head): output row and the head's
-// normalised per-chunk softmax mass (Eq. 2 for this head), all in double.  COMBINE_THREADS
-// threads: the tiles of every output column are split over COMBINE_THREADS / D groups, summed
-// in a fixed order.
 constexpr int COMBINE_THREADS = 1024;
-constexpr int CGROUPS = COMBINE_THREADS / D;
 
 // One output element: fp32, or bf16 rounded to nearest (ties to even; NaN stays a quiet NaN).
 __device__ inline void store_out(void *out, size_t i, float v, bool bf16)
@@ -473,57 +443,204 @@ __device__ inline void store_out(void *out, size_t i, float v, bool bf16)
     static_cast<uint16_t *>(out)[i] = (uint16_t)r;
 }
 
-template <int G>
-__global__ __launch_bounds__(COMBINE_THREADS) void anchor_combine_kernel(Geometry g, Tiers t, StepBuffers s, void *out)
+// Block-wide max / sum of G values per thread (THREADS threads, in double).
+template <int G, int THREADS>
+__device__ inline void block_reduce_g(double v[G], bool is_max, double (*red)[G])
 {
-    const int ai = blockIdx.x, h = blockIdx.y, b = blockIdx.z, tid = threadIdx.x;
-    extern __shared__ double fac[];      // [n_tiles_a]
-    __shared__ double red[COMBINE_THREADS / 64];
-    __shared__ double ocol[CGROUPS][D];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+        v[h] = is_max ? wave_max(v[h]) : wave_sum(v[h]);
+        if (lane == 0) red[wave][h] = v[h];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+        double m = red[0][h];
+        for (int w = 1; w < THREADS / 64; ++w) m = is_max ? fmax(m, red[w][h]) : m + red[w][h];
+        v[h] = m;
+    }
+    __syncthreads();
+}
+
+constexpr int MASS_THREADS = 256;
+
+// Chunk masses of one anchor KV-head (the part of the anchor merge that the selection needs):
+// the log-sum-exp normalisers of its G q-heads from the tile partials, kept for the output merge
+// (anchor_out_merge, in the final launch), and the normalised per-chunk softmax mass of Eq. 2
+// summed over the G q-heads in order, all in double.
+template <int G>
+__global__ __launch_bounds__(MASS_THREADS) void anchor_mass_kernel(Geometry g, StepBuffers s)
+{
+    const int ai = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+    extern __shared__ double fac[];      // [G][n_tiles_a]
+    __shared__ double red[MASS_THREADS / 64][G];
+    __shared__ double inv_l[G];
     const int nt = g.n_tiles_a;
     const size_t base = ((size_t)b * g.nA + ai) * nt;
-    double m = -INFINITY;
-    for (int i = tid; i < nt; i += COMBINE_THREADS) m = fmax(m, s.pa_m[(base + i) * G + h]);
-    const double M = block_max1(m, red);
-    double l = 0.0;
-    for (int i = tid; i < nt; i += COMBINE_THREADS) {
-        const double mi = s.pa_m[(base + i) * G + h];
-        const double f = (M > -INFINITY && mi > -INFINITY) ? exp(mi - M) : 0.0;
-        fac[i] = f;
-        l += s.pa_l[(base + i) * G + h] * f;
-    }
-    const double L = block_sum1(l, red);      // also publishes fac[]
-    const double inv = L > 0.0 ? 1.0 / L : 0.0;
-    {
-        const int d = tid % D, grp = tid / D;
-        const int i0 = grp * nt / CGROUPS, i1 = (grp + 1) * nt / CGROUPS;
-        double acc = 0.0;
-#pragma unroll 8
-        for (int i = i0; i < i1; ++i) acc += (double)s.pa_o[((base + i) * G + h) * D + d] * fac[i];
-        ocol[grp][d] = acc;
-        __syncthreads();
-        if (grp == 0) {
+    // a segment of at most MAX_CHUNK positions spans at most MAXT tiles
+    constexpr int MAXT = (MAX_CHUNK + TILE_A - 2) / TILE_A + 1;
+    // every load of the first round (this thread's tile maxima and sums, its segment's mass
+    // partials) is issued before any is used: one memory round trip for caches of up to
+    // MASS_THREADS tiles and segments
+    double pm[G], pl[G], v[G][MAXT];
+    const int c0 = tid, t_lo0 = c0 < g.nc ? (c0 * g.cl) / TILE_A : 0;
+    const int t_hi0 = c0 < g.nc ? (min((c0 + 1) * g.cl, g.Ta) - 1) / TILE_A : -1;
 #pragma unroll
-            for (int j = 1; j < CGROUPS; ++j) acc += ocol[j][d];
-            const int lk = t.anchor_lk[ai], ll = lk / g.Hkv, kv = lk - ll * g.Hkv;
-            store_out(out, (((size_t)b * g.L + ll) * g.Hq + (size_t)kv * G + h) * D + d, (float)(acc * inv), g.out_bf16);
+    for (int h = 0; h < G; ++h) {
+        pm[h] = tid < nt ? s.pa_m[(base + tid) * G + h] : -INFINITY;
+        pl[h] = tid < nt ? s.pa_l[(base + tid) * G + h] : 0.0;
+    }
+#pragma unroll
+    for (int u = 0; u < MAXT; ++u) {
+        const int i = t_lo0 + u, j = c0 - (i * TILE_A) / g.cl;
+#pragma unroll
+        for (int h = 0; h < G; ++h) v[h][u] = i <= t_hi0 ? s.pa_mass[((base + i) * G + h) * g.maxc + j] : 0.0;
+    }
+    double m[G], l[G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+        m[h] = pm[h];
+        if (tid < nt) fac[h * nt + tid] = pm[h];
+    }
+    for (int i = tid + MASS_THREADS; i < nt; i += MASS_THREADS)
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+            const double x = s.pa_m[(base + i) * G + h];
+            fac[h * nt + i] = x;
+            m[h] = fmax(m[h], x);
+        }
+    block_reduce_g<G, MASS_THREADS>(m, true, red);
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+        l[h] = 0.0;
+        if (tid < nt) {
+            const double f = (m[h] > -INFINITY && pm[h] > -INFINITY) ? exp(pm[h] - m[h]) : 0.0;
+            fac[h * nt + tid] = f;
+            l[h] = pl[h] * f;
         }
     }
-    double *mass = s.mass + (((size_t)b * g.nA + ai) * G + h) * (size_t)g.nc;
-    for (int c = tid; c < g.nc; c += COMBINE_THREADS) {
-        const int t_lo = (c * g.cl) / TILE_A, t_hi = (min((c + 1) * g.cl, g.Ta) - 1) / TILE_A;
-        double acc = 0.0;
-        for (int i = t_lo; i <= t_hi; ++i) {
-            const int j = c - (i * TILE_A) / g.cl;
-            acc += s.pa_mass[((base + i) * G + h) * g.maxc + j] * fac[i];
+    for (int i = tid + MASS_THREADS; i < nt; i += MASS_THREADS)
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+            const double mi = fac[h * nt + i];
+            const double f = (m[h] > -INFINITY && mi > -INFINITY) ? exp(mi - m[h]) : 0.0;
+            fac[h * nt + i] = f;
+            l[h] += s.pa_l[(base + i) * G + h] * f;
         }
-        mass[c] = acc * inv;
+    block_reduce_g<G, MASS_THREADS>(l, false, red);   // also publishes fac[]
+    if (tid < G) {
+        double M = m[0], L = l[0];
+#pragma unroll
+        for (int h = 1; h < G; ++h)
+            if (tid == h) M = m[h], L = l[h];
+        const double inv = L > 0.0 ? 1.0 / L : 0.0;
+        inv_l[tid] = inv;
+        s.a_stat[(((size_t)b * g.nA + ai) * G + tid) * 2] = M;
+        s.a_stat[(((size_t)b * g.nA + ai) * G + tid) * 2 + 1] = inv;
+    }
+    __syncthreads();
+    double *mass = s.mass + ((size_t)b * g.nA + ai) * (size_t)g.nc;
+    for (int c = c0; c < g.nc; c += MASS_THREADS) {
+        const int t_lo = (c * g.cl) / TILE_A, t_hi = (min((c + 1) * g.cl, g.Ta) - 1) / TILE_A;
+        if (c != c0) {
+#pragma unroll
+            for (int u = 0; u < MAXT; ++u) {
+                const int i = t_lo + u, j = c - (i * TILE_A) / g.cl;
+#pragma unroll
+                for (int h = 0; h < G; ++h) v[h][u] = i <= t_hi ? s.pa_mass[((base + i) * G + h) * g.maxc + j] : 0.0;
+            }
+        }
+        double acc = 0.0;
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+            double a = 0.0;
+#pragma unroll
+            for (int u = 0; u < MAXT; ++u)
+                if (t_lo + u <= t_hi) a += v[h][u] * fac[h * nt + t_lo + u];
+            acc += a * inv_l[h];
+        }
+        mass[c] = acc;
+    }
+}
+
+// Output rows of one anchor KV-head's G q-heads from the tile partials and the normalisers
+// anchor_mass_kernel kept (COMBINE_THREADS threads, one work-group of the final merge launch):
+// per 16-byte column of the G * d outputs, the tiles are split over groups of threads summed in
+// a fixed order, in double.  fac: [G][n_tiles_a] doubles of shared memory.
+template <int G>
+__device__ inline void anchor_out_merge(const Geometry &g, const Tiers &t, const StepBuffers &s, void *out, int ai,
+                                        int b, double *fac, double *opart)
+{
+    constexpr int NC4 = G * D / 4, GR = COMBINE_THREADS / NC4;   // 16-byte columns, groups
+    const int tid = threadIdx.x, nt = g.n_tiles_a;
+    const size_t base = ((size_t)b * g.nA + ai) * nt;
+    const double *st = s.a_stat + ((size_t)b * g.nA + ai) * G * 2;
+    const int col = tid % NC4, grp = tid / NC4, h = col / (D / 4);
+    const int i0 = grp * nt / GR, i1 = grp < GR ? (grp + 1) * nt / GR : i0;
+    const float4 *po = (const float4 *)s.pa_o;
+    // this thread's first PF tile partials are loaded with the maxima (one memory round trip)
+    constexpr int PF = G <= 4 ? 8 : 4;
+    float4 pf[PF];
+#pragma unroll
+    for (int u = 0; u < PF; ++u) pf[u] = i0 + u < i1 ? po[(base + i0 + u) * NC4 + col] : make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int idx = tid; idx < G * nt; idx += COMBINE_THREADS) {
+        const int hh = idx / nt, i = idx - hh * nt;
+        const double M = st[hh * 2], mi = s.pa_m[(base + i) * G + hh];
+        fac[idx] = (M > -INFINITY && mi > -INFINITY) ? exp(mi - M) : 0.0;
+    }
+    __syncthreads();
+    double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
+    if (grp < GR) {
+#pragma unroll
+        for (int u = 0; u < PF; ++u)
+            if (i0 + u < i1) {
+                const double f = fac[h * nt + i0 + u];
+                a0 += (double)pf[u].x * f;
+                a1 += (double)pf[u].y * f;
+                a2 += (double)pf[u].z * f;
+                a3 += (double)pf[u].w * f;
+            }
+#pragma unroll 4
+        for (int i = i0 + PF; i < i1; ++i) {
+            const float4 v = po[(base + i) * NC4 + col];
+            const double f = fac[h * nt + i];
+            a0 += (double)v.x * f;
+            a1 += (double)v.y * f;
+            a2 += (double)v.z * f;
+            a3 += (double)v.w * f;
+        }
+        double *o = opart + ((size_t)grp * NC4 + col) * 4;
+        o[0] = a0, o[1] = a1, o[2] = a2, o[3] = a3;
+    }
+    __syncthreads();
+    if (grp == 0) {
+#pragma unroll 4
+        for (int r = 1; r < GR; ++r) {
+            const double *o = opart + ((size_t)r * NC4 + col) * 4;
+            a0 += o[0], a1 += o[1], a2 += o[2], a3 += o[3];
+        }
+        const double inv = st[h * 2 + 1];
+        const int lk = t.anchor_lk[ai], ll = lk / g.Hkv, kv = lk - ll * g.Hkv;
+        const size_t ob = (((size_t)b * g.L + ll) * g.Hq + (size_t)kv * G) * D + (size_t)col * 4;
+        store_out(out, ob, (float)(a0 * inv), g.out_bf16);
+        store_out(out, ob + 1, (float)(a1 * inv), g.out_bf16);
+        store_out(out, ob + 2, (float)(a2 * inv), g.out_bf16);
+        store_out(out, ob + 3, (float)(a3 * inv), g.out_bf16);
     }
 }
 
 // -------------------------------------------------------------------------------------------
 // Chunk scores, selection, residency and slot bookkeeping: one work-group per sequence.
 // -------------------------------------------------------------------------------------------
+// Work-group barrier for communication through shared memory only: waits for this wavefront's
+// shared-memory operations, not for its global stores (the select kernel never reads its global
+// outputs back, and waiting for them at every barrier would expose their latency each time).
+__device__ inline void lds_barrier()
+{
+    __asm__ volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 __device__ int block_scan_excl(int *a, int n, int *wsum)
 {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = blockDim.x >> 6;
@@ -538,20 +655,23 @@ __device__ int block_scan_excl(int *a, int n, int *wsum)
             if (lane >= o) x += y;
         }
         if (lane == 63) wsum[wave] = x;
-        __syncthreads();
-        if (tid == 0) {
-            int acc = 0;
-            for (int w = 0; w < nw; ++w) {
-                const int tt = wsum[w];
-                wsum[w] = acc;
-                acc += tt;
+        lds_barrier();
+        if (wave == 0) {
+            // exclusive scan of the wavefront totals by the first wavefront (nw <= 64)
+            const int tt = lane < nw ? wsum[lane] : 0;
+            int y = tt;
+#pragma unroll
+            for (int o = 1; o < 64; o <<= 1) {
+                const int z = __shfl_up(y, o);
+                if (lane >= o) y += z;
             }
-            wsum[nw] = acc;
+            if (lane < nw) wsum[lane] = y - tt;
+            if (lane == nw - 1) wsum[nw] = y;
         }
-        __syncthreads();
+        lds_barrier();
         if (i < n) a[i] = carry + wsum[wave] + x - v;
         carry += wsum[nw];
-        __syncthreads();
+        lds_barrier();
     }
     return carry;
 }
@@ -581,7 +701,7 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
                                                              const int32_t *__restrict__ ovr, int32_t *__restrict__ selected)
 {
     const int b = blockIdx.x, tid = threadIdx.x, nthr = blockDim.x;
-    const int nu = g.nc, nk = g.nchk, k = g.k, ns = g.n_slots, naq = g.nA * g.G;
+    const int nu = g.nc, nk = g.nchk, k = g.k, ns = g.n_slots, naq = g.nA;   // mass rows: one per anchor KV-head
     const bool nxt = g.next_step, two = g.span == 2;
     extern __shared__ double sdyn[];
     double *part = sdyn;                              // [SCORE_PARTS][nu]; row 0 then segment sums
@@ -600,8 +720,9 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
     int *skey = since + ns;                           // [ns] ordering key of free slots
     int *freelist = skey + ns;                        // [ns] free slots in order
     int *frank = freelist + ns;                       // [ns] rank of a free slot among the free ones
+    int *srows = frank + ns;                          // [nu] complement rows of the segment (all tidal heads)
     __shared__ int wsum[SEL_THREADS / 64 + 1];
-    __shared__ int ndrop, nrows, nrev, nfree;
+    __shared__ int ndrop, nrows, nrev, nfree, nkrows;
 
     int32_t *g_streak = s.streak + (size_t)b * nk, *g_slot_of = s.slot_of + (size_t)b * nu;
     int32_t *g_slot_last = s.slot_last + (size_t)b * nu;
@@ -610,38 +731,47 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
     int32_t *g_since = s.slot_since + (size_t)b * ns;
     const int step = s.step[b];
 
-    // state in, segment masses
-    for (int c = tid; c < nk; c += nthr) {
-        st[c] = g_streak[c];
-        fsel[c] = 0;
-    }
-    for (int u = tid; u < nu; u += nthr) {
-        sof[u] = g_slot_of[u];
-        slast[u] = g_slot_last[u];
-    }
-    for (int i = tid; i < ns; i += nthr) {
-        const int bz = g_busy[i];
-        busy[i] = bz == 2 ? 0 : bz;                   // frees deferred by the previous step
-        sdata[i] = g_data[i];
-        since[i] = g_since[i];
-    }
-    for (int idx = tid; idx < SCORE_PARTS * nu; idx += nthr) {
-        const int p = idx / nu, u = idx - p * nu;
-        const int a0 = p * naq / SCORE_PARTS, a1 = (p + 1) * naq / SCORE_PARTS;
-        const double *m = s.mass + ((size_t)b * naq + a0) * nu + u;
+    // state in, segment masses: in each round every load is issued before any store to shared
+    // memory (one memory round trip per round; one round while the arrays fit the work-group)
+    const int n_in = max(max(nk, nu), max(ns, SCORE_PARTS * nu));
+    for (int i0 = 0; i0 < n_in; i0 += nthr) {
+        const int i = i0 + tid;
+        const int v_st = i < nk ? g_streak[i] : 0;
+        const int v_sof = i < nu ? g_slot_of[i] : 0, v_slast = i < nu ? g_slot_last[i] : 0;
+        const int v_rows = i < nu ? s.seg_rows[(size_t)b * nu + i] : 0;
+        const int v_busy = i < ns ? g_busy[i] : 0, v_data = i < ns ? g_data[i] : 0, v_since = i < ns ? g_since[i] : 0;
         double acc = 0.0;
+        if (i < SCORE_PARTS * nu) {
+            const int p = i / nu, u = i - p * nu;
+            const int a0 = p * naq / SCORE_PARTS, a1 = (p + 1) * naq / SCORE_PARTS;
+            const double *m = s.mass + ((size_t)b * naq + a0) * nu + u;
 #pragma unroll 8
-        for (int a = a0; a < a1; ++a) acc += m[(size_t)(a - a0) * nu];
-        part[idx] = acc;
+            for (int a = a0; a < a1; ++a) acc += m[(size_t)(a - a0) * nu];
+            part[i] = acc;
+        }
+        if (i < nk) {
+            st[i] = v_st;
+            fsel[i] = 0;
+        }
+        if (i < nu) {
+            sof[i] = v_sof;
+            slast[i] = v_slast;
+            srows[i] = v_rows;
+        }
+        if (i < ns) {
+            busy[i] = v_busy == 2 ? 0 : v_busy;       // frees deferred by the previous step
+            sdata[i] = v_data;
+            since[i] = v_since;
+        }
     }
-    if (tid == 0) ndrop = nrows = nrev = nfree = 0;
-    __syncthreads();
+    if (tid == 0) ndrop = nrows = nrev = nfree = nkrows = 0;
+    lds_barrier();
     for (int u = tid; u < nu; u += nthr) {
         double acc = part[u];
         for (int p = 1; p < SCORE_PARTS; ++p) acc += part[p * nu + u];
         part[u] = acc;                                // each thread rewrites only its own segment
     }
-    __syncthreads();
+    lds_barrier();
     for (int c = tid; c < nk; c += nthr) {
         const bool pair = two && c + 1 < nu;
         const double acc = pair ? part[c] + part[c + 1] : part[c];
@@ -650,7 +780,7 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
         sc[c] = v;
         scores[(size_t)b * nk + c] = v;
     }
-    __syncthreads();
+    lds_barrier();
 
     // selection
     if (ovr) {
@@ -659,37 +789,52 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
             if (c >= 0 && c < nk) fsel[c] = 1;
         }
     } else {
-        for (int c = tid; c < nk; c += nthr) {
-            const float v = sc[c];
+        // rank of every chunk among all: P adjacent lanes per chunk each compare it with a
+        // contiguous share of the chunks (independent shared-memory reads, unrolled), then add
+        // their counts across the P lanes
+        int P = 1;
+        while (P < 32 && 2 * P * nk <= nthr) P *= 2;
+        const int span = (nk + P - 1) / P;
+        for (int c0 = 0; c0 < nk * P; c0 += nthr) {
+            const int w = c0 + tid, c = w / P, part = w - c * P;
             int cnt = 0;
-            for (int j = 0; j < nk; ++j) {
-                const float w = sc[j];
-                cnt += (w > v) || (w == v && j < c);
+            float v = 0.f;
+            if (c < nk) {
+                v = sc[c];
+                const int ja = part * span, jb = min(nk, ja + span);
+#pragma unroll 8
+                for (int j = ja; j < jb; ++j) {
+                    const float x = sc[j];
+                    cnt += (x > v) || (x == v && j < c);
+                }
             }
-            fsel[c] = cnt < k;
+            for (int o = 1; o < P; o <<= 1) cnt += __shfl_xor(cnt, o);
+            if (c < nk && part == 0) fsel[c] = cnt < k;
         }
     }
-    __syncthreads();
+    lds_barrier();
     for (int c = tid; c < nk; c += nthr) st[c] = fsel[c] ? 0 : min(st[c] + 1, g.delta);
-    __syncthreads();
+    lds_barrier();
 
-    // segment residency, drops
+    // segment residency, drops (counters summed per thread, then per wavefront: one shared-memory
+    // atomic per wavefront)
+    int c_rows = 0, c_drop = 0, c_rev = 0;
     for (int u = tid; u < nu; u += nthr) {
         const bool now = (u < nk && st[u] < g.delta) || (two && u >= 1 && u - 1 < nk && st[u - 1] < g.delta);
         const bool owned = sof[u] >= 0;     // has a slot: resident after the previous step
         fdrop[u] = owned && !now;
         fnew[u] = now && !owned;
-        fkept[u] = nxt ? owned : (now && owned);
+        fkept[u] = now && owned;
         const bool att = nxt ? owned : now;
         g_att[u] = att;
-        if (att) atomicAdd(&nrows, s.seg_rows[(size_t)b * nu + u]);
+        if (att) c_rows += srows[u];
         if (fdrop[u]) {
             busy[sof[u]] = nxt ? 2 : 0;
             since[sof[u]] = step;
-            atomicAdd(&ndrop, 1);
+            ++c_drop;
         }
     }
-    __syncthreads();
+    lds_barrier();
     // revival: the segment's bytes are still in the free slot it last occupied
     for (int u = tid; u < nu; u += nthr)
         if (fnew[u]) {
@@ -698,15 +843,23 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
                 busy[sl] = 1;
                 sof[u] = sl;
                 fnew[u] = 0;
-                if (!nxt) fkept[u] = 1;
-                atomicAdd(&nrev, 1);
+                fkept[u] = 1;
+                ++c_rev;
             }
         }
-    __syncthreads();
+    c_rows = wave_sum(c_rows);
+    c_drop = wave_sum(c_drop);
+    c_rev = wave_sum(c_rev);
+    if ((tid & 63) == 0) {
+        if (c_rows) atomicAdd(&nrows, c_rows);
+        if (c_drop) atomicAdd(&ndrop, c_drop);
+        if (c_rev) atomicAdd(&nrev, c_rev);
+    }
+    lds_barrier();
 
     // selected chunk ids, ascending
     for (int c = tid; c < nk; c += nthr) rank[c] = fsel[c];
-    __syncthreads();
+    lds_barrier();
     const int nsel = block_scan_excl(rank, nk, wsum);
     if (selected) {
         for (int c = tid; c < nk; c += nthr)
@@ -726,7 +879,7 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
         const unsigned long long bal = __ballot(fr);   // free slots: one count per wavefront
         if ((tid & 63) == 0 && bal) atomicAdd(&nfree, __popcll(bal));
     }
-    __syncthreads();
+    lds_barrier();
     {
         // every free slot counts the free slots ordered before it; the comparisons of one slot are
         // split over `split` threads that add their counts (integer sums: any order)
@@ -736,7 +889,7 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
             const int ki = skey[i];
             if (ki < 0) continue;
             int r = 0;
-#pragma unroll 8
+#pragma unroll 16
             for (int j = part * span_j, je = min(ns, (part + 1) * span_j); j < je; ++j) {
                 const int kj = skey[j];
                 r += kj >= 0 && (kj < ki || (kj == ki && j < i));
@@ -744,30 +897,14 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
             if (r) atomicAdd(&frank[i], r);
         }
     }
-    __syncthreads();
+    lds_barrier();
     for (int i = tid; i < ns; i += nthr)
         if (skey[i] >= 0) freelist[frank[i]] = i;   // the ranks of the free slots are 0 .. nfree-1, each once
-    __syncthreads();
-
-    // kept list first (it needs the slots of segments dropped now under next-step timing)
-    for (int u = tid; u < nu; u += nthr) rank[u] = fkept[u];
-    __syncthreads();
-    const int nkept = block_scan_excl(rank, nu, wsum);
-    // bit 30 of a kept entry's slot: every tidal head's complement of the segment has its full
-    // stride of rows (the tiles then skip the per-head row count)
-    int32_t *kl = s.kept_list + (size_t)b * ns * 2;
-    for (int u = tid; u < nu; u += nthr)
-        if (fkept[u]) {
-            kl[rank[u] * 2] = u;
-            kl[rank[u] * 2 + 1] = sof[u] | (s.seg_rows[(size_t)b * nu + u] * 2 == g.blk_rows ? 1 << 30 : 0);
-        }
-    __syncthreads();
-    for (int u = tid; u < nu; u += nthr)
-        if (fdrop[u]) sof[u] = -1;
+    lds_barrier();
 
     // segments to recall take the free slots in that order (lowest id first)
     for (int u = tid; u < nu; u += nthr) rank[u] = fnew[u];
-    __syncthreads();
+    lds_barrier();
     const int nnew = block_scan_excl(rank, nu, wsum);
     int32_t *nl = s.new_list + (size_t)b * g.knew * 2;
     for (int u = tid; u < nu; u += nthr)
@@ -786,7 +923,29 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
                 hl[rank[u] * 2 + 1] = slot;
             }
         }
-    __syncthreads();
+    // kept list: the resident segments whose bytes are on the device already (kept from the
+    // previous step or revived), attended by this step (same-step timing) or by the next one
+    // (next-step timing, which also attends the new list's segments once they are copied).
+    // Bit 30 of an entry's slot: every tidal head's complement of the segment has its full
+    // stride of rows (the tiles then skip the per-head row count).
+    for (int u = tid; u < nu; u += nthr) rank[u] = fkept[u];
+    lds_barrier();
+    const int nkept = block_scan_excl(rank, nu, wsum);
+    int32_t *kl = s.kept_list + (size_t)b * ns * 2;
+    int c_krows = 0;
+    for (int u = tid; u < nu; u += nthr)
+        if (fkept[u]) {
+            const int rows = srows[u];
+            kl[rank[u] * 2] = u;
+            kl[rank[u] * 2 + 1] = sof[u] | (rows * 2 == g.blk_rows ? 1 << 30 : 0);
+            c_krows += rows;
+        }
+    c_krows = wave_sum(c_krows);
+    if ((tid & 63) == 0 && c_krows) atomicAdd(&nkrows, c_krows);
+    lds_barrier();
+    for (int u = tid; u < nu; u += nthr)
+        if (fdrop[u]) sof[u] = -1;
+    lds_barrier();
 
     // state out
     for (int c = tid; c < nk; c += nthr) g_streak[c] = st[c];
@@ -807,11 +966,17 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
             s.pub[b * 2] = nkept;
             s.pub[b * 2 + 1] = nn;
         }
+        if (s.items) {
+            // items (TILE_S-row pieces of one head's listed complements) of the lists, the most
+            // over the sequences: the next step's launches size their work from it
+            atomicMax(&s.items[0], (int)(((long long)nkept * g.comp_max + TILE_S - 1) / TILE_S));
+            atomicMax(&s.items[1], (int)(((long long)nn * g.comp_max + TILE_S - 1) / TILE_S));
+        }
         s.step[b] = step + 1;
         atomicAdd(&s.stats[0], (unsigned long long)nn);
         atomicAdd(&s.stats[1], (unsigned long long)ndrop);
         // resident segments after the step
-        const int nres = nxt ? nkept - ndrop + nrev + nn : nkept + nn;
+        const int nres = nkept + nn;
         atomicAdd(&s.stats[2], (unsigned long long)nres);
         atomicAdd(&s.stats[3], (unsigned long long)nrows);
         atomicMax(&s.stats[4], (unsigned long long)nres);
@@ -823,6 +988,7 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
             if (s.exhausted) *(volatile int32_t *)s.exhausted = 1;
         }
         atomicAdd(&s.stats[6], (unsigned long long)nrev);
+        atomicAdd(&s.stats[7], (unsigned long long)nkrows);
     }
 }
 
@@ -854,11 +1020,15 @@ struct RowPtr {
 // Shared memory of one subset tile; one instance per work-group, whichever row map it runs.
 template <int G, int RPL>
 struct SubsetSmem {
-    static constexpr int NR = 4 * RPL, HS = (G + 3) / 4, QS = 136;
+    static constexpr int NR = 4 * RPL, HS = (G + 3) / 4, QS = 136, MAXE = NR * WAVES;
     uint4 kst[WAVES][NR * 16];                // K rows, then the P.V partials of each wavefront
     uint16_t qs[HS * 4 * QS];                 // q, rows padded to 272 bytes
     float xf[G * WAVES * NR];                 // probabilities
     float wm[WAVES * G], wl[WAVES * G];
+    // entries of a run of slot rows (slot_rows_tile; a tile's entries never exceed its rows)
+    const uint16_t *kbase[MAXE];
+    unsigned koff[MAXE];
+    int nrows[MAXE];
 };
 
 template <int G, int RPL, class RowMap>
@@ -880,10 +1050,13 @@ __device__ inline void subset_tile(const uint16_t *__restrict__ qh, const RowMap
     float *xf = sm.xf, *wm = sm.wm, *wl = sm.wl;
     float *wo = (float *)&kst[wave][0];
 
-    for (int i = tid; i < HS * 4 * (D / 8); i += NT) {
-        const int h = i / (D / 8), u = i - h * (D / 8);
-        *(uint4 *)(qs + h * QS + u * 8) = h < G ? *(const uint4 *)(qh + h * D + u * 8) : make_uint4(0, 0, 0, 0);
-    }
+    // q: loaded into a register first and written to shared memory only once the K/V loads are
+    // issued, so that no wavefront waits for it before starting its stream
+    static_assert(HS * 4 * (D / 8) <= NT, "one 16-byte piece of q per thread");
+    const bool q_lane = tid < HS * 4 * (D / 8);
+    const int qh_i = tid / (D / 8), qu = tid - qh_i * (D / 8);
+    uint4 qv = make_uint4(0, 0, 0, 0);
+    if (q_lane && qh_i < G) qv = *(const uint4 *)(qh + qh_i * D + qu * 8);
     uint4 kr[RPL], vr[RPL];
     bool ok[RPL];
     if constexpr (RowMap::contiguous) {
@@ -905,16 +1078,23 @@ __device__ inline void subset_tile(const uint16_t *__restrict__ qh, const RowMap
         const int cm = map.comp_max;
         const unsigned vd = (unsigned)cm * (D * 2);   // an entry's V rows follow its K rows
         const int v0 = map.first + wave * NR + rg;     // row within the entries, from entry 0's first
-        int e = v0 / cm, rr = v0 - e * cm;
+        // every row's entry and offset first (independent shared-memory reads, one wait), then
+        // all the loads back to back
+        unsigned off[RPL];
+        const unsigned off0 = map.koff[0] + sub * 16;
 #pragma unroll
         for (int i = 0; i < RPL; ++i) {
-            ok[i] = e < map.n_entries && rr < map.nrows[e < map.n_entries ? e : 0];
-            const unsigned o = (ok[i] ? map.koff[e] + (unsigned)rr * (D * 2) : map.koff[0]) + sub * 16;
-            kr[i] = buf_load_nt(rs, o);
-            vr[i] = buf_load_nt(rs, o + vd);
-            rr += 4;
-            while (rr >= cm) rr -= cm, ++e;
+            const int v = v0 + 4 * i, e = v / cm, rr = v - e * cm;
+            const int ec = e < map.n_entries ? e : 0;
+            const int nr = map.nrows[ec];
+            const unsigned ko = map.koff[ec];
+            ok[i] = e < map.n_entries && rr < nr;
+            off[i] = ok[i] ? ko + (unsigned)rr * (D * 2) + sub * 16 : off0;
         }
+#pragma unroll
+        for (int i = 0; i < RPL; ++i) kr[i] = buf_load_nt(rs, off[i]);
+#pragma unroll
+        for (int i = 0; i < RPL; ++i) vr[i] = buf_load_nt(rs, off[i] + vd);
     } else {
 #pragma unroll
         for (int i = 0; i < RPL; ++i) {
@@ -935,6 +1115,7 @@ __device__ inline void subset_tile(const uint16_t *__restrict__ qh, const RowMap
                 vr[i] = ok[i] ? load_nt(rp.v + sub * 8) : make_uint4(0, 0, 0, 0);
         }
     }
+    if (q_lane) *(uint4 *)(qs + qh_i * QS + qu * 8) = qv;
     // valid rows of this wavefront as a mask (bit i * 4 + rg), for the logits
     unsigned long long rowmask = 0;
 #pragma unroll
@@ -1202,10 +1383,9 @@ __device__ inline void slot_rows_tile(const Geometry &g, const Tiers &t, const S
                                       const int32_t *list, int e0, int n_entries, int first, int ti, int b, size_t p,
                                       SubsetSmem<G, RPL> &sm)
 {
-    constexpr int MAXE = 4 * RPL * WAVES;   // entries of one tile never exceed its rows
-    __shared__ const uint16_t *kbase[MAXE];
-    __shared__ unsigned koff[MAXE];
-    __shared__ int nrows[MAXE];
+    const uint16_t **kbase = sm.kbase;
+    unsigned *koff = sm.koff;
+    int *nrows = sm.nrows;
     const HeadRows hr = t.hr[ti];
     const uint16_t *region = t.slots + (size_t)b * g.n_slots * g.chunk_elems;
     const size_t region_bytes = (size_t)g.n_slots * g.chunk_elems * sizeof(uint16_t);
@@ -1229,23 +1409,24 @@ __device__ inline void slot_rows_tile(const Geometry &g, const Tiers &t, const S
     }
 }
 
-// Kept item j of tidal head ti, sequence b: the head's complements in the kept list, taken as
-// one run of rows (kept entries one after the other, cfull rows each), cut into TILE_S-row items;
-// item j is rows [j * TILE_S, (j + 1) * TILE_S) of that run.  An item may start or end inside an
-// entry, so every work-group streams a full tile whatever the complement length.  Returns at
-// once when the head has fewer items this step.
+// Item j of list `which` (0 kept, 1 new) of tidal head ti, sequence b: the head's complements
+// of the listed segments, taken as one run of rows (entries one after the other, cfull rows
+// each), cut into TILE_S-row items; item j is rows [j * TILE_S, (j + 1) * TILE_S) of that run.
+// An item may start or end inside an entry, so every work-group streams a full tile whatever the
+// complement length.  Returns at once when the head has fewer items this step.
 template <int G>
-__device__ inline void kept_item(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, int j,
-                                 int ti, int b, SubsetSmem<G, RPL_S> &sm)
+__device__ inline void list_item(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, int which,
+                                 int j, int ti, int b, SubsetSmem<G, RPL_S> &sm)
 {
     const HeadRows hr = t.hr[ti];
-    const int cm = hr.cfull, cnt = s.counts[b * 2];
+    const int cm = hr.cfull, cnt = s.counts[b * 2 + which];
     const long long v0 = (long long)j * TILE_S;
-    if (cm == 0 || j >= hr.ngk || v0 >= (long long)cnt * cm) return;
+    if (cm == 0 || j >= (which ? hr.ngn : hr.ngk) || v0 >= (long long)cnt * cm) return;
     const int e0 = (int)(v0 / cm), e1 = (int)min((long long)cnt - 1, (v0 + TILE_S - 1) / cm);
-    const int32_t *list = s.kept_list + (size_t)b * g.n_slots * 2;
-    const size_t p = (size_t)b * g.P + hr.pbase + hr.nts + j;
-    slot_rows_tile<G, RPL_S>(g, t, s, q, list, e0, e1 - e0 + 1, (int)(v0 - (long long)e0 * cm), ti, b, p, sm);
+    const int32_t *list = which ? s.new_list + (size_t)b * g.knew * 2 : s.kept_list + (size_t)b * g.n_slots * 2;
+    const size_t p = (size_t)b * g.P + hr.pbase + hr.nts + (which ? hr.ngk : 0) + j;
+    const int n_entries = e1 - e0 + 1, first = (int)(v0 - (long long)e0 * cm);
+    slot_rows_tile<G, RPL_S>(g, t, s, q, list, e0, n_entries, first, ti, b, p, sm);
 }
 
 // New entry e of tidal head ti, sequence b (complements copied by the host-issued recall with
@@ -1297,7 +1478,7 @@ __device__ inline void recall_units(const Geometry &g, const Tiers &t, const Ste
 }
 
 // Fixed heads, tidal kept rows and tidal complements already in their slots: static tiles
-// first (unless the attention launch ran them), then the kept items (kept_item).  The
+// first (unless the attention launch ran them), then the items of one list (list_item).  The
 // work-groups loop over those tiles with the grid's stride, so the launch holds about as many
 // work-groups as the compute units keep resident and none of them is spent on an item that
 // this step does not have.  With REC (same-step timing), the first RECALL_WGS work-groups copy
@@ -1305,7 +1486,7 @@ __device__ inline void recall_units(const Geometry &g, const Tiers &t, const Ste
 // them: the step is bound by the host link then, and the copies start with the launch.
 template <int G, int RPLK, bool REC>
 __global__ __launch_bounds__(NT, REC ? (RPLK == RPL_S ? 2 : 1) : (G <= 4 ? 4 : 3)) void tidal_fixed_kernel(
-    Geometry g, Tiers t, StepBuffers s, const uint16_t *__restrict__ q, int with_static)
+    Geometry g, Tiers t, StepBuffers s, const uint16_t *__restrict__ q, int with_static, int which)
 {
     union Smem {
         SubsetSmem<G, RPL_S> st;
@@ -1322,18 +1503,29 @@ __global__ __launch_bounds__(NT, REC ? (RPLK == RPL_S ? 2 : 1) : (G <= 4 ? 4 : 3
         nw -= RECALL_WGS;
     }
     const long long n_static = with_static ? (long long)g.n_static * g.B : 0;
-    // kept items in item-major order over (sequence, tidal head); the loop ends after the last
+    // list items in item-major order over (sequence, tidal head); the loop ends after the last
     // item any head has this step (a head with fewer returns at once from the ones past its own)
-    int kmax = 0;
-    for (int b = 0; b < g.B; ++b) kmax = max(kmax, s.counts[b * 2]);
-    const long long n_items = min((long long)g.ng_kept, ((long long)kmax * g.comp_max + TILE_S - 1) / TILE_S);
-    const long long nh = (long long)g.nT * g.B, total = n_static + n_items * nh;
+    // which = 2: the kept list's items, then the new list's
+    long long n_items[2] = {0, 0};
+    for (int lst = 0; lst < 2; ++lst) {
+        if (which != 2 && which != lst) continue;
+        if (s.items) {
+            n_items[lst] = s.items[lst];
+        } else {
+            int kmax = 0;
+            for (int b = 0; b < g.B; ++b) kmax = max(kmax, s.counts[b * 2 + lst]);
+            n_items[lst] = ((long long)kmax * g.comp_max + TILE_S - 1) / TILE_S;
+        }
+        n_items[lst] = min(n_items[lst], (long long)(lst ? g.ng_new : g.ng_kept));
+    }
+    const long long nh = (long long)g.nT * g.B, nk = n_items[0] * nh;
+    const long long total = n_static + nk + n_items[1] * nh;
     for (long long it = w; it < total; it += nw) {
         if (it < n_static) {
             static_tile<G>(g, t, s, q, (int)(it % g.n_static), (int)(it / g.n_static), sm.st);
         } else {
-            const long long i2 = it - n_static, j = i2 / nh, rest = i2 - j * nh;
-            kept_item<G>(g, t, s, q, (int)j, (int)(rest % g.nT), (int)(rest / g.nT), sm.st);
+            const long long i2 = it - n_static, lst = i2 >= nk, i3 = i2 - (lst ? nk : 0), j = i3 / nh, rest = i3 - j * nh;
+            list_item<G>(g, t, s, q, (int)lst, (int)j, (int)(rest % g.nT), (int)(rest / g.nT), sm.st);
         }
     }
 }
@@ -1351,8 +1543,9 @@ __global__ __launch_bounds__(NT, G <= 4 ? 4 : 2) void attention_kernel(Geometry 
         SubsetSmem<G, RPL_S> st;
     };
     __shared__ Smem sm;
-    // one tile per work-group (the hardware's dynamic dispatch balances the slower anchor tiles
-    // against the static ones better than a grid-stride loop: measured 98 vs 107 us)
+    // One tile per work-group (the hardware's dynamic dispatch balances the slower anchor tiles
+    // against the static ones better than a grid-stride loop: measured 98 vs 107 us).
+    if (s.items_clear && blockIdx.x == 0 && threadIdx.x < 2) s.items_clear[threadIdx.x] = 0;
     const long long na = (long long)g.n_tiles_a * g.nA * g.B;
     const long long n = na + (long long)g.n_static * g.B;
     const long long p = blockIdx.x, a0 = p * na / n, a1 = (p + 1) * na / n;
@@ -1411,25 +1604,34 @@ __global__ __launch_bounds__(NT, RPL == RPL_S ? 4 : 2) void new_slots_kernel(Geo
     new_entry<G, RPL>(g, t, s, q, blockIdx.x, blockIdx.y, blockIdx.z, sm);
 }
 
-// Merge of one tidal/fixed KV-head's partials (static tiles, kept groups, new groups):
-// COMBINE_THREADS threads; the partials of every output column are split over groups of
-// threads and summed in a fixed order.
+// Final merge of a step.  Work-groups 0 .. nT + nF - 1: one tidal/fixed KV-head's partials
+// (static tiles, kept items, new items or entries) -> its G output rows; the next nA: one
+// anchor KV-head's tile partials -> its G output rows (anchor_out_merge; the anchors' chunk
+// masses were merged earlier, on the selection's path).  Per 16-byte column of the G * d outputs
+// the partials are split over groups of threads and summed in a fixed order.
 template <int G>
 __global__ __launch_bounds__(COMBINE_THREADS) void subset_combine_kernel(Geometry g, Tiers t, StepBuffers s, void *out)
 {
     const int hi = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+    extern __shared__ double dsm[];      // subset heads: float [np_max][G]; anchors: double [G][n_tiles_a]
+    constexpr int NC4 = G * D / 4, GR = COMBINE_THREADS / NC4, NW = COMBINE_THREADS / 64;
+    __shared__ double opart[GR * NC4 * 4];
+    if (hi >= g.nT + g.nF) {
+        anchor_out_merge<G>(g, t, s, out, hi - g.nT - g.nF, b, dsm, opart);
+        return;
+    }
+    float *sfac = (float *)dsm;
     const bool tidal = hi < g.nT;
-    extern __shared__ float sfac[];      // [np_max][G]
-    constexpr int NW = COMBINE_THREADS / 64;
-    constexpr int OG = COMBINE_THREADS / (G * D) > 0 ? COMBINE_THREADS / (G * D) : 1;   // groups per output
     __shared__ float red[NW * G];
     __shared__ float Linv[G];
-    __shared__ float opart[OG > 1 ? OG : 1][G * D > COMBINE_THREADS ? 1 : G * D];
     const HeadRows hr = t.hr[hi];
     const bool recalls = tidal && hr.cfull > 0;   // no complement at retention 1
     const int nk = recalls ? (int)min(((long long)s.counts[b * 2] * hr.cfull + TILE_S - 1) / TILE_S, (long long)hr.ngk) : 0;
-    // one partial per new entry (same-step timing)
-    const int nn = (recalls && !g.next_step) ? min(s.counts[b * 2 + 1], g.knew) : 0;
+    // new complements: packed items (next-step timing: the previous step's recall) or one
+    // partial per entry (same-step timing)
+    const int nn = !recalls ? 0
+                   : g.next_step ? (int)min(((long long)s.counts[b * 2 + 1] * hr.cfull + TILE_S - 1) / TILE_S, (long long)hr.ngn)
+                                 : min(s.counts[b * 2 + 1], g.knew);
     const int nts = hr.nts, ngk = hr.ngk, nvalid = nts + nk + nn;
     auto part = [&](int j) {
         if (j < nts) return j;
@@ -1439,38 +1641,61 @@ __global__ __launch_bounds__(COMBINE_THREADS) void subset_combine_kernel(Geometr
     };
     const size_t base = (size_t)b * g.P + hr.pbase;
     const int lane = tid & 63, wave = tid >> 6;
+    const int col = tid % NC4, grp = tid / NC4, h = col / (D / 4);
+    const int j0 = grp * nvalid / GR, j1 = grp < GR ? (grp + 1) * nvalid / GR : j0;
+    const float4 *po = (const float4 *)s.ps_o;
+    // the first loads of every phase are issued together (one memory round trip): this
+    // thread's partial maximum and sum, and its first PF output partials
+    constexpr int PF = G <= 4 ? 8 : 4;
+    float4 pf[PF];
+#pragma unroll
+    for (int u = 0; u < PF; ++u)
+        pf[u] = j0 + u < j1 ? po[(base + part(j0 + u)) * NC4 + col] : make_float4(0.f, 0.f, 0.f, 0.f);
+    float m0[G], l0[G];
+#pragma unroll
+    for (int hh = 0; hh < G; ++hh) {
+        m0[hh] = tid < nvalid ? s.ps_m[(base + part(tid)) * G + hh] : -INFINITY;
+        l0[hh] = tid < nvalid ? s.ps_l[(base + part(tid)) * G + hh] : 0.f;
+    }
     float mloc[G];
 #pragma unroll
-    for (int h = 0; h < G; ++h) mloc[h] = -INFINITY;
-    for (int j = tid; j < nvalid; j += COMBINE_THREADS)
+    for (int hh = 0; hh < G; ++hh) mloc[hh] = m0[hh];
+    for (int j = tid + COMBINE_THREADS; j < nvalid; j += COMBINE_THREADS)
 #pragma unroll
-        for (int h = 0; h < G; ++h) mloc[h] = fmaxf(mloc[h], s.ps_m[(base + part(j)) * G + h]);
+        for (int hh = 0; hh < G; ++hh) mloc[hh] = fmaxf(mloc[hh], s.ps_m[(base + part(j)) * G + hh]);
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-        mloc[h] = wave_max(mloc[h]);
-        if (lane == 0) red[wave * G + h] = mloc[h];
+    for (int hh = 0; hh < G; ++hh) {
+        mloc[hh] = wave_max(mloc[hh]);
+        if (lane == 0) red[wave * G + hh] = mloc[hh];
     }
     __syncthreads();
     float M[G], lsum[G];
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-        M[h] = red[h];
-        for (int w = 1; w < NW; ++w) M[h] = fmaxf(M[h], red[w * G + h]);
-        lsum[h] = 0.f;
+    for (int hh = 0; hh < G; ++hh) {
+        M[hh] = red[hh];
+        for (int w = 1; w < NW; ++w) M[hh] = fmaxf(M[hh], red[w * G + hh]);
+        lsum[hh] = 0.f;
     }
     __syncthreads();
-    for (int j = tid; j < nvalid; j += COMBINE_THREADS)
+    if (tid < nvalid)
 #pragma unroll
-        for (int h = 0; h < G; ++h) {
-            const float mj = s.ps_m[(base + part(j)) * G + h];
-            const float f = (M[h] > -INFINITY && mj > -INFINITY) ? __expf(mj - M[h]) : 0.f;
-            sfac[j * G + h] = f;
-            lsum[h] += s.ps_l[(base + part(j)) * G + h] * f;
+        for (int hh = 0; hh < G; ++hh) {
+            const float f = (M[hh] > -INFINITY && m0[hh] > -INFINITY) ? __expf(m0[hh] - M[hh]) : 0.f;
+            sfac[tid * G + hh] = f;
+            lsum[hh] += l0[hh] * f;
+        }
+    for (int j = tid + COMBINE_THREADS; j < nvalid; j += COMBINE_THREADS)
+#pragma unroll
+        for (int hh = 0; hh < G; ++hh) {
+            const float mj = s.ps_m[(base + part(j)) * G + hh];
+            const float f = (M[hh] > -INFINITY && mj > -INFINITY) ? __expf(mj - M[hh]) : 0.f;
+            sfac[j * G + hh] = f;
+            lsum[hh] += s.ps_l[(base + part(j)) * G + hh] * f;
         }
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-        lsum[h] = wave_sum(lsum[h]);
-        if (lane == 0) red[wave * G + h] = lsum[h];
+    for (int hh = 0; hh < G; ++hh) {
+        lsum[hh] = wave_sum(lsum[hh]);
+        if (lane == 0) red[wave * G + hh] = lsum[hh];
     }
     __syncthreads();
     if (tid < G) {
@@ -1479,33 +1704,37 @@ __global__ __launch_bounds__(COMBINE_THREADS) void subset_combine_kernel(Geometr
         Linv[tid] = L > 0.f ? 1.f / L : 0.f;
     }
     __syncthreads();
-    const int lk = tidal ? t.tidal_lk[hi] : t.fixed_lk[hi - g.nT], l = lk / g.Hkv, kv = lk - l * g.Hkv;
-    const size_t ob = (((size_t)b * g.L + l) * g.Hq + (size_t)kv * G) * D;
-    if constexpr (OG > 1) {
-        // threads beyond OG * G * D (when G * D does not divide the block) only join the barrier
-        const int idx = tid % (G * D), grp = tid / (G * D), h = idx / D;
-        const bool act = grp < OG;
-        float acc = 0.f;
-        if (act) {
-            const int j0 = grp * nvalid / OG, j1 = (grp + 1) * nvalid / OG;
-#pragma unroll 8
-            for (int j = j0; j < j1; ++j) acc += s.ps_o[(base + part(j)) * G * D + idx] * sfac[j * G + h];
-            opart[grp][idx] = acc;
-        }
-        __syncthreads();
-        if (grp == 0) {
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    float4 *op = (float4 *)opart;   // [GR][NC4] float4 (the double buffer, reused)
+    if (grp < GR) {
 #pragma unroll
-            for (int q2 = 1; q2 < OG; ++q2) acc += opart[q2][idx];
-            store_out(out, ob + idx, acc * Linv[h], g.out_bf16);
+        for (int u = 0; u < PF; ++u)
+            if (j0 + u < j1) {
+                const float f = sfac[(j0 + u) * G + h];
+                acc.x += pf[u].x * f, acc.y += pf[u].y * f, acc.z += pf[u].z * f, acc.w += pf[u].w * f;
+            }
+#pragma unroll 4
+        for (int j = j0 + PF; j < j1; ++j) {
+            const float4 v = po[(base + part(j)) * NC4 + col];
+            const float f = sfac[j * G + h];
+            acc.x += v.x * f, acc.y += v.y * f, acc.z += v.z * f, acc.w += v.w * f;
         }
-    } else {
-        for (int idx = tid; idx < G * D; idx += COMBINE_THREADS) {
-            const int h = idx / D;
-            float acc = 0.f;
-#pragma unroll 8
-            for (int j = 0; j < nvalid; ++j) acc += s.ps_o[(base + part(j)) * G * D + idx] * sfac[j * G + h];
-            store_out(out, ob + idx, acc * Linv[h], g.out_bf16);
+        op[grp * NC4 + col] = acc;
+    }
+    __syncthreads();
+    if (grp == 0) {
+#pragma unroll 4
+        for (int r = 1; r < GR; ++r) {
+            const float4 o = op[r * NC4 + col];
+            acc.x += o.x, acc.y += o.y, acc.z += o.z, acc.w += o.w;
         }
+        const int lk = tidal ? t.tidal_lk[hi] : t.fixed_lk[hi - g.nT], l = lk / g.Hkv, kv = lk - l * g.Hkv;
+        const size_t ob = (((size_t)b * g.L + l) * g.Hq + (size_t)kv * G) * D + (size_t)col * 4;
+        const float li = Linv[h];
+        store_out(out, ob, acc.x * li, g.out_bf16);
+        store_out(out, ob + 1, acc.y * li, g.out_bf16);
+        store_out(out, ob + 2, acc.z * li, g.out_bf16);
+        store_out(out, ob + 3, acc.w * li, g.out_bf16);
     }
 }
 
@@ -1590,12 +1819,12 @@ struct AnchorL {
     }
 };
 template <int G>
-struct AnchorCombineL {
-    static hipError_t run(const Geometry &g, const Tiers &t, const StepBuffers &s, void *out, hipStream_t st)
+struct AnchorMassL {
+    static hipError_t run(const Geometry &g, const StepBuffers &s, hipStream_t st)
     {
         if (g.nA == 0) return hipSuccess;
-        const size_t shm = (size_t)g.n_tiles_a * sizeof(double);
-        hipLaunchKernelGGL(anchor_combine_kernel<G>, dim3(g.nA, G, g.B), dim3(COMBINE_THREADS), shm, st, g, t, s, out);
+        const size_t shm = (size_t)G * g.n_tiles_a * sizeof(double);
+        hipLaunchKernelGGL(anchor_mass_kernel<G>, dim3(g.nA, g.B), dim3(MASS_THREADS), shm, st, g, s);
         return hipGetLastError();
     }
 };
@@ -1618,10 +1847,12 @@ long long resident_grid(K kernel, std::atomic<int> &cache, const Geometry &g, lo
 template <int G>
 struct TidalFixedL {
     static hipError_t run(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, bool recall,
-                          bool with_static, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
+                          bool with_static, int which, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
     {
         recall = recall && g.nT > 0 && g.k > 0 && g.comp_max > 0;
-        const long long tiles = (with_static ? (long long)g.n_static * g.B : 0) + (long long)g.ng_kept * g.nT * g.B;
+        const long long tiles = (with_static ? (long long)g.n_static * g.B : 0) +
+                                (long long)(which == 0 ? g.ng_kept : which == 1 ? g.ng_new : g.ng_kept + g.ng_new) *
+                                    g.nT * g.B;
         if (tiles == 0 && !recall) return record_pair(e0, e1, st);
         const dim3 block(NT);
         const int ws = with_static ? 1 : 0;
@@ -1629,15 +1860,15 @@ struct TidalFixedL {
         if (!recall) {
             auto k = tidal_fixed_kernel<G, RPL_S, false>;
             const dim3 grid((unsigned)resident_grid(k, occ[0], g, tiles));
-            hipExtLaunchKernelGGL(k, grid, block, 0, st, e0, e1, 0, g, t, s, q, ws);
+            hipExtLaunchKernelGGL(k, grid, block, 0, st, e0, e1, 0, g, t, s, q, ws, which);
         } else if (g.slot_tile == TILE_S) {
             auto k = tidal_fixed_kernel<G, RPL_S, true>;
             const dim3 grid((unsigned)(RECALL_WGS + std::max(1LL, resident_grid(k, occ[1], g, tiles))));
-            hipExtLaunchKernelGGL(k, grid, block, 0, st, e0, e1, 0, g, t, s, q, ws);
+            hipExtLaunchKernelGGL(k, grid, block, 0, st, e0, e1, 0, g, t, s, q, ws, which);
         } else {
             auto k = tidal_fixed_kernel<G, 2 * RPL_S, true>;
             const dim3 grid((unsigned)(RECALL_WGS + std::max(1LL, resident_grid(k, occ[2], g, tiles))));
-            hipExtLaunchKernelGGL(k, grid, block, 0, st, e0, e1, 0, g, t, s, q, ws);
+            hipExtLaunchKernelGGL(k, grid, block, 0, st, e0, e1, 0, g, t, s, q, ws, which);
         }
         return hipGetLastError();
     }
@@ -1649,6 +1880,7 @@ struct AttentionL {
     {
         const long long n = (long long)g.n_tiles_a * g.nA * g.B + (long long)g.n_static * g.B;
         if (n == 0) return record_pair(e0, e1, st);
+        if (n > INT32_MAX) return hipErrorInvalidValue;
         hipExtLaunchKernelGGL(attention_kernel<G>, dim3((unsigned)n), dim3(NT), 0, st, e0, e1, 0, g, t, s, q);
         return hipGetLastError();
     }
@@ -1669,9 +1901,11 @@ template <int G>
 struct CombineL {
     static hipError_t run(const Geometry &g, const Tiers &t, const StepBuffers &s, void *out, hipStream_t st)
     {
-        if (g.nT + g.nF == 0) return hipSuccess;
-        const size_t shm = (size_t)(g.np_max ? g.np_max : 1) * G * sizeof(float);
-        hipLaunchKernelGGL(subset_combine_kernel<G>, dim3(g.nT + g.nF, g.B), dim3(COMBINE_THREADS), shm, st, g, t, s, out);
+        if (g.nT + g.nF + g.nA == 0) return hipSuccess;
+        const size_t shm = std::max((size_t)(g.np_max ? g.np_max : 1) * G * sizeof(float),
+                                    (size_t)G * g.n_tiles_a * sizeof(double));
+        hipLaunchKernelGGL(subset_combine_kernel<G>, dim3(g.nT + g.nF + g.nA, g.B), dim3(COMBINE_THREADS), shm, st, g, t, s,
+                           out);
         return hipGetLastError();
     }
 };
@@ -1684,9 +1918,9 @@ hipError_t launch_anchor(const Geometry &g, const Tiers &t, const StepBuffers &s
     return dispatch_g<AnchorL>(g.G, g, t, s, q, st, e0, e1);
 }
 
-hipError_t launch_anchor_combine(const Geometry &g, const Tiers &t, const StepBuffers &s, void *out, hipStream_t st)
+hipError_t launch_anchor_mass(const Geometry &g, const StepBuffers &s, hipStream_t st)
 {
-    return dispatch_g<AnchorCombineL>(g.G, g, t, s, out, st);
+    return dispatch_g<AnchorMassL>(g.G, g, s, st);
 }
 
 hipError_t launch_select(const Geometry &g, const StepBuffers &s, float *scores, const int32_t *ovr,
@@ -1698,9 +1932,9 @@ hipError_t launch_select(const Geometry &g, const StepBuffers &s, float *scores,
 }
 
 hipError_t launch_tidal_fixed(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, bool recall,
-                              bool with_static, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
+                              bool with_static, int which, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
 {
-    return dispatch_g<TidalFixedL>(g.G, g, t, s, q, recall, with_static, st, e0, e1);
+    return dispatch_g<TidalFixedL>(g.G, g, t, s, q, recall, with_static, which, st, e0, e1);
 }
 
 hipError_t launch_attention(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st,

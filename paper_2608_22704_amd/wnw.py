@@ -25,7 +25,7 @@ EXPORTS = ("wnw_init_cache", "wnw_set_retention", "wnw_set_roles", "wnw_prefill_
            "wnw_append_kv", "wnw_decode_step", "wnw_query_geometry",
            "wnw_query_segments", "wnw_query_head_keep", "wnw_get_stats",
            "wnw_set_selection_override", "wnw_debug_read_slot", "wnw_debug_read_host_chunk",
-           "wnw_debug_set_slot_offset_limit",
+           "wnw_debug_set_slot_offset_limit", "wnw_debug_set_recall_delay",
            "wnw_debug_read_resident", "wnw_last_error", "wnw_destroy", "wnw_voice_hits", "wnw_key_sensitivity",
            "wnw_triage", "wnw_triage_last_error")
 
@@ -46,7 +46,7 @@ class wnw_stats(C.Structure):
                 ("timed_steps", C.c_int64), ("t_anchor_ms", C.c_double), ("t_select_ms", C.c_double),
                 ("t_tidal_fixed_ms", C.c_double), ("t_new_ms", C.c_double), ("t_combine_ms", C.c_double),
                 ("t_step_ms", C.c_double), ("t_recall_ms", C.c_double), ("slot_exhausted", C.c_int64),
-                ("t_host_wait_ms", C.c_double), ("t_recall_wait_ms", C.c_double)]
+                ("t_host_wait_ms", C.c_double), ("t_recall_wait_ms", C.c_double), ("kept_rows", C.c_int64)]
 
     def as_dict(self) -> dict:
         return {name: getattr(self, name) for name, _ in self._fields_}
@@ -85,6 +85,7 @@ def _load():
         "wnw_debug_read_host_chunk": ([P, I32, I32, P, SZ], C.c_int),
         "wnw_debug_read_resident": ([P, P], C.c_int),
         "wnw_debug_set_slot_offset_limit": ([P, I64], C.c_int),
+        "wnw_debug_set_recall_delay": ([P, I32], C.c_int),
         "wnw_last_error": ([P], C.c_char_p),
         "wnw_destroy": ([P], None),
     }
@@ -304,6 +305,10 @@ def wnw_set_selection_override(ctx, sel_dev):
 
 def wnw_debug_set_slot_offset_limit(ctx, nbytes: int):
     _check(lib.wnw_debug_set_slot_offset_limit(ctx, nbytes), ctx)
+
+
+def wnw_debug_set_recall_delay(ctx, us: int):
+    _check(lib.wnw_debug_set_recall_delay(ctx, us), ctx)
 
 
 def wnw_debug_read_slot(ctx, b: int, chunk: int, host_dst, nbytes: int):

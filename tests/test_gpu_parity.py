@@ -958,3 +958,53 @@ def test_feature_combinations(combo):
     if combo.get("importance"):
         kw.update(importance=_imp(w, 701, ((0, 1),), ((1, 3),)), lam=0.9)
     _run(w, **kw)
+
+
+# ---- stream ordering of the recall: every reader of a recalled slot waits for the recall ------
+
+@pytest.mark.parametrize("mode", ["next_memcpy", "next_kernel", "same_memcpy"])
+def test_delayed_recall_gives_identical_results(mode):
+    """Each recall delayed by 3 ms (the host waits before issuing the copies and a host function
+    sleeps ahead of them on every copy stream; ahead of the copy kernel without copy engines):
+    twelve steps enqueued back to back with no host synchronisation between them (outputs, scores
+    and selections copied on the caller's stream after each step) are bit-identical to an
+    undelayed run.  With next-step timing and copy engines the copies are issued by the library's
+    recall thread while the caller keeps enqueueing steps."""
+    import torch
+    from paper_2608_22704_amd import wnw as W
+    from tests.wnw_harness import log, to_dev
+    flags = {"next_memcpy": W.WNW_F_SELECT_NEXT_STEP | W.WNW_F_RECALL_MEMCPY,
+             "next_kernel": W.WNW_F_SELECT_NEXT_STEP, "same_memcpy": W.WNW_F_RECALL_MEMCPY}[mode]
+    w = _small("recall_delay", 180, L=2, Hq=8, Hkv=4, Ta=480, Tt=5, cl=16, budget=2000, steps=12)
+    log(f"[case] delayed recall, {mode}")
+    B, L, H, T, D = w.batch, w.layers, w.kv_heads, w.total_len, w.head_dim
+    seqs = [gen.sequence(w, b) for b in range(B)]
+    kd = torch.stack([to_dev(sq["k"]) for sq in seqs])
+    vd = torch.stack([to_dev(sq["v"]) for sq in seqs])
+    qd = torch.stack([to_dev(np.stack([sq["q"][s] for sq in seqs])) for s in range(w.steps)])
+    prefill = np.stack([sq["prefill"] for sq in seqs])
+    runs = []
+    for delay in (0, 3000):
+        cfg = W.make_config(B, L, w.q_heads, H, w.audio_len, w.text_len, w.chunk_len, w.budget_bp, flags=flags)
+        ctx = W.wnw_init_cache(cfg, kd, vd)
+        try:
+            W.wnw_set_roles(ctx, gen.roles(w), prefill)
+            W.wnw_debug_set_recall_delay(ctx, delay)
+            geo = W.wnw_query_geometry(ctx)
+            out = torch.empty((B, L, w.q_heads, D), dtype=torch.float32, device="cuda")
+            sc = torch.empty((B, geo["n_chunks"]), dtype=torch.float32, device="cuda")
+            sel = torch.empty((B, geo["k"]), dtype=torch.int32, device="cuda")
+            kept = []
+            for s in range(w.steps):
+                W.wnw_decode_step(ctx, qd[s], out, sc, sel)
+                kept.append((out.clone(), sc.clone(), sel.clone()))
+            torch.cuda.synchronize()
+            st = W.wnw_get_stats(ctx)
+            assert st["recalled_chunks"] > 0
+            runs.append([[x.cpu().numpy() for x in step] for step in kept])
+        finally:
+            W.wnw_destroy(ctx)
+    for s, (a, b) in enumerate(zip(*runs)):
+        for x, y in zip(a, b):
+            assert np.array_equal(x.view(np.uint32) if x.dtype == np.float32 else x,
+                                  y.view(np.uint32) if y.dtype == np.float32 else y), f"step {s} differs"
