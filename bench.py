@@ -186,7 +186,7 @@ def run_timing(W, torch, w, timing, recall, kd, vd, qd, roles, prefill, args, ch
         res["kernels"] = {
             first: {"avg_ms": a_ms, "bytes": first_bytes, "GBps": first_bytes / a_ms / 1e6},
             first + "_pinned_selection": {"avg_ms": a2_ms, "bytes": first2_bytes, "GBps": first2_bytes / a2_ms / 1e6},
-            "merge_select": {"avg_ms": d["t_select_ms"] / n},
+            "mass_select": {"avg_ms": d["t_select_ms"] / n},
             "recall_wait": {"avg_ms": d["t_recall_wait_ms"] / n},
             "tidal_fixed": {"avg_ms": tf_ms, "bytes": tf_bytes, "GBps": tf_bytes / tf_ms / 1e6 if tf_ms > 0 else None},
             "tidal_fixed_pinned_selection": {"avg_ms": tf2_ms, "bytes": tf2_bytes,
