@@ -97,12 +97,12 @@ struct wnw_ctx {
     // which are joined back into `side` (one stream queues copies with a gap between them)
     hipStream_t copy_st[N_COPY_STREAMS - 1] = {};
     // by step parity: the end of each copy stream's share of that step's host-issued recall, and
-    // the end of that step's select kernel
+    // the end of that step's select kernel (next-step timing with the copy kernel)
     hipEvent_t ev_copy[2][N_COPY_STREAMS] = {};
     hipEvent_t ev_sel[2] = {}, ev_rec = nullptr;
     bool rec_pending = false;          // next-step timing: a recall issued on `side` not yet joined
-    int32_t *h_newinfo = nullptr;      // pinned, two mirrors by step parity: counts [B][2] then new
-                                       // lists [B][knew][2]
+    int32_t *h_newinfo = nullptr;      // pinned, two mirrors by step parity: counts [B][2], new
+                                       // lists [B][knew][2], publication tags [B]
     int32_t *d_newinfo = nullptr;      // the same memory as the device addresses it
     size_t mirror_ints = 0;            // int32 entries of one mirror
     unsigned copy_mask[2] = {0, 0};    // by step parity: copy streams that received a copy
@@ -113,6 +113,7 @@ struct wnw_ctx {
     // the previous step's copies to be issued before it enqueues the launch that reads them.
     struct RecallJob {
         int64_t step;
+        hipStream_t stream;            // the caller's stream of the step
         bool timed;
         hipEvent_t r0, rc[N_COPY_STREAMS];
     };
@@ -228,7 +229,7 @@ wnw_status dalloc(wnw_ctx *c, T **p, size_t n, const char *what)
 
 // Pinned host memory (hipHostMalloc).  WNW_TEST_PINNED_LIMIT=<bytes> makes every request above
 // that size fail as if the host were out of pinned memory (a test hook for the failure path).
-wnw_status palloc(wnw_ctx *c, void **p, size_t bytes, const char *what)
+wnw_status palloc(wnw_ctx *c, void **p, size_t bytes, const char *what, unsigned flags = hipHostMallocDefault)
 {
     *p = nullptr;
     if (const char *lim = std::getenv("WNW_TEST_PINNED_LIMIT")) {
@@ -236,7 +237,7 @@ wnw_status palloc(wnw_ctx *c, void **p, size_t bytes, const char *what)
         if (cap >= 0 && bytes > (size_t)cap)
             return fail(c, WNW_ERR_OOM, "pinned %s of %zu bytes: above WNW_TEST_PINNED_LIMIT (%lld)", what, bytes, cap);
     }
-    hipError_t e = hipHostMalloc(p, bytes, hipHostMallocDefault);
+    hipError_t e = hipHostMalloc(p, bytes, flags);
     if (e != hipSuccess) {
         (void)hipGetLastError();
         *p = nullptr;
@@ -407,7 +408,9 @@ wnw_status plan_comp(wnw_ctx *c, const uint8_t *flags)
         HeadRows &h = c->hrows[hi];
         if (h.cfull > 0) {
             h.ngk = (int)(((int64_t)kept_max * h.cfull + TILE_S - 1) / TILE_S);
-            h.ngn = (int)std::max<int64_t>(g.knew, ((int64_t)g.knew * h.cfull + TILE_S - 1) / TILE_S);
+            // next-step timing: the new segments join the kept list (no partials of their own);
+            // same-step timing: one partial per new entry, or TILE_S-row pieces
+            h.ngn = g.next_step ? 0 : (int)std::max<int64_t>(g.knew, ((int64_t)g.knew * h.cfull + TILE_S - 1) / TILE_S);
         }
         g.ng_kept = std::max(g.ng_kept, h.ngk);
         g.ng_new = std::max(g.ng_new, h.ngn);
@@ -493,12 +496,40 @@ void parallel_for(int n, const std::function<void(int)> &fn)
 
 // Waits on the host for an event by polling it: a sleeping wait wakes tens to hundreds of
 // microseconds late, and with host-issued copies the link idles for that long.
-hipError_t poll_event(hipEvent_t e)
+// Tag the select kernel of `step` publishes with the mirror (nonzero; steps two apart, which
+// share a mirror, differ).
+int32_t pub_tag(int64_t step)
 {
-    hipError_t r;
-    while ((r = hipEventQuery(e)) == hipErrorNotReady) {
+    return (int32_t)(step % 0x7ffffffe) + 1;
+}
+
+// Waits (busy polling: a sleeping wait wakes tens to hundreds of microseconds late) until the
+// select kernel of `step`, enqueued on `st`, has published the mirror of parity step & 1 for
+// every sequence.  Every millisecond it also asks whether `st` has failed, or has completed
+// without the tags (which would be a defect): either is returned as an error.
+hipError_t wait_published(const wnw_ctx *c, int64_t step, hipStream_t st)
+{
+    const int B = c->g.B;
+    const int32_t *tags = c->h_newinfo + (step & 1) * c->mirror_ints + B * 2 + (size_t)B * c->g.knew * 2;
+    const int32_t want = pub_tag(step);
+    auto published = [&] {
+        for (int b = 0; b < B; ++b)
+            if (__atomic_load_n(tags + b, __ATOMIC_ACQUIRE) != want) return false;
+        return true;
+    };
+    auto next_check = std::chrono::steady_clock::now() + std::chrono::milliseconds(1);
+    bool drained = false;
+    for (;;) {
+        for (int i = 0; i < 256; ++i)
+            if (published()) return hipSuccess;
+        const auto now = std::chrono::steady_clock::now();
+        if (now < next_check) continue;
+        if (drained) return hipErrorUnknown;   // the stream completed 1 ms ago, no tag since
+        const hipError_t e = hipStreamQuery(st);
+        if (e != hipSuccess && e != hipErrorNotReady) return e;
+        drained = e == hipSuccess;
+        next_check = now + std::chrono::milliseconds(1);
     }
-    return r;
 }
 
 // Test hook: a host function that sleeps `us` microseconds, queued ahead of a recall on its
@@ -597,11 +628,9 @@ void recall_thread(wnw_ctx *c)
         const char *what = "";
         if (c->rerr == hipSuccess) {
             const auto w0 = std::chrono::steady_clock::now();
-            // a sleeping wait wakes tens to hundreds of microseconds late: poll
-            while ((e = hipEventQuery(c->ev_sel[par])) == hipErrorNotReady) {
-            }
+            e = wait_published(c, job.step, job.stream);
             const double waited = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - w0).count();
-            if (e != hipSuccess) what = "hipEventQuery of a selection";
+            if (e != hipSuccess) what = "the wait for a selection";
             if (e == hipSuccess && c->delay_us > 0) std::this_thread::sleep_for(std::chrono::microseconds(c->delay_us));
             if (e == hipSuccess && job.timed) {
                 e = hipEventRecord(job.r0, c->side);
@@ -876,10 +905,13 @@ wnw_status build_tiers(wnw_ctx *c, const uint8_t *keep_all)
         HIPCHECK(c, hipHostGetDevicePointer(&dp, c->host_comp, 0));
         c->t.host_comp = (const uint16_t *)dp;
     }
-    c->mirror_ints = B * 2 + B * g.knew * 2 + 1;
-    if ((r = palloc(c, (void **)&c->h_newinfo, 2 * c->mirror_ints * sizeof(int32_t), "recall lists")) != WNW_OK)
+    // coherent: the select kernel's stores reach host memory without a cache write-back
+    c->mirror_ints = B * 2 + B * g.knew * 2 + B;
+    if ((r = palloc(c, (void **)&c->h_newinfo, 2 * c->mirror_ints * sizeof(int32_t), "recall lists",
+                    hipHostMallocCoherent)) != WNW_OK)
         return r;
     {
+        memset(c->h_newinfo, 0, 2 * c->mirror_ints * sizeof(int32_t));   // no tag published yet
         void *dp = nullptr;
         HIPCHECK(c, hipHostGetDevicePointer(&dp, c->h_newinfo, 0));
         c->d_newinfo = (int32_t *)dp;
@@ -1245,12 +1277,12 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, void *out, float *scor
     // Lists (kept, new, their counts and item counts) alternate between two buffers by step.
     // Same-step timing: the select kernel of step s fills buffer s & 1 and step s reads it.
     // Next-step timing: the select kernel of step s fills buffer (s + 1) & 1 for step s + 1, and
-    // step s reads buffer s & 1, filled by step s - 1: its tidal launch streams the kept list's
-    // complements (on the device before step s - 1's recall) and the new list's (the complements
-    // step s - 1 recalled, once their copies have landed).  Neither select kernel ever rewrites
-    // a list a launch or a recall still reads.  (The kept complements could join the attention
-    // launch, which runs before the wait for the copies; measured, that launch then streams
-    // slower than the two launches apart.)
+    // step s reads buffer s & 1, filled by step s - 1: its tidal launch streams the kept list,
+    // which then holds every resident complement (those on the device before step s - 1's
+    // recall, then those step s - 1 recalled, once their copies have landed).  Neither select
+    // kernel ever rewrites a list a launch or a recall still reads.  (The complements already
+    // on the device could join the attention launch, which runs before the wait for the copies;
+    // measured, that launch then streams slower than the two launches apart.)
     const int par = (int)(c->steps & 1), nxt = (int)((c->steps + 1) & 1);
     auto lists_of = [&](StepBuffers b, int i) {
         b.counts += (size_t)i * g.B * 2;
@@ -1265,8 +1297,7 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, void *out, float *scor
     if (g.next_step) sb.items_clear = sn.items;                   // zeroed before the select kernel
 
     // (1) anchor attention + chunk mass, (2) scores, top-k and residency.  With next-step
-    // timing the static tidal/fixed tiles (kept rows + text) and the kept list's complements
-    // join the anchor launch.
+    // timing the static tidal/fixed tiles (kept rows + text) join the anchor launch.
     // markers 0 and 1 are the first launch's own start and end (its dispatch excluded)
     hipEvent_t e0 = timing ? ev.e[0] : nullptr, e1 = timing ? ev.e[1] : nullptr;
     if (g.next_step)
@@ -1276,12 +1307,15 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, void *out, float *scor
     HIPCHECK(c, launch_anchor_mass(g, sb, s0));
     const bool memcpy_path = c->cfg.flags & WNW_F_RECALL_MEMCPY;
     // host-issued copies: the select kernel also writes the counts and new lists to mapped pinned
-    // memory (one mirror per step parity), so the host reads them once the selection is done,
-    // never behind copies still running on the side streams
+    // memory (one mirror per step parity) and then publishes a tag there, so the host reads them
+    // once the selection is done, never behind copies still running on the side streams
     sn.pub = memcpy_path ? c->d_newinfo + (size_t)par * c->mirror_ints : nullptr;
+    sn.pub_tag = pub_tag(c->steps);
     HIPCHECK(c, launch_select(g, sn, sc, c->override_sel, sel, s0));
     MARK(6);
-    HIPCHECK(c, hipEventRecord(c->ev_sel[par], s0));
+    // the copy kernel of the next-step recall follows the selection on the device (an event; the
+    // host-issued copies follow the published tag instead)
+    if (g.next_step && !memcpy_path) HIPCHECK(c, hipEventRecord(c->ev_sel[par], s0));
     bool combined = false;
     if (g.next_step) {
         // Next-step timing: the chunks that became resident now are copied on the side stream
@@ -1307,7 +1341,7 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, void *out, float *scor
             }
         }
         // markers 2 and 3: the launch's own start and end
-        HIPCHECK(c, launch_tidal_fixed(g, c->t, sb, q, false, false, 2, s0, timing ? ev.e[2] : nullptr,
+        HIPCHECK(c, launch_tidal_fixed(g, c->t, sb, q, false, false, s0, timing ? ev.e[2] : nullptr,
                                        timing ? ev.e[3] : nullptr));
         // the final merge is queued before the host waits for the selection below, so that the
         // device never idles behind that wait
@@ -1317,7 +1351,7 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, void *out, float *scor
         if (memcpy_path) {
             // the recall thread issues this step's copies once its selection is done; the copy
             // engines queue them behind the previous step's copies, so the link stays busy
-            wnw_ctx::RecallJob job{(int64_t)c->steps, timing, timing ? ev.r[0] : nullptr, {}};
+            wnw_ctx::RecallJob job{(int64_t)c->steps, s0, timing, timing ? ev.r[0] : nullptr, {}};
             if (timing)
                 for (int i = 0; i < N_COPY_STREAMS; ++i) job.rc[i] = ev.rc[i];
             ev.split = timing;
@@ -1340,21 +1374,21 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, void *out, float *scor
         // this step's select kernel; every kernel that could still read them (the previous
         // step's) precedes it on this stream.
         if (timing) HIPCHECK(c, hipEventRecord(ev.r[0], s0));
-        HIPCHECK(c, launch_tidal_fixed(g, c->t, sb, q, true, true, 0, s0));
+        HIPCHECK(c, launch_tidal_fixed(g, c->t, sb, q, true, true, s0));
         if (timing) HIPCHECK(c, hipEventRecord(ev.r[1], s0));
         MARK(3);
     } else {
         MARK(2);
         // (4a) device-resident rows while the host waits for the selection and issues the copies
-        HIPCHECK(c, launch_tidal_fixed(g, c->t, sb, q, false, true, 0, s0));
+        HIPCHECK(c, launch_tidal_fixed(g, c->t, sb, q, false, true, s0));
         MARK(3);
         // (3) copies on the side stream.  The target slots were freed by this step's select
-        // kernel, which follows every earlier reader on s0; the copies start after ev_sel.
-        HIPCHECK(c, hipStreamWaitEvent(c->side, c->ev_sel[par], 0));
-        if (timing) HIPCHECK(c, hipEventRecord(ev.r[0], c->side));
+        // kernel, which follows every earlier reader on s0: once it has published its tag, no
+        // reader of them is left and the copies need no device-side wait.
         const auto w0 = std::chrono::steady_clock::now();
-        HIPCHECK(c, poll_event(c->ev_sel[par]));
+        HIPCHECK(c, wait_published(c, (int64_t)c->steps, s0));
         c->host_wait_ms += std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - w0).count();
+        if (timing) HIPCHECK(c, hipEventRecord(ev.r[0], c->side));
         wnw_status r = check_exhaustion(c);
         if (r != WNW_OK) return r;
         r = issue_copies(c, par, c->side);

@@ -46,7 +46,7 @@ struct Geometry {
     int ng_kept;                // kept items (TILE_S rows of resident complements) of the head with
                                 // the most
     int ng_new;                 // partial entries for newly resident complements of the head with
-                                // the most (packed items or one per entry)
+                                // the most (same-step timing: one per entry or TILE_S-row pieces)
     int n_cu;                   // compute units of the device (grid-stride launches)
     int64_t chunk_elems;        // bf16 elements of one segment's complement block (blk_rows * D)
     int64_t slot_off_max;       // slot regions below this many bytes use buffer offsets
@@ -55,7 +55,7 @@ struct Geometry {
 
 // Rows of one non-anchor head (tidal heads 0..nT-1, then fixed heads), whose audio retention
 // may differ from head to head (Eq. 1).  Partials of a head: its static tiles, then (tidal) its
-// kept groups, then one per newly resident segment.
+// kept-list items, then (same-step timing) one per newly resident segment.
 struct HeadRows {
     int srow;    // first row of the head in its sequence's static tier (tidal or fixed)
     int rs;      // static rows at set-up: kept audio rows (ascending) + text rows; appended tokens
@@ -66,9 +66,10 @@ struct HeadRows {
     // tidal heads (0 for fixed heads)
     int cfull;   // block stride: the head's largest complement of one segment over the batch
     int coff;    // first row of the head in a segment's complement block: cfull K rows, cfull V rows
-    int ngk;     // kept items: TILE_S-row pieces of the head's resident complements at most
-    int ngn;     // partials for newly resident complements: TILE_S-row pieces (next-step timing)
-                 // or one per entry (same-step timing), whichever is more
+    int ngk;     // kept items: TILE_S-row pieces of the head's listed complements at most
+    int ngn;     // same-step timing: partials for newly resident complements, one per entry or
+                 // TILE_S-row pieces, whichever is more (next-step timing: 0, the kept list holds
+                 // them)
     int kfull;   // kept positions of a full segment (set-up)
     int klast;   // kept positions of the last segment (set-up)
 };
@@ -120,14 +121,17 @@ struct StepBuffers {
     // segments to recall.
     int32_t *kept_list;         // [B][n_slots][2] (segment, slot | full-stride bit 30)
     int32_t *new_list;          // [B][knew][2]    (segment, slot)
-    int32_t *counts;            // [B][2] kept, new
-    int32_t *items;             // [2] most kept / new items (TILE_S-row pieces of one head's listed
+    int32_t *counts;            // [B][2] kept-list entries (next-step timing: kept + new), new
+    int32_t *items;             // [2] most kept items, unused (TILE_S-row pieces of one head's listed
                                 // complements) over the sequences: written by the select kernel
                                 // (next-step timing), read by the next step's launches; else null
     int32_t *items_clear;       // [2] the other step's items, zeroed by the attention launch for the
                                 // select kernel that follows it; else null
-    int32_t *pub;               // host-issued recall: mapped pinned mirror of counts [B][2] and new
-                                // lists [B][knew][2], written by the select kernel; else null
+    int32_t *pub;               // host-issued recall: mapped pinned mirror of counts [B][2], new
+                                // lists [B][knew][2] and publication tags [B], written by the select
+                                // kernel; else null
+    int32_t pub_tag;            // the tag the select kernel stores for each sequence once that
+                                // sequence's mirror is visible to the host (nonzero, new each step)
     unsigned long long *stats;  // [8] recalled, dropped, resident, slot_rows, peak, exhausted, revived,
                                 // kept-list rows
     int32_t *exhausted;         // mapped pinned flag, set to 1 by a step that found no free slot for a
@@ -155,11 +159,9 @@ inline size_t select_shared_bytes(const Geometry &g)
 // slots; with `recall`
 // (same-step timing), also the copy of the complements listed for recall from mapped pinned
 // memory into their slots and the attention over them.
-// `which`: 0 the kept list's items (after the static tiles when with_static), 1 the new list's
-// items (next-step timing: the complements the previous step copied), 2 both.
+// The slot tiles are the kept list's items (after the static tiles when with_static).
 hipError_t launch_tidal_fixed(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, bool recall,
-                              bool with_static, int which, hipStream_t st, hipEvent_t e0 = nullptr,
-                              hipEvent_t e1 = nullptr);
+                              bool with_static, hipStream_t st, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 // Anchor attention + chunk mass together with the static tidal/fixed tiles (next-step timing).
 hipError_t launch_attention(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st,
                             hipEvent_t e0, hipEvent_t e1);

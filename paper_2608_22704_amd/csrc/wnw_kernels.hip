@@ -694,9 +694,9 @@ __device__ int block_scan_excl(int *a, int n, int *wsum)
 //            bytes still sit in a free slot (never overwritten since) takes it back with no copy;
 //            the others take free slots in least-recently-freed order (never-used slots first)
 //            and are listed for recall
-//   lists    kept list = attended this step with bytes already on the device; new list = to
-//            recall (attended in the same launch with same-step timing, from the next step on
-//            with next-step timing)
+//   lists    kept list = attended with bytes already on the device; new list = to recall
+//            (attended in the same launch with same-step timing; with next-step timing the new
+//            segments also follow the kept ones in the kept list, which the next step attends)
 __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuffers s, float *__restrict__ scores,
                                                              const int32_t *__restrict__ ovr, int32_t *__restrict__ selected)
 {
@@ -867,6 +867,28 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
         for (int i = nsel + tid; i < k; i += nthr) selected[(size_t)b * k + i] = -1;
     }
 
+    // kept list: the resident segments whose bytes are on the device already (kept from the
+    // previous step or revived), attended by this step (same-step timing) or by the next one.
+    // With next-step timing the new list's segments follow them in the same list (below): the
+    // step that reads the list finds them copied, and each tidal head streams one run of rows.
+    // Bit 30 of an entry's slot: every tidal head's complement of the segment has its full
+    // stride of rows (the tiles then skip the per-head row count).
+    lds_barrier();   // rank is rewritten
+    for (int u = tid; u < nu; u += nthr) rank[u] = fkept[u];
+    lds_barrier();
+    const int nkept = block_scan_excl(rank, nu, wsum);
+    int32_t *kl = s.kept_list + (size_t)b * ns * 2;
+    int c_krows = 0;
+    for (int u = tid; u < nu; u += nthr)
+        if (fkept[u]) {
+            const int rows = srows[u];
+            kl[rank[u] * 2] = u;
+            kl[rank[u] * 2 + 1] = sof[u] | (rows * 2 == g.blk_rows ? 1 << 30 : 0);
+            c_krows += rows;
+        }
+    c_krows = wave_sum(c_krows);
+    if ((tid & 63) == 0 && c_krows) atomicAdd(&nkrows, c_krows);
+
     // free slots ordered by (holds data, freed at step, slot id): never-used first, then the
     // least recently freed.  Key: -1 for slots not free, else (holds data) * 2^30 + freed-at step.
     for (int i0 = 0; i0 < ns; i0 += nthr) {
@@ -916,33 +938,17 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
             sdata[slot] = u;
             nl[rank[u] * 2] = u;
             nl[rank[u] * 2 + 1] = slot;
+            if (nxt) {
+                kl[(nkept + rank[u]) * 2] = u;
+                kl[(nkept + rank[u]) * 2 + 1] = slot | (srows[u] * 2 == g.blk_rows ? 1 << 30 : 0);
+            }
             if (s.pub) {
-                // the host reads this mirror once the step's selection event has completed
+                // the host reads this mirror once the sequence's tag is published (below)
                 int32_t *hl = s.pub + g.B * 2 + (size_t)b * g.knew * 2;
                 hl[rank[u] * 2] = u;
                 hl[rank[u] * 2 + 1] = slot;
             }
         }
-    // kept list: the resident segments whose bytes are on the device already (kept from the
-    // previous step or revived), attended by this step (same-step timing) or by the next one
-    // (next-step timing, which also attends the new list's segments once they are copied).
-    // Bit 30 of an entry's slot: every tidal head's complement of the segment has its full
-    // stride of rows (the tiles then skip the per-head row count).
-    for (int u = tid; u < nu; u += nthr) rank[u] = fkept[u];
-    lds_barrier();
-    const int nkept = block_scan_excl(rank, nu, wsum);
-    int32_t *kl = s.kept_list + (size_t)b * ns * 2;
-    int c_krows = 0;
-    for (int u = tid; u < nu; u += nthr)
-        if (fkept[u]) {
-            const int rows = srows[u];
-            kl[rank[u] * 2] = u;
-            kl[rank[u] * 2 + 1] = sof[u] | (rows * 2 == g.blk_rows ? 1 << 30 : 0);
-            c_krows += rows;
-        }
-    c_krows = wave_sum(c_krows);
-    if ((tid & 63) == 0 && c_krows) atomicAdd(&nkrows, c_krows);
-    lds_barrier();
     for (int u = tid; u < nu; u += nthr)
         if (fdrop[u]) sof[u] = -1;
     lds_barrier();
@@ -960,17 +966,17 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
     }
     if (tid == 0) {
         const int nn = min(nnew, min(nfree, g.knew));
-        s.counts[b * 2] = nkept;
+        const int nlist = nxt ? nkept + nn : nkept;   // entries of the kept list
+        s.counts[b * 2] = nlist;
         s.counts[b * 2 + 1] = nn;
         if (s.pub) {
-            s.pub[b * 2] = nkept;
+            s.pub[b * 2] = nlist;
             s.pub[b * 2 + 1] = nn;
         }
         if (s.items) {
-            // items (TILE_S-row pieces of one head's listed complements) of the lists, the most
-            // over the sequences: the next step's launches size their work from it
-            atomicMax(&s.items[0], (int)(((long long)nkept * g.comp_max + TILE_S - 1) / TILE_S));
-            atomicMax(&s.items[1], (int)(((long long)nn * g.comp_max + TILE_S - 1) / TILE_S));
+            // items (TILE_S-row pieces of one head's listed complements) of the kept list, the
+            // most over the sequences: the next step's tidal launch sizes its work from it
+            atomicMax(&s.items[0], (int)(((long long)nlist * g.comp_max + TILE_S - 1) / TILE_S));
         }
         s.step[b] = step + 1;
         atomicAdd(&s.stats[0], (unsigned long long)nn);
@@ -989,6 +995,21 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
         }
         atomicAdd(&s.stats[6], (unsigned long long)nrev);
         atomicAdd(&s.stats[7], (unsigned long long)nkrows);
+    }
+    if (s.pub) {
+        // publication: the host polls this sequence's tag instead of an event after the kernel
+        // (an event costs the stream a gap before the next launch).  Every wavefront waits for
+        // its own stores to the mirror (and the exhaustion flag) to complete before the barrier
+        // (a work-group barrier alone does not wait for global stores); the first thread's
+        // system-scope fence then writes back whatever of them the cache holds, and the tag is
+        // stored last, write-through
+        __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+        if (tid == 0) {
+            __threadfence_system();
+            __hip_atomic_store(s.pub + g.B * 2 + (size_t)g.B * g.knew * 2 + b, s.pub_tag, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_SYSTEM);
+        }
     }
 }
 
@@ -1409,22 +1430,22 @@ __device__ inline void slot_rows_tile(const Geometry &g, const Tiers &t, const S
     }
 }
 
-// Item j of list `which` (0 kept, 1 new) of tidal head ti, sequence b: the head's complements
-// of the listed segments, taken as one run of rows (entries one after the other, cfull rows
-// each), cut into TILE_S-row items; item j is rows [j * TILE_S, (j + 1) * TILE_S) of that run.
-// An item may start or end inside an entry, so every work-group streams a full tile whatever the
-// complement length.  Returns at once when the head has fewer items this step.
+// Item j of the kept list of tidal head ti, sequence b: the head's complements of the listed
+// segments, taken as one run of rows (entries one after the other, cfull rows each), cut into
+// TILE_S-row items; item j is rows [j * TILE_S, (j + 1) * TILE_S) of that run.  An item may
+// start or end inside an entry, so every work-group streams a full tile whatever the complement
+// length.  Returns at once when the head has fewer items this step.
 template <int G>
-__device__ inline void list_item(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, int which,
-                                 int j, int ti, int b, SubsetSmem<G, RPL_S> &sm)
+__device__ inline void list_item(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, int j,
+                                 int ti, int b, SubsetSmem<G, RPL_S> &sm)
 {
     const HeadRows hr = t.hr[ti];
-    const int cm = hr.cfull, cnt = s.counts[b * 2 + which];
+    const int cm = hr.cfull, cnt = s.counts[b * 2];
     const long long v0 = (long long)j * TILE_S;
-    if (cm == 0 || j >= (which ? hr.ngn : hr.ngk) || v0 >= (long long)cnt * cm) return;
+    if (cm == 0 || j >= hr.ngk || v0 >= (long long)cnt * cm) return;
     const int e0 = (int)(v0 / cm), e1 = (int)min((long long)cnt - 1, (v0 + TILE_S - 1) / cm);
-    const int32_t *list = which ? s.new_list + (size_t)b * g.knew * 2 : s.kept_list + (size_t)b * g.n_slots * 2;
-    const size_t p = (size_t)b * g.P + hr.pbase + hr.nts + (which ? hr.ngk : 0) + j;
+    const int32_t *list = s.kept_list + (size_t)b * g.n_slots * 2;
+    const size_t p = (size_t)b * g.P + hr.pbase + hr.nts + j;
     const int n_entries = e1 - e0 + 1, first = (int)(v0 - (long long)e0 * cm);
     slot_rows_tile<G, RPL_S>(g, t, s, q, list, e0, n_entries, first, ti, b, p, sm);
 }
@@ -1486,7 +1507,7 @@ __device__ inline void recall_units(const Geometry &g, const Tiers &t, const Ste
 // them: the step is bound by the host link then, and the copies start with the launch.
 template <int G, int RPLK, bool REC>
 __global__ __launch_bounds__(NT, REC ? (RPLK == RPL_S ? 2 : 1) : (G <= 4 ? 4 : 3)) void tidal_fixed_kernel(
-    Geometry g, Tiers t, StepBuffers s, const uint16_t *__restrict__ q, int with_static, int which)
+    Geometry g, Tiers t, StepBuffers s, const uint16_t *__restrict__ q, int with_static)
 {
     union Smem {
         SubsetSmem<G, RPL_S> st;
@@ -1503,29 +1524,25 @@ __global__ __launch_bounds__(NT, REC ? (RPLK == RPL_S ? 2 : 1) : (G <= 4 ? 4 : 3
         nw -= RECALL_WGS;
     }
     const long long n_static = with_static ? (long long)g.n_static * g.B : 0;
-    // list items in item-major order over (sequence, tidal head); the loop ends after the last
-    // item any head has this step (a head with fewer returns at once from the ones past its own)
-    // which = 2: the kept list's items, then the new list's
-    long long n_items[2] = {0, 0};
-    for (int lst = 0; lst < 2; ++lst) {
-        if (which != 2 && which != lst) continue;
-        if (s.items) {
-            n_items[lst] = s.items[lst];
-        } else {
-            int kmax = 0;
-            for (int b = 0; b < g.B; ++b) kmax = max(kmax, s.counts[b * 2 + lst]);
-            n_items[lst] = ((long long)kmax * g.comp_max + TILE_S - 1) / TILE_S;
-        }
-        n_items[lst] = min(n_items[lst], (long long)(lst ? g.ng_new : g.ng_kept));
+    // kept-list items in item-major order over (sequence, tidal head); the loop ends after the
+    // last item any head has this step (a head with fewer returns at once from the ones past its
+    // own)
+    long long n_items;
+    if (s.items) {
+        n_items = s.items[0];
+    } else {
+        int kmax = 0;
+        for (int b = 0; b < g.B; ++b) kmax = max(kmax, s.counts[b * 2]);
+        n_items = ((long long)kmax * g.comp_max + TILE_S - 1) / TILE_S;
     }
-    const long long nh = (long long)g.nT * g.B, nk = n_items[0] * nh;
-    const long long total = n_static + nk + n_items[1] * nh;
+    n_items = min(n_items, (long long)g.ng_kept);
+    const long long nh = (long long)g.nT * g.B, total = n_static + n_items * nh;
     for (long long it = w; it < total; it += nw) {
         if (it < n_static) {
             static_tile<G>(g, t, s, q, (int)(it % g.n_static), (int)(it / g.n_static), sm.st);
         } else {
-            const long long i2 = it - n_static, lst = i2 >= nk, i3 = i2 - (lst ? nk : 0), j = i3 / nh, rest = i3 - j * nh;
-            list_item<G>(g, t, s, q, (int)lst, (int)j, (int)(rest % g.nT), (int)(rest / g.nT), sm.st);
+            const long long i2 = it - n_static, j = i2 / nh, rest = i2 - j * nh;
+            list_item<G>(g, t, s, q, (int)j, (int)(rest % g.nT), (int)(rest / g.nT), sm.st);
         }
     }
 }
@@ -1627,11 +1644,9 @@ __global__ __launch_bounds__(COMBINE_THREADS) void subset_combine_kernel(Geometr
     const HeadRows hr = t.hr[hi];
     const bool recalls = tidal && hr.cfull > 0;   // no complement at retention 1
     const int nk = recalls ? (int)min(((long long)s.counts[b * 2] * hr.cfull + TILE_S - 1) / TILE_S, (long long)hr.ngk) : 0;
-    // new complements: packed items (next-step timing: the previous step's recall) or one
-    // partial per entry (same-step timing)
-    const int nn = !recalls ? 0
-                   : g.next_step ? (int)min(((long long)s.counts[b * 2 + 1] * hr.cfull + TILE_S - 1) / TILE_S, (long long)hr.ngn)
-                                 : min(s.counts[b * 2 + 1], g.knew);
+    // new complements with same-step timing: one partial per entry (with next-step timing they
+    // are items of the kept list)
+    const int nn = !recalls || g.next_step ? 0 : min(s.counts[b * 2 + 1], g.knew);
     const int nts = hr.nts, ngk = hr.ngk, nvalid = nts + nk + nn;
     auto part = [&](int j) {
         if (j < nts) return j;
@@ -1847,12 +1862,10 @@ long long resident_grid(K kernel, std::atomic<int> &cache, const Geometry &g, lo
 template <int G>
 struct TidalFixedL {
     static hipError_t run(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, bool recall,
-                          bool with_static, int which, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
+                          bool with_static, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
     {
         recall = recall && g.nT > 0 && g.k > 0 && g.comp_max > 0;
-        const long long tiles = (with_static ? (long long)g.n_static * g.B : 0) +
-                                (long long)(which == 0 ? g.ng_kept : which == 1 ? g.ng_new : g.ng_kept + g.ng_new) *
-                                    g.nT * g.B;
+        const long long tiles = (with_static ? (long long)g.n_static * g.B : 0) + (long long)g.ng_kept * g.nT * g.B;
         if (tiles == 0 && !recall) return record_pair(e0, e1, st);
         const dim3 block(NT);
         const int ws = with_static ? 1 : 0;
@@ -1860,15 +1873,15 @@ struct TidalFixedL {
         if (!recall) {
             auto k = tidal_fixed_kernel<G, RPL_S, false>;
             const dim3 grid((unsigned)resident_grid(k, occ[0], g, tiles));
-            hipExtLaunchKernelGGL(k, grid, block, 0, st, e0, e1, 0, g, t, s, q, ws, which);
+            hipExtLaunchKernelGGL(k, grid, block, 0, st, e0, e1, 0, g, t, s, q, ws);
         } else if (g.slot_tile == TILE_S) {
             auto k = tidal_fixed_kernel<G, RPL_S, true>;
             const dim3 grid((unsigned)(RECALL_WGS + std::max(1LL, resident_grid(k, occ[1], g, tiles))));
-            hipExtLaunchKernelGGL(k, grid, block, 0, st, e0, e1, 0, g, t, s, q, ws, which);
+            hipExtLaunchKernelGGL(k, grid, block, 0, st, e0, e1, 0, g, t, s, q, ws);
         } else {
             auto k = tidal_fixed_kernel<G, 2 * RPL_S, true>;
             const dim3 grid((unsigned)(RECALL_WGS + std::max(1LL, resident_grid(k, occ[2], g, tiles))));
-            hipExtLaunchKernelGGL(k, grid, block, 0, st, e0, e1, 0, g, t, s, q, ws, which);
+            hipExtLaunchKernelGGL(k, grid, block, 0, st, e0, e1, 0, g, t, s, q, ws);
         }
         return hipGetLastError();
     }
@@ -1932,9 +1945,9 @@ hipError_t launch_select(const Geometry &g, const StepBuffers &s, float *scores,
 }
 
 hipError_t launch_tidal_fixed(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, bool recall,
-                              bool with_static, int which, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
+                              bool with_static, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
 {
-    return dispatch_g<TidalFixedL>(g.G, g, t, s, q, recall, with_static, which, st, e0, e1);
+    return dispatch_g<TidalFixedL>(g.G, g, t, s, q, recall, with_static, st, e0, e1);
 }
 
 hipError_t launch_attention(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st,
