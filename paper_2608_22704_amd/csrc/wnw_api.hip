@@ -1340,8 +1340,17 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, void *out, float *scor
                 HIPCHECK(c, hipStreamWaitEvent(s0, c->ev_rec, 0));
             }
         }
+        // with host-issued copies the host has read the previous step's mirror (its copies are
+        // issued), so it knows the length of the list this launch streams
+        long long items = -1;
+        if (memcpy_path && c->rec_pending) {
+            const int32_t *cnt = c->h_newinfo + (size_t)nxt * c->mirror_ints;
+            int nmax = 0;
+            for (int b = 0; b < g.B; ++b) nmax = std::max(nmax, cnt[b * 2]);
+            items = ((long long)nmax * g.comp_max + TILE_S - 1) / TILE_S;
+        }
         // markers 2 and 3: the launch's own start and end
-        HIPCHECK(c, launch_tidal_fixed(g, c->t, sb, q, false, false, s0, timing ? ev.e[2] : nullptr,
+        HIPCHECK(c, launch_tidal_fixed(g, c->t, sb, q, false, false, items, s0, timing ? ev.e[2] : nullptr,
                                        timing ? ev.e[3] : nullptr));
         // the final merge is queued before the host waits for the selection below, so that the
         // device never idles behind that wait
@@ -1374,13 +1383,13 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, void *out, float *scor
         // this step's select kernel; every kernel that could still read them (the previous
         // step's) precedes it on this stream.
         if (timing) HIPCHECK(c, hipEventRecord(ev.r[0], s0));
-        HIPCHECK(c, launch_tidal_fixed(g, c->t, sb, q, true, true, s0));
+        HIPCHECK(c, launch_tidal_fixed(g, c->t, sb, q, true, true, -1, s0));
         if (timing) HIPCHECK(c, hipEventRecord(ev.r[1], s0));
         MARK(3);
     } else {
         MARK(2);
         // (4a) device-resident rows while the host waits for the selection and issues the copies
-        HIPCHECK(c, launch_tidal_fixed(g, c->t, sb, q, false, true, s0));
+        HIPCHECK(c, launch_tidal_fixed(g, c->t, sb, q, false, true, -1, s0));
         MARK(3);
         // (3) copies on the side stream.  The target slots were freed by this step's select
         // kernel, which follows every earlier reader on s0: once it has published its tag, no

@@ -159,9 +159,12 @@ inline size_t select_shared_bytes(const Geometry &g)
 // slots; with `recall`
 // (same-step timing), also the copy of the complements listed for recall from mapped pinned
 // memory into their slots and the attention over them.
-// The slot tiles are the kept list's items (after the static tiles when with_static).
+// The slot tiles are the kept list's items (after the static tiles when with_static); `items`:
+// the most items of any head this step when the host knows it (the kernel's own count from the
+// select kernel then agrees), else -1.
 hipError_t launch_tidal_fixed(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, bool recall,
-                              bool with_static, hipStream_t st, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
+                              bool with_static, long long items, hipStream_t st, hipEvent_t e0 = nullptr,
+                              hipEvent_t e1 = nullptr);
 // Anchor attention + chunk mass together with the static tidal/fixed tiles (next-step timing).
 hipError_t launch_attention(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st,
                             hipEvent_t e0, hipEvent_t e1);

@@ -1099,18 +1099,38 @@ __device__ inline void subset_tile(const uint16_t *__restrict__ qh, const RowMap
         const int cm = map.comp_max;
         const unsigned vd = (unsigned)cm * (D * 2);   // an entry's V rows follow its K rows
         const int v0 = map.first + wave * NR + rg;     // row within the entries, from entry 0's first
-        // every row's entry and offset first (independent shared-memory reads, one wait), then
-        // all the loads back to back
+        // every row's entry first (one division, then steps of 4 rows), then the entries'
+        // shared-memory reads back to back (one wait), then all the loads back to back
         unsigned off[RPL];
+        int ent[RPL], rrs[RPL];
+        {
+            int e = v0 / cm, rr = v0 - e * cm;
+#pragma unroll
+            for (int i = 0; i < RPL; ++i) {
+                if (i) {
+                    rr += 4;
+                    while (rr >= cm) {
+                        rr -= cm;
+                        ++e;
+                    }
+                }
+                ent[i] = e < map.n_entries ? e : -1;
+                rrs[i] = rr;
+            }
+        }
+        int nrs[RPL];
+        unsigned kos[RPL];
+#pragma unroll
+        for (int i = 0; i < RPL; ++i) {
+            const int ec = ent[i] < 0 ? 0 : ent[i];
+            nrs[i] = map.nrows[ec];
+            kos[i] = map.koff[ec];
+        }
         const unsigned off0 = map.koff[0] + sub * 16;
 #pragma unroll
         for (int i = 0; i < RPL; ++i) {
-            const int v = v0 + 4 * i, e = v / cm, rr = v - e * cm;
-            const int ec = e < map.n_entries ? e : 0;
-            const int nr = map.nrows[ec];
-            const unsigned ko = map.koff[ec];
-            ok[i] = e < map.n_entries && rr < nr;
-            off[i] = ok[i] ? ko + (unsigned)rr * (D * 2) + sub * 16 : off0;
+            ok[i] = ent[i] >= 0 && rrs[i] < nrs[i];
+            off[i] = ok[i] ? kos[i] + (unsigned)rrs[i] * (D * 2) + sub * 16 : off0;
         }
 #pragma unroll
         for (int i = 0; i < RPL; ++i) kr[i] = buf_load_nt(rs, off[i]);
@@ -1862,17 +1882,21 @@ long long resident_grid(K kernel, std::atomic<int> &cache, const Geometry &g, lo
 template <int G>
 struct TidalFixedL {
     static hipError_t run(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, bool recall,
-                          bool with_static, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
+                          bool with_static, long long items, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
     {
         recall = recall && g.nT > 0 && g.k > 0 && g.comp_max > 0;
-        const long long tiles = (with_static ? (long long)g.n_static * g.B : 0) + (long long)g.ng_kept * g.nT * g.B;
+        const bool known = items >= 0 && !recall;
+        const long long tiles = (with_static ? (long long)g.n_static * g.B : 0) +
+                                (known ? std::min<long long>(items, g.ng_kept) : g.ng_kept) * g.nT * g.B;
         if (tiles == 0 && !recall) return record_pair(e0, e1, st);
         const dim3 block(NT);
         const int ws = with_static ? 1 : 0;
         static std::atomic<int> occ[3];
         if (!recall) {
+            // the step's item count known on the host: one tile per work-group (the hardware
+            // dispatches each work-group as another ends); else as many as stay resident, looping
             auto k = tidal_fixed_kernel<G, RPL_S, false>;
-            const dim3 grid((unsigned)resident_grid(k, occ[0], g, tiles));
+            const dim3 grid((unsigned)(known ? tiles : resident_grid(k, occ[0], g, tiles)));
             hipExtLaunchKernelGGL(k, grid, block, 0, st, e0, e1, 0, g, t, s, q, ws);
         } else if (g.slot_tile == TILE_S) {
             auto k = tidal_fixed_kernel<G, RPL_S, true>;
@@ -1945,9 +1969,9 @@ hipError_t launch_select(const Geometry &g, const StepBuffers &s, float *scores,
 }
 
 hipError_t launch_tidal_fixed(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, bool recall,
-                              bool with_static, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
+                              bool with_static, long long items, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
 {
-    return dispatch_g<TidalFixedL>(g.G, g, t, s, q, recall, with_static, st, e0, e1);
+    return dispatch_g<TidalFixedL>(g.G, g, t, s, q, recall, with_static, items, st, e0, e1);
 }
 
 hipError_t launch_attention(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st,
