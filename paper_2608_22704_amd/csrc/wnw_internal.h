@@ -153,7 +153,7 @@ hipError_t launch_select(const Geometry &g, const StepBuffers &s, float *scores,
 // Shared memory of the select kernel (bounded at set-up).
 inline size_t select_shared_bytes(const Geometry &g)
 {
-    return (size_t)g.nc * (SCORE_PARTS * 8 + 4 + 9 * 4) + (size_t)g.n_slots * 6 * 4;
+    return (size_t)g.nc * (SCORE_PARTS * 8 + 4 + 11 * 4) + (size_t)g.n_slots * 6 * 4 + 3 * (size_t)((g.nc + 63) / 64) * 4;
 }
 // Fixed heads (with `with_static`), tidal kept rows and the tidal complements already in their
 // slots; with `recall`

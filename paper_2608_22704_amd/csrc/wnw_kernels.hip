@@ -641,43 +641,6 @@ __device__ inline void lds_barrier()
     __asm__ volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-__device__ int block_scan_excl(int *a, int n, int *wsum)
-{
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = blockDim.x >> 6;
-    int carry = 0;
-    for (int base = 0; base < n; base += blockDim.x) {
-        const int i = base + tid;
-        const int v = i < n ? a[i] : 0;
-        int x = v;
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-            const int y = __shfl_up(x, o);
-            if (lane >= o) x += y;
-        }
-        if (lane == 63) wsum[wave] = x;
-        lds_barrier();
-        if (wave == 0) {
-            // exclusive scan of the wavefront totals by the first wavefront (nw <= 64)
-            const int tt = lane < nw ? wsum[lane] : 0;
-            int y = tt;
-#pragma unroll
-            for (int o = 1; o < 64; o <<= 1) {
-                const int z = __shfl_up(y, o);
-                if (lane >= o) y += z;
-            }
-            if (lane < nw) wsum[lane] = y - tt;
-            if (lane == nw - 1) wsum[nw] = y;
-        }
-        lds_barrier();
-        if (i < n) a[i] = carry + wsum[wave] + x - v;
-        carry += wsum[nw];
-        lds_barrier();
-    }
-    return carry;
-}
-
-
-
 // Per sequence b (state staged in shared memory, written back at the end).  Chunks (nchk) are
 // the selection's candidates; segments (nc) are the unit of masses, residency, slots and
 // recall.  With disjoint chunks a chunk is a segment; with overlapping chunks chunk c is
@@ -705,6 +668,9 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
     const bool nxt = g.next_step, two = g.span == 2;
     extern __shared__ double sdyn[];
     double *part = sdyn;                              // [SCORE_PARTS][nu]; row 0 then segment sums
+    unsigned long long *ckey = (unsigned long long *)(part + nu);       // [nk] in row 1: ranking keys
+    unsigned long long *fkey = (unsigned long long *)(part + 2 * nu);   // [ns] in row 2: free-slot keys
+    static_assert(SCORE_PARTS >= 3, "rows 1 and 2 of the score partials hold the ranking keys");
     float *sc = (float *)(part + SCORE_PARTS * nu);   // [nk] chunk scores
     int *fsel = (int *)(sc + nu);                     // [nk] selected
     int *st = fsel + nu;                              // [nk] streak
@@ -713,7 +679,7 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
     int *fnew = slast + nu;                           // [nu] to recall
     int *fkept = fnew + nu;                           // [nu] attended from a slot already filled
     int *fdrop = fkept + nu;                          // [nu] leaves the resident set
-    int *rank = fdrop + nu;                           // [nu] scan scratch
+    int *rank = fdrop + nu;                           // [nk] rank of a selected chunk
     int *busy = rank + nu;                            // [ns] 0 free, 1 owned, 2 freed after this step
     int *sdata = busy + ns;                           // [ns] segment whose bytes the slot holds
     int *since = sdata + ns;                          // [ns] step at which the slot was freed
@@ -721,7 +687,9 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
     int *freelist = skey + ns;                        // [ns] free slots in order
     int *frank = freelist + ns;                       // [ns] rank of a free slot among the free ones
     int *srows = frank + ns;                          // [nu] complement rows of the segment (all tidal heads)
-    __shared__ int wsum[SEL_THREADS / 64 + 1];
+    int *rank_k = srows + nu;                         // [nu] rank of a kept segment
+    int *rank_n = rank_k + nu;                        // [nu] rank of a new segment
+    int *bcnt = rank_n + nu;                          // [3][ceil(nu / 64)] flags set per 64-entry block
     __shared__ int ndrop, nrows, nrev, nfree, nkrows;
 
     int32_t *g_streak = s.streak + (size_t)b * nk, *g_slot_of = s.slot_of + (size_t)b * nu;
@@ -779,6 +747,11 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
         const float v = (float)(acc / (double)len);
         sc[c] = v;
         scores[(size_t)b * nk + c] = v;
+        // ranking key: the fp32 score's bits made order-preserving, then the complement of the
+        // id, so that a larger key is a higher score, or an equal score and a lower id
+        unsigned u32 = v == 0.f ? 0u : __float_as_uint(v);   // -0 ranks as +0
+        u32 = (u32 >> 31) ? ~u32 : u32 | 0x80000000u;
+        ckey[c] = ((unsigned long long)u32 << 32) | (0xffffffffu - (unsigned)c);
     }
     lds_barrier();
 
@@ -789,24 +762,20 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
             if (c >= 0 && c < nk) fsel[c] = 1;
         }
     } else {
-        // rank of every chunk among all: P adjacent lanes per chunk each compare it with a
-        // contiguous share of the chunks (independent shared-memory reads, unrolled), then add
-        // their counts across the P lanes
+        // rank of every chunk among all (the number of larger keys): P adjacent lanes per chunk
+        // each compare it with a contiguous share of the chunks (independent shared-memory
+        // reads, unrolled), then add their counts across the P lanes
         int P = 1;
         while (P < 32 && 2 * P * nk <= nthr) P *= 2;
         const int span = (nk + P - 1) / P;
         for (int c0 = 0; c0 < nk * P; c0 += nthr) {
             const int w = c0 + tid, c = w / P, part = w - c * P;
             int cnt = 0;
-            float v = 0.f;
             if (c < nk) {
-                v = sc[c];
+                const unsigned long long kc = ckey[c];
                 const int ja = part * span, jb = min(nk, ja + span);
 #pragma unroll 8
-                for (int j = ja; j < jb; ++j) {
-                    const float x = sc[j];
-                    cnt += (x > v) || (x == v && j < c);
-                }
+                for (int j = ja; j < jb; ++j) cnt += ckey[j] > kc;
             }
             for (int o = 1; o < P; o <<= 1) cnt += __shfl_xor(cnt, o);
             if (c < nk && part == 0) fsel[c] = cnt < k;
@@ -857,10 +826,50 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
     }
     lds_barrier();
 
-    // selected chunk ids, ascending
-    for (int c = tid; c < nk; c += nthr) rank[c] = fsel[c];
+    // ranks in index order of the selected chunks (rank), the kept segments (rank_k) and the
+    // new segments (rank_n), all three at once: a ballot per wavefront and flag gives each entry
+    // its rank inside its 64-entry block and the block's count (kept in shared memory); after
+    // one barrier each entry adds the counts of the blocks before its own
+    const int nb = (nu + 63) >> 6, lane = tid & 63;
+    for (int i0 = 0; i0 < nu; i0 += nthr) {
+        const int i = i0 + tid;
+        const unsigned long long m0 = __ballot(i < nk && fsel[i]), m1 = __ballot(i < nu && fkept[i]),
+                                 m2 = __ballot(i < nu && fnew[i]);
+        const unsigned long long below = (1ull << lane) - 1ull;
+        if (i < nk) rank[i] = __popcll(m0 & below);
+        if (i < nu) {
+            rank_k[i] = __popcll(m1 & below);
+            rank_n[i] = __popcll(m2 & below);
+            if (lane == 0) {
+                const int blk = i >> 6;
+                bcnt[blk] = __popcll(m0);
+                bcnt[nb + blk] = __popcll(m1);
+                bcnt[2 * nb + blk] = __popcll(m2);
+            }
+        }
+    }
     lds_barrier();
-    const int nsel = block_scan_excl(rank, nk, wsum);
+    int nsel = 0, nkept = 0, nnew = 0;
+    for (int i0 = 0; i0 < nu; i0 += nthr) {
+        const int i = i0 + tid, blk = i >> 6;
+        int p0 = 0, p1 = 0, p2 = 0;
+        for (int j = (i0 >> 6); j < blk && j < nb; ++j) {
+            p0 += bcnt[j];
+            p1 += bcnt[nb + j];
+            p2 += bcnt[2 * nb + j];
+        }
+        if (i < nk) rank[i] += nsel + p0;
+        if (i < nu) {
+            rank_k[i] += nkept + p1;
+            rank_n[i] += nnew + p2;
+        }
+        // totals up to the end of this round (the same for every thread)
+        for (int j = i0 >> 6; j < min(nb, (i0 + nthr) >> 6); ++j) {
+            nsel += bcnt[j];
+            nkept += bcnt[nb + j];
+            nnew += bcnt[2 * nb + j];
+        }
+    }
     if (selected) {
         for (int c = tid; c < nk; c += nthr)
             if (fsel[c]) selected[(size_t)b * k + rank[c]] = c;
@@ -873,17 +882,13 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
     // step that reads the list finds them copied, and each tidal head streams one run of rows.
     // Bit 30 of an entry's slot: every tidal head's complement of the segment has its full
     // stride of rows (the tiles then skip the per-head row count).
-    lds_barrier();   // rank is rewritten
-    for (int u = tid; u < nu; u += nthr) rank[u] = fkept[u];
-    lds_barrier();
-    const int nkept = block_scan_excl(rank, nu, wsum);
     int32_t *kl = s.kept_list + (size_t)b * ns * 2;
     int c_krows = 0;
     for (int u = tid; u < nu; u += nthr)
         if (fkept[u]) {
             const int rows = srows[u];
-            kl[rank[u] * 2] = u;
-            kl[rank[u] * 2 + 1] = sof[u] | (rows * 2 == g.blk_rows ? 1 << 30 : 0);
+            kl[rank_k[u] * 2] = u;
+            kl[rank_k[u] * 2 + 1] = sof[u] | (rows * 2 == g.blk_rows ? 1 << 30 : 0);
             c_krows += rows;
         }
     c_krows = wave_sum(c_krows);
@@ -896,6 +901,8 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
         const bool fr = i < ns && !busy[i];
         if (i < ns) {
             skey[i] = fr ? ((sdata[i] >= 0 ? 1 : 0) << 30) + since[i] : -1;
+            // the key and the slot id in one 64-bit word (slots not free: above every free one)
+            fkey[i] = fr ? ((unsigned long long)skey[i] << 32) | (unsigned)i : ~0ull;
             frank[i] = 0;
         }
         const unsigned long long bal = __ballot(fr);   // free slots: one count per wavefront
@@ -908,14 +915,11 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
         const int split = max(1, nthr / max(ns, 1)), span_j = (ns + split - 1) / split;
         for (int w = tid; w < ns * split; w += nthr) {
             const int i = w % ns, part = w / ns;
-            const int ki = skey[i];
-            if (ki < 0) continue;
+            if (skey[i] < 0) continue;
+            const unsigned long long ki = fkey[i];
             int r = 0;
 #pragma unroll 16
-            for (int j = part * span_j, je = min(ns, (part + 1) * span_j); j < je; ++j) {
-                const int kj = skey[j];
-                r += kj >= 0 && (kj < ki || (kj == ki && j < i));
-            }
+            for (int j = part * span_j, je = min(ns, (part + 1) * span_j); j < je; ++j) r += fkey[j] < ki;
             if (r) atomicAdd(&frank[i], r);
         }
     }
@@ -925,28 +929,25 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
     lds_barrier();
 
     // segments to recall take the free slots in that order (lowest id first)
-    for (int u = tid; u < nu; u += nthr) rank[u] = fnew[u];
-    lds_barrier();
-    const int nnew = block_scan_excl(rank, nu, wsum);
     int32_t *nl = s.new_list + (size_t)b * g.knew * 2;
     for (int u = tid; u < nu; u += nthr)
-        if (fnew[u] && rank[u] < nfree && rank[u] < g.knew) {
-            const int slot = freelist[rank[u]];
+        if (fnew[u] && rank_n[u] < nfree && rank_n[u] < g.knew) {
+            const int slot = freelist[rank_n[u]];
             sof[u] = slot;
             slast[u] = slot;
             busy[slot] = 1;
             sdata[slot] = u;
-            nl[rank[u] * 2] = u;
-            nl[rank[u] * 2 + 1] = slot;
+            nl[rank_n[u] * 2] = u;
+            nl[rank_n[u] * 2 + 1] = slot;
             if (nxt) {
-                kl[(nkept + rank[u]) * 2] = u;
-                kl[(nkept + rank[u]) * 2 + 1] = slot | (srows[u] * 2 == g.blk_rows ? 1 << 30 : 0);
+                kl[(nkept + rank_n[u]) * 2] = u;
+                kl[(nkept + rank_n[u]) * 2 + 1] = slot | (srows[u] * 2 == g.blk_rows ? 1 << 30 : 0);
             }
             if (s.pub) {
                 // the host reads this mirror once the sequence's tag is published (below)
                 int32_t *hl = s.pub + g.B * 2 + (size_t)b * g.knew * 2;
-                hl[rank[u] * 2] = u;
-                hl[rank[u] * 2 + 1] = slot;
+                hl[rank_n[u] * 2] = u;
+                hl[rank_n[u] * 2 + 1] = slot;
             }
         }
     for (int u = tid; u < nu; u += nthr)
