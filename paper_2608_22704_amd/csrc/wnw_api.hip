@@ -106,6 +106,7 @@ struct wnw_ctx {
     int32_t *d_newinfo = nullptr;      // the same memory as the device addresses it
     size_t mirror_ints = 0;            // int32 entries of one mirror
     unsigned copy_mask[2] = {0, 0};    // by step parity: copy streams that received a copy
+    unsigned copy_rr = 0;              // copy stream of the next recall's first run
 
     // Recall thread (next-step timing with host-issued copies): for each step it waits for the
     // step's selection, then issues the step's copies and records their end events, so that
@@ -557,7 +558,10 @@ hipError_t issue_copies_raw(wnw_ctx *c, int par, hipStream_t st, const char **wh
             e = hipLaunchHostFunc(i == 0 ? st : c->copy_st[i - 1], delay_fn, &c->delay_us);
         mask = (1u << N_COPY_STREAMS) - 1;   // every stream holds a delay
     }
-    int n_runs = 0;
+    // the round-robin continues from the previous step's last stream, so that over the steps
+    // every copy stream carries the same share (restarting at the first stream each step would
+    // give the first ones one run more per step)
+    unsigned n_runs = c->copy_rr;
     for (int b = 0; b < g.B && cb && e == hipSuccess; ++b) {
         const int n = cnt[b * 2 + 1];
         for (int i = 0; i < n && e == hipSuccess;) {
@@ -568,7 +572,7 @@ hipError_t issue_copies_raw(wnw_ctx *c, int par, hipStream_t st, const char **wh
                 if (ej[0] != e0[0] + (j - i) || ej[1] != e0[1] + (j - i)) break;
                 ++j;
             }
-            const int w = n_runs++ % N_COPY_STREAMS;
+            const int w = (int)(n_runs++ % N_COPY_STREAMS);
             mask |= 1u << w;
             e = hipMemcpyAsync(c->slots + ((size_t)b * g.n_slots + e0[1]) * g.chunk_elems,
                                c->host_comp + ((size_t)b * g.nc + e0[0]) * g.chunk_elems, cb * (j - i),
@@ -591,6 +595,7 @@ hipError_t issue_copies_raw(wnw_ctx *c, int par, hipStream_t st, const char **wh
         }
     }
     c->copy_mask[par] = mask;
+    c->copy_rr = n_runs % N_COPY_STREAMS;
     return hipSuccess;
 }
 
