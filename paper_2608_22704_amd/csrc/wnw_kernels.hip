@@ -1527,7 +1527,7 @@ __device__ inline void recall_units(const Geometry &g, const Tiers &t, const Ste
 // the complements listed for recall from mapped pinned memory into their slots and attend to
 // them: the step is bound by the host link then, and the copies start with the launch.
 template <int G, int RPLK, bool REC>
-__global__ __launch_bounds__(NT, REC ? (RPLK == RPL_S ? 2 : 1) : (G <= 4 ? 4 : 3)) void tidal_fixed_kernel(
+__global__ __launch_bounds__(NT, REC ? (RPLK == RPL_S ? 2 : 1) : (G <= 4 ? 4 : G <= 6 ? 3 : 2)) void tidal_fixed_kernel(
     Geometry g, Tiers t, StepBuffers s, const uint16_t *__restrict__ q, int with_static)
 {
     union Smem {
@@ -1636,7 +1636,7 @@ __global__ __launch_bounds__(NT) void recall_copy_kernel(Geometry g, Tiers t, St
 
 // Complements copied by hipMemcpyAsync (host-waited recall path): one entry per work-group.
 template <int G, int RPL>
-__global__ __launch_bounds__(NT, RPL == RPL_S ? 4 : 2) void new_slots_kernel(Geometry g, Tiers t, StepBuffers s, const uint16_t *__restrict__ q)
+__global__ __launch_bounds__(NT, RPL == RPL_S ? (G <= 4 ? 4 : 3) : 2) void new_slots_kernel(Geometry g, Tiers t, StepBuffers s, const uint16_t *__restrict__ q)
 {
     __shared__ SubsetSmem<G, RPL> sm;
     new_entry<G, RPL>(g, t, s, q, blockIdx.x, blockIdx.y, blockIdx.z, sm);
@@ -1660,8 +1660,7 @@ __global__ __launch_bounds__(COMBINE_THREADS) void subset_combine_kernel(Geometr
     }
     float *sfac = (float *)dsm;
     const bool tidal = hi < g.nT;
-    __shared__ float red[NW * G];
-    __shared__ float Linv[G];
+    __shared__ float red[NW * G], redl[NW * G];   // per wavefront: maxima, sums
     const HeadRows hr = t.hr[hi];
     const bool recalls = tidal && hr.cfull > 0;   // no complement at retention 1
     const int nk = recalls ? (int)min(((long long)s.counts[b * 2] * hr.cfull + TILE_S - 1) / TILE_S, (long long)hr.ngk) : 0;
@@ -1682,7 +1681,7 @@ __global__ __launch_bounds__(COMBINE_THREADS) void subset_combine_kernel(Geometr
     const float4 *po = (const float4 *)s.ps_o;
     // the first loads of every phase are issued together (one memory round trip): this
     // thread's partial maximum and sum, and its first PF output partials
-    constexpr int PF = G <= 4 ? 8 : 4;
+    constexpr int PF = G <= 2 ? 8 : (G <= 4 ? 7 : 4);   // 7 for G = 4: eight spill at 1024 threads
     float4 pf[PF];
 #pragma unroll
     for (int u = 0; u < PF; ++u)
@@ -1712,7 +1711,6 @@ __global__ __launch_bounds__(COMBINE_THREADS) void subset_combine_kernel(Geometr
         for (int w = 1; w < NW; ++w) M[hh] = fmaxf(M[hh], red[w * G + hh]);
         lsum[hh] = 0.f;
     }
-    __syncthreads();
     if (tid < nvalid)
 #pragma unroll
         for (int hh = 0; hh < G; ++hh) {
@@ -1731,13 +1729,7 @@ __global__ __launch_bounds__(COMBINE_THREADS) void subset_combine_kernel(Geometr
 #pragma unroll
     for (int hh = 0; hh < G; ++hh) {
         lsum[hh] = wave_sum(lsum[hh]);
-        if (lane == 0) red[wave * G + hh] = lsum[hh];
-    }
-    __syncthreads();
-    if (tid < G) {
-        float L = red[tid];
-        for (int w = 1; w < NW; ++w) L += red[w * G + tid];
-        Linv[tid] = L > 0.f ? 1.f / L : 0.f;
+        if (lane == 0) redl[wave * G + hh] = lsum[hh];   // red still holds the maxima others read
     }
     __syncthreads();
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -1766,7 +1758,9 @@ __global__ __launch_bounds__(COMBINE_THREADS) void subset_combine_kernel(Geometr
         }
         const int lk = tidal ? t.tidal_lk[hi] : t.fixed_lk[hi - g.nT], l = lk / g.Hkv, kv = lk - l * g.Hkv;
         const size_t ob = (((size_t)b * g.L + l) * g.Hq + (size_t)kv * G) * D + (size_t)col * 4;
-        const float li = Linv[h];
+        float L = redl[h];
+        for (int w = 1; w < NW; ++w) L += redl[w * G + h];
+        const float li = L > 0.f ? 1.f / L : 0.f;
         store_out(out, ob, acc.x * li, g.out_bf16);
         store_out(out, ob + 1, acc.y * li, g.out_bf16);
         store_out(out, ob + 2, acc.z * li, g.out_bf16);
