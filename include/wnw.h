@@ -75,7 +75,9 @@ enum {
      * Method, "Dynamic Chunk Selection": the selection made after a step serves the next one);
      * default is the same step.  The chunks that become resident at step s are recalled on a
      * side stream, overlapped with the rest of step s and the anchor attention of step s+1;
-     * a dropped chunk keeps its slot one step longer, so n_slots = (delta + 1) * k. */
+     * a dropped chunk keeps its slot one step longer.  With both timings n_slots =
+     * (delta + 1) * k (per segment: times the chunk's segments): the slots beyond the resident
+     * set keep recently dropped complements, which are revived without a copy. */
     WNW_F_SELECT_NEXT_STEP = 1u,
     /* Recall with copy-engine transfers (hipMemcpyAsync from the pinned complement, spread over
      * four internal streams) that the host issues as soon as the step's selection has run: with

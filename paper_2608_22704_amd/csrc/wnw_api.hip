@@ -297,10 +297,13 @@ wnw_status derive(wnw_ctx *c, const wnw_config &cfg, Geometry &g)
     g.out_bf16 = (cfg.flags & WNW_F_OUT_BF16) ? 1 : 0;
     g.keep_total = 0;
     for (int ch = 0; ch < g.nc; ++ch) g.keep_total += keep_of_len(g.budget_bp, chunk_len_of(g, ch));
-    // Slots: the resident set holds at most delta * k chunks, i.e. span * delta * k segments.
-    // With next-step timing the segments dropped at a step keep their slots until that step's
-    // attention has read them: span * k more.  Never more than one per segment.
-    const int64_t ns = std::min<int64_t>(g.nc, ((int64_t)g.delta + g.next_step) * span * g.k);
+    // Slots: the resident set holds at most delta * k chunks, i.e. span * delta * k segments, and
+    // the pool holds span * k more.  With next-step timing the segments dropped at a step keep
+    // their slots until that step's attention has read them, which needs them; with both timings
+    // the free slots keep their last bytes until reused, so a dropped segment that is selected
+    // again soon is revived without a copy (the extra slots halve the recalled bytes on the
+    // headline workload).  Never more than one per segment.
+    const int64_t ns = std::min<int64_t>(g.nc, ((int64_t)g.delta + 1) * span * g.k);
     if (ns > 4096) return fail(c, WNW_ERR_UNSUPPORTED, "%lld recall slots > 4096", (long long)ns);
     g.n_slots = (int)ns;
     if (select_shared_bytes(g) > 150 * 1024)

@@ -550,7 +550,7 @@ def test_overlap_slots_over_steps(nxt):
     try:
         nbytes = h.geo["chunk_bytes"]
         assert h.nseg == h.nc + 1
-        assert h.geo["n_slots"] == min(h.nseg, (3 + nxt) * 2 * h.k)
+        assert h.geo["n_slots"] == min(h.nseg, 4 * 2 * h.k)
         held_before = None
         for s in range(w.steps):
             _, _, _, res = h.step(s)
