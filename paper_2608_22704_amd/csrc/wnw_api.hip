@@ -372,8 +372,8 @@ wnw_status plan_keep(wnw_ctx *c)
 
 // Complement layout from the keep flags [B][nT + nF][T_a]: rows of every (sequence, segment,
 // tidal head) complement (comp_rows) and their sum per (sequence, segment) (seg_rows); per
-// tidal head the largest over the batch is its block stride (cfull); block offsets, slot groups
-// and partial entries follow.
+// tidal head the largest over the batch is its block stride (cfull); block offsets, kept-list
+// items and partial entries follow.
 wnw_status plan_comp(wnw_ctx *c, const uint8_t *flags)
 {
     Geometry &g = c->g;
