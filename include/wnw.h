@@ -264,7 +264,7 @@ wnw_status wnw_append_kv(wnw_ctx *ctx, const void *k_new_dev, const void *v_new_
  *   chunk_scores_dev  device fp32 [B][n_chunks]      this step's chunk scores
  *   selected_dev      device int32 [B][k]            selected chunk ids, ascending
  *   hip_stream        caller's stream (NULL = null stream); outputs are valid once it has
- *                     completed.  Buffers must stay valid until then.
+ *                     completed.  Buffers and the stream must stay valid until then.
  * The default recall path does not block the host.  With WNW_F_RECALL_MEMCPY and same-step
  * timing the call waits once, mid-step (busy polling), for the selection before issuing the
  * copies.  With WNW_F_RECALL_MEMCPY and WNW_F_SELECT_NEXT_STEP the call returns once its work is
