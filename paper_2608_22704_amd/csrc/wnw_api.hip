@@ -498,8 +498,6 @@ void parallel_for(int n, const std::function<void(int)> &fn)
     for (auto &x : th) x.join();
 }
 
-// Waits on the host for an event by polling it: a sleeping wait wakes tens to hundreds of
-// microseconds late, and with host-issued copies the link idles for that long.
 // Tag the select kernel of `step` publishes with the mirror (nonzero; steps two apart, which
 // share a mirror, differ).
 int32_t pub_tag(int64_t step)
