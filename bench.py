@@ -243,7 +243,7 @@ def main():
                     help="first run a plain 256 MiB device copy (the reference for hardware byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only: --gpus {args.gpus} is not supported by this build "
+        print(f"bench.py runs on one GPU only: --gpus {args.gpus} is not supported "
               "(the decode step is measured on one MI355X)", file=sys.stderr)
         sys.exit(2)
 

@@ -65,7 +65,7 @@ typedef enum {
     WNW_ERR_OOM = -2,          /* device or pinned host allocation failed                     */
     WNW_ERR_HIP = -3,          /* a HIP runtime call failed (context is now sticky)           */
     WNW_ERR_STATE = -4,        /* call out of order, or context in the sticky error state     */
-    WNW_ERR_UNSUPPORTED = -5   /* configuration outside what this build implements           */
+    WNW_ERR_UNSUPPORTED = -5   /* configuration outside what this library implements         */
 } wnw_status;
 
 typedef enum { WNW_ANCHOR = 0, WNW_TIDAL = 1, WNW_FIXED = 2 } wnw_role;
