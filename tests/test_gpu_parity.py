@@ -1008,3 +1008,50 @@ def test_delayed_recall_gives_identical_results(mode):
         for x, y in zip(a, b):
             assert np.array_equal(x.view(np.uint32) if x.dtype == np.float32 else x,
                                   y.view(np.uint32) if y.dtype == np.float32 else y), f"step {s} differs"
+
+
+def test_next_step_recall_paths_bit_identical():
+    """With next-step timing the copy engines (the host knows each step's list length from the
+    mirror and launches one work-group per slot item) and the copy kernel (the item count comes
+    from the select kernel, and resident work-groups loop over the items, here more than a full
+    round of them) attend to the same slot items into the same partials: outputs, scores and
+    selections are bit-identical step by step, four sequences with lists of their own lengths."""
+    import torch
+    from paper_2608_22704_amd import wnw as W
+    from tests.wnw_harness import log, to_dev
+    w = _small("recall_paths", 190, B=4, L=4, Hq=16, Hkv=8, Ta=8000, Tt=40, cl=32, budget=2000, steps=16)
+    log("[case] next-step recall paths, bit for bit")
+    B, L, H, D = w.batch, w.layers, w.kv_heads, w.head_dim
+    seqs = [gen.sequence(w, b) for b in range(B)]
+    kd = torch.stack([to_dev(sq["k"]) for sq in seqs])
+    vd = torch.stack([to_dev(sq["v"]) for sq in seqs])
+    qd = torch.stack([to_dev(np.stack([sq["q"][s] for sq in seqs])) for s in range(w.steps)])
+    prefill = np.stack([sq["prefill"] for sq in seqs])
+    runs, items = [], []
+    for flags in (W.WNW_F_SELECT_NEXT_STEP | W.WNW_F_RECALL_MEMCPY, W.WNW_F_SELECT_NEXT_STEP):
+        cfg = W.make_config(B, L, w.q_heads, H, w.audio_len, w.text_len, w.chunk_len, w.budget_bp, flags=flags)
+        ctx = W.wnw_init_cache(cfg, kd, vd)
+        try:
+            W.wnw_set_roles(ctx, gen.roles(w), prefill)
+            geo = W.wnw_query_geometry(ctx)
+            out = torch.empty((B, L, w.q_heads, D), dtype=torch.float32, device="cuda")
+            sc = torch.empty((B, geo["n_chunks"]), dtype=torch.float32, device="cuda")
+            sel = torch.empty((B, geo["k"]), dtype=torch.int32, device="cuda")
+            kept = []
+            for s in range(w.steps):
+                W.wnw_decode_step(ctx, qd[s], out, sc, sel)
+                kept.append((out.clone(), sc.clone(), sel.clone()))
+            torch.cuda.synchronize()
+            st = W.wnw_get_stats(ctx)
+            assert st["recalled_chunks"] > geo["n_slots"], "the slot pool was not wrapped"
+            # complement rows attended per step and tidal head, in 128-row items
+            items.append(st["slot_rows"] / w.steps / B / w.n_tidal / 128.0)
+            runs.append([[x.cpu().numpy() for x in step] for step in kept])
+        finally:
+            W.wnw_destroy(ctx)
+    # more slot items per step than 1 024 resident work-groups take in one round
+    assert items[0] * w.n_tidal * B > 1024, items
+    for s, (a, b) in enumerate(zip(*runs)):
+        for x, y in zip(a, b):
+            assert np.array_equal(x.view(np.uint32) if x.dtype == np.float32 else x,
+                                  y.view(np.uint32) if y.dtype == np.float32 else y), f"step {s} differs"
