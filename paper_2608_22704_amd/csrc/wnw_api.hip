@@ -50,6 +50,11 @@ enum State { CREATED = 0, READY = 1, FAILED = 2 };
 // stream leave a gap between transfers (3 MB copies reach ~49 of ~57 GB/s on one stream, ~56
 // on four).
 constexpr int N_COPY_STREAMS = 4;
+// Next-step timing with host-issued copies: the largest previous-step recall behind which the
+// selection still joins the tidal/fixed launch.  4 MiB take ~80 us over the host link (~50 GB/s
+// measured), less than the attention launch that precedes the wait for them on the headline
+// cache (~96 us), so the selection does not wait.
+constexpr int64_t SEL_IN_TIDAL_BYTES = 4ll << 20;
 
 struct StepEvents {
     hipEvent_t e[7];
@@ -753,7 +758,7 @@ void free_all(wnw_ctx *c)
                     c->scores_int, c->sel_int,
                     c->s.pa_m, c->s.pa_l, c->s.pa_o, c->s.pa_mass, c->s.mass, c->s.a_stat, c->s.ps_m, c->s.ps_l, c->s.ps_o,
                     c->s.streak, c->s.slot_of, c->s.slot_last, c->s.att, c->s.slot_data, c->s.slot_busy, c->s.slot_since,
-                    c->s.step, c->s.kept_list, c->s.new_list, c->s.counts, c->s.items, c->s.stats};
+                    c->s.step, c->s.kept_list, c->s.new_list, c->s.counts, c->s.arrive, c->s.stats};
     for (void *p : ptrs)
         if (p) (void)hipFree(p);
     if (c->host_comp) (void)hipHostFree(c->host_comp);
@@ -901,7 +906,7 @@ wnw_status build_tiers(wnw_ctx *c, const uint8_t *keep_all)
     ALLOC(s.kept_list, 2 * B * g.n_slots * 2, "kept lists");   // two of each, alternating by step
     ALLOC(s.new_list, 2 * B * g.knew * 2, "new lists");
     ALLOC(s.counts, 2 * B * 2, "counts");
-    ALLOC(s.items, 4, "list items");
+    ALLOC(s.arrive, B, "arrival counters");
     ALLOC(s.stats, 8, "stats");
 #undef ALLOC
     const size_t host_bytes = B * g.nc * (size_t)g.chunk_elems * sizeof(uint16_t);
@@ -1080,7 +1085,7 @@ wnw_status build_tiers(wnw_ctx *c, const uint8_t *keep_all)
     }
     HIPCHECK(c, hipMemset(s.step, 0, B * sizeof(int32_t)));
     HIPCHECK(c, hipMemset(s.counts, 0, 2 * B * 2 * sizeof(int32_t)));
-    HIPCHECK(c, hipMemset(s.items, 0, 4 * sizeof(int32_t)));
+    HIPCHECK(c, hipMemset(s.arrive, 0, B * sizeof(int32_t)));
     HIPCHECK(c, hipMemset(s.stats, 0, 8 * sizeof(unsigned long long)));
     HIPCHECK(c, hipDeviceSynchronize());
     c->full_k = c->full_v = nullptr;
@@ -1294,30 +1299,48 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, void *out, float *scor
         b.counts += (size_t)i * g.B * 2;
         b.new_list += (size_t)i * g.B * g.knew * 2;
         b.kept_list += (size_t)i * g.B * g.n_slots * 2;
-        b.items = g.next_step ? c->s.items + 2 * i : nullptr;
-        b.items_clear = nullptr;
+        b.arrive = nullptr;
         return b;
     };
     StepBuffers sb = lists_of(c->s, par);                         // what this step reads
     StepBuffers sn = g.next_step ? lists_of(c->s, nxt) : sb;      // what its select kernel writes
-    if (g.next_step) sb.items_clear = sn.items;                   // zeroed before the select kernel
 
     // (1) anchor attention + chunk mass, (2) scores, top-k and residency.  With next-step
     // timing the static tidal/fixed tiles (kept rows + text) join the anchor launch.
     // markers 0 and 1 are the first launch's own start and end (its dispatch excluded)
     hipEvent_t e0 = timing ? ev.e[0] : nullptr, e1 = timing ? ev.e[1] : nullptr;
-    if (g.next_step)
-        HIPCHECK(c, launch_attention(g, c->t, sb, q, s0, e0, e1));
-    else
-        HIPCHECK(c, launch_anchor(g, c->t, sb, q, s0, e0, e1));
-    HIPCHECK(c, launch_anchor_mass(g, sb, s0));
     const bool memcpy_path = c->cfg.flags & WNW_F_RECALL_MEMCPY;
-    // host-issued copies: the select kernel also writes the counts and new lists to mapped pinned
+    // host-issued copies: the selection also writes the counts and new lists to mapped pinned
     // memory (one mirror per step parity) and then publishes a tag there, so the host reads them
     // once the selection is done, never behind copies still running on the side streams
     sn.pub = memcpy_path ? c->d_newinfo + (size_t)par * c->mirror_ints : nullptr;
     sn.pub_tag = pub_tag(c->steps);
-    HIPCHECK(c, launch_select(g, sn, sc, c->override_sel, sel, s0));
+    if (g.next_step)
+        HIPCHECK(c, launch_attention(g, c->t, sb, q, s0, e0, e1));
+    else
+        HIPCHECK(c, launch_anchor(g, c->t, sb, q, s0, e0, e1));
+    // Next-step timing with host-issued copies: the chunk-mass merge and the selection run inside
+    // the tidal/fixed launch (its first work-groups, beside the slot items) when the previous
+    // step recalled little.  That launch waits for the previous step's copies, and so would the
+    // selection; a small recall has landed by then (SEL_IN_TIDAL_BYTES), while a large one keeps
+    // the selection ahead of the wait, so that this step's copies queue behind the previous
+    // step's and the link stays busy.  The host reads the previous step's recall size from its
+    // mirror once the recall thread has issued it (the attention launch runs meanwhile).
+    bool sel_in_tidal = false;
+    if (g.next_step && memcpy_path && tidal_select_fits(g)) {
+        int64_t prev_bytes = 0;
+        if (c->rec_pending) {
+            wnw_status r = recall_wait_issued(c, (int64_t)c->steps - 1);
+            if (r != WNW_OK) return r;
+            const int32_t *cnt = c->h_newinfo + (size_t)nxt * c->mirror_ints;
+            for (int b = 0; b < g.B; ++b) prev_bytes += (int64_t)cnt[b * 2 + 1] * g.chunk_elems * (int64_t)sizeof(uint16_t);
+        }
+        sel_in_tidal = prev_bytes <= SEL_IN_TIDAL_BYTES;
+    }
+    if (!sel_in_tidal) {
+        HIPCHECK(c, launch_anchor_mass(g, sb, s0));
+        HIPCHECK(c, launch_select(g, sn, sc, c->override_sel, sel, s0));
+    }
     MARK(6);
     // the copy kernel of the next-step recall follows the selection on the device (an event; the
     // host-issued copies follow the published tag instead)
@@ -1356,8 +1379,16 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, void *out, float *scor
             items = ((long long)nmax * g.comp_max + TILE_S - 1) / TILE_S;
         }
         // markers 2 and 3: the launch's own start and end
+        SelectArgs sa{};
+        if (sel_in_tidal) {
+            sa.s = sn;
+            sa.s.arrive = c->s.arrive;
+            sa.scores = sc;
+            sa.ovr = c->override_sel;
+            sa.selected = sel;
+        }
         HIPCHECK(c, launch_tidal_fixed(g, c->t, sb, q, false, false, items, s0, timing ? ev.e[2] : nullptr,
-                                       timing ? ev.e[3] : nullptr));
+                                       timing ? ev.e[3] : nullptr, sel_in_tidal ? &sa : nullptr));
         // the final merge is queued before the host waits for the selection below, so that the
         // device never idles behind that wait
         HIPCHECK(c, launch_subset_combine(g, c->t, sb, out, s0));

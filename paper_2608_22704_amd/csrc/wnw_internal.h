@@ -12,7 +12,7 @@ constexpr int TILE_A = 128;     // anchor key rows per work-group
 constexpr int TILE_S = 128;     // tidal/fixed kept rows per work-group (slot groups: 128 or 256)
 constexpr int MAX_CHUNK = 256;  // longest chunk the slot kernels handle
 constexpr int SEL_THREADS = 1024;
-constexpr int SCORE_PARTS = 4;   // fixed ranges of anchor q-heads summed per chunk score
+constexpr int SCORE_PARTS = 4;   // fixed ranges of anchor KV-heads summed per segment mass
 
 // Everything the kernels need to know about the cache and the step, fixed at set-up.
 struct Geometry {
@@ -122,11 +122,8 @@ struct StepBuffers {
     int32_t *kept_list;         // [B][n_slots][2] (segment, slot | full-stride bit 30)
     int32_t *new_list;          // [B][knew][2]    (segment, slot)
     int32_t *counts;            // [B][2] kept-list entries (next-step timing: kept + new), new
-    int32_t *items;             // [2] most kept items, unused (TILE_S-row pieces of one head's listed
-                                // complements) over the sequences: written by the select kernel
-                                // (next-step timing), read by the next step's launches; else null
-    int32_t *items_clear;       // [2] the other step's items, zeroed by the attention launch for the
-                                // select kernel that follows it; else null
+    int32_t *arrive;            // [B] the selection in the tidal/fixed launch: anchor heads whose chunk
+                                // masses are merged, per sequence (zero between launches); else null
     int32_t *pub;               // host-issued recall: mapped pinned mirror of counts [B][2], new
                                 // lists [B][knew][2] and publication tags [B], written by the select
                                 // kernel; else null
@@ -137,6 +134,16 @@ struct StepBuffers {
     int32_t *exhausted;         // mapped pinned flag, set to 1 by a step that found no free slot for a
                                 // newly resident segment (the host fails the context on it)
     const int32_t *seg_rows;    // [B][nc] complement rows of a segment over the tidal heads
+};
+
+// The selection as part of the next-step tidal/fixed launch: the select kernel's arguments, s
+// with the lists the selection writes and the arrival counters.
+struct SelectArgs {
+    StepBuffers s;
+    float *scores;
+    const int32_t *ovr;
+    int32_t *selected;
+    int n_mass;                 // work-groups that merge chunk masses (set by the launcher)
 };
 
 // Launchers (wnw_kernels.hip).  Each returns the launch status.  Where a launcher takes two
@@ -153,7 +160,7 @@ hipError_t launch_select(const Geometry &g, const StepBuffers &s, float *scores,
 // Shared memory of the select kernel (bounded at set-up).
 inline size_t select_shared_bytes(const Geometry &g)
 {
-    return (size_t)g.nc * (SCORE_PARTS * 8 + 4 + 11 * 4) + (size_t)g.n_slots * 6 * 4 + 3 * (size_t)((g.nc + 63) / 64) * 4;
+    return (size_t)g.nc * (3 * 8 + 4 + 11 * 4) + (size_t)g.n_slots * 6 * 4 + 3 * (size_t)((g.nc + 63) / 64) * 4;
 }
 // Fixed heads (with `with_static`), tidal kept rows and the tidal complements already in their
 // slots; with `recall`
@@ -161,10 +168,15 @@ inline size_t select_shared_bytes(const Geometry &g)
 // memory into their slots and the attention over them.
 // The slot tiles are the kept list's items (after the static tiles when with_static); `items`:
 // the most items of any head this step when the host knows it (the kernel's own count from the
-// select kernel then agrees), else -1.
+// list counts then agrees), else -1.
+// With sel (next-step timing, no recall in the launch), the launch also merges the anchor heads'
+// chunk masses and runs the selection, in place of launch_anchor_mass and launch_select (which
+// needs tidal_select_fits(g)).
 hipError_t launch_tidal_fixed(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, bool recall,
                               bool with_static, long long items, hipStream_t st, hipEvent_t e0 = nullptr,
-                              hipEvent_t e1 = nullptr);
+                              hipEvent_t e1 = nullptr, const SelectArgs *sel = nullptr);
+// Whether the tidal/fixed launch's shared memory holds the mass merge and the selection of g.
+bool tidal_select_fits(const Geometry &g);
 // Anchor attention + chunk mass together with the static tidal/fixed tiles (next-step timing).
 hipError_t launch_attention(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st,
                             hipEvent_t e0, hipEvent_t e1);

@@ -202,6 +202,19 @@ __device__ inline int lane_id_opaque()
 }
 
 // Shared memory of one anchor tile.
+// Values that pass between work-groups of one launch (tile partials to the chunk-mass merge, and
+// masses to the selection, see last_arrival) are stored and loaded as agent-scope relaxed
+// atomics: coherent across the dies' caches with no cache write-back or invalidation, which an
+// agent-scope fence would cost every work-group.
+__device__ inline void st_agent(double *p, double v)
+{
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline double ld_agent(const double *p)
+{
+    return __hip_atomic_load(const_cast<double *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 template <int G>
 struct AnchorSmem {
     static constexpr int RW = TILE_A / WAVES;
@@ -378,8 +391,8 @@ __device__ inline void anchor_tile(const Geometry &g, const Tiers &t, const Step
         for (int w = 1; w < WAVES; ++w) M = fmax(M, wm[w * G + tid]);
 #pragma unroll
         for (int w = 0; w < WAVES; ++w) L += wl[w * G + tid];
-        s.pa_m[pidx * G + tid] = M;
-        s.pa_l[pidx * G + tid] = L;
+        st_agent(&s.pa_m[pidx * G + tid], M);
+        st_agent(&s.pa_l[pidx * G + tid], L);
     }
     for (int idx = tid; idx < G * D; idx += NT) {
         float o = 0.f;
@@ -401,7 +414,7 @@ __device__ inline void anchor_tile(const Geometry &g, const Tiers &t, const Step
                 const int r0 = t0 + w * RW;
                 if (r0 >= c * g.cl && r0 < (c + 1) * g.cl && r0 < g.Ta) acc2 += wl[w * G + h];
             }
-            s.pa_mass[pidx * G * g.maxc + tid] = acc2;
+            st_agent(&s.pa_mass[pidx * G * g.maxc + tid], acc2);
         }
         return;
     }
@@ -417,7 +430,7 @@ __device__ inline void anchor_tile(const Geometry &g, const Tiers &t, const Step
             for (int rr = r0 + k; rr < r1; rr += 16) acc2 += xs[h * TILE_A + (rr - t0)];
         }
         acc2 = sum16(acc2);
-        if (valid && k == 0) s.pa_mass[pidx * G * g.maxc + grp] = acc2;
+        if (valid && k == 0) st_agent(&s.pa_mass[pidx * G * g.maxc + grp], acc2);
     }
 }
 
@@ -469,13 +482,23 @@ constexpr int MASS_THREADS = 256;
 // the log-sum-exp normalisers of its G q-heads from the tile partials, kept for the output merge
 // (anchor_out_merge, in the final launch), and the normalised per-chunk softmax mass of Eq. 2
 // summed over the G q-heads in order, all in double.
+// Shared memory of anchor_mass_head besides fac[G][n_tiles_a].
 template <int G>
-__global__ __launch_bounds__(MASS_THREADS) void anchor_mass_kernel(Geometry g, StepBuffers s)
+struct MassSmem {
+    double red[MASS_THREADS / 64][G];
+    double inv_l[G];
+};
+
+// One anchor KV-head ai of sequence b, MASS_THREADS threads; fac: [G][n_tiles_a] doubles of
+// shared memory.
+static_assert(MASS_THREADS == NT, "the attention launch's work-groups merge the chunk masses");
+template <int G>
+__device__ inline void anchor_mass_head(const Geometry &g, const StepBuffers &s, int ai, int b, double *fac,
+                                        MassSmem<G> &ms)
 {
-    const int ai = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
-    extern __shared__ double fac[];      // [G][n_tiles_a]
-    __shared__ double red[MASS_THREADS / 64][G];
-    __shared__ double inv_l[G];
+    const int tid = threadIdx.x;
+    auto &red = ms.red;
+    double *inv_l = ms.inv_l;
     const int nt = g.n_tiles_a;
     const size_t base = ((size_t)b * g.nA + ai) * nt;
     // a segment of at most MAX_CHUNK positions spans at most MAXT tiles
@@ -488,14 +511,14 @@ __global__ __launch_bounds__(MASS_THREADS) void anchor_mass_kernel(Geometry g, S
     const int t_hi0 = c0 < g.nc ? (min((c0 + 1) * g.cl, g.Ta) - 1) / TILE_A : -1;
 #pragma unroll
     for (int h = 0; h < G; ++h) {
-        pm[h] = tid < nt ? s.pa_m[(base + tid) * G + h] : -INFINITY;
-        pl[h] = tid < nt ? s.pa_l[(base + tid) * G + h] : 0.0;
+        pm[h] = tid < nt ? ld_agent(&s.pa_m[(base + tid) * G + h]) : -INFINITY;
+        pl[h] = tid < nt ? ld_agent(&s.pa_l[(base + tid) * G + h]) : 0.0;
     }
 #pragma unroll
     for (int u = 0; u < MAXT; ++u) {
         const int i = t_lo0 + u, j = c0 - (i * TILE_A) / g.cl;
 #pragma unroll
-        for (int h = 0; h < G; ++h) v[h][u] = i <= t_hi0 ? s.pa_mass[((base + i) * G + h) * g.maxc + j] : 0.0;
+        for (int h = 0; h < G; ++h) v[h][u] = i <= t_hi0 ? ld_agent(&s.pa_mass[((base + i) * G + h) * g.maxc + j]) : 0.0;
     }
     double m[G], l[G];
 #pragma unroll
@@ -506,7 +529,7 @@ __global__ __launch_bounds__(MASS_THREADS) void anchor_mass_kernel(Geometry g, S
     for (int i = tid + MASS_THREADS; i < nt; i += MASS_THREADS)
 #pragma unroll
         for (int h = 0; h < G; ++h) {
-            const double x = s.pa_m[(base + i) * G + h];
+            const double x = ld_agent(&s.pa_m[(base + i) * G + h]);
             fac[h * nt + i] = x;
             m[h] = fmax(m[h], x);
         }
@@ -526,7 +549,7 @@ __global__ __launch_bounds__(MASS_THREADS) void anchor_mass_kernel(Geometry g, S
             const double mi = fac[h * nt + i];
             const double f = (m[h] > -INFINITY && mi > -INFINITY) ? exp(mi - m[h]) : 0.0;
             fac[h * nt + i] = f;
-            l[h] += s.pa_l[(base + i) * G + h] * f;
+            l[h] += ld_agent(&s.pa_l[(base + i) * G + h]) * f;
         }
     block_reduce_g<G, MASS_THREADS>(l, false, red);   // also publishes fac[]
     if (tid < G) {
@@ -548,7 +571,7 @@ __global__ __launch_bounds__(MASS_THREADS) void anchor_mass_kernel(Geometry g, S
             for (int u = 0; u < MAXT; ++u) {
                 const int i = t_lo + u, j = c - (i * TILE_A) / g.cl;
 #pragma unroll
-                for (int h = 0; h < G; ++h) v[h][u] = i <= t_hi ? s.pa_mass[((base + i) * G + h) * g.maxc + j] : 0.0;
+                for (int h = 0; h < G; ++h) v[h][u] = i <= t_hi ? ld_agent(&s.pa_mass[((base + i) * G + h) * g.maxc + j]) : 0.0;
             }
         }
         double acc = 0.0;
@@ -560,8 +583,16 @@ __global__ __launch_bounds__(MASS_THREADS) void anchor_mass_kernel(Geometry g, S
                 if (t_lo + u <= t_hi) a += v[h][u] * fac[h * nt + t_lo + u];
             acc += a * inv_l[h];
         }
-        mass[c] = acc;
+        st_agent(&mass[c], acc);
     }
+}
+
+template <int G>
+__global__ __launch_bounds__(MASS_THREADS) void anchor_mass_kernel(Geometry g, StepBuffers s)
+{
+    extern __shared__ double fac[];      // [G][n_tiles_a]
+    __shared__ MassSmem<G> ms;
+    anchor_mass_head<G>(g, s, blockIdx.x, blockIdx.y, fac, ms);
 }
 
 // Output rows of one anchor KV-head's G q-heads from the tile partials and the normalisers
@@ -641,6 +672,13 @@ __device__ inline void lds_barrier()
     __asm__ volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
+// Counters of select_seq in shared memory (and a flag of last_arrival).
+struct SelectShared {
+    int ndrop, nrows, nrev, nfree, nkrows;
+    int last;
+};
+
+
 // Per sequence b (state staged in shared memory, written back at the end).  Chunks (nchk) are
 // the selection's candidates; segments (nc) are the unit of masses, residency, slots and
 // recall.  With disjoint chunks a chunk is a segment; with overlapping chunks chunk c is
@@ -660,18 +698,19 @@ __device__ inline void lds_barrier()
 //   lists    kept list = attended with bytes already on the device; new list = to recall
 //            (attended in the same launch with same-step timing; with next-step timing the new
 //            segments also follow the kept ones in the kept list, which the next step attends)
-__global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuffers s, float *__restrict__ scores,
-                                                             const int32_t *__restrict__ ovr, int32_t *__restrict__ selected)
+// Any number of threads (blockDim.x, a multiple of 64); sdyn: select_shared_bytes(g) bytes of
+// shared memory.
+__device__ inline void select_seq(const Geometry &g, const StepBuffers &s, float *__restrict__ scores,
+                                  const int32_t *__restrict__ ovr, int32_t *__restrict__ selected, int b, double *sdyn,
+                                  SelectShared &sh)
 {
-    const int b = blockIdx.x, tid = threadIdx.x, nthr = blockDim.x;
+    const int tid = threadIdx.x, nthr = blockDim.x;
     const int nu = g.nc, nk = g.nchk, k = g.k, ns = g.n_slots, naq = g.nA;   // mass rows: one per anchor KV-head
     const bool nxt = g.next_step, two = g.span == 2;
-    extern __shared__ double sdyn[];
-    double *part = sdyn;                              // [SCORE_PARTS][nu]; row 0 then segment sums
-    unsigned long long *ckey = (unsigned long long *)(part + nu);       // [nk] in row 1: ranking keys
-    unsigned long long *fkey = (unsigned long long *)(part + 2 * nu);   // [ns] in row 2: free-slot keys
-    static_assert(SCORE_PARTS >= 3, "rows 1 and 2 of the score partials hold the ranking keys");
-    float *sc = (float *)(part + SCORE_PARTS * nu);   // [nk] chunk scores
+    double *part = sdyn;                              // [nu] segment mass sums
+    unsigned long long *ckey = (unsigned long long *)(part + nu);       // [nk] ranking keys
+    unsigned long long *fkey = (unsigned long long *)(part + 2 * nu);   // [ns] free-slot keys
+    float *sc = (float *)(part + 3 * nu);             // [nk] chunk scores
     int *fsel = (int *)(sc + nu);                     // [nk] selected
     int *st = fsel + nu;                              // [nk] streak
     int *sof = st + nu;                               // [nu] slot of the segment or -1
@@ -690,7 +729,7 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
     int *rank_k = srows + nu;                         // [nu] rank of a kept segment
     int *rank_n = rank_k + nu;                        // [nu] rank of a new segment
     int *bcnt = rank_n + nu;                          // [3][ceil(nu / 64)] flags set per 64-entry block
-    __shared__ int ndrop, nrows, nrev, nfree, nkrows;
+    int &ndrop = sh.ndrop, &nrows = sh.nrows, &nrev = sh.nrev, &nfree = sh.nfree, &nkrows = sh.nkrows;
 
     int32_t *g_streak = s.streak + (size_t)b * nk, *g_slot_of = s.slot_of + (size_t)b * nu;
     int32_t *g_slot_last = s.slot_last + (size_t)b * nu;
@@ -699,46 +738,74 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
     int32_t *g_since = s.slot_since + (size_t)b * ns;
     const int step = s.step[b];
 
-    // state in, segment masses: in each round every load is issued before any store to shared
-    // memory (one memory round trip per round; one round while the arrays fit the work-group)
-    const int n_in = max(max(nk, nu), max(ns, SCORE_PARTS * nu));
-    for (int i0 = 0; i0 < n_in; i0 += nthr) {
-        const int i = i0 + tid;
-        const int v_st = i < nk ? g_streak[i] : 0;
-        const int v_sof = i < nu ? g_slot_of[i] : 0, v_slast = i < nu ? g_slot_last[i] : 0;
-        const int v_rows = i < nu ? s.seg_rows[(size_t)b * nu + i] : 0;
-        const int v_busy = i < ns ? g_busy[i] : 0, v_data = i < ns ? g_data[i] : 0, v_since = i < ns ? g_since[i] : 0;
-        double acc = 0.0;
-        if (i < SCORE_PARTS * nu) {
-            const int p = i / nu, u = i - p * nu;
-            const int a0 = p * naq / SCORE_PARTS, a1 = (p + 1) * naq / SCORE_PARTS;
-            const double *m = s.mass + ((size_t)b * naq + a0) * nu + u;
-#pragma unroll 8
-            for (int a = a0; a < a1; ++a) acc += m[(size_t)(a - a0) * nu];
-            part[i] = acc;
+    // state in: every load of up to IN_ROUNDS rounds of the work-group is issued before any store
+    // to shared memory (one memory round trip while the arrays fit)
+    constexpr int IN_ROUNDS = 4;
+    const int n_in = max(max(nk, nu), ns);
+    for (int i00 = 0; i00 < n_in; i00 += IN_ROUNDS * nthr) {
+        int v_st[IN_ROUNDS], v_sof[IN_ROUNDS], v_slast[IN_ROUNDS], v_rows[IN_ROUNDS];
+        int v_busy[IN_ROUNDS], v_data[IN_ROUNDS], v_since[IN_ROUNDS];
+#pragma unroll
+        for (int r = 0; r < IN_ROUNDS; ++r) {
+            const int i = i00 + r * nthr + tid;
+            v_st[r] = i < nk ? g_streak[i] : 0;
+            v_sof[r] = i < nu ? g_slot_of[i] : 0;
+            v_slast[r] = i < nu ? g_slot_last[i] : 0;
+            v_rows[r] = i < nu ? s.seg_rows[(size_t)b * nu + i] : 0;
+            v_busy[r] = i < ns ? g_busy[i] : 0;
+            v_data[r] = i < ns ? g_data[i] : 0;
+            v_since[r] = i < ns ? g_since[i] : 0;
         }
-        if (i < nk) {
-            st[i] = v_st;
-            fsel[i] = 0;
+#pragma unroll
+        for (int r = 0; r < IN_ROUNDS; ++r) {
+            const int i = i00 + r * nthr + tid;
+            if (i < nk) {
+                st[i] = v_st[r];
+                fsel[i] = 0;
+            }
+            if (i < nu) {
+                sof[i] = v_sof[r];
+                slast[i] = v_slast[r];
+                srows[i] = v_rows[r];
+            }
+            if (i < ns) {
+                busy[i] = v_busy[r] == 2 ? 0 : v_busy[r];   // frees deferred by the previous step
+                sdata[i] = v_data[r];
+                since[i] = v_since[r];
+            }
         }
-        if (i < nu) {
-            sof[i] = v_sof;
-            slast[i] = v_slast;
-            srows[i] = v_rows;
+    }
+    // segment masses: the anchor heads' masses of a segment summed over SCORE_PARTS fixed ranges
+    // of heads, each in head order, then the ranges' sums in order.  A thread's loads are issued
+    // MB at a time before any is added.
+    constexpr int MB = 16;
+    for (int u = tid; u < nu; u += nthr) {
+        const double *m = s.mass + (size_t)b * naq * nu + u;
+        double tot = 0.0, acc = 0.0;
+        int p = 0, pend = naq / SCORE_PARTS;   // the range being summed and its end
+        for (int a = 0; a < naq; a += MB) {
+            double v[MB];
+#pragma unroll
+            for (int e = 0; e < MB; ++e) v[e] = a + e < naq ? ld_agent(m + (size_t)(a + e) * nu) : 0.0;
+#pragma unroll
+            for (int e = 0; e < MB; ++e) {
+                if (a + e >= naq) break;
+                while (a + e >= pend) {   // the range ends (ranges are empty when naq < SCORE_PARTS)
+                    tot = p == 0 ? acc : tot + acc;
+                    acc = 0.0;
+                    ++p;
+                    pend = (p + 1) * naq / SCORE_PARTS;
+                }
+                acc += v[e];
+            }
         }
-        if (i < ns) {
-            busy[i] = v_busy == 2 ? 0 : v_busy;       // frees deferred by the previous step
-            sdata[i] = v_data;
-            since[i] = v_since;
+        for (; p < SCORE_PARTS; ++p) {
+            tot = p == 0 ? acc : tot + acc;
+            acc = 0.0;
         }
+        part[u] = tot;
     }
     if (tid == 0) ndrop = nrows = nrev = nfree = nkrows = 0;
-    lds_barrier();
-    for (int u = tid; u < nu; u += nthr) {
-        double acc = part[u];
-        for (int p = 1; p < SCORE_PARTS; ++p) acc += part[p * nu + u];
-        part[u] = acc;                                // each thread rewrites only its own segment
-    }
     lds_barrier();
     for (int c = tid; c < nk; c += nthr) {
         const bool pair = two && c + 1 < nu;
@@ -974,11 +1041,6 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
             s.pub[b * 2] = nlist;
             s.pub[b * 2 + 1] = nn;
         }
-        if (s.items) {
-            // items (TILE_S-row pieces of one head's listed complements) of the kept list, the
-            // most over the sequences: the next step's tidal launch sizes its work from it
-            atomicMax(&s.items[0], (int)(((long long)nlist * g.comp_max + TILE_S - 1) / TILE_S));
-        }
         s.step[b] = step + 1;
         atomicAdd(&s.stats[0], (unsigned long long)nn);
         atomicAdd(&s.stats[1], (unsigned long long)ndrop);
@@ -1012,6 +1074,14 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuf
                                __HIP_MEMORY_SCOPE_SYSTEM);
         }
     }
+}
+
+__global__ __launch_bounds__(SEL_THREADS) void select_kernel(Geometry g, StepBuffers s, float *__restrict__ scores,
+                                                             const int32_t *__restrict__ ovr, int32_t *__restrict__ selected)
+{
+    extern __shared__ double sdyn[];
+    __shared__ SelectShared sh;
+    select_seq(g, s, scores, ovr, selected, blockIdx.x, sdyn, sh);
 }
 
 // -------------------------------------------------------------------------------------------
@@ -1519,6 +1589,30 @@ __device__ inline void recall_units(const Geometry &g, const Tiers &t, const Ste
     }
 }
 
+constexpr int SEL_SHARED_OFF = 512;   // bytes of counters before the mass or selection arrays
+
+// True in every thread of the work-group that arrives last of n at the counter *cnt (an
+// agent-scope atomic), which that work-group resets for the next launch.  The values passed on
+// are agent-scope atomic stores (st_agent) that every wavefront waits to complete before the
+// work-group counts itself in (a work-group barrier alone does not wait for global stores); the
+// last work-group reads them with agent-scope atomic loads (ld_agent) after the count.
+__device__ inline bool last_arrival(int32_t *cnt, int n, SelectShared &sh)
+{
+    __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const int old = atomicAdd(cnt, 1);
+        sh.last = old == n - 1;
+        if (old == n - 1) atomicExch(cnt, 0);
+    }
+    __syncthreads();
+    return sh.last;
+}
+
+// Anchor tiles and the static tidal/fixed tiles (kept rows + text, which no selection changes)
+// in one launch, interleaved along the grid: the anchor tiles' arithmetic (fp64 logits)
+// overlaps the static tiles' streaming.  Used with next-step timing, where the static tiles need
+// not wait for this step's selection.
 // Fixed heads, tidal kept rows and tidal complements already in their slots: static tiles
 // first (unless the attention launch ran them), then the items of one list (list_item).  The
 // work-groups loop over those tiles with the grid's stride, so the launch holds about as many
@@ -1526,9 +1620,13 @@ __device__ inline void recall_units(const Geometry &g, const Tiers &t, const Ste
 // this step does not have.  With REC (same-step timing), the first RECALL_WGS work-groups copy
 // the complements listed for recall from mapped pinned memory into their slots and attend to
 // them: the step is bound by the host link then, and the copies start with the launch.
+// With sel.n_mass (next-step timing, sel.s.arrive set), the first n_mass = nA * B work-groups
+// merge the anchor heads' chunk masses of this step's attention launch, one head each, and the
+// last of a sequence's heads to finish runs the sequence's selection (sel.s: the lists it
+// writes, which this launch does not read; the items read the lists of s).
 template <int G, int RPLK, bool REC>
 __global__ __launch_bounds__(NT, REC ? (RPLK == RPL_S ? 2 : 1) : (G <= 4 ? 4 : G <= 6 ? 3 : 2)) void tidal_fixed_kernel(
-    Geometry g, Tiers t, StepBuffers s, const uint16_t *__restrict__ q, int with_static)
+    Geometry g, Tiers t, StepBuffers s, const uint16_t *__restrict__ q, int with_static, SelectArgs sel)
 {
     union Smem {
         SubsetSmem<G, RPL_S> st;
@@ -1536,6 +1634,18 @@ __global__ __launch_bounds__(NT, REC ? (RPLK == RPL_S ? 2 : 1) : (G <= 4 ? 4 : G
     };
     __shared__ Smem sm;   // one block for whichever path this work-group runs
     int w = blockIdx.x, nw = gridDim.x;
+    if (w < sel.n_mass) {
+        const int ai = w % g.nA, b = w / g.nA;
+        char *base = (char *)&sm;
+        SelectShared &sh = *(SelectShared *)base;
+        static_assert(sizeof(SelectShared) + sizeof(MassSmem<G>) <= SEL_SHARED_OFF, "counters before the arrays");
+        anchor_mass_head<G>(g, sel.s, ai, b, (double *)(base + SEL_SHARED_OFF), *(MassSmem<G> *)(base + sizeof(SelectShared)));
+        if (last_arrival(sel.s.arrive + b, g.nA, sh))
+            select_seq(g, sel.s, sel.scores, sel.ovr, sel.selected, b, (double *)(base + SEL_SHARED_OFF), sh);
+        return;
+    }
+    w -= sel.n_mass;
+    nw -= sel.n_mass;
     if constexpr (REC) {
         if (w < RECALL_WGS) {
             recall_units<G, RPLK>(g, t, s, q, w, RECALL_WGS, sm.sl);
@@ -1548,15 +1658,9 @@ __global__ __launch_bounds__(NT, REC ? (RPLK == RPL_S ? 2 : 1) : (G <= 4 ? 4 : G
     // kept-list items in item-major order over (sequence, tidal head); the loop ends after the
     // last item any head has this step (a head with fewer returns at once from the ones past its
     // own)
-    long long n_items;
-    if (s.items) {
-        n_items = s.items[0];
-    } else {
-        int kmax = 0;
-        for (int b = 0; b < g.B; ++b) kmax = max(kmax, s.counts[b * 2]);
-        n_items = ((long long)kmax * g.comp_max + TILE_S - 1) / TILE_S;
-    }
-    n_items = min(n_items, (long long)g.ng_kept);
+    int kmax = 0;
+    for (int b = 0; b < g.B; ++b) kmax = max(kmax, s.counts[b * 2]);
+    const long long n_items = min(((long long)kmax * g.comp_max + TILE_S - 1) / TILE_S, (long long)g.ng_kept);
     const long long nh = (long long)g.nT * g.B, total = n_static + n_items * nh;
     for (long long it = w; it < total; it += nw) {
         if (it < n_static) {
@@ -1568,10 +1672,6 @@ __global__ __launch_bounds__(NT, REC ? (RPLK == RPL_S ? 2 : 1) : (G <= 4 ? 4 : G
     }
 }
 
-// Anchor tiles and the static tidal/fixed tiles (kept rows + text, which no selection changes)
-// in one launch, interleaved along the grid: the anchor tiles' arithmetic (fp64 logits)
-// overlaps the static tiles' streaming.  Used with next-step timing, where the static tiles need
-// not wait for this step's selection.
 template <int G>
 __global__ __launch_bounds__(NT, G <= 4 ? 4 : 2) void attention_kernel(Geometry g, Tiers t, StepBuffers s,
                                                                        const uint16_t *__restrict__ q)
@@ -1583,7 +1683,6 @@ __global__ __launch_bounds__(NT, G <= 4 ? 4 : 2) void attention_kernel(Geometry 
     __shared__ Smem sm;
     // One tile per work-group (the hardware's dynamic dispatch balances the slower anchor tiles
     // against the static ones better than a grid-stride loop: measured 98 vs 107 us).
-    if (s.items_clear && blockIdx.x == 0 && threadIdx.x < 2) s.items_clear[threadIdx.x] = 0;
     // The anchor tiles are spread evenly over the first half of the grid (all of it's first
     // part when they are more than half the tiles), so that the launch ends on static tiles only:
     // an anchor tile takes longer, and one dispatched last would stretch the launch's tail
@@ -1882,13 +1981,19 @@ long long resident_grid(K kernel, std::atomic<int> &cache, const Geometry &g, lo
 template <int G>
 struct TidalFixedL {
     static hipError_t run(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, bool recall,
-                          bool with_static, long long items, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
+                          bool with_static, long long items, hipStream_t st, hipEvent_t e0, hipEvent_t e1,
+                          const SelectArgs *selp)
     {
         recall = recall && g.nT > 0 && g.k > 0 && g.comp_max > 0;
         const bool known = items >= 0 && !recall;
+        SelectArgs sel{};
+        if (selp) {
+            sel = *selp;
+            sel.n_mass = g.nA * g.B;
+        }
         const long long tiles = (with_static ? (long long)g.n_static * g.B : 0) +
                                 (known ? std::min<long long>(items, g.ng_kept) : g.ng_kept) * g.nT * g.B;
-        if (tiles == 0 && !recall) return record_pair(e0, e1, st);
+        if (tiles == 0 && !recall && sel.n_mass == 0) return record_pair(e0, e1, st);
         const dim3 block(NT);
         const int ws = with_static ? 1 : 0;
         static std::atomic<int> occ[3];
@@ -1896,18 +2001,26 @@ struct TidalFixedL {
             // the step's item count known on the host: one tile per work-group (the hardware
             // dispatches each work-group as another ends); else as many as stay resident, looping
             auto k = tidal_fixed_kernel<G, RPL_S, false>;
-            const dim3 grid((unsigned)(known ? tiles : resident_grid(k, occ[0], g, tiles)));
-            hipExtLaunchKernelGGL(k, grid, block, 0, st, e0, e1, 0, g, t, s, q, ws);
+            const long long n = sel.n_mass + (known ? tiles : (tiles ? resident_grid(k, occ[0], g, tiles) : 0));
+            hipExtLaunchKernelGGL(k, dim3((unsigned)n), block, 0, st, e0, e1, 0, g, t, s, q, ws, sel);
         } else if (g.slot_tile == TILE_S) {
             auto k = tidal_fixed_kernel<G, RPL_S, true>;
             const dim3 grid((unsigned)(RECALL_WGS + std::max(1LL, resident_grid(k, occ[1], g, tiles))));
-            hipExtLaunchKernelGGL(k, grid, block, 0, st, e0, e1, 0, g, t, s, q, ws);
+            hipExtLaunchKernelGGL(k, grid, block, 0, st, e0, e1, 0, g, t, s, q, ws, SelectArgs{});
         } else {
             auto k = tidal_fixed_kernel<G, 2 * RPL_S, true>;
             const dim3 grid((unsigned)(RECALL_WGS + std::max(1LL, resident_grid(k, occ[2], g, tiles))));
-            hipExtLaunchKernelGGL(k, grid, block, 0, st, e0, e1, 0, g, t, s, q, ws);
+            hipExtLaunchKernelGGL(k, grid, block, 0, st, e0, e1, 0, g, t, s, q, ws, SelectArgs{});
         }
         return hipGetLastError();
+    }
+};
+template <int G>
+struct TidalSelectFits {
+    static bool run(const Geometry &g)
+    {
+        const size_t room = sizeof(SubsetSmem<G, RPL_S>) - SEL_SHARED_OFF;
+        return g.nA > 0 && g.nc > 0 && select_shared_bytes(g) <= room && (size_t)G * g.n_tiles_a * sizeof(double) <= room;
     }
 };
 template <int G>
@@ -1969,9 +2082,24 @@ hipError_t launch_select(const Geometry &g, const StepBuffers &s, float *scores,
 }
 
 hipError_t launch_tidal_fixed(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, bool recall,
-                              bool with_static, long long items, hipStream_t st, hipEvent_t e0, hipEvent_t e1)
+                              bool with_static, long long items, hipStream_t st, hipEvent_t e0, hipEvent_t e1,
+                              const SelectArgs *sel)
 {
-    return dispatch_g<TidalFixedL>(g.G, g, t, s, q, recall, with_static, items, st, e0, e1);
+    if (sel && (recall || !sel->s.arrive || !tidal_select_fits(g))) return hipErrorInvalidValue;
+    return dispatch_g<TidalFixedL>(g.G, g, t, s, q, recall, with_static, items, st, e0, e1, sel);
+}
+
+bool tidal_select_fits(const Geometry &g)
+{
+    switch (g.G) {
+    case 1: return TidalSelectFits<1>::run(g);
+    case 2: return TidalSelectFits<2>::run(g);
+    case 3: return TidalSelectFits<3>::run(g);
+    case 4: return TidalSelectFits<4>::run(g);
+    case 6: return TidalSelectFits<6>::run(g);
+    case 8: return TidalSelectFits<8>::run(g);
+    default: return false;
+    }
 }
 
 hipError_t launch_attention(const Geometry &g, const Tiers &t, const StepBuffers &s, const uint16_t *q, hipStream_t st,
