@@ -39,11 +39,12 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def overlap_sweep(W, torch, w, ctx, geo, qd, out, sc, sel, stream, args, ms_no_recall):
+def overlap_sweep(W, torch, w, ctx, geo, qd, out, sc, sel, stream, args):
     """Force about N newly resident chunks per step through the selection override: k - N chunks
-    stay selected, N more rotate through the remaining chunks.  For each N: steps/s, chunks
-    copied and revived per step, recall time, and overlap = 1 - (T_step - T_no_recall) / T_recall
-    (the share of the recall hidden behind the rest of the step)."""
+    stay selected, N more rotate through the remaining chunks.  For each N: step time, chunks
+    copied and revived per step, and (in a context with timing events) the recall time.  The
+    same schedule from the same state gives the same recall in both contexts; merge_sweep joins
+    them."""
     B, S, k, nc = w.batch, w.steps, geo["k"], geo["n_chunks"]
     res = []
     for n_new in (1, 2, 4, 8, 24):
@@ -72,14 +73,26 @@ def overlap_sweep(W, torch, w, ctx, geo, qd, out, sc, sel, stream, args, ms_no_r
         ms = el * 1e3 / steps
         nt = b["timed_steps"] - a["timed_steps"]
         rec_ms = (b["t_recall_ms"] - a["t_recall_ms"]) / nt if nt else None
-        ov = None
-        if rec_ms:
-            ov = max(0.0, min(1.0, 1.0 - (ms - ms_no_recall) / rec_ms))
-        res.append({"new_per_step": n_new, "steps_per_s": 1e3 / ms, "ms_per_step": ms,
+        res.append({"new_per_step": n_new, "ms_per_step": ms,
                     "copied_per_step": (b["recalled_chunks"] - a["recalled_chunks"]) / steps / B,
                     "revived_per_step": (b["revived_chunks"] - a["revived_chunks"]) / steps / B,
+                    "recall_ms": rec_ms})
+        log(f"[bench] sweep {n_new} new/step: {1e3 / ms:.0f} steps/s" + (" (timing events)" if nt else ""))
+    return res
+
+
+def merge_sweep(plain, timed, ms_no_recall):
+    """Steps/s from the context without timing events (plain), the recall time from the one with
+    them (timed), and overlap = 1 - (T_step - T_no_recall) / T_recall: the share of the recall
+    hidden behind the rest of the step."""
+    rec = {r["new_per_step"]: r["recall_ms"] for r in timed}
+    res = []
+    for r in plain:
+        ms, rec_ms = r["ms_per_step"], rec.get(r["new_per_step"])
+        ov = max(0.0, min(1.0, 1.0 - (ms - ms_no_recall) / rec_ms)) if rec_ms else None
+        res.append({"new_per_step": r["new_per_step"], "steps_per_s": 1e3 / ms, "ms_per_step": ms,
+                    "copied_per_step": r["copied_per_step"], "revived_per_step": r["revived_per_step"],
                     "recall_ms": rec_ms, "overlap": ov})
-        log(f"[bench] sweep {n_new} new/step: {1e3 / ms:.0f} steps/s, overlap {ov}")
     return res
 
 
@@ -99,8 +112,9 @@ def run_timing(W, torch, w, timing, recall, kd, vd, qd, roles, prefill, args, ch
     contexts.  The first has no timing events: its warm-up and timed steps give steps/s, and a
     second region with the selection pinned to resident chunks (no recall) gives the step time
     without recall.  The second context records HIP events around the launches (WNW_F_TIMING)
-    and runs the same steps for the per-kernel breakdown, then the overlap sweep.  Returns the
-    context-independent numbers; both contexts are destroyed."""
+    and runs the same steps for the per-kernel breakdown.  Each runs the overlap sweep: its
+    steps/s from the first, its recall time from the second.  Returns the context-independent
+    numbers; both contexts are destroyed."""
     B, L, H, D, S = w.batch, w.layers, w.kv_heads, w.head_dim, w.steps
     base = ((W.WNW_F_RECALL_MEMCPY if recall == "memcpy" else 0)
             | (W.WNW_F_SELECT_NEXT_STEP if timing == "next" else 0)
@@ -149,8 +163,8 @@ def run_timing(W, torch, w, timing, recall, kd, vd, qd, roles, prefill, args, ch
             t2 = _steps(W, torch, ctx, qd, out, sc, sel, stream, 0, nr, S)
             st3 = W.wnw_get_stats(ctx)
             sweep = []
-            if timed_events and args.sweep and timing == "next" and geo["k"] > 0:
-                sweep = overlap_sweep(W, torch, w, ctx, geo, qd, out, sc, sel, stream, args, t2 * 1e3 / nr)
+            if args.sweep and timing == "next" and geo["k"] > 0:
+                sweep = overlap_sweep(W, torch, w, ctx, geo, qd, out, sc, sel, stream, args)
             W.wnw_set_selection_override(ctx, None)
             del pinned
         finally:
@@ -168,8 +182,9 @@ def run_timing(W, torch, w, timing, recall, kd, vd, qd, roles, prefill, args, ch
                                    "chunk_MB": geo.get("chunk_bytes", 0) / 1e6,
                                    "step_ms_no_recall": t2 * 1e3 / nr,
                                    "host_wait_ms_per_step": d["t_host_wait_ms"] / K}})
+            res["sweep_plain"] = sweep
             continue
-        res["sweep"] = sweep
+        res["sweep"] = merge_sweep(res.pop("sweep_plain", []), sweep, res["recall"]["step_ms_no_recall"])
         n, n2 = d["timed_steps"], d2["timed_steps"]
         row_bytes = 2 * D * 2                      # K + V of one position, bf16
         # slot_rows: complement rows attended, summed over steps, sequences and tidal heads.  With
@@ -205,6 +220,8 @@ def run_timing(W, torch, w, timing, recall, kd, vd, qd, roles, prefill, args, ch
         rms = d["t_recall_ms"] / n
         res["recall"]["ms"] = rms
         res["recall"]["GBps"] = (d["recalled_bytes"] / n) / rms / 1e6 if rms > 0 else None
+    if "sweep_plain" in res:   # no context with timing events ran
+        res["sweep"] = merge_sweep(res.pop("sweep_plain"), [], res["recall"]["step_ms_no_recall"])
     return res
 
 

@@ -152,7 +152,10 @@ typedef struct {
                                   WNW_F_SELECT_NEXT_STEP also the fixed heads and the tidal kept
                                   rows)                                                         */
     double t_select_ms;        /* anchor merge, chunk scores, top-k, residency, slots (up to the
-                                  end of the select kernel)                                     */
+                                  end of the select kernel).  Near zero in steps that run them
+                                  inside the tidal/fixed launch (WNW_F_SELECT_NEXT_STEP with
+                                  WNW_F_RECALL_MEMCPY, after a previous-step recall of at most
+                                  4 MiB): t_tidal_fixed_ms holds them then                      */
     double t_tidal_fixed_ms;   /* the tidal/fixed launch after the selection.  Same-step timing:
                                   fixed heads, tidal kept rows, complements already on the
                                   device (default recall: also the recall and the attention over
