@@ -1620,21 +1620,23 @@ __device__ inline bool last_arrival(int32_t *cnt, int n, SelectShared &sh)
 // this step does not have.  With REC (same-step timing), the first RECALL_WGS work-groups copy
 // the complements listed for recall from mapped pinned memory into their slots and attend to
 // them: the step is bound by the host link then, and the copies start with the launch.
-// With sel.n_mass (next-step timing, sel.s.arrive set), the first n_mass = nA * B work-groups
+// With SEL (next-step timing, sel.s.arrive set), the first sel.n_mass = nA * B work-groups
 // merge the anchor heads' chunk masses of this step's attention launch, one head each, and the
 // last of a sequence's heads to finish runs the sequence's selection (sel.s: the lists it
-// writes, which this launch does not read; the items read the lists of s).
-template <int G, int RPLK, bool REC>
+// writes, which this launch does not read; the items read the lists of s).  A separate
+// instantiation: the branch alone, never taken, slowed the items by about 1.5 %.
+template <int G, int RPLK, bool REC, bool SEL>
 __global__ __launch_bounds__(NT, REC ? (RPLK == RPL_S ? 2 : 1) : (G <= 4 ? 4 : G <= 6 ? 3 : 2)) void tidal_fixed_kernel(
     Geometry g, Tiers t, StepBuffers s, const uint16_t *__restrict__ q, int with_static, SelectArgs sel)
 {
+    static_assert(!(SEL && REC), "the selection joins only the launch without recall");
     union Smem {
         SubsetSmem<G, RPL_S> st;
         SubsetSmem<G, RPLK> sl;
     };
     __shared__ Smem sm;   // one block for whichever path this work-group runs
     int w = blockIdx.x, nw = gridDim.x;
-    if (w < sel.n_mass) {
+    if (SEL && w < sel.n_mass) {
         const int ai = w % g.nA, b = w / g.nA;
         char *base = (char *)&sm;
         SelectShared &sh = *(SelectShared *)base;
@@ -1644,8 +1646,10 @@ __global__ __launch_bounds__(NT, REC ? (RPLK == RPL_S ? 2 : 1) : (G <= 4 ? 4 : G
             select_seq(g, sel.s, sel.scores, sel.ovr, sel.selected, b, (double *)(base + SEL_SHARED_OFF), sh);
         return;
     }
-    w -= sel.n_mass;
-    nw -= sel.n_mass;
+    if constexpr (SEL) {
+        w -= sel.n_mass;
+        nw -= sel.n_mass;
+    }
     if constexpr (REC) {
         if (w < RECALL_WGS) {
             recall_units<G, RPLK>(g, t, s, q, w, RECALL_WGS, sm.sl);
@@ -1996,19 +2000,19 @@ struct TidalFixedL {
         if (tiles == 0 && !recall && sel.n_mass == 0) return record_pair(e0, e1, st);
         const dim3 block(NT);
         const int ws = with_static ? 1 : 0;
-        static std::atomic<int> occ[3];
+        static std::atomic<int> occ[4];
         if (!recall) {
             // the step's item count known on the host: one tile per work-group (the hardware
             // dispatches each work-group as another ends); else as many as stay resident, looping
-            auto k = tidal_fixed_kernel<G, RPL_S, false>;
-            const long long n = sel.n_mass + (known ? tiles : (tiles ? resident_grid(k, occ[0], g, tiles) : 0));
+            auto k = sel.n_mass ? tidal_fixed_kernel<G, RPL_S, false, true> : tidal_fixed_kernel<G, RPL_S, false, false>;
+            const long long n = sel.n_mass + (known ? tiles : (tiles ? resident_grid(k, occ[sel.n_mass ? 3 : 0], g, tiles) : 0));
             hipExtLaunchKernelGGL(k, dim3((unsigned)n), block, 0, st, e0, e1, 0, g, t, s, q, ws, sel);
         } else if (g.slot_tile == TILE_S) {
-            auto k = tidal_fixed_kernel<G, RPL_S, true>;
+            auto k = tidal_fixed_kernel<G, RPL_S, true, false>;
             const dim3 grid((unsigned)(RECALL_WGS + std::max(1LL, resident_grid(k, occ[1], g, tiles))));
             hipExtLaunchKernelGGL(k, grid, block, 0, st, e0, e1, 0, g, t, s, q, ws, SelectArgs{});
         } else {
-            auto k = tidal_fixed_kernel<G, 2 * RPL_S, true>;
+            auto k = tidal_fixed_kernel<G, 2 * RPL_S, true, false>;
             const dim3 grid((unsigned)(RECALL_WGS + std::max(1LL, resident_grid(k, occ[2], g, tiles))));
             hipExtLaunchKernelGGL(k, grid, block, 0, st, e0, e1, 0, g, t, s, q, ws, SelectArgs{});
         }
