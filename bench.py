@@ -392,7 +392,9 @@ def main():
 
 
 # rocprofv3 names of the launches behind the bench's kernel keys (the headline's group of 4)
-PROFILE_NAMES = {"attention": "attention_kernel<4>", "tidal_fixed": "tidal_fixed_kernel<4, 8, false>"}
+# (the tidal/fixed launch of next-step timing has two instantiations: without and with the
+# chunk-mass merge and the selection inside it)
+PROFILE_NAMES = {"attention": "attention_kernel<4>", "tidal_fixed": "tidal_fixed_kernel<4, 8, false, false/true>"}
 
 
 def attention_roofline(k, first, workload):
