@@ -1285,7 +1285,7 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, void *out, float *scor
 #define MARK(i) \
     if (timing) HIPCHECK(c, hipEventRecord(ev.e[i], s0))
 
-    // Lists (kept, new, their counts and item counts) alternate between two buffers by step.
+    // Lists (kept, new and their counts) alternate between two buffers by step.
     // Same-step timing: the select kernel of step s fills buffer s & 1 and step s reads it.
     // Next-step timing: the select kernel of step s fills buffer (s + 1) & 1 for step s + 1, and
     // step s reads buffer s & 1, filled by step s - 1: its tidal launch streams the kept list,
