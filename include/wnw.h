@@ -178,8 +178,10 @@ typedef struct {
     double t_host_wait_ms;     /* WNW_F_RECALL_MEMCPY: host time spent polling for the step's
                                   selection before issuing the copies, summed over steps         */
     double t_recall_wait_ms;   /* WNW_F_TIMING: on the caller's stream, from the end of the
-                                  select kernel to the start of the tidal/fixed launch: with
-                                  WNW_F_SELECT_NEXT_STEP the wait for the previous step's recall */
+                                  select kernel (of the first launch when the selection runs
+                                  inside the tidal/fixed launch) to the start of the tidal/fixed
+                                  launch: with WNW_F_SELECT_NEXT_STEP the wait for the previous
+                                  step's recall                                                  */
     int64_t kept_rows;         /* complement rows of the kept lists (segments whose bytes were
                                   on the device before the step's recall), summed over steps,
                                   sequences and tidal heads; the rest of slot_rows were recalled

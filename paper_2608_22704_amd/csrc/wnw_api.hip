@@ -102,7 +102,8 @@ struct wnw_ctx {
     // which are joined back into `side` (one stream queues copies with a gap between them)
     hipStream_t copy_st[N_COPY_STREAMS - 1] = {};
     // by step parity: the end of each copy stream's share of that step's host-issued recall, and
-    // the end of that step's select kernel (next-step timing with the copy kernel)
+    // the end of that step's select kernel (next-step timing with the copy kernel, which never
+    // runs the selection inside the tidal launch)
     hipEvent_t ev_copy[2][N_COPY_STREAMS] = {};
     hipEvent_t ev_sel[2] = {}, ev_rec = nullptr;
     bool rec_pending = false;          // next-step timing: a recall issued on `side` not yet joined
@@ -132,7 +133,7 @@ struct wnw_ctx {
     hipError_t rerr = hipSuccess;      // first failure of the recall thread
     std::string rerr_msg;
     int32_t delay_us = 0;              // test hook: delay before every recall (wnw_debug_set_recall_delay)
-    int32_t *h_flag = nullptr;         // pinned, mapped: [0] slot exhaustion seen by a select kernel
+    int32_t *h_flag = nullptr;         // pinned, mapped: [0] slot exhaustion seen by a selection
     int32_t *d_flag = nullptr;         // the same memory as the device addresses it
     double host_wait_ms = 0.0;         // host time spent waiting for selections (copy-engine recall)
     bool log = false;                  // WNW_LOG set: one trace line per step on stderr
@@ -503,7 +504,7 @@ void parallel_for(int n, const std::function<void(int)> &fn)
     for (auto &x : th) x.join();
 }
 
-// Tag the select kernel of `step` publishes with the mirror (nonzero; steps two apart, which
+// Tag the selection of `step` publishes with the mirror (nonzero; steps two apart, which
 // share a mirror, differ).
 int32_t pub_tag(int64_t step)
 {
@@ -511,7 +512,7 @@ int32_t pub_tag(int64_t step)
 }
 
 // Waits (busy polling: a sleeping wait wakes tens to hundreds of microseconds late) until the
-// select kernel of `step`, enqueued on `st`, has published the mirror of parity step & 1 for
+// selection of `step`, enqueued on `st`, has published the mirror of parity step & 1 for
 // every sequence.  Every millisecond it also asks whether `st` has failed, or has completed
 // without the tags (which would be a defect): either is returned as an error.
 hipError_t wait_published(const wnw_ctx *c, int64_t step, hipStream_t st)
@@ -547,7 +548,7 @@ void delay_fn(void *us)
 }
 
 // Host-issued recall of the step of parity `par`: one hipMemcpyAsync per run of consecutive
-// chunks landing in consecutive slots, from the counts and new lists that step's select kernel
+// chunks landing in consecutive slots, from the counts and new lists that step's selection
 // mirrored to pinned memory (already complete on the host).  The runs go round-robin to `st` and
 // the extra copy streams; ev_copy[par][i] marks the end of each stream's share.  The caller has
 // seen the step's selection complete on the host, so every earlier reader of the target slots
@@ -695,7 +696,7 @@ void recall_stop(wnw_ctx *c)
     c->rthread.join();
 }
 
-// Slot exhaustion reported by a select kernel (mapped pinned flag): the context fails, since
+// Slot exhaustion reported by a selection (mapped pinned flag): the context fails, since
 // tidal heads of that step missed a resident segment.  Reads host memory only (no wait).
 wnw_status check_exhaustion(wnw_ctx *c)
 {
@@ -916,7 +917,7 @@ wnw_status build_tiers(wnw_ctx *c, const uint8_t *keep_all)
         HIPCHECK(c, hipHostGetDevicePointer(&dp, c->host_comp, 0));
         c->t.host_comp = (const uint16_t *)dp;
     }
-    // coherent: the select kernel's stores reach host memory without a cache write-back
+    // coherent: the selection's stores reach host memory without a cache write-back
     c->mirror_ints = B * 2 + B * g.knew * 2 + B;
     if ((r = palloc(c, (void **)&c->h_newinfo, 2 * c->mirror_ints * sizeof(int32_t), "recall lists",
                     hipHostMallocCoherent)) != WNW_OK)
@@ -1286,8 +1287,8 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, void *out, float *scor
     if (timing) HIPCHECK(c, hipEventRecord(ev.e[i], s0))
 
     // Lists (kept, new and their counts) alternate between two buffers by step.
-    // Same-step timing: the select kernel of step s fills buffer s & 1 and step s reads it.
-    // Next-step timing: the select kernel of step s fills buffer (s + 1) & 1 for step s + 1, and
+    // Same-step timing: the selection of step s fills buffer s & 1 and step s reads it.
+    // Next-step timing: the selection of step s fills buffer (s + 1) & 1 for step s + 1, and
     // step s reads buffer s & 1, filled by step s - 1: its tidal launch streams the kept list,
     // which then holds every resident complement (those on the device before step s - 1's
     // recall, then those step s - 1 recalled, once their copies have landed).  Neither select
@@ -1303,7 +1304,7 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, void *out, float *scor
         return b;
     };
     StepBuffers sb = lists_of(c->s, par);                         // what this step reads
-    StepBuffers sn = g.next_step ? lists_of(c->s, nxt) : sb;      // what its select kernel writes
+    StepBuffers sn = g.next_step ? lists_of(c->s, nxt) : sb;      // what its selection writes
 
     // (1) anchor attention + chunk mass, (2) scores, top-k and residency.  With next-step
     // timing the static tidal/fixed tiles (kept rows + text) join the anchor launch.

@@ -127,7 +127,7 @@ struct StepBuffers {
     int32_t *pub;               // host-issued recall: mapped pinned mirror of counts [B][2], new
                                 // lists [B][knew][2] and publication tags [B], written by the select
                                 // kernel; else null
-    int32_t pub_tag;            // the tag the select kernel stores for each sequence once that
+    int32_t pub_tag;            // the tag the selection stores for each sequence once that
                                 // sequence's mirror is visible to the host (nonzero, new each step)
     unsigned long long *stats;  // [8] recalled, dropped, resident, slot_rows, peak, exhausted, revived,
                                 // kept-list rows
