@@ -186,6 +186,10 @@ typedef struct {
                                   on the device before the step's recall), summed over steps,
                                   sequences and tidal heads; the rest of slot_rows were recalled
                                   by the step before (WNW_F_SELECT_NEXT_STEP) or the step itself */
+    int64_t selections_in_tidal; /* steps whose anchor mass merge and selection ran inside the
+                                  tidal/fixed launch (WNW_F_SELECT_NEXT_STEP with
+                                  WNW_F_RECALL_MEMCPY, after a previous-step recall of at most
+                                  4 MiB); the other steps ran the two kernels before it         */
 } wnw_stats;
 
 /* Create a context for one batch of caches: the full KV cache as prefill leaves it, before any

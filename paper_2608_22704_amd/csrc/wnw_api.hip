@@ -136,6 +136,7 @@ struct wnw_ctx {
     int32_t *h_flag = nullptr;         // pinned, mapped: [0] slot exhaustion seen by a selection
     int32_t *d_flag = nullptr;         // the same memory as the device addresses it
     double host_wait_ms = 0.0;         // host time spent waiting for selections (copy-engine recall)
+    int64_t sel_in_tidal = 0;          // steps whose selection ran inside the tidal launch
     bool log = false;                  // WNW_LOG set: one trace line per step on stderr
 
     std::vector<StepEvents> pending, spare;
@@ -1338,6 +1339,7 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, void *out, float *scor
         }
         sel_in_tidal = prev_bytes <= SEL_IN_TIDAL_BYTES;
     }
+    c->sel_in_tidal += sel_in_tidal ? 1 : 0;
     if (!sel_in_tidal) {
         HIPCHECK(c, launch_anchor_mass(g, sb, s0));
         HIPCHECK(c, launch_select(g, sn, sc, c->override_sel, sel, s0));
@@ -1574,6 +1576,7 @@ wnw_status wnw_get_stats(wnw_ctx *c, wnw_stats *o)
     }
     o->t_recall_wait_ms = c->t_acc[7];
     o->kept_rows = (int64_t)st[7];
+    o->selections_in_tidal = c->sel_in_tidal;
     return WNW_OK;
 }
 

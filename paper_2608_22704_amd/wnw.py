@@ -46,7 +46,8 @@ class wnw_stats(C.Structure):
                 ("timed_steps", C.c_int64), ("t_anchor_ms", C.c_double), ("t_select_ms", C.c_double),
                 ("t_tidal_fixed_ms", C.c_double), ("t_new_ms", C.c_double), ("t_combine_ms", C.c_double),
                 ("t_step_ms", C.c_double), ("t_recall_ms", C.c_double), ("slot_exhausted", C.c_int64),
-                ("t_host_wait_ms", C.c_double), ("t_recall_wait_ms", C.c_double), ("kept_rows", C.c_int64)]
+                ("t_host_wait_ms", C.c_double), ("t_recall_wait_ms", C.c_double), ("kept_rows", C.c_int64),
+                ("selections_in_tidal", C.c_int64)]
 
     def as_dict(self) -> dict:
         return {name: getattr(self, name) for name, _ in self._fields_}

@@ -143,3 +143,34 @@ def test_binding_checks_buffers_before_passing_them():
         W._host_out(buf, 30)
     with pytest.raises(TypeError):
         W._host_out(np.empty(32, dtype=np.uint8)[::2], 16)
+
+
+def test_structs_match_the_header(W, tmp_path):
+    """The binding's ctypes structures have the header's size and field offsets (a C program
+    compiled against the header prints them)."""
+    import ctypes
+    lines = []
+    for st in (W.wnw_config, W.wnw_stats):
+        name = st.__name__
+        lines.append(f'printf("{name} sizeof %zu\\n", sizeof({name}));')
+        for f, _ in st._fields_:
+            lines.append(f'printf("{name} {f} %zu\\n", offsetof({name}, {f}));')
+    src = tmp_path / "layout.c"
+    src.write_text('#include <stddef.h>\n#include <stdio.h>\n#include "wnw.h"\nint main(void){\n' + "\n".join(lines) +
+                   "\nreturn 0; }\n")
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c99", "-Wall", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split("\n")
+    got = {tuple(l.split()[:2]): int(l.split()[2]) for l in out if l}
+    for st in (W.wnw_config, W.wnw_stats):
+        name = st.__name__
+        assert got[(name, "sizeof")] == ctypes.sizeof(st), name
+        for f, _ in st._fields_:
+            assert got[(name, f)] == getattr(st, f).offset, (name, f)
+    # every field of the header's structures is in the binding
+    src_h = open(HEADER).read()
+    for st in (W.wnw_config, W.wnw_stats):
+        body = src_h[:src_h.index("} " + st.__name__ + ";")]
+        body = body[body.rindex("typedef struct {"):]
+        fields = re.findall(r"^\s+(?:int32_t|int64_t|uint32_t|double|float)\s+(\w+);", body, re.M)
+        assert fields == [f for f, _ in st._fields_], st.__name__

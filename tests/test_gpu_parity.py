@@ -1010,6 +1010,62 @@ def test_delayed_recall_gives_identical_results(mode):
                                   y.view(np.uint32) if y.dtype == np.float32 else y), f"step {s} differs"
 
 
+def test_selection_inside_and_before_the_tidal_launch_bit_identical():
+    """With next-step timing and copy-engine recall a step runs the chunk-mass merge and the
+    selection inside the tidal launch after a previous-step recall of at most 4 MiB, else as two
+    kernels before it; the copy-kernel path always runs the two kernels.  A forced schedule whose
+    selected set moves to a disjoint one every second step alternates recalls of tens of MB with
+    steps that recall nothing, so the copy-engine run takes both routes, switching back and forth;
+    outputs, scores and selections match the other path bit for bit at every step."""
+    import torch
+    from paper_2608_22704_amd import wnw as W
+    from tests.wnw_harness import log, to_dev
+    w = _small("selection_place", 191, B=4, L=4, Hq=16, Hkv=8, Ta=8000, Tt=40, cl=32, budget=2000, steps=24)
+    log("[case] selection inside / before the tidal launch, bit for bit")
+    B, L, H, D = w.batch, w.layers, w.kv_heads, w.head_dim
+    seqs = [gen.sequence(w, b) for b in range(B)]
+    kd = torch.stack([to_dev(sq["k"]) for sq in seqs])
+    vd = torch.stack([to_dev(sq["v"]) for sq in seqs])
+    qd = torch.stack([to_dev(np.stack([sq["q"][s] for sq in seqs])) for s in range(w.steps)])
+    prefill = np.stack([sq["prefill"] for sq in seqs])
+    runs, placed = [], []
+    for flags in (W.WNW_F_SELECT_NEXT_STEP | W.WNW_F_RECALL_MEMCPY, W.WNW_F_SELECT_NEXT_STEP):
+        cfg = W.make_config(B, L, w.q_heads, H, w.audio_len, w.text_len, w.chunk_len, w.budget_bp, flags=flags)
+        ctx = W.wnw_init_cache(cfg, kd, vd)
+        try:
+            W.wnw_set_roles(ctx, gen.roles(w), prefill)
+            geo = W.wnw_query_geometry(ctx)
+            k, nch = geo["k"], geo["n_chunks"]
+            # disjoint sets of k chunks, a new one every second step (sequences offset)
+            sched = np.empty((w.steps, B, k), dtype=np.int32)
+            for s in range(w.steps):
+                for b in range(B):
+                    sched[s, b] = np.sort((np.arange(k) + (s // 2 + b) * k) % nch)
+            sd = torch.from_numpy(sched).cuda()
+            out = torch.empty((B, L, w.q_heads, D), dtype=torch.float32, device="cuda")
+            sc = torch.empty((B, nch), dtype=torch.float32, device="cuda")
+            sel = torch.empty((B, k), dtype=torch.int32, device="cuda")
+            kept = []
+            for s in range(w.steps):
+                W.wnw_set_selection_override(ctx, sd[s])
+                W.wnw_decode_step(ctx, qd[s], out, sc, sel)
+                kept.append((out.clone(), sc.clone(), sel.clone()))
+            torch.cuda.synchronize()
+            W.wnw_set_selection_override(ctx, None)
+            st = W.wnw_get_stats(ctx)
+            assert st["recalled_bytes"] > 2 * (4 << 20) * (w.steps // 4), st["recalled_bytes"]
+            placed.append(st["selections_in_tidal"])
+            runs.append([[x.cpu().numpy() for x in step] for step in kept])
+        finally:
+            W.wnw_destroy(ctx)
+    # the copy-engine run switched between the two routes; the copy-kernel run never used the first
+    assert 0 < placed[0] < w.steps and placed[1] == 0, placed
+    for s, (a, b) in enumerate(zip(*runs)):
+        for x, y in zip(a, b):
+            assert np.array_equal(x.view(np.uint32) if x.dtype == np.float32 else x,
+                                  y.view(np.uint32) if y.dtype == np.float32 else y), f"step {s} differs"
+
+
 def test_next_step_recall_paths_bit_identical():
     """With next-step timing the copy engines (the host knows each step's list length from the
     mirror and launches one work-group per slot item) and the copy kernel (the item count comes
