@@ -1397,7 +1397,7 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, void *out, float *scor
         HIPCHECK(c, launch_subset_combine(g, c->t, sb, out, s0));
         MARK(5);
         combined = true;
-        if (memcpy_path) {
+        if (memcpy_path && g.nc > 0) {
             // the recall thread issues this step's copies once its selection is done; the copy
             // engines queue them behind the previous step's copies, so the link stays busy
             wnw_ctx::RecallJob job{(int64_t)c->steps, s0, timing, timing ? ev.r[0] : nullptr, {}};
@@ -1413,8 +1413,13 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, void *out, float *scor
         if (!memcpy_path) {
             if (timing) HIPCHECK(c, hipEventRecord(ev.r[1], c->side));
             HIPCHECK(c, hipEventRecord(c->ev_rec, c->side));   // host-issued copies: ev_copy[] instead
+        } else if (g.nc == 0 && timing) {
+            // no recall: an empty interval on the side stream
+            HIPCHECK(c, hipEventRecord(ev.r[0], c->side));
+            HIPCHECK(c, hipEventRecord(ev.r[1], c->side));
         }
-        c->rec_pending = true;
+        // with no chunks (no audio) no selection runs, and the recall thread gets no job
+        c->rec_pending = !memcpy_path || g.nc > 0;
     } else if (!memcpy_path) {
         MARK(2);
         // (3) + (4) in one launch: its first work-groups copy the complements listed for recall
@@ -1434,14 +1439,21 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, void *out, float *scor
         // (3) copies on the side stream.  The target slots were freed by this step's select
         // kernel, which follows every earlier reader on s0: once it has published its tag, no
         // reader of them is left and the copies need no device-side wait.
-        const auto w0 = std::chrono::steady_clock::now();
-        HIPCHECK(c, wait_published(c, (int64_t)c->steps, s0));
-        c->host_wait_ms += std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - w0).count();
-        if (timing) HIPCHECK(c, hipEventRecord(ev.r[0], c->side));
-        wnw_status r = check_exhaustion(c);
-        if (r != WNW_OK) return r;
-        r = issue_copies(c, par, c->side);
-        if (r != WNW_OK) return r;
+        wnw_status r = WNW_OK;
+        if (g.nc > 0) {
+            const auto w0 = std::chrono::steady_clock::now();
+            HIPCHECK(c, wait_published(c, (int64_t)c->steps, s0));
+            c->host_wait_ms += std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - w0).count();
+            if (timing) HIPCHECK(c, hipEventRecord(ev.r[0], c->side));
+            r = check_exhaustion(c);
+            if (r != WNW_OK) return r;
+            r = issue_copies(c, par, c->side);
+            if (r != WNW_OK) return r;
+        } else {
+            // no chunks (no audio): no selection ran, so no tag comes, and nothing is recalled
+            c->copy_mask[par] = 0;
+            if (timing) HIPCHECK(c, hipEventRecord(ev.r[0], c->side));
+        }
         if (timing) {
             r = wait_copies(c, par, c->side);
             if (r != WNW_OK) return r;

@@ -371,6 +371,29 @@ def test_next_step_memcpy_recall_path():
          flags=_next(W.WNW_F_RECALL_MEMCPY))
 
 
+@pytest.mark.parametrize("timed", [0, 1], ids=["plain", "timing_events"])
+@pytest.mark.parametrize("nxt", [0, 1], ids=["same_step", "next_step"])
+def test_copy_engine_paths_without_audio(nxt, timed):
+    """No audio, so no chunk to select: with copy-engine recall no selection runs and no tag is
+    published, and neither the step nor the library's recall thread may wait for one (both
+    timings, with and without timing events, whose recall interval is then empty)."""
+    from paper_2608_22704_amd import wnw as W
+    flags = W.WNW_F_RECALL_MEMCPY | (W.WNW_F_SELECT_NEXT_STEP if nxt else 0) | (W.WNW_F_TIMING if timed else 0)
+    h = _run(_small("memcpy_text_only", 116, Ta=0, Tt=40), flags=flags)
+    assert h.final_stats["recalled_chunks"] == 0 and h.final_stats["selections_in_tidal"] == 0
+
+
+@pytest.mark.parametrize("w", EDGE, ids=[w.name for w in EDGE])
+def test_next_step_memcpy_edge_shapes(w):
+    """Copy-engine recall with next-step timing on the edge shapes: their recalls are small, so
+    every step's chunk-mass merge and selection run inside the tidal launch (group sizes 1 to 8,
+    ragged tiles, no text, no audio, anchors only), against the oracle step by step."""
+    from paper_2608_22704_amd import wnw as W
+    h = _run(w, flags=_next(W.WNW_F_RECALL_MEMCPY))
+    if w.audio_len > 0:   # chunks to select
+        assert h.final_stats["selections_in_tidal"] == w.steps, h.final_stats["selections_in_tidal"]
+
+
 @pytest.mark.parametrize("timing", ["same", "next"])
 def test_slot_rows_pointer_path(timing):
     """Slot groups read through per-row pointers (forced by a zero slot offset limit; the default
