@@ -540,6 +540,16 @@ def test_overlap_next_step_edge_shapes(w):
     _run(w, flags=_ovl(_next()))
 
 
+@pytest.mark.parametrize("w", EDGE_OVL, ids=[w.name for w in EDGE_OVL])
+def test_overlap_next_step_memcpy_edge_shapes(w):
+    """Overlapping chunks (two segments each) with copy-engine recall and next-step timing: the
+    selection inside the tidal launch scores segment pairs, against the oracle step by step."""
+    from paper_2608_22704_amd import wnw as W
+    h = _run(w, flags=_ovl(_next(W.WNW_F_RECALL_MEMCPY)))
+    if w.audio_len > 0:
+        assert h.final_stats["selections_in_tidal"] == w.steps, h.final_stats["selections_in_tidal"]
+
+
 def test_overlap_two_segments_one_chunk():
     """Two segments make one chunk, which top-k 1 selects at every step."""
     _run(_small("ovl_two_segments", 214, Ta=60, cl=64, budget=2000), flags=_ovl(), top_k=1)
