@@ -202,10 +202,10 @@ __device__ inline int lane_id_opaque()
 }
 
 // Shared memory of one anchor tile.
-// Values that pass between work-groups of one launch (tile partials to the chunk-mass merge, and
-// masses to the selection, see last_arrival) are stored and loaded as agent-scope relaxed
-// atomics: coherent across the dies' caches with no cache write-back or invalidation, which an
-// agent-scope fence would cost every work-group.
+// Values that pass between work-groups of one launch (the chunk masses, from the work-groups that
+// merge them to the selection in the same launch, see last_arrival) are stored and loaded as
+// agent-scope relaxed atomics: coherent across the dies' caches with no cache write-back or
+// invalidation, which an agent-scope fence would cost every work-group.
 __device__ inline void st_agent(double *p, double v)
 {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -391,8 +391,8 @@ __device__ inline void anchor_tile(const Geometry &g, const Tiers &t, const Step
         for (int w = 1; w < WAVES; ++w) M = fmax(M, wm[w * G + tid]);
 #pragma unroll
         for (int w = 0; w < WAVES; ++w) L += wl[w * G + tid];
-        st_agent(&s.pa_m[pidx * G + tid], M);
-        st_agent(&s.pa_l[pidx * G + tid], L);
+        s.pa_m[pidx * G + tid] = M;
+        s.pa_l[pidx * G + tid] = L;
     }
     for (int idx = tid; idx < G * D; idx += NT) {
         float o = 0.f;
@@ -414,7 +414,7 @@ __device__ inline void anchor_tile(const Geometry &g, const Tiers &t, const Step
                 const int r0 = t0 + w * RW;
                 if (r0 >= c * g.cl && r0 < (c + 1) * g.cl && r0 < g.Ta) acc2 += wl[w * G + h];
             }
-            st_agent(&s.pa_mass[pidx * G * g.maxc + tid], acc2);
+            s.pa_mass[pidx * G * g.maxc + tid] = acc2;
         }
         return;
     }
@@ -430,7 +430,7 @@ __device__ inline void anchor_tile(const Geometry &g, const Tiers &t, const Step
             for (int rr = r0 + k; rr < r1; rr += 16) acc2 += xs[h * TILE_A + (rr - t0)];
         }
         acc2 = sum16(acc2);
-        if (valid && k == 0) st_agent(&s.pa_mass[pidx * G * g.maxc + grp], acc2);
+        if (valid && k == 0) s.pa_mass[pidx * G * g.maxc + grp] = acc2;
     }
 }
 
@@ -511,14 +511,14 @@ __device__ inline void anchor_mass_head(const Geometry &g, const StepBuffers &s,
     const int t_hi0 = c0 < g.nc ? (min((c0 + 1) * g.cl, g.Ta) - 1) / TILE_A : -1;
 #pragma unroll
     for (int h = 0; h < G; ++h) {
-        pm[h] = tid < nt ? ld_agent(&s.pa_m[(base + tid) * G + h]) : -INFINITY;
-        pl[h] = tid < nt ? ld_agent(&s.pa_l[(base + tid) * G + h]) : 0.0;
+        pm[h] = tid < nt ? s.pa_m[(base + tid) * G + h] : -INFINITY;
+        pl[h] = tid < nt ? s.pa_l[(base + tid) * G + h] : 0.0;
     }
 #pragma unroll
     for (int u = 0; u < MAXT; ++u) {
         const int i = t_lo0 + u, j = c0 - (i * TILE_A) / g.cl;
 #pragma unroll
-        for (int h = 0; h < G; ++h) v[h][u] = i <= t_hi0 ? ld_agent(&s.pa_mass[((base + i) * G + h) * g.maxc + j]) : 0.0;
+        for (int h = 0; h < G; ++h) v[h][u] = i <= t_hi0 ? s.pa_mass[((base + i) * G + h) * g.maxc + j] : 0.0;
     }
     double m[G], l[G];
 #pragma unroll
@@ -529,7 +529,7 @@ __device__ inline void anchor_mass_head(const Geometry &g, const StepBuffers &s,
     for (int i = tid + MASS_THREADS; i < nt; i += MASS_THREADS)
 #pragma unroll
         for (int h = 0; h < G; ++h) {
-            const double x = ld_agent(&s.pa_m[(base + i) * G + h]);
+            const double x = s.pa_m[(base + i) * G + h];
             fac[h * nt + i] = x;
             m[h] = fmax(m[h], x);
         }
@@ -549,7 +549,7 @@ __device__ inline void anchor_mass_head(const Geometry &g, const StepBuffers &s,
             const double mi = fac[h * nt + i];
             const double f = (m[h] > -INFINITY && mi > -INFINITY) ? exp(mi - m[h]) : 0.0;
             fac[h * nt + i] = f;
-            l[h] += ld_agent(&s.pa_l[(base + i) * G + h]) * f;
+            l[h] += s.pa_l[(base + i) * G + h] * f;
         }
     block_reduce_g<G, MASS_THREADS>(l, false, red);   // also publishes fac[]
     if (tid < G) {
@@ -571,7 +571,7 @@ __device__ inline void anchor_mass_head(const Geometry &g, const StepBuffers &s,
             for (int u = 0; u < MAXT; ++u) {
                 const int i = t_lo + u, j = c - (i * TILE_A) / g.cl;
 #pragma unroll
-                for (int h = 0; h < G; ++h) v[h][u] = i <= t_hi ? ld_agent(&s.pa_mass[((base + i) * G + h) * g.maxc + j]) : 0.0;
+                for (int h = 0; h < G; ++h) v[h][u] = i <= t_hi ? s.pa_mass[((base + i) * G + h) * g.maxc + j] : 0.0;
             }
         }
         double acc = 0.0;
