@@ -1609,10 +1609,6 @@ __device__ inline bool last_arrival(int32_t *cnt, int n, SelectShared &sh)
     return sh.last;
 }
 
-// Anchor tiles and the static tidal/fixed tiles (kept rows + text, which no selection changes)
-// in one launch, interleaved along the grid: the anchor tiles' arithmetic (fp64 logits)
-// overlaps the static tiles' streaming.  Used with next-step timing, where the static tiles need
-// not wait for this step's selection.
 // Fixed heads, tidal kept rows and tidal complements already in their slots: static tiles
 // first (unless the attention launch ran them), then the items of one list (list_item).  The
 // work-groups loop over those tiles with the grid's stride, so the launch holds about as many
@@ -1676,6 +1672,10 @@ __global__ __launch_bounds__(NT, REC ? (RPLK == RPL_S ? 2 : 1) : (G <= 4 ? 4 : G
     }
 }
 
+// Anchor tiles and the static tidal/fixed tiles (kept rows + text, which no selection changes)
+// in one launch, interleaved along the grid: the anchor tiles' arithmetic (fp64 logits)
+// overlaps the static tiles' streaming.  Used with next-step timing, where the static tiles need
+// not wait for this step's selection.
 template <int G>
 __global__ __launch_bounds__(NT, G <= 4 ? 4 : 2) void attention_kernel(Geometry g, Tiers t, StepBuffers s,
                                                                        const uint16_t *__restrict__ q)
