@@ -1477,9 +1477,11 @@ wnw_status wnw_decode_step(wnw_ctx *c, const void *q_dev, void *out, float *scor
         int n_new = -1;
         if (memcpy_path && !g.next_step)
             for (int b = n_new = 0; b < g.B; ++b) n_new += c->h_newinfo[par * c->mirror_ints + b * 2 + 1];
-        fprintf(stderr, "[wnw] step %lld: %s timing, %s recall, %d sequences, new segments copied %d, host wait %.3f ms total\n",
+        fprintf(stderr, "[wnw] step %lld: %s timing, %s recall, %d sequences, new segments copied %d, host wait %.3f ms "
+                        "total, selection %s\n",
                 (long long)c->steps, g.next_step ? "next-step" : "same-step",
-                memcpy_path ? "copy-engine" : "work-group", g.B, n_new, c->host_wait_ms);
+                memcpy_path ? "copy-engine" : "work-group", g.B, n_new, c->host_wait_ms,
+                sel_in_tidal ? "inside the tidal launch" : "before the tidal launch");
     }
     c->steps++;
     return WNW_OK;

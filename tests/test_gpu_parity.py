@@ -371,6 +371,18 @@ def test_next_step_memcpy_recall_path():
          flags=_next(W.WNW_F_RECALL_MEMCPY))
 
 
+def test_wnw_log_trace(capfd, monkeypatch):
+    """WNW_LOG=1 at context creation: one trace line per step on stderr, naming the timing, the
+    recall path and where the selection ran (small recalls: inside the tidal launch)."""
+    from paper_2608_22704_amd import wnw as W
+    monkeypatch.setenv("WNW_LOG", "1")
+    _run(_small("log_trace", 117, steps=3), flags=_next(W.WNW_F_RECALL_MEMCPY))
+    err = capfd.readouterr().err
+    lines = [l for l in err.splitlines() if l.startswith("[wnw] step ")]
+    assert len(lines) == 3, err[-2000:]
+    assert all("next-step timing, copy-engine recall" in l and "selection inside the tidal launch" in l for l in lines), lines
+
+
 @pytest.mark.parametrize("timed", [0, 1], ids=["plain", "timing_events"])
 @pytest.mark.parametrize("nxt", [0, 1], ids=["same_step", "next_step"])
 def test_copy_engine_paths_without_audio(nxt, timed):
