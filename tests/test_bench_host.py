@@ -48,3 +48,22 @@ def test_traffic_from_counter_summary(tmp_path, monkeypatch):
     src.write_bytes(b"kernel source v1\n")
     path.write_text(f"kernels_source_sha256: {sha}\nfetch_kib_per_dispatch: 1\n")
     assert bench.measured_traffic("attention", "w") is None
+
+
+def test_merge_sweep_takes_steps_from_the_plain_context_and_recall_from_the_timed_one():
+    import bench
+    plain = [{"new_per_step": 1, "ms_per_step": 0.15, "copied_per_step": 0.25, "revived_per_step": 0.75, "recall_ms": None},
+             {"new_per_step": 4, "ms_per_step": 0.20, "copied_per_step": 2.0, "revived_per_step": 2.0, "recall_ms": None}]
+    timed = [{"new_per_step": 1, "ms_per_step": 0.16, "copied_per_step": 0.25, "revived_per_step": 0.75, "recall_ms": 0.05},
+             {"new_per_step": 4, "ms_per_step": 0.21, "copied_per_step": 2.0, "revived_per_step": 2.0, "recall_ms": 0.12}]
+    out = bench.merge_sweep(plain, timed, 0.145)
+    assert [r["new_per_step"] for r in out] == [1, 4]
+    assert abs(out[0]["steps_per_s"] - 1e3 / 0.15) < 1e-9 and out[0]["ms_per_step"] == 0.15
+    assert out[0]["recall_ms"] == 0.05 and out[1]["recall_ms"] == 0.12
+    # overlap = 1 - (T_step - T_no_recall) / T_recall, clamped to [0, 1]
+    assert abs(out[0]["overlap"] - (1 - (0.15 - 0.145) / 0.05)) < 1e-12
+    assert abs(out[1]["overlap"] - (1 - (0.20 - 0.145) / 0.12)) < 1e-12
+    # without the timed context there is no recall time and no overlap
+    bare = bench.merge_sweep(plain, [], 0.145)
+    assert all(r["recall_ms"] is None and r["overlap"] is None for r in bare)
+    assert bench.merge_sweep(plain, [dict(timed[0], recall_ms=0.001)], 0.145)[0]["overlap"] == 0.0
