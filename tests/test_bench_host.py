@@ -1,6 +1,6 @@
-"""Host-side behaviour of bench.py (no GPU): the single-GPU guard and the traffic figure read from
-a rocprofv3 counter summary, which must be dropped once the kernel source differs from the one
-the counters were taken on."""
+"""Host-side behaviour of bench.py (no GPU): the single-GPU guard, the traffic figure read from a
+rocprofv3 counter summary (dropped once the kernel source differs from the one the counters were
+taken on), and the overlap sweep's merge of its two contexts."""
 import hashlib
 import os
 import subprocess
